@@ -1,0 +1,156 @@
+/*
+ * tla.h -- C ABI of the MI355X (gfx950) triadic linear attention library.
+ *
+ * The operator (Section 2 of "Triadic Linear Attention: Three-Dimensional
+ * Recurrent States for Long-Context Sequence Modeling") keeps, per batch
+ * entry b and head h, a third-order state S[E][K][V] and for t = 1..T computes
+ *
+ *   Sbar = a_t (.)_e S_{t-1},       a_t[e] = exp(g_t[e])     (Eq. forget3)
+ *   GDN :  w = beta_t (v_t - sum_{e,k} k2_t[e] k_t[k] Sbar[e,k,:])   (Eq. gdn3;
+ *          decay before the erase, Alg. 2)
+ *   sGLA:  w = beta_t v_t  (beta_t = 1 when beta is NULL; Alg. 2 writes
+ *          k (x) beta k' (x) v)
+ *   S_t = Sbar + k2_t (x) k_t (x) w
+ *   o_t = sum_{e,k} q2_t[e] q_t[k] S_t[e,k,:]                (Eq. la3)
+ *
+ * k2, q2 are the paper's second key k' and second query q' (dimension E),
+ * K = V = d is the key/value dimension.  The library evaluates it with the
+ * chunkwise-parallel form of Appendix A (Eq. joint-gram, joint-solve,
+ * joint-chunk), with the state tiled along the value axis (Section 2.5,
+ * "Tiling the state").  No 1/sqrt(K) scaling is applied: q, k, q2, k2 are
+ * used as given (the paper L2-normalises them before the operator, Alg. 2).
+ *
+ * Conventions for every entry point
+ *  - Tensors are dense, row-major DEVICE pointers:
+ *      q, k, dq, dk      [B][T][H][K]       v, o, dO, dv   [B][T][H][V]
+ *      q2, k2, dq2, dk2  [B][T][H][E]       g, dg          [B][T][H][E] fp32
+ *      beta, dbeta       [B][T][H] fp32     states         [B][H][E][K][V] fp32
+ *    q, k, v, q2, k2, dO and the gradients dq, dk, dv, dq2, dk2 have the
+ *    element type desc->in_dtype (TLA_F32: float, TLA_BF16: bfloat16); o has
+ *    desc->out_dtype.  g (log-gates, g <= 0 assumed, not checked), beta and
+ *    every state are fp32.
+ *  - Every pointer must be 16-byte aligned.
+ *  - The caller owns every buffer.  The library allocates nothing, keeps no
+ *    per-call state and never synchronises: work is enqueued on `stream`
+ *    (a hipStream_t; NULL = the default stream) in a fixed order, so results
+ *    are bitwise reproducible (no floating-point atomics anywhere).
+ *  - Arguments are validated on the host before anything is enqueued; on
+ *    error nothing is launched and a TLA_E_* code is returned
+ *    (tla_last_error() then describes it).  TLA_E_DEVICE reports a failed
+ *    launch.
+ *  - T need not be a multiple of the chunk: the last chunk is zero-padded
+ *    (k = k2 = 0, g = 0), which leaves the state and the outputs exact.
+ */
+#ifndef TLA_H_
+#define TLA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define TLA_VERSION 1
+
+enum tla_status {
+  TLA_OK = 0,
+  TLA_E_NULL = 1,        /* a required pointer is NULL */
+  TLA_E_SHAPE = 2,       /* a dimension is out of range */
+  TLA_E_UNSUPPORTED = 3, /* no kernel instance for (K, E, chunk, dtype) */
+  TLA_E_ALIGN = 4,       /* a pointer is not 16-byte aligned */
+  TLA_E_WORKSPACE = 5,   /* workspace (or saved buffer) too small */
+  TLA_E_ALIAS = 6,       /* an output overlaps an input it may not alias */
+  TLA_E_DEVICE = 7       /* a HIP launch failed */
+};
+
+enum tla_variant { TLA_SGLA = 0, TLA_GDN = 1 };
+enum tla_dtype { TLA_F32 = 0, TLA_BF16 = 1 };
+enum tla_op { TLA_OP_FWD = 0, TLA_OP_BWD = 1 };
+
+/* Problem description.  struct_size must be sizeof(tla_desc). */
+typedef struct tla_desc {
+  int32_t struct_size;
+  int32_t variant;   /* TLA_SGLA or TLA_GDN */
+  int32_t B, T, H;   /* batch, sequence length, heads */
+  int32_t K, V, E;   /* key dim, value dim, second-key dim */
+  int32_t chunk;     /* chunk length C of the chunkwise form (Appendix A) */
+  int32_t in_dtype;  /* TLA_F32 or TLA_BF16 */
+  int32_t out_dtype; /* element type of o (TLA_F32 or TLA_BF16) */
+} tla_desc;
+
+/*
+ * Supported shapes: K in {16, 32, 64, 128}, V a multiple of 16 up to 1024,
+ * E in {1, 2, 4, 8, 16}, chunk in {16, 32, 64} with chunk <= 64 and the
+ * (K, chunk) pairs instantiated in the library (tla_supported() tells).
+ * Returns 1 if the description is valid and has a kernel instance, else 0.
+ */
+int tla_supported(const tla_desc* desc);
+
+/* Bytes of device workspace needed by tla_fwd (op = TLA_OP_FWD) or tla_bwd
+ * (op = TLA_OP_BWD).  0 if desc is invalid. */
+size_t tla_workspace_bytes(const tla_desc* desc, int op);
+
+/* Bytes of the `saved` buffer that a training forward fills for tla_bwd:
+ * chunk-start states (Appendix A, "Kernels": the forward stores the state at
+ * the start of every chunk so the backward need not recompute it), the
+ * delta-corrected values U and the residual V - W of every chunk, in an
+ * opaque layout.  0 if desc is invalid. */
+size_t tla_saved_bytes(const tla_desc* desc);
+
+/*
+ * Forward (Appendix A, Eq. joint-chunk, with the in-chunk terms of
+ * Eq. joint-gram / joint-solve).
+ *   beta   : may be NULL only for TLA_SGLA (then beta = 1); required for GDN.
+ *   s0     : initial state or NULL (zero).
+ *   o      : output [B][T][H][V] of type out_dtype.
+ *   s_final: final state or NULL.  It may alias s0 (in place).
+ *   saved  : NULL for inference; else a buffer of tla_saved_bytes() that the
+ *            backward consumes (training mode).
+ *   ws     : device workspace of at least tla_workspace_bytes(desc, FWD).
+ */
+int tla_fwd(const tla_desc* desc, const void* q, const void* k, const void* v,
+            const void* q2, const void* k2, const float* g, const float* beta,
+            const float* s0, void* o, float* s_final, void* saved, void* ws,
+            size_t ws_bytes, void* stream);
+
+/*
+ * Backward of tla_fwd.  The eight inputs must be the ones given to the
+ * training forward that filled `saved`.  dO has type in_dtype; dS_final is
+ * the gradient of the final state or NULL (zero).  Outputs: dq, dk, dv, dq2,
+ * dk2 (type in_dtype); dg: gradient with respect to the log-gates g (fp32);
+ * dbeta (fp32) must be NULL exactly when beta is NULL; ds0 (fp32) may be NULL.
+ * Paper reference for the structure: Appendix A, "Kernels" (a reverse
+ * recurrence over chunks for the state gradient, then every other gradient
+ * chunk-parallel, fixed-order reductions).
+ */
+int tla_bwd(const tla_desc* desc, const void* q, const void* k, const void* v,
+            const void* q2, const void* k2, const float* g, const float* beta,
+            const float* s0, const void* dO, const float* dS_final,
+            const void* saved, void* dq, void* dk, void* dv, void* dq2,
+            void* dk2, float* dg, float* dbeta, float* ds0, void* ws,
+            size_t ws_bytes, void* stream);
+
+/*
+ * Recurrent single-token decode step (Eq. forget3 / gdn3 and the read of
+ * Eq. la3, one token): for each of N = desc->B sequences and each head,
+ * decays, (GDN) erases, writes and reads the state in one pass, updating
+ * `state` [N][H][E][K][V] (fp32) in place.  desc->T and desc->chunk are
+ * ignored.  q, k [N][H][K]; v, o [N][H][V]; q2, k2, g [N][H][E]; beta [N][H]
+ * (NULL allowed for sGLA).  o has type out_dtype.
+ */
+int tla_step(const tla_desc* desc, const void* q, const void* k, const void* v,
+             const void* q2, const void* k2, const float* g, const float* beta,
+             float* state, void* o, void* stream);
+
+/* Static description of a status code. */
+const char* tla_status_string(int status);
+/* Message of the last failed call on this host thread ("" if none). */
+const char* tla_last_error(void);
+/* TLA_VERSION of the built library. */
+int tla_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TLA_H_ */

@@ -1,0 +1,206 @@
+"""Triadic linear attention on MI355X (gfx950): Python binding of ``libtla.so``.
+
+The binding only marshals arguments: every step of the operator runs in the
+HIP kernels of the library, behind the C ABI declared in ``include/tla.h``
+(``tla_fwd`` / ``tla_bwd`` / ``tla_step``).  PyTorch supplies device memory and
+the current HIP stream.  There is no fallback: if the library is missing or a
+call fails, an exception is raised.
+
+Shapes (row-major, contiguous):
+  q, k [B,T,H,K]; v [B,T,H,V]; q2, k2 [B,T,H,E]; g (log-gates) [B,T,H,E] fp32;
+  beta [B,T,H] fp32 or None (sGLA only); states [B,H,E,K,V] fp32.
+"""
+import ctypes
+import os
+
+import torch
+
+SGLA, GDN = 0, 1
+F32, BF16 = 0, 1
+OP_FWD, OP_BWD = 0, 1
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtla.so")
+_lib = None
+
+
+class Desc(ctypes.Structure):
+    _fields_ = [(name, ctypes.c_int32) for name in
+                ("struct_size", "variant", "B", "T", "H", "K", "V", "E", "chunk",
+                 "in_dtype", "out_dtype")]
+
+
+class TLAError(RuntimeError):
+    pass
+
+
+def lib():
+    """Loads the built HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with "
+                          "`python -m paper_2609_36529_amd.build` (hipcc, gfx950)")
+    L = ctypes.CDLL(LIB_PATH)
+    P, S, I = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int
+    DP = ctypes.POINTER(Desc)
+    L.tla_version.restype = I
+    L.tla_last_error.restype = ctypes.c_char_p
+    L.tla_status_string.restype = ctypes.c_char_p
+    L.tla_status_string.argtypes = [I]
+    L.tla_supported.argtypes = [DP]
+    L.tla_supported.restype = I
+    L.tla_workspace_bytes.argtypes = [DP, I]
+    L.tla_workspace_bytes.restype = S
+    L.tla_saved_bytes.argtypes = [DP]
+    L.tla_saved_bytes.restype = S
+    L.tla_fwd.argtypes = [DP] + [P] * 12 + [S, P]
+    L.tla_fwd.restype = I
+    L.tla_bwd.argtypes = [DP] + [P] * 20 + [S, P]
+    L.tla_bwd.restype = I
+    L.tla_step.argtypes = [DP] + [P] * 9 + [P]
+    L.tla_step.restype = I
+    _lib = L
+    return L
+
+
+def _dtype_code(t):
+    if t == torch.float32:
+        return F32
+    if t == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported dtype {t}")
+
+
+def make_desc(variant, B, T, H, K, V, E, chunk, in_dtype, out_dtype):
+    d = Desc()
+    d.struct_size = ctypes.sizeof(Desc)
+    d.variant, d.B, d.T, d.H, d.K, d.V, d.E, d.chunk = variant, B, T, H, K, V, E, chunk
+    d.in_dtype, d.out_dtype = in_dtype, out_dtype
+    return d
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _check(rc):
+    if rc != 0:
+        L = lib()
+        raise TLAError(f"{L.tla_status_string(rc).decode()} ({L.tla_last_error().decode()})")
+
+
+def _stream(device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _need(t, name, dtype=None, device=None):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+    return t
+
+
+def describe(variant, q, v, q2, chunk, out_dtype=None):
+    B, T, H, K = q.shape
+    return make_desc(variant, B, T, H, K, v.shape[-1], q2.shape[-1], chunk, _dtype_code(q.dtype),
+                     _dtype_code(out_dtype if out_dtype is not None else q.dtype))
+
+
+def supported(desc):
+    return bool(lib().tla_supported(ctypes.byref(desc)))
+
+
+def workspace_bytes(desc, op):
+    return int(lib().tla_workspace_bytes(ctypes.byref(desc), op))
+
+
+def saved_bytes(desc):
+    return int(lib().tla_saved_bytes(ctypes.byref(desc)))
+
+
+def fwd(variant, q, k, v, q2, k2, g, beta=None, s0=None, chunk=64, out_dtype=None,
+        want_final=True, training=False, o=None, s_final=None, ws=None, saved=None):
+    """Chunkwise forward.  Returns (o, s_final or None, saved or None)."""
+    dev = q.device
+    dt = q.dtype
+    for name, t in (("q", q), ("k", k), ("v", v), ("q2", q2), ("k2", k2)):
+        _need(t, name, dt, dev)
+    _need(g, "g", torch.float32, dev)
+    _need(beta, "beta", torch.float32, dev)
+    _need(s0, "s0", torch.float32, dev)
+    desc = describe(variant, q, v, q2, chunk, out_dtype)
+    B, T, H, K = q.shape
+    V, E = v.shape[-1], q2.shape[-1]
+    if o is None:
+        o = torch.empty((B, T, H, V), dtype=out_dtype or dt, device=dev)
+    if want_final and s_final is None:
+        s_final = torch.empty((B, H, E, K, V), dtype=torch.float32, device=dev)
+    if ws is None:
+        ws = torch.empty(max(workspace_bytes(desc, OP_FWD), 1), dtype=torch.uint8, device=dev)
+    if training and saved is None:
+        saved = torch.empty(max(saved_bytes(desc), 1), dtype=torch.uint8, device=dev)
+    rc = lib().tla_fwd(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(q2), _ptr(k2), _ptr(g),
+                       _ptr(beta), _ptr(s0), _ptr(o), _ptr(s_final if want_final else None),
+                       _ptr(saved if training else None), _ptr(ws), ws.numel(), _stream(dev))
+    _check(rc)
+    return o, (s_final if want_final else None), (saved if training else None)
+
+
+def bwd(variant, q, k, v, q2, k2, g, beta, s0, dO, saved, dS_final=None, chunk=64,
+        want_ds0=True, ws=None, grads=None):
+    """Backward of a training forward.  Returns a dict of gradients
+    (dq, dk, dv, dq2, dk2, dg, dbeta or None, ds0 or None)."""
+    dev = q.device
+    dt = q.dtype
+    desc = describe(variant, q, v, q2, chunk)
+    B, T, H, K = q.shape
+    V, E = v.shape[-1], q2.shape[-1]
+    _need(dO, "dO", dt, dev)
+    _need(dS_final, "dS_final", torch.float32, dev)
+    if grads is None:
+        grads = {
+            "dq": torch.empty_like(q), "dk": torch.empty_like(k), "dv": torch.empty_like(v),
+            "dq2": torch.empty_like(q2), "dk2": torch.empty_like(k2),
+            "dg": torch.empty((B, T, H, E), dtype=torch.float32, device=dev),
+            "dbeta": None if beta is None else torch.empty((B, T, H), dtype=torch.float32, device=dev),
+            "ds0": torch.empty((B, H, E, K, V), dtype=torch.float32, device=dev) if want_ds0 else None,
+        }
+    if ws is None:
+        ws = torch.empty(max(workspace_bytes(desc, OP_BWD), 1), dtype=torch.uint8, device=dev)
+    rc = lib().tla_bwd(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(q2), _ptr(k2), _ptr(g),
+                       _ptr(beta), _ptr(s0), _ptr(dO), _ptr(dS_final), _ptr(saved),
+                       _ptr(grads["dq"]), _ptr(grads["dk"]), _ptr(grads["dv"]), _ptr(grads["dq2"]),
+                       _ptr(grads["dk2"]), _ptr(grads["dg"]), _ptr(grads["dbeta"]),
+                       _ptr(grads["ds0"]), _ptr(ws), ws.numel(), _stream(dev))
+    _check(rc)
+    return grads
+
+
+def step(variant, q, k, v, q2, k2, g, beta, state, out_dtype=None, o=None):
+    """One decode token per (sequence, head); updates `state` in place.
+    q, k [N,H,K]; v [N,H,V]; q2, k2, g [N,H,E]; beta [N,H] or None."""
+    dev = q.device
+    N, H, K = q.shape
+    V, E = v.shape[-1], q2.shape[-1]
+    for name, t in (("q", q), ("k", k), ("v", v), ("q2", q2), ("k2", k2)):
+        _need(t, name, q.dtype, dev)
+    _need(g, "g", torch.float32, dev)
+    _need(beta, "beta", torch.float32, dev)
+    _need(state, "state", torch.float32, dev)
+    desc = make_desc(variant, N, 1, H, K, V, E, 16, _dtype_code(q.dtype),
+                     _dtype_code(out_dtype or q.dtype))
+    if o is None:
+        o = torch.empty((N, H, V), dtype=out_dtype or q.dtype, device=dev)
+    rc = lib().tla_step(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(q2), _ptr(k2), _ptr(g),
+                        _ptr(beta), _ptr(state), _ptr(o), _stream(dev))
+    _check(rc)
+    return o

@@ -1,0 +1,338 @@
+// C ABI of the triadic linear attention library: host-side validation,
+// workspace carving and the fixed launch sequence of each entry point.
+// Validation never touches the device, so a rejected call launches nothing.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <hip/hip_runtime.h>
+
+#include "../../include/tla.h"
+#include "tla_internal.hpp"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+bool misaligned(const void* p) { return p && ((uintptr_t)p & 15u) != 0; }
+
+bool pow2_in(int x, const int* set, int n) {
+  for (int i = 0; i < n; ++i)
+    if (x == set[i]) return true;
+  return false;
+}
+
+// Validates a description; fills the internal shape.  `for_step` skips the
+// chunk-related checks.
+int check_desc(const tla_desc* d, tla::Shape* s, bool for_step) {
+  if (!d) return fail(TLA_E_NULL, "desc is NULL");
+  if (d->struct_size != (int32_t)sizeof(tla_desc))
+    return fail(TLA_E_SHAPE, "desc->struct_size %d != %d", d->struct_size, (int)sizeof(tla_desc));
+  if (d->variant != TLA_SGLA && d->variant != TLA_GDN)
+    return fail(TLA_E_SHAPE, "variant %d is neither TLA_SGLA nor TLA_GDN", d->variant);
+  if (d->in_dtype != TLA_F32 && d->in_dtype != TLA_BF16)
+    return fail(TLA_E_SHAPE, "in_dtype %d", d->in_dtype);
+  if (d->out_dtype != TLA_F32 && d->out_dtype != TLA_BF16)
+    return fail(TLA_E_SHAPE, "out_dtype %d", d->out_dtype);
+  if (d->B < 1 || d->H < 1) return fail(TLA_E_SHAPE, "B=%d H=%d must be >= 1", d->B, d->H);
+  if (!for_step && d->T < 0) return fail(TLA_E_SHAPE, "T=%d must be >= 0", d->T);
+  static const int Ks[] = {16, 32, 64, 128};
+  static const int Es[] = {1, 2, 4, 8, 16};
+  static const int Cs[] = {16, 32, 64};
+  if (!pow2_in(d->K, Ks, 4)) return fail(TLA_E_UNSUPPORTED, "K=%d not in {16,32,64,128}", d->K);
+  if (d->V < 16 || d->V > 1024 || d->V % 16 != 0)
+    return fail(TLA_E_UNSUPPORTED, "V=%d must be a multiple of 16 in [16, 1024]", d->V);
+  if (!pow2_in(d->E, Es, 5)) return fail(TLA_E_UNSUPPORTED, "E=%d not in {1,2,4,8,16}", d->E);
+  if (!for_step) {
+    if (!pow2_in(d->chunk, Cs, 3)) return fail(TLA_E_UNSUPPORTED, "chunk=%d not in {16,32,64}", d->chunk);
+    if (!tla::have_instance(d->K, d->chunk, d->E))
+      return fail(TLA_E_UNSUPPORTED, "no kernel instance for K=%d chunk=%d E=%d", d->K, d->chunk, d->E);
+    if (!tla::fits_lds(d->K, d->chunk, d->E, d->in_dtype == TLA_BF16))
+      return fail(TLA_E_UNSUPPORTED, "K=%d chunk=%d E=%d with %s operands exceeds the LDS budget",
+                  d->K, d->chunk, d->E, d->in_dtype == TLA_BF16 ? "bf16" : "fp32");
+  } else {
+    const bool ok = (d->K == 16 && d->E == 4) || (d->K == 32 && d->E == 4) ||
+                    (d->K == 64 && d->E == 8) ||
+                    (d->K == 128 && (d->E == 1 || d->E == 4 || d->E == 8 || d->E == 16));
+    if (!ok) return fail(TLA_E_UNSUPPORTED, "no step instance for K=%d E=%d", d->K, d->E);
+  }
+  if ((double)d->B * d->H * (for_step ? 1 : (d->T > 0 ? d->T : 1)) * (d->K > d->V ? d->K : d->V) >
+      (double)(1ull << 40))
+    return fail(TLA_E_SHAPE, "problem too large");
+  s->variant = d->variant;
+  s->B = d->B;
+  s->T = for_step ? 1 : d->T;
+  s->H = d->H;
+  s->K = d->K;
+  s->V = d->V;
+  s->E = d->E;
+  s->C = for_step ? 16 : d->chunk;
+  s->Nc = for_step ? 1 : (d->T + d->chunk - 1) / d->chunk;
+  s->NH = d->B * d->H;
+  s->in_bf16 = d->in_dtype == TLA_BF16;
+  s->out_bf16 = d->out_dtype == TLA_BF16;
+  s->has_beta = 0;
+  return TLA_OK;
+}
+
+size_t esize(const tla::Shape& s) { return s.in_bf16 ? 2 : 4; }
+
+struct Layout {
+  size_t prep_coef, prep_gC, prep_M, prep_Tu, prep_end;
+  size_t bwd_dS, bwd_dU, bwd_dW, bwd_dqs, bwd_dks, bwd_dcoef, bwd_dgC, bwd_end;
+  size_t sv_S, sv_U, sv_X, sv_end;
+};
+
+Layout layout(const tla::Shape& s) {
+  Layout L;
+  const size_t nch = (size_t)s.NH * s.Nc;
+  const size_t es = esize(s);
+  const size_t E4 = tla::round4(s.E);
+  size_t o = 0;
+  L.prep_coef = o; o += align256(nch * 3 * s.E * s.C * 4);
+  L.prep_gC = o;   o += align256(nch * E4 * 4);
+  L.prep_M = o;    o += align256(nch * s.C * s.C * 4);
+  L.prep_Tu = o;   o += align256(nch * s.C * s.C * 4);
+  L.prep_end = o;
+  L.bwd_dS = o;    o += align256(nch * s.E * s.K * s.V * es);
+  L.bwd_dU = o;    o += align256(nch * s.C * s.V * 4);
+  L.bwd_dW = o;    o += align256(nch * s.C * s.V * 4);
+  L.bwd_dqs = o;   o += align256(nch * s.C * s.K * 4);
+  L.bwd_dks = o;   o += align256(nch * s.C * s.K * 4);
+  L.bwd_dcoef = o; o += align256(nch * 3 * s.E * s.C * 4);
+  L.bwd_dgC = o;   o += align256(nch * E4 * 4);
+  L.bwd_end = o;
+  o = 0;
+  L.sv_S = o; o += align256(nch * s.E * s.K * s.V * es);
+  L.sv_U = o; o += align256(nch * s.C * s.V * 4);
+  L.sv_X = o; o += align256(nch * s.C * s.V * 4);
+  L.sv_end = o;
+  return L;
+}
+
+tla::PrepBufs prep_bufs(const Layout& L, void* ws) {
+  char* b = (char*)ws;
+  return tla::PrepBufs{(float*)(b + L.prep_coef), (float*)(b + L.prep_gC),
+                       (float*)(b + L.prep_M), (float*)(b + L.prep_Tu)};
+}
+tla::SavedBufs saved_bufs(const Layout& L, const void* saved) {
+  char* b = (char*)saved;
+  return tla::SavedBufs{b + L.sv_S, (float*)(b + L.sv_U), (float*)(b + L.sv_X)};
+}
+
+struct Range {
+  const void* p;
+  size_t n;
+};
+bool overlap(Range a, Range b) {
+  if (!a.p || !b.p || !a.n || !b.n) return false;
+  const char* a0 = (const char*)a.p;
+  const char* b0 = (const char*)b.p;
+  return a0 < b0 + b.n && b0 < a0 + a.n;
+}
+
+int device_fail(hipError_t e, const char* what) {
+  return fail(TLA_E_DEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+}  // namespace
+
+extern "C" {
+
+int tla_version(void) { return TLA_VERSION; }
+
+const char* tla_last_error(void) { return g_err; }
+
+const char* tla_status_string(int st) {
+  switch (st) {
+    case TLA_OK: return "TLA_OK";
+    case TLA_E_NULL: return "TLA_E_NULL: a required pointer is NULL";
+    case TLA_E_SHAPE: return "TLA_E_SHAPE: a dimension is out of range";
+    case TLA_E_UNSUPPORTED: return "TLA_E_UNSUPPORTED: no kernel instance for this shape";
+    case TLA_E_ALIGN: return "TLA_E_ALIGN: a pointer is not 16-byte aligned";
+    case TLA_E_WORKSPACE: return "TLA_E_WORKSPACE: workspace or saved buffer too small";
+    case TLA_E_ALIAS: return "TLA_E_ALIAS: an output overlaps an input";
+    case TLA_E_DEVICE: return "TLA_E_DEVICE: a HIP launch failed";
+    default: return "unknown tla status";
+  }
+}
+
+int tla_supported(const tla_desc* d) {
+  tla::Shape s;
+  return check_desc(d, &s, false) == TLA_OK ? 1 : 0;
+}
+
+size_t tla_workspace_bytes(const tla_desc* d, int op) {
+  tla::Shape s;
+  if (check_desc(d, &s, false) != TLA_OK) return 0;
+  const Layout L = layout(s);
+  if (op == TLA_OP_FWD) return L.prep_end;
+  if (op == TLA_OP_BWD) return L.bwd_end;
+  return 0;
+}
+
+size_t tla_saved_bytes(const tla_desc* d) {
+  tla::Shape s;
+  if (check_desc(d, &s, false) != TLA_OK) return 0;
+  return layout(s).sv_end;
+}
+
+int tla_fwd(const tla_desc* d, const void* q, const void* k, const void* v, const void* q2,
+            const void* k2, const float* g, const float* beta, const float* s0, void* o,
+            float* s_final, void* saved, void* ws, size_t ws_bytes, void* stream) {
+  g_err[0] = 0;
+  tla::Shape s;
+  int rc = check_desc(d, &s, false);
+  if (rc) return rc;
+  const size_t ntok = (size_t)s.B * s.T * s.H;
+  if (s.T > 0 && (!q || !k || !v || !q2 || !k2 || !g || !o))
+    return fail(TLA_E_NULL, "q, k, v, q2, k2, g and o are required");
+  if (s.variant == TLA_GDN && s.T > 0 && !beta) return fail(TLA_E_NULL, "GDN needs beta");
+  const void* ptrs[] = {q, k, v, q2, k2, g, beta, s0, o, s_final, saved, ws};
+  for (const void* p : ptrs)
+    if (misaligned(p)) return fail(TLA_E_ALIGN, "pointer %p is not 16-byte aligned", p);
+  const Layout L = layout(s);
+  if (s.T > 0 && (!ws || ws_bytes < L.prep_end))
+    return fail(TLA_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, L.prep_end);
+  const size_t es = esize(s), os = s.out_bf16 ? 2 : 4;
+  const size_t sbytes = (size_t)s.NH * s.E * s.K * s.V * 4;
+  const Range ins[] = {{q, ntok * s.K * es}, {k, ntok * s.K * es}, {v, ntok * s.V * es},
+                       {q2, ntok * s.E * es}, {k2, ntok * s.E * es}, {g, ntok * s.E * 4},
+                       {beta, beta ? ntok * 4 : 0}, {s0, s0 ? sbytes : 0}};
+  const Range outs[] = {{o, ntok * s.V * os}, {saved, saved ? L.sv_end : 0},
+                        {ws, s.T > 0 ? L.prep_end : 0}};
+  for (const Range& a : outs)
+    for (const Range& b : ins)
+      if (overlap(a, b)) return fail(TLA_E_ALIAS, "an output or buffer overlaps an input");
+  if (s_final) {
+    for (const Range& b : ins) {
+      if (b.p == s0) continue;  // in place is allowed
+      if (overlap({s_final, sbytes}, b)) return fail(TLA_E_ALIAS, "s_final overlaps an input");
+    }
+    if (s0 && s0 != s_final && overlap({s_final, sbytes}, {s0, sbytes}))
+      return fail(TLA_E_ALIAS, "s_final partially overlaps s0");
+    for (const Range& b : outs)
+      if (overlap({s_final, sbytes}, b)) return fail(TLA_E_ALIAS, "s_final overlaps an output");
+  }
+  if (overlap(outs[0], outs[1]) || overlap(outs[0], outs[2]) || overlap(outs[1], outs[2]))
+    return fail(TLA_E_ALIAS, "o, saved and ws must not overlap");
+
+  hipStream_t st = (hipStream_t)stream;
+  s.has_beta = beta != nullptr;
+  tla::FwdIn in{q, k, v, q2, k2, g, beta, s0};
+  const tla::PrepBufs pb = prep_bufs(L, ws);
+  hipError_t e;
+  if (s.T > 0) {
+    e = tla::launch_prep(s, in, pb, st);
+    if (e != hipSuccess) return device_fail(e, "prep kernel");
+  }
+  if (s.T > 0 || s_final) {
+    tla::SavedBufs sv = saved_bufs(L, saved);
+    e = tla::launch_fwd(s, in, pb, o, s_final, saved ? &sv : nullptr, st);
+    if (e != hipSuccess) return device_fail(e, "forward kernel");
+  }
+  return TLA_OK;
+}
+
+int tla_bwd(const tla_desc* d, const void* q, const void* k, const void* v, const void* q2,
+            const void* k2, const float* g, const float* beta, const float* s0, const void* dO,
+            const float* dS_final, const void* saved, void* dq, void* dk, void* dv, void* dq2,
+            void* dk2, float* dg, float* dbeta, float* ds0, void* ws, size_t ws_bytes,
+            void* stream) {
+  g_err[0] = 0;
+  tla::Shape s;
+  int rc = check_desc(d, &s, false);
+  if (rc) return rc;
+  if (s.T < 1) return fail(TLA_E_SHAPE, "the backward needs T >= 1");
+  if (!q || !k || !v || !q2 || !k2 || !g || !dO || !saved || !dq || !dk || !dv || !dq2 || !dk2 ||
+      !dg || !ws)
+    return fail(TLA_E_NULL, "a required pointer is NULL");
+  if (s.variant == TLA_GDN && !beta) return fail(TLA_E_NULL, "GDN needs beta");
+  if ((beta == nullptr) != (dbeta == nullptr))
+    return fail(TLA_E_NULL, "dbeta must be given exactly when beta is");
+  const void* ptrs[] = {q, k, v, q2, k2, g, beta, s0, dO, dS_final, saved, dq,
+                        dk, dv, dq2, dk2, dg, dbeta, ds0, ws};
+  for (const void* p : ptrs)
+    if (misaligned(p)) return fail(TLA_E_ALIGN, "pointer %p is not 16-byte aligned", p);
+  const Layout L = layout(s);
+  if (ws_bytes < L.bwd_end) return fail(TLA_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, L.bwd_end);
+  const size_t ntok = (size_t)s.B * s.T * s.H;
+  const size_t es = esize(s);
+  const size_t sbytes = (size_t)s.NH * s.E * s.K * s.V * 4;
+  const Range ins[] = {{q, ntok * s.K * es}, {k, ntok * s.K * es}, {v, ntok * s.V * es},
+                       {q2, ntok * s.E * es}, {k2, ntok * s.E * es}, {g, ntok * s.E * 4},
+                       {beta, beta ? ntok * 4 : 0}, {s0, s0 ? sbytes : 0},
+                       {dO, ntok * s.V * es}, {dS_final, dS_final ? sbytes : 0},
+                       {saved, L.sv_end}};
+  const Range outs[] = {{dq, ntok * s.K * es}, {dk, ntok * s.K * es}, {dv, ntok * s.V * es},
+                        {dq2, ntok * s.E * es}, {dk2, ntok * s.E * es}, {dg, ntok * s.E * 4},
+                        {dbeta, dbeta ? ntok * 4 : 0}, {ds0, ds0 ? sbytes : 0},
+                        {ws, L.bwd_end}};
+  const int nouts = sizeof(outs) / sizeof(outs[0]);
+  for (const Range& a : outs)
+    for (const Range& b : ins)
+      if (overlap(a, b)) return fail(TLA_E_ALIAS, "a gradient or the workspace overlaps an input");
+  for (int i = 0; i < nouts; ++i)
+    for (int j = i + 1; j < nouts; ++j)
+      if (overlap(outs[i], outs[j])) return fail(TLA_E_ALIAS, "two outputs overlap");
+
+  hipStream_t st = (hipStream_t)stream;
+  s.has_beta = beta != nullptr;
+  tla::FwdIn in{q, k, v, q2, k2, g, beta, s0};
+  const tla::PrepBufs pb = prep_bufs(L, ws);
+  char* wb = (char*)ws;
+  const tla::BwdBufs bb{wb + L.bwd_dS, (float*)(wb + L.bwd_dU), (float*)(wb + L.bwd_dW),
+                        (float*)(wb + L.bwd_dqs), (float*)(wb + L.bwd_dks),
+                        (float*)(wb + L.bwd_dcoef), (float*)(wb + L.bwd_dgC)};
+  const tla::SavedBufs sv = saved_bufs(L, saved);
+  hipError_t e = tla::launch_prep(s, in, pb, st);
+  if (e != hipSuccess) return device_fail(e, "prep kernel");
+  e = tla::launch_bwd_rec(s, in, dO, dS_final, pb, bb, ds0, st);
+  if (e != hipSuccess) return device_fail(e, "backward recurrent kernel");
+  e = tla::launch_bwd_state(s, in, dO, pb, sv, bb, st);
+  if (e != hipSuccess) return device_fail(e, "backward state-gradient kernel");
+  e = tla::launch_bwd_chunk(s, in, dO, sv, bb, dq, dk, dv, dq2, dk2, dg, dbeta, st);
+  if (e != hipSuccess) return device_fail(e, "backward chunk kernel");
+  return TLA_OK;
+}
+
+int tla_step(const tla_desc* d, const void* q, const void* k, const void* v, const void* q2,
+             const void* k2, const float* g, const float* beta, float* state, void* o,
+             void* stream) {
+  g_err[0] = 0;
+  tla::Shape s;
+  int rc = check_desc(d, &s, true);
+  if (rc) return rc;
+  if (!q || !k || !v || !q2 || !k2 || !g || !state || !o)
+    return fail(TLA_E_NULL, "q, k, v, q2, k2, g, state and o are required");
+  if (s.variant == TLA_GDN && !beta) return fail(TLA_E_NULL, "GDN needs beta");
+  const void* ptrs[] = {q, k, v, q2, k2, g, beta, state, o};
+  for (const void* p : ptrs)
+    if (misaligned(p)) return fail(TLA_E_ALIGN, "pointer %p is not 16-byte aligned", p);
+  const size_t n = (size_t)s.NH, es = esize(s), os = s.out_bf16 ? 2 : 4;
+  const Range ins[] = {{q, n * s.K * es}, {k, n * s.K * es}, {v, n * s.V * es},
+                       {q2, n * s.E * es}, {k2, n * s.E * es}, {g, n * s.E * 4},
+                       {beta, beta ? n * 4 : 0}};
+  const Range outs[] = {{state, n * s.E * s.K * s.V * 4}, {o, n * s.V * os}};
+  for (const Range& a : outs)
+    for (const Range& b : ins)
+      if (overlap(a, b)) return fail(TLA_E_ALIAS, "state or o overlaps an input");
+  if (overlap(outs[0], outs[1])) return fail(TLA_E_ALIAS, "state and o overlap");
+  s.has_beta = beta != nullptr;
+  tla::FwdIn in{q, k, v, q2, k2, g, beta, nullptr};
+  hipError_t e = tla::launch_step(s, in, state, o, (hipStream_t)stream);
+  if (e != hipSuccess) return device_fail(e, "step kernel");
+  return TLA_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,168 @@
+// Device helpers shared by the triadic linear attention kernels (gfx950).
+//
+// Fragment convention (64-wide wavefront, 16x16 MFMA tiles):
+//   lane l, group g = l / 16, index n = l % 16
+//   A fragment of a 16 x 16k block: lane holds A[n][4g + j], j = 0..3
+//   B fragment of a 16k x 16 block: lane holds B[4g + j][n], j = 0..3
+//   accumulator (16 x 16, fp32):    lane holds C[4g + j][n], j = 0..3
+// An accumulator is therefore already the B fragment of itself (its row index
+// is the contraction index) and the A fragment of its transpose.  Two 16-deep
+// bf16 fragments feed one v_mfma_f32_16x16x32_bf16 (slots 0..3 from the first
+// block, 4..7 from the second); the contraction does not depend on how the
+// hardware orders k inside an instruction as long as A and B agree.  fp32
+// operands go through four v_mfma_f32_16x16x4_f32 per 16-deep block.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace tla {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef uint16_t bf16_t;  // bf16 storage in global memory
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+__device__ __forceinline__ int wave_id() { return threadIdx.x >> 6; }
+
+__device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
+
+// ---------------------------------------------------------------- scalar I/O
+template <typename T> struct Elem;
+template <> struct Elem<float> {
+  typedef float storage;
+  typedef f32x4 frag;  // 4 operand values of a 16-deep fragment
+  __device__ static __forceinline__ float to_f(float x) { return x; }
+  __device__ static __forceinline__ float from_f(float x) { return x; }
+};
+template <> struct Elem<bf16_t> {
+  typedef bf16_t storage;
+  typedef bf16x4 frag;
+  __device__ static __forceinline__ float to_f(bf16_t x) {
+    return __uint_as_float(((uint32_t)x) << 16);
+  }
+  __device__ static __forceinline__ bf16_t from_f(float x) {
+    __bf16 b = (__bf16)x;  // round to nearest even
+    return __builtin_bit_cast(bf16_t, b);
+  }
+};
+
+template <typename T>
+__device__ __forceinline__ float ld_f(const T* p) { return Elem<T>::to_f(*p); }
+
+// 4 consecutive elements as floats (p aligned to 4 elements)
+__device__ __forceinline__ f32x4 ld4_f(const float* p) { return *(const f32x4*)p; }
+__device__ __forceinline__ f32x4 ld4_f(const bf16_t* p) {
+  uint2 u = *(const uint2*)p;
+  f32x4 r;
+  r[0] = __uint_as_float(u.x << 16);
+  r[1] = __uint_as_float(u.x & 0xffff0000u);
+  r[2] = __uint_as_float(u.y << 16);
+  r[3] = __uint_as_float(u.y & 0xffff0000u);
+  return r;
+}
+
+// ------------------------------------------------------------- fragments
+// Load a 4-element fragment from contiguous storage.
+__device__ __forceinline__ f32x4 ld_frag(const float* p) { return *(const f32x4*)p; }
+__device__ __forceinline__ bf16x4 ld_frag(const bf16_t* p) {
+  return __builtin_bit_cast(bf16x4, *(const uint2*)p);
+}
+
+// Convert 4 fp32 values (e.g. an accumulator) into an operand fragment.
+template <typename T> __device__ __forceinline__ typename Elem<T>::frag cvt_frag(f32x4 x);
+template <> __device__ __forceinline__ f32x4 cvt_frag<float>(f32x4 x) { return x; }
+template <> __device__ __forceinline__ bf16x4 cvt_frag<bf16_t>(f32x4 x) {
+  bf16x4 r;
+  r[0] = (__bf16)x[0];
+  r[1] = (__bf16)x[1];
+  r[2] = (__bf16)x[2];
+  r[3] = (__bf16)x[3];
+  return r;
+}
+
+// Split 4 fp32 values into a bf16 pair hi + lo whose sum carries ~16
+// mantissa bits: hi = rne(x), lo = rne(x - hi).  Used for the fp32-computed
+// operands (U, M, Tu) whose plain bf16 rounding would dominate the error.
+__device__ __forceinline__ f32x4 bf16x4_to_f(bf16x4 x) {
+  return f32x4{(float)x[0], (float)x[1], (float)x[2], (float)x[3]};
+}
+__device__ __forceinline__ void split_frag(f32x4 x, bf16x4& hi, bf16x4& lo) {
+  hi = cvt_frag<bf16_t>(x);
+  lo = cvt_frag<bf16_t>(x - bf16x4_to_f(hi));
+}
+__device__ __forceinline__ void split_frag(f32x4 x, f32x4& hi, f32x4& lo) {
+  hi = x;
+  lo = zero4();
+}
+
+// Gather 4 strided elements into a fragment (stride in elements).
+template <typename T>
+__device__ __forceinline__ typename Elem<T>::frag ld_frag_strided(const T* p, int stride) {
+  f32x4 x;
+  x[0] = Elem<T>::to_f(p[0]);
+  x[1] = Elem<T>::to_f(p[stride]);
+  x[2] = Elem<T>::to_f(p[2 * stride]);
+  x[3] = Elem<T>::to_f(p[3 * stride]);
+  return cvt_frag<T>(x);
+}
+
+// ------------------------------------------------------------------ MFMA
+__device__ __forceinline__ void mma16(f32x4& acc, f32x4 a, f32x4 b) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[0], b[0], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[1], b[1], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[2], b[2], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[3], b[3], acc, 0, 0, 0);
+}
+__device__ __forceinline__ void mma16(f32x4& acc, bf16x4 a, bf16x4 b) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(i16x4, a),
+                                                  __builtin_bit_cast(i16x4, b), acc, 0, 0, 0);
+}
+// Two 16-deep blocks at once.
+__device__ __forceinline__ void mma32(f32x4& acc, f32x4 a0, f32x4 a1, f32x4 b0, f32x4 b1) {
+  mma16(acc, a0, b0);
+  mma16(acc, a1, b1);
+}
+__device__ __forceinline__ void mma32(f32x4& acc, bf16x4 a0, bf16x4 a1, bf16x4 b0, bf16x4 b1) {
+  bf16x8 a = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
+  bf16x8 b = __builtin_shufflevector(b0, b1, 0, 1, 2, 3, 4, 5, 6, 7);
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc, 0, 0, 0);
+}
+
+// Fast exp of a non-positive argument (every decay factor here is exp of a
+// difference of accumulated log-gates that is <= 0).
+__device__ __forceinline__ float exp_nonpos(float x) { return __expf(x); }
+
+// ------------------------------------------------------------- reductions
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+  return x;
+}
+// Sum over the 16 lanes that share a group g (lanes 16g .. 16g + 15).
+__device__ __forceinline__ float group16_sum(float x) {
+#pragma unroll
+  for (int o = 8; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+  return x;
+}
+
+// XCD-aware block mapping: the 8 accelerator dies each have their own L2 and
+// receive blocks round-robin by linear id.  Blocks that share a head (the
+// value tiles of one head read the same chunk inputs) are placed on one die.
+// Returns the (head, tile) pair for a linear block id.
+__device__ __forceinline__ void xcd_map(int bid, int nheads, int ntiles, int& head, int& tile) {
+  if ((nheads & 7) == 0) {
+    const int xcd = bid & 7;
+    const int j = bid >> 3;
+    tile = j % ntiles;
+    head = (j / ntiles) * 8 + xcd;
+  } else {
+    head = bid / ntiles;
+    tile = bid % ntiles;
+  }
+}
+
+}  // namespace tla

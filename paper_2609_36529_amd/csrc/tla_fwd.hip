@@ -1,0 +1,606 @@
+// Forward of chunkwise triadic linear attention on gfx950.
+//
+//   k_prep  one workgroup per (head, chunk), chunk-parallel:
+//           in-chunk cumulative log-gates G (Appendix A: gamma^r_e is the
+//           product of the slice's gates over positions 1..r), the row
+//           coefficient vectors a_e = k'_e o gamma_e, b_e = q'_e o gamma_e,
+//           c_e = k'_e o gamma^C_e / gamma_e, gamma^C_e; A_qk = Q K^T and
+//           A_kk = K K^T on MFMA; the decayed second-key Grams R (Eq.
+//           joint-gram) and R' formed element by element from exponentials of
+//           non-positive log-gate differences (Appendix A, numerical
+//           stability); M = A_qk o R'; and the UT transform
+//           Tu = (I + tril(diag(beta)(A_kk o R), -1))^{-1} diag(beta)
+//           (Eq. joint-solve) by fp32 forward substitution.
+//   k_fwd   one workgroup per (head, 16-column value tile), sequential over
+//           chunks (Eq. joint-chunk).  The E x K x 16 fp32 state tile lives
+//           in MFMA accumulators for the whole sequence; each wave owns
+//           E / waves slices.  Per chunk:
+//             P^K_e = K S_e,  P^Q_e = Q S_e                     (MFMA)
+//             W = sum_e diag(a_e) P^K_e                         (LDS reduce)
+//             U = Tu (V - W)   [GDN]   or   diag(beta) V  [sGLA]
+//             O = sum_e diag(b_e) P^Q_e + M U
+//             S_e <- gamma^C_e S_e + K^T diag(c_e) U            (MFMA)
+//           Tu is applied to the residual (no per-slice W = T K precompute).
+//           Value columns never interact (Eq. slices), which is what makes
+//           the 16-column tiling exact.
+#include "tla_common.hpp"
+#include "tla_internal.hpp"
+
+namespace tla {
+
+template <typename T>
+__device__ __forceinline__ void copy8(T* dst, const T* src) {
+  if constexpr (sizeof(T) == 2) {
+    *(uint4*)dst = *(const uint4*)src;
+  } else {
+    ((float4*)dst)[0] = ((const float4*)src)[0];
+    ((float4*)dst)[1] = ((const float4*)src)[1];
+  }
+}
+template <typename T>
+__device__ __forceinline__ void zero8(T* dst) {
+  if constexpr (sizeof(T) == 2) {
+    *(uint4*)dst = make_uint4(0, 0, 0, 0);
+  } else {
+    ((float4*)dst)[0] = make_float4(0, 0, 0, 0);
+    ((float4*)dst)[1] = make_float4(0, 0, 0, 0);
+  }
+}
+
+// Contraction over a D-deep axis given fragment accessors for A and B.
+// fa(kb) / fb(kb) return the 16-deep fragment of block kb.
+template <int D, typename FA, typename FB>
+__device__ __forceinline__ void mma_k(f32x4& acc, FA fa, FB fb) {
+  constexpr int NB = D / 16;
+#pragma unroll
+  for (int kb = 0; kb + 1 < NB; kb += 2) mma32(acc, fa(kb), fa(kb + 1), fb(kb), fb(kb + 1));
+  if constexpr (NB & 1) mma16(acc, fa(NB - 1), fb(NB - 1));
+}
+
+// ------------------------------------------------------------------- prep
+template <typename T, int KD, int C, int E>
+__global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
+  constexpr int NT = C / 16;
+  constexpr int E4 = (E + 3) & ~3;
+  // G is accumulated and differenced in fp64: after a very negative gate the
+  // running sum is large and fp32 would lose the small gates that follow it.
+  __shared__ float sq2[C][E], sk2[C][E], sbeta[C];
+  __shared__ double sG[C][E];
+  __shared__ float sAqk[C][C + 1], sAkk[C][C + 1], sL[C][C + 1];
+
+  const int ch = blockIdx.x;
+  const int head = ch / s.Nc, ci = ch % s.Nc;
+  const int b = head / s.H, h = head % s.H;
+  const int t0 = ci * C;
+  const int tid = threadIdx.x;
+  const int w = wave_id(), l = lane_id(), g = l >> 4, n = l & 15;
+
+  for (int idx = tid; idx < C * E; idx += 256) {
+    const int r = idx / E, e = idx % E;
+    const int t = t0 + r;
+    const bool ok = t < s.T;
+    const size_t off = (((size_t)b * s.T + t) * s.H + h) * E + e;
+    sq2[r][e] = ok ? ld_f((const T*)in.q2 + off) : 0.f;
+    sk2[r][e] = ok ? ld_f((const T*)in.k2 + off) : 0.f;
+    sG[r][e] = ok ? (double)in.g[off] : 0.0;
+  }
+  for (int r = tid; r < C; r += 256) {
+    const int t = t0 + r;
+    sbeta[r] = (t < s.T) ? (in.beta ? in.beta[((size_t)b * s.T + t) * s.H + h] : 1.f) : 0.f;
+  }
+  __syncthreads();
+  if (tid < E) {  // in-chunk inclusive cumulative sum of the log-gates
+    double acc = 0.0;
+    for (int r = 0; r < C; ++r) {
+      acc += sG[r][tid];
+      sG[r][tid] = acc;
+    }
+  }
+  __syncthreads();
+
+  float* coef = p.coef + (size_t)ch * 3 * E * C;
+  for (int idx = tid; idx < E * C; idx += 256) {
+    const int e = idx / C, r = idx % C;
+    const double G = sG[r][e], GC = sG[C - 1][e];
+    const float gam = exp_nonpos((float)G);
+    coef[(0 * E + e) * C + r] = sk2[r][e] * gam;
+    coef[(1 * E + e) * C + r] = sq2[r][e] * gam;
+    coef[(2 * E + e) * C + r] = sk2[r][e] * exp_nonpos((float)(GC - G));
+  }
+  if (tid < E4) p.gC[(size_t)ch * E4 + tid] = (tid < E) ? exp_nonpos((float)sG[C - 1][tid]) : 0.f;
+
+  // A_qk = Q K^T and A_kk = K K^T, lower-triangular 16x16 tiles
+  {
+    const T* Qg = (const T*)in.q;
+    const T* Kg = (const T*)in.k;
+    const size_t rstride = (size_t)s.H * KD;
+    const size_t base = (((size_t)b * s.T) * s.H + h) * KD;
+    for (int tile = w; tile < NT * NT; tile += 4) {
+      const int rt = tile / NT, st = tile % NT;
+      if (st > rt) continue;
+      const int r = 16 * rt + n, c = 16 * st + n;
+      const bool rok = t0 + r < s.T, cok = t0 + c < s.T;
+      const T* qrow = Qg + base + (size_t)(t0 + r) * rstride;
+      const T* krow = Kg + base + (size_t)(t0 + r) * rstride;
+      const T* kcol = Kg + base + (size_t)(t0 + c) * rstride;
+      typedef typename Elem<T>::frag F;
+      F zf = cvt_frag<T>(zero4());
+      f32x4 aq = zero4(), ak = zero4();
+      mma_k<KD>(aq, [&](int kb) { return rok ? ld_frag(qrow + 16 * kb + 4 * g) : zf; },
+                [&](int kb) { return cok ? ld_frag(kcol + 16 * kb + 4 * g) : zf; });
+      mma_k<KD>(ak, [&](int kb) { return rok ? ld_frag(krow + 16 * kb + 4 * g) : zf; },
+                [&](int kb) { return cok ? ld_frag(kcol + 16 * kb + 4 * g) : zf; });
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        sAqk[16 * rt + 4 * g + j][16 * st + n] = aq[j];
+        sAkk[16 * rt + 4 * g + j][16 * st + n] = ak[j];
+      }
+    }
+  }
+  __syncthreads();
+
+  // R', R element by element; M = A_qk o R' (r >= s); L = diag(beta)(A_kk o R) (r > s)
+  float* Mg = p.M + (size_t)ch * C * C;
+  for (int idx = tid; idx < C * C; idx += 256) {
+    const int r = idx / C, c = idx % C;
+    float m = 0.f, lv = 0.f;
+    if (c <= r) {
+      float rq = 0.f, rk = 0.f;
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const float d = exp_nonpos((float)(sG[r][e] - sG[c][e]));
+        rq += sq2[r][e] * sk2[c][e] * d;
+        rk += sk2[r][e] * sk2[c][e] * d;
+      }
+      m = sAqk[r][c] * rq;
+      if (c < r) lv = sbeta[r] * sAkk[r][c] * rk;
+    }
+    Mg[idx] = m;
+    sL[r][c] = lv;
+  }
+  __syncthreads();
+
+  // Tu = (I + L)^{-1} diag(beta): thread c forward-substitutes column c
+  if (s.variant == 1 && tid < C) {
+    const int c = tid;
+    float x[C];
+#pragma unroll
+    for (int r = 0; r < C; ++r) {
+      float acc = 0.f;
+#pragma unroll
+      for (int j = 0; j < r; ++j) acc += sL[r][j] * x[j];
+      x[r] = (r < c) ? 0.f : ((r == c) ? 1.f : -acc);
+    }
+    float* Tg = p.Tu + (size_t)ch * C * C;
+    const float bc = sbeta[c];
+#pragma unroll
+    for (int r = 0; r < C; ++r) Tg[r * C + c] = x[r] * bc;
+  }
+}
+
+// ---------------------------------------------------------------- forward
+template <typename T, int KD, int C, int E, int NW>
+struct FwdSmem {
+  static constexpr int KP = KD + 8;  // padded row lengths (elements)
+  static constexpr int CP = C + 8;
+  static constexpr int NT = C / 16;
+  static constexpr int E4 = (E + 3) & ~3;
+  // bf16 operands carry Tu and M as hi + lo pairs (SPLIT).  The largest
+  // instances read the queries straight from global memory so that the plan
+  // fits the 160 KiB of LDS.
+  static constexpr bool SPLIT = sizeof(T) == 2;
+  static constexpr bool STAGE_Q = sizeof(T) == 2 && E < 16;
+  alignas(16) T K[C][KP];
+  alignas(16) T Q[STAGE_Q ? C : 1][KP];
+  alignas(16) T Kt[KD][CP];
+  alignas(16) T Vt[16][CP];
+  alignas(16) T Tu[C][CP];
+  alignas(16) T M[C][CP];
+  alignas(16) T TuL[SPLIT ? C : 1][CP];
+  alignas(16) T ML[SPLIT ? C : 1][CP];
+  alignas(16) float coef[3][E][C];
+  alignas(16) float gC[E4];
+  alignas(16) float beta[C];
+  alignas(16) f32x4 W[NW][NT][64];
+  alignas(16) f32x4 O[NW][NT][64];
+};
+
+template <typename T, int KD, int C, int E, int NW>
+__global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, void* out,
+                                                 float* s_final, SavedBufs sv, int train) {
+  constexpr int SPW = (E + NW - 1) / NW;
+  constexpr int NT = C / 16;
+  constexpr int KT = KD / 16;
+  constexpr int NTHR = NW * 64;
+  constexpr int E4 = (E + 3) & ~3;
+  typedef typename Elem<T>::frag F;
+  typedef FwdSmem<T, KD, C, E, NW> Sm;
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  Sm& sm = *reinterpret_cast<Sm*>(smem_raw);
+
+  const int tid = threadIdx.x, w = wave_id(), l = lane_id(), g = l >> 4, n = l & 15;
+  const int V = s.V;
+  int head, vt;
+  xcd_map(blockIdx.x, s.NH, V / 16, head, vt);
+  const int b = head / s.H, h = head % s.H;
+  const int v0 = vt * 16;
+
+  // state tiles S[i][kt] = S_e[16 kt + 4 g + j][v0 + n], e = w * SPW + i
+  f32x4 S[SPW][KT];
+#pragma unroll
+  for (int i = 0; i < SPW; ++i) {
+    const int e = w * SPW + i;
+#pragma unroll
+    for (int kt = 0; kt < KT; ++kt) {
+      f32x4 x = zero4();
+      if (in.s0 && e < E) {
+        const float* src = in.s0 + (((size_t)head * E + e) * KD + 16 * kt + 4 * g) * V + v0 + n;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) x[j] = src[(size_t)j * V];
+      }
+      S[i][kt] = x;
+    }
+  }
+
+  const T* Kg = (const T*)in.k + (((size_t)b * s.T) * s.H + h) * KD;
+  const T* Qg = (const T*)in.q + (((size_t)b * s.T) * s.H + h) * KD;
+  const T* Vg = (const T*)in.v + (((size_t)b * s.T) * s.H + h) * (size_t)V + v0;
+  const size_t krs = (size_t)s.H * KD;  // row stride between positions
+  const size_t vrs = (size_t)s.H * V;
+
+  for (int ci = 0; ci < s.Nc; ++ci) {
+    const int t0 = ci * C;
+    const size_t ch = (size_t)head * s.Nc + ci;
+    __syncthreads();  // the previous chunk is done with shared memory
+
+    // ---- stage the chunk: K, Q (row-major), K^T, V tile (transposed), Tu, M, coefficients
+    constexpr int RB = C / 4, CB = KD / 8;
+    for (int blk = tid; blk < RB * CB; blk += NTHR) {
+      const int rb = blk % RB, cb = blk / RB;
+      T kv[4][8];
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        const int r = 4 * rb + rr;
+        if (t0 + r < s.T) {
+          copy8(kv[rr], Kg + (size_t)(t0 + r) * krs + 8 * cb);
+          if constexpr (Sm::STAGE_Q) copy8(&sm.Q[r][8 * cb], Qg + (size_t)(t0 + r) * krs + 8 * cb);
+        } else {
+          zero8(kv[rr]);
+          if constexpr (Sm::STAGE_Q) zero8(&sm.Q[r][8 * cb]);
+        }
+        copy8(&sm.K[r][8 * cb], kv[rr]);
+      }
+#pragma unroll
+      for (int cc = 0; cc < 8; ++cc) {
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) sm.Kt[8 * cb + cc][4 * rb + rr] = kv[rr][cc];
+      }
+    }
+    for (int blk = tid; blk < RB * 2; blk += NTHR) {
+      const int rb = blk % RB, cb = blk / RB;
+      T vv[4][8];
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        const int r = 4 * rb + rr;
+        if (t0 + r < s.T)
+          copy8(vv[rr], Vg + (size_t)(t0 + r) * vrs + 8 * cb);
+        else
+          zero8(vv[rr]);
+      }
+#pragma unroll
+      for (int cc = 0; cc < 8; ++cc) {
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) sm.Vt[8 * cb + cc][4 * rb + rr] = vv[rr][cc];
+      }
+    }
+    {
+      const float* Mg = p.M + ch * C * C;
+      const float* Tg = p.Tu + ch * C * C;
+      for (int idx = tid; idx < C * C / 4; idx += NTHR) {
+        const int r = idx / (C / 4), c4 = idx % (C / 4);
+        F hi, lo;
+        split_frag(*(const f32x4*)(Mg + r * C + 4 * c4), hi, lo);
+        *(F*)&sm.M[r][4 * c4] = hi;
+        if constexpr (Sm::SPLIT) *(F*)&sm.ML[r][4 * c4] = lo;
+        if (s.variant == 1) {
+          split_frag(*(const f32x4*)(Tg + r * C + 4 * c4), hi, lo);
+          *(F*)&sm.Tu[r][4 * c4] = hi;
+          if constexpr (Sm::SPLIT) *(F*)&sm.TuL[r][4 * c4] = lo;
+        }
+      }
+      const float* cg = p.coef + ch * 3 * E * C;
+      float* cs = &sm.coef[0][0][0];
+      for (int idx = tid; idx < 3 * E * C / 4; idx += NTHR)
+        ((float4*)cs)[idx] = ((const float4*)cg)[idx];
+      if (tid < E4) sm.gC[tid] = p.gC[ch * E4 + tid];
+      for (int r = tid; r < C; r += NTHR) {
+        const int t = t0 + r;
+        sm.beta[r] = (t < s.T) ? (in.beta ? in.beta[((size_t)b * s.T + t) * s.H + h] : 1.f) : 0.f;
+      }
+    }
+    __syncthreads();
+
+    // ---- operand copies of the chunk-start state
+    F Sop[SPW][KT];
+#pragma unroll
+    for (int i = 0; i < SPW; ++i)
+#pragma unroll
+      for (int kt = 0; kt < KT; ++kt) Sop[i][kt] = cvt_frag<T>(S[i][kt]);
+
+    if (train) {  // chunk-start state for the backward: [ch][E][V/16][K][16]
+#pragma unroll
+      for (int i = 0; i < SPW; ++i) {
+        const int e = w * SPW + i;
+        if (e >= E) continue;
+        T* dst = (T*)sv.Sck + ((ch * E + e) * (size_t)(V / 16) + vt) * KD * 16;
+#pragma unroll
+        for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            dst[(16 * kt + 4 * g + j) * 16 + n] = Elem<T>::from_f(S[i][kt][j]);
+      }
+    }
+
+    // ---- P^K_e = K S_e and P^Q_e = Q S_e for the owned slices
+    f32x4 PK[SPW][NT], PQ[SPW][NT];
+#pragma unroll
+    for (int rt = 0; rt < NT; ++rt) {
+#pragma unroll
+      for (int i = 0; i < SPW; ++i) {
+        PK[i][rt] = zero4();
+        PQ[i][rt] = zero4();
+      }
+      const int r = 16 * rt + n;
+      // query row r of the chunk (zero past the end of the sequence)
+      const bool qok = t0 + r < s.T;
+      const T* qrow = Qg + (size_t)(qok ? t0 + r : 0) * krs;
+      auto qfrag = [&](int kb) -> F {
+        if constexpr (Sm::STAGE_Q) return ld_frag(&sm.Q[r][16 * kb + 4 * g]);
+        else return qok ? ld_frag(qrow + 16 * kb + 4 * g) : cvt_frag<T>(zero4());
+      };
+#pragma unroll
+      for (int kb = 0; kb < KT; kb += (KT > 1 ? 2 : 1)) {
+        if constexpr (KT > 1) {
+          const F ak0 = ld_frag(&sm.K[r][16 * kb + 4 * g]);
+          const F ak1 = ld_frag(&sm.K[r][16 * kb + 16 + 4 * g]);
+          const F aq0 = qfrag(kb);
+          const F aq1 = qfrag(kb + 1);
+#pragma unroll
+          for (int i = 0; i < SPW; ++i) {
+            if (w * SPW + i >= E) continue;
+            mma32(PK[i][rt], ak0, ak1, Sop[i][kb], Sop[i][kb + 1]);
+            mma32(PQ[i][rt], aq0, aq1, Sop[i][kb], Sop[i][kb + 1]);
+          }
+        } else {
+          const F ak = ld_frag(&sm.K[r][4 * g]);
+          const F aq = qfrag(0);
+#pragma unroll
+          for (int i = 0; i < SPW; ++i) {
+            if (w * SPW + i >= E) continue;
+            mma16(PK[i][rt], ak, Sop[i][0]);
+            mma16(PQ[i][rt], aq, Sop[i][0]);
+          }
+        }
+      }
+    }
+    // ---- per-wave partial sums over the owned slices, exchanged through LDS
+#pragma unroll
+    for (int rt = 0; rt < NT; ++rt) {
+      f32x4 wp = zero4(), op = zero4();
+#pragma unroll
+      for (int i = 0; i < SPW; ++i) {
+        const int e = w * SPW + i;
+        if (e >= E) continue;
+        const f32x4 ca = *(const f32x4*)&sm.coef[0][e][16 * rt + 4 * g];
+        const f32x4 cb = *(const f32x4*)&sm.coef[1][e][16 * rt + 4 * g];
+        wp += ca * PK[i][rt];
+        op += cb * PQ[i][rt];
+      }
+      sm.W[w][rt][l] = wp;
+      sm.O[w][rt][l] = op;
+    }
+    __syncthreads();
+
+    // ---- U = Tu (V - W) (GDN) or diag(beta) V (sGLA); every wave keeps all of U
+    f32x4 U[NT];
+    if (s.variant == 1) {
+      F Xh[NT], Xl[NT];
+#pragma unroll
+      for (int rt = 0; rt < NT; ++rt) {
+        f32x4 x = ld4_f(&sm.Vt[n][16 * rt + 4 * g]);
+#pragma unroll
+        for (int ww = 0; ww < NW; ++ww) x -= sm.W[ww][rt][l];
+        split_frag(x, Xh[rt], Xl[rt]);
+        if (train && rt == w) {
+          float* dst = sv.X + ch * C * (size_t)V + (size_t)(16 * rt + 4 * g) * V + v0 + n;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) dst[(size_t)j * V] = x[j];
+        }
+      }
+#pragma unroll
+      for (int rt = 0; rt < NT; ++rt) {
+        U[rt] = zero4();
+        const int r = 16 * rt + n;
+        auto th = [&](int kb) { return ld_frag(&sm.Tu[r][16 * kb + 4 * g]); };
+        mma_k<C>(U[rt], th, [&](int kb) { return Xh[kb]; });
+        if constexpr (Sm::SPLIT) {
+          mma_k<C>(U[rt], th, [&](int kb) { return Xl[kb]; });
+          mma_k<C>(U[rt], [&](int kb) { return ld_frag(&sm.TuL[r][16 * kb + 4 * g]); },
+                   [&](int kb) { return Xh[kb]; });
+        }
+      }
+    } else {
+#pragma unroll
+      for (int rt = 0; rt < NT; ++rt)
+        U[rt] = ld4_f(&sm.Vt[n][16 * rt + 4 * g]) * *(const f32x4*)&sm.beta[16 * rt + 4 * g];
+    }
+    F Uh[NT], Ul[NT];
+#pragma unroll
+    for (int rt = 0; rt < NT; ++rt) split_frag(U[rt], Uh[rt], Ul[rt]);
+
+    // ---- O for row tile w: sum of the partials plus M U
+    if (w < NT) {
+      const int rt = w;
+      f32x4 acc = zero4();
+#pragma unroll
+      for (int ww = 0; ww < NW; ++ww) acc += sm.O[ww][rt][l];
+      const int r = 16 * rt + n;
+      auto mh = [&](int kb) { return ld_frag(&sm.M[r][16 * kb + 4 * g]); };
+      mma_k<C>(acc, mh, [&](int kb) { return Uh[kb]; });
+      if constexpr (Sm::SPLIT) {
+        mma_k<C>(acc, mh, [&](int kb) { return Ul[kb]; });
+        mma_k<C>(acc, [&](int kb) { return ld_frag(&sm.ML[r][16 * kb + 4 * g]); },
+                 [&](int kb) { return Uh[kb]; });
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int t = t0 + 16 * rt + 4 * g + j;
+        if (t < s.T) {
+          const size_t off = (((size_t)b * s.T + t) * s.H + h) * (size_t)V + v0 + n;
+          if (s.out_bf16)
+            ((bf16_t*)out)[off] = Elem<bf16_t>::from_f(acc[j]);
+          else
+            ((float*)out)[off] = acc[j];
+        }
+      }
+      if (train) {
+        float* dst = sv.U + ch * C * (size_t)V + (size_t)(16 * rt + 4 * g) * V + v0 + n;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) dst[(size_t)j * V] = U[rt][j];
+      }
+    }
+
+    // ---- state update S_e <- gamma^C_e S_e + K^T diag(c_e) U
+    F Uc[SPW][NT], Ucl[SPW][NT];
+#pragma unroll
+    for (int i = 0; i < SPW; ++i) {
+      const int e = w * SPW + i;
+      if (e >= E) continue;
+      const float gc = sm.gC[e];
+#pragma unroll
+      for (int kt = 0; kt < KT; ++kt) S[i][kt] *= gc;
+#pragma unroll
+      for (int kb = 0; kb < NT; ++kb)
+        split_frag(U[kb] * *(const f32x4*)&sm.coef[2][e][16 * kb + 4 * g], Uc[i][kb], Ucl[i][kb]);
+    }
+#pragma unroll
+    for (int kt = 0; kt < KT; ++kt) {
+      const int r = 16 * kt + n;
+      if constexpr (NT > 1) {
+#pragma unroll
+        for (int kb = 0; kb + 1 < NT; kb += 2) {
+          const F a0 = ld_frag(&sm.Kt[r][16 * kb + 4 * g]);
+          const F a1 = ld_frag(&sm.Kt[r][16 * kb + 16 + 4 * g]);
+#pragma unroll
+          for (int i = 0; i < SPW; ++i) {
+            if (w * SPW + i >= E) continue;
+            mma32(S[i][kt], a0, a1, Uc[i][kb], Uc[i][kb + 1]);
+            if constexpr (Sm::SPLIT) mma32(S[i][kt], a0, a1, Ucl[i][kb], Ucl[i][kb + 1]);
+          }
+        }
+      }
+      if constexpr (NT & 1) {
+        const F a = ld_frag(&sm.Kt[r][16 * (NT - 1) + 4 * g]);
+#pragma unroll
+        for (int i = 0; i < SPW; ++i) {
+          if (w * SPW + i >= E) continue;
+          mma16(S[i][kt], a, Uc[i][NT - 1]);
+          if constexpr (Sm::SPLIT) mma16(S[i][kt], a, Ucl[i][NT - 1]);
+        }
+      }
+    }
+  }
+
+  if (s_final) {
+#pragma unroll
+    for (int i = 0; i < SPW; ++i) {
+      const int e = w * SPW + i;
+      if (e >= E) continue;
+#pragma unroll
+      for (int kt = 0; kt < KT; ++kt) {
+        float* dst = s_final + (((size_t)head * E + e) * KD + 16 * kt + 4 * g) * V + v0 + n;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) dst[(size_t)j * V] = S[i][kt][j];
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------- launchers
+template <int E> constexpr int fwd_waves() { return E >= 16 ? 8 : 4; }
+
+template <typename T, int KD, int C, int E>
+static hipError_t prep_inst(const Shape& s, const FwdIn& in, const PrepBufs& p, hipStream_t st) {
+  hipLaunchKernelGGL((k_prep<T, KD, C, E>), dim3(s.NH * s.Nc), dim3(256), 0, st, s, in, p);
+  return hipGetLastError();
+}
+
+template <typename T, int KD, int C, int E>
+static hipError_t fwd_inst(const Shape& s, const FwdIn& in, const PrepBufs& p, void* o,
+                           float* s_final, const SavedBufs* sv, hipStream_t st) {
+  constexpr int NW = fwd_waves<E>();
+  typedef FwdSmem<T, KD, C, E, NW> Sm;
+  const size_t smem = sizeof(Sm);
+  static bool attr_set = false;
+  if (!attr_set) {  // allow more than the default dynamic LDS (best effort)
+    (void)hipFuncSetAttribute((const void*)k_fwd<T, KD, C, E, NW>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+    attr_set = true;
+  }
+  SavedBufs none{nullptr, nullptr, nullptr};
+  hipLaunchKernelGGL((k_fwd<T, KD, C, E, NW>), dim3(s.NH * (s.V / 16)), dim3(NW * 64), smem, st,
+                     s, in, p, o, s_final, sv ? *sv : none, sv ? 1 : 0);
+  return hipGetLastError();
+}
+
+#define TLA_DISPATCH(KD_, C_, E_, CALL)                          \
+  if (s.K == KD_ && s.C == C_ && s.E == E_) {                    \
+    if (s.in_bf16) return CALL(bf16_t, KD_, C_, E_);             \
+    return CALL(float, KD_, C_, E_);                             \
+  }
+
+#define TLA_FOR_EACH_INSTANCE(CALL) \
+  TLA_DISPATCH(16, 16, 4, CALL)     \
+  TLA_DISPATCH(32, 32, 4, CALL)     \
+  TLA_DISPATCH(64, 32, 8, CALL)     \
+  TLA_DISPATCH(128, 64, 1, CALL)    \
+  TLA_DISPATCH(128, 64, 4, CALL)    \
+  TLA_DISPATCH(128, 64, 8, CALL)    \
+  TLA_DISPATCH(128, 64, 16, CALL)   \
+  TLA_DISPATCH(128, 32, 8, CALL)
+
+hipError_t launch_prep(const Shape& s, const FwdIn& in, const PrepBufs& p, hipStream_t st) {
+#define CALL_PREP(T_, KD_, C_, E_) prep_inst<T_, KD_, C_, E_>(s, in, p, st)
+  TLA_FOR_EACH_INSTANCE(CALL_PREP)
+#undef CALL_PREP
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_fwd(const Shape& s, const FwdIn& in, const PrepBufs& p, void* o, float* s_final,
+                      const SavedBufs* saved, hipStream_t st) {
+#define CALL_FWD(T_, KD_, C_, E_) fwd_inst<T_, KD_, C_, E_>(s, in, p, o, s_final, saved, st)
+  TLA_FOR_EACH_INSTANCE(CALL_FWD)
+#undef CALL_FWD
+  return hipErrorInvalidValue;
+}
+
+template <typename T, int KD, int C, int E>
+static bool fits_inst() {
+  return sizeof(FwdSmem<T, KD, C, E, fwd_waves<E>()>) <= 160 * 1024;
+}
+
+bool fits_lds(int K, int C, int E, bool bf16) {
+#define FITS(T_, KD_, C_, E_) fits_inst<T_, KD_, C_, E_>()
+  const tla::Shape s{0, 1, 1, 1, K, 16, E, C, 1, 1, bf16 ? 1 : 0, 0, 0};
+  TLA_FOR_EACH_INSTANCE(FITS)
+#undef FITS
+  return false;
+}
+
+bool have_instance(int K, int C, int E) {
+  return (K == 16 && C == 16 && E == 4) || (K == 32 && C == 32 && E == 4) ||
+         (K == 64 && C == 32 && E == 8) || (K == 128 && C == 64 && (E == 1 || E == 4 || E == 8 || E == 16)) ||
+         (K == 128 && C == 32 && E == 8);
+}
+
+}  // namespace tla

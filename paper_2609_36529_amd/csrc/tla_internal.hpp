@@ -1,0 +1,71 @@
+// Internal interface between the C-ABI host code and the kernel files.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace tla {
+
+// Shapes and derived sizes shared by every launch of one call.
+struct Shape {
+  int variant;   // 0 sGLA, 1 GDN
+  int B, T, H, K, V, E, C;
+  int Nc;        // number of chunks = ceil(T / C)
+  int NH;        // B * H
+  int in_bf16;   // operand type of q, k, v, q2, k2, dO and gradients
+  int out_bf16;  // type of o
+  int has_beta;
+};
+
+// Per-chunk quantities written by the forward prep kernel (and again by the
+// backward).  All arrays are indexed by ch = (b * H + h) * Nc + chunk.
+struct PrepBufs {
+  float* coef;   // [ch][3][E][C]  a = k2*gamma, b = q2*gamma, c = k2*gamma^C/gamma
+  float* gC;     // [ch][E4]       gamma^C (E4 = E rounded up to 4)
+  float* M;      // [ch][C][C]     (Q K^T) o R'   lower incl. diagonal
+  float* Tu;     // [ch][C][C]     (I + L)^{-1} diag(beta) (GDN)
+};
+
+// Buffers the training forward stores for the backward (opaque layout).
+struct SavedBufs {
+  void* Sck;     // [ch][E][V/16][K][16] chunk-start states, operand type
+  float* U;      // [ch][C][V] delta-corrected values U
+  float* X;      // [ch][C][V] residual V - W (GDN)
+};
+
+struct BwdBufs {
+  void* dSck;    // [ch][E][V/16][K][16] state gradients at chunk ends, operand type
+  float* dU;     // [ch][C][V]
+  float* dW;     // [ch][C][V]
+  float* dqs;    // [ch][C][K] state contributions to dq
+  float* dks;    // [ch][C][K] state contributions to dk
+  float* dcoef;  // [ch][3][E][C] gradients of the coefficient vectors a, b, c
+  float* dgC;    // [ch][E4] gradient of gamma^C
+};
+
+struct FwdIn {
+  const void *q, *k, *v, *q2, *k2;
+  const float *g, *beta, *s0;
+};
+
+inline int round4(int x) { return (x + 3) & ~3; }
+
+// Kernel launchers (return hipGetLastError() after the launch).
+hipError_t launch_prep(const Shape& s, const FwdIn& in, const PrepBufs& p, hipStream_t st);
+hipError_t launch_fwd(const Shape& s, const FwdIn& in, const PrepBufs& p, void* o,
+                      float* s_final, const SavedBufs* saved, hipStream_t st);
+hipError_t launch_bwd_rec(const Shape& s, const FwdIn& in, const void* dO, const float* dS_final,
+                          const PrepBufs& p, const BwdBufs& bb, float* ds0, hipStream_t st);
+hipError_t launch_bwd_state(const Shape& s, const FwdIn& in, const void* dO, const PrepBufs& p,
+                            const SavedBufs& sv, const BwdBufs& bb, hipStream_t st);
+hipError_t launch_bwd_chunk(const Shape& s, const FwdIn& in, const void* dO, const SavedBufs& sv,
+                            const BwdBufs& bb, void* dq, void* dk, void* dv, void* dq2,
+                            void* dk2, float* dg, float* dbeta, hipStream_t st);
+hipError_t launch_step(const Shape& s, const FwdIn& in, float* state, void* o, hipStream_t st);
+
+// Which (K, C, E) combinations have kernel instances, and whether the
+// forward/backward shared-memory plan of an instance fits 160 KiB.
+bool have_instance(int K, int C, int E);
+bool fits_lds(int K, int C, int E, bool bf16);
+
+}  // namespace tla

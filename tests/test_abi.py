@@ -1,0 +1,167 @@
+"""CPU tests of the C ABI: the library loads without a GPU, exports every
+function that include/tla.h declares, and rejects bad arguments on the host
+(with status codes) before anything reaches the device.  Pointers passed here
+are fake addresses; every call is built to fail validation."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_36529_amd as tla
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tla.h")
+
+OK, E_NULL, E_SHAPE, E_UNSUP, E_ALIGN, E_WS, E_ALIAS, E_DEVICE = range(8)
+FAKE = 0x7f0000000000  # 16-byte aligned fake device address; never dereferenced
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^[A-Za-z_][\w\s\*]*?\b(tla_\w+)\(", text, flags=re.M)))
+
+
+def test_header_declares_the_entry_points():
+    names = declared_functions()
+    for n in ("tla_fwd", "tla_bwd", "tla_step", "tla_workspace_bytes", "tla_saved_bytes",
+              "tla_status_string", "tla_last_error", "tla_version", "tla_supported"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    L = tla.lib()
+    for n in declared_functions():
+        assert hasattr(L, n), n
+
+
+def test_version_and_status_strings():
+    L = tla.lib()
+    assert L.tla_version() == 1
+    for code in range(8):
+        assert L.tla_status_string(code)
+    assert b"unknown" in L.tla_status_string(99)
+
+
+def desc(**kw):
+    base = dict(variant=tla.GDN, B=2, T=100, H=2, K=128, V=128, E=8, chunk=64,
+                in_dtype=tla.BF16, out_dtype=tla.F32)
+    base.update(kw)
+    return tla.make_desc(base["variant"], base["B"], base["T"], base["H"], base["K"], base["V"],
+                         base["E"], base["chunk"], base["in_dtype"], base["out_dtype"])
+
+
+def fwd_call(d, q=FAKE, k=FAKE + 0x100000, v=FAKE + 0x200000, q2=FAKE + 0x300000,
+             k2=FAKE + 0x400000, g=FAKE + 0x500000, beta=FAKE + 0x600000, s0=None,
+             o=FAKE + 0x1000000, sf=None, saved=None, ws=FAKE + 0x2000000, ws_bytes=None):
+    L = tla.lib()
+    if ws_bytes is None:
+        ws_bytes = 1 << 40
+    P = ctypes.c_void_p
+    return L.tla_fwd(ctypes.byref(d), P(q), P(k), P(v), P(q2), P(k2), P(g), P(beta), P(s0), P(o),
+                     P(sf), P(saved), P(ws), ws_bytes, None)
+
+
+def last_error():
+    return tla.lib().tla_last_error().decode()
+
+
+def test_null_desc():
+    L = tla.lib()
+    P = ctypes.c_void_p
+    assert L.tla_fwd(None, *([P(FAKE)] * 11), P(FAKE), 1 << 30, None) == E_NULL
+    assert L.tla_workspace_bytes(None, 0) == 0
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(variant=7), E_SHAPE),
+    (dict(in_dtype=5), E_SHAPE),
+    (dict(B=0), E_SHAPE),
+    (dict(T=-1), E_SHAPE),
+    (dict(K=48), E_UNSUP),
+    (dict(V=100), E_UNSUP),
+    (dict(V=2048), E_UNSUP),
+    (dict(E=3), E_UNSUP),
+    (dict(chunk=128), E_UNSUP),
+    (dict(K=64, chunk=64, E=2), E_UNSUP),
+    (dict(in_dtype=tla.F32, E=16), E_UNSUP),   # fp32 plan exceeds the LDS budget
+])
+def test_bad_shapes(kw, code):
+    assert fwd_call(desc(**kw)) == code
+    assert last_error()
+
+
+def test_struct_size_checked():
+    d = desc()
+    d.struct_size = 12
+    assert fwd_call(d) == E_SHAPE
+
+
+def test_required_pointers():
+    assert fwd_call(desc(), q=None) == E_NULL
+    assert fwd_call(desc(), o=None) == E_NULL
+    assert fwd_call(desc(variant=tla.GDN), beta=None) == E_NULL
+
+
+def test_alignment():
+    assert fwd_call(desc(), k=FAKE + 0x100008) == E_ALIGN
+    assert fwd_call(desc(), ws=FAKE + 0x2000004) == E_ALIGN
+
+
+def test_workspace_size():
+    d = desc()
+    need = tla.workspace_bytes(d, tla.OP_FWD)
+    assert need > 0
+    assert fwd_call(d, ws_bytes=need - 1) == E_WS
+    assert fwd_call(d, ws=None) == E_WS
+
+
+def test_aliasing():
+    assert fwd_call(desc(), o=FAKE) == E_ALIAS                  # o overlaps q
+    assert fwd_call(desc(), sf=FAKE + 0x400000) == E_ALIAS      # s_final overlaps k2
+    assert fwd_call(desc(), ws=FAKE + 0x1000000) == E_ALIAS     # workspace overlaps o
+
+
+def test_bwd_validation():
+    L = tla.lib()
+    P = ctypes.c_void_p
+    d = desc()
+    base = [P(FAKE + i * 0x1000000) for i in range(19)]
+
+    def call(args, ws_bytes=1 << 40):
+        return L.tla_bwd(ctypes.byref(d), *args, P(FAKE + 0x40000000), ws_bytes, None)
+    # dbeta (index 17) must be given exactly when beta (index 6) is
+    args = list(base)
+    args[17] = None
+    assert call(args) == E_NULL
+    args = list(base)
+    args[9] = P(FAKE + 8)  # dS_final misaligned
+    assert call(args) == E_ALIGN
+    assert call(base, ws_bytes=16) == E_WS
+    args = list(base)
+    args[12] = args[0]  # dk aliases q
+    assert call(args) == E_ALIAS
+
+
+def test_step_validation():
+    L = tla.lib()
+    P = ctypes.c_void_p
+    d = desc(B=4)
+    ptrs = [P(FAKE + i * 0x100000) for i in range(9)]
+    assert L.tla_step(ctypes.byref(d), *ptrs[:6], None, *ptrs[7:], None) == E_NULL  # GDN without beta
+    ptrs2 = list(ptrs)
+    ptrs2[8] = ptrs2[7]  # o aliases the state
+    assert L.tla_step(ctypes.byref(d), *ptrs2, None) == E_ALIAS
+    assert L.tla_step(ctypes.byref(desc(K=128, E=2)), *ptrs, None) == E_UNSUP
+
+
+def test_size_queries():
+    d = desc(B=4, T=4096, H=8)
+    ws_f, ws_b, sv = (tla.workspace_bytes(d, tla.OP_FWD), tla.workspace_bytes(d, tla.OP_BWD),
+                      tla.saved_bytes(d))
+    nch = 4 * 8 * 64
+    # saved: bf16 chunk-start states plus fp32 U and V - W per chunk
+    assert sv == nch * (8 * 128 * 128 * 2 + 2 * 64 * 128 * 4)
+    assert ws_b > ws_f > 0
+    assert tla.supported(d)
+    assert not tla.supported(desc(K=48))
