@@ -25,10 +25,10 @@
  *      q, k, dq, dk      [B][T][H][K]       v, o, dO, dv   [B][T][H][V]
  *      q2, k2, dq2, dk2  [B][T][H][E]       g, dg          [B][T][H][E] fp32
  *      beta, dbeta       [B][T][H] fp32     states         [B][H][E][K][V] fp32
- *    q, k, v, q2, k2, dO and the gradients dq, dk, dv, dq2, dk2 have the
- *    element type desc->in_dtype (TLA_F32: float, TLA_BF16: bfloat16); o has
- *    desc->out_dtype.  g (log-gates, g <= 0 assumed, not checked), beta and
- *    every state are fp32.
+ *    q, k, v, q2, k2 and dO have the element type desc->in_dtype (TLA_F32:
+ *    float, TLA_BF16: bfloat16); o and the gradients dq, dk, dv, dq2, dk2 have
+ *    desc->out_dtype.  g (log-gates, g <= 0 assumed, not checked), beta, dg,
+ *    dbeta and every state are fp32.
  *  - Every pointer must be 16-byte aligned.
  *  - The caller owns every buffer.  The library allocates nothing, keeps no
  *    per-call state and never synchronises: work is enqueued on `stream`
@@ -76,7 +76,7 @@ typedef struct tla_desc {
   int32_t K, V, E;   /* key dim, value dim, second-key dim */
   int32_t chunk;     /* chunk length C of the chunkwise form (Appendix A) */
   int32_t in_dtype;  /* TLA_F32 or TLA_BF16 */
-  int32_t out_dtype; /* element type of o (TLA_F32 or TLA_BF16) */
+  int32_t out_dtype; /* element type of o and of dq, dk, dv, dq2, dk2 */
 } tla_desc;
 
 /*
@@ -118,7 +118,8 @@ int tla_fwd(const tla_desc* desc, const void* q, const void* k, const void* v,
  * Backward of tla_fwd.  The eight inputs must be the ones given to the
  * training forward that filled `saved`.  dO has type in_dtype; dS_final is
  * the gradient of the final state or NULL (zero).  Outputs: dq, dk, dv, dq2,
- * dk2 (type in_dtype); dg: gradient with respect to the log-gates g (fp32);
+ * dk2 (type out_dtype, like o in the forward); dg: gradient with respect to
+ * the log-gates g (fp32);
  * dbeta (fp32) must be NULL exactly when beta is NULL; ds0 (fp32) may be NULL.
  * Paper reference for the structure: Appendix A, "Kernels" (a reverse
  * recurrence over chunks for the state gradient, then every other gradient

@@ -156,20 +156,23 @@ def fwd(variant, q, k, v, q2, k2, g, beta=None, s0=None, chunk=64, out_dtype=Non
 
 
 def bwd(variant, q, k, v, q2, k2, g, beta, s0, dO, saved, dS_final=None, chunk=64,
-        want_ds0=True, ws=None, grads=None):
+        out_dtype=None, want_ds0=True, ws=None, grads=None):
     """Backward of a training forward.  Returns a dict of gradients
-    (dq, dk, dv, dq2, dk2, dg, dbeta or None, ds0 or None)."""
+    (dq, dk, dv, dq2, dk2 in out_dtype (default: the input dtype); dg, dbeta or
+    None, ds0 or None in fp32)."""
     dev = q.device
     dt = q.dtype
-    desc = describe(variant, q, v, q2, chunk)
+    gt = out_dtype or dt
+    desc = describe(variant, q, v, q2, chunk, gt)
     B, T, H, K = q.shape
     V, E = v.shape[-1], q2.shape[-1]
     _need(dO, "dO", dt, dev)
     _need(dS_final, "dS_final", torch.float32, dev)
     if grads is None:
         grads = {
-            "dq": torch.empty_like(q), "dk": torch.empty_like(k), "dv": torch.empty_like(v),
-            "dq2": torch.empty_like(q2), "dk2": torch.empty_like(k2),
+            "dq": torch.empty_like(q, dtype=gt), "dk": torch.empty_like(k, dtype=gt),
+            "dv": torch.empty_like(v, dtype=gt), "dq2": torch.empty_like(q2, dtype=gt),
+            "dk2": torch.empty_like(k2, dtype=gt),
             "dg": torch.empty((B, T, H, E), dtype=torch.float32, device=dev),
             "dbeta": None if beta is None else torch.empty((B, T, H), dtype=torch.float32, device=dev),
             "ds0": torch.empty((B, H, E, K, V), dtype=torch.float32, device=dev) if want_ds0 else None,

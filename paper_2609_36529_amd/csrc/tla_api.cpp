@@ -57,7 +57,8 @@ int check_desc(const tla_desc* d, tla::Shape* s, bool for_step) {
     if (!pow2_in(d->chunk, Cs, 3)) return fail(TLA_E_UNSUPPORTED, "chunk=%d not in {16,32,64}", d->chunk);
     if (!tla::have_instance(d->K, d->chunk, d->E))
       return fail(TLA_E_UNSUPPORTED, "no kernel instance for K=%d chunk=%d E=%d", d->K, d->chunk, d->E);
-    if (!tla::fits_lds(d->K, d->chunk, d->E, d->in_dtype == TLA_BF16))
+    if (!tla::fits_lds(d->K, d->chunk, d->E, d->in_dtype == TLA_BF16) ||
+        !tla::bwd_fits_lds(d->K, d->chunk, d->E, d->in_dtype == TLA_BF16))
       return fail(TLA_E_UNSUPPORTED, "K=%d chunk=%d E=%d with %s operands exceeds the LDS budget",
                   d->K, d->chunk, d->E, d->in_dtype == TLA_BF16 ? "bf16" : "fp32");
   } else {
@@ -267,15 +268,15 @@ int tla_bwd(const tla_desc* d, const void* q, const void* k, const void* v, cons
   const Layout L = layout(s);
   if (ws_bytes < L.bwd_end) return fail(TLA_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, L.bwd_end);
   const size_t ntok = (size_t)s.B * s.T * s.H;
-  const size_t es = esize(s);
+  const size_t es = esize(s), os = s.out_bf16 ? 2 : 4;
   const size_t sbytes = (size_t)s.NH * s.E * s.K * s.V * 4;
   const Range ins[] = {{q, ntok * s.K * es}, {k, ntok * s.K * es}, {v, ntok * s.V * es},
                        {q2, ntok * s.E * es}, {k2, ntok * s.E * es}, {g, ntok * s.E * 4},
                        {beta, beta ? ntok * 4 : 0}, {s0, s0 ? sbytes : 0},
                        {dO, ntok * s.V * es}, {dS_final, dS_final ? sbytes : 0},
                        {saved, L.sv_end}};
-  const Range outs[] = {{dq, ntok * s.K * es}, {dk, ntok * s.K * es}, {dv, ntok * s.V * es},
-                        {dq2, ntok * s.E * es}, {dk2, ntok * s.E * es}, {dg, ntok * s.E * 4},
+  const Range outs[] = {{dq, ntok * s.K * os}, {dk, ntok * s.K * os}, {dv, ntok * s.V * os},
+                        {dq2, ntok * s.E * os}, {dk2, ntok * s.E * os}, {dg, ntok * s.E * 4},
                         {dbeta, dbeta ? ntok * 4 : 0}, {ds0, ds0 ? sbytes : 0},
                         {ws, L.bwd_end}};
   const int nouts = sizeof(outs) / sizeof(outs[0]);

@@ -1,21 +1,985 @@
-// Backward kernels (placeholder until the backward lands).
+// Backward of chunkwise triadic linear attention on gfx950.
+//
+// The structure follows the paper's backward (Appendix A, "Kernels"): a
+// short reverse recurrence over chunks produces the gradient of every
+// chunk-end state, after which every other gradient is computed for all
+// chunks in parallel, with fixed-order reductions and no atomics.  The chunk
+// equations are the reverse-mode derivative of Eq. joint-chunk (with
+// Eq. joint-gram / joint-solve) and are restated per kernel below.  With
+// N = I + L, Tu = N^{-1} diag(beta), A_hat = A_kk o R, and dS'_e the gradient
+// of the state at the end of the chunk:
+//
+//   k_bwd_rec   (head, 16-column value tile), chunks in reverse:
+//     dU   = M^T dO + sum_e diag(c_e) K dS'_e
+//     dW   = -Tu^T dU                        (GDN; sGLA has no W)
+//     dS_e = gamma^C_e dS'_e + Q^T diag(b_e) dO + K^T diag(a_e) dW
+//   k_bwd_state (head, chunk):
+//     X_e = dO S_e^T, Y_e = dW S_e^T, V'_e = U dS'_e^T
+//     dq_s = sum_e diag(b_e) X_e;  dk_s = sum_e diag(a_e) Y_e + diag(c_e) V'_e
+//     db_e = rowsum(Q o X_e), da_e = rowsum(K o Y_e), dc_e = rowsum(K o V'_e)
+//     dgamma^C_e = <S_e, dS'_e>
+//   k_bwd_chunk (head, chunk):
+//     dM = dO U^T (lower incl. diagonal); dA_qk = dM o R'; dR' = dM o A_qk
+//     GDN: dTu = dU (V - W)^T; P = N^{-T} dTu; dbeta_r = P_rr + sum_s dL_rs A_hat_rs
+//          dL = tril(-P Tu^T, -1); dA_hat = diag(beta) dL
+//          dA_kk = dA_hat o R; dR = dA_hat o A_kk; dv = Tu^T dU = -dW
+//     sGLA: dv = diag(beta) dU; dbeta_r = <dU_r, v_r>
+//     dq = dq_s + dA_qk K;  dk = dk_s + dA_qk^T Q + (dA_kk + dA_kk^T) K
+//     R, R' (Eq. joint-gram):  phi_e[r,s] = (dR'[r,s] q2_r[e] + dR[r,s] k2_r[e]) k2_s[e] Gamma_e[r,s]
+//          dq2_r[e] += sum_s dR'[r,s] k2_s[e] Gamma_e;  dk2_s[e] += sum_r (dR' q2_r + dR k2_r) Gamma_e
+//          dk2_r[e] += sum_s dR[r,s] k2_s[e] Gamma_e;   dG_r[e] += sum_s phi;  dG_s[e] -= sum_r phi
+//     coefficient vectors: dk2 += da o gamma + dc o gamma^C/gamma;  dq2 += db o gamma
+//          dG += da o a + db o b - dc o c;  dG_C += sum_r dc c + gamma^C dgamma^C
+//     dg_j = sum_{r >= j in the chunk} dG_r   (G is the in-chunk cumulative log-gate)
 #include "tla_common.hpp"
 #include "tla_internal.hpp"
 
 namespace tla {
 
-hipError_t launch_bwd_rec(const Shape&, const FwdIn&, const void*, const float*, const PrepBufs&,
-                          const BwdBufs&, float*, hipStream_t) {
-  return hipErrorNotSupported;
+template <typename T>
+__device__ __forceinline__ void bcopy8(T* dst, const T* src) {
+  if constexpr (sizeof(T) == 2) {
+    *(uint4*)dst = *(const uint4*)src;
+  } else {
+    ((float4*)dst)[0] = ((const float4*)src)[0];
+    ((float4*)dst)[1] = ((const float4*)src)[1];
+  }
 }
-hipError_t launch_bwd_state(const Shape&, const FwdIn&, const void*, const PrepBufs&,
-                            const SavedBufs&, const BwdBufs&, hipStream_t) {
-  return hipErrorNotSupported;
+template <typename T>
+__device__ __forceinline__ void bzero8(T* dst) {
+  if constexpr (sizeof(T) == 2) {
+    *(uint4*)dst = make_uint4(0, 0, 0, 0);
+  } else {
+    ((float4*)dst)[0] = make_float4(0, 0, 0, 0);
+    ((float4*)dst)[1] = make_float4(0, 0, 0, 0);
+  }
 }
-hipError_t launch_bwd_chunk(const Shape&, const FwdIn&, const void*, const SavedBufs&,
-                            const BwdBufs&, void*, void*, void*, void*, void*, float*, float*,
-                            hipStream_t) {
-  return hipErrorNotSupported;
+
+// Gradients are written in the call's output type (fp32 or bf16).
+__device__ __forceinline__ void store_out(void* base, size_t off, float x, int out_bf16) {
+  if (out_bf16)
+    ((bf16_t*)base)[off] = Elem<bf16_t>::from_f(x);
+  else
+    ((float*)base)[off] = x;
+}
+
+template <int D, typename FA, typename FB>
+__device__ __forceinline__ void bmma_k(f32x4& acc, FA fa, FB fb) {
+  constexpr int NB = D / 16;
+#pragma unroll
+  for (int kb = 0; kb + 1 < NB; kb += 2) mma32(acc, fa(kb), fa(kb + 1), fb(kb), fb(kb + 1));
+  if constexpr (NB & 1) mma16(acc, fa(NB - 1), fb(NB - 1));
+}
+
+template <int E> constexpr int bwd_waves() { return E >= 16 ? 8 : 4; }
+
+// ============================================================ reverse recurrence
+template <typename T, int KD, int C, int E, int NW>
+struct RecSmem {
+  static constexpr int KP = KD + 8;
+  static constexpr int CP = C + 8;
+  static constexpr int NT = C / 16;
+  static constexpr int E4 = (E + 3) & ~3;
+  static constexpr bool SPLIT = sizeof(T) == 2;
+  // rows of K (A operand of K dS'); fp32 operands read them from global memory
+  // so that the fp32 plan fits the 160 KiB of LDS
+  static constexpr bool STAGE_K = sizeof(T) == 2;
+  alignas(16) T K[STAGE_K ? C : 1][KP];
+  alignas(16) T Kt[KD][CP];      // K^T
+  alignas(16) T Qt[KD][CP];      // Q^T
+  alignas(16) T dOt[16][CP];     // dO tile, transposed
+  alignas(16) T MT[C][CP];       // M^T (hi)
+  alignas(16) T TuT[C][CP];      // Tu^T (hi)
+  alignas(16) T MTL[SPLIT ? C : 1][CP];
+  alignas(16) T TuTL[SPLIT ? C : 1][CP];
+  alignas(16) float coef[3][E][C];
+  alignas(16) float gC[E4];
+  alignas(16) f32x4 X[NW][NT][64];  // per-wave partials of sum_e diag(c_e) K dS'_e
+};
+
+template <typename T, int KD, int C, int E, int NW>
+__global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const void* dOv,
+                                                     const float* dS_final, PrepBufs p,
+                                                     BwdBufs bb, float* ds0) {
+  constexpr int SPW = (E + NW - 1) / NW;
+  constexpr int NT = C / 16;
+  constexpr int KT = KD / 16;
+  constexpr int NTHR = NW * 64;
+  constexpr int E4 = (E + 3) & ~3;
+  typedef typename Elem<T>::frag F;
+  typedef RecSmem<T, KD, C, E, NW> Sm;
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  Sm& sm = *reinterpret_cast<Sm*>(smem_raw);
+
+  const int tid = threadIdx.x, w = wave_id(), l = lane_id(), g = l >> 4, n = l & 15;
+  const int V = s.V;
+  int head, vt;
+  xcd_map(blockIdx.x, s.NH, V / 16, head, vt);
+  const int b = head / s.H, h = head % s.H;
+  const int v0 = vt * 16;
+
+  // dS[i][kt] = dS_e[16 kt + 4 g + j][v0 + n], e = w * SPW + i
+  f32x4 dS[SPW][KT];
+#pragma unroll
+  for (int i = 0; i < SPW; ++i) {
+    const int e = w * SPW + i;
+#pragma unroll
+    for (int kt = 0; kt < KT; ++kt) {
+      f32x4 x = zero4();
+      if (dS_final && e < E) {
+        const float* src = dS_final + (((size_t)head * E + e) * KD + 16 * kt + 4 * g) * V + v0 + n;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) x[j] = src[(size_t)j * V];
+      }
+      dS[i][kt] = x;
+    }
+  }
+
+  const T* Kg = (const T*)in.k + (((size_t)b * s.T) * s.H + h) * KD;
+  const T* Qg = (const T*)in.q + (((size_t)b * s.T) * s.H + h) * KD;
+  const T* dOg = (const T*)dOv + (((size_t)b * s.T) * s.H + h) * (size_t)V + v0;
+  const size_t krs = (size_t)s.H * KD;
+  const size_t vrs = (size_t)s.H * V;
+
+  for (int ci = s.Nc - 1; ci >= 0; --ci) {
+    const int t0 = ci * C;
+    const size_t ch = (size_t)head * s.Nc + ci;
+    __syncthreads();
+    // ---- stage: K rows, K^T, Q^T, dO tile^T, M^T, Tu^T (split), coefficients
+    constexpr int RB = C / 4, CB = KD / 8;
+    for (int blk = tid; blk < RB * CB; blk += NTHR) {
+      const int rb = blk % RB, cb = blk / RB;
+      T kv[4][8], qv[4][8];
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        const int t = t0 + 4 * rb + rr;
+        if (t < s.T) {
+          bcopy8(kv[rr], Kg + (size_t)t * krs + 8 * cb);
+          bcopy8(qv[rr], Qg + (size_t)t * krs + 8 * cb);
+        } else {
+          bzero8(kv[rr]);
+          bzero8(qv[rr]);
+        }
+      }
+      if constexpr (Sm::STAGE_K) {
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) bcopy8(&sm.K[4 * rb + rr][8 * cb], kv[rr]);
+      }
+#pragma unroll
+      for (int cc = 0; cc < 8; ++cc)
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) {
+          sm.Kt[8 * cb + cc][4 * rb + rr] = kv[rr][cc];
+          sm.Qt[8 * cb + cc][4 * rb + rr] = qv[rr][cc];
+        }
+    }
+    for (int idx = tid; idx < C * 4; idx += NTHR) {
+      const int r = idx >> 2, c4 = idx & 3;
+      const int t = t0 + r;
+      T x[4];
+      if (t < s.T) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) x[j] = dOg[(size_t)t * vrs + 4 * c4 + j];
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) x[j] = T(0);
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) sm.dOt[4 * c4 + j][r] = x[j];
+    }
+    {
+      const float* Mg = p.M + ch * C * C;
+      const float* Tg = p.Tu + ch * C * C;
+      for (int idx = tid; idx < C * C; idx += NTHR) {
+        const int r = idx / C, c = idx % C;  // writes M^T[c][r] = M[r][c]
+        const float m = Mg[idx];
+        const T mh = Elem<T>::from_f(m);
+        sm.MT[c][r] = mh;
+        if constexpr (Sm::SPLIT) sm.MTL[c][r] = Elem<T>::from_f(m - Elem<T>::to_f(mh));
+        if (s.variant == 1) {
+          const float tv = Tg[idx];
+          const T th = Elem<T>::from_f(tv);
+          sm.TuT[c][r] = th;
+          if constexpr (Sm::SPLIT) sm.TuTL[c][r] = Elem<T>::from_f(tv - Elem<T>::to_f(th));
+        }
+      }
+      const float* cg = p.coef + ch * 3 * E * C;
+      float* cs = &sm.coef[0][0][0];
+      for (int idx = tid; idx < 3 * E * C / 4; idx += NTHR)
+        ((float4*)cs)[idx] = ((const float4*)cg)[idx];
+      if (tid < E4) sm.gC[tid] = p.gC[ch * E4 + tid];
+    }
+    __syncthreads();
+
+    // ---- store dS' (gradient of the chunk-end state) for the chunk-parallel kernel
+#pragma unroll
+    for (int i = 0; i < SPW; ++i) {
+      const int e = w * SPW + i;
+      if (e >= E) continue;
+      T* dst = (T*)bb.dSck + ((ch * E + e) * (size_t)(V / 16) + vt) * KD * 16;
+#pragma unroll
+      for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          dst[(16 * kt + 4 * g + j) * 16 + n] = Elem<T>::from_f(dS[i][kt][j]);
+    }
+
+    // ---- partial of sum_e diag(c_e) K dS'_e over the owned slices
+    F dSop[SPW][KT];
+#pragma unroll
+    for (int i = 0; i < SPW; ++i)
+#pragma unroll
+      for (int kt = 0; kt < KT; ++kt) dSop[i][kt] = cvt_frag<T>(dS[i][kt]);
+#pragma unroll
+    for (int rt = 0; rt < NT; ++rt) {
+      f32x4 acc = zero4();
+      const int r = 16 * rt + n;
+      const bool kok = t0 + r < s.T;
+      const T* krow = Kg + (size_t)(kok ? t0 + r : 0) * krs;
+      auto kfrag = [&](int kb) -> F {
+        if constexpr (Sm::STAGE_K) return ld_frag(&sm.K[r][16 * kb + 4 * g]);
+        else return kok ? ld_frag(krow + 16 * kb + 4 * g) : cvt_frag<T>(zero4());
+      };
+#pragma unroll
+      for (int i = 0; i < SPW; ++i) {
+        const int e = w * SPW + i;
+        if (e >= E) continue;
+        f32x4 z = zero4();
+        bmma_k<KD>(z, kfrag, [&](int kb) { return dSop[i][kb]; });
+        acc += *(const f32x4*)&sm.coef[2][e][16 * rt + 4 * g] * z;
+      }
+      sm.X[w][rt][l] = acc;
+    }
+    __syncthreads();
+
+    // ---- dU = M^T dO + sum of the partials; dW = -Tu^T dU (every wave keeps both)
+    f32x4 dU[NT], dW[NT];
+    F dUh[NT], dUl[NT];
+#pragma unroll
+    for (int rt = 0; rt < NT; ++rt) {
+      f32x4 acc = zero4();
+#pragma unroll
+      for (int ww = 0; ww < NW; ++ww) acc += sm.X[ww][rt][l];
+      const int r = 16 * rt + n;
+      auto dof = [&](int kb) { return ld_frag(&sm.dOt[n][16 * kb + 4 * g]); };
+      bmma_k<C>(acc, [&](int kb) { return ld_frag(&sm.MT[r][16 * kb + 4 * g]); }, dof);
+      if constexpr (Sm::SPLIT)
+        bmma_k<C>(acc, [&](int kb) { return ld_frag(&sm.MTL[r][16 * kb + 4 * g]); }, dof);
+      dU[rt] = acc;
+      split_frag(acc, dUh[rt], dUl[rt]);
+    }
+    if (s.variant == 1) {
+#pragma unroll
+      for (int rt = 0; rt < NT; ++rt) {
+        f32x4 acc = zero4();
+        const int r = 16 * rt + n;
+        auto th = [&](int kb) { return ld_frag(&sm.TuT[r][16 * kb + 4 * g]); };
+        bmma_k<C>(acc, th, [&](int kb) { return dUh[kb]; });
+        if constexpr (Sm::SPLIT) {
+          bmma_k<C>(acc, th, [&](int kb) { return dUl[kb]; });
+          bmma_k<C>(acc, [&](int kb) { return ld_frag(&sm.TuTL[r][16 * kb + 4 * g]); },
+                    [&](int kb) { return dUh[kb]; });
+        }
+        dW[rt] = -acc;
+      }
+    } else {
+#pragma unroll
+      for (int rt = 0; rt < NT; ++rt) dW[rt] = zero4();
+    }
+    if (w < NT) {
+      const int rt = w;
+      float* du = bb.dU + ch * C * (size_t)V + (size_t)(16 * rt + 4 * g) * V + v0 + n;
+      float* dw = bb.dW + ch * C * (size_t)V + (size_t)(16 * rt + 4 * g) * V + v0 + n;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        du[(size_t)j * V] = dU[rt][j];
+        dw[(size_t)j * V] = dW[rt][j];
+      }
+    }
+
+    // ---- dS_e <- gamma^C_e dS'_e + Q^T diag(b_e) dO + K^T diag(a_e) dW
+#pragma unroll
+    for (int i = 0; i < SPW; ++i) {
+      const int e = w * SPW + i;
+      if (e >= E) continue;
+      const float gc = sm.gC[e];
+      F bh[NT], bl[NT], ah[NT], al[NT];
+#pragma unroll
+      for (int kb = 0; kb < NT; ++kb) {
+        const f32x4 dov = ld4_f(&sm.dOt[n][16 * kb + 4 * g]);
+        split_frag(dov * *(const f32x4*)&sm.coef[1][e][16 * kb + 4 * g], bh[kb], bl[kb]);
+        split_frag(dW[kb] * *(const f32x4*)&sm.coef[0][e][16 * kb + 4 * g], ah[kb], al[kb]);
+      }
+#pragma unroll
+      for (int kt = 0; kt < KT; ++kt) {
+        f32x4 acc = dS[i][kt] * gc;
+        const int r = 16 * kt + n;
+        auto qf = [&](int kb) { return ld_frag(&sm.Qt[r][16 * kb + 4 * g]); };
+        auto kf = [&](int kb) { return ld_frag(&sm.Kt[r][16 * kb + 4 * g]); };
+        bmma_k<C>(acc, qf, [&](int kb) { return bh[kb]; });
+        if constexpr (Sm::SPLIT) bmma_k<C>(acc, qf, [&](int kb) { return bl[kb]; });
+        if (s.variant == 1) {
+          bmma_k<C>(acc, kf, [&](int kb) { return ah[kb]; });
+          if constexpr (Sm::SPLIT) bmma_k<C>(acc, kf, [&](int kb) { return al[kb]; });
+        }
+        dS[i][kt] = acc;
+      }
+    }
+  }
+
+  if (ds0) {
+#pragma unroll
+    for (int i = 0; i < SPW; ++i) {
+      const int e = w * SPW + i;
+      if (e >= E) continue;
+#pragma unroll
+      for (int kt = 0; kt < KT; ++kt) {
+        float* dst = ds0 + (((size_t)head * E + e) * KD + 16 * kt + 4 * g) * V + v0 + n;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) dst[(size_t)j * V] = dS[i][kt][j];
+      }
+    }
+  }
+}
+
+// ===================================================== state-gradient contractions
+// One workgroup per (head, chunk); wave w owns the key columns [32 w, 32 w + 32)
+// (KD = 128) or a share of them.  A operands (dO, dW, U) come from LDS, the
+// chunk-start state and the chunk-end state gradient from their tiled stores.
+template <typename T, int KD, int C, int E>
+struct StateSmem {
+  static constexpr int NT = C / 16;
+  alignas(16) T dO[C][16 + 4];           // staged per 16-column block of V
+  alignas(16) T dWh[C][16 + 4], dWl[C][16 + 4];
+  alignas(16) T Uh[C][16 + 4], Ul[C][16 + 4];
+  alignas(16) float Qt[KD][C + 4];       // Q^T and K^T in fp32 for the row sums
+  alignas(16) float Kt[KD][C + 4];
+  alignas(16) float coef[3][E][C];
+  alignas(16) float red[4][3][E][C];     // per-wave row-sum partials
+  alignas(16) float gred[4][E];
+};
+
+template <typename T, int KD, int C, int E>
+__global__ __launch_bounds__(256) void k_bwd_state(Shape s, FwdIn in, const void* dOv,
+                                                   PrepBufs p, SavedBufs sv, BwdBufs bb) {
+  constexpr int NT = C / 16;
+  constexpr int KT = KD / 16;
+  constexpr int CTW = (KT + 3) / 4;      // key column tiles per wave
+  constexpr int E4 = (E + 3) & ~3;
+  typedef typename Elem<T>::frag F;
+  typedef StateSmem<T, KD, C, E> Sm;
+  constexpr bool SPLIT = sizeof(T) == 2;
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  Sm& sm = *reinterpret_cast<Sm*>(smem_raw);
+
+  const int tid = threadIdx.x, w = wave_id(), l = lane_id(), g = l >> 4, n = l & 15;
+  const int V = s.V;
+  const int ch = blockIdx.x;
+  const int head = ch / s.Nc, ci = ch % s.Nc;
+  const int b = head / s.H, h = head % s.H;
+  const int t0 = ci * C;
+  const size_t krs = (size_t)s.H * KD, vrs = (size_t)s.H * V;
+  const T* Kg = (const T*)in.k + (((size_t)b * s.T) * s.H + h) * KD;
+  const T* Qg = (const T*)in.q + (((size_t)b * s.T) * s.H + h) * KD;
+  const T* dOg = (const T*)dOv + (((size_t)b * s.T) * s.H + h) * (size_t)V;
+
+  for (int idx = tid; idx < C * KD; idx += 256) {
+    const int r = idx / KD, c = idx % KD;
+    const int t = t0 + r;
+    sm.Qt[c][r] = (t < s.T) ? ld_f(Qg + (size_t)t * krs + c) : 0.f;
+    sm.Kt[c][r] = (t < s.T) ? ld_f(Kg + (size_t)t * krs + c) : 0.f;
+  }
+  {
+    const float* cg = p.coef + (size_t)ch * 3 * E * C;
+    for (int idx = tid; idx < 3 * E * C; idx += 256) (&sm.coef[0][0][0])[idx] = cg[idx];
+  }
+
+  // accumulators: dq_s, dk_s tiles (rt, ct) for this wave's key columns
+  f32x4 dq[NT][CTW], dk[NT][CTW];
+#pragma unroll
+  for (int rt = 0; rt < NT; ++rt)
+#pragma unroll
+    for (int c = 0; c < CTW; ++c) {
+      dq[rt][c] = zero4();
+      dk[rt][c] = zero4();
+    }
+  float rsum_db[NT][4], rsum_da[NT][4], rsum_dc[NT][4];
+  const T* Sck = (const T*)sv.Sck;
+  const T* dSck = (const T*)bb.dSck;
+
+  for (int e = 0; e < E; ++e) {
+    f32x4 X[NT][CTW], Y[NT][CTW], Vp[NT][CTW];
+#pragma unroll
+    for (int rt = 0; rt < NT; ++rt)
+#pragma unroll
+      for (int c = 0; c < CTW; ++c) {
+        X[rt][c] = zero4();
+        Y[rt][c] = zero4();
+        Vp[rt][c] = zero4();
+      }
+    float gpart = 0.f;
+    for (int vb = 0; vb < V / 16; ++vb) {
+      __syncthreads();
+      // stage the 16-column block vb of dO, dW, U for all chunk rows
+      for (int idx = tid; idx < C * 4; idx += 256) {
+        const int r = idx >> 2, c4 = idx & 3;
+        const int t = t0 + r;
+        const int col = 16 * vb + 4 * c4;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          sm.dO[r][4 * c4 + j] = (t < s.T) ? dOg[(size_t)t * vrs + col + j] : T(0);
+        const f32x4 dw = *(const f32x4*)(bb.dW + (size_t)ch * C * V + (size_t)r * V + col);
+        const f32x4 u = *(const f32x4*)(sv.U + (size_t)ch * C * V + (size_t)r * V + col);
+        F hi, lo;
+        split_frag(dw, hi, lo);
+        *(F*)&sm.dWh[r][4 * c4] = hi;
+        if constexpr (SPLIT) *(F*)&sm.dWl[r][4 * c4] = lo;
+        split_frag(u, hi, lo);
+        *(F*)&sm.Uh[r][4 * c4] = hi;
+        if constexpr (SPLIT) *(F*)&sm.Ul[r][4 * c4] = lo;
+      }
+      __syncthreads();
+      const size_t tile = ((size_t)ch * E + e) * (V / 16) + vb;
+#pragma unroll
+      for (int c = 0; c < CTW; ++c) {
+        const int ct = w * CTW + c;
+        if (ct >= KT) continue;
+        // B fragments: S_e^T and dS'_e^T for key columns 16 ct + n, values 4 g + j
+        const F sb = ld_frag(Sck + tile * KD * 16 + (16 * ct + n) * 16 + 4 * g);
+        const F db = ld_frag(dSck + tile * KD * 16 + (16 * ct + n) * 16 + 4 * g);
+        {  // <S_e, dS'_e> over this block
+          const f32x4 a = frag_to_f(sb), d = frag_to_f(db);
+          gpart += a[0] * d[0] + a[1] * d[1] + a[2] * d[2] + a[3] * d[3];
+        }
+#pragma unroll
+        for (int rt = 0; rt < NT; ++rt) {
+          const int r = 16 * rt + n;
+          mma16(X[rt][c], ld_frag(&sm.dO[r][4 * g]), sb);
+          mma16(Y[rt][c], ld_frag(&sm.dWh[r][4 * g]), sb);
+          mma16(Vp[rt][c], ld_frag(&sm.Uh[r][4 * g]), db);
+          if constexpr (SPLIT) {
+            mma16(Y[rt][c], ld_frag(&sm.dWl[r][4 * g]), sb);
+            mma16(Vp[rt][c], ld_frag(&sm.Ul[r][4 * g]), db);
+          }
+        }
+      }
+    }
+    // fold slice e into dq_s, dk_s and the row sums
+#pragma unroll
+    for (int rt = 0; rt < NT; ++rt) {
+      const f32x4 ca = *(const f32x4*)&sm.coef[0][e][16 * rt + 4 * g];
+      const f32x4 cb = *(const f32x4*)&sm.coef[1][e][16 * rt + 4 * g];
+      const f32x4 cc = *(const f32x4*)&sm.coef[2][e][16 * rt + 4 * g];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        rsum_db[rt][j] = 0.f;
+        rsum_da[rt][j] = 0.f;
+        rsum_dc[rt][j] = 0.f;
+      }
+#pragma unroll
+      for (int c = 0; c < CTW; ++c) {
+        const int ct = w * CTW + c;
+        if (ct >= KT) continue;
+        dq[rt][c] += cb * X[rt][c];
+        dk[rt][c] += ca * Y[rt][c] + cc * Vp[rt][c];
+        const f32x4 qv = *(const f32x4*)&sm.Qt[16 * ct + n][16 * rt + 4 * g];
+        const f32x4 kv = *(const f32x4*)&sm.Kt[16 * ct + n][16 * rt + 4 * g];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          rsum_db[rt][j] += qv[j] * X[rt][c][j];
+          rsum_da[rt][j] += kv[j] * Y[rt][c][j];
+          rsum_dc[rt][j] += kv[j] * Vp[rt][c][j];
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float x0 = group16_sum(rsum_db[rt][j]);
+        const float x1 = group16_sum(rsum_da[rt][j]);
+        const float x2 = group16_sum(rsum_dc[rt][j]);
+        if (n == 0) {
+          sm.red[w][1][e][16 * rt + 4 * g + j] = x0;
+          sm.red[w][0][e][16 * rt + 4 * g + j] = x1;
+          sm.red[w][2][e][16 * rt + 4 * g + j] = x2;
+        }
+      }
+    }
+    gpart = wave_sum(gpart);
+    if (l == 0) sm.gred[w][e] = gpart;
+  }
+  __syncthreads();
+  // fixed-order sums over the four waves
+  for (int idx = tid; idx < 3 * E * C; idx += 256) {
+    const int kind = idx / (E * C), rem = idx % (E * C);
+    const int e = rem / C, r = rem % C;
+    bb.dcoef[(size_t)ch * 3 * E * C + idx] =
+        ((sm.red[0][kind][e][r] + sm.red[1][kind][e][r]) + sm.red[2][kind][e][r]) + sm.red[3][kind][e][r];
+  }
+  if (tid < E4)
+    bb.dgC[(size_t)ch * E4 + tid] =
+        (tid < E) ? ((sm.gred[0][tid] + sm.gred[1][tid]) + sm.gred[2][tid]) + sm.gred[3][tid] : 0.f;
+  // dq_s, dk_s
+#pragma unroll
+  for (int rt = 0; rt < NT; ++rt)
+#pragma unroll
+    for (int c = 0; c < CTW; ++c) {
+      const int ct = w * CTW + c;
+      if (ct >= KT) continue;
+      float* q = bb.dqs + (size_t)ch * C * KD + (size_t)(16 * rt + 4 * g) * KD + 16 * ct + n;
+      float* k = bb.dks + (size_t)ch * C * KD + (size_t)(16 * rt + 4 * g) * KD + 16 * ct + n;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        q[(size_t)j * KD] = dq[rt][c][j];
+        k[(size_t)j * KD] = dk[rt][c][j];
+      }
+    }
+}
+
+// ========================================================= per-chunk gradients
+template <int C, int E>
+struct ChunkSmem {
+  static constexpr int CP = C + 1;
+  float Aqk[C][CP];               // A_qk, then dR' = dM o A_qk
+  float Akk[C][CP];               // A_kk, then dR = dA_hat o A_kk
+  float R[C][CP];                 // R (strictly lower)
+  float Ninv[C][CP];              // (I + L)^{-1}, then dL o A_hat
+  float dM[C][CP];                // dM, then dA_qk
+  float dT[C][CP];                // dTu, then P = N^{-T} dTu, then dA_kk
+  float q2[C][E], k2[C][E], gam[C][E], gtail[C][E];
+  double G[C][E];
+  float dG[C][E];
+  float beta[C], dbeta[C];
+  float dcf[3][E][C];
+  float dgC[E];
+};
+
+template <typename T, int KD, int C, int E>
+__global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void* dOv,
+                                                   SavedBufs sv, BwdBufs bb, void* dqv, void* dkv,
+                                                   void* dvv, void* dq2v, void* dk2v, float* dg,
+                                                   float* dbeta) {
+  constexpr int NT = C / 16;
+  constexpr int E4 = (E + 3) & ~3;
+  typedef ChunkSmem<C, E> Sm;
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  Sm& sm = *reinterpret_cast<Sm*>(smem_raw);
+  const int tid = threadIdx.x, w = wave_id(), l = lane_id(), g = l >> 4, n = l & 15;
+  const int V = s.V;
+  const int ch = blockIdx.x;
+  const int head = ch / s.Nc, ci = ch % s.Nc;
+  const int b = head / s.H, h = head % s.H;
+  const int t0 = ci * C;
+  const size_t krs = (size_t)s.H * KD, vrs = (size_t)s.H * V;
+  const T* Kg = (const T*)in.k + (((size_t)b * s.T) * s.H + h) * KD;
+  const T* Qg = (const T*)in.q + (((size_t)b * s.T) * s.H + h) * KD;
+  const T* Vg = (const T*)in.v + (((size_t)b * s.T) * s.H + h) * (size_t)V;
+  const T* dOg = (const T*)dOv + (((size_t)b * s.T) * s.H + h) * (size_t)V;
+  const size_t eoff = (((size_t)b * s.T) * s.H + h) * E;
+  const size_t erow = (size_t)s.H * E;
+  const bool gdn = s.variant == 1;  // the C x C work below runs on fp32 MFMA
+
+  // ---- per-position vectors
+  for (int idx = tid; idx < C * E; idx += 256) {
+    const int r = idx / E, e = idx % E;
+    const int t = t0 + r;
+    const bool ok = t < s.T;
+    sm.q2[r][e] = ok ? ld_f((const T*)in.q2 + eoff + (size_t)t * erow + e) : 0.f;
+    sm.k2[r][e] = ok ? ld_f((const T*)in.k2 + eoff + (size_t)t * erow + e) : 0.f;
+    sm.G[r][e] = ok ? (double)in.g[eoff + (size_t)t * erow + e] : 0.0;
+  }
+  for (int r = tid; r < C; r += 256) {
+    const int t = t0 + r;
+    sm.beta[r] = (t < s.T) ? (in.beta ? in.beta[((size_t)b * s.T + t) * s.H + h] : 1.f) : 0.f;
+  }
+  for (int idx = tid; idx < 3 * E * C; idx += 256)
+    (&sm.dcf[0][0][0])[idx] = bb.dcoef[(size_t)ch * 3 * E * C + idx];
+  if (tid < E) sm.dgC[tid] = bb.dgC[(size_t)ch * E4 + tid];
+  __syncthreads();
+  if (tid < E) {
+    double acc = 0.0;
+    for (int r = 0; r < C; ++r) {
+      acc += sm.G[r][tid];
+      sm.G[r][tid] = acc;
+    }
+  }
+  __syncthreads();
+  for (int idx = tid; idx < C * E; idx += 256) {
+    const int r = idx / E, e = idx % E;
+    const double G = sm.G[r][e], GC = sm.G[C - 1][e];
+    sm.gam[r][e] = __expf((float)G);
+    sm.gtail[r][e] = __expf((float)(GC - G));
+  }
+
+  // ---- A_qk = Q K^T, A_kk = K K^T; dM = dO U^T; dTu = dU X^T  (full C x C tiles)
+  for (int tile = w; tile < NT * NT; tile += 4) {
+    const int rt = tile / NT, st = tile % NT;
+    const int r = 16 * rt + n, c = 16 * st + n;
+    const bool rok = t0 + r < s.T, cok = t0 + c < s.T;
+    f32x4 aq = zero4(), ak = zero4(), dm = zero4(), dt = zero4();
+    if (st <= rt) {
+      const T* qr = Qg + (size_t)(rok ? t0 + r : 0) * krs;
+      const T* kr = Kg + (size_t)(rok ? t0 + r : 0) * krs;
+      const T* kc = Kg + (size_t)(cok ? t0 + c : 0) * krs;
+      for (int kb = 0; kb < KD / 16; ++kb) {
+        const f32x4 bq = cok ? ld4_f(kc + 16 * kb + 4 * g) : zero4();
+        const f32x4 a1 = rok ? ld4_f(qr + 16 * kb + 4 * g) : zero4();
+        const f32x4 a2 = rok ? ld4_f(kr + 16 * kb + 4 * g) : zero4();
+        mma16(aq, a1, bq);
+        mma16(ak, a2, bq);
+      }
+      const T* dor = dOg + (size_t)(rok ? t0 + r : 0) * vrs;
+      const float* ur = sv.U + (size_t)ch * C * V + (size_t)c * V;
+      const float* dur = bb.dU + (size_t)ch * C * V + (size_t)r * V;
+      const float* xr = sv.X + (size_t)ch * C * V + (size_t)c * V;
+      for (int kb = 0; kb < V / 16; ++kb) {
+        const f32x4 a1 = rok ? ld4_f(dor + 16 * kb + 4 * g) : zero4();
+        mma16(dm, a1, *(const f32x4*)(ur + 16 * kb + 4 * g));
+        if (gdn) mma16(dt, *(const f32x4*)(dur + 16 * kb + 4 * g), *(const f32x4*)(xr + 16 * kb + 4 * g));
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int rr = 16 * rt + 4 * g + j, cc = 16 * st + n;
+      sm.Aqk[rr][cc] = aq[j];
+      sm.Akk[rr][cc] = ak[j];
+      sm.dM[rr][cc] = (cc <= rr) ? dm[j] : 0.f;
+      sm.dT[rr][cc] = dt[j];
+    }
+  }
+  // dTu is needed in full (upper part too): the tiles above the diagonal
+  if (gdn) {
+    for (int tile = w; tile < NT * NT; tile += 4) {
+      const int rt = tile / NT, st = tile % NT;
+      if (st <= rt) continue;
+      const int r = 16 * rt + n, c = 16 * st + n;
+      f32x4 dt = zero4();
+      const float* dur = bb.dU + (size_t)ch * C * V + (size_t)r * V;
+      const float* xr = sv.X + (size_t)ch * C * V + (size_t)c * V;
+      for (int kb = 0; kb < V / 16; ++kb)
+        mma16(dt, *(const f32x4*)(dur + 16 * kb + 4 * g), *(const f32x4*)(xr + 16 * kb + 4 * g));
+#pragma unroll
+      for (int j = 0; j < 4; ++j) sm.dT[16 * rt + 4 * g + j][16 * st + n] = dt[j];
+    }
+  }
+  __syncthreads();
+
+  // ---- R', R element by element; dA_qk = dM o R', dR' = dM o A_qk
+  for (int idx = tid; idx < C * C; idx += 256) {
+    const int r = idx / C, c = idx % C;
+    float rq = 0.f, rk = 0.f;
+    if (c <= r) {
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const float d = __expf((float)(sm.G[r][e] - sm.G[c][e]));
+        rq += sm.q2[r][e] * sm.k2[c][e] * d;
+        rk += sm.k2[r][e] * sm.k2[c][e] * d;
+      }
+    }
+    sm.R[r][c] = (c < r) ? rk : 0.f;
+    const float dm = sm.dM[r][c];
+    sm.Aqk[r][c] = dm * sm.Aqk[r][c];  // dR'
+    sm.dM[r][c] = dm * rq;             // dA_qk
+  }
+  __syncthreads();
+
+  if (gdn) {
+    // N^{-1} by forward substitution, one column per thread
+    if (tid < C) {
+      const int c = tid;
+      float x[C];
+#pragma unroll
+      for (int r = 0; r < C; ++r) {
+        float acc = 0.f;
+#pragma unroll
+        for (int j = 0; j < r; ++j) acc += (sm.beta[r] * sm.Akk[r][j] * sm.R[r][j]) * x[j];
+        x[r] = (r < c) ? 0.f : ((r == c) ? 1.f : -acc);
+      }
+#pragma unroll
+      for (int r = 0; r < C; ++r) sm.Ninv[r][c] = x[r];
+    }
+    __syncthreads();
+    // P = N^{-T} dTu: P[r][c] = sum_k Ninv[k][r] dT[k][c]
+    float pv[(C * C + 255) / 256];
+#pragma unroll
+    for (int i = 0; i < (C * C + 255) / 256; ++i) {
+      const int idx = tid + 256 * i;
+      float acc = 0.f;
+      if (idx < C * C) {
+        const int r = idx / C, c = idx % C;
+        for (int k = r; k < C; ++k) acc += sm.Ninv[k][r] * sm.dT[k][c];
+      }
+      pv[i] = acc;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < (C * C + 255) / 256; ++i) {
+      const int idx = tid + 256 * i;
+      if (idx < C * C) sm.dT[idx / C][idx % C] = pv[i];
+    }
+    __syncthreads();
+    // dbeta_r = P_rr + sum_{s<r} dL_rs A_hat_rs, with dN = -P Tu^T, Tu = Ninv diag(beta)
+    //   dN[r][s] = -sum_k P[r][k] Ninv[s][k] beta[k]   (k <= s)
+    float dl[(C * C + 255) / 256];
+#pragma unroll
+    for (int i = 0; i < (C * C + 255) / 256; ++i) {
+      const int idx = tid + 256 * i;
+      float acc = 0.f;
+      if (idx < C * C) {
+        const int r = idx / C, c = idx % C;
+        if (c < r)
+          for (int k = 0; k <= c; ++k) acc -= sm.dT[r][k] * sm.Ninv[c][k] * sm.beta[k];
+      }
+      dl[i] = acc;
+    }
+    if (tid < C) sm.dbeta[tid] = sm.dT[tid][tid];
+    __syncthreads();
+    // dA_hat = diag(beta) dL; dA_kk = dA_hat o R (into dT); dR = dA_hat o A_kk (into Akk)
+#pragma unroll
+    for (int i = 0; i < (C * C + 255) / 256; ++i) {
+      const int idx = tid + 256 * i;
+      if (idx < C * C) {
+        const int r = idx / C, c = idx % C;
+        const float dah = sm.beta[r] * dl[i];
+        const float akk = sm.Akk[r][c], rr = sm.R[r][c];
+        sm.Akk[r][c] = dah * akk;          // dR
+        sm.dT[r][c] = dah * rr;            // dA_kk
+        // dL_rs * A_hat_rs, summed per row below (A_hat = A_kk o R)
+        sm.Ninv[r][c] = dl[i] * akk * rr;
+      }
+    }
+    __syncthreads();
+    if (tid < C) {
+      float acc = 0.f;
+      for (int c = 0; c < tid; ++c) acc += sm.Ninv[tid][c];
+      sm.dbeta[tid] += acc;
+    }
+  } else {
+    for (int idx = tid; idx < C * C; idx += 256) {
+      sm.Akk[idx / C][idx % C] = 0.f;  // dR
+      sm.dT[idx / C][idx % C] = 0.f;   // dA_kk
+    }
+    if (tid < C) {  // sGLA: dbeta_r = <dU_r, v_r>
+      const int r = tid, t = t0 + r;
+      float acc = 0.f;
+      if (t < s.T)
+        for (int c = 0; c < V; ++c)
+          acc += bb.dU[(size_t)ch * C * V + (size_t)r * V + c] * ld_f(Vg + (size_t)t * vrs + c);
+      sm.dbeta[r] = acc;
+    }
+  }
+  __syncthreads();
+
+  // ---- dq = dq_s + dA_qk K;  dk = dk_s + dA_qk^T Q + (dA_kk + dA_kk^T) K
+  {
+    constexpr int KT = KD / 16;
+    for (int tile = w; tile < NT * KT; tile += 4) {
+      const int rt = tile / KT, kt = tile % KT;
+      f32x4 aq = zero4(), ak = zero4();
+      const int r = 16 * rt + n;  // A row
+      for (int sb = 0; sb < NT; ++sb) {
+        f32x4 bk, bqv;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int srow = 16 * sb + 4 * g + j;
+          const int t = t0 + srow;
+          bk[j] = (t < s.T) ? ld_f(Kg + (size_t)t * krs + 16 * kt + n) : 0.f;
+          bqv[j] = (t < s.T) ? ld_f(Qg + (size_t)t * krs + 16 * kt + n) : 0.f;
+        }
+        f32x4 a1, a2, a3;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int cidx = 16 * sb + 4 * g + j;
+          a1[j] = sm.dM[r][cidx];                        // dA_qk[r][s]
+          a2[j] = sm.dM[cidx][r];                        // dA_qk^T[r][s]
+          a3[j] = sm.dT[r][cidx] + sm.dT[cidx][r];       // dA_kk + dA_kk^T
+        }
+        mma16(aq, a1, bk);
+        mma16(ak, a2, bqv);
+        mma16(ak, a3, bk);
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int rr = 16 * rt + 4 * g + j;
+        const int t = t0 + rr;
+        if (t < s.T) {
+          const size_t o = (((size_t)b * s.T + t) * s.H + h) * KD + 16 * kt + n;
+          const float vq = aq[j] + bb.dqs[(size_t)ch * C * KD + (size_t)rr * KD + 16 * kt + n];
+          const float vk = ak[j] + bb.dks[(size_t)ch * C * KD + (size_t)rr * KD + 16 * kt + n];
+          store_out(dqv, o, vq, s.out_bf16);
+          store_out(dkv, o, vk, s.out_bf16);
+        }
+      }
+    }
+  }
+  // ---- dv
+  for (int idx = tid; idx < C * V; idx += 256) {
+    const int r = idx / V, c = idx % V;
+    const int t = t0 + r;
+    if (t >= s.T) continue;
+    const float val = gdn ? -bb.dW[(size_t)ch * C * V + idx]
+                          : sm.beta[r] * bb.dU[(size_t)ch * C * V + idx];
+    store_out(dvv, (((size_t)b * s.T + t) * s.H + h) * (size_t)V + c, val, s.out_bf16);
+  }
+
+  // ---- Gram backward: rows (dq2, dk2 via dR rows, dG row sums) and columns
+  for (int idx = tid; idx < C * E; idx += 256) {
+    const int r = idx / E, e = idx % E;
+    float aq2 = 0.f, ak2 = 0.f, grow = 0.f;
+    for (int c = 0; c <= r; ++c) {
+      const float d = __expf((float)(sm.G[r][e] - sm.G[c][e]));
+      const float drq = sm.Aqk[r][c] * d;
+      const float drk = (c < r) ? sm.Akk[r][c] * d : 0.f;
+      aq2 += drq * sm.k2[c][e];
+      ak2 += drk * sm.k2[c][e];
+      grow += (drq * sm.q2[r][e] + drk * sm.k2[r][e]) * sm.k2[c][e];
+    }
+    float acol = 0.f, gcol = 0.f;
+    for (int rr = r; rr < C; ++rr) {  // r as the column index s
+      const float d = __expf((float)(sm.G[rr][e] - sm.G[r][e]));
+      const float drq = sm.Aqk[rr][r] * d;
+      const float drk = (rr > r) ? sm.Akk[rr][r] * d : 0.f;
+      acol += drq * sm.q2[rr][e] + drk * sm.k2[rr][e];
+      gcol += (drq * sm.q2[rr][e] + drk * sm.k2[rr][e]) * sm.k2[r][e];
+    }
+    const float da = sm.dcf[0][e][r], db = sm.dcf[1][e][r], dc = sm.dcf[2][e][r];
+    const float gm = sm.gam[r][e], gt = sm.gtail[r][e];
+    // coefficient vectors a = k2 gamma, b = q2 gamma, c = k2 gamma^C / gamma
+    sm.dG[r][e] = grow - gcol + da * sm.k2[r][e] * gm + db * sm.q2[r][e] * gm -
+                  dc * sm.k2[r][e] * gt;
+    const int t = t0 + r;
+    if (t < s.T) {
+      const size_t o = eoff + (size_t)t * erow + e;
+      store_out(dq2v, o, aq2 + db * gm, s.out_bf16);
+      store_out(dk2v, o, ak2 + acol + da * gm + dc * gt, s.out_bf16);
+    }
+  }
+  __syncthreads();
+  if (tid < E) {
+    const int e = tid;
+    float acc = 0.f;
+    for (int r = 0; r < C; ++r) acc += sm.dcf[2][e][r] * sm.k2[r][e] * sm.gtail[r][e];
+    sm.dG[C - 1][e] += acc + sm.gam[C - 1][e] * sm.dgC[e];
+    // reverse cumulative sum within the chunk: dg_j = sum_{r >= j} dG_r
+    float run = 0.f;
+    for (int r = C - 1; r >= 0; --r) {
+      run += sm.dG[r][e];
+      sm.dG[r][e] = run;
+    }
+  }
+  __syncthreads();
+  for (int idx = tid; idx < C * E; idx += 256) {
+    const int r = idx / E, e = idx % E;
+    const int t = t0 + r;
+    if (t >= s.T) continue;
+    dg[eoff + (size_t)t * erow + e] = sm.dG[r][e];
+  }
+  if (dbeta && tid < C) {
+    const int t = t0 + tid;
+    if (t < s.T) dbeta[((size_t)b * s.T + t) * s.H + h] = sm.dbeta[tid];
+  }
+  (void)l;
+}
+
+// ----------------------------------------------------------------- launchers
+template <typename T, int KD, int C, int E>
+static hipError_t rec_inst(const Shape& s, const FwdIn& in, const void* dO, const float* dSf,
+                           const PrepBufs& p, const BwdBufs& bb, float* ds0, hipStream_t st) {
+  constexpr int NW = bwd_waves<E>();
+  const size_t smem = sizeof(RecSmem<T, KD, C, E, NW>);
+  static bool attr = false;
+  if (!attr) {
+    (void)hipFuncSetAttribute((const void*)k_bwd_rec<T, KD, C, E, NW>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+    attr = true;
+  }
+  hipLaunchKernelGGL((k_bwd_rec<T, KD, C, E, NW>), dim3(s.NH * (s.V / 16)), dim3(NW * 64), smem,
+                     st, s, in, dO, dSf, p, bb, ds0);
+  return hipGetLastError();
+}
+
+template <typename T, int KD, int C, int E>
+static hipError_t state_inst(const Shape& s, const FwdIn& in, const void* dO, const PrepBufs& p,
+                             const SavedBufs& sv, const BwdBufs& bb, hipStream_t st) {
+  const size_t smem = sizeof(StateSmem<T, KD, C, E>);
+  static bool attr = false;
+  if (!attr) {
+    (void)hipFuncSetAttribute((const void*)k_bwd_state<T, KD, C, E>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+    attr = true;
+  }
+  hipLaunchKernelGGL((k_bwd_state<T, KD, C, E>), dim3(s.NH * s.Nc), dim3(256), smem, st, s, in, dO,
+                     p, sv, bb);
+  return hipGetLastError();
+}
+
+template <typename T, int KD, int C, int E>
+static hipError_t chunk_inst(const Shape& s, const FwdIn& in, const void* dO, const SavedBufs& sv,
+                             const BwdBufs& bb, void* dq, void* dk, void* dv, void* dq2, void* dk2,
+                             float* dg, float* dbeta, hipStream_t st) {
+  const size_t smem = sizeof(ChunkSmem<C, E>);
+  static bool attr = false;
+  if (!attr) {
+    (void)hipFuncSetAttribute((const void*)k_bwd_chunk<T, KD, C, E>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+    attr = true;
+  }
+  hipLaunchKernelGGL((k_bwd_chunk<T, KD, C, E>), dim3(s.NH * s.Nc), dim3(256), smem, st, s, in, dO,
+                     sv, bb, dq, dk, dv, dq2, dk2, dg, dbeta);
+  return hipGetLastError();
+}
+
+#define TLA_BWD_DISPATCH(KD_, C_, E_, CALL)              \
+  if (s.K == KD_ && s.C == C_ && s.E == E_) {            \
+    if (s.in_bf16) return CALL(bf16_t, KD_, C_, E_);     \
+    return CALL(float, KD_, C_, E_);                     \
+  }
+#define TLA_BWD_FOR_EACH(CALL)      \
+  TLA_BWD_DISPATCH(16, 16, 4, CALL) \
+  TLA_BWD_DISPATCH(32, 32, 4, CALL) \
+  TLA_BWD_DISPATCH(64, 32, 8, CALL) \
+  TLA_BWD_DISPATCH(128, 64, 1, CALL) \
+  TLA_BWD_DISPATCH(128, 64, 4, CALL) \
+  TLA_BWD_DISPATCH(128, 64, 8, CALL) \
+  TLA_BWD_DISPATCH(128, 64, 16, CALL) \
+  TLA_BWD_DISPATCH(128, 32, 8, CALL)
+
+template <typename T, int KD, int C, int E>
+static bool bwd_fits_inst() {
+  return sizeof(RecSmem<T, KD, C, E, bwd_waves<E>()>) <= 160 * 1024 &&
+         sizeof(StateSmem<T, KD, C, E>) <= 160 * 1024 && sizeof(ChunkSmem<C, E>) <= 160 * 1024;
+}
+
+bool bwd_fits_lds(int K, int C, int E, bool bf16) {
+  const Shape s{0, 1, 1, 1, K, 16, E, C, 1, 1, bf16 ? 1 : 0, 0, 0};
+#define FITS_B(T_, KD_, C_, E_) bwd_fits_inst<T_, KD_, C_, E_>()
+  TLA_BWD_FOR_EACH(FITS_B)
+#undef FITS_B
+  return false;
+}
+
+hipError_t launch_bwd_rec(const Shape& s, const FwdIn& in, const void* dO, const float* dS_final,
+                          const PrepBufs& p, const BwdBufs& bb, float* ds0, hipStream_t st) {
+#define CALL_REC(T_, KD_, C_, E_) rec_inst<T_, KD_, C_, E_>(s, in, dO, dS_final, p, bb, ds0, st)
+  TLA_BWD_FOR_EACH(CALL_REC)
+#undef CALL_REC
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_bwd_state(const Shape& s, const FwdIn& in, const void* dO, const PrepBufs& p,
+                            const SavedBufs& sv, const BwdBufs& bb, hipStream_t st) {
+#define CALL_ST(T_, KD_, C_, E_) state_inst<T_, KD_, C_, E_>(s, in, dO, p, sv, bb, st)
+  TLA_BWD_FOR_EACH(CALL_ST)
+#undef CALL_ST
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_bwd_chunk(const Shape& s, const FwdIn& in, const void* dO, const SavedBufs& sv,
+                            const BwdBufs& bb, void* dq, void* dk, void* dv, void* dq2, void* dk2,
+                            float* dg, float* dbeta, hipStream_t st) {
+#define CALL_CH(T_, KD_, C_, E_) \
+  chunk_inst<T_, KD_, C_, E_>(s, in, dO, sv, bb, dq, dk, dv, dq2, dk2, dg, dbeta, st)
+  TLA_BWD_FOR_EACH(CALL_CH)
+#undef CALL_CH
+  return hipErrorInvalidValue;
 }
 
 }  // namespace tla

@@ -90,6 +90,8 @@ template <> __device__ __forceinline__ bf16x4 cvt_frag<bf16_t>(f32x4 x) {
 __device__ __forceinline__ f32x4 bf16x4_to_f(bf16x4 x) {
   return f32x4{(float)x[0], (float)x[1], (float)x[2], (float)x[3]};
 }
+__device__ __forceinline__ f32x4 frag_to_f(bf16x4 x) { return bf16x4_to_f(x); }
+__device__ __forceinline__ f32x4 frag_to_f(f32x4 x) { return x; }
 __device__ __forceinline__ void split_frag(f32x4 x, bf16x4& hi, bf16x4& lo) {
   hi = cvt_frag<bf16_t>(x);
   lo = cvt_frag<bf16_t>(x - bf16x4_to_f(hi));

@@ -205,6 +205,157 @@ struct FwdSmem {
   alignas(16) f32x4 O[NW][NT][64];
 };
 
+template <typename T>
+struct Raw8 {
+  T x[8];
+};
+template <typename T>
+__device__ __forceinline__ Raw8<T> load8(const T* src) {
+  Raw8<T> r;
+  copy8(r.x, src);
+  return r;
+}
+template <typename T>
+__device__ __forceinline__ Raw8<T> zero_raw8() {
+  Raw8<T> r;
+  zero8(r.x);
+  return r;
+}
+
+// Register staging of one chunk's inputs for the recurrent forward: global
+// loads are issued one chunk ahead into registers and written to shared
+// memory (including the transposed copies) at the top of the next chunk.
+template <typename T, int KD, int C, int E, int NTHR, bool STAGE_Q, bool SPLIT>
+struct FwdStage {
+  static constexpr int RB = C / 4, CB = KD / 8;
+  static constexpr int NKB = (RB * CB + NTHR - 1) / NTHR;  // 4x8 blocks of K (and Q)
+  static constexpr int NV4 = (C * 4 + NTHR - 1) / NTHR;    // 4-element pieces of the V tile
+  static constexpr int NMB = (C * C / 4 + NTHR - 1) / NTHR;
+  static constexpr int NCB = (3 * E * C / 4 + NTHR - 1) / NTHR;
+  static constexpr int E4 = (E + 3) & ~3;
+  Raw8<T> k[NKB][4];
+  Raw8<T> q[STAGE_Q ? NKB : 1][4];
+  T v[NV4][4];
+  f32x4 m[NMB], tu[NMB], c[NCB];
+  float gc, beta;
+
+  __device__ __forceinline__ void load(const Shape& s, const FwdIn& in, const PrepBufs& p,
+                                       const T* Kg, const T* Qg, const T* Vg, int b, int h,
+                                       int ci) {
+    const int tid = threadIdx.x;
+    const int t0 = ci * C;
+    const size_t ch = (size_t)(b * s.H + h) * s.Nc + ci;
+    const size_t krs = (size_t)s.H * KD, vrs = (size_t)s.H * s.V;
+#pragma unroll
+    for (int i = 0; i < NKB; ++i) {
+      const int blk = tid + i * NTHR;
+      const int rb = blk % RB, cb = blk / RB;
+      if (blk < RB * CB) {
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) {
+          const int t = t0 + 4 * rb + rr;
+          k[i][rr] = (t < s.T) ? load8(Kg + (size_t)t * krs + 8 * cb) : zero_raw8<T>();
+          if constexpr (STAGE_Q)
+            q[i][rr] = (t < s.T) ? load8(Qg + (size_t)t * krs + 8 * cb) : zero_raw8<T>();
+        }
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < NV4; ++i) {
+      const int idx = tid + i * NTHR;
+      const int r = idx >> 2, c4 = idx & 3;
+      if (idx < C * 4) {
+        const int t = t0 + r;
+        if (t < s.T) {
+          if constexpr (sizeof(T) == 2)
+            *(uint2*)v[i] = *(const uint2*)(Vg + (size_t)t * vrs + 4 * c4);
+          else
+            *(float4*)v[i] = *(const float4*)(Vg + (size_t)t * vrs + 4 * c4);
+        } else {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) v[i][j] = T(0);
+        }
+      }
+    }
+    const float* Mg = p.M + ch * C * C;
+    const float* Tg = p.Tu + ch * C * C;
+#pragma unroll
+    for (int i = 0; i < NMB; ++i) {
+      const int idx = tid + i * NTHR;
+      if (idx < C * C / 4) {
+        m[i] = *(const f32x4*)(Mg + 4 * idx);
+        if (s.variant == 1) tu[i] = *(const f32x4*)(Tg + 4 * idx);
+      }
+    }
+    const float* cg = p.coef + ch * 3 * E * C;
+#pragma unroll
+    for (int i = 0; i < NCB; ++i) {
+      const int idx = tid + i * NTHR;
+      if (idx < 3 * E * C / 4) c[i] = *(const f32x4*)(cg + 4 * idx);
+    }
+    if (tid < E4) gc = p.gC[ch * E4 + tid];
+    if (tid < C) {
+      const int t = t0 + tid;
+      beta = (t < s.T) ? (in.beta ? in.beta[((size_t)b * s.T + t) * s.H + h] : 1.f) : 0.f;
+    }
+  }
+
+  template <typename Sm>
+  __device__ __forceinline__ void store(Sm& sm, int variant) const {
+    typedef typename Elem<T>::frag F;
+    const int tid = threadIdx.x;
+#pragma unroll
+    for (int i = 0; i < NKB; ++i) {
+      const int blk = tid + i * NTHR;
+      const int rb = blk % RB, cb = blk / RB;
+      if (blk < RB * CB) {
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) {
+          copy8(&sm.K[4 * rb + rr][8 * cb], k[i][rr].x);
+          if constexpr (STAGE_Q) copy8(&sm.Q[4 * rb + rr][8 * cb], q[i][rr].x);
+        }
+#pragma unroll
+        for (int cc = 0; cc < 8; ++cc)
+#pragma unroll
+          for (int rr = 0; rr < 4; ++rr) sm.Kt[8 * cb + cc][4 * rb + rr] = k[i][rr].x[cc];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < NV4; ++i) {
+      const int idx = tid + i * NTHR;
+      const int r = idx >> 2, c4 = idx & 3;
+      if (idx < C * 4) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) sm.Vt[4 * c4 + j][r] = v[i][j];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < NMB; ++i) {
+      const int idx = tid + i * NTHR;
+      if (idx < C * C / 4) {
+        const int r = idx / (C / 4), c4 = idx % (C / 4);
+        F hi, lo;
+        split_frag(m[i], hi, lo);
+        *(F*)&sm.M[r][4 * c4] = hi;
+        if constexpr (SPLIT) *(F*)&sm.ML[r][4 * c4] = lo;
+        if (variant == 1) {
+          split_frag(tu[i], hi, lo);
+          *(F*)&sm.Tu[r][4 * c4] = hi;
+          if constexpr (SPLIT) *(F*)&sm.TuL[r][4 * c4] = lo;
+        }
+      }
+    }
+    float* cs = &sm.coef[0][0][0];
+#pragma unroll
+    for (int i = 0; i < NCB; ++i) {
+      const int idx = tid + i * NTHR;
+      if (idx < 3 * E * C / 4) ((f32x4*)cs)[idx] = c[i];
+    }
+    if (tid < E4) sm.gC[tid] = gc;
+    if (tid < C) sm.beta[tid] = beta;
+  }
+};
+
 template <typename T, int KD, int C, int E, int NW>
 __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, void* out,
                                                  float* s_final, SavedBufs sv, int train) {
@@ -212,13 +363,12 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
   constexpr int NT = C / 16;
   constexpr int KT = KD / 16;
   constexpr int NTHR = NW * 64;
-  constexpr int E4 = (E + 3) & ~3;
   typedef typename Elem<T>::frag F;
   typedef FwdSmem<T, KD, C, E, NW> Sm;
   extern __shared__ __align__(16) unsigned char smem_raw[];
   Sm& sm = *reinterpret_cast<Sm*>(smem_raw);
 
-  const int tid = threadIdx.x, w = wave_id(), l = lane_id(), g = l >> 4, n = l & 15;
+  const int w = wave_id(), l = lane_id(), g = l >> 4, n = l & 15;
   const int V = s.V;
   int head, vt;
   xcd_map(blockIdx.x, s.NH, V / 16, head, vt);
@@ -246,79 +396,20 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
   const T* Qg = (const T*)in.q + (((size_t)b * s.T) * s.H + h) * KD;
   const T* Vg = (const T*)in.v + (((size_t)b * s.T) * s.H + h) * (size_t)V + v0;
   const size_t krs = (size_t)s.H * KD;  // row stride between positions
-  const size_t vrs = (size_t)s.H * V;
+
+  FwdStage<T, KD, C, E, NTHR, Sm::STAGE_Q, Sm::SPLIT> stage;
+  if (s.Nc > 0) stage.load(s, in, p, Kg, Qg, Vg, b, h, 0);
 
   for (int ci = 0; ci < s.Nc; ++ci) {
     const int t0 = ci * C;
     const size_t ch = (size_t)head * s.Nc + ci;
     __syncthreads();  // the previous chunk is done with shared memory
 
-    // ---- stage the chunk: K, Q (row-major), K^T, V tile (transposed), Tu, M, coefficients
-    constexpr int RB = C / 4, CB = KD / 8;
-    for (int blk = tid; blk < RB * CB; blk += NTHR) {
-      const int rb = blk % RB, cb = blk / RB;
-      T kv[4][8];
-#pragma unroll
-      for (int rr = 0; rr < 4; ++rr) {
-        const int r = 4 * rb + rr;
-        if (t0 + r < s.T) {
-          copy8(kv[rr], Kg + (size_t)(t0 + r) * krs + 8 * cb);
-          if constexpr (Sm::STAGE_Q) copy8(&sm.Q[r][8 * cb], Qg + (size_t)(t0 + r) * krs + 8 * cb);
-        } else {
-          zero8(kv[rr]);
-          if constexpr (Sm::STAGE_Q) zero8(&sm.Q[r][8 * cb]);
-        }
-        copy8(&sm.K[r][8 * cb], kv[rr]);
-      }
-#pragma unroll
-      for (int cc = 0; cc < 8; ++cc) {
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr) sm.Kt[8 * cb + cc][4 * rb + rr] = kv[rr][cc];
-      }
-    }
-    for (int blk = tid; blk < RB * 2; blk += NTHR) {
-      const int rb = blk % RB, cb = blk / RB;
-      T vv[4][8];
-#pragma unroll
-      for (int rr = 0; rr < 4; ++rr) {
-        const int r = 4 * rb + rr;
-        if (t0 + r < s.T)
-          copy8(vv[rr], Vg + (size_t)(t0 + r) * vrs + 8 * cb);
-        else
-          zero8(vv[rr]);
-      }
-#pragma unroll
-      for (int cc = 0; cc < 8; ++cc) {
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr) sm.Vt[8 * cb + cc][4 * rb + rr] = vv[rr][cc];
-      }
-    }
-    {
-      const float* Mg = p.M + ch * C * C;
-      const float* Tg = p.Tu + ch * C * C;
-      for (int idx = tid; idx < C * C / 4; idx += NTHR) {
-        const int r = idx / (C / 4), c4 = idx % (C / 4);
-        F hi, lo;
-        split_frag(*(const f32x4*)(Mg + r * C + 4 * c4), hi, lo);
-        *(F*)&sm.M[r][4 * c4] = hi;
-        if constexpr (Sm::SPLIT) *(F*)&sm.ML[r][4 * c4] = lo;
-        if (s.variant == 1) {
-          split_frag(*(const f32x4*)(Tg + r * C + 4 * c4), hi, lo);
-          *(F*)&sm.Tu[r][4 * c4] = hi;
-          if constexpr (Sm::SPLIT) *(F*)&sm.TuL[r][4 * c4] = lo;
-        }
-      }
-      const float* cg = p.coef + ch * 3 * E * C;
-      float* cs = &sm.coef[0][0][0];
-      for (int idx = tid; idx < 3 * E * C / 4; idx += NTHR)
-        ((float4*)cs)[idx] = ((const float4*)cg)[idx];
-      if (tid < E4) sm.gC[tid] = p.gC[ch * E4 + tid];
-      for (int r = tid; r < C; r += NTHR) {
-        const int t = t0 + r;
-        sm.beta[r] = (t < s.T) ? (in.beta ? in.beta[((size_t)b * s.T + t) * s.H + h] : 1.f) : 0.f;
-      }
-    }
+    // ---- stage the chunk from registers (loaded during the previous chunk)
+    stage.store(sm, s.variant);
     __syncthreads();
+    // next chunk's inputs are in flight while this chunk computes
+    if (ci + 1 < s.Nc) stage.load(s, in, p, Kg, Qg, Vg, b, h, ci + 1);
 
     // ---- operand copies of the chunk-start state
     F Sop[SPW][KT];
@@ -341,63 +432,57 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
       }
     }
 
-    // ---- P^K_e = K S_e and P^Q_e = Q S_e for the owned slices
-    f32x4 PK[SPW][NT], PQ[SPW][NT];
+    // ---- P^K_e = K S_e, then P^Q_e = Q S_e for the owned slices, each folded
+    // straight into this wave's partial of W = sum_e diag(a_e) P^K_e and of
+    // sum_e diag(b_e) P^Q_e (the two passes keep one set of accumulators live)
 #pragma unroll
-    for (int rt = 0; rt < NT; ++rt) {
+    for (int pass = 0; pass < 2; ++pass) {
+      f32x4 P[SPW][NT];
 #pragma unroll
-      for (int i = 0; i < SPW; ++i) {
-        PK[i][rt] = zero4();
-        PQ[i][rt] = zero4();
-      }
-      const int r = 16 * rt + n;
-      // query row r of the chunk (zero past the end of the sequence)
-      const bool qok = t0 + r < s.T;
-      const T* qrow = Qg + (size_t)(qok ? t0 + r : 0) * krs;
-      auto qfrag = [&](int kb) -> F {
-        if constexpr (Sm::STAGE_Q) return ld_frag(&sm.Q[r][16 * kb + 4 * g]);
-        else return qok ? ld_frag(qrow + 16 * kb + 4 * g) : cvt_frag<T>(zero4());
-      };
+      for (int rt = 0; rt < NT; ++rt) {
 #pragma unroll
-      for (int kb = 0; kb < KT; kb += (KT > 1 ? 2 : 1)) {
-        if constexpr (KT > 1) {
-          const F ak0 = ld_frag(&sm.K[r][16 * kb + 4 * g]);
-          const F ak1 = ld_frag(&sm.K[r][16 * kb + 16 + 4 * g]);
-          const F aq0 = qfrag(kb);
-          const F aq1 = qfrag(kb + 1);
+        for (int i = 0; i < SPW; ++i) P[i][rt] = zero4();
+        const int r = 16 * rt + n;
+        const bool qok = t0 + r < s.T;
+        const T* qrow = Qg + (size_t)(qok ? t0 + r : 0) * krs;
+        auto afrag = [&](int kb) -> F {
+          if (pass == 0) return ld_frag(&sm.K[r][16 * kb + 4 * g]);
+          if constexpr (Sm::STAGE_Q) return ld_frag(&sm.Q[r][16 * kb + 4 * g]);
+          else return qok ? ld_frag(qrow + 16 * kb + 4 * g) : cvt_frag<T>(zero4());
+        };
 #pragma unroll
-          for (int i = 0; i < SPW; ++i) {
-            if (w * SPW + i >= E) continue;
-            mma32(PK[i][rt], ak0, ak1, Sop[i][kb], Sop[i][kb + 1]);
-            mma32(PQ[i][rt], aq0, aq1, Sop[i][kb], Sop[i][kb + 1]);
-          }
-        } else {
-          const F ak = ld_frag(&sm.K[r][4 * g]);
-          const F aq = qfrag(0);
+        for (int kb = 0; kb < KT; kb += (KT > 1 ? 2 : 1)) {
+          if constexpr (KT > 1) {
+            const F a0 = afrag(kb), a1 = afrag(kb + 1);
 #pragma unroll
-          for (int i = 0; i < SPW; ++i) {
-            if (w * SPW + i >= E) continue;
-            mma16(PK[i][rt], ak, Sop[i][0]);
-            mma16(PQ[i][rt], aq, Sop[i][0]);
+            for (int i = 0; i < SPW; ++i) {
+              if (w * SPW + i >= E) continue;
+              mma32(P[i][rt], a0, a1, Sop[i][kb], Sop[i][kb + 1]);
+            }
+          } else {
+            const F a = afrag(0);
+#pragma unroll
+            for (int i = 0; i < SPW; ++i) {
+              if (w * SPW + i >= E) continue;
+              mma16(P[i][rt], a, Sop[i][0]);
+            }
           }
         }
       }
-    }
-    // ---- per-wave partial sums over the owned slices, exchanged through LDS
 #pragma unroll
-    for (int rt = 0; rt < NT; ++rt) {
-      f32x4 wp = zero4(), op = zero4();
+      for (int rt = 0; rt < NT; ++rt) {
+        f32x4 acc = zero4();
 #pragma unroll
-      for (int i = 0; i < SPW; ++i) {
-        const int e = w * SPW + i;
-        if (e >= E) continue;
-        const f32x4 ca = *(const f32x4*)&sm.coef[0][e][16 * rt + 4 * g];
-        const f32x4 cb = *(const f32x4*)&sm.coef[1][e][16 * rt + 4 * g];
-        wp += ca * PK[i][rt];
-        op += cb * PQ[i][rt];
+        for (int i = 0; i < SPW; ++i) {
+          const int e = w * SPW + i;
+          if (e >= E) continue;
+          acc += *(const f32x4*)&sm.coef[pass][e][16 * rt + 4 * g] * P[i][rt];
+        }
+        if (pass == 0)
+          sm.W[w][rt][l] = acc;
+        else
+          sm.O[w][rt][l] = acc;
       }
-      sm.W[w][rt][l] = wp;
-      sm.O[w][rt][l] = op;
     }
     __syncthreads();
 

@@ -67,5 +67,6 @@ hipError_t launch_step(const Shape& s, const FwdIn& in, float* state, void* o, h
 // forward/backward shared-memory plan of an instance fits 160 KiB.
 bool have_instance(int K, int C, int E);
 bool fits_lds(int K, int C, int E, bool bf16);
+bool bwd_fits_lds(int K, int C, int E, bool bf16);
 
 }  // namespace tla
