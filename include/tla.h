@@ -144,6 +144,21 @@ int tla_step(const tla_desc* desc, const void* q, const void* k, const void* v,
              const void* q2, const void* k2, const float* g, const float* beta,
              float* state, void* o, void* stream);
 
+/*
+ * Per-kernel timing, for diagnostics and benchmarks (not needed otherwise).
+ * tla_prof_enable(1) clears previous records and starts bracketing every
+ * kernel launch of the library with a pair of HIP events on the launch
+ * stream (events are created once and pooled); tla_prof_enable(0) stops and
+ * clears.  tla_prof_read() waits for the recorded events and fills, for each
+ * of the 6 kernel kinds named by tla_prof_name(0..5) ("prep",
+ * "fwd_recurrent", "bwd_recurrent", "bwd_state", "bwd_chunk", "step"), the
+ * summed event time in milliseconds and the number of launches; n must be
+ * at least 6.  Not meant for use while another thread launches.
+ */
+int tla_prof_enable(int on);
+int tla_prof_read(double* total_ms, int* launches, int n);
+const char* tla_prof_name(int kind);
+
 /* Static description of a status code. */
 const char* tla_status_string(int status);
 /* Message of the last failed call on this host thread ("" if none). */

@@ -61,6 +61,12 @@ def lib():
     L.tla_bwd.restype = I
     L.tla_step.argtypes = [DP] + [P] * 9 + [P]
     L.tla_step.restype = I
+    L.tla_prof_enable.argtypes = [I]
+    L.tla_prof_enable.restype = I
+    L.tla_prof_read.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I), I]
+    L.tla_prof_read.restype = I
+    L.tla_prof_name.argtypes = [I]
+    L.tla_prof_name.restype = ctypes.c_char_p
     _lib = L
     return L
 
@@ -207,3 +213,17 @@ def step(variant, q, k, v, q2, k2, g, beta, state, out_dtype=None, o=None):
                         _ptr(beta), _ptr(state), _ptr(o), _stream(dev))
     _check(rc)
     return o
+
+
+def prof_enable(on=True):
+    """Start (clearing old records) or stop per-kernel HIP-event timing."""
+    _check(lib().tla_prof_enable(1 if on else 0))
+
+
+def prof_read():
+    """{kernel name: (total ms, launches)} for the launches since prof_enable()."""
+    L = lib()
+    tot = (ctypes.c_double * 6)()
+    cnt = (ctypes.c_int * 6)()
+    _check(L.tla_prof_read(tot, cnt, 6))
+    return {L.tla_prof_name(i).decode(): (tot[i], cnt[i]) for i in range(6)}

@@ -5,6 +5,9 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
+#include <vector>
+
 #include <hip/hip_runtime.h>
 
 #include "../../include/tla.h"
@@ -146,6 +149,54 @@ int device_fail(hipError_t e, const char* what) {
   return fail(TLA_E_DEVICE, "%s: %s", what, hipGetErrorString(e));
 }
 
+// ------------------------------------------------------------- kernel timing
+// Diagnostics only: while enabled, every kernel launch of the library is
+// bracketed by a pair of HIP events recorded on the launch stream.  Events are
+// pooled and reused; nothing is recorded when timing is off.
+enum { PROF_PREP, PROF_FWD, PROF_BWD_REC, PROF_BWD_STATE, PROF_BWD_CHUNK, PROF_STEP, PROF_N };
+const char* const kProfNames[PROF_N] = {"prep", "fwd_recurrent", "bwd_recurrent",
+                                        "bwd_state", "bwd_chunk", "step"};
+struct ProfRec {
+  int kind;
+  hipEvent_t a, b;
+};
+std::mutex g_prof_mu;
+bool g_prof_on = false;
+std::vector<ProfRec> g_prof;        // recorded launches since enable
+std::vector<hipEvent_t> g_ev_pool;  // events available for reuse
+
+hipEvent_t take_event() {
+  if (!g_ev_pool.empty()) {
+    hipEvent_t e = g_ev_pool.back();
+    g_ev_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// Launch wrapper: runs `launch` between two events when timing is enabled.
+template <typename F>
+hipError_t timed(int kind, hipStream_t st, F launch) {
+  hipEvent_t a = nullptr, b = nullptr;
+  {
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    if (g_prof_on) {
+      a = take_event();
+      b = take_event();
+    }
+  }
+  if (a && b) (void)hipEventRecord(a, st);
+  hipError_t e = launch();
+  if (a && b) {
+    (void)hipEventRecord(b, st);
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    g_prof.push_back(ProfRec{kind, a, b});
+  }
+  return e;
+}
+
 }  // namespace
 
 extern "C" {
@@ -234,12 +285,14 @@ int tla_fwd(const tla_desc* d, const void* q, const void* k, const void* v, cons
   const tla::PrepBufs pb = prep_bufs(L, ws);
   hipError_t e;
   if (s.T > 0) {
-    e = tla::launch_prep(s, in, pb, st);
+    e = timed(PROF_PREP, st, [&] { return tla::launch_prep(s, in, pb, st); });
     if (e != hipSuccess) return device_fail(e, "prep kernel");
   }
   if (s.T > 0 || s_final) {
     tla::SavedBufs sv = saved_bufs(L, saved);
-    e = tla::launch_fwd(s, in, pb, o, s_final, saved ? &sv : nullptr, st);
+    e = timed(PROF_FWD, st, [&] {
+      return tla::launch_fwd(s, in, pb, o, s_final, saved ? &sv : nullptr, st);
+    });
     if (e != hipSuccess) return device_fail(e, "forward kernel");
   }
   return TLA_OK;
@@ -296,13 +349,16 @@ int tla_bwd(const tla_desc* d, const void* q, const void* k, const void* v, cons
                         (float*)(wb + L.bwd_dqs), (float*)(wb + L.bwd_dks),
                         (float*)(wb + L.bwd_dcoef), (float*)(wb + L.bwd_dgC)};
   const tla::SavedBufs sv = saved_bufs(L, saved);
-  hipError_t e = tla::launch_prep(s, in, pb, st);
+  hipError_t e = timed(PROF_PREP, st, [&] { return tla::launch_prep(s, in, pb, st); });
   if (e != hipSuccess) return device_fail(e, "prep kernel");
-  e = tla::launch_bwd_rec(s, in, dO, dS_final, pb, bb, ds0, st);
+  e = timed(PROF_BWD_REC, st,
+            [&] { return tla::launch_bwd_rec(s, in, dO, dS_final, pb, bb, ds0, st); });
   if (e != hipSuccess) return device_fail(e, "backward recurrent kernel");
-  e = tla::launch_bwd_state(s, in, dO, pb, sv, bb, st);
+  e = timed(PROF_BWD_STATE, st, [&] { return tla::launch_bwd_state(s, in, dO, pb, sv, bb, st); });
   if (e != hipSuccess) return device_fail(e, "backward state-gradient kernel");
-  e = tla::launch_bwd_chunk(s, in, dO, sv, bb, dq, dk, dv, dq2, dk2, dg, dbeta, st);
+  e = timed(PROF_BWD_CHUNK, st, [&] {
+    return tla::launch_bwd_chunk(s, in, dO, sv, bb, dq, dk, dv, dq2, dk2, dg, dbeta, st);
+  });
   if (e != hipSuccess) return device_fail(e, "backward chunk kernel");
   return TLA_OK;
 }
@@ -331,9 +387,42 @@ int tla_step(const tla_desc* d, const void* q, const void* k, const void* v, con
   if (overlap(outs[0], outs[1])) return fail(TLA_E_ALIAS, "state and o overlap");
   s.has_beta = beta != nullptr;
   tla::FwdIn in{q, k, v, q2, k2, g, beta, nullptr};
-  hipError_t e = tla::launch_step(s, in, state, o, (hipStream_t)stream);
+  hipError_t e = timed(PROF_STEP, (hipStream_t)stream,
+                       [&] { return tla::launch_step(s, in, state, o, (hipStream_t)stream); });
   if (e != hipSuccess) return device_fail(e, "step kernel");
   return TLA_OK;
 }
+
+int tla_prof_enable(int on) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  for (ProfRec& r : g_prof) {
+    g_ev_pool.push_back(r.a);
+    g_ev_pool.push_back(r.b);
+  }
+  g_prof.clear();
+  g_prof_on = on != 0;
+  return TLA_OK;
+}
+
+int tla_prof_read(double* total_ms, int* launches, int n) {
+  if (!total_ms || !launches || n < 6) return fail(TLA_E_NULL, "tla_prof_read needs 6 slots");
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  for (int i = 0; i < n; ++i) {
+    total_ms[i] = 0.0;
+    launches[i] = 0;
+  }
+  for (const ProfRec& r : g_prof) {
+    hipError_t e = hipEventSynchronize(r.b);
+    if (e != hipSuccess) return device_fail(e, "event synchronize");
+    float ms = 0.f;
+    e = hipEventElapsedTime(&ms, r.a, r.b);
+    if (e != hipSuccess) return device_fail(e, "event elapsed time");
+    total_ms[r.kind] += ms;
+    launches[r.kind] += 1;
+  }
+  return TLA_OK;
+}
+
+const char* tla_prof_name(int i) { return (i >= 0 && i < PROF_N) ? kProfNames[i] : ""; }
 
 }  // extern "C"
