@@ -76,8 +76,8 @@ template <int E> constexpr int bwd_waves() { return E >= 16 ? 8 : 4; }
 // ============================================================ reverse recurrence
 template <typename T, int KD, int C, int E, int NW>
 struct RecSmem {
-  static constexpr int KP = KD + 8;
-  static constexpr int CP = C + 8;
+  static constexpr int KP = KD + 4;
+  static constexpr int CP = C + 4;
   static constexpr int NT = C / 16;
   static constexpr int E4 = (E + 3) & ~3;
   static constexpr bool SPLIT = sizeof(T) == 2;
@@ -163,45 +163,45 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
       }
       if constexpr (Sm::STAGE_K) {
 #pragma unroll
-        for (int rr = 0; rr < 4; ++rr) bcopy8(&sm.K[4 * rb + rr][8 * cb], kv[rr]);
+        for (int rr = 0; rr < 4; ++rr) lds_put8(&sm.K[4 * rb + rr][8 * cb], kv[rr]);
       }
 #pragma unroll
-      for (int cc = 0; cc < 8; ++cc)
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr) {
-          sm.Kt[8 * cb + cc][4 * rb + rr] = kv[rr][cc];
-          sm.Qt[8 * cb + cc][4 * rb + rr] = qv[rr][cc];
-        }
+      for (int cc = 0; cc < 8; ++cc) {
+        lds_put4(&sm.Kt[8 * cb + cc][4 * rb], kv[0][cc], kv[1][cc], kv[2][cc], kv[3][cc]);
+        lds_put4(&sm.Qt[8 * cb + cc][4 * rb], qv[0][cc], qv[1][cc], qv[2][cc], qv[3][cc]);
+      }
     }
-    for (int idx = tid; idx < C * 4; idx += NTHR) {
-      const int r = idx >> 2, c4 = idx & 3;
-      const int t = t0 + r;
+    for (int idx = tid; idx < (C / 4) * 16; idx += NTHR) {  // 4 rows x 1 column per thread
+      const int rb = idx % (C / 4), col = idx / (C / 4);
       T x[4];
-      if (t < s.T) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) x[j] = dOg[(size_t)t * vrs + 4 * c4 + j];
-      } else {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) x[j] = T(0);
+      for (int rr = 0; rr < 4; ++rr) {
+        const int t = t0 + 4 * rb + rr;
+        x[rr] = (t < s.T) ? dOg[(size_t)t * vrs + col] : T(0);
       }
-#pragma unroll
-      for (int j = 0; j < 4; ++j) sm.dOt[4 * c4 + j][r] = x[j];
+      lds_put4(&sm.dOt[col][4 * rb], x[0], x[1], x[2], x[3]);
     }
     {
+      // M^T and Tu^T (hi / lo) from 4x4 blocks: 4 row loads, 4 column stores
       const float* Mg = p.M + ch * C * C;
       const float* Tg = p.Tu + ch * C * C;
-      for (int idx = tid; idx < C * C; idx += NTHR) {
-        const int r = idx / C, c = idx % C;  // writes M^T[c][r] = M[r][c]
-        const float m = Mg[idx];
-        const T mh = Elem<T>::from_f(m);
-        sm.MT[c][r] = mh;
-        if constexpr (Sm::SPLIT) sm.MTL[c][r] = Elem<T>::from_f(m - Elem<T>::to_f(mh));
-        if (s.variant == 1) {
-          const float tv = Tg[idx];
-          const T th = Elem<T>::from_f(tv);
-          sm.TuT[c][r] = th;
-          if constexpr (Sm::SPLIT) sm.TuTL[c][r] = Elem<T>::from_f(tv - Elem<T>::to_f(th));
+      auto put_t = [&](const float* src, T (*hi)[Sm::CP], T (*lo)[Sm::CP], int rb, int cb) {
+        f32x4 x[4];
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) x[rr] = *(const f32x4*)(src + (4 * rb + rr) * C + 4 * cb);
+#pragma unroll
+        for (int cc = 0; cc < 4; ++cc) {
+          const f32x4 col{x[0][cc], x[1][cc], x[2][cc], x[3][cc]};
+          F h, lw;
+          split_frag(col, h, lw);
+          *(F*)&hi[4 * cb + cc][4 * rb] = h;
+          if constexpr (Sm::SPLIT) *(F*)&lo[4 * cb + cc][4 * rb] = lw;
         }
+      };
+      for (int idx = tid; idx < (C / 4) * (C / 4); idx += NTHR) {
+        const int rb = idx % (C / 4), cb = idx / (C / 4);
+        put_t(Mg, sm.MT, sm.MTL, rb, cb);
+        if (s.variant == 1) put_t(Tg, sm.TuT, sm.TuTL, rb, cb);
       }
       const float* cg = p.coef + ch * 3 * E * C;
       float* cs = &sm.coef[0][0][0];
@@ -343,19 +343,26 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
 }
 
 // ===================================================== state-gradient contractions
-// One workgroup per (head, chunk); wave w owns the key columns [32 w, 32 w + 32)
-// (KD = 128) or a share of them.  A operands (dO, dW, U) come from LDS, the
-// chunk-start state and the chunk-end state gradient from their tiled stores.
+// One workgroup per (head, chunk); wave w owns the key columns [16 CTW w,
+// 16 CTW (w + 1)).  The chunk's dO, dW and U rows (A operands; dW and U as
+// bf16 hi + lo pairs) are staged in LDS once; the chunk-start state S_e and
+// the chunk-end state gradient dS'_e stream from their tiled stores as B
+// fragments, one slice ahead of the MFMAs.
 template <typename T, int KD, int C, int E>
 struct StateSmem {
-  static constexpr int NT = C / 16;
-  alignas(16) T dO[C][16 + 4];           // staged per 16-column block of V
-  alignas(16) T dWh[C][16 + 4], dWl[C][16 + 4];
-  alignas(16) T Uh[C][16 + 4], Ul[C][16 + 4];
-  alignas(16) float Qt[KD][C + 4];       // Q^T and K^T in fp32 for the row sums
-  alignas(16) float Kt[KD][C + 4];
+  static constexpr int VP = 128 + 8;       // V <= 128
+  static constexpr bool SPLIT = sizeof(T) == 2;
+  // fp32 instances stage one 16-column block of V at a time (LDS budget)
+  static constexpr bool STAGE_ALL = sizeof(T) == 2;
+  static constexpr int VS = STAGE_ALL ? VP : 16 + 4;
+  alignas(16) T dO[C][VS];
+  alignas(16) T dWh[C][VS], Uh[C][VS];
+  alignas(16) T dWl[SPLIT ? C : 1][VS], Ul[SPLIT ? C : 1][VS];
+  alignas(16) T Qt[KD][C + 8];  // Q^T, K^T for the row sums
+  alignas(16) T Kt[KD][C + 8];
   alignas(16) float coef[3][E][C];
-  alignas(16) float red[4][3][E][C];     // per-wave row-sum partials
+  alignas(16) float red[2][4][3][C];  // per-wave row-sum partials, by slice parity
+  alignas(16) float dcf[3][E][C];
   alignas(16) float gred[4][E];
 };
 
@@ -366,14 +373,16 @@ __global__ __launch_bounds__(256) void k_bwd_state(Shape s, FwdIn in, const void
   constexpr int KT = KD / 16;
   constexpr int CTW = (KT + 3) / 4;      // key column tiles per wave
   constexpr int E4 = (E + 3) & ~3;
+  constexpr int VBMAX = 8;               // V <= 128
   typedef typename Elem<T>::frag F;
   typedef StateSmem<T, KD, C, E> Sm;
-  constexpr bool SPLIT = sizeof(T) == 2;
+  constexpr bool SPLIT = Sm::SPLIT;
   extern __shared__ __align__(16) unsigned char smem_raw[];
   Sm& sm = *reinterpret_cast<Sm*>(smem_raw);
 
   const int tid = threadIdx.x, w = wave_id(), l = lane_id(), g = l >> 4, n = l & 15;
   const int V = s.V;
+  const int VB = V / 16;
   const int ch = blockIdx.x;
   const int head = ch / s.Nc, ci = ch % s.Nc;
   const int b = head / s.H, h = head % s.H;
@@ -382,19 +391,69 @@ __global__ __launch_bounds__(256) void k_bwd_state(Shape s, FwdIn in, const void
   const T* Kg = (const T*)in.k + (((size_t)b * s.T) * s.H + h) * KD;
   const T* Qg = (const T*)in.q + (((size_t)b * s.T) * s.H + h) * KD;
   const T* dOg = (const T*)dOv + (((size_t)b * s.T) * s.H + h) * (size_t)V;
+  const float* dWg = bb.dW + (size_t)ch * C * V;
+  const float* Ug = sv.U + (size_t)ch * C * V;
+
+  // stage A-operand columns [c0, c0 + ncols) into LDS columns [0, ncols)
+  auto stage = [&](int c0, int ncols) {
+    const int n4 = ncols / 4;
+    for (int idx = tid; idx < C * n4; idx += 256) {
+      const int r = idx / n4, c4 = idx % n4;
+      const int t = t0 + r;
+      const int col = c0 + 4 * c4;
+      T x[4];
+      if (t < s.T) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) x[j] = dOg[(size_t)t * vrs + col + j];
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) x[j] = T(0);
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) sm.dO[r][4 * c4 + j] = x[j];
+      F hi, lo;
+      split_frag(*(const f32x4*)(dWg + (size_t)r * V + col), hi, lo);
+      *(F*)&sm.dWh[r][4 * c4] = hi;
+      if constexpr (SPLIT) *(F*)&sm.dWl[r][4 * c4] = lo;
+      split_frag(*(const f32x4*)(Ug + (size_t)r * V + col), hi, lo);
+      *(F*)&sm.Uh[r][4 * c4] = hi;
+      if constexpr (SPLIT) *(F*)&sm.Ul[r][4 * c4] = lo;
+    }
+  };
 
   for (int idx = tid; idx < C * KD; idx += 256) {
     const int r = idx / KD, c = idx % KD;
     const int t = t0 + r;
-    sm.Qt[c][r] = (t < s.T) ? ld_f(Qg + (size_t)t * krs + c) : 0.f;
-    sm.Kt[c][r] = (t < s.T) ? ld_f(Kg + (size_t)t * krs + c) : 0.f;
+    sm.Qt[c][r] = (t < s.T) ? Qg[(size_t)t * krs + c] : T(0);
+    sm.Kt[c][r] = (t < s.T) ? Kg[(size_t)t * krs + c] : T(0);
   }
   {
     const float* cg = p.coef + (size_t)ch * 3 * E * C;
     for (int idx = tid; idx < 3 * E * C; idx += 256) (&sm.coef[0][0][0])[idx] = cg[idx];
   }
+  if constexpr (Sm::STAGE_ALL) stage(0, V);
 
-  // accumulators: dq_s, dk_s tiles (rt, ct) for this wave's key columns
+  // B fragments of S_e^T and dS'_e^T for this wave's key columns, all V blocks
+  const T* Sck = (const T*)sv.Sck;
+  const T* dSck = (const T*)bb.dSck;
+  F sbuf[CTW][VBMAX], dbuf[CTW][VBMAX];
+  auto load_slice = [&](int e) {
+#pragma unroll
+    for (int c = 0; c < CTW; ++c) {
+      const int ct = w * CTW + c;
+#pragma unroll
+      for (int vb = 0; vb < VBMAX; ++vb) {
+        if (ct < KT && vb < VB) {
+          const size_t tile = ((size_t)ch * E + e) * (V / 16) + vb;
+          sbuf[c][vb] = ld_frag(Sck + tile * KD * 16 + (16 * ct + n) * 16 + 4 * g);
+          dbuf[c][vb] = ld_frag(dSck + tile * KD * 16 + (16 * ct + n) * 16 + 4 * g);
+        }
+      }
+    }
+  };
+  load_slice(0);
+  __syncthreads();
+
   f32x4 dq[NT][CTW], dk[NT][CTW];
 #pragma unroll
   for (int rt = 0; rt < NT; ++rt)
@@ -403,11 +462,19 @@ __global__ __launch_bounds__(256) void k_bwd_state(Shape s, FwdIn in, const void
       dq[rt][c] = zero4();
       dk[rt][c] = zero4();
     }
-  float rsum_db[NT][4], rsum_da[NT][4], rsum_dc[NT][4];
-  const T* Sck = (const T*)sv.Sck;
-  const T* dSck = (const T*)bb.dSck;
 
   for (int e = 0; e < E; ++e) {
+    F scur[CTW][VBMAX], dcur[CTW][VBMAX];
+#pragma unroll
+    for (int c = 0; c < CTW; ++c)
+#pragma unroll
+      for (int vb = 0; vb < VBMAX; ++vb) {
+        scur[c][vb] = sbuf[c][vb];
+        dcur[c][vb] = dbuf[c][vb];
+      }
+    if (e + 1 < E) load_slice(e + 1);  // in flight during this slice
+
+    float gpart = 0.f;
     f32x4 X[NT][CTW], Y[NT][CTW], Vp[NT][CTW];
 #pragma unroll
     for (int rt = 0; rt < NT; ++rt)
@@ -417,107 +484,93 @@ __global__ __launch_bounds__(256) void k_bwd_state(Shape s, FwdIn in, const void
         Y[rt][c] = zero4();
         Vp[rt][c] = zero4();
       }
-    float gpart = 0.f;
-    for (int vb = 0; vb < V / 16; ++vb) {
-      __syncthreads();
-      // stage the 16-column block vb of dO, dW, U for all chunk rows
-      for (int idx = tid; idx < C * 4; idx += 256) {
-        const int r = idx >> 2, c4 = idx & 3;
-        const int t = t0 + r;
-        const int col = 16 * vb + 4 * c4;
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-          sm.dO[r][4 * c4 + j] = (t < s.T) ? dOg[(size_t)t * vrs + col + j] : T(0);
-        const f32x4 dw = *(const f32x4*)(bb.dW + (size_t)ch * C * V + (size_t)r * V + col);
-        const f32x4 u = *(const f32x4*)(sv.U + (size_t)ch * C * V + (size_t)r * V + col);
-        F hi, lo;
-        split_frag(dw, hi, lo);
-        *(F*)&sm.dWh[r][4 * c4] = hi;
-        if constexpr (SPLIT) *(F*)&sm.dWl[r][4 * c4] = lo;
-        split_frag(u, hi, lo);
-        *(F*)&sm.Uh[r][4 * c4] = hi;
-        if constexpr (SPLIT) *(F*)&sm.Ul[r][4 * c4] = lo;
+    for (int vb = 0; vb < VBMAX; ++vb) {
+      if (vb >= VB) continue;
+      int col = 16 * vb;
+      if constexpr (!Sm::STAGE_ALL) {
+        __syncthreads();
+        stage(16 * vb, 16);
+        __syncthreads();
+        col = 0;
       }
-      __syncthreads();
-      const size_t tile = ((size_t)ch * E + e) * (V / 16) + vb;
 #pragma unroll
       for (int c = 0; c < CTW; ++c) {
-        const int ct = w * CTW + c;
-        if (ct >= KT) continue;
-        // B fragments: S_e^T and dS'_e^T for key columns 16 ct + n, values 4 g + j
-        const F sb = ld_frag(Sck + tile * KD * 16 + (16 * ct + n) * 16 + 4 * g);
-        const F db = ld_frag(dSck + tile * KD * 16 + (16 * ct + n) * 16 + 4 * g);
-        {  // <S_e, dS'_e> over this block
-          const f32x4 a = frag_to_f(sb), d = frag_to_f(db);
-          gpart += a[0] * d[0] + a[1] * d[1] + a[2] * d[2] + a[3] * d[3];
+        if (w * CTW + c >= KT) continue;
+        const f32x4 a = frag_to_f(scur[c][vb]), d = frag_to_f(dcur[c][vb]);
+        gpart += a[0] * d[0] + a[1] * d[1] + a[2] * d[2] + a[3] * d[3];
+      }
+#pragma unroll
+      for (int rt = 0; rt < NT; ++rt) {
+        const int r = 16 * rt + n;
+        const F ao = ld_frag(&sm.dO[r][col + 4 * g]);
+        const F awh = ld_frag(&sm.dWh[r][col + 4 * g]);
+        const F auh = ld_frag(&sm.Uh[r][col + 4 * g]);
+        F awl, aul;
+        if constexpr (SPLIT) {
+          awl = ld_frag(&sm.dWl[r][col + 4 * g]);
+          aul = ld_frag(&sm.Ul[r][col + 4 * g]);
         }
 #pragma unroll
-        for (int rt = 0; rt < NT; ++rt) {
-          const int r = 16 * rt + n;
-          mma16(X[rt][c], ld_frag(&sm.dO[r][4 * g]), sb);
-          mma16(Y[rt][c], ld_frag(&sm.dWh[r][4 * g]), sb);
-          mma16(Vp[rt][c], ld_frag(&sm.Uh[r][4 * g]), db);
+        for (int c = 0; c < CTW; ++c) {
+          if (w * CTW + c >= KT) continue;
+          mma16(X[rt][c], ao, scur[c][vb]);
+          mma16(Y[rt][c], awh, scur[c][vb]);
+          mma16(Vp[rt][c], auh, dcur[c][vb]);
           if constexpr (SPLIT) {
-            mma16(Y[rt][c], ld_frag(&sm.dWl[r][4 * g]), sb);
-            mma16(Vp[rt][c], ld_frag(&sm.Ul[r][4 * g]), db);
+            mma16(Y[rt][c], awl, scur[c][vb]);
+            mma16(Vp[rt][c], aul, dcur[c][vb]);
           }
         }
       }
     }
-    // fold slice e into dq_s, dk_s and the row sums
+    // fold slice e into dq_s, dk_s; per-row sums of Q o X, K o Y, K o V'
+    const int par = e & 1;
 #pragma unroll
     for (int rt = 0; rt < NT; ++rt) {
       const f32x4 ca = *(const f32x4*)&sm.coef[0][e][16 * rt + 4 * g];
       const f32x4 cb = *(const f32x4*)&sm.coef[1][e][16 * rt + 4 * g];
       const f32x4 cc = *(const f32x4*)&sm.coef[2][e][16 * rt + 4 * g];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        rsum_db[rt][j] = 0.f;
-        rsum_da[rt][j] = 0.f;
-        rsum_dc[rt][j] = 0.f;
-      }
+      f32x4 rdb = zero4(), rda = zero4(), rdc = zero4();
 #pragma unroll
       for (int c = 0; c < CTW; ++c) {
         const int ct = w * CTW + c;
         if (ct >= KT) continue;
         dq[rt][c] += cb * X[rt][c];
         dk[rt][c] += ca * Y[rt][c] + cc * Vp[rt][c];
-        const f32x4 qv = *(const f32x4*)&sm.Qt[16 * ct + n][16 * rt + 4 * g];
-        const f32x4 kv = *(const f32x4*)&sm.Kt[16 * ct + n][16 * rt + 4 * g];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          rsum_db[rt][j] += qv[j] * X[rt][c][j];
-          rsum_da[rt][j] += kv[j] * Y[rt][c][j];
-          rsum_dc[rt][j] += kv[j] * Vp[rt][c][j];
-        }
+        const f32x4 qv = ld4_f(&sm.Qt[16 * ct + n][16 * rt + 4 * g]);
+        const f32x4 kv = ld4_f(&sm.Kt[16 * ct + n][16 * rt + 4 * g]);
+        rdb += qv * X[rt][c];
+        rda += kv * Y[rt][c];
+        rdc += kv * Vp[rt][c];
       }
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const float x0 = group16_sum(rsum_db[rt][j]);
-        const float x1 = group16_sum(rsum_da[rt][j]);
-        const float x2 = group16_sum(rsum_dc[rt][j]);
+        const float x0 = group16_sum(rdb[j]);
+        const float x1 = group16_sum(rda[j]);
+        const float x2 = group16_sum(rdc[j]);
         if (n == 0) {
-          sm.red[w][1][e][16 * rt + 4 * g + j] = x0;
-          sm.red[w][0][e][16 * rt + 4 * g + j] = x1;
-          sm.red[w][2][e][16 * rt + 4 * g + j] = x2;
+          sm.red[par][w][0][16 * rt + 4 * g + j] = x1;
+          sm.red[par][w][1][16 * rt + 4 * g + j] = x0;
+          sm.red[par][w][2][16 * rt + 4 * g + j] = x2;
         }
       }
     }
     gpart = wave_sum(gpart);
     if (l == 0) sm.gred[w][e] = gpart;
+    __syncthreads();
+    for (int idx = tid; idx < 3 * C; idx += 256) {  // fixed-order sum over the waves
+      const int kind = idx / C, r = idx % C;
+      sm.dcf[kind][e][r] = ((sm.red[par][0][kind][r] + sm.red[par][1][kind][r]) +
+                            sm.red[par][2][kind][r]) + sm.red[par][3][kind][r];
+    }
   }
   __syncthreads();
-  // fixed-order sums over the four waves
-  for (int idx = tid; idx < 3 * E * C; idx += 256) {
-    const int kind = idx / (E * C), rem = idx % (E * C);
-    const int e = rem / C, r = rem % C;
-    bb.dcoef[(size_t)ch * 3 * E * C + idx] =
-        ((sm.red[0][kind][e][r] + sm.red[1][kind][e][r]) + sm.red[2][kind][e][r]) + sm.red[3][kind][e][r];
-  }
+  for (int idx = tid; idx < 3 * E * C; idx += 256)
+    bb.dcoef[(size_t)ch * 3 * E * C + idx] = (&sm.dcf[0][0][0])[idx];
   if (tid < E4)
     bb.dgC[(size_t)ch * E4 + tid] =
         (tid < E) ? ((sm.gred[0][tid] + sm.gred[1][tid]) + sm.gred[2][tid]) + sm.gred[3][tid] : 0.f;
-  // dq_s, dk_s
 #pragma unroll
   for (int rt = 0; rt < NT; ++rt)
 #pragma unroll
@@ -535,21 +588,48 @@ __global__ __launch_bounds__(256) void k_bwd_state(Shape s, FwdIn in, const void
 }
 
 // ========================================================= per-chunk gradients
-template <int C, int E>
+// fp32 x fp32 products on MFMA: bf16 operands split into hi + lo (three
+// products), fp32 operands on the fp32 MFMA.
+__device__ __forceinline__ void mma_ff(f32x4& acc, f32x4 a, f32x4 b, bf16_t*) {
+  bf16x4 ah, al, bh, bl;
+  split_frag(a, ah, al);
+  split_frag(b, bh, bl);
+  mma16(acc, ah, bh);
+  mma16(acc, ah, bl);
+  mma16(acc, al, bh);
+}
+__device__ __forceinline__ void mma_ff(f32x4& acc, f32x4 a, f32x4 b, float*) { mma16(acc, a, b); }
+// fp32 A times an exactly representable B (an input)
+__device__ __forceinline__ void mma_fx(f32x4& acc, f32x4 a, f32x4 b, bf16_t*) {
+  bf16x4 ah, al;
+  split_frag(a, ah, al);
+  const bf16x4 bb = cvt_frag<bf16_t>(b);
+  mma16(acc, ah, bb);
+  mma16(acc, al, bb);
+}
+__device__ __forceinline__ void mma_fx(f32x4& acc, f32x4 a, f32x4 b, float*) { mma16(acc, a, b); }
+
+template <typename T, int KD, int C, int E>
 struct ChunkSmem {
   static constexpr int CP = C + 1;
-  float Aqk[C][CP];               // A_qk, then dR' = dM o A_qk
-  float Akk[C][CP];               // A_kk, then dR = dA_hat o A_kk
-  float R[C][CP];                 // R (strictly lower)
-  float Ninv[C][CP];              // (I + L)^{-1}, then dL o A_hat
-  float dM[C][CP];                // dM, then dA_qk
-  float dT[C][CP];                // dTu, then P = N^{-T} dTu, then dA_kk
-  float q2[C][E], k2[C][E], gam[C][E], gtail[C][E];
+  static constexpr int KP = KD + 8;
+  static constexpr int NT = C / 16;
+  // bf16 instances keep the chunk's Q and K rows in LDS; fp32 ones read them
+  // from global memory so that the plan fits 160 KiB
+  static constexpr bool STAGE_QK = sizeof(T) == 2;
+  alignas(16) T sQ[STAGE_QK ? C : 1][KP];
+  alignas(16) T sK[STAGE_QK ? C : 1][KP];
+  float Aqk[C][CP];   // A_qk, then dR' = dM o A_qk
+  float Akk[C][CP];   // A_kk, then dR = dA_hat o A_kk
+  float R[C][CP];     // R (strictly lower)
+  float X1[C][CP];    // (I + L)^{-1}, then dL o A_hat
+  float dM[C][CP];    // dM = dO U^T (lower), then dA_qk = dM o R'
+  float dT[C][CP];    // dTu = dU X^T, then P = N^{-T} dTu, then dA_kk = dA_hat o R
+  float Y[NT > 1 ? NT - 1 : 1][16][17];
+  float q2[C][E], k2[C][E];
   double G[C][E];
   float dG[C][E];
   float beta[C], dbeta[C];
-  float dcf[3][E][C];
-  float dgC[E];
 };
 
 template <typename T, int KD, int C, int E>
@@ -558,12 +638,17 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
                                                    void* dvv, void* dq2v, void* dk2v, float* dg,
                                                    float* dbeta) {
   constexpr int NT = C / 16;
+  constexpr int KT = KD / 16;
   constexpr int E4 = (E + 3) & ~3;
-  typedef ChunkSmem<C, E> Sm;
+  constexpr int VBMAX = 8;  // V <= 128
+  typedef typename Elem<T>::frag F;
+  typedef ChunkSmem<T, KD, C, E> Sm;
   extern __shared__ __align__(16) unsigned char smem_raw[];
   Sm& sm = *reinterpret_cast<Sm*>(smem_raw);
+  T* tag = nullptr;  // selects the MFMA flavour of mma_ff / mma_fx
   const int tid = threadIdx.x, w = wave_id(), l = lane_id(), g = l >> 4, n = l & 15;
   const int V = s.V;
+  const int VB = V / 16;
   const int ch = blockIdx.x;
   const int head = ch / s.Nc, ci = ch % s.Nc;
   const int b = head / s.H, h = head % s.H;
@@ -573,11 +658,14 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
   const T* Qg = (const T*)in.q + (((size_t)b * s.T) * s.H + h) * KD;
   const T* Vg = (const T*)in.v + (((size_t)b * s.T) * s.H + h) * (size_t)V;
   const T* dOg = (const T*)dOv + (((size_t)b * s.T) * s.H + h) * (size_t)V;
+  const float* Ug = sv.U + (size_t)ch * C * V;
+  const float* Xg = sv.X + (size_t)ch * C * V;
+  const float* dUg = bb.dU + (size_t)ch * C * V;
   const size_t eoff = (((size_t)b * s.T) * s.H + h) * E;
   const size_t erow = (size_t)s.H * E;
-  const bool gdn = s.variant == 1;  // the C x C work below runs on fp32 MFMA
+  const bool gdn = s.variant == 1;
 
-  // ---- per-position vectors
+  // ---- phase 0: per-position vectors, Q and K rows
   for (int idx = tid; idx < C * E; idx += 256) {
     const int r = idx / E, e = idx % E;
     const int t = t0 + r;
@@ -590,9 +678,19 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
     const int t = t0 + r;
     sm.beta[r] = (t < s.T) ? (in.beta ? in.beta[((size_t)b * s.T + t) * s.H + h] : 1.f) : 0.f;
   }
-  for (int idx = tid; idx < 3 * E * C; idx += 256)
-    (&sm.dcf[0][0][0])[idx] = bb.dcoef[(size_t)ch * 3 * E * C + idx];
-  if (tid < E) sm.dgC[tid] = bb.dgC[(size_t)ch * E4 + tid];
+  if constexpr (Sm::STAGE_QK) {
+    for (int idx = tid; idx < C * KD / 8; idx += 256) {
+      const int r = idx / (KD / 8), c8 = idx % (KD / 8);
+      const int t = t0 + r;
+      uint4 qv = make_uint4(0, 0, 0, 0), kv = make_uint4(0, 0, 0, 0);
+      if (t < s.T) {
+        qv = *(const uint4*)(Qg + (size_t)t * krs + 8 * c8);
+        kv = *(const uint4*)(Kg + (size_t)t * krs + 8 * c8);
+      }
+      *(uint4*)&sm.sQ[r][8 * c8] = qv;
+      *(uint4*)&sm.sK[r][8 * c8] = kv;
+    }
+  }
   __syncthreads();
   if (tid < E) {
     double acc = 0.0;
@@ -601,155 +699,172 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
       sm.G[r][tid] = acc;
     }
   }
-  __syncthreads();
-  for (int idx = tid; idx < C * E; idx += 256) {
-    const int r = idx / E, e = idx % E;
-    const double G = sm.G[r][e], GC = sm.G[C - 1][e];
-    sm.gam[r][e] = __expf((float)G);
-    sm.gtail[r][e] = __expf((float)(GC - G));
-  }
+  // fragment accessors for Q and K rows (A or B operand over the key axis)
+  auto qrow = [&](int r, int kb) -> F {
+    if constexpr (Sm::STAGE_QK) return ld_frag(&sm.sQ[r][16 * kb + 4 * g]);
+    else return (t0 + r < s.T) ? ld_frag(Qg + (size_t)(t0 + r) * krs + 16 * kb + 4 * g)
+                               : cvt_frag<T>(zero4());
+  };
+  auto krow = [&](int r, int kb) -> F {
+    if constexpr (Sm::STAGE_QK) return ld_frag(&sm.sK[r][16 * kb + 4 * g]);
+    else return (t0 + r < s.T) ? ld_frag(Kg + (size_t)(t0 + r) * krs + 16 * kb + 4 * g)
+                               : cvt_frag<T>(zero4());
+  };
 
-  // ---- A_qk = Q K^T, A_kk = K K^T; dM = dO U^T; dTu = dU X^T  (full C x C tiles)
+  // ---- phase 1: A_qk, A_kk, dM = dO U^T (lower tiles), dTu = dU X^T (all tiles)
   for (int tile = w; tile < NT * NT; tile += 4) {
     const int rt = tile / NT, st = tile % NT;
     const int r = 16 * rt + n, c = 16 * st + n;
-    const bool rok = t0 + r < s.T, cok = t0 + c < s.T;
+    const bool lower = st <= rt;
+    const bool rok = t0 + r < s.T;
     f32x4 aq = zero4(), ak = zero4(), dm = zero4(), dt = zero4();
-    if (st <= rt) {
-      const T* qr = Qg + (size_t)(rok ? t0 + r : 0) * krs;
-      const T* kr = Kg + (size_t)(rok ? t0 + r : 0) * krs;
-      const T* kc = Kg + (size_t)(cok ? t0 + c : 0) * krs;
-      for (int kb = 0; kb < KD / 16; ++kb) {
-        const f32x4 bq = cok ? ld4_f(kc + 16 * kb + 4 * g) : zero4();
-        const f32x4 a1 = rok ? ld4_f(qr + 16 * kb + 4 * g) : zero4();
-        const f32x4 a2 = rok ? ld4_f(kr + 16 * kb + 4 * g) : zero4();
-        mma16(aq, a1, bq);
-        mma16(ak, a2, bq);
+    if (lower) {
+      bmma_k<KD>(aq, [&](int kb) { return qrow(r, kb); }, [&](int kb) { return krow(c, kb); });
+      bmma_k<KD>(ak, [&](int kb) { return krow(r, kb); }, [&](int kb) { return krow(c, kb); });
+      f32x4 da[VBMAX], ub[VBMAX];
+#pragma unroll
+      for (int kb = 0; kb < VBMAX; ++kb) {
+        if (kb < VB) {
+          da[kb] = rok ? ld4_f(dOg + (size_t)(t0 + r) * vrs + 16 * kb + 4 * g) : zero4();
+          ub[kb] = *(const f32x4*)(Ug + (size_t)c * V + 16 * kb + 4 * g);
+        }
       }
-      const T* dor = dOg + (size_t)(rok ? t0 + r : 0) * vrs;
-      const float* ur = sv.U + (size_t)ch * C * V + (size_t)c * V;
-      const float* dur = bb.dU + (size_t)ch * C * V + (size_t)r * V;
-      const float* xr = sv.X + (size_t)ch * C * V + (size_t)c * V;
-      for (int kb = 0; kb < V / 16; ++kb) {
-        const f32x4 a1 = rok ? ld4_f(dor + 16 * kb + 4 * g) : zero4();
-        mma16(dm, a1, *(const f32x4*)(ur + 16 * kb + 4 * g));
-        if (gdn) mma16(dt, *(const f32x4*)(dur + 16 * kb + 4 * g), *(const f32x4*)(xr + 16 * kb + 4 * g));
+#pragma unroll
+      for (int kb = 0; kb < VBMAX; ++kb)
+        if (kb < VB) mma_fx(dm, ub[kb], da[kb], tag);  // (U B-frag) x exact dO: swap below
+    }
+    if (gdn) {
+      f32x4 xa[VBMAX], xb[VBMAX];
+#pragma unroll
+      for (int kb = 0; kb < VBMAX; ++kb) {
+        if (kb < VB) {
+          xa[kb] = *(const f32x4*)(dUg + (size_t)r * V + 16 * kb + 4 * g);
+          xb[kb] = *(const f32x4*)(Xg + (size_t)c * V + 16 * kb + 4 * g);
+        }
       }
+#pragma unroll
+      for (int kb = 0; kb < VBMAX; ++kb)
+        if (kb < VB) mma_ff(dt, xa[kb], xb[kb], tag);
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int rr = 16 * rt + 4 * g + j, cc = 16 * st + n;
       sm.Aqk[rr][cc] = aq[j];
       sm.Akk[rr][cc] = ak[j];
-      sm.dM[rr][cc] = (cc <= rr) ? dm[j] : 0.f;
       sm.dT[rr][cc] = dt[j];
-    }
-  }
-  // dTu is needed in full (upper part too): the tiles above the diagonal
-  if (gdn) {
-    for (int tile = w; tile < NT * NT; tile += 4) {
-      const int rt = tile / NT, st = tile % NT;
-      if (st <= rt) continue;
-      const int r = 16 * rt + n, c = 16 * st + n;
-      f32x4 dt = zero4();
-      const float* dur = bb.dU + (size_t)ch * C * V + (size_t)r * V;
-      const float* xr = sv.X + (size_t)ch * C * V + (size_t)c * V;
-      for (int kb = 0; kb < V / 16; ++kb)
-        mma16(dt, *(const f32x4*)(dur + 16 * kb + 4 * g), *(const f32x4*)(xr + 16 * kb + 4 * g));
-#pragma unroll
-      for (int j = 0; j < 4; ++j) sm.dT[16 * rt + 4 * g + j][16 * st + n] = dt[j];
+      // dm was formed with U (split) as the A operand and dO as the B
+      // operand, so it holds (U dO^T) = dM^T: element (4g+j, n) of the tile is
+      // dM[16 rt + n][16 st + 4 g + j]; keep the lower triangle incl. diagonal
+      const int sidx = 16 * st + 4 * g + j, ridx = 16 * rt + n;
+      if (lower) sm.dM[ridx][sidx] = (sidx <= ridx) ? dm[j] : 0.f;
+      else sm.dM[ridx][sidx] = 0.f;
     }
   }
   __syncthreads();
 
-  // ---- R', R element by element; dA_qk = dM o R', dR' = dM o A_qk
+  // ---- R' and R element by element; dR' = dM o A_qk, dA_qk = dM o R'
   for (int idx = tid; idx < C * C; idx += 256) {
     const int r = idx / C, c = idx % C;
     float rq = 0.f, rk = 0.f;
     if (c <= r) {
 #pragma unroll
       for (int e = 0; e < E; ++e) {
-        const float d = __expf((float)(sm.G[r][e] - sm.G[c][e]));
+        const float d = exp_nonpos((float)(sm.G[r][e] - sm.G[c][e]));
         rq += sm.q2[r][e] * sm.k2[c][e] * d;
         rk += sm.k2[r][e] * sm.k2[c][e] * d;
       }
     }
     sm.R[r][c] = (c < r) ? rk : 0.f;
     const float dm = sm.dM[r][c];
-    sm.Aqk[r][c] = dm * sm.Aqk[r][c];  // dR'
-    sm.dM[r][c] = dm * rq;             // dA_qk
+    sm.Aqk[r][c] = dm * sm.Aqk[r][c];
+    sm.dM[r][c] = dm * rq;
   }
   __syncthreads();
 
   if (gdn) {
-    // N^{-1} by forward substitution, one column per thread
+    // ---- (I + L)^{-1} with L = diag(beta)(A_kk o R), strictly lower
+    unit_lower_inverse<C, 256>(
+        [&](int r, int c) { return sm.beta[r] * sm.Akk[r][c] * sm.R[r][c]; }, &sm.X1[0][0],
+        Sm::CP, &sm.Y[0][0][0]);
+    // ---- P = N^{-T} dTu on MFMA (fp32 operands); N^{-T} is upper triangular
+    f32x4 pt[(NT * NT + 3) / 4];
+#pragma unroll
+    for (int i = 0; i < (NT * NT + 3) / 4; ++i) {
+      const int tile = w + 4 * i;
+      f32x4 acc = zero4();
+      if (tile < NT * NT) {
+        const int rt = tile / NT, ct = tile % NT;
+        for (int kb = rt; kb < NT; ++kb) {
+          f32x4 a, bv;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            a[j] = sm.X1[16 * kb + 4 * g + j][16 * rt + n];  // (N^{-1})^T[r][k]
+            bv[j] = sm.dT[16 * kb + 4 * g + j][16 * ct + n];
+          }
+          mma_ff(acc, a, bv, tag);
+        }
+      }
+      pt[i] = acc;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < (NT * NT + 3) / 4; ++i) {
+      const int tile = w + 4 * i;
+      if (tile < NT * NT) {
+        const int rt = tile / NT, ct = tile % NT;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) sm.dT[16 * rt + 4 * g + j][16 * ct + n] = pt[i][j];
+      }
+    }
+    __syncthreads();
+    if (tid < C) sm.dbeta[tid] = sm.dT[tid][tid];  // diag(N^{-T} dTu)
+    // ---- dL = tril(-P Tu^T, -1) with Tu = N^{-1} diag(beta)
+#pragma unroll
+    for (int i = 0; i < (NT * NT + 3) / 4; ++i) {
+      const int tile = w + 4 * i;
+      f32x4 acc = zero4();
+      if (tile < NT * NT) {
+        const int rt = tile / NT, st = tile % NT;
+        if (st <= rt) {
+          for (int kb = 0; kb <= st; ++kb) {
+            f32x4 a, bv;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const int k = 16 * kb + 4 * g + j;
+              a[j] = sm.dT[16 * rt + n][k];
+              bv[j] = sm.X1[16 * st + n][k] * sm.beta[k];
+            }
+            mma_ff(acc, a, bv, tag);
+          }
+        }
+      }
+      pt[i] = -acc;
+    }
+    __syncthreads();
+    // the products above used P rows as the A operand and (N^{-1} diag beta)
+    // rows as the B operand: element (4g+j, n) of tile (rt, st) is
+    // dN[16 rt + 4 g + j][16 st + n]
+#pragma unroll
+    for (int i = 0; i < (NT * NT + 3) / 4; ++i) {
+      const int tile = w + 4 * i;
+      if (tile < NT * NT) {
+        const int rt = tile / NT, st = tile % NT;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int r = 16 * rt + 4 * g + j, c = 16 * st + n;
+          const float dl = (c < r) ? pt[i][j] : 0.f;
+          const float akk = sm.Akk[r][c], rr = sm.R[r][c];
+          const float dah = sm.beta[r] * dl;
+          sm.Akk[r][c] = dah * akk;  // dR
+          sm.dT[r][c] = dah * rr;    // dA_kk
+          sm.X1[r][c] = dl * akk * rr;  // dL o A_hat
+        }
+      }
+    }
+    __syncthreads();
     if (tid < C) {
-      const int c = tid;
-      float x[C];
-#pragma unroll
-      for (int r = 0; r < C; ++r) {
-        float acc = 0.f;
-#pragma unroll
-        for (int j = 0; j < r; ++j) acc += (sm.beta[r] * sm.Akk[r][j] * sm.R[r][j]) * x[j];
-        x[r] = (r < c) ? 0.f : ((r == c) ? 1.f : -acc);
-      }
-#pragma unroll
-      for (int r = 0; r < C; ++r) sm.Ninv[r][c] = x[r];
-    }
-    __syncthreads();
-    // P = N^{-T} dTu: P[r][c] = sum_k Ninv[k][r] dT[k][c]
-    float pv[(C * C + 255) / 256];
-#pragma unroll
-    for (int i = 0; i < (C * C + 255) / 256; ++i) {
-      const int idx = tid + 256 * i;
       float acc = 0.f;
-      if (idx < C * C) {
-        const int r = idx / C, c = idx % C;
-        for (int k = r; k < C; ++k) acc += sm.Ninv[k][r] * sm.dT[k][c];
-      }
-      pv[i] = acc;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int i = 0; i < (C * C + 255) / 256; ++i) {
-      const int idx = tid + 256 * i;
-      if (idx < C * C) sm.dT[idx / C][idx % C] = pv[i];
-    }
-    __syncthreads();
-    // dbeta_r = P_rr + sum_{s<r} dL_rs A_hat_rs, with dN = -P Tu^T, Tu = Ninv diag(beta)
-    //   dN[r][s] = -sum_k P[r][k] Ninv[s][k] beta[k]   (k <= s)
-    float dl[(C * C + 255) / 256];
-#pragma unroll
-    for (int i = 0; i < (C * C + 255) / 256; ++i) {
-      const int idx = tid + 256 * i;
-      float acc = 0.f;
-      if (idx < C * C) {
-        const int r = idx / C, c = idx % C;
-        if (c < r)
-          for (int k = 0; k <= c; ++k) acc -= sm.dT[r][k] * sm.Ninv[c][k] * sm.beta[k];
-      }
-      dl[i] = acc;
-    }
-    if (tid < C) sm.dbeta[tid] = sm.dT[tid][tid];
-    __syncthreads();
-    // dA_hat = diag(beta) dL; dA_kk = dA_hat o R (into dT); dR = dA_hat o A_kk (into Akk)
-#pragma unroll
-    for (int i = 0; i < (C * C + 255) / 256; ++i) {
-      const int idx = tid + 256 * i;
-      if (idx < C * C) {
-        const int r = idx / C, c = idx % C;
-        const float dah = sm.beta[r] * dl[i];
-        const float akk = sm.Akk[r][c], rr = sm.R[r][c];
-        sm.Akk[r][c] = dah * akk;          // dR
-        sm.dT[r][c] = dah * rr;            // dA_kk
-        // dL_rs * A_hat_rs, summed per row below (A_hat = A_kk o R)
-        sm.Ninv[r][c] = dl[i] * akk * rr;
-      }
-    }
-    __syncthreads();
-    if (tid < C) {
-      float acc = 0.f;
-      for (int c = 0; c < tid; ++c) acc += sm.Ninv[tid][c];
+      for (int c = 0; c < tid; ++c) acc += sm.X1[tid][c];
       sm.dbeta[tid] += acc;
     }
   } else {
@@ -761,71 +876,65 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
       const int r = tid, t = t0 + r;
       float acc = 0.f;
       if (t < s.T)
-        for (int c = 0; c < V; ++c)
-          acc += bb.dU[(size_t)ch * C * V + (size_t)r * V + c] * ld_f(Vg + (size_t)t * vrs + c);
+        for (int c = 0; c < V; ++c) acc += dUg[(size_t)r * V + c] * ld_f(Vg + (size_t)t * vrs + c);
       sm.dbeta[r] = acc;
     }
   }
   __syncthreads();
 
   // ---- dq = dq_s + dA_qk K;  dk = dk_s + dA_qk^T Q + (dA_kk + dA_kk^T) K
-  {
-    constexpr int KT = KD / 16;
-    for (int tile = w; tile < NT * KT; tile += 4) {
-      const int rt = tile / KT, kt = tile % KT;
-      f32x4 aq = zero4(), ak = zero4();
-      const int r = 16 * rt + n;  // A row
-      for (int sb = 0; sb < NT; ++sb) {
-        f32x4 bk, bqv;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int srow = 16 * sb + 4 * g + j;
-          const int t = t0 + srow;
-          bk[j] = (t < s.T) ? ld_f(Kg + (size_t)t * krs + 16 * kt + n) : 0.f;
-          bqv[j] = (t < s.T) ? ld_f(Qg + (size_t)t * krs + 16 * kt + n) : 0.f;
-        }
-        f32x4 a1, a2, a3;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int cidx = 16 * sb + 4 * g + j;
-          a1[j] = sm.dM[r][cidx];                        // dA_qk[r][s]
-          a2[j] = sm.dM[cidx][r];                        // dA_qk^T[r][s]
-          a3[j] = sm.dT[r][cidx] + sm.dT[cidx][r];       // dA_kk + dA_kk^T
-        }
-        mma16(aq, a1, bk);
-        mma16(ak, a2, bqv);
-        mma16(ak, a3, bk);
-      }
+  for (int tile = w; tile < NT * KT; tile += 4) {
+    const int rt = tile / KT, kt = tile % KT;
+    const int r = 16 * rt + n;
+    f32x4 aq = zero4(), ak = zero4();
+    for (int sb = 0; sb < NT; ++sb) {
+      f32x4 a1, a2, a3, bk, bq;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int rr = 16 * rt + 4 * g + j;
-        const int t = t0 + rr;
-        if (t < s.T) {
-          const size_t o = (((size_t)b * s.T + t) * s.H + h) * KD + 16 * kt + n;
-          const float vq = aq[j] + bb.dqs[(size_t)ch * C * KD + (size_t)rr * KD + 16 * kt + n];
-          const float vk = ak[j] + bb.dks[(size_t)ch * C * KD + (size_t)rr * KD + 16 * kt + n];
-          store_out(dqv, o, vq, s.out_bf16);
-          store_out(dkv, o, vk, s.out_bf16);
+        const int sidx = 16 * sb + 4 * g + j;
+        a1[j] = sm.dM[r][sidx];
+        a2[j] = sm.dM[sidx][r];
+        a3[j] = sm.dT[r][sidx] + sm.dT[sidx][r];
+        if constexpr (Sm::STAGE_QK) {
+          bk[j] = Elem<T>::to_f(sm.sK[sidx][16 * kt + n]);
+          bq[j] = Elem<T>::to_f(sm.sQ[sidx][16 * kt + n]);
+        } else {
+          const bool ok = t0 + sidx < s.T;
+          bk[j] = ok ? ld_f(Kg + (size_t)(t0 + sidx) * krs + 16 * kt + n) : 0.f;
+          bq[j] = ok ? ld_f(Qg + (size_t)(t0 + sidx) * krs + 16 * kt + n) : 0.f;
         }
+      }
+      mma_fx(aq, a1, bk, tag);
+      mma_fx(ak, a2, bq, tag);
+      mma_fx(ak, a3, bk, tag);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int rr = 16 * rt + 4 * g + j;
+      const int t = t0 + rr;
+      if (t < s.T) {
+        const size_t o = (((size_t)b * s.T + t) * s.H + h) * KD + 16 * kt + n;
+        const size_t wo = (size_t)ch * C * KD + (size_t)rr * KD + 16 * kt + n;
+        store_out(dqv, o, aq[j] + bb.dqs[wo], s.out_bf16);
+        store_out(dkv, o, ak[j] + bb.dks[wo], s.out_bf16);
       }
     }
   }
-  // ---- dv
+  // ---- dv = Tu^T dU = -dW (GDN) or diag(beta) dU (sGLA)
   for (int idx = tid; idx < C * V; idx += 256) {
     const int r = idx / V, c = idx % V;
     const int t = t0 + r;
     if (t >= s.T) continue;
-    const float val = gdn ? -bb.dW[(size_t)ch * C * V + idx]
-                          : sm.beta[r] * bb.dU[(size_t)ch * C * V + idx];
+    const float val = gdn ? -bb.dW[(size_t)ch * C * V + idx] : sm.beta[r] * dUg[idx];
     store_out(dvv, (((size_t)b * s.T + t) * s.H + h) * (size_t)V + c, val, s.out_bf16);
   }
 
-  // ---- Gram backward: rows (dq2, dk2 via dR rows, dG row sums) and columns
+  // ---- backward of the decayed Grams R, R' and of the coefficient vectors
   for (int idx = tid; idx < C * E; idx += 256) {
     const int r = idx / E, e = idx % E;
     float aq2 = 0.f, ak2 = 0.f, grow = 0.f;
     for (int c = 0; c <= r; ++c) {
-      const float d = __expf((float)(sm.G[r][e] - sm.G[c][e]));
+      const float d = exp_nonpos((float)(sm.G[r][e] - sm.G[c][e]));
       const float drq = sm.Aqk[r][c] * d;
       const float drk = (c < r) ? sm.Akk[r][c] * d : 0.f;
       aq2 += drq * sm.k2[c][e];
@@ -834,14 +943,18 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
     }
     float acol = 0.f, gcol = 0.f;
     for (int rr = r; rr < C; ++rr) {  // r as the column index s
-      const float d = __expf((float)(sm.G[rr][e] - sm.G[r][e]));
+      const float d = exp_nonpos((float)(sm.G[rr][e] - sm.G[r][e]));
       const float drq = sm.Aqk[rr][r] * d;
       const float drk = (rr > r) ? sm.Akk[rr][r] * d : 0.f;
-      acol += drq * sm.q2[rr][e] + drk * sm.k2[rr][e];
-      gcol += (drq * sm.q2[rr][e] + drk * sm.k2[rr][e]) * sm.k2[r][e];
+      const float t2 = drq * sm.q2[rr][e] + drk * sm.k2[rr][e];
+      acol += t2;
+      gcol += t2 * sm.k2[r][e];
     }
-    const float da = sm.dcf[0][e][r], db = sm.dcf[1][e][r], dc = sm.dcf[2][e][r];
-    const float gm = sm.gam[r][e], gt = sm.gtail[r][e];
+    const float* dcf = bb.dcoef + (size_t)ch * 3 * E * C;
+    const float da = dcf[(0 * E + e) * C + r], db = dcf[(1 * E + e) * C + r],
+                dc = dcf[(2 * E + e) * C + r];
+    const double G = sm.G[r][e], GC = sm.G[C - 1][e];
+    const float gm = exp_nonpos((float)G), gt = exp_nonpos((float)(GC - G));
     // coefficient vectors a = k2 gamma, b = q2 gamma, c = k2 gamma^C / gamma
     sm.dG[r][e] = grow - gcol + da * sm.k2[r][e] * gm + db * sm.q2[r][e] * gm -
                   dc * sm.k2[r][e] * gt;
@@ -855,9 +968,12 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
   __syncthreads();
   if (tid < E) {
     const int e = tid;
+    const float* dcf = bb.dcoef + (size_t)ch * 3 * E * C;
+    const double GC = sm.G[C - 1][e];
     float acc = 0.f;
-    for (int r = 0; r < C; ++r) acc += sm.dcf[2][e][r] * sm.k2[r][e] * sm.gtail[r][e];
-    sm.dG[C - 1][e] += acc + sm.gam[C - 1][e] * sm.dgC[e];
+    for (int r = 0; r < C; ++r)
+      acc += dcf[(2 * E + e) * C + r] * sm.k2[r][e] * exp_nonpos((float)(GC - sm.G[r][e]));
+    sm.dG[C - 1][e] += acc + exp_nonpos((float)GC) * bb.dgC[(size_t)ch * E4 + e];
     // reverse cumulative sum within the chunk: dg_j = sum_{r >= j} dG_r
     float run = 0.f;
     for (int r = C - 1; r >= 0; --r) {
@@ -876,8 +992,8 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
     const int t = t0 + tid;
     if (t < s.T) dbeta[((size_t)b * s.T + t) * s.H + h] = sm.dbeta[tid];
   }
-  (void)l;
 }
+
 
 // ----------------------------------------------------------------- launchers
 template <typename T, int KD, int C, int E>
@@ -915,7 +1031,7 @@ template <typename T, int KD, int C, int E>
 static hipError_t chunk_inst(const Shape& s, const FwdIn& in, const void* dO, const SavedBufs& sv,
                              const BwdBufs& bb, void* dq, void* dk, void* dv, void* dq2, void* dk2,
                              float* dg, float* dbeta, hipStream_t st) {
-  const size_t smem = sizeof(ChunkSmem<C, E>);
+  const size_t smem = sizeof(ChunkSmem<T, KD, C, E>);
   static bool attr = false;
   if (!attr) {
     (void)hipFuncSetAttribute((const void*)k_bwd_chunk<T, KD, C, E>,
@@ -945,7 +1061,8 @@ static hipError_t chunk_inst(const Shape& s, const FwdIn& in, const void* dO, co
 template <typename T, int KD, int C, int E>
 static bool bwd_fits_inst() {
   return sizeof(RecSmem<T, KD, C, E, bwd_waves<E>()>) <= 160 * 1024 &&
-         sizeof(StateSmem<T, KD, C, E>) <= 160 * 1024 && sizeof(ChunkSmem<C, E>) <= 160 * 1024;
+         sizeof(StateSmem<T, KD, C, E>) <= 160 * 1024 &&
+         sizeof(ChunkSmem<T, KD, C, E>) <= 160 * 1024;
 }
 
 bool bwd_fits_lds(int K, int C, int E, bool bf16) {

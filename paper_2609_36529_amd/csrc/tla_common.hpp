@@ -101,6 +101,33 @@ __device__ __forceinline__ void split_frag(f32x4 x, f32x4& hi, f32x4& lo) {
   lo = zero4();
 }
 
+// LDS row strides are padded to (2 mod 32) dwords for bf16 rows and (4 mod
+// 32) for fp32 rows (row length + 4 elements), so the 16 lanes that read one
+// fragment column hit distinct banks.  Such bf16 rows are only 8-byte aligned:
+// 8-element copies into them use two 8-byte stores.
+template <typename T>
+__device__ __forceinline__ void lds_put8(T* dst, const T* src) {
+  if constexpr (sizeof(T) == 2) {
+    ((uint2*)dst)[0] = ((const uint2*)src)[0];
+    ((uint2*)dst)[1] = ((const uint2*)src)[1];
+  } else {
+    ((float4*)dst)[0] = ((const float4*)src)[0];
+    ((float4*)dst)[1] = ((const float4*)src)[1];
+  }
+}
+// Store 4 elements (a column segment of a transposed tile) with one write.
+template <typename T>
+__device__ __forceinline__ void lds_put4(T* dst, T a, T b, T c, T d) {
+  if constexpr (sizeof(T) == 2) {
+    uint2 u;
+    u.x = (uint32_t)a | ((uint32_t)b << 16);
+    u.y = (uint32_t)c | ((uint32_t)d << 16);
+    *(uint2*)dst = u;
+  } else {
+    *(float4*)dst = make_float4(a, b, c, d);
+  }
+}
+
 // Gather 4 strided elements into a fragment (stride in elements).
 template <typename T>
 __device__ __forceinline__ typename Elem<T>::frag ld_frag_strided(const T* p, int stride) {
@@ -149,6 +176,54 @@ __device__ __forceinline__ float group16_sum(float x) {
 #pragma unroll
   for (int o = 8; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
   return x;
+}
+
+// X = (I + L)^{-1} for a strictly lower-triangular C x C matrix L (C a
+// multiple of 16), blockwise: the 16 x 16 diagonal blocks by forward
+// substitution (one column per thread), then the blocks below the diagonal
+// level by level, X_IJ = -X_II sum_{K=J}^{I-1} L_IK X_KJ (all blocks of one
+// level at once).  L(r, c) is an accessor; X is a C x ldx fp32 LDS array;
+// Y is (C/16 - 1) x 16 x 17 floats of LDS scratch.  Every thread of the
+// workgroup must call it; it ends with a barrier.
+template <int C, int NTHR, typename LF>
+__device__ void unit_lower_inverse(LF L, float* X, int ldx, float* Y) {
+  constexpr int NT = C / 16;
+  const int tid = threadIdx.x;
+  for (int idx = tid; idx < C * C; idx += NTHR) X[(idx / C) * ldx + idx % C] = 0.f;
+  __syncthreads();
+  if (tid < C) {
+    const int r0 = 16 * (tid / 16), col = tid % 16;
+    float x[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      float acc = 0.f;
+#pragma unroll
+      for (int j = 0; j < i; ++j) acc += L(r0 + i, r0 + j) * x[j];
+      x[i] = (i < col) ? 0.f : ((i == col) ? 1.f : -acc);
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i) X[(r0 + i) * ldx + r0 + col] = x[i];
+  }
+  __syncthreads();
+  for (int d = 1; d < NT; ++d) {
+    const int npairs = NT - d;
+    for (int idx = tid; idx < npairs * 256; idx += NTHR) {
+      const int pr = idx / 256, i = (idx / 16) % 16, j = idx % 16;
+      const int I = d + pr, J = pr;
+      float acc = 0.f;
+      for (int kk = 16 * J; kk < 16 * I; ++kk) acc += L(16 * I + i, kk) * X[kk * ldx + 16 * J + j];
+      Y[(pr * 16 + i) * 17 + j] = acc;
+    }
+    __syncthreads();
+    for (int idx = tid; idx < npairs * 256; idx += NTHR) {
+      const int pr = idx / 256, i = (idx / 16) % 16, j = idx % 16;
+      const int I = d + pr, J = pr;
+      float acc = 0.f;
+      for (int m = 0; m <= i; ++m) acc += X[(16 * I + i) * ldx + 16 * I + m] * Y[(pr * 16 + m) * 17 + j];
+      X[(16 * I + i) * ldx + 16 * J + j] = -acc;
+    }
+    __syncthreads();
+  }
 }
 
 // XCD-aware block mapping: the 8 accelerator dies each have their own L2 and

@@ -181,8 +181,8 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
 // ---------------------------------------------------------------- forward
 template <typename T, int KD, int C, int E, int NW>
 struct FwdSmem {
-  static constexpr int KP = KD + 8;  // padded row lengths (elements)
-  static constexpr int CP = C + 8;
+  static constexpr int KP = KD + 4;  // padded row lengths (elements)
+  static constexpr int CP = C + 4;
   static constexpr int NT = C / 16;
   static constexpr int E4 = (E + 3) & ~3;
   // bf16 operands carry Tu and M as hi + lo pairs (SPLIT).  The largest
@@ -311,13 +311,13 @@ struct FwdStage {
       if (blk < RB * CB) {
 #pragma unroll
         for (int rr = 0; rr < 4; ++rr) {
-          copy8(&sm.K[4 * rb + rr][8 * cb], k[i][rr].x);
-          if constexpr (STAGE_Q) copy8(&sm.Q[4 * rb + rr][8 * cb], q[i][rr].x);
+          lds_put8(&sm.K[4 * rb + rr][8 * cb], k[i][rr].x);
+          if constexpr (STAGE_Q) lds_put8(&sm.Q[4 * rb + rr][8 * cb], q[i][rr].x);
         }
 #pragma unroll
         for (int cc = 0; cc < 8; ++cc)
-#pragma unroll
-          for (int rr = 0; rr < 4; ++rr) sm.Kt[8 * cb + cc][4 * rb + rr] = k[i][rr].x[cc];
+          lds_put4(&sm.Kt[8 * cb + cc][4 * rb], k[i][0].x[cc], k[i][1].x[cc], k[i][2].x[cc],
+                   k[i][3].x[cc]);
       }
     }
 #pragma unroll
