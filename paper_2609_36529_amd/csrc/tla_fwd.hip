@@ -205,21 +205,45 @@ struct FwdSmem {
   alignas(16) f32x4 O[NW][NT][64];
 };
 
+// 8 consecutive elements kept as raw 32-bit words, so that a prefetch load is
+// not unpacked (and waited for) before the data is written to LDS.
 template <typename T>
 struct Raw8 {
-  T x[8];
+  uint4 w[sizeof(T) / 2];  // bf16: one 16-byte word; fp32: two
+  __device__ __forceinline__ T get(int i) const {
+    if constexpr (sizeof(T) == 2) {
+      const uint32_t d = (i < 2) ? w[0].x : (i < 4) ? w[0].y : (i < 6) ? w[0].z : w[0].w;
+      return (T)((i & 1) ? (d >> 16) : (d & 0xffffu));
+    } else {
+      const uint4& q = w[i >> 2];
+      const uint32_t d = ((i & 3) == 0) ? q.x : ((i & 3) == 1) ? q.y : ((i & 3) == 2) ? q.z : q.w;
+      return __uint_as_float(d);
+    }
+  }
 };
 template <typename T>
 __device__ __forceinline__ Raw8<T> load8(const T* src) {
   Raw8<T> r;
-  copy8(r.x, src);
+#pragma unroll
+  for (int i = 0; i < (int)(sizeof(T) / 2); ++i) r.w[i] = ((const uint4*)src)[i];
   return r;
 }
 template <typename T>
 __device__ __forceinline__ Raw8<T> zero_raw8() {
   Raw8<T> r;
-  zero8(r.x);
+#pragma unroll
+  for (int i = 0; i < (int)(sizeof(T) / 2); ++i) r.w[i] = make_uint4(0, 0, 0, 0);
   return r;
+}
+template <typename T>
+__device__ __forceinline__ void lds_put_raw8(T* dst, const Raw8<T>& r) {
+  if constexpr (sizeof(T) == 2) {
+    ((uint2*)dst)[0] = make_uint2(r.w[0].x, r.w[0].y);
+    ((uint2*)dst)[1] = make_uint2(r.w[0].z, r.w[0].w);
+  } else {
+    ((uint4*)dst)[0] = r.w[0];
+    ((uint4*)dst)[1] = r.w[1];
+  }
 }
 
 // Register staging of one chunk's inputs for the recurrent forward: global
@@ -235,7 +259,7 @@ struct FwdStage {
   static constexpr int E4 = (E + 3) & ~3;
   Raw8<T> k[NKB][4];
   Raw8<T> q[STAGE_Q ? NKB : 1][4];
-  T v[NV4][4];
+  uint32_t v[NV4][sizeof(T) == 2 ? 2 : 4];  // 4 elements as raw words
   f32x4 m[NMB], tu[NMB], c[NCB];
   float gc, beta;
 
@@ -266,14 +290,17 @@ struct FwdStage {
       const int r = idx >> 2, c4 = idx & 3;
       if (idx < C * 4) {
         const int t = t0 + r;
-        if (t < s.T) {
-          if constexpr (sizeof(T) == 2)
-            *(uint2*)v[i] = *(const uint2*)(Vg + (size_t)t * vrs + 4 * c4);
-          else
-            *(float4*)v[i] = *(const float4*)(Vg + (size_t)t * vrs + 4 * c4);
+        if constexpr (sizeof(T) == 2) {
+          const uint2 x = (t < s.T) ? *(const uint2*)(Vg + (size_t)t * vrs + 4 * c4) : make_uint2(0, 0);
+          v[i][0] = x.x;
+          v[i][1] = x.y;
         } else {
-#pragma unroll
-          for (int j = 0; j < 4; ++j) v[i][j] = T(0);
+          const uint4 x = (t < s.T) ? *(const uint4*)(Vg + (size_t)t * vrs + 4 * c4)
+                                    : make_uint4(0, 0, 0, 0);
+          v[i][0] = x.x;
+          v[i][1] = x.y;
+          v[i][2] = x.z;
+          v[i][3] = x.w;
         }
       }
     }
@@ -311,13 +338,13 @@ struct FwdStage {
       if (blk < RB * CB) {
 #pragma unroll
         for (int rr = 0; rr < 4; ++rr) {
-          lds_put8(&sm.K[4 * rb + rr][8 * cb], k[i][rr].x);
-          if constexpr (STAGE_Q) lds_put8(&sm.Q[4 * rb + rr][8 * cb], q[i][rr].x);
+          lds_put_raw8(&sm.K[4 * rb + rr][8 * cb], k[i][rr]);
+          if constexpr (STAGE_Q) lds_put_raw8(&sm.Q[4 * rb + rr][8 * cb], q[i][rr]);
         }
 #pragma unroll
         for (int cc = 0; cc < 8; ++cc)
-          lds_put4(&sm.Kt[8 * cb + cc][4 * rb], k[i][0].x[cc], k[i][1].x[cc], k[i][2].x[cc],
-                   k[i][3].x[cc]);
+          lds_put4(&sm.Kt[8 * cb + cc][4 * rb], k[i][0].get(cc), k[i][1].get(cc),
+                   k[i][2].get(cc), k[i][3].get(cc));
       }
     }
 #pragma unroll
@@ -326,7 +353,14 @@ struct FwdStage {
       const int r = idx >> 2, c4 = idx & 3;
       if (idx < C * 4) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) sm.Vt[4 * c4 + j][r] = v[i][j];
+        for (int j = 0; j < 4; ++j) {
+          T x;
+          if constexpr (sizeof(T) == 2)
+            x = (T)((j & 1) ? (v[i][j >> 1] >> 16) : (v[i][j >> 1] & 0xffffu));
+          else
+            x = __uint_as_float(v[i][j]);
+          sm.Vt[4 * c4 + j][r] = x;
+        }
       }
     }
 #pragma unroll
@@ -439,33 +473,46 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
     for (int pass = 0; pass < 2; ++pass) {
       f32x4 P[SPW][NT];
 #pragma unroll
-      for (int rt = 0; rt < NT; ++rt) {
+      for (int rt = 0; rt < NT; ++rt)
 #pragma unroll
         for (int i = 0; i < SPW; ++i) P[i][rt] = zero4();
+      // A fragment of K (pass 0) or Q (pass 1) rows for row tile rt, block kb
+      auto afrag = [&](int rt, int kb) -> F {
         const int r = 16 * rt + n;
-        const bool qok = t0 + r < s.T;
-        const T* qrow = Qg + (size_t)(qok ? t0 + r : 0) * krs;
-        auto afrag = [&](int kb) -> F {
-          if (pass == 0) return ld_frag(&sm.K[r][16 * kb + 4 * g]);
-          if constexpr (Sm::STAGE_Q) return ld_frag(&sm.Q[r][16 * kb + 4 * g]);
-          else return qok ? ld_frag(qrow + 16 * kb + 4 * g) : cvt_frag<T>(zero4());
-        };
+        if (pass == 0) return ld_frag(&sm.K[r][16 * kb + 4 * g]);
+        if constexpr (Sm::STAGE_Q) {
+          return ld_frag(&sm.Q[r][16 * kb + 4 * g]);
+        } else {
+          const bool qok = t0 + r < s.T;
+          return qok ? ld_frag(Qg + (size_t)(t0 + r) * krs + 16 * kb + 4 * g) : cvt_frag<T>(zero4());
+        }
+      };
+      // k-block outer: the fragments of all row tiles are loaded together and
+      // NT x SPW independent accumulators advance per step
 #pragma unroll
-        for (int kb = 0; kb < KT; kb += (KT > 1 ? 2 : 1)) {
-          if constexpr (KT > 1) {
-            const F a0 = afrag(kb), a1 = afrag(kb + 1);
+      for (int kb = 0; kb < KT; kb += (KT > 1 ? 2 : 1)) {
+        if constexpr (KT > 1) {
+          F a0[NT], a1[NT];
 #pragma unroll
-            for (int i = 0; i < SPW; ++i) {
-              if (w * SPW + i >= E) continue;
-              mma32(P[i][rt], a0, a1, Sop[i][kb], Sop[i][kb + 1]);
-            }
-          } else {
-            const F a = afrag(0);
+          for (int rt = 0; rt < NT; ++rt) {
+            a0[rt] = afrag(rt, kb);
+            a1[rt] = afrag(rt, kb + 1);
+          }
 #pragma unroll
-            for (int i = 0; i < SPW; ++i) {
-              if (w * SPW + i >= E) continue;
-              mma16(P[i][rt], a, Sop[i][0]);
-            }
+          for (int i = 0; i < SPW; ++i) {
+            if (w * SPW + i >= E) continue;
+#pragma unroll
+            for (int rt = 0; rt < NT; ++rt) mma32(P[i][rt], a0[rt], a1[rt], Sop[i][kb], Sop[i][kb + 1]);
+          }
+        } else {
+          F a[NT];
+#pragma unroll
+          for (int rt = 0; rt < NT; ++rt) a[rt] = afrag(rt, 0);
+#pragma unroll
+          for (int i = 0; i < SPW; ++i) {
+            if (w * SPW + i >= E) continue;
+#pragma unroll
+            for (int rt = 0; rt < NT; ++rt) mma16(P[i][rt], a[rt], Sop[i][0]);
           }
         }
       }
@@ -503,15 +550,36 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
         }
       }
 #pragma unroll
-      for (int rt = 0; rt < NT; ++rt) {
-        U[rt] = zero4();
-        const int r = 16 * rt + n;
-        auto th = [&](int kb) { return ld_frag(&sm.Tu[r][16 * kb + 4 * g]); };
-        mma_k<C>(U[rt], th, [&](int kb) { return Xh[kb]; });
-        if constexpr (Sm::SPLIT) {
-          mma_k<C>(U[rt], th, [&](int kb) { return Xl[kb]; });
-          mma_k<C>(U[rt], [&](int kb) { return ld_frag(&sm.TuL[r][16 * kb + 4 * g]); },
-                   [&](int kb) { return Xh[kb]; });
+      for (int rt = 0; rt < NT; ++rt) U[rt] = zero4();
+      // k-block outer: NT independent accumulators per step
+#pragma unroll
+      for (int kb = 0; kb < NT; kb += (NT > 1 ? 2 : 1)) {
+        if constexpr (NT > 1) {
+          F h0[NT], h1[NT], l0[NT], l1[NT];
+#pragma unroll
+          for (int rt = 0; rt < NT; ++rt) {
+            h0[rt] = ld_frag(&sm.Tu[16 * rt + n][16 * kb + 4 * g]);
+            h1[rt] = ld_frag(&sm.Tu[16 * rt + n][16 * kb + 16 + 4 * g]);
+            if constexpr (Sm::SPLIT) {
+              l0[rt] = ld_frag(&sm.TuL[16 * rt + n][16 * kb + 4 * g]);
+              l1[rt] = ld_frag(&sm.TuL[16 * rt + n][16 * kb + 16 + 4 * g]);
+            }
+          }
+#pragma unroll
+          for (int rt = 0; rt < NT; ++rt) mma32(U[rt], h0[rt], h1[rt], Xh[kb], Xh[kb + 1]);
+          if constexpr (Sm::SPLIT) {
+#pragma unroll
+            for (int rt = 0; rt < NT; ++rt) mma32(U[rt], h0[rt], h1[rt], Xl[kb], Xl[kb + 1]);
+#pragma unroll
+            for (int rt = 0; rt < NT; ++rt) mma32(U[rt], l0[rt], l1[rt], Xh[kb], Xh[kb + 1]);
+          }
+        } else {
+          const F hh = ld_frag(&sm.Tu[n][4 * g]);
+          mma16(U[0], hh, Xh[0]);
+          if constexpr (Sm::SPLIT) {
+            mma16(U[0], hh, Xl[0]);
+            mma16(U[0], ld_frag(&sm.TuL[n][4 * g]), Xh[0]);
+          }
         }
       }
     } else {
@@ -568,29 +636,39 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
       for (int kb = 0; kb < NT; ++kb)
         split_frag(U[kb] * *(const f32x4*)&sm.coef[2][e][16 * kb + 4 * g], Uc[i][kb], Ucl[i][kb]);
     }
+    // k-block outer: KT x SPW independent accumulators per step
 #pragma unroll
-    for (int kt = 0; kt < KT; ++kt) {
-      const int r = 16 * kt + n;
+    for (int kb = 0; kb < NT; kb += (NT > 1 ? 2 : 1)) {
       if constexpr (NT > 1) {
+        F a0[KT], a1[KT];
 #pragma unroll
-        for (int kb = 0; kb + 1 < NT; kb += 2) {
-          const F a0 = ld_frag(&sm.Kt[r][16 * kb + 4 * g]);
-          const F a1 = ld_frag(&sm.Kt[r][16 * kb + 16 + 4 * g]);
-#pragma unroll
-          for (int i = 0; i < SPW; ++i) {
-            if (w * SPW + i >= E) continue;
-            mma32(S[i][kt], a0, a1, Uc[i][kb], Uc[i][kb + 1]);
-            if constexpr (Sm::SPLIT) mma32(S[i][kt], a0, a1, Ucl[i][kb], Ucl[i][kb + 1]);
-          }
+        for (int kt = 0; kt < KT; ++kt) {
+          a0[kt] = ld_frag(&sm.Kt[16 * kt + n][16 * kb + 4 * g]);
+          a1[kt] = ld_frag(&sm.Kt[16 * kt + n][16 * kb + 16 + 4 * g]);
         }
-      }
-      if constexpr (NT & 1) {
-        const F a = ld_frag(&sm.Kt[r][16 * (NT - 1) + 4 * g]);
 #pragma unroll
         for (int i = 0; i < SPW; ++i) {
           if (w * SPW + i >= E) continue;
-          mma16(S[i][kt], a, Uc[i][NT - 1]);
-          if constexpr (Sm::SPLIT) mma16(S[i][kt], a, Ucl[i][NT - 1]);
+#pragma unroll
+          for (int kt = 0; kt < KT; ++kt) mma32(S[i][kt], a0[kt], a1[kt], Uc[i][kb], Uc[i][kb + 1]);
+          if constexpr (Sm::SPLIT) {
+#pragma unroll
+            for (int kt = 0; kt < KT; ++kt)
+              mma32(S[i][kt], a0[kt], a1[kt], Ucl[i][kb], Ucl[i][kb + 1]);
+          }
+        }
+      } else {
+        F a[KT];
+#pragma unroll
+        for (int kt = 0; kt < KT; ++kt) a[kt] = ld_frag(&sm.Kt[16 * kt + n][4 * g]);
+#pragma unroll
+        for (int i = 0; i < SPW; ++i) {
+          if (w * SPW + i >= E) continue;
+#pragma unroll
+          for (int kt = 0; kt < KT; ++kt) {
+            mma16(S[i][kt], a[kt], Uc[i][0]);
+            if constexpr (Sm::SPLIT) mma16(S[i][kt], a[kt], Ucl[i][0]);
+          }
         }
       }
     }
