@@ -83,6 +83,7 @@ typedef struct tla_desc {
  * Supported shapes: K in {16, 32, 64, 128}, V a multiple of 16 up to 1024,
  * E in {1, 2, 4, 8, 16}, chunk in {16, 32, 64} with chunk <= 64 and the
  * (K, chunk) pairs instantiated in the library (tla_supported() tells).
+ * tla_bwd further needs V <= 128 (TLA_E_UNSUPPORTED otherwise).
  * Returns 1 if the description is valid and has a kernel instance, else 0.
  */
 int tla_supported(const tla_desc* desc);

@@ -308,6 +308,7 @@ int tla_bwd(const tla_desc* d, const void* q, const void* k, const void* v, cons
   int rc = check_desc(d, &s, false);
   if (rc) return rc;
   if (s.T < 1) return fail(TLA_E_SHAPE, "the backward needs T >= 1");
+  if (s.V > 128) return fail(TLA_E_UNSUPPORTED, "the backward supports V <= 128 (V=%d)", s.V);
   if (!q || !k || !v || !q2 || !k2 || !g || !dO || !saved || !dq || !dk || !dv || !dq2 || !dk2 ||
       !dg || !ws)
     return fail(TLA_E_NULL, "a required pointer is NULL");

@@ -347,19 +347,19 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
 // 16 CTW (w + 1)).  The chunk's dO, dW and U rows (A operands; dW and U as
 // bf16 hi + lo pairs) are staged in LDS once; the chunk-start state S_e and
 // the chunk-end state gradient dS'_e stream from their tiled stores as B
-// fragments, one slice ahead of the MFMAs.
+// operands of 32-deep MFMAs over pairs of 16-column value blocks, each pair
+// reloaded for the next slice as soon as this slice is done with it.  The
+// rows of Q and K that the row sums need live in registers.
 template <typename T, int KD, int C, int E>
 struct StateSmem {
-  static constexpr int VP = 128 + 8;       // V <= 128
   static constexpr bool SPLIT = sizeof(T) == 2;
-  // fp32 instances stage one 16-column block of V at a time (LDS budget)
+  // fp32 instances stage one 32-column pair of value blocks at a time (LDS budget)
   static constexpr bool STAGE_ALL = sizeof(T) == 2;
-  static constexpr int VS = STAGE_ALL ? VP : 16 + 4;
+  static constexpr int NCOL = STAGE_ALL ? 128 : 32;    // staged columns (V <= 128)
+  static constexpr int VS = NCOL + (SPLIT ? 8 : 4);     // row stride, conflict-free b128 reads
   alignas(16) T dO[C][VS];
   alignas(16) T dWh[C][VS], Uh[C][VS];
   alignas(16) T dWl[SPLIT ? C : 1][VS], Ul[SPLIT ? C : 1][VS];
-  alignas(16) T Qt[KD][C + 8];  // Q^T, K^T for the row sums
-  alignas(16) T Kt[KD][C + 8];
   alignas(16) float coef[3][E][C];
   alignas(16) float red[2][4][3][C];  // per-wave row-sum partials, by slice parity
   alignas(16) float dcf[3][E][C];
@@ -373,8 +373,7 @@ __global__ __launch_bounds__(256) void k_bwd_state(Shape s, FwdIn in, const void
   constexpr int KT = KD / 16;
   constexpr int CTW = (KT + 3) / 4;      // key column tiles per wave
   constexpr int E4 = (E + 3) & ~3;
-  constexpr int VBMAX = 8;               // V <= 128
-  typedef typename Elem<T>::frag F;
+  constexpr int NPMAX = 4;               // pairs of value blocks, V <= 128
   typedef StateSmem<T, KD, C, E> Sm;
   constexpr bool SPLIT = Sm::SPLIT;
   extern __shared__ __align__(16) unsigned char smem_raw[];
@@ -383,6 +382,7 @@ __global__ __launch_bounds__(256) void k_bwd_state(Shape s, FwdIn in, const void
   const int tid = threadIdx.x, w = wave_id(), l = lane_id(), g = l >> 4, n = l & 15;
   const int V = s.V;
   const int VB = V / 16;
+  const int NP = (VB + 1) / 2;
   const int ch = blockIdx.x;
   const int head = ch / s.Nc, ci = ch % s.Nc;
   const int b = head / s.H, h = head % s.H;
@@ -394,64 +394,100 @@ __global__ __launch_bounds__(256) void k_bwd_state(Shape s, FwdIn in, const void
   const float* dWg = bb.dW + (size_t)ch * C * V;
   const float* Ug = sv.U + (size_t)ch * C * V;
 
-  // stage A-operand columns [c0, c0 + ncols) into LDS columns [0, ncols)
+  // Stage A-operand columns [c0, c0 + ncols) (ncols a multiple of 32) into LDS
+  // columns [0, ncols); columns at or beyond V, and rows past T, are zero.
+  // Every load of the batch is issued before the first LDS write.
   auto stage = [&](int c0, int ncols) {
-    const int n4 = ncols / 4;
-    for (int idx = tid; idx < C * n4; idx += 256) {
-      const int r = idx / n4, c4 = idx % n4;
-      const int t = t0 + r;
-      const int col = c0 + 4 * c4;
-      T x[4];
-      if (t < s.T) {
+    constexpr int IT = (C * Sm::NCOL / 8 + 255) / 256;
+    const int n8 = ncols / 8;
+    Raw8<T> ro[IT];
+    f32x4 rw[IT][2], ru[IT][2];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) x[j] = dOg[(size_t)t * vrs + col + j];
-      } else {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) x[j] = T(0);
+    for (int it = 0; it < IT; ++it) {
+      const int idx = tid + 256 * it;
+      const int r = idx / n8, col = c0 + 8 * (idx % n8);
+      ro[it] = zero_raw8<T>();
+      rw[it][0] = rw[it][1] = ru[it][0] = ru[it][1] = zero4();
+      if (idx < C * n8 && col < V) {
+        if (t0 + r < s.T) ro[it] = load8(dOg + (size_t)(t0 + r) * vrs + col);
+        const float* pw = dWg + (size_t)r * V + col;
+        const float* pu = Ug + (size_t)r * V + col;
+        rw[it][0] = *(const f32x4*)pw;
+        rw[it][1] = *(const f32x4*)(pw + 4);
+        ru[it][0] = *(const f32x4*)pu;
+        ru[it][1] = *(const f32x4*)(pu + 4);
       }
+    }
 #pragma unroll
-      for (int j = 0; j < 4; ++j) sm.dO[r][4 * c4 + j] = x[j];
-      F hi, lo;
-      split_frag(*(const f32x4*)(dWg + (size_t)r * V + col), hi, lo);
-      *(F*)&sm.dWh[r][4 * c4] = hi;
-      if constexpr (SPLIT) *(F*)&sm.dWl[r][4 * c4] = lo;
-      split_frag(*(const f32x4*)(Ug + (size_t)r * V + col), hi, lo);
-      *(F*)&sm.Uh[r][4 * c4] = hi;
-      if constexpr (SPLIT) *(F*)&sm.Ul[r][4 * c4] = lo;
+    for (int it = 0; it < IT; ++it) {
+      const int idx = tid + 256 * it;
+      if (idx >= C * n8) continue;
+      const int r = idx / n8, c = 8 * (idx % n8);
+      if constexpr (SPLIT) {
+        *(uint4*)&sm.dO[r][c] = ro[it].w[0];
+        bf16x4 h0, l0, h1, l1;
+        split_frag(rw[it][0], h0, l0);
+        split_frag(rw[it][1], h1, l1);
+        *(bf16x8*)&sm.dWh[r][c] = __builtin_shufflevector(h0, h1, 0, 1, 2, 3, 4, 5, 6, 7);
+        *(bf16x8*)&sm.dWl[r][c] = __builtin_shufflevector(l0, l1, 0, 1, 2, 3, 4, 5, 6, 7);
+        split_frag(ru[it][0], h0, l0);
+        split_frag(ru[it][1], h1, l1);
+        *(bf16x8*)&sm.Uh[r][c] = __builtin_shufflevector(h0, h1, 0, 1, 2, 3, 4, 5, 6, 7);
+        *(bf16x8*)&sm.Ul[r][c] = __builtin_shufflevector(l0, l1, 0, 1, 2, 3, 4, 5, 6, 7);
+      } else {
+        lds_put_raw8(&sm.dO[r][c], ro[it]);
+        *(f32x4*)&sm.dWh[r][c] = rw[it][0];
+        *(f32x4*)&sm.dWh[r][c + 4] = rw[it][1];
+        *(f32x4*)&sm.Uh[r][c] = ru[it][0];
+        *(f32x4*)&sm.Uh[r][c + 4] = ru[it][1];
+      }
     }
   };
 
-  for (int idx = tid; idx < C * KD; idx += 256) {
-    const int r = idx / KD, c = idx % KD;
-    const int t = t0 + r;
-    sm.Qt[c][r] = (t < s.T) ? Qg[(size_t)t * krs + c] : T(0);
-    sm.Kt[c][r] = (t < s.T) ? Kg[(size_t)t * krs + c] : T(0);
-  }
-  {
-    const float* cg = p.coef + (size_t)ch * 3 * E * C;
-    for (int idx = tid; idx < 3 * E * C; idx += 256) (&sm.coef[0][0][0])[idx] = cg[idx];
-  }
-  if constexpr (Sm::STAGE_ALL) stage(0, V);
-
-  // B fragments of S_e^T and dS'_e^T for this wave's key columns, all V blocks
-  const T* Sck = (const T*)sv.Sck;
-  const T* dSck = (const T*)bb.dSck;
-  F sbuf[CTW][VBMAX], dbuf[CTW][VBMAX];
-  auto load_slice = [&](int e) {
+  // rows of Q and K at the accumulator positions (row 16 rt + 4 g + j, key 16 ct + n)
+  float qv[NT][CTW][4], kv[NT][CTW][4];
+#pragma unroll
+  for (int rt = 0; rt < NT; ++rt)
 #pragma unroll
     for (int c = 0; c < CTW; ++c) {
       const int ct = w * CTW + c;
 #pragma unroll
-      for (int vb = 0; vb < VBMAX; ++vb) {
-        if (ct < KT && vb < VB) {
-          const size_t tile = ((size_t)ch * E + e) * (V / 16) + vb;
-          sbuf[c][vb] = ld_frag(Sck + tile * KD * 16 + (16 * ct + n) * 16 + 4 * g);
-          dbuf[c][vb] = ld_frag(dSck + tile * KD * 16 + (16 * ct + n) * 16 + 4 * g);
-        }
+      for (int j = 0; j < 4; ++j) {
+        const int t = t0 + 16 * rt + 4 * g + j;
+        const bool ok = ct < KT && t < s.T;
+        const size_t off = (size_t)t * krs + 16 * ct + n;
+        qv[rt][c][j] = ok ? Elem<T>::to_f(Qg[off]) : 0.f;
+        kv[rt][c][j] = ok ? Elem<T>::to_f(Kg[off]) : 0.f;
       }
     }
+  {
+    const float* cg = p.coef + (size_t)ch * 3 * E * C;
+    for (int idx = tid; idx < 3 * E * C; idx += 256) (&sm.coef[0][0][0])[idx] = cg[idx];
+  }
+  if constexpr (Sm::STAGE_ALL) stage(0, 32 * NP);
+
+  // B operands: S_e^T and dS'_e^T for this wave's key columns; lane (g, n)
+  // takes key row 16 ct + n of value block 2 pp + g / 2, columns 8 (g & 1) + 0..7
+  const T* Sck = (const T*)sv.Sck;
+  const T* dSck = (const T*)bb.dSck;
+  Raw8<T> sbuf[CTW][NPMAX], dbuf[CTW][NPMAX];
+  auto load_pair = [&](int e, int c, int pp) {
+    const int ct = w * CTW + c;
+    const int vb = 2 * pp + (g >> 1);
+    if (ct < KT && vb < VB) {
+      const size_t off = ((((size_t)ch * E + e) * VB + vb) * KD + 16 * ct + n) * 16 + 8 * (g & 1);
+      sbuf[c][pp] = load8(Sck + off);
+      dbuf[c][pp] = load8(dSck + off);
+    } else {
+      sbuf[c][pp] = zero_raw8<T>();
+      dbuf[c][pp] = zero_raw8<T>();
+    }
   };
-  load_slice(0);
+#pragma unroll
+  for (int pp = 0; pp < NPMAX; ++pp)
+#pragma unroll
+    for (int c = 0; c < CTW; ++c)
+      if (pp < NP) load_pair(0, c, pp);
   __syncthreads();
 
   f32x4 dq[NT][CTW], dk[NT][CTW];
@@ -464,16 +500,6 @@ __global__ __launch_bounds__(256) void k_bwd_state(Shape s, FwdIn in, const void
     }
 
   for (int e = 0; e < E; ++e) {
-    F scur[CTW][VBMAX], dcur[CTW][VBMAX];
-#pragma unroll
-    for (int c = 0; c < CTW; ++c)
-#pragma unroll
-      for (int vb = 0; vb < VBMAX; ++vb) {
-        scur[c][vb] = sbuf[c][vb];
-        dcur[c][vb] = dbuf[c][vb];
-      }
-    if (e + 1 < E) load_slice(e + 1);  // in flight during this slice
-
     float gpart = 0.f;
     f32x4 X[NT][CTW], Y[NT][CTW], Vp[NT][CTW];
 #pragma unroll
@@ -485,76 +511,84 @@ __global__ __launch_bounds__(256) void k_bwd_state(Shape s, FwdIn in, const void
         Vp[rt][c] = zero4();
       }
 #pragma unroll
-    for (int vb = 0; vb < VBMAX; ++vb) {
-      if (vb >= VB) continue;
-      int col = 16 * vb;
+    for (int pp = 0; pp < NPMAX; ++pp) {
+      if (pp >= NP) continue;
+      int col = 32 * pp;
       if constexpr (!Sm::STAGE_ALL) {
         __syncthreads();
-        stage(16 * vb, 16);
+        stage(32 * pp, 32);
         __syncthreads();
         col = 0;
       }
 #pragma unroll
       for (int c = 0; c < CTW; ++c) {
         if (w * CTW + c >= KT) continue;
-        const f32x4 a = frag_to_f(scur[c][vb]), d = frag_to_f(dcur[c][vb]);
-        gpart += a[0] * d[0] + a[1] * d[1] + a[2] * d[2] + a[3] * d[3];
+        float a[8], d[8];
+        raw8_to_f(sbuf[c][pp], a);
+        raw8_to_f(dbuf[c][pp], d);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) gpart += a[i] * d[i];
       }
 #pragma unroll
       for (int rt = 0; rt < NT; ++rt) {
         const int r = 16 * rt + n;
-        const F ao = ld_frag(&sm.dO[r][col + 4 * g]);
-        const F awh = ld_frag(&sm.dWh[r][col + 4 * g]);
-        const F auh = ld_frag(&sm.Uh[r][col + 4 * g]);
-        F awl, aul;
+        const int cc = col + 8 * g;
+        const Raw8<T> ao = *(const Raw8<T>*)&sm.dO[r][cc];
+        const Raw8<T> awh = *(const Raw8<T>*)&sm.dWh[r][cc];
+        const Raw8<T> auh = *(const Raw8<T>*)&sm.Uh[r][cc];
+        Raw8<T> awl, aul;
         if constexpr (SPLIT) {
-          awl = ld_frag(&sm.dWl[r][col + 4 * g]);
-          aul = ld_frag(&sm.Ul[r][col + 4 * g]);
+          awl = *(const Raw8<T>*)&sm.dWl[r][cc];
+          aul = *(const Raw8<T>*)&sm.Ul[r][cc];
         }
 #pragma unroll
         for (int c = 0; c < CTW; ++c) {
           if (w * CTW + c >= KT) continue;
-          mma16(X[rt][c], ao, scur[c][vb]);
-          mma16(Y[rt][c], awh, scur[c][vb]);
-          mma16(Vp[rt][c], auh, dcur[c][vb]);
+          mma8(X[rt][c], ao, sbuf[c][pp]);
+          mma8(Y[rt][c], awh, sbuf[c][pp]);
+          mma8(Vp[rt][c], auh, dbuf[c][pp]);
           if constexpr (SPLIT) {
-            mma16(Y[rt][c], awl, scur[c][vb]);
-            mma16(Vp[rt][c], aul, dcur[c][vb]);
+            mma8(Y[rt][c], awl, sbuf[c][pp]);
+            mma8(Vp[rt][c], aul, dbuf[c][pp]);
           }
         }
+      }
+      // this pair is done for slice e: fetch it for slice e + 1
+      if (e + 1 < E) {
+#pragma unroll
+        for (int c = 0; c < CTW; ++c) load_pair(e + 1, c, pp);
       }
     }
     // fold slice e into dq_s, dk_s; per-row sums of Q o X, K o Y, K o V'
     const int par = e & 1;
+    float rs[3][16];
 #pragma unroll
-    for (int rt = 0; rt < NT; ++rt) {
+    for (int rt = 0; rt < 4; ++rt) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) rs[0][4 * rt + j] = rs[1][4 * rt + j] = rs[2][4 * rt + j] = 0.f;
+      if (rt >= NT) continue;
       const f32x4 ca = *(const f32x4*)&sm.coef[0][e][16 * rt + 4 * g];
       const f32x4 cb = *(const f32x4*)&sm.coef[1][e][16 * rt + 4 * g];
       const f32x4 cc = *(const f32x4*)&sm.coef[2][e][16 * rt + 4 * g];
-      f32x4 rdb = zero4(), rda = zero4(), rdc = zero4();
 #pragma unroll
       for (int c = 0; c < CTW; ++c) {
-        const int ct = w * CTW + c;
-        if (ct >= KT) continue;
+        if (w * CTW + c >= KT) continue;
         dq[rt][c] += cb * X[rt][c];
         dk[rt][c] += ca * Y[rt][c] + cc * Vp[rt][c];
-        const f32x4 qv = ld4_f(&sm.Qt[16 * ct + n][16 * rt + 4 * g]);
-        const f32x4 kv = ld4_f(&sm.Kt[16 * ct + n][16 * rt + 4 * g]);
-        rdb += qv * X[rt][c];
-        rda += kv * Y[rt][c];
-        rdc += kv * Vp[rt][c];
-      }
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const float x0 = group16_sum(rdb[j]);
-        const float x1 = group16_sum(rda[j]);
-        const float x2 = group16_sum(rdc[j]);
-        if (n == 0) {
-          sm.red[par][w][0][16 * rt + 4 * g + j] = x1;
-          sm.red[par][w][1][16 * rt + 4 * g + j] = x0;
-          sm.red[par][w][2][16 * rt + 4 * g + j] = x2;
+        for (int j = 0; j < 4; ++j) {
+          rs[0][4 * rt + j] += kv[rt][c][j] * Y[rt][c][j];   // d a_e
+          rs[1][4 * rt + j] += qv[rt][c][j] * X[rt][c][j];   // d b_e
+          rs[2][4 * rt + j] += kv[rt][c][j] * Vp[rt][c][j];  // d c_e
         }
       }
+    }
+    // lane n of group g now receives the row sum of row 16 (n / 4) + 4 g + n % 4
+    const int rrow = 16 * (n >> 2) + 4 * g + (n & 3);
+#pragma unroll
+    for (int kind = 0; kind < 3; ++kind) {
+      const float x = group16_transpose_sum(rs[kind], n);
+      if ((n >> 2) < NT) sm.red[par][w][kind][rrow] = x;
     }
     gpart = wave_sum(gpart);
     if (l == 0) sm.gred[w][e] = gpart;

@@ -171,10 +171,19 @@ __device__ __forceinline__ float wave_sum(float x) {
   for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
   return x;
 }
-// Sum over the 16 lanes that share a group g (lanes 16g .. 16g + 15).
+// Sum over the 16 lanes that share a group g (lanes 16g .. 16g + 15), with
+// DPP lane permutations (VALU, no LDS round trip): swap neighbours, swap
+// pairs, mirror within each 8-lane half, mirror within the 16-lane row.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), CTRL, 0xF,
+                                                            0xF, true));
+}
 __device__ __forceinline__ float group16_sum(float x) {
-#pragma unroll
-  for (int o = 8; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+  x += dpp_f<0xB1>(x);   // quad_perm [1,0,3,2]
+  x += dpp_f<0x4E>(x);   // quad_perm [2,3,0,1]
+  x += dpp_f<0x141>(x);  // row_half_mirror
+  x += dpp_f<0x140>(x);  // row_mirror
   return x;
 }
 
@@ -224,6 +233,95 @@ __device__ void unit_lower_inverse(LF L, float* X, int ldx, float* Y) {
     }
     __syncthreads();
   }
+}
+
+// 8 consecutive elements kept as raw 32-bit words, so that a prefetch load is
+// not unpacked (and waited for) before the data is written to LDS.
+template <typename T>
+struct Raw8 {
+  uint4 w[sizeof(T) / 2];  // bf16: one 16-byte word; fp32: two
+  __device__ __forceinline__ T get(int i) const {
+    if constexpr (sizeof(T) == 2) {
+      const uint32_t d = (i < 2) ? w[0].x : (i < 4) ? w[0].y : (i < 6) ? w[0].z : w[0].w;
+      return (T)((i & 1) ? (d >> 16) : (d & 0xffffu));
+    } else {
+      const uint4& q = w[i >> 2];
+      const uint32_t d = ((i & 3) == 0) ? q.x : ((i & 3) == 1) ? q.y : ((i & 3) == 2) ? q.z : q.w;
+      return __uint_as_float(d);
+    }
+  }
+};
+template <typename T>
+__device__ __forceinline__ Raw8<T> load8(const T* src) {
+  Raw8<T> r;
+#pragma unroll
+  for (int i = 0; i < (int)(sizeof(T) / 2); ++i) r.w[i] = ((const uint4*)src)[i];
+  return r;
+}
+template <typename T>
+__device__ __forceinline__ Raw8<T> zero_raw8() {
+  Raw8<T> r;
+#pragma unroll
+  for (int i = 0; i < (int)(sizeof(T) / 2); ++i) r.w[i] = make_uint4(0, 0, 0, 0);
+  return r;
+}
+template <typename T>
+__device__ __forceinline__ void lds_put_raw8(T* dst, const Raw8<T>& r) {
+  if constexpr (sizeof(T) == 2) {
+    ((uint2*)dst)[0] = make_uint2(r.w[0].x, r.w[0].y);
+    ((uint2*)dst)[1] = make_uint2(r.w[0].z, r.w[0].w);
+  } else {
+    ((uint4*)dst)[0] = r.w[0];
+    ((uint4*)dst)[1] = r.w[1];
+  }
+}
+
+// 32-deep MFMA step on raw 8-element operands: lane (g, n) holds the
+// contraction indices 8g .. 8g + 7 of row n of A and of column n of B (any
+// assignment of the 32 indices to lanes works as long as A and B agree).
+// bf16: one 16x16x32 MFMA; fp32: two 16-deep fp32 steps.
+__device__ __forceinline__ void mma8(f32x4& acc, const Raw8<bf16_t>& a, const Raw8<bf16_t>& b) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a.w[0]),
+                                                __builtin_bit_cast(bf16x8, b.w[0]), acc, 0, 0, 0);
+}
+__device__ __forceinline__ void mma8(f32x4& acc, const Raw8<float>& a, const Raw8<float>& b) {
+  mma16(acc, __builtin_bit_cast(f32x4, a.w[0]), __builtin_bit_cast(f32x4, b.w[0]));
+  mma16(acc, __builtin_bit_cast(f32x4, a.w[1]), __builtin_bit_cast(f32x4, b.w[1]));
+}
+// The 8 values as floats.
+template <typename T>
+__device__ __forceinline__ void raw8_to_f(const Raw8<T>& r, float* x) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) x[i] = Elem<T>::to_f(r.get(i));
+}
+
+// Transposed reduction over the 16 lanes of a group: every lane brings 16
+// values v[0..15]; afterwards lane n (of the group) holds the sum over the 16
+// lanes of v[n].  Four exchange rounds halve the live values each time (15
+// lane moves instead of 64 for sixteen separate reductions).  The lane pairs
+// of each round differ in the bit that decides which half a lane keeps:
+// rotate by 8 (bit 3), mirror within 8 (bit 2), reverse within 4 (bit 1),
+// swap neighbours (bit 0).
+__device__ __forceinline__ float group16_transpose_sum(const float (&v)[16], int n) {
+  float a[8], b[4], c[2];
+  const bool b3 = n & 8, b2 = n & 4, b1 = n & 2, b0 = n & 1;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const float send = b3 ? v[i] : v[i + 8];
+    a[i] = (b3 ? v[i + 8] : v[i]) + dpp_f<0x128>(send);  // row_ror:8
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float send = b2 ? a[i] : a[i + 4];
+    b[i] = (b2 ? a[i + 4] : a[i]) + dpp_f<0x141>(send);  // row_half_mirror
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const float send = b1 ? b[i] : b[i + 2];
+    c[i] = (b1 ? b[i + 2] : b[i]) + dpp_f<0x1B>(send);   // quad_perm [3,2,1,0]
+  }
+  const float send = b0 ? c[0] : c[1];
+  return (b0 ? c[1] : c[0]) + dpp_f<0xB1>(send);        // quad_perm [1,0,3,2]
 }
 
 // XCD-aware block mapping: the 8 accelerator dies each have their own L2 and

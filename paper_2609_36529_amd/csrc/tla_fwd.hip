@@ -205,47 +205,6 @@ struct FwdSmem {
   alignas(16) f32x4 O[NW][NT][64];
 };
 
-// 8 consecutive elements kept as raw 32-bit words, so that a prefetch load is
-// not unpacked (and waited for) before the data is written to LDS.
-template <typename T>
-struct Raw8 {
-  uint4 w[sizeof(T) / 2];  // bf16: one 16-byte word; fp32: two
-  __device__ __forceinline__ T get(int i) const {
-    if constexpr (sizeof(T) == 2) {
-      const uint32_t d = (i < 2) ? w[0].x : (i < 4) ? w[0].y : (i < 6) ? w[0].z : w[0].w;
-      return (T)((i & 1) ? (d >> 16) : (d & 0xffffu));
-    } else {
-      const uint4& q = w[i >> 2];
-      const uint32_t d = ((i & 3) == 0) ? q.x : ((i & 3) == 1) ? q.y : ((i & 3) == 2) ? q.z : q.w;
-      return __uint_as_float(d);
-    }
-  }
-};
-template <typename T>
-__device__ __forceinline__ Raw8<T> load8(const T* src) {
-  Raw8<T> r;
-#pragma unroll
-  for (int i = 0; i < (int)(sizeof(T) / 2); ++i) r.w[i] = ((const uint4*)src)[i];
-  return r;
-}
-template <typename T>
-__device__ __forceinline__ Raw8<T> zero_raw8() {
-  Raw8<T> r;
-#pragma unroll
-  for (int i = 0; i < (int)(sizeof(T) / 2); ++i) r.w[i] = make_uint4(0, 0, 0, 0);
-  return r;
-}
-template <typename T>
-__device__ __forceinline__ void lds_put_raw8(T* dst, const Raw8<T>& r) {
-  if constexpr (sizeof(T) == 2) {
-    ((uint2*)dst)[0] = make_uint2(r.w[0].x, r.w[0].y);
-    ((uint2*)dst)[1] = make_uint2(r.w[0].z, r.w[0].w);
-  } else {
-    ((uint4*)dst)[0] = r.w[0];
-    ((uint4*)dst)[1] = r.w[1];
-  }
-}
-
 // Register staging of one chunk's inputs for the recurrent forward: global
 // loads are issued one chunk ahead into registers and written to shared
 // memory (including the transposed copies) at the top of the next chunk.
