@@ -643,27 +643,99 @@ __device__ __forceinline__ void mma_fx(f32x4& acc, f32x4 a, f32x4 b, bf16_t*) {
 }
 __device__ __forceinline__ void mma_fx(f32x4& acc, f32x4 a, f32x4 b, float*) { mma16(acc, a, b); }
 
+// 8-value fp32 pieces as (hi, lo) bf16 pairs
+__device__ __forceinline__ void split8(f32x4 x0, f32x4 x1, Raw8<bf16_t>& hi, Raw8<bf16_t>& lo) {
+  bf16x4 h0, l0, h1, l1;
+  split_frag(x0, h0, l0);
+  split_frag(x1, h1, l1);
+  hi.w[0] = __builtin_bit_cast(uint4, __builtin_shufflevector(h0, h1, 0, 1, 2, 3, 4, 5, 6, 7));
+  lo.w[0] = __builtin_bit_cast(uint4, __builtin_shufflevector(l0, l1, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+// 32-deep step: exact operand a (an input) times fp32 values b (split for bf16)
+__device__ __forceinline__ void mma8_xs(f32x4& acc, const Raw8<bf16_t>& a, f32x4 b0, f32x4 b1) {
+  Raw8<bf16_t> bh, bl;
+  split8(b0, b1, bh, bl);
+  mma8(acc, a, bh);
+  mma8(acc, a, bl);
+}
+__device__ __forceinline__ void mma8_xs(f32x4& acc, const Raw8<float>& a, f32x4 b0, f32x4 b1) {
+  mma16(acc, __builtin_bit_cast(f32x4, a.w[0]), b0);
+  mma16(acc, __builtin_bit_cast(f32x4, a.w[1]), b1);
+}
+// 32-deep step, fp32 x fp32 (three bf16 products, or fp32 MFMAs)
+__device__ __forceinline__ void mma8_ss(f32x4& acc, f32x4 a0, f32x4 a1, f32x4 b0, f32x4 b1,
+                                        bf16_t*) {
+  Raw8<bf16_t> ah, al, bh, bl;
+  split8(a0, a1, ah, al);
+  split8(b0, b1, bh, bl);
+  mma8(acc, ah, bh);
+  mma8(acc, ah, bl);
+  mma8(acc, al, bh);
+}
+__device__ __forceinline__ void mma8_ss(f32x4& acc, f32x4 a0, f32x4 a1, f32x4 b0, f32x4 b1,
+                                        float*) {
+  mma16(acc, a0, b0);
+  mma16(acc, a1, b1);
+}
+// fp32 A (split for bf16) times two exact 16-deep B fragments: a 32-deep step
+__device__ __forceinline__ void mma_fx2(f32x4& acc, f32x4 a0, f32x4 a1, bf16x4 b0, bf16x4 b1) {
+  bf16x4 h0, l0, h1, l1;
+  split_frag(a0, h0, l0);
+  split_frag(a1, h1, l1);
+  mma32(acc, h0, h1, b0, b1);
+  mma32(acc, l0, l1, b0, b1);
+}
+__device__ __forceinline__ void mma_fx2(f32x4& acc, f32x4 a0, f32x4 a1, f32x4 b0, f32x4 b1) {
+  mma16(acc, a0, b0);
+  mma16(acc, a1, b1);
+}
+// 8 gradient values to an out_dtype row
+__device__ __forceinline__ void store8_out(void* base, size_t off, f32x4 a, f32x4 b, int out_bf16) {
+  if (out_bf16) {
+    const bf16x4 h0 = cvt_frag<bf16_t>(a), h1 = cvt_frag<bf16_t>(b);
+    *(uint4*)((bf16_t*)base + off) =
+        __builtin_bit_cast(uint4, __builtin_shufflevector(h0, h1, 0, 1, 2, 3, 4, 5, 6, 7));
+  } else {
+    *(f32x4*)((float*)base + off) = a;
+    *(f32x4*)((float*)base + off + 4) = b;
+  }
+}
+
+// LDS plan of the per-chunk kernel.  C x C fp32 matrices use a row stride of
+// C + 4 floats (16-byte rows, conflict-free fragment reads).  Two regions are
+// reused once their first contents are dead: the Q / K rows become dM^T and
+// dA_kk + dA_kk^T, and R / (I + L)^{-1} become K^T / Q^T (bf16 instances;
+// fp32 ones read Q and K from global memory so that the plan fits 160 KiB).
 template <typename T, int KD, int C, int E>
 struct ChunkSmem {
-  static constexpr int CP = C + 1;
+  static constexpr int CP = C + 4;
   static constexpr int KP = KD + 8;
+  static constexpr int CT = C + 4;
   static constexpr int NT = C / 16;
-  // bf16 instances keep the chunk's Q and K rows in LDS; fp32 ones read them
-  // from global memory so that the plan fits 160 KiB
   static constexpr bool STAGE_QK = sizeof(T) == 2;
-  alignas(16) T sQ[STAGE_QK ? C : 1][KP];
-  alignas(16) T sK[STAGE_QK ? C : 1][KP];
-  float Aqk[C][CP];   // A_qk, then dR' = dM o A_qk
-  float Akk[C][CP];   // A_kk, then dR = dA_hat o A_kk
-  float R[C][CP];     // R (strictly lower)
-  float X1[C][CP];    // (I + L)^{-1}, then dL o A_hat
-  float dM[C][CP];    // dM = dO U^T (lower), then dA_qk = dM o R'
-  float dT[C][CP];    // dTu = dU X^T, then P = N^{-T} dTu, then dA_kk = dA_hat o R
-  float Y[NT > 1 ? NT - 1 : 1][16][17];
-  float q2[C][E], k2[C][E];
-  double G[C][E];
-  float dG[C][E];
-  float beta[C], dbeta[C];
+  static constexpr int QR = STAGE_QK ? C : 1;
+  static constexpr int KR = STAGE_QK ? KD : 1;
+  union U1 {
+    struct { T sQ[QR][KP]; T sK[QR][KP]; } qk;           // Q, K rows
+    struct { float dMT[C][CP]; float Dsym[C][CP]; } tr;  // dA_qk^T, dA_kk + dA_kk^T
+  };
+  union U2 {
+    struct { float R[C][CP]; float X1[C][CP]; } r;       // R; (I + L)^{-1}, then dL o A_hat
+    struct { T Kt[KR][CT]; T Qt[KR][CT]; } kq;           // K^T, Q^T
+  };
+  alignas(16) U1 u1;
+  alignas(16) U2 u2;
+  alignas(16) float Aqk[C][CP];  // A_qk, then dR' = dM o A_qk
+  alignas(16) float Akk[C][CP];  // A_kk, then dR = dA_hat o A_kk
+  alignas(16) float dM[C][CP];   // dA_qk = dM o R'
+  alignas(16) float dT[C][CP];   // dTu, P = N^{-T} dTu, dA_kk; then the Gram-backward sums
+  alignas(16) float Y[NT > 1 ? NT - 1 : 1][16][17];
+  alignas(16) float q2[C][E];
+  alignas(16) float k2[C][E];
+  alignas(16) double G[C][E];
+  alignas(16) float dG[C][E];
+  alignas(16) float beta[C];
+  alignas(16) float dbeta[C];
 };
 
 template <typename T, int KD, int C, int E>
@@ -674,15 +746,16 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
   constexpr int NT = C / 16;
   constexpr int KT = KD / 16;
   constexpr int E4 = (E + 3) & ~3;
-  constexpr int VBMAX = 8;  // V <= 128
+  constexpr int NVPMAX = 4;  // pairs of 16-column value blocks, V <= 128
   typedef typename Elem<T>::frag F;
   typedef ChunkSmem<T, KD, C, E> Sm;
+  constexpr bool STAGE_QK = Sm::STAGE_QK;
   extern __shared__ __align__(16) unsigned char smem_raw[];
   Sm& sm = *reinterpret_cast<Sm*>(smem_raw);
-  T* tag = nullptr;  // selects the MFMA flavour of mma_ff / mma_fx
+  T* tag = nullptr;  // selects the MFMA flavour of the mixed-precision helpers
   const int tid = threadIdx.x, w = wave_id(), l = lane_id(), g = l >> 4, n = l & 15;
   const int V = s.V;
-  const int VB = V / 16;
+  const int NVP = (V / 16 + 1) / 2;
   const int ch = blockIdx.x;
   const int head = ch / s.Nc, ci = ch % s.Nc;
   const int b = head / s.H, h = head % s.H;
@@ -695,131 +768,180 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
   const float* Ug = sv.U + (size_t)ch * C * V;
   const float* Xg = sv.X + (size_t)ch * C * V;
   const float* dUg = bb.dU + (size_t)ch * C * V;
+  const float* dWg = bb.dW + (size_t)ch * C * V;
+  const float* dcf = bb.dcoef + (size_t)ch * 3 * E * C;
   const size_t eoff = (((size_t)b * s.T) * s.H + h) * E;
   const size_t erow = (size_t)s.H * E;
   const bool gdn = s.variant == 1;
 
-  // ---- phase 0: per-position vectors, Q and K rows
+  // ---- phase 0: per-position vectors, Q and K rows, in-chunk cumulative log-gates
   for (int idx = tid; idx < C * E; idx += 256) {
     const int r = idx / E, e = idx % E;
     const int t = t0 + r;
     const bool ok = t < s.T;
     sm.q2[r][e] = ok ? ld_f((const T*)in.q2 + eoff + (size_t)t * erow + e) : 0.f;
     sm.k2[r][e] = ok ? ld_f((const T*)in.k2 + eoff + (size_t)t * erow + e) : 0.f;
-    sm.G[r][e] = ok ? (double)in.g[eoff + (size_t)t * erow + e] : 0.0;
   }
   for (int r = tid; r < C; r += 256) {
     const int t = t0 + r;
     sm.beta[r] = (t < s.T) ? (in.beta ? in.beta[((size_t)b * s.T + t) * s.H + h] : 1.f) : 0.f;
   }
-  if constexpr (Sm::STAGE_QK) {
-    for (int idx = tid; idx < C * KD / 8; idx += 256) {
+  if constexpr (STAGE_QK) {
+    constexpr int IT = (C * KD / 8 + 255) / 256;
+    Raw8<T> qv[IT], kv[IT];
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int idx = tid + 256 * it;
       const int r = idx / (KD / 8), c8 = idx % (KD / 8);
       const int t = t0 + r;
-      uint4 qv = make_uint4(0, 0, 0, 0), kv = make_uint4(0, 0, 0, 0);
-      if (t < s.T) {
-        qv = *(const uint4*)(Qg + (size_t)t * krs + 8 * c8);
-        kv = *(const uint4*)(Kg + (size_t)t * krs + 8 * c8);
+      qv[it] = zero_raw8<T>();
+      kv[it] = zero_raw8<T>();
+      if (idx < C * KD / 8 && t < s.T) {
+        qv[it] = load8(Qg + (size_t)t * krs + 8 * c8);
+        kv[it] = load8(Kg + (size_t)t * krs + 8 * c8);
       }
-      *(uint4*)&sm.sQ[r][8 * c8] = qv;
-      *(uint4*)&sm.sK[r][8 * c8] = kv;
     }
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int idx = tid + 256 * it;
+      if (idx >= C * KD / 8) continue;
+      const int r = idx / (KD / 8), c8 = idx % (KD / 8);
+      *(Raw8<T>*)&sm.u1.qk.sQ[r][8 * c8] = qv[it];
+      *(Raw8<T>*)&sm.u1.qk.sK[r][8 * c8] = kv[it];
+    }
+  }
+  // G = inclusive cumulative sum of g over the chunk, in fp64: one wave per
+  // slice, lane r holds row r
+  for (int e = w; e < E; e += 4) {
+    const int t = t0 + l;
+    double x = (l < C && t < s.T) ? (double)in.g[eoff + (size_t)t * erow + e] : 0.0;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const double y = __shfl_up(x, off, 64);
+      if (l >= off) x += y;
+    }
+    if (l < C) sm.G[l][e] = x;
   }
   __syncthreads();
-  if (tid < E) {
-    double acc = 0.0;
-    for (int r = 0; r < C; ++r) {
-      acc += sm.G[r][tid];
-      sm.G[r][tid] = acc;
-    }
-  }
-  // fragment accessors for Q and K rows (A or B operand over the key axis)
-  auto qrow = [&](int r, int kb) -> F {
-    if constexpr (Sm::STAGE_QK) return ld_frag(&sm.sQ[r][16 * kb + 4 * g]);
-    else return (t0 + r < s.T) ? ld_frag(Qg + (size_t)(t0 + r) * krs + 16 * kb + 4 * g)
-                               : cvt_frag<T>(zero4());
+
+  // Q / K rows as 8-element operands at columns [col, col + 8) (zero past KD or T)
+  auto qrow8 = [&](int r, int col) -> Raw8<T> {
+    if (col >= KD) return zero_raw8<T>();
+    if constexpr (STAGE_QK) return *(const Raw8<T>*)&sm.u1.qk.sQ[r][col];
+    else return (t0 + r < s.T) ? load8(Qg + (size_t)(t0 + r) * krs + col) : zero_raw8<T>();
   };
-  auto krow = [&](int r, int kb) -> F {
-    if constexpr (Sm::STAGE_QK) return ld_frag(&sm.sK[r][16 * kb + 4 * g]);
-    else return (t0 + r < s.T) ? ld_frag(Kg + (size_t)(t0 + r) * krs + 16 * kb + 4 * g)
-                               : cvt_frag<T>(zero4());
+  auto krow8 = [&](int r, int col) -> Raw8<T> {
+    if (col >= KD) return zero_raw8<T>();
+    if constexpr (STAGE_QK) return *(const Raw8<T>*)&sm.u1.qk.sK[r][col];
+    else return (t0 + r < s.T) ? load8(Kg + (size_t)(t0 + r) * krs + col) : zero_raw8<T>();
   };
 
-  // ---- phase 1: A_qk, A_kk, dM = dO U^T (lower tiles), dTu = dU X^T (all tiles)
+  // ---- phase 1, per 16 x 16 tile (rt, st); lane (g, n) holds rows 16 rt + 4 g + j
+  // of column 16 st + n:  A_qk, A_kk, dM = dO U^T (lower), dTu = dU X^T (GDN),
+  // then R', R and  dR' = dM o A_qk, dA_qk = dM o R'  element by element
+  // tiles in the order: the NT (NT + 1) / 2 lower ones, then the upper ones,
+  // dealt round-robin to the waves
   for (int tile = w; tile < NT * NT; tile += 4) {
-    const int rt = tile / NT, st = tile % NT;
-    const int r = 16 * rt + n, c = 16 * st + n;
+    constexpr int NL = NT * (NT + 1) / 2;
+    int rt = 0, st = 0;
+    if (tile < NL) {
+      while ((rt + 1) * (rt + 2) / 2 <= tile) ++rt;
+      st = tile - rt * (rt + 1) / 2;
+    } else {
+      int u = tile - NL;
+      while (u >= NT - 1 - rt) {
+        u -= NT - 1 - rt;
+        ++rt;
+      }
+      st = rt + 1 + u;
+    }
     const bool lower = st <= rt;
-    const bool rok = t0 + r < s.T;
+    const int ra = 16 * rt + n, cb = 16 * st + n;  // A-operand row, B-operand row
+    const bool raok = t0 + ra < s.T;
+    // global operand loads first (value columns 32 vp + 8 g .. + 7)
+    Raw8<T> dOa[NVPMAX];
+    f32x4 Ub[NVPMAX][2], dUa[NVPMAX][2], Xb[NVPMAX][2];
+#pragma unroll
+    for (int vp = 0; vp < NVPMAX; ++vp) {
+      const int col = 32 * vp + 8 * g;
+      const bool cok = vp < NVP && col < V;
+      dOa[vp] = zero_raw8<T>();
+      Ub[vp][0] = Ub[vp][1] = dUa[vp][0] = dUa[vp][1] = Xb[vp][0] = Xb[vp][1] = zero4();
+      if (lower && cok) {
+        if (raok) dOa[vp] = load8(dOg + (size_t)(t0 + ra) * vrs + col);
+        Ub[vp][0] = *(const f32x4*)(Ug + (size_t)cb * V + col);
+        Ub[vp][1] = *(const f32x4*)(Ug + (size_t)cb * V + col + 4);
+      }
+      if (gdn && cok) {
+        dUa[vp][0] = *(const f32x4*)(dUg + (size_t)ra * V + col);
+        dUa[vp][1] = *(const f32x4*)(dUg + (size_t)ra * V + col + 4);
+        Xb[vp][0] = *(const f32x4*)(Xg + (size_t)cb * V + col);
+        Xb[vp][1] = *(const f32x4*)(Xg + (size_t)cb * V + col + 4);
+      }
+    }
     f32x4 aq = zero4(), ak = zero4(), dm = zero4(), dt = zero4();
     if (lower) {
-      bmma_k<KD>(aq, [&](int kb) { return qrow(r, kb); }, [&](int kb) { return krow(c, kb); });
-      bmma_k<KD>(ak, [&](int kb) { return krow(r, kb); }, [&](int kb) { return krow(c, kb); });
-      f32x4 da[VBMAX], ub[VBMAX];
 #pragma unroll
-      for (int kb = 0; kb < VBMAX; ++kb) {
-        if (kb < VB) {
-          da[kb] = rok ? ld4_f(dOg + (size_t)(t0 + r) * vrs + 16 * kb + 4 * g) : zero4();
-          ub[kb] = *(const f32x4*)(Ug + (size_t)c * V + 16 * kb + 4 * g);
-        }
+      for (int kp = 0; kp < (KD + 31) / 32; ++kp) {
+        const int col = 32 * kp + 8 * g;
+        const Raw8<T> kb = krow8(cb, col);
+        mma8(aq, qrow8(ra, col), kb);
+        mma8(ak, krow8(ra, col), kb);
+      }
+    }
+    // decayed Grams of the lane's four (r, c) pairs
+    float rq[4], rk[4];
+    {
+      const int c = 16 * st + n;
+      double Gc[E];
+      float k2c[E];
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        Gc[e] = sm.G[c][e];
+        k2c[e] = sm.k2[c][e];
       }
 #pragma unroll
-      for (int kb = 0; kb < VBMAX; ++kb)
-        if (kb < VB) mma_fx(dm, ub[kb], da[kb], tag);  // (U B-frag) x exact dO: swap below
+      for (int j = 0; j < 4; ++j) {
+        const int r = 16 * rt + 4 * g + j;
+        rq[j] = rk[j] = 0.f;
+        if (lower && c <= r) {
+#pragma unroll
+          for (int e = 0; e < E; ++e) {
+            const float d = exp_nonpos((float)(sm.G[r][e] - Gc[e])) * k2c[e];
+            rq[j] += sm.q2[r][e] * d;
+            rk[j] += sm.k2[r][e] * d;
+          }
+        }
+      }
+    }
+    if (lower) {
+#pragma unroll
+      for (int vp = 0; vp < NVPMAX; ++vp)
+        if (vp < NVP) mma8_xs(dm, dOa[vp], Ub[vp][0], Ub[vp][1]);
     }
     if (gdn) {
-      f32x4 xa[VBMAX], xb[VBMAX];
 #pragma unroll
-      for (int kb = 0; kb < VBMAX; ++kb) {
-        if (kb < VB) {
-          xa[kb] = *(const f32x4*)(dUg + (size_t)r * V + 16 * kb + 4 * g);
-          xb[kb] = *(const f32x4*)(Xg + (size_t)c * V + 16 * kb + 4 * g);
-        }
-      }
-#pragma unroll
-      for (int kb = 0; kb < VBMAX; ++kb)
-        if (kb < VB) mma_ff(dt, xa[kb], xb[kb], tag);
+      for (int vp = 0; vp < NVPMAX; ++vp)
+        if (vp < NVP) mma8_ss(dt, dUa[vp][0], dUa[vp][1], Xb[vp][0], Xb[vp][1], tag);
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int rr = 16 * rt + 4 * g + j, cc = 16 * st + n;
-      sm.Aqk[rr][cc] = aq[j];
-      sm.Akk[rr][cc] = ak[j];
-      sm.dT[rr][cc] = dt[j];
-      // dm was formed with U (split) as the A operand and dO as the B
-      // operand, so it holds (U dO^T) = dM^T: element (4g+j, n) of the tile is
-      // dM[16 rt + n][16 st + 4 g + j]; keep the lower triangle incl. diagonal
-      const int sidx = 16 * st + 4 * g + j, ridx = 16 * rt + n;
-      if (lower) sm.dM[ridx][sidx] = (sidx <= ridx) ? dm[j] : 0.f;
-      else sm.dM[ridx][sidx] = 0.f;
+      const int r = 16 * rt + 4 * g + j, c = 16 * st + n;
+      const bool le = lower && c <= r;
+      sm.Aqk[r][c] = le ? dm[j] * aq[j] : 0.f;  // dR'
+      sm.dM[r][c] = le ? dm[j] * rq[j] : 0.f;   // dA_qk
+      sm.u2.r.R[r][c] = (lower && c < r) ? rk[j] : 0.f;
+      sm.Akk[r][c] = ak[j];
+      sm.dT[r][c] = dt[j];
     }
-  }
-  __syncthreads();
-
-  // ---- R' and R element by element; dR' = dM o A_qk, dA_qk = dM o R'
-  for (int idx = tid; idx < C * C; idx += 256) {
-    const int r = idx / C, c = idx % C;
-    float rq = 0.f, rk = 0.f;
-    if (c <= r) {
-#pragma unroll
-      for (int e = 0; e < E; ++e) {
-        const float d = exp_nonpos((float)(sm.G[r][e] - sm.G[c][e]));
-        rq += sm.q2[r][e] * sm.k2[c][e] * d;
-        rk += sm.k2[r][e] * sm.k2[c][e] * d;
-      }
-    }
-    sm.R[r][c] = (c < r) ? rk : 0.f;
-    const float dm = sm.dM[r][c];
-    sm.Aqk[r][c] = dm * sm.Aqk[r][c];
-    sm.dM[r][c] = dm * rq;
   }
   __syncthreads();
 
   if (gdn) {
     // ---- (I + L)^{-1} with L = diag(beta)(A_kk o R), strictly lower
     unit_lower_inverse<C, 256>(
-        [&](int r, int c) { return sm.beta[r] * sm.Akk[r][c] * sm.R[r][c]; }, &sm.X1[0][0],
-        Sm::CP, &sm.Y[0][0][0]);
+        [&](int r, int c) { return sm.beta[r] * sm.Akk[r][c] * sm.u2.r.R[r][c]; },
+        &sm.u2.r.X1[0][0], Sm::CP, &sm.Y[0][0][0]);
     // ---- P = N^{-T} dTu on MFMA (fp32 operands); N^{-T} is upper triangular
     f32x4 pt[(NT * NT + 3) / 4];
 #pragma unroll
@@ -832,7 +954,7 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
           f32x4 a, bv;
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
-            a[j] = sm.X1[16 * kb + 4 * g + j][16 * rt + n];  // (N^{-1})^T[r][k]
+            a[j] = sm.u2.r.X1[16 * kb + 4 * g + j][16 * rt + n];  // (N^{-1})^T[r][k]
             bv[j] = sm.dT[16 * kb + 4 * g + j][16 * ct + n];
           }
           mma_ff(acc, a, bv, tag);
@@ -861,13 +983,9 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
         const int rt = tile / NT, st = tile % NT;
         if (st <= rt) {
           for (int kb = 0; kb <= st; ++kb) {
-            f32x4 a, bv;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              const int k = 16 * kb + 4 * g + j;
-              a[j] = sm.dT[16 * rt + n][k];
-              bv[j] = sm.X1[16 * st + n][k] * sm.beta[k];
-            }
+            const f32x4 a = *(const f32x4*)&sm.dT[16 * rt + n][16 * kb + 4 * g];
+            const f32x4 bv = *(const f32x4*)&sm.u2.r.X1[16 * st + n][16 * kb + 4 * g] *
+                             *(const f32x4*)&sm.beta[16 * kb + 4 * g];
             mma_ff(acc, a, bv, tag);
           }
         }
@@ -875,9 +993,7 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
       pt[i] = -acc;
     }
     __syncthreads();
-    // the products above used P rows as the A operand and (N^{-1} diag beta)
-    // rows as the B operand: element (4g+j, n) of tile (rt, st) is
-    // dN[16 rt + 4 g + j][16 st + n]
+    // element (4g+j, n) of tile (rt, st) is dL[16 rt + 4 g + j][16 st + n]
 #pragma unroll
     for (int i = 0; i < (NT * NT + 3) / 4; ++i) {
       const int tile = w + 4 * i;
@@ -887,18 +1003,18 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
         for (int j = 0; j < 4; ++j) {
           const int r = 16 * rt + 4 * g + j, c = 16 * st + n;
           const float dl = (c < r) ? pt[i][j] : 0.f;
-          const float akk = sm.Akk[r][c], rr = sm.R[r][c];
+          const float akk = sm.Akk[r][c], rr = sm.u2.r.R[r][c];
           const float dah = sm.beta[r] * dl;
-          sm.Akk[r][c] = dah * akk;  // dR
-          sm.dT[r][c] = dah * rr;    // dA_kk
-          sm.X1[r][c] = dl * akk * rr;  // dL o A_hat
+          sm.Akk[r][c] = dah * akk;          // dR
+          sm.dT[r][c] = dah * rr;            // dA_kk
+          sm.u2.r.X1[r][c] = dl * akk * rr;  // dL o A_hat
         }
       }
     }
     __syncthreads();
     if (tid < C) {
       float acc = 0.f;
-      for (int c = 0; c < tid; ++c) acc += sm.X1[tid][c];
+      for (int c = 0; c < tid; ++c) acc += sm.u2.r.X1[tid][c];
       sm.dbeta[tid] += acc;
     }
   } else {
@@ -906,92 +1022,247 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
       sm.Akk[idx / C][idx % C] = 0.f;  // dR
       sm.dT[idx / C][idx % C] = 0.f;   // dA_kk
     }
-    if (tid < C) {  // sGLA: dbeta_r = <dU_r, v_r>
-      const int r = tid, t = t0 + r;
+    // sGLA: dbeta_r = <dU_r, v_r>; four lanes per row
+    if (tid < 4 * C) {
+      const int r = tid >> 2, q = tid & 3, t = t0 + r;
       float acc = 0.f;
-      if (t < s.T)
-        for (int c = 0; c < V; ++c) acc += dUg[(size_t)r * V + c] * ld_f(Vg + (size_t)t * vrs + c);
-      sm.dbeta[r] = acc;
+      if (t < s.T) {
+        for (int c = 8 * q; c < V; c += 32) {
+          const f32x4 u0 = *(const f32x4*)(dUg + (size_t)r * V + c);
+          const f32x4 u1 = *(const f32x4*)(dUg + (size_t)r * V + c + 4);
+          float vv[8];
+          raw8_to_f(load8(Vg + (size_t)t * vrs + c), vv);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) acc += u0[i] * vv[i] + u1[i] * vv[4 + i];
+        }
+      }
+      acc += dpp_f<0xB1>(acc);
+      acc += dpp_f<0x4E>(acc);
+      if (q == 0) sm.dbeta[r] = acc;
     }
   }
   __syncthreads();
 
-  // ---- dq = dq_s + dA_qk K;  dk = dk_s + dA_qk^T Q + (dA_kk + dA_kk^T) K
-  for (int tile = w; tile < NT * KT; tile += 4) {
-    const int rt = tile / KT, kt = tile % KT;
-    const int r = 16 * rt + n;
-    f32x4 aq = zero4(), ak = zero4();
-    for (int sb = 0; sb < NT; ++sb) {
-      f32x4 a1, a2, a3, bk, bq;
+  // ---- operand layouts for dq, dk: K^T and Q^T (bf16, over the dead R / X1),
+  // then dA_qk^T and dA_kk + dA_kk^T (over the dead Q / K rows)
+  if constexpr (STAGE_QK) {
+    constexpr int NB = (C / 4) * (KD / 4);
+    for (int idx = tid; idx < 2 * NB; idx += 256) {
+      const int m = idx / NB, bi = idx % NB;
+      const int rb = bi / (KD / 4), kb = bi % (KD / 4);
+      const T* src = m ? &sm.u1.qk.sQ[0][0] : &sm.u1.qk.sK[0][0];
+      T* dst = m ? &sm.u2.kq.Qt[0][0] : &sm.u2.kq.Kt[0][0];
+      uint2 v[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] = *(const uint2*)(src + (4 * rb + i) * Sm::KP + 4 * kb);
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const int sh = (jj & 1) * 16, wsel = jj >> 1;
+        uint32_t e4[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) e4[i] = ((wsel ? v[i].y : v[i].x) >> sh) & 0xffffu;
+        *(uint2*)(dst + (4 * kb + jj) * Sm::CT + 4 * rb) =
+            make_uint2(e4[0] | (e4[1] << 16), e4[2] | (e4[3] << 16));
+      }
+    }
+    __syncthreads();
+  }
+  {
+    constexpr int NB = (C / 4) * (C / 4);
+    for (int idx = tid; idx < NB; idx += 256) {
+      const int rb = idx / (C / 4), cb4 = idx % (C / 4);
+      f32x4 a[4], p[4], q[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        a[i] = *(const f32x4*)&sm.dM[4 * rb + i][4 * cb4];
+        p[i] = *(const f32x4*)&sm.dT[4 * rb + i][4 * cb4];
+        q[i] = *(const f32x4*)&sm.dT[4 * cb4 + i][4 * rb];
+      }
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        f32x4 at, ds;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          at[i] = a[i][jj];
+          ds[i] = p[jj][i] + q[i][jj];
+        }
+        *(f32x4*)&sm.u1.tr.dMT[4 * cb4 + jj][4 * rb] = at;
+        *(f32x4*)&sm.u1.tr.Dsym[4 * rb + jj][4 * cb4] = ds;
+      }
+    }
+  }
+  __syncthreads();
+
+  // K^T / Q^T fragments: rows 16 kt + n, token columns [16 sb + 4 g, + 4)
+  auto ktf = [&](int kt, int sb) -> F {
+    if constexpr (STAGE_QK) return ld_frag(&sm.u2.kq.Kt[16 * kt + n][16 * sb + 4 * g]);
+    else {
+      f32x4 x;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int sidx = 16 * sb + 4 * g + j;
-        a1[j] = sm.dM[r][sidx];
-        a2[j] = sm.dM[sidx][r];
-        a3[j] = sm.dT[r][sidx] + sm.dT[sidx][r];
-        if constexpr (Sm::STAGE_QK) {
-          bk[j] = Elem<T>::to_f(sm.sK[sidx][16 * kt + n]);
-          bq[j] = Elem<T>::to_f(sm.sQ[sidx][16 * kt + n]);
-        } else {
-          const bool ok = t0 + sidx < s.T;
-          bk[j] = ok ? ld_f(Kg + (size_t)(t0 + sidx) * krs + 16 * kt + n) : 0.f;
-          bq[j] = ok ? ld_f(Qg + (size_t)(t0 + sidx) * krs + 16 * kt + n) : 0.f;
-        }
+        const int r = 16 * sb + 4 * g + j;
+        x[j] = (t0 + r < s.T) ? ld_f(Kg + (size_t)(t0 + r) * krs + 16 * kt + n) : 0.f;
       }
-      mma_fx(aq, a1, bk, tag);
-      mma_fx(ak, a2, bq, tag);
-      mma_fx(ak, a3, bk, tag);
+      return cvt_frag<T>(x);
+    }
+  };
+  auto qtf = [&](int kt, int sb) -> F {
+    if constexpr (STAGE_QK) return ld_frag(&sm.u2.kq.Qt[16 * kt + n][16 * sb + 4 * g]);
+    else {
+      f32x4 x;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int r = 16 * sb + 4 * g + j;
+        x[j] = (t0 + r < s.T) ? ld_f(Qg + (size_t)(t0 + r) * krs + 16 * kt + n) : 0.f;
+      }
+      return cvt_frag<T>(x);
+    }
+  };
+
+  // ---- dq = dq_s + dA_qk K;  dk = dk_s + dA_qk^T Q + (dA_kk + dA_kk^T) K
+  for (int tile = w; tile < NT * KT; tile += 4) {
+    const int rt = tile % NT, kt = tile / NT;
+    float pq[4], pk[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const size_t wo = (size_t)ch * C * KD + (size_t)(16 * rt + 4 * g + j) * KD + 16 * kt + n;
+      pq[j] = bb.dqs[wo];
+      pk[j] = bb.dks[wo];
+    }
+    f32x4 aq = zero4(), ak = zero4();
+    const int r = 16 * rt + n;
+#pragma unroll
+    for (int sb = 0; sb + 1 < NT; sb += 2) {
+      const int c0 = 16 * sb + 4 * g, c1 = c0 + 16;
+      const F bk0 = ktf(kt, sb), bk1 = ktf(kt, sb + 1);
+      const F bq0 = qtf(kt, sb), bq1 = qtf(kt, sb + 1);
+      mma_fx2(aq, *(const f32x4*)&sm.dM[r][c0], *(const f32x4*)&sm.dM[r][c1], bk0, bk1);
+      mma_fx2(ak, *(const f32x4*)&sm.u1.tr.dMT[r][c0], *(const f32x4*)&sm.u1.tr.dMT[r][c1], bq0,
+              bq1);
+      mma_fx2(ak, *(const f32x4*)&sm.u1.tr.Dsym[r][c0], *(const f32x4*)&sm.u1.tr.Dsym[r][c1], bk0,
+              bk1);
+    }
+    if constexpr (NT & 1) {
+      const int sb = NT - 1, c0 = 16 * sb + 4 * g;
+      const F bk0 = ktf(kt, sb), bq0 = qtf(kt, sb);
+      mma_fx(aq, *(const f32x4*)&sm.dM[r][c0], frag_to_f(bk0), tag);
+      mma_fx(ak, *(const f32x4*)&sm.u1.tr.dMT[r][c0], frag_to_f(bq0), tag);
+      mma_fx(ak, *(const f32x4*)&sm.u1.tr.Dsym[r][c0], frag_to_f(bk0), tag);
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int rr = 16 * rt + 4 * g + j;
-      const int t = t0 + rr;
+      const int t = t0 + 16 * rt + 4 * g + j;
       if (t < s.T) {
         const size_t o = (((size_t)b * s.T + t) * s.H + h) * KD + 16 * kt + n;
-        const size_t wo = (size_t)ch * C * KD + (size_t)rr * KD + 16 * kt + n;
-        store_out(dqv, o, aq[j] + bb.dqs[wo], s.out_bf16);
-        store_out(dkv, o, ak[j] + bb.dks[wo], s.out_bf16);
+        store_out(dqv, o, aq[j] + pq[j], s.out_bf16);
+        store_out(dkv, o, ak[j] + pk[j], s.out_bf16);
       }
     }
   }
-  // ---- dv = Tu^T dU = -dW (GDN) or diag(beta) dU (sGLA)
-  for (int idx = tid; idx < C * V; idx += 256) {
-    const int r = idx / V, c = idx % V;
-    const int t = t0 + r;
-    if (t >= s.T) continue;
-    const float val = gdn ? -bb.dW[(size_t)ch * C * V + idx] : sm.beta[r] * dUg[idx];
-    store_out(dvv, (((size_t)b * s.T + t) * s.H + h) * (size_t)V + c, val, s.out_bf16);
+
+  // ---- dv = Tu^T dU = -dW (GDN) or diag(beta) dU (sGLA), 8 values per item
+  {
+    constexpr int IT = (C * 128 / 8 + 255) / 256;
+    const int n8 = V / 8;
+    f32x4 x[IT][2];
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int idx = tid + 256 * it;
+      const int r = idx / n8, c = 8 * (idx % n8);
+      x[it][0] = x[it][1] = zero4();
+      if (idx < C * n8 && t0 + r < s.T) {
+        const float* src = (gdn ? dWg : dUg) + (size_t)r * V + c;
+        x[it][0] = *(const f32x4*)src;
+        x[it][1] = *(const f32x4*)(src + 4);
+      }
+    }
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int idx = tid + 256 * it;
+      const int r = idx / n8, c = 8 * (idx % n8);
+      const int t = t0 + r;
+      if (idx >= C * n8 || t >= s.T) continue;
+      const float sc = gdn ? -1.f : sm.beta[r];
+      store8_out(dvv, (((size_t)b * s.T + t) * s.H + h) * (size_t)V + c, sc * x[it][0],
+                 sc * x[it][1], s.out_bf16);
+    }
   }
 
-  // ---- backward of the decayed Grams R, R' and of the coefficient vectors
+  // ---- backward of the decayed Grams R, R'.  Per slice e (one wave), lane
+  // tiles of (r, c) pairs, c <= r:  d = Gamma_e[r, c] = exp(G_r[e] - G_c[e]),
+  //   aq2[r] = sum_c dR'[r,c] d k2_c,   ak2[r] = sum_c dR[r,c] d k2_c,
+  //   acol[c] = sum_r (dR'[r,c] q2_r + dR[r,c] k2_r) d
+  float* aq2s = &sm.dT[0][0];  // dA_kk is dead: its space holds the three sums
+  float* ak2s = aq2s + C * E;
+  float* acols = ak2s + C * E;
+  __syncthreads();
+  for (int e = w; e < E; e += 4) {
+    float rowq[16], rowk[16], colacc[NT];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) rowq[i] = rowk[i] = 0.f;
+#pragma unroll
+    for (int ct = 0; ct < NT; ++ct) colacc[ct] = 0.f;
+#pragma unroll
+    for (int rt = 0; rt < NT; ++rt) {
+      double Gr[4];
+      float q2r[4], k2r[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int r = 16 * rt + 4 * g + j;
+        Gr[j] = sm.G[r][e];
+        q2r[j] = sm.q2[r][e];
+        k2r[j] = sm.k2[r][e];
+      }
+#pragma unroll
+      for (int ct = 0; ct <= rt; ++ct) {
+        const int c = 16 * ct + n;
+        const double Gc = sm.G[c][e];
+        const float k2c = sm.k2[c][e];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int r = 16 * rt + 4 * g + j;
+          if (c <= r) {
+            const float d = exp_nonpos((float)(Gr[j] - Gc));
+            const float drq = sm.Aqk[r][c] * d;
+            const float drk = (c < r) ? sm.Akk[r][c] * d : 0.f;
+            rowq[4 * rt + j] += drq * k2c;
+            rowk[4 * rt + j] += drk * k2c;
+            colacc[ct] += drq * q2r[j] + drk * k2r[j];
+          }
+        }
+      }
+    }
+    // rows: sum over the 16 lanes of a group; lane n receives row 16 (n / 4) + 4 g + n % 4
+    const float sq = group16_transpose_sum(rowq, n);
+    const float sk = group16_transpose_sum(rowk, n);
+    const int row = 16 * (n >> 2) + 4 * g + (n & 3);
+    if ((n >> 2) < NT) {
+      aq2s[row * E + e] = sq;
+      ak2s[row * E + e] = sk;
+    }
+    // columns: sum over the four groups
+#pragma unroll
+    for (int ct = 0; ct < NT; ++ct) {
+      float x = colacc[ct];
+      x += __shfl_xor(x, 16, 64);
+      x += __shfl_xor(x, 32, 64);
+      if (g == 0) acols[(16 * ct + n) * E + e] = x;
+    }
+  }
+  __syncthreads();
+
+  // ---- per (r, e): Gram terms and the coefficient vectors
+  //   a = k2 gamma, b = q2 gamma, c = k2 gamma^C / gamma
   for (int idx = tid; idx < C * E; idx += 256) {
     const int r = idx / E, e = idx % E;
-    float aq2 = 0.f, ak2 = 0.f, grow = 0.f;
-    for (int c = 0; c <= r; ++c) {
-      const float d = exp_nonpos((float)(sm.G[r][e] - sm.G[c][e]));
-      const float drq = sm.Aqk[r][c] * d;
-      const float drk = (c < r) ? sm.Akk[r][c] * d : 0.f;
-      aq2 += drq * sm.k2[c][e];
-      ak2 += drk * sm.k2[c][e];
-      grow += (drq * sm.q2[r][e] + drk * sm.k2[r][e]) * sm.k2[c][e];
-    }
-    float acol = 0.f, gcol = 0.f;
-    for (int rr = r; rr < C; ++rr) {  // r as the column index s
-      const float d = exp_nonpos((float)(sm.G[rr][e] - sm.G[r][e]));
-      const float drq = sm.Aqk[rr][r] * d;
-      const float drk = (rr > r) ? sm.Akk[rr][r] * d : 0.f;
-      const float t2 = drq * sm.q2[rr][e] + drk * sm.k2[rr][e];
-      acol += t2;
-      gcol += t2 * sm.k2[r][e];
-    }
-    const float* dcf = bb.dcoef + (size_t)ch * 3 * E * C;
+    const float aq2 = aq2s[idx], ak2 = ak2s[idx], acol = acols[idx];
+    const float q2 = sm.q2[r][e], k2 = sm.k2[r][e];
     const float da = dcf[(0 * E + e) * C + r], db = dcf[(1 * E + e) * C + r],
                 dc = dcf[(2 * E + e) * C + r];
     const double G = sm.G[r][e], GC = sm.G[C - 1][e];
     const float gm = exp_nonpos((float)G), gt = exp_nonpos((float)(GC - G));
-    // coefficient vectors a = k2 gamma, b = q2 gamma, c = k2 gamma^C / gamma
-    sm.dG[r][e] = grow - gcol + da * sm.k2[r][e] * gm + db * sm.q2[r][e] * gm -
-                  dc * sm.k2[r][e] * gt;
+    sm.dG[r][e] = (q2 * aq2 + k2 * ak2) - acol * k2 + da * k2 * gm + db * q2 * gm - dc * k2 * gt;
+    acols[idx] = dc * k2 * gt;  // this row's share of dG at the chunk end
     const int t = t0 + r;
     if (t < s.T) {
       const size_t o = eoff + (size_t)t * erow + e;
@@ -1000,27 +1271,20 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
     }
   }
   __syncthreads();
-  if (tid < E) {
-    const int e = tid;
-    const float* dcf = bb.dcoef + (size_t)ch * 3 * E * C;
-    const double GC = sm.G[C - 1][e];
-    float acc = 0.f;
-    for (int r = 0; r < C; ++r)
-      acc += dcf[(2 * E + e) * C + r] * sm.k2[r][e] * exp_nonpos((float)(GC - sm.G[r][e]));
-    sm.dG[C - 1][e] += acc + exp_nonpos((float)GC) * bb.dgC[(size_t)ch * E4 + e];
-    // reverse cumulative sum within the chunk: dg_j = sum_{r >= j} dG_r
-    float run = 0.f;
-    for (int r = C - 1; r >= 0; --r) {
-      run += sm.dG[r][e];
-      sm.dG[r][e] = run;
+  // dG at the chunk end gains sum_r dc c + gamma^C dgamma^C; then dg_j = sum_{r >= j} dG_r
+  // (one wave per slice, lane r holds row r)
+  for (int e = w; e < E; e += 4) {
+    const float tail = wave_sum(l < C ? acols[l * E + e] : 0.f);
+    float x = (l < C) ? sm.dG[l][e] : 0.f;
+    if (l == C - 1)
+      x += tail + exp_nonpos((float)sm.G[C - 1][e]) * bb.dgC[(size_t)ch * E4 + e];
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const float y = __shfl_down(x, off, 64);
+      if (l + off < 64) x += y;
     }
-  }
-  __syncthreads();
-  for (int idx = tid; idx < C * E; idx += 256) {
-    const int r = idx / E, e = idx % E;
-    const int t = t0 + r;
-    if (t >= s.T) continue;
-    dg[eoff + (size_t)t * erow + e] = sm.dG[r][e];
+    const int t = t0 + l;
+    if (l < C && t < s.T) dg[eoff + (size_t)t * erow + e] = x;
   }
   if (dbeta && tid < C) {
     const int t = t0 + tid;
