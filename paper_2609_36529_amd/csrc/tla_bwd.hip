@@ -71,7 +71,7 @@ __device__ __forceinline__ void bmma_k(f32x4& acc, FA fa, FB fb) {
   if constexpr (NB & 1) mma16(acc, fa(NB - 1), fb(NB - 1));
 }
 
-template <int E> constexpr int bwd_waves() { return E >= 16 ? 8 : 4; }
+template <int E> constexpr int bwd_waves() { return E >= 8 ? 8 : 4; }
 
 // ============================================================ reverse recurrence
 template <typename T, int KD, int C, int E, int NW>
@@ -97,6 +97,201 @@ struct RecSmem {
   alignas(16) f32x4 X[NW][NT][64];  // per-wave partials of sum_e diag(c_e) K dS'_e
 };
 
+// Register staging of one chunk's inputs for the reverse recurrence: the
+// global loads for chunk ci - 1 are issued while chunk ci is computed, and
+// written to LDS (with the transposed copies) at the top of the next step.
+// K and Q are moved in blocks of 4 rows x KW columns, M and Tu in blocks of
+// 4 rows x MW columns; eight-wave workgroups use the narrower blocks so that
+// every thread holds a share and the registers per lane stay low.
+template <int N>
+__device__ __forceinline__ void ld_words(uint32_t (&w)[N], const void* src) {
+  if constexpr (N % 4 == 0) {
+#pragma unroll
+    for (int i = 0; i < N / 4; ++i) {
+      const uint4 x = ((const uint4*)src)[i];
+      w[4 * i] = x.x;
+      w[4 * i + 1] = x.y;
+      w[4 * i + 2] = x.z;
+      w[4 * i + 3] = x.w;
+    }
+  } else {
+    static_assert(N == 2, "word count");
+    const uint2 x = *(const uint2*)src;
+    w[0] = x.x;
+    w[1] = x.y;
+  }
+}
+template <typename T, int N>
+__device__ __forceinline__ T word_elem(const uint32_t (&w)[N], int i) {
+  if constexpr (sizeof(T) == 2) return (T)((i & 1) ? (w[i >> 1] >> 16) : (w[i >> 1] & 0xffffu));
+  else return __uint_as_float(w[i]);
+}
+
+template <typename T, int KD, int C, int E, int NTHR>
+struct RecStage {
+  static constexpr int KW = NTHR >= 512 ? 4 : 8;
+  static constexpr int MW = NTHR >= 512 ? 2 : 4;
+  static constexpr int RB = C / 4;
+  static constexpr int KCB = KD / KW, MCB = C / MW;
+  static constexpr int KWD = KW * (int)sizeof(T) / 4;          // words per block row
+  static constexpr int NKB = (RB * KCB + NTHR - 1) / NTHR;
+  static constexpr int NDB = (RB * 4 + NTHR - 1) / NTHR;       // 4 x 4 blocks of the dO tile
+  static constexpr int NMB = (RB * MCB + NTHR - 1) / NTHR;
+  static constexpr int NCB = (3 * E * C / 4 + NTHR - 1) / NTHR;
+  static constexpr int E4 = (E + 3) & ~3;
+  static constexpr int DW = sizeof(T) == 2 ? 2 : 4;            // words per 4 elements
+  uint32_t k[NKB][4][KWD], q[NKB][4][KWD];
+  uint32_t d[NDB][4][DW];
+  float m[NMB][4][MW], tu[NMB][4][MW];
+  f32x4 c[NCB];
+  float gc;
+
+  // Every load is unconditional: a row past T is read from row T - 1 and a
+  // block index past the end from the last block, and store() zeroes or
+  // skips them.  (A per-lane branch around a load would make the compiler
+  // wait for the load right away, which defeats the prefetch.)
+  __device__ __forceinline__ void load(const Shape& s, const PrepBufs& p, const T* Kg,
+                                       const T* Qg, const T* dOg, size_t ch, int ci) {
+    const int tid = threadIdx.x;
+    const int t0 = ci * C;
+    const size_t krs = (size_t)s.H * KD, vrs = (size_t)s.H * s.V;
+#pragma unroll
+    for (int i = 0; i < NKB; ++i) {
+      const int blk = min(tid + i * NTHR, RB * KCB - 1);
+      const int rb = blk % RB, cb = blk / RB;
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        const int t = min(t0 + 4 * rb + rr, s.T - 1);
+        ld_words(k[i][rr], Kg + (size_t)t * krs + KW * cb);
+        ld_words(q[i][rr], Qg + (size_t)t * krs + KW * cb);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < NDB; ++i) {
+      const int blk = min(tid + i * NTHR, RB * 4 - 1);
+      const int rb = blk % RB, c4 = blk / RB;
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        const int t = min(t0 + 4 * rb + rr, s.T - 1);
+        ld_words(d[i][rr], dOg + (size_t)t * vrs + 4 * c4);
+      }
+    }
+    const float* Mg = p.M + ch * C * C;
+    const float* Tg = p.Tu + ch * C * C;
+#pragma unroll
+    for (int i = 0; i < NMB; ++i) {
+      const int blk = min(tid + i * NTHR, RB * MCB - 1);
+      const int rb = blk % RB, cb = blk / RB;
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        const size_t off = (size_t)(4 * rb + rr) * C + MW * cb;
+        if constexpr (MW == 4) {
+          const f32x4 x = *(const f32x4*)(Mg + off);
+          const f32x4 y = *(const f32x4*)(Tg + off);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            m[i][rr][j] = x[j];
+            tu[i][rr][j] = y[j];
+          }
+        } else {
+          const float2 x = *(const float2*)(Mg + off);
+          const float2 y = *(const float2*)(Tg + off);
+          m[i][rr][0] = x.x;
+          m[i][rr][1] = x.y;
+          tu[i][rr][0] = y.x;
+          tu[i][rr][1] = y.y;
+        }
+      }
+    }
+    const float* cg = p.coef + ch * 3 * E * C;
+#pragma unroll
+    for (int i = 0; i < NCB; ++i) c[i] = *(const f32x4*)(cg + 4 * min(tid + i * NTHR, 3 * E * C / 4 - 1));
+    gc = p.gC[ch * E4 + min(tid, E4 - 1)];
+  }
+
+  template <typename Sm>
+  __device__ __forceinline__ void store(Sm& sm, int variant, int t0, int nT) const {
+    typedef typename Elem<T>::frag F;
+    const int tid = threadIdx.x;
+#pragma unroll
+    for (int i = 0; i < NKB; ++i) {
+      const int blk = tid + i * NTHR;
+      const int rb = blk % RB, cb = blk / RB;
+      if (blk < RB * KCB) {
+        uint32_t kk[4][KWD], qq[4][KWD];
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) {
+          const bool ok = t0 + 4 * rb + rr < nT;
+#pragma unroll
+          for (int j = 0; j < KWD; ++j) {
+            kk[rr][j] = ok ? k[i][rr][j] : 0u;
+            qq[rr][j] = ok ? q[i][rr][j] : 0u;
+          }
+        }
+        if constexpr (Sm::STAGE_K) {
+#pragma unroll
+          for (int rr = 0; rr < 4; ++rr)
+#pragma unroll
+            for (int j = 0; j < KWD; j += 2)
+              *(uint2*)((uint32_t*)&sm.K[4 * rb + rr][KW * cb] + j) =
+                  make_uint2(kk[rr][j], kk[rr][j + 1]);
+        }
+#pragma unroll
+        for (int cc = 0; cc < KW; ++cc) {
+          lds_put4(&sm.Kt[KW * cb + cc][4 * rb], word_elem<T>(kk[0], cc), word_elem<T>(kk[1], cc),
+                   word_elem<T>(kk[2], cc), word_elem<T>(kk[3], cc));
+          lds_put4(&sm.Qt[KW * cb + cc][4 * rb], word_elem<T>(qq[0], cc), word_elem<T>(qq[1], cc),
+                   word_elem<T>(qq[2], cc), word_elem<T>(qq[3], cc));
+        }
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < NDB; ++i) {
+      const int blk = tid + i * NTHR;
+      const int rb = blk % RB, c4 = blk / RB;
+      if (blk < RB * 4) {
+        uint32_t dd[4][DW];
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) {
+          const bool ok = t0 + 4 * rb + rr < nT;
+#pragma unroll
+          for (int j = 0; j < DW; ++j) dd[rr][j] = ok ? d[i][rr][j] : 0u;
+        }
+#pragma unroll
+        for (int cc = 0; cc < 4; ++cc)
+          lds_put4(&sm.dOt[4 * c4 + cc][4 * rb], word_elem<T>(dd[0], cc), word_elem<T>(dd[1], cc),
+                   word_elem<T>(dd[2], cc), word_elem<T>(dd[3], cc));
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < NMB; ++i) {
+      const int blk = tid + i * NTHR;
+      const int rb = blk % RB, cb = blk / RB;
+      if (blk < RB * MCB) {
+#pragma unroll
+        for (int cc = 0; cc < MW; ++cc) {
+          F h, lw;
+          split_frag(f32x4{m[i][0][cc], m[i][1][cc], m[i][2][cc], m[i][3][cc]}, h, lw);
+          *(F*)&sm.MT[MW * cb + cc][4 * rb] = h;
+          if constexpr (Sm::SPLIT) *(F*)&sm.MTL[MW * cb + cc][4 * rb] = lw;
+          if (variant == 1) {
+            split_frag(f32x4{tu[i][0][cc], tu[i][1][cc], tu[i][2][cc], tu[i][3][cc]}, h, lw);
+            *(F*)&sm.TuT[MW * cb + cc][4 * rb] = h;
+            if constexpr (Sm::SPLIT) *(F*)&sm.TuTL[MW * cb + cc][4 * rb] = lw;
+          }
+        }
+      }
+    }
+    float* cs = &sm.coef[0][0][0];
+#pragma unroll
+    for (int i = 0; i < NCB; ++i) {
+      const int idx = tid + i * NTHR;
+      if (idx < 3 * E * C / 4) *(f32x4*)(cs + 4 * idx) = c[i];
+    }
+    if (tid < E4) sm.gC[tid] = gc;
+  }
+};
+
 template <typename T, int KD, int C, int E, int NW>
 __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const void* dOv,
                                                      const float* dS_final, PrepBufs p,
@@ -108,6 +303,10 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
   constexpr int E4 = (E + 3) & ~3;
   typedef typename Elem<T>::frag F;
   typedef RecSmem<T, KD, C, E, NW> Sm;
+  // eight-wave instances (E = 16) have half the registers per lane: they load
+  // each chunk's inputs at its own start instead of one chunk ahead, and
+  // reuse operand fragments over fewer slices at a time
+  constexpr bool PREFETCH = SPW == 1 || NW <= 4;
   extern __shared__ __align__(16) unsigned char smem_raw[];
   Sm& sm = *reinterpret_cast<Sm*>(smem_raw);
 
@@ -141,73 +340,81 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
   const size_t krs = (size_t)s.H * KD;
   const size_t vrs = (size_t)s.H * V;
 
+  RecStage<T, KD, C, E, NTHR> stage;
+  if constexpr (PREFETCH) stage.load(s, p, Kg, Qg, dOg, (size_t)head * s.Nc + s.Nc - 1, s.Nc - 1);
   for (int ci = s.Nc - 1; ci >= 0; --ci) {
     const int t0 = ci * C;
     const size_t ch = (size_t)head * s.Nc + ci;
     __syncthreads();
-    // ---- stage: K rows, K^T, Q^T, dO tile^T, M^T, Tu^T (split), coefficients
-    constexpr int RB = C / 4, CB = KD / 8;
-    for (int blk = tid; blk < RB * CB; blk += NTHR) {
-      const int rb = blk % RB, cb = blk / RB;
-      T kv[4][8], qv[4][8];
+    // ---- this chunk's inputs to LDS; the next chunk's loads go in flight
+    if constexpr (PREFETCH) {
+      stage.store(sm, s.variant, t0, s.T);
+      if (ci > 0) stage.load(s, p, Kg, Qg, dOg, ch - 1, ci - 1);
+    } else {
+      // ---- stage: K rows, K^T, Q^T, dO tile^T, M^T, Tu^T (split), coefficients
+      constexpr int RB = C / 4, CB = KD / 8;
+      for (int blk = tid; blk < RB * CB; blk += NTHR) {
+        const int rb = blk % RB, cb = blk / RB;
+        T kv[4][8], qv[4][8];
 #pragma unroll
-      for (int rr = 0; rr < 4; ++rr) {
-        const int t = t0 + 4 * rb + rr;
-        if (t < s.T) {
-          bcopy8(kv[rr], Kg + (size_t)t * krs + 8 * cb);
-          bcopy8(qv[rr], Qg + (size_t)t * krs + 8 * cb);
-        } else {
-          bzero8(kv[rr]);
-          bzero8(qv[rr]);
+        for (int rr = 0; rr < 4; ++rr) {
+          const int t = t0 + 4 * rb + rr;
+          if (t < s.T) {
+            bcopy8(kv[rr], Kg + (size_t)t * krs + 8 * cb);
+            bcopy8(qv[rr], Qg + (size_t)t * krs + 8 * cb);
+          } else {
+            bzero8(kv[rr]);
+            bzero8(qv[rr]);
+          }
+        }
+        if constexpr (Sm::STAGE_K) {
+#pragma unroll
+          for (int rr = 0; rr < 4; ++rr) lds_put8(&sm.K[4 * rb + rr][8 * cb], kv[rr]);
+        }
+#pragma unroll
+        for (int cc = 0; cc < 8; ++cc) {
+          lds_put4(&sm.Kt[8 * cb + cc][4 * rb], kv[0][cc], kv[1][cc], kv[2][cc], kv[3][cc]);
+          lds_put4(&sm.Qt[8 * cb + cc][4 * rb], qv[0][cc], qv[1][cc], qv[2][cc], qv[3][cc]);
         }
       }
-      if constexpr (Sm::STAGE_K) {
+      for (int idx = tid; idx < (C / 4) * 16; idx += NTHR) {  // 4 rows x 1 column per thread
+        const int rb = idx % (C / 4), col = idx / (C / 4);
+        T x[4];
 #pragma unroll
-        for (int rr = 0; rr < 4; ++rr) lds_put8(&sm.K[4 * rb + rr][8 * cb], kv[rr]);
-      }
-#pragma unroll
-      for (int cc = 0; cc < 8; ++cc) {
-        lds_put4(&sm.Kt[8 * cb + cc][4 * rb], kv[0][cc], kv[1][cc], kv[2][cc], kv[3][cc]);
-        lds_put4(&sm.Qt[8 * cb + cc][4 * rb], qv[0][cc], qv[1][cc], qv[2][cc], qv[3][cc]);
-      }
-    }
-    for (int idx = tid; idx < (C / 4) * 16; idx += NTHR) {  // 4 rows x 1 column per thread
-      const int rb = idx % (C / 4), col = idx / (C / 4);
-      T x[4];
-#pragma unroll
-      for (int rr = 0; rr < 4; ++rr) {
-        const int t = t0 + 4 * rb + rr;
-        x[rr] = (t < s.T) ? dOg[(size_t)t * vrs + col] : T(0);
-      }
-      lds_put4(&sm.dOt[col][4 * rb], x[0], x[1], x[2], x[3]);
-    }
-    {
-      // M^T and Tu^T (hi / lo) from 4x4 blocks: 4 row loads, 4 column stores
-      const float* Mg = p.M + ch * C * C;
-      const float* Tg = p.Tu + ch * C * C;
-      auto put_t = [&](const float* src, T (*hi)[Sm::CP], T (*lo)[Sm::CP], int rb, int cb) {
-        f32x4 x[4];
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr) x[rr] = *(const f32x4*)(src + (4 * rb + rr) * C + 4 * cb);
-#pragma unroll
-        for (int cc = 0; cc < 4; ++cc) {
-          const f32x4 col{x[0][cc], x[1][cc], x[2][cc], x[3][cc]};
-          F h, lw;
-          split_frag(col, h, lw);
-          *(F*)&hi[4 * cb + cc][4 * rb] = h;
-          if constexpr (Sm::SPLIT) *(F*)&lo[4 * cb + cc][4 * rb] = lw;
+        for (int rr = 0; rr < 4; ++rr) {
+          const int t = t0 + 4 * rb + rr;
+          x[rr] = (t < s.T) ? dOg[(size_t)t * vrs + col] : T(0);
         }
-      };
-      for (int idx = tid; idx < (C / 4) * (C / 4); idx += NTHR) {
-        const int rb = idx % (C / 4), cb = idx / (C / 4);
-        put_t(Mg, sm.MT, sm.MTL, rb, cb);
-        if (s.variant == 1) put_t(Tg, sm.TuT, sm.TuTL, rb, cb);
+        lds_put4(&sm.dOt[col][4 * rb], x[0], x[1], x[2], x[3]);
       }
-      const float* cg = p.coef + ch * 3 * E * C;
-      float* cs = &sm.coef[0][0][0];
-      for (int idx = tid; idx < 3 * E * C / 4; idx += NTHR)
-        ((float4*)cs)[idx] = ((const float4*)cg)[idx];
-      if (tid < E4) sm.gC[tid] = p.gC[ch * E4 + tid];
+      {
+        // M^T and Tu^T (hi / lo) from 4x4 blocks: 4 row loads, 4 column stores
+        const float* Mg = p.M + ch * C * C;
+        const float* Tg = p.Tu + ch * C * C;
+        auto put_t = [&](const float* src, T (*hi)[Sm::CP], T (*lo)[Sm::CP], int rb, int cb) {
+          f32x4 x[4];
+#pragma unroll
+          for (int rr = 0; rr < 4; ++rr) x[rr] = *(const f32x4*)(src + (4 * rb + rr) * C + 4 * cb);
+#pragma unroll
+          for (int cc = 0; cc < 4; ++cc) {
+            const f32x4 col{x[0][cc], x[1][cc], x[2][cc], x[3][cc]};
+            F h, lw;
+            split_frag(col, h, lw);
+            *(F*)&hi[4 * cb + cc][4 * rb] = h;
+            if constexpr (Sm::SPLIT) *(F*)&lo[4 * cb + cc][4 * rb] = lw;
+          }
+        };
+        for (int idx = tid; idx < (C / 4) * (C / 4); idx += NTHR) {
+          const int rb = idx % (C / 4), cb = idx / (C / 4);
+          put_t(Mg, sm.MT, sm.MTL, rb, cb);
+          if (s.variant == 1) put_t(Tg, sm.TuT, sm.TuTL, rb, cb);
+        }
+        const float* cg = p.coef + ch * 3 * E * C;
+        float* cs = &sm.coef[0][0][0];
+        for (int idx = tid; idx < 3 * E * C / 4; idx += NTHR)
+          ((float4*)cs)[idx] = ((const float4*)cg)[idx];
+        if (tid < E4) sm.gC[tid] = p.gC[ch * E4 + tid];
+      }
     }
     __syncthreads();
 
@@ -230,9 +437,9 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
     for (int i = 0; i < SPW; ++i)
 #pragma unroll
       for (int kt = 0; kt < KT; ++kt) dSop[i][kt] = cvt_frag<T>(dS[i][kt]);
+    // (K fragments are read once per key block and reused for every owned slice)
 #pragma unroll
     for (int rt = 0; rt < NT; ++rt) {
-      f32x4 acc = zero4();
       const int r = 16 * rt + n;
       const bool kok = t0 + r < s.T;
       const T* krow = Kg + (size_t)(kok ? t0 + r : 0) * krs;
@@ -240,13 +447,31 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
         if constexpr (Sm::STAGE_K) return ld_frag(&sm.K[r][16 * kb + 4 * g]);
         else return kok ? ld_frag(krow + 16 * kb + 4 * g) : cvt_frag<T>(zero4());
       };
+      constexpr int GZ = PREFETCH ? SPW : 1;  // slices per pass over the K fragments
+      f32x4 z[SPW];
+#pragma unroll
+      for (int i = 0; i < SPW; ++i) z[i] = zero4();
+#pragma unroll
+      for (int i0 = 0; i0 < SPW; i0 += GZ) {
+#pragma unroll
+        for (int kb = 0; kb + 1 < KT; kb += 2) {
+          const F k0 = kfrag(kb), k1 = kfrag(kb + 1);
+#pragma unroll
+          for (int i = i0; i < i0 + GZ; ++i)
+            if (w * SPW + i < E) mma32(z[i], k0, k1, dSop[i][kb], dSop[i][kb + 1]);
+        }
+        if constexpr (KT & 1) {
+          const F k0 = kfrag(KT - 1);
+#pragma unroll
+          for (int i = i0; i < i0 + GZ; ++i)
+            if (w * SPW + i < E) mma16(z[i], k0, dSop[i][KT - 1]);
+        }
+      }
+      f32x4 acc = zero4();
 #pragma unroll
       for (int i = 0; i < SPW; ++i) {
         const int e = w * SPW + i;
-        if (e >= E) continue;
-        f32x4 z = zero4();
-        bmma_k<KD>(z, kfrag, [&](int kb) { return dSop[i][kb]; });
-        acc += *(const f32x4*)&sm.coef[2][e][16 * rt + 4 * g] * z;
+        if (e < E) acc += *(const f32x4*)&sm.coef[2][e][16 * rt + 4 * g] * z[i];
       }
       sm.X[w][rt][l] = acc;
     }
@@ -298,31 +523,72 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
     }
 
     // ---- dS_e <- gamma^C_e dS'_e + Q^T diag(b_e) dO + K^T diag(a_e) dW
+    // (B operands of a group of owned slices first; each Q^T / K^T fragment is
+    // read once per group; four-wave instances take all owned slices at once)
+    constexpr int GS = PREFETCH ? SPW : 1;
+    const bool gdn = s.variant == 1;
 #pragma unroll
-    for (int i = 0; i < SPW; ++i) {
-      const int e = w * SPW + i;
-      if (e >= E) continue;
-      const float gc = sm.gC[e];
-      F bh[NT], bl[NT], ah[NT], al[NT];
+    for (int i0 = 0; i0 < SPW; i0 += GS) {
+      F bh[GS][NT], bl[GS][NT], ah[GS][NT], al[GS][NT];
+      float gcs[GS];
 #pragma unroll
-      for (int kb = 0; kb < NT; ++kb) {
-        const f32x4 dov = ld4_f(&sm.dOt[n][16 * kb + 4 * g]);
-        split_frag(dov * *(const f32x4*)&sm.coef[1][e][16 * kb + 4 * g], bh[kb], bl[kb]);
-        split_frag(dW[kb] * *(const f32x4*)&sm.coef[0][e][16 * kb + 4 * g], ah[kb], al[kb]);
+      for (int ii = 0; ii < GS; ++ii) {
+        const int e = w * SPW + i0 + ii;
+        if (e >= E) continue;
+        gcs[ii] = sm.gC[e];
+#pragma unroll
+        for (int kb = 0; kb < NT; ++kb) {
+          const f32x4 dov = ld4_f(&sm.dOt[n][16 * kb + 4 * g]);
+          split_frag(dov * *(const f32x4*)&sm.coef[1][e][16 * kb + 4 * g], bh[ii][kb], bl[ii][kb]);
+          split_frag(dW[kb] * *(const f32x4*)&sm.coef[0][e][16 * kb + 4 * g], ah[ii][kb],
+                     al[ii][kb]);
+        }
       }
 #pragma unroll
       for (int kt = 0; kt < KT; ++kt) {
-        f32x4 acc = dS[i][kt] * gc;
         const int r = 16 * kt + n;
-        auto qf = [&](int kb) { return ld_frag(&sm.Qt[r][16 * kb + 4 * g]); };
-        auto kf = [&](int kb) { return ld_frag(&sm.Kt[r][16 * kb + 4 * g]); };
-        bmma_k<C>(acc, qf, [&](int kb) { return bh[kb]; });
-        if constexpr (Sm::SPLIT) bmma_k<C>(acc, qf, [&](int kb) { return bl[kb]; });
-        if (s.variant == 1) {
-          bmma_k<C>(acc, kf, [&](int kb) { return ah[kb]; });
-          if constexpr (Sm::SPLIT) bmma_k<C>(acc, kf, [&](int kb) { return al[kb]; });
+        f32x4 acc[GS];
+#pragma unroll
+        for (int ii = 0; ii < GS; ++ii) acc[ii] = dS[i0 + ii][kt] * gcs[ii];
+#pragma unroll
+        for (int kb = 0; kb + 1 < NT; kb += 2) {
+          const F q0 = ld_frag(&sm.Qt[r][16 * kb + 4 * g]);
+          const F q1 = ld_frag(&sm.Qt[r][16 * kb + 16 + 4 * g]);
+          F k0, k1;
+          if (gdn) {
+            k0 = ld_frag(&sm.Kt[r][16 * kb + 4 * g]);
+            k1 = ld_frag(&sm.Kt[r][16 * kb + 16 + 4 * g]);
+          }
+#pragma unroll
+          for (int ii = 0; ii < GS; ++ii) {
+            if (w * SPW + i0 + ii >= E) continue;
+            mma32(acc[ii], q0, q1, bh[ii][kb], bh[ii][kb + 1]);
+            if constexpr (Sm::SPLIT) mma32(acc[ii], q0, q1, bl[ii][kb], bl[ii][kb + 1]);
+            if (gdn) {
+              mma32(acc[ii], k0, k1, ah[ii][kb], ah[ii][kb + 1]);
+              if constexpr (Sm::SPLIT) mma32(acc[ii], k0, k1, al[ii][kb], al[ii][kb + 1]);
+            }
+          }
         }
-        dS[i][kt] = acc;
+        if constexpr (NT & 1) {
+          const int kb = NT - 1;
+          const F q0 = ld_frag(&sm.Qt[r][16 * kb + 4 * g]);
+          F k0;
+          if (gdn) k0 = ld_frag(&sm.Kt[r][16 * kb + 4 * g]);
+#pragma unroll
+          for (int ii = 0; ii < GS; ++ii) {
+            if (w * SPW + i0 + ii >= E) continue;
+            mma16(acc[ii], q0, bh[ii][kb]);
+            if constexpr (Sm::SPLIT) mma16(acc[ii], q0, bl[ii][kb]);
+            if (gdn) {
+              mma16(acc[ii], k0, ah[ii][kb]);
+              if constexpr (Sm::SPLIT) mma16(acc[ii], k0, al[ii][kb]);
+            }
+          }
+        }
+#pragma unroll
+        for (int ii = 0; ii < GS; ++ii)
+          if (w * SPW + i0 + ii < E) dS[i0 + ii][kt] = acc[ii];
       }
     }
   }
