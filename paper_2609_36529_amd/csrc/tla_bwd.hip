@@ -103,30 +103,6 @@ struct RecSmem {
 // K and Q are moved in blocks of 4 rows x KW columns, M and Tu in blocks of
 // 4 rows x MW columns; eight-wave workgroups use the narrower blocks so that
 // every thread holds a share and the registers per lane stay low.
-template <int N>
-__device__ __forceinline__ void ld_words(uint32_t (&w)[N], const void* src) {
-  if constexpr (N % 4 == 0) {
-#pragma unroll
-    for (int i = 0; i < N / 4; ++i) {
-      const uint4 x = ((const uint4*)src)[i];
-      w[4 * i] = x.x;
-      w[4 * i + 1] = x.y;
-      w[4 * i + 2] = x.z;
-      w[4 * i + 3] = x.w;
-    }
-  } else {
-    static_assert(N == 2, "word count");
-    const uint2 x = *(const uint2*)src;
-    w[0] = x.x;
-    w[1] = x.y;
-  }
-}
-template <typename T, int N>
-__device__ __forceinline__ T word_elem(const uint32_t (&w)[N], int i) {
-  if constexpr (sizeof(T) == 2) return (T)((i & 1) ? (w[i >> 1] >> 16) : (w[i >> 1] & 0xffffu));
-  else return __uint_as_float(w[i]);
-}
-
 template <typename T, int KD, int C, int E, int NTHR>
 struct RecStage {
   static constexpr int KW = NTHR >= 512 ? 4 : 8;

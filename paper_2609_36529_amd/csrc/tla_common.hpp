@@ -276,6 +276,32 @@ __device__ __forceinline__ void lds_put_raw8(T* dst, const Raw8<T>& r) {
   }
 }
 
+// Loads of N consecutive 32-bit words (16- or 8-byte accesses) and element
+// access into such words.
+template <int N>
+__device__ __forceinline__ void ld_words(uint32_t (&w)[N], const void* src) {
+  if constexpr (N % 4 == 0) {
+#pragma unroll
+    for (int i = 0; i < N / 4; ++i) {
+      const uint4 x = ((const uint4*)src)[i];
+      w[4 * i] = x.x;
+      w[4 * i + 1] = x.y;
+      w[4 * i + 2] = x.z;
+      w[4 * i + 3] = x.w;
+    }
+  } else {
+    static_assert(N == 2, "word count");
+    const uint2 x = *(const uint2*)src;
+    w[0] = x.x;
+    w[1] = x.y;
+  }
+}
+template <typename T, int N>
+__device__ __forceinline__ T word_elem(const uint32_t (&w)[N], int i) {
+  if constexpr (sizeof(T) == 2) return (T)((i & 1) ? (w[i >> 1] >> 16) : (w[i >> 1] & 0xffffu));
+  else return __uint_as_float(w[i]);
+}
+
 // 32-deep MFMA step on raw 8-element operands: lane (g, n) holds the
 // contraction indices 8g .. 8g + 7 of row n of A and of column n of B (any
 // assignment of the 32 indices to lanes works as long as A and B agree).

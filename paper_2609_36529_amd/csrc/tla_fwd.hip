@@ -210,18 +210,26 @@ struct FwdSmem {
 // memory (including the transposed copies) at the top of the next chunk.
 template <typename T, int KD, int C, int E, int NTHR, bool STAGE_Q, bool SPLIT>
 struct FwdStage {
-  static constexpr int RB = C / 4, CB = KD / 8;
-  static constexpr int NKB = (RB * CB + NTHR - 1) / NTHR;  // 4x8 blocks of K (and Q)
+  // K and Q move in blocks of 4 rows x KW columns (narrower for eight-wave
+  // workgroups, so that every thread holds a share)
+  static constexpr int KW = NTHR >= 512 ? 4 : 8;
+  static constexpr int KWD = KW * (int)sizeof(T) / 4;  // words per block row
+  static constexpr int RB = C / 4, CB = KD / KW;
+  static constexpr int NKB = (RB * CB + NTHR - 1) / NTHR;
   static constexpr int NV4 = (C * 4 + NTHR - 1) / NTHR;    // 4-element pieces of the V tile
   static constexpr int NMB = (C * C / 4 + NTHR - 1) / NTHR;
   static constexpr int NCB = (3 * E * C / 4 + NTHR - 1) / NTHR;
   static constexpr int E4 = (E + 3) & ~3;
-  Raw8<T> k[NKB][4];
-  Raw8<T> q[STAGE_Q ? NKB : 1][4];
+  uint32_t k[NKB][4][KWD];
+  uint32_t q[STAGE_Q ? NKB : 1][4][KWD];
   uint32_t v[NV4][sizeof(T) == 2 ? 2 : 4];  // 4 elements as raw words
   f32x4 m[NMB], tu[NMB], c[NCB];
   float gc, beta;
 
+  // Every load is unconditional (a row past T is read from row T - 1, an
+  // index past the end from the last element) and store() zeroes or skips
+  // what is out of range: a per-lane branch around a load would make the
+  // compiler wait for it at once, which defeats the prefetch.
   __device__ __forceinline__ void load(const Shape& s, const FwdIn& in, const PrepBufs& p,
                                        const T* Kg, const T* Qg, const T* Vg, int b, int h,
                                        int ci) {
@@ -231,63 +239,50 @@ struct FwdStage {
     const size_t krs = (size_t)s.H * KD, vrs = (size_t)s.H * s.V;
 #pragma unroll
     for (int i = 0; i < NKB; ++i) {
-      const int blk = tid + i * NTHR;
+      const int blk = min(tid + i * NTHR, RB * CB - 1);
       const int rb = blk % RB, cb = blk / RB;
-      if (blk < RB * CB) {
 #pragma unroll
-        for (int rr = 0; rr < 4; ++rr) {
-          const int t = t0 + 4 * rb + rr;
-          k[i][rr] = (t < s.T) ? load8(Kg + (size_t)t * krs + 8 * cb) : zero_raw8<T>();
-          if constexpr (STAGE_Q)
-            q[i][rr] = (t < s.T) ? load8(Qg + (size_t)t * krs + 8 * cb) : zero_raw8<T>();
-        }
+      for (int rr = 0; rr < 4; ++rr) {
+        const int t = min(t0 + 4 * rb + rr, s.T - 1);
+        ld_words(k[i][rr], Kg + (size_t)t * krs + KW * cb);
+        if constexpr (STAGE_Q) ld_words(q[i][rr], Qg + (size_t)t * krs + KW * cb);
       }
     }
 #pragma unroll
     for (int i = 0; i < NV4; ++i) {
-      const int idx = tid + i * NTHR;
+      const int idx = min(tid + i * NTHR, C * 4 - 1);
       const int r = idx >> 2, c4 = idx & 3;
-      if (idx < C * 4) {
-        const int t = t0 + r;
-        if constexpr (sizeof(T) == 2) {
-          const uint2 x = (t < s.T) ? *(const uint2*)(Vg + (size_t)t * vrs + 4 * c4) : make_uint2(0, 0);
-          v[i][0] = x.x;
-          v[i][1] = x.y;
-        } else {
-          const uint4 x = (t < s.T) ? *(const uint4*)(Vg + (size_t)t * vrs + 4 * c4)
-                                    : make_uint4(0, 0, 0, 0);
-          v[i][0] = x.x;
-          v[i][1] = x.y;
-          v[i][2] = x.z;
-          v[i][3] = x.w;
-        }
+      const int t = min(t0 + r, s.T - 1);
+      if constexpr (sizeof(T) == 2) {
+        const uint2 x = *(const uint2*)(Vg + (size_t)t * vrs + 4 * c4);
+        v[i][0] = x.x;
+        v[i][1] = x.y;
+      } else {
+        const uint4 x = *(const uint4*)(Vg + (size_t)t * vrs + 4 * c4);
+        v[i][0] = x.x;
+        v[i][1] = x.y;
+        v[i][2] = x.z;
+        v[i][3] = x.w;
       }
     }
     const float* Mg = p.M + ch * C * C;
     const float* Tg = p.Tu + ch * C * C;
 #pragma unroll
     for (int i = 0; i < NMB; ++i) {
-      const int idx = tid + i * NTHR;
-      if (idx < C * C / 4) {
-        m[i] = *(const f32x4*)(Mg + 4 * idx);
-        if (s.variant == 1) tu[i] = *(const f32x4*)(Tg + 4 * idx);
-      }
+      const int idx = min(tid + i * NTHR, C * C / 4 - 1);
+      m[i] = *(const f32x4*)(Mg + 4 * idx);
+      tu[i] = *(const f32x4*)(Tg + 4 * idx);
     }
     const float* cg = p.coef + ch * 3 * E * C;
 #pragma unroll
-    for (int i = 0; i < NCB; ++i) {
-      const int idx = tid + i * NTHR;
-      if (idx < 3 * E * C / 4) c[i] = *(const f32x4*)(cg + 4 * idx);
-    }
-    if (tid < E4) gc = p.gC[ch * E4 + tid];
-    if (tid < C) {
-      const int t = t0 + tid;
-      beta = (t < s.T) ? (in.beta ? in.beta[((size_t)b * s.T + t) * s.H + h] : 1.f) : 0.f;
-    }
+    for (int i = 0; i < NCB; ++i) c[i] = *(const f32x4*)(cg + 4 * min(tid + i * NTHR, 3 * E * C / 4 - 1));
+    gc = p.gC[ch * E4 + min(tid, E4 - 1)];
+    const int tb = min(t0 + min(tid, C - 1), s.T - 1);
+    beta = in.beta ? in.beta[((size_t)b * s.T + tb) * s.H + h] : 1.f;
   }
 
   template <typename Sm>
-  __device__ __forceinline__ void store(Sm& sm, int variant) const {
+  __device__ __forceinline__ void store(Sm& sm, int variant, int t0, int nT) const {
     typedef typename Elem<T>::frag F;
     const int tid = threadIdx.x;
 #pragma unroll
@@ -295,15 +290,24 @@ struct FwdStage {
       const int blk = tid + i * NTHR;
       const int rb = blk % RB, cb = blk / RB;
       if (blk < RB * CB) {
+        uint32_t kk[4][KWD];
 #pragma unroll
         for (int rr = 0; rr < 4; ++rr) {
-          lds_put_raw8(&sm.K[4 * rb + rr][8 * cb], k[i][rr]);
-          if constexpr (STAGE_Q) lds_put_raw8(&sm.Q[4 * rb + rr][8 * cb], q[i][rr]);
+          const bool ok = t0 + 4 * rb + rr < nT;
+#pragma unroll
+          for (int j = 0; j < KWD; j += 2) {
+            kk[rr][j] = ok ? k[i][rr][j] : 0u;
+            kk[rr][j + 1] = ok ? k[i][rr][j + 1] : 0u;
+            *(uint2*)((uint32_t*)&sm.K[4 * rb + rr][KW * cb] + j) = make_uint2(kk[rr][j], kk[rr][j + 1]);
+            if constexpr (STAGE_Q)
+              *(uint2*)((uint32_t*)&sm.Q[4 * rb + rr][KW * cb] + j) =
+                  make_uint2(ok ? q[i][rr][j] : 0u, ok ? q[i][rr][j + 1] : 0u);
+          }
         }
 #pragma unroll
-        for (int cc = 0; cc < 8; ++cc)
-          lds_put4(&sm.Kt[8 * cb + cc][4 * rb], k[i][0].get(cc), k[i][1].get(cc),
-                   k[i][2].get(cc), k[i][3].get(cc));
+        for (int cc = 0; cc < KW; ++cc)
+          lds_put4(&sm.Kt[KW * cb + cc][4 * rb], word_elem<T>(kk[0], cc), word_elem<T>(kk[1], cc),
+                   word_elem<T>(kk[2], cc), word_elem<T>(kk[3], cc));
       }
     }
 #pragma unroll
@@ -311,6 +315,7 @@ struct FwdStage {
       const int idx = tid + i * NTHR;
       const int r = idx >> 2, c4 = idx & 3;
       if (idx < C * 4) {
+        const bool ok = t0 + r < nT;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           T x;
@@ -318,7 +323,7 @@ struct FwdStage {
             x = (T)((j & 1) ? (v[i][j >> 1] >> 16) : (v[i][j >> 1] & 0xffffu));
           else
             x = __uint_as_float(v[i][j]);
-          sm.Vt[4 * c4 + j][r] = x;
+          sm.Vt[4 * c4 + j][r] = ok ? x : T(0);
         }
       }
     }
@@ -345,7 +350,7 @@ struct FwdStage {
       if (idx < 3 * E * C / 4) ((f32x4*)cs)[idx] = c[i];
     }
     if (tid < E4) sm.gC[tid] = gc;
-    if (tid < C) sm.beta[tid] = beta;
+    if (tid < C) sm.beta[tid] = (t0 + tid < nT) ? beta : 0.f;
   }
 };
 
@@ -399,7 +404,7 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
     __syncthreads();  // the previous chunk is done with shared memory
 
     // ---- stage the chunk from registers (loaded during the previous chunk)
-    stage.store(sm, s.variant);
+    stage.store(sm, s.variant, ci * C, s.T);
     __syncthreads();
     // next chunk's inputs are in flight while this chunk computes
     if (ci + 1 < s.Nc) stage.load(s, in, p, Kg, Qg, Vg, b, h, ci + 1);
@@ -649,7 +654,9 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
 }
 
 // ---------------------------------------------------------------- launchers
-template <int E> constexpr int fwd_waves() { return E >= 16 ? 8 : 4; }
+// Eight waves (two per SIMD) for E = 16, whose state does not fit four waves'
+// registers; four waves otherwise (measured faster at E = 8).
+template <typename T, int E> constexpr int fwd_waves() { return E >= 16 ? 8 : 4; }
 
 template <typename T, int KD, int C, int E>
 static hipError_t prep_inst(const Shape& s, const FwdIn& in, const PrepBufs& p, hipStream_t st) {
@@ -660,7 +667,7 @@ static hipError_t prep_inst(const Shape& s, const FwdIn& in, const PrepBufs& p, 
 template <typename T, int KD, int C, int E>
 static hipError_t fwd_inst(const Shape& s, const FwdIn& in, const PrepBufs& p, void* o,
                            float* s_final, const SavedBufs* sv, hipStream_t st) {
-  constexpr int NW = fwd_waves<E>();
+  constexpr int NW = fwd_waves<T, E>();
   typedef FwdSmem<T, KD, C, E, NW> Sm;
   const size_t smem = sizeof(Sm);
   static bool attr_set = false;
@@ -708,7 +715,7 @@ hipError_t launch_fwd(const Shape& s, const FwdIn& in, const PrepBufs& p, void* 
 
 template <typename T, int KD, int C, int E>
 static bool fits_inst() {
-  return sizeof(FwdSmem<T, KD, C, E, fwd_waves<E>()>) <= 160 * 1024;
+  return sizeof(FwdSmem<T, KD, C, E, fwd_waves<T, E>()>) <= 160 * 1024;
 }
 
 bool fits_lds(int K, int C, int E, bool bf16) {
