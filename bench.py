@@ -7,12 +7,24 @@ accumulation (the 1.3B-model head shape of the paper's efficiency study at
 batch 4).  Inputs are seeded synthetic tensors with the paper's distributions,
 resident in HBM before timing starts.
 
-Prints one JSON line: throughput in tokens/s (B*T per step), the roofline of
-the dominant kernel (algorithmic FLOPs or bytes per launch over its average
-HIP-event duration inside the timed region), and the fp64 CPU oracle timed
-on a bounded sample of the same workload.
+Prints one JSON line: throughput in tokens/s (B*T per step), every kernel's
+average HIP-event time with its algorithmic FLOP and byte rates, the
+roofline of the dominant kernel, and the fp64 CPU oracle timed on a bounded
+sample of the same workload.
+
+Helper modes for the HBM-traffic measurement (run under rocprofv3 --pmc):
+  --copy-calibration     a plain fp32 copy kernel of known size
+  --pmc-summary F W CF CW  reduce four rocprofv3 counter directories (bench
+                         FETCH_SIZE, bench WRITE_SIZE, copy FETCH_SIZE, copy
+                         WRITE_SIZE) to per-kernel bytes per launch, written
+                         to profiles/hbm_traffic.json with the hash of each
+                         kernel's sources (bench.py reports it only while the
+                         sources are unchanged)
 """
 import argparse
+import csv
+import glob
+import hashlib
 import json
 import os
 import sys
@@ -23,45 +35,161 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+TRAFFIC_JSON = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+CSRC = os.path.join(ROOT, "paper_2609_36529_amd", "csrc")
+KERNEL_SOURCES = {
+    "prep": "tla_fwd.hip", "fwd_recurrent": "tla_fwd.hip", "bwd_recurrent": "tla_bwd.hip",
+    "bwd_state": "tla_bwd.hip", "bwd_chunk": "tla_bwd.hip", "step": "tla_step.hip",
+}
+KERNEL_SYMBOLS = {  # rocprofv3 kernel-name prefix -> timing slot
+    "tla::k_prep<": "prep", "tla::k_fwd<": "fwd_recurrent", "tla::k_bwd_rec<": "bwd_recurrent",
+    "tla::k_bwd_state<": "bwd_state", "tla::k_bwd_chunk<": "bwd_chunk", "tla::k_step<": "step",
+}
+COPY_BYTES = 1 << 28         # copy-calibration buffer (fp32)
+
+
+def source_hash(kind):
+    h = hashlib.sha256()
+    for f in (KERNEL_SOURCES[kind], "tla_common.hpp", "tla_internal.hpp"):
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
 
 
 def algorithmic(cfg):
-    """Per token-head algorithmic FLOPs / bytes of each kernel (GDN).  FLOPs
-    count the method's own contractions (not split-operand or recompute
-    work); bytes count each kernel's compulsory HBM reads and writes."""
+    """Per token-head algorithmic FLOPs and HBM bytes of each kernel (GDN,
+    bf16 operands and outputs).  FLOPs count the method's own contractions
+    (dense, no split-operand or recompute work); bytes count each kernel's
+    compulsory reads and writes, every tensor once (re-reads of the same
+    chunk by the value-tile workgroups are cache traffic, not algorithmic)."""
     K, V, E, C = cfg.K, cfg.V, cfg.E, cfg.chunk
     ckpt = 2.0 * E * K * V / C          # one bf16 chunk state per token-head
     return {
-        "prep": {"flops": 4 * C * K + C * C / 3.0},
+        # Grams A_qk, A_kk and the (I + L) solve; reads q, k, q2, k2, g, beta,
+        # writes the coefficient vectors and M, Tu (fp32)
+        "prep": {"flops": 4 * C * K + C * C / 3.0,
+                 "bytes": 2 * 2 * K + 2 * 2 * E + 4 * E + 4 + 12 * E + 8 * C},
+        # W, Q S_e, K^T diag(c) U over E slices, Tu (V - W), M U; reads q, k, v,
+        # M, Tu, coefficients, writes o, the chunk-start state, U and V - W
         "fwd_recurrent": {"flops": 6 * K * V * E + 4 * C * V,
-                          "bytes": 2 * (2 * K + V) + 2 * V + ckpt + 8 * V},
+                          "bytes": 2 * (2 * K + V) + 8 * C + 12 * E + 2 * V + ckpt + 8 * V},
+        # K dS', M^T dO, Tu^T dU, Q^T diag(b) dO, K^T diag(a) dW; reads q, k,
+        # dO, M, Tu, coefficients, writes dS', dU, dW
         "bwd_recurrent": {"flops": 6 * K * V * E + 4 * C * V,
-                          "bytes": 2 * (2 * K + V) + ckpt + 8 * V},
+                          "bytes": 2 * (2 * K + V) + 8 * C + 12 * E + ckpt + 8 * V},
+        # dO S^T, dW S^T, U dS'^T per slice; reads both chunk states, dO, dW,
+        # U, q, k, writes the dq / dk partials and the coefficient gradients
         "bwd_state": {"flops": 6 * K * V * E,
-                      "bytes": 2 * ckpt + 2 * V + 8 * V + 4 * K + 8 * K},
-        "bwd_chunk": {"flops": 6 * C * K + 4 * C * V + 2 * C * C / 3.0},
-        "total_flops": 18 * K * V * E + 12 * C * K + 12 * C * V + C * C,
+                      "bytes": 2 * ckpt + 2 * V + 8 * V + 4 * K + 8 * K + 12 * E},
+        # Grams, dM, dTu, dq / dk products; reads q, k, v, dO, U, V - W, dU, dW,
+        # the partials and vectors, writes every input gradient
+        "bwd_chunk": {"flops": 10 * C * K + 4 * C * V + 2 * C * C / 3.0,
+                      "bytes": 2 * (2 * K + 2 * V) + 16 * V + 8 * K + 12 * E + 16 * E + 8
+                      + 2 * (2 * K + V) + 2 * 2 * E + 4 * E + 4},
+        "total_flops": 18 * K * V * E + 14 * C * K + 12 * C * V + 2 * C * C,
     }
 
 
-def cpu_baseline(cfg, inp, dO, nb=2):
+def bound_of(a):
+    """'mfma' or 'hbm', whichever roofline time is longer for these counts."""
+    t_f = a.get("flops", 0.0) / (PEAK_BF16_TFLOPS * 1e12)
+    t_b = a.get("bytes", 0.0) / (PEAK_HBM_GBS * 1e9)
+    return "mfma" if t_f >= t_b else "hbm"
+
+
+def cpu_baseline(cfg, inp, dO, min_seconds=10.0):
     """The fp64 oracle (token-by-token recurrence + reverse mode, OpenMP over
-    heads) on the first `nb` batch entries, all heads, full T."""
+    heads) on the whole workload (all batch entries and heads, full T),
+    repeated until at least `min_seconds` have elapsed."""
     import oracle
     from paper_2609_36529_amd import synth
-    sl = lambda x: None if x is None else synth.to64(x[:nb])
-    args = [sl(inp[n]) for n in ("q", "k", "v", "q2", "k2", "g", "beta", "s0")]
-    d = sl(dO)
-    t0 = time.perf_counter()
-    oracle.fwd(cfg.variant, *args)
-    oracle.bwd(cfg.variant, *args, d)
-    dt = time.perf_counter() - t0
-    tokens = nb * cfg.T
-    return {"value": tokens / dt, "unit": "tokens/s", "cores": oracle.num_threads(),
+    args = [synth.to64(inp[n]) if inp[n] is not None else None
+            for n in ("q", "k", "v", "q2", "k2", "g", "beta", "s0")]
+    d = synth.to64(dO)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        oracle.fwd(cfg.variant, *args)
+        oracle.bwd(cfg.variant, *args, d)
+        reps += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_seconds:
+            break
+    tokens = reps * cfg.B * cfg.T
+    return {"value": round(tokens / dt, 1), "unit": "tokens/s", "cores": oracle.num_threads(),
             "kind": "oracle",
-            "sample": f"GDN fwd+bwd (fp64 oracle: forward, then reverse-mode backward "
-                      f"with its own recompute) on {nb} of {cfg.B} batch entries x {cfg.H} heads, "
-                      f"full T={cfg.T}: {tokens} tokens in {dt:.1f} s"}
+            "sample": f"GDN fwd+bwd of the whole workload ({cfg.B} x {cfg.T} tokens x {cfg.H} "
+                      f"heads; fp64 oracle: forward, then reverse-mode backward with its own "
+                      f"recompute), {reps} repetition(s) in {dt:.1f} s"}
+
+
+def traffic_for(kind, alg_bytes, token_heads):
+    """Measured HBM bytes per launch of `kind` from profiles/hbm_traffic.json,
+    or None when absent or taken from different kernel sources."""
+    try:
+        with open(TRAFFIC_JSON) as fh:
+            rec = json.load(fh)["kernels"][kind]
+    except (OSError, KeyError, ValueError):
+        return None, None
+    if rec.get("source_hash") != source_hash(kind):
+        return None, None
+    t = rec["fetch_bytes"] + rec["write_bytes"]
+    return t, round(t / (alg_bytes * token_heads), 3)
+
+
+def copy_calibration():
+    import torch
+    n = COPY_BYTES // 4
+    x = torch.rand(n, device="cuda")
+    y = torch.empty_like(x)
+    for _ in range(5):
+        torch.mul(x, 1.0, out=y)   # reads and writes COPY_BYTES each
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": COPY_BYTES, "launches": 5}), flush=True)
+
+
+def _pmc_table(d, counter):
+    """{kernel slot: average counter value per dispatch} from a rocprofv3 dir."""
+    sums, disp = {}, {}
+    for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        for r in csv.DictReader(open(f)):
+            if r["Counter_Name"] != counter:
+                continue
+            name = r["Kernel_Name"]
+            slot = next((v for k, v in KERNEL_SYMBOLS.items() if k in name), None)
+            if slot is None:
+                slot = "copy" if ("mul" in name.lower() or "elementwise" in name.lower()) else None
+            if slot is None:
+                continue
+            sums[slot] = sums.get(slot, 0.0) + float(r["Counter_Value"])
+            disp.setdefault(slot, set()).add(r["Dispatch_Id"])
+    return {k: sums[k] / len(disp[k]) for k in sums}
+
+
+def pmc_summary(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir):
+    fe, wr = _pmc_table(fetch_dir, "FETCH_SIZE"), _pmc_table(write_dir, "WRITE_SIZE")
+    cf, cw = _pmc_table(copy_fetch_dir, "FETCH_SIZE"), _pmc_table(copy_write_dir, "WRITE_SIZE")
+    # counters read KiB; the copy kernel moves COPY_BYTES each way
+    f_scale = COPY_BYTES / (cf["copy"] * 1024.0)
+    w_scale = COPY_BYTES / (cw["copy"] * 1024.0)
+    out = {"units": "bytes per launch", "fetch_scale": f_scale, "write_scale": w_scale,
+           "copy_fetch_kib": cf["copy"], "copy_write_kib": cw["copy"], "kernels": {}}
+    for kind in sorted(set(fe) & set(wr)):
+        if kind == "copy":
+            continue
+        out["kernels"][kind] = {"fetch_kib": fe[kind], "write_kib": wr[kind],
+                                "fetch_bytes": fe[kind] * 1024.0 * f_scale,
+                                "write_bytes": wr[kind] * 1024.0 * w_scale,
+                                "source_hash": source_hash(kind)}
+    os.makedirs(os.path.dirname(TRAFFIC_JSON), exist_ok=True)
+    with open(TRAFFIC_JSON, "w") as fh:
+        json.dump(out, fh, indent=1)
+    print(f"copy kernel: FETCH_SIZE {cf['copy']:.0f} KiB, WRITE_SIZE {cw['copy']:.0f} KiB per "
+          f"launch for {COPY_BYTES >> 20} MiB each way -> scale {f_scale:.4f} / {w_scale:.4f}")
+    print("| kernel | FETCH_SIZE KiB | WRITE_SIZE KiB | HBM bytes per launch (scaled) |")
+    print("|---|---|---|---|")
+    for kind, r in out["kernels"].items():
+        print(f"| {kind} | {r['fetch_kib']:.0f} | {r['write_kib']:.0f} | "
+              f"{r['fetch_bytes'] + r['write_bytes']:.4g} |")
 
 
 def main():
@@ -70,12 +198,20 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--pmc-summary", nargs=4, metavar="DIR")
     args = ap.parse_args()
+    if args.pmc_summary:
+        pmc_summary(*args.pmc_summary)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the operator's work shards over batch, heads "
               "and value tiles with no exchange, so per-GPU throughput at N GPUs is the N=1 "
               "figure; multi-GPU runs are not part of this build.", file=sys.stderr)
         sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration()
+        return
 
     import torch
     import paper_2609_36529_amd as tla
@@ -132,23 +268,26 @@ def main():
         if n == 0:
             continue
         avg_ms = tot / n
-        entry = {"avg_ms": round(avg_ms, 4), "launches": n}
-        a = alg.get(name, {})
-        if "flops" in a:
-            entry["tflops"] = round(a["flops"] * token_heads / (avg_ms * 1e-3) / 1e12, 2)
-        if "bytes" in a:
-            entry["gbs"] = round(a["bytes"] * token_heads / (avg_ms * 1e-3) / 1e9, 1)
+        a = alg[name]
+        entry = {"avg_ms": round(avg_ms, 4), "launches": n, "bound": bound_of(a),
+                 "tflops": round(a["flops"] * token_heads / (avg_ms * 1e-3) / 1e12, 2),
+                 "gbs": round(a["bytes"] * token_heads / (avg_ms * 1e-3) / 1e9, 1)}
+        entry["frac"] = round(entry["tflops"] / PEAK_BF16_TFLOPS if entry["bound"] == "mfma"
+                              else entry["gbs"] / PEAK_HBM_GBS, 4)
         kernels[name] = entry
     dom = max(kernels, key=lambda k: kernels[k]["avg_ms"] * kernels[k]["launches"])
-    a = alg[dom]
-    if dom == "bwd_state":
-        roof = {"bound": "hbm", "achieved": kernels[dom]["gbs"], "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+    kd = kernels[dom]
+    if kd["bound"] == "hbm":
+        roof = {"bound": "hbm", "achieved": kd["gbs"], "peak": PEAK_HBM_GBS, "unit": "GB/s"}
     else:
-        roof = {"bound": "mfma", "achieved": kernels[dom]["tflops"], "peak": PEAK_BF16_TFLOPS,
+        roof = {"bound": "mfma", "achieved": kd["tflops"], "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s"}
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    roof["traffic"] = None
+    roof["traffic"], roof["traffic_over_algorithmic"] = traffic_for(dom, alg[dom]["bytes"],
+                                                                    token_heads)
     roof["kernel"] = dom
+    roof["algorithmic_per_launch"] = {"flops": alg[dom]["flops"] * token_heads,
+                                      "bytes": alg[dom]["bytes"] * token_heads}
     step_tflops = alg["total_flops"] * token_heads / (ms_per_step * 1e-3) / 1e12
 
     result = {
@@ -168,7 +307,6 @@ def main():
                    "B": B, "T": T, "H": H, "K": K, "V": V, "E": E, "chunk": C,
                    "operands": "bf16, fp32 accumulation, fp32 state", "outputs": "bf16",
                    "seed": cfg.seed},
-        "mfma_frac_of_bf16_peak": round(step_tflops / PEAK_BF16_TFLOPS, 4),
         "step_tflops": round(step_tflops, 2),
         "kernels": kernels,
         "roofline": roof,
