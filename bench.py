@@ -291,7 +291,7 @@ def main():
     step_tflops = alg["total_flops"] * token_heads / (ms_per_step * 1e-3) / 1e12
 
     result = {
-        "metric": "fwd+bwd tokens/s, triadic GDN H=8 K=V=128 E=8 T=4096",
+        "metric": "fwd+bwd tokens/s and MFMA % of bf16 peak, triadic GDN H=8 K=V=128 E=8 T=4096",
         "value": round(tokens / (ms_per_step * 1e-3), 1),
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -308,6 +308,7 @@ def main():
                    "operands": "bf16, fp32 accumulation, fp32 state", "outputs": "bf16",
                    "seed": cfg.seed},
         "step_tflops": round(step_tflops, 2),
+        "mfma_pct_of_bf16_peak": round(100.0 * step_tflops / PEAK_BF16_TFLOPS, 2),
         "kernels": kernels,
         "roofline": roof,
     }
