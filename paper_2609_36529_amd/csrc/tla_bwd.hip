@@ -644,44 +644,46 @@ __global__ __launch_bounds__(256) void k_bwd_state(Shape s, FwdIn in, const void
     const int n8 = ncols / 8;
     Raw8<T> ro[IT];
     f32x4 rw[IT][2], ru[IT][2];
+    // unconditional loads from clamped positions (masked below), so that
+    // every load of the batch is in flight before the first wait
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
-      const int idx = tid + 256 * it;
-      const int r = idx / n8, col = c0 + 8 * (idx % n8);
-      ro[it] = zero_raw8<T>();
-      rw[it][0] = rw[it][1] = ru[it][0] = ru[it][1] = zero4();
-      if (idx < C * n8 && col < V) {
-        if (t0 + r < s.T) ro[it] = load8(dOg + (size_t)(t0 + r) * vrs + col);
-        const float* pw = dWg + (size_t)r * V + col;
-        const float* pu = Ug + (size_t)r * V + col;
-        rw[it][0] = *(const f32x4*)pw;
-        rw[it][1] = *(const f32x4*)(pw + 4);
-        ru[it][0] = *(const f32x4*)pu;
-        ru[it][1] = *(const f32x4*)(pu + 4);
-      }
+      const int idx = min(tid + 256 * it, C * n8 - 1);
+      const int r = idx / n8, col = min(c0 + 8 * (idx % n8), V - 8);
+      ro[it] = load8(dOg + (size_t)min(t0 + r, s.T - 1) * vrs + col);
+      const float* pw = dWg + (size_t)r * V + col;
+      const float* pu = Ug + (size_t)r * V + col;
+      rw[it][0] = *(const f32x4*)pw;
+      rw[it][1] = *(const f32x4*)(pw + 4);
+      ru[it][0] = *(const f32x4*)pu;
+      ru[it][1] = *(const f32x4*)(pu + 4);
     }
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
       const int idx = tid + 256 * it;
       if (idx >= C * n8) continue;
       const int r = idx / n8, c = 8 * (idx % n8);
+      const bool cok = c0 + c < V;
+      const Raw8<T> dov = (cok && t0 + r < s.T) ? ro[it] : zero_raw8<T>();
+      const f32x4 w0 = cok ? rw[it][0] : zero4(), w1 = cok ? rw[it][1] : zero4();
+      const f32x4 u0 = cok ? ru[it][0] : zero4(), u1 = cok ? ru[it][1] : zero4();
       if constexpr (SPLIT) {
-        *(uint4*)&sm.dO[r][c] = ro[it].w[0];
+        *(uint4*)&sm.dO[r][c] = dov.w[0];
         bf16x4 h0, l0, h1, l1;
-        split_frag(rw[it][0], h0, l0);
-        split_frag(rw[it][1], h1, l1);
+        split_frag(w0, h0, l0);
+        split_frag(w1, h1, l1);
         *(bf16x8*)&sm.dWh[r][c] = __builtin_shufflevector(h0, h1, 0, 1, 2, 3, 4, 5, 6, 7);
         *(bf16x8*)&sm.dWl[r][c] = __builtin_shufflevector(l0, l1, 0, 1, 2, 3, 4, 5, 6, 7);
-        split_frag(ru[it][0], h0, l0);
-        split_frag(ru[it][1], h1, l1);
+        split_frag(u0, h0, l0);
+        split_frag(u1, h1, l1);
         *(bf16x8*)&sm.Uh[r][c] = __builtin_shufflevector(h0, h1, 0, 1, 2, 3, 4, 5, 6, 7);
         *(bf16x8*)&sm.Ul[r][c] = __builtin_shufflevector(l0, l1, 0, 1, 2, 3, 4, 5, 6, 7);
       } else {
-        lds_put_raw8(&sm.dO[r][c], ro[it]);
-        *(f32x4*)&sm.dWh[r][c] = rw[it][0];
-        *(f32x4*)&sm.dWh[r][c + 4] = rw[it][1];
-        *(f32x4*)&sm.Uh[r][c] = ru[it][0];
-        *(f32x4*)&sm.Uh[r][c + 4] = ru[it][1];
+        lds_put_raw8(&sm.dO[r][c], dov);
+        *(f32x4*)&sm.dWh[r][c] = w0;
+        *(f32x4*)&sm.dWh[r][c + 4] = w1;
+        *(f32x4*)&sm.Uh[r][c] = u0;
+        *(f32x4*)&sm.Uh[r][c + 4] = u1;
       }
     }
   };
@@ -697,9 +699,10 @@ __global__ __launch_bounds__(256) void k_bwd_state(Shape s, FwdIn in, const void
       for (int j = 0; j < 4; ++j) {
         const int t = t0 + 16 * rt + 4 * g + j;
         const bool ok = ct < KT && t < s.T;
-        const size_t off = (size_t)t * krs + 16 * ct + n;
-        qv[rt][c][j] = ok ? Elem<T>::to_f(Qg[off]) : 0.f;
-        kv[rt][c][j] = ok ? Elem<T>::to_f(Kg[off]) : 0.f;
+        const size_t off = (size_t)min(t, s.T - 1) * krs + 16 * min(ct, KT - 1) + n;
+        const float qx = Elem<T>::to_f(Qg[off]), kx = Elem<T>::to_f(Kg[off]);
+        qv[rt][c][j] = ok ? qx : 0.f;
+        kv[rt][c][j] = ok ? kx : 0.f;
       }
     }
   {
@@ -713,17 +716,15 @@ __global__ __launch_bounds__(256) void k_bwd_state(Shape s, FwdIn in, const void
   const T* Sck = (const T*)sv.Sck;
   const T* dSck = (const T*)bb.dSck;
   Raw8<T> sbuf[CTW][NPMAX], dbuf[CTW][NPMAX];
+  // (loads from clamped tiles, never under a per-lane branch: a value block
+  // past V meets zero A-operand columns, and the state-gradient dot product
+  // below masks it)
   auto load_pair = [&](int e, int c, int pp) {
-    const int ct = w * CTW + c;
-    const int vb = 2 * pp + (g >> 1);
-    if (ct < KT && vb < VB) {
-      const size_t off = ((((size_t)ch * E + e) * VB + vb) * KD + 16 * ct + n) * 16 + 8 * (g & 1);
-      sbuf[c][pp] = load8(Sck + off);
-      dbuf[c][pp] = load8(dSck + off);
-    } else {
-      sbuf[c][pp] = zero_raw8<T>();
-      dbuf[c][pp] = zero_raw8<T>();
-    }
+    const int ct = min(w * CTW + c, KT - 1);
+    const int vb = min(2 * pp + (g >> 1), VB - 1);
+    const size_t off = ((((size_t)ch * E + e) * VB + vb) * KD + 16 * ct + n) * 16 + 8 * (g & 1);
+    sbuf[c][pp] = load8(Sck + off);
+    dbuf[c][pp] = load8(dSck + off);
   };
 #pragma unroll
   for (int pp = 0; pp < NPMAX; ++pp)
@@ -765,11 +766,12 @@ __global__ __launch_bounds__(256) void k_bwd_state(Shape s, FwdIn in, const void
 #pragma unroll
       for (int c = 0; c < CTW; ++c) {
         if (w * CTW + c >= KT) continue;
-        float a[8], d[8];
+        float a[8], d[8], part = 0.f;
         raw8_to_f(sbuf[c][pp], a);
         raw8_to_f(dbuf[c][pp], d);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) gpart += a[i] * d[i];
+        for (int i = 0; i < 8; ++i) part += a[i] * d[i];
+        gpart += (2 * pp + (g >> 1) < VB) ? part : 0.f;
       }
 #pragma unroll
       for (int rt = 0; rt < NT; ++rt) {
@@ -1103,18 +1105,20 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
     // global operand loads first (value columns 32 vp + 8 g .. + 7)
     Raw8<T> dOa[NVPMAX];
     f32x4 Ub[NVPMAX][2], dUa[NVPMAX][2], Xb[NVPMAX][2];
+    // (unconditional loads from clamped positions under wave-uniform
+    // conditions only, masked once the values are used)
 #pragma unroll
     for (int vp = 0; vp < NVPMAX; ++vp) {
-      const int col = 32 * vp + 8 * g;
-      const bool cok = vp < NVP && col < V;
+      const int col = min(32 * vp + 8 * g, V - 8);
       dOa[vp] = zero_raw8<T>();
       Ub[vp][0] = Ub[vp][1] = dUa[vp][0] = dUa[vp][1] = Xb[vp][0] = Xb[vp][1] = zero4();
-      if (lower && cok) {
-        if (raok) dOa[vp] = load8(dOg + (size_t)(t0 + ra) * vrs + col);
+      if (vp >= NVP) continue;
+      if (lower) {
+        dOa[vp] = load8(dOg + (size_t)min(t0 + ra, s.T - 1) * vrs + col);
         Ub[vp][0] = *(const f32x4*)(Ug + (size_t)cb * V + col);
         Ub[vp][1] = *(const f32x4*)(Ug + (size_t)cb * V + col + 4);
       }
-      if (gdn && cok) {
+      if (gdn) {
         dUa[vp][0] = *(const f32x4*)(dUg + (size_t)ra * V + col);
         dUa[vp][1] = *(const f32x4*)(dUg + (size_t)ra * V + col + 4);
         Xb[vp][0] = *(const f32x4*)(Xg + (size_t)cb * V + col);
@@ -1158,13 +1162,20 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
     }
     if (lower) {
 #pragma unroll
-      for (int vp = 0; vp < NVPMAX; ++vp)
-        if (vp < NVP) mma8_xs(dm, dOa[vp], Ub[vp][0], Ub[vp][1]);
+      for (int vp = 0; vp < NVPMAX; ++vp) {
+        if (vp >= NVP) continue;
+        const bool cok = 32 * vp + 8 * g < V;  // columns past V (odd V / 16) contribute zero
+        mma8_xs(dm, (cok && raok) ? dOa[vp] : zero_raw8<T>(), Ub[vp][0], Ub[vp][1]);
+      }
     }
     if (gdn) {
 #pragma unroll
-      for (int vp = 0; vp < NVPMAX; ++vp)
-        if (vp < NVP) mma8_ss(dt, dUa[vp][0], dUa[vp][1], Xb[vp][0], Xb[vp][1], tag);
+      for (int vp = 0; vp < NVPMAX; ++vp) {
+        if (vp >= NVP) continue;
+        const bool cok = 32 * vp + 8 * g < V;
+        mma8_ss(dt, cok ? dUa[vp][0] : zero4(), cok ? dUa[vp][1] : zero4(), Xb[vp][0], Xb[vp][1],
+                tag);
+      }
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
