@@ -95,8 +95,9 @@ size_t tla_workspace_bytes(const tla_desc* desc, int op);
 /* Bytes of the `saved` buffer that a training forward fills for tla_bwd:
  * chunk-start states (Appendix A, "Kernels": the forward stores the state at
  * the start of every chunk so the backward need not recompute it), the
- * delta-corrected values U and the residual V - W of every chunk, in an
- * opaque layout.  0 if desc is invalid. */
+ * delta-corrected values U and the residual V - W of every chunk, and the
+ * per-chunk terms of Eq. joint-gram / joint-solve (coefficient vectors, M,
+ * Tu), in an opaque layout.  0 if desc is invalid. */
 size_t tla_saved_bytes(const tla_desc* desc);
 
 /*
@@ -108,7 +109,8 @@ size_t tla_saved_bytes(const tla_desc* desc);
  *   s_final: final state or NULL.  It may alias s0 (in place).
  *   saved  : NULL for inference; else a buffer of tla_saved_bytes() that the
  *            backward consumes (training mode).
- *   ws     : device workspace of at least tla_workspace_bytes(desc, FWD).
+ *   ws     : device workspace of at least tla_workspace_bytes(desc, FWD);
+ *            unused (may be NULL) when saved is given.
  */
 int tla_fwd(const tla_desc* desc, const void* q, const void* k, const void* v,
             const void* q2, const void* k2, const float* g, const float* beta,

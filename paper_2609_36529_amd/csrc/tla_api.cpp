@@ -91,10 +91,13 @@ int check_desc(const tla_desc* d, tla::Shape* s, bool for_step) {
 
 size_t esize(const tla::Shape& s) { return s.in_bf16 ? 2 : 4; }
 
+// Buffer layouts.  The per-chunk prep results (coefficient vectors, gamma^C,
+// M, Tu) live in the forward workspace for inference; a training forward
+// writes them into `saved`, where the backward reads them again.
 struct Layout {
-  size_t prep_coef, prep_gC, prep_M, prep_Tu, prep_end;
+  size_t p_coef, p_gC, p_M, p_Tu, p_size;  // prep region, relative offsets
   size_t bwd_dS, bwd_dU, bwd_dW, bwd_dqs, bwd_dks, bwd_dcoef, bwd_dgC, bwd_end;
-  size_t sv_S, sv_U, sv_X, sv_end;
+  size_t sv_S, sv_U, sv_X, sv_prep, sv_end;
 };
 
 Layout layout(const tla::Shape& s) {
@@ -103,11 +106,12 @@ Layout layout(const tla::Shape& s) {
   const size_t es = esize(s);
   const size_t E4 = tla::round4(s.E);
   size_t o = 0;
-  L.prep_coef = o; o += align256(nch * 3 * s.E * s.C * 4);
-  L.prep_gC = o;   o += align256(nch * E4 * 4);
-  L.prep_M = o;    o += align256(nch * s.C * s.C * 4);
-  L.prep_Tu = o;   o += align256(nch * s.C * s.C * 4);
-  L.prep_end = o;
+  L.p_coef = o; o += align256(nch * 3 * s.E * s.C * 4);
+  L.p_gC = o;   o += align256(nch * E4 * 4);
+  L.p_M = o;    o += align256(nch * s.C * s.C * 4);
+  L.p_Tu = o;   o += align256(nch * s.C * s.C * 4);
+  L.p_size = o;
+  o = 0;
   L.bwd_dS = o;    o += align256(nch * s.E * s.K * s.V * es);
   L.bwd_dU = o;    o += align256(nch * s.C * s.V * 4);
   L.bwd_dW = o;    o += align256(nch * s.C * s.V * 4);
@@ -117,17 +121,18 @@ Layout layout(const tla::Shape& s) {
   L.bwd_dgC = o;   o += align256(nch * E4 * 4);
   L.bwd_end = o;
   o = 0;
-  L.sv_S = o; o += align256(nch * s.E * s.K * s.V * es);
-  L.sv_U = o; o += align256(nch * s.C * s.V * 4);
-  L.sv_X = o; o += align256(nch * s.C * s.V * 4);
+  L.sv_S = o;    o += align256(nch * s.E * s.K * s.V * es);
+  L.sv_U = o;    o += align256(nch * s.C * s.V * 4);
+  L.sv_X = o;    o += align256(nch * s.C * s.V * 4);
+  L.sv_prep = o; o += L.p_size;
   L.sv_end = o;
   return L;
 }
 
-tla::PrepBufs prep_bufs(const Layout& L, void* ws) {
-  char* b = (char*)ws;
-  return tla::PrepBufs{(float*)(b + L.prep_coef), (float*)(b + L.prep_gC),
-                       (float*)(b + L.prep_M), (float*)(b + L.prep_Tu)};
+tla::PrepBufs prep_bufs(const Layout& L, const void* base) {
+  char* b = (char*)base;
+  return tla::PrepBufs{(float*)(b + L.p_coef), (float*)(b + L.p_gC), (float*)(b + L.p_M),
+                       (float*)(b + L.p_Tu)};
 }
 tla::SavedBufs saved_bufs(const Layout& L, const void* saved) {
   char* b = (char*)saved;
@@ -228,7 +233,7 @@ size_t tla_workspace_bytes(const tla_desc* d, int op) {
   tla::Shape s;
   if (check_desc(d, &s, false) != TLA_OK) return 0;
   const Layout L = layout(s);
-  if (op == TLA_OP_FWD) return L.prep_end;
+  if (op == TLA_OP_FWD) return L.p_size;
   if (op == TLA_OP_BWD) return L.bwd_end;
   return 0;
 }
@@ -254,15 +259,16 @@ int tla_fwd(const tla_desc* d, const void* q, const void* k, const void* v, cons
   for (const void* p : ptrs)
     if (misaligned(p)) return fail(TLA_E_ALIGN, "pointer %p is not 16-byte aligned", p);
   const Layout L = layout(s);
-  if (s.T > 0 && (!ws || ws_bytes < L.prep_end))
-    return fail(TLA_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, L.prep_end);
+  const bool use_ws = s.T > 0 && !saved;  // a training forward keeps its prep results in saved
+  if (use_ws && (!ws || ws_bytes < L.p_size))
+    return fail(TLA_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, L.p_size);
   const size_t es = esize(s), os = s.out_bf16 ? 2 : 4;
   const size_t sbytes = (size_t)s.NH * s.E * s.K * s.V * 4;
   const Range ins[] = {{q, ntok * s.K * es}, {k, ntok * s.K * es}, {v, ntok * s.V * es},
                        {q2, ntok * s.E * es}, {k2, ntok * s.E * es}, {g, ntok * s.E * 4},
                        {beta, beta ? ntok * 4 : 0}, {s0, s0 ? sbytes : 0}};
   const Range outs[] = {{o, ntok * s.V * os}, {saved, saved ? L.sv_end : 0},
-                        {ws, s.T > 0 ? L.prep_end : 0}};
+                        {ws, use_ws ? L.p_size : 0}};
   for (const Range& a : outs)
     for (const Range& b : ins)
       if (overlap(a, b)) return fail(TLA_E_ALIAS, "an output or buffer overlaps an input");
@@ -282,7 +288,7 @@ int tla_fwd(const tla_desc* d, const void* q, const void* k, const void* v, cons
   hipStream_t st = (hipStream_t)stream;
   s.has_beta = beta != nullptr;
   tla::FwdIn in{q, k, v, q2, k2, g, beta, s0};
-  const tla::PrepBufs pb = prep_bufs(L, ws);
+  const tla::PrepBufs pb = saved ? prep_bufs(L, (char*)saved + L.sv_prep) : prep_bufs(L, ws);
   hipError_t e;
   if (s.T > 0) {
     e = timed(PROF_PREP, st, [&] { return tla::launch_prep(s, in, pb, st); });
@@ -344,15 +350,13 @@ int tla_bwd(const tla_desc* d, const void* q, const void* k, const void* v, cons
   hipStream_t st = (hipStream_t)stream;
   s.has_beta = beta != nullptr;
   tla::FwdIn in{q, k, v, q2, k2, g, beta, s0};
-  const tla::PrepBufs pb = prep_bufs(L, ws);
+  const tla::PrepBufs pb = prep_bufs(L, (const char*)saved + L.sv_prep);  // from the forward
   char* wb = (char*)ws;
   const tla::BwdBufs bb{wb + L.bwd_dS, (float*)(wb + L.bwd_dU), (float*)(wb + L.bwd_dW),
                         (float*)(wb + L.bwd_dqs), (float*)(wb + L.bwd_dks),
                         (float*)(wb + L.bwd_dcoef), (float*)(wb + L.bwd_dgC)};
   const tla::SavedBufs sv = saved_bufs(L, saved);
-  hipError_t e = timed(PROF_PREP, st, [&] { return tla::launch_prep(s, in, pb, st); });
-  if (e != hipSuccess) return device_fail(e, "prep kernel");
-  e = timed(PROF_BWD_REC, st,
+  hipError_t e = timed(PROF_BWD_REC, st,
             [&] { return tla::launch_bwd_rec(s, in, dO, dS_final, pb, bb, ds0, st); });
   if (e != hipSuccess) return device_fail(e, "backward recurrent kernel");
   e = timed(PROF_BWD_STATE, st, [&] { return tla::launch_bwd_state(s, in, dO, pb, sv, bb, st); });

@@ -10,7 +10,7 @@
 //           non-positive log-gate differences (Appendix A, numerical
 //           stability); M = A_qk o R'; and the UT transform
 //           Tu = (I + tril(diag(beta)(A_kk o R), -1))^{-1} diag(beta)
-//           (Eq. joint-solve) by fp32 forward substitution.
+//           (Eq. joint-solve) by a blocked fp32 unit-lower inverse.
 //   k_fwd   one workgroup per (head, 16-column value tile), sequential over
 //           chunks (Eq. joint-chunk).  The E x K x 16 fp32 state tile lives
 //           in MFMA accumulators for the whole sequence; each wave owns
@@ -58,15 +58,34 @@ __device__ __forceinline__ void mma_k(f32x4& acc, FA fa, FB fb) {
 }
 
 // ------------------------------------------------------------------- prep
+// LDS plan: Q and K rows (bf16 instances) share their space with the inverse
+// of (I + L) and its scratch, which are formed after the Grams.
+template <typename T, int KD, int C, int E>
+struct PrepSmem {
+  static constexpr int KP = KD + 8;  // 16-byte rows, conflict-free 16-byte fragment reads
+  static constexpr int CP = C + 4;
+  static constexpr int NT = C / 16;
+  static constexpr bool STAGE = sizeof(T) == 2;  // fp32 rows are read from global memory
+  union U {
+    struct { T sQ[STAGE ? C : 1][KP]; T sK[STAGE ? C : 1][KP]; } qk;
+    struct { float X[C][CP]; float Y[NT > 1 ? NT - 1 : 1][16][17]; } inv;
+  };
+  alignas(16) U u;
+  alignas(16) float L[C][CP];  // diag(beta)(A_kk o R), strictly lower
+  alignas(16) float q2[C][E];
+  alignas(16) float k2[C][E];
+  alignas(16) double G[C][E];  // in-chunk cumulative log-gates
+  alignas(16) float beta[C];
+};
+
 template <typename T, int KD, int C, int E>
 __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
   constexpr int NT = C / 16;
   constexpr int E4 = (E + 3) & ~3;
-  // G is accumulated and differenced in fp64: after a very negative gate the
-  // running sum is large and fp32 would lose the small gates that follow it.
-  __shared__ float sq2[C][E], sk2[C][E], sbeta[C];
-  __shared__ double sG[C][E];
-  __shared__ float sAqk[C][C + 1], sAkk[C][C + 1], sL[C][C + 1];
+  typedef PrepSmem<T, KD, C, E> Sm;
+  constexpr bool STAGE = Sm::STAGE;
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  Sm& sm = *reinterpret_cast<Sm*>(smem_raw);
 
   const int ch = blockIdx.x;
   const int head = ch / s.Nc, ci = ch % s.Nc;
@@ -74,107 +93,162 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
   const int t0 = ci * C;
   const int tid = threadIdx.x;
   const int w = wave_id(), l = lane_id(), g = l >> 4, n = l & 15;
+  const size_t krs = (size_t)s.H * KD;
+  const T* Qg = (const T*)in.q + (((size_t)b * s.T) * s.H + h) * KD;
+  const T* Kg = (const T*)in.k + (((size_t)b * s.T) * s.H + h) * KD;
+  const size_t eoff = (((size_t)b * s.T) * s.H + h) * E, erow = (size_t)s.H * E;
 
+  // ---- per-position vectors; Q and K rows (rows past T read clamped, then zeroed)
   for (int idx = tid; idx < C * E; idx += 256) {
     const int r = idx / E, e = idx % E;
-    const int t = t0 + r;
-    const bool ok = t < s.T;
-    const size_t off = (((size_t)b * s.T + t) * s.H + h) * E + e;
-    sq2[r][e] = ok ? ld_f((const T*)in.q2 + off) : 0.f;
-    sk2[r][e] = ok ? ld_f((const T*)in.k2 + off) : 0.f;
-    sG[r][e] = ok ? (double)in.g[off] : 0.0;
+    const size_t off = eoff + (size_t)min(t0 + r, s.T - 1) * erow + e;
+    const float x2 = ld_f((const T*)in.q2 + off), y2 = ld_f((const T*)in.k2 + off);
+    const bool ok = t0 + r < s.T;
+    sm.q2[r][e] = ok ? x2 : 0.f;
+    sm.k2[r][e] = ok ? y2 : 0.f;
   }
-  for (int r = tid; r < C; r += 256) {
-    const int t = t0 + r;
-    sbeta[r] = (t < s.T) ? (in.beta ? in.beta[((size_t)b * s.T + t) * s.H + h] : 1.f) : 0.f;
+  if (tid < C) {
+    const int t = min(t0 + tid, s.T - 1);
+    const float bv = in.beta ? in.beta[((size_t)b * s.T + t) * s.H + h] : 1.f;
+    sm.beta[tid] = (t0 + tid < s.T) ? bv : 0.f;
   }
-  __syncthreads();
-  if (tid < E) {  // in-chunk inclusive cumulative sum of the log-gates
-    double acc = 0.0;
-    for (int r = 0; r < C; ++r) {
-      acc += sG[r][tid];
-      sG[r][tid] = acc;
+  if constexpr (STAGE) {
+    constexpr int IT = (C * KD / 8 + 255) / 256;
+    Raw8<T> qv[IT], kv[IT];
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int idx = min(tid + 256 * it, C * KD / 8 - 1);
+      const int r = idx / (KD / 8), c8 = idx % (KD / 8);
+      const size_t off = (size_t)min(t0 + r, s.T - 1) * krs + 8 * c8;
+      qv[it] = load8(Qg + off);
+      kv[it] = load8(Kg + off);
     }
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int idx = tid + 256 * it;
+      if (idx >= C * KD / 8) continue;
+      const int r = idx / (KD / 8), c8 = idx % (KD / 8);
+      const bool ok = t0 + r < s.T;
+      *(Raw8<T>*)&sm.u.qk.sQ[r][8 * c8] = ok ? qv[it] : zero_raw8<T>();
+      *(Raw8<T>*)&sm.u.qk.sK[r][8 * c8] = ok ? kv[it] : zero_raw8<T>();
+    }
+  }
+  // G: inclusive cumulative sum over the chunk in fp64 (one wave per slice,
+  // lane r holds row r); after a very negative gate the running sum is large
+  // and fp32 would lose the small gates that follow it
+  for (int e = w; e < E; e += 4) {
+    const double gx = (double)in.g[eoff + (size_t)min(t0 + l, s.T - 1) * erow + e];
+    double x = (l < C && t0 + l < s.T) ? gx : 0.0;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const double y = __shfl_up(x, off, 64);
+      if (l >= off) x += y;
+    }
+    if (l < C) sm.G[l][e] = x;
   }
   __syncthreads();
 
+  // ---- coefficient vectors a = k2 gamma, b = q2 gamma, c = k2 gamma^C / gamma; gamma^C
   float* coef = p.coef + (size_t)ch * 3 * E * C;
   for (int idx = tid; idx < E * C; idx += 256) {
     const int e = idx / C, r = idx % C;
-    const double G = sG[r][e], GC = sG[C - 1][e];
+    const double G = sm.G[r][e], GC = sm.G[C - 1][e];
     const float gam = exp_nonpos((float)G);
-    coef[(0 * E + e) * C + r] = sk2[r][e] * gam;
-    coef[(1 * E + e) * C + r] = sq2[r][e] * gam;
-    coef[(2 * E + e) * C + r] = sk2[r][e] * exp_nonpos((float)(GC - G));
+    coef[(0 * E + e) * C + r] = sm.k2[r][e] * gam;
+    coef[(1 * E + e) * C + r] = sm.q2[r][e] * gam;
+    coef[(2 * E + e) * C + r] = sm.k2[r][e] * exp_nonpos((float)(GC - G));
   }
-  if (tid < E4) p.gC[(size_t)ch * E4 + tid] = (tid < E) ? exp_nonpos((float)sG[C - 1][tid]) : 0.f;
+  if (tid < E4) p.gC[(size_t)ch * E4 + tid] = (tid < E) ? exp_nonpos((float)sm.G[C - 1][tid]) : 0.f;
 
-  // A_qk = Q K^T and A_kk = K K^T, lower-triangular 16x16 tiles
-  {
-    const T* Qg = (const T*)in.q;
-    const T* Kg = (const T*)in.k;
-    const size_t rstride = (size_t)s.H * KD;
-    const size_t base = (((size_t)b * s.T) * s.H + h) * KD;
-    for (int tile = w; tile < NT * NT; tile += 4) {
-      const int rt = tile / NT, st = tile % NT;
-      if (st > rt) continue;
-      const int r = 16 * rt + n, c = 16 * st + n;
-      const bool rok = t0 + r < s.T, cok = t0 + c < s.T;
-      const T* qrow = Qg + base + (size_t)(t0 + r) * rstride;
-      const T* krow = Kg + base + (size_t)(t0 + r) * rstride;
-      const T* kcol = Kg + base + (size_t)(t0 + c) * rstride;
-      typedef typename Elem<T>::frag F;
-      F zf = cvt_frag<T>(zero4());
-      f32x4 aq = zero4(), ak = zero4();
-      mma_k<KD>(aq, [&](int kb) { return rok ? ld_frag(qrow + 16 * kb + 4 * g) : zf; },
-                [&](int kb) { return cok ? ld_frag(kcol + 16 * kb + 4 * g) : zf; });
-      mma_k<KD>(ak, [&](int kb) { return rok ? ld_frag(krow + 16 * kb + 4 * g) : zf; },
-                [&](int kb) { return cok ? ld_frag(kcol + 16 * kb + 4 * g) : zf; });
+  // ---- 16 x 16 tiles: A_qk, A_kk on MFMA, then per lane (rows 16 rt + 4 g + j,
+  // column 16 st + n) the decayed Grams R', R, M = A_qk o R' (r >= c) and
+  // L = diag(beta)(A_kk o R) (r > c); tiles above the diagonal are zero
+  auto qrow8 = [&](int r, int col) -> Raw8<T> {
+    if (col >= KD) return zero_raw8<T>();
+    if constexpr (STAGE) {
+      return *(const Raw8<T>*)&sm.u.qk.sQ[r][col];
+    } else {
+      const Raw8<T> x = load8(Qg + (size_t)min(t0 + r, s.T - 1) * krs + col);
+      return (t0 + r < s.T) ? x : zero_raw8<T>();
+    }
+  };
+  auto krow8 = [&](int r, int col) -> Raw8<T> {
+    if (col >= KD) return zero_raw8<T>();
+    if constexpr (STAGE) {
+      return *(const Raw8<T>*)&sm.u.qk.sK[r][col];
+    } else {
+      const Raw8<T> x = load8(Kg + (size_t)min(t0 + r, s.T - 1) * krs + col);
+      return (t0 + r < s.T) ? x : zero_raw8<T>();
+    }
+  };
+  float* Mg = p.M + (size_t)ch * C * C;
+  for (int tile = w; tile < NT * NT; tile += 4) {
+    constexpr int NL = NT * (NT + 1) / 2;  // lower tiles first, then the upper ones
+    int rt = 0, st = 0;
+    if (tile < NL) {
+      while ((rt + 1) * (rt + 2) / 2 <= tile) ++rt;
+      st = tile - rt * (rt + 1) / 2;
+    } else {
+      int u = tile - NL;
+      while (u >= NT - 1 - rt) {
+        u -= NT - 1 - rt;
+        ++rt;
+      }
+      st = rt + 1 + u;
+    }
+    const int c = 16 * st + n;
+    if (st > rt) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        sAqk[16 * rt + 4 * g + j][16 * st + n] = aq[j];
-        sAkk[16 * rt + 4 * g + j][16 * st + n] = ak[j];
+        const int r = 16 * rt + 4 * g + j;
+        Mg[r * C + c] = 0.f;
+        sm.L[r][c] = 0.f;
       }
+      continue;
     }
-  }
-  __syncthreads();
-
-  // R', R element by element; M = A_qk o R' (r >= s); L = diag(beta)(A_kk o R) (r > s)
-  float* Mg = p.M + (size_t)ch * C * C;
-  for (int idx = tid; idx < C * C; idx += 256) {
-    const int r = idx / C, c = idx % C;
-    float m = 0.f, lv = 0.f;
-    if (c <= r) {
+    f32x4 aq = zero4(), ak = zero4();
+#pragma unroll
+    for (int kp = 0; kp < (KD + 31) / 32; ++kp) {
+      const int col = 32 * kp + 8 * g;
+      const Raw8<T> kb = krow8(c, col);
+      mma8(aq, qrow8(16 * rt + n, col), kb);
+      mma8(ak, krow8(16 * rt + n, col), kb);
+    }
+    double Gc[E];
+    float k2c[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      Gc[e] = sm.G[c][e];
+      k2c[e] = sm.k2[c][e];
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int r = 16 * rt + 4 * g + j;
       float rq = 0.f, rk = 0.f;
+      if (c <= r) {
 #pragma unroll
-      for (int e = 0; e < E; ++e) {
-        const float d = exp_nonpos((float)(sG[r][e] - sG[c][e]));
-        rq += sq2[r][e] * sk2[c][e] * d;
-        rk += sk2[r][e] * sk2[c][e] * d;
+        for (int e = 0; e < E; ++e) {
+          const float d = exp_nonpos((float)(sm.G[r][e] - Gc[e])) * k2c[e];
+          rq += sm.q2[r][e] * d;
+          rk += sm.k2[r][e] * d;
+        }
       }
-      m = sAqk[r][c] * rq;
-      if (c < r) lv = sbeta[r] * sAkk[r][c] * rk;
+      Mg[r * C + c] = (c <= r) ? aq[j] * rq : 0.f;
+      sm.L[r][c] = (c < r) ? sm.beta[r] * ak[j] * rk : 0.f;
     }
-    Mg[idx] = m;
-    sL[r][c] = lv;
   }
   __syncthreads();
 
-  // Tu = (I + L)^{-1} diag(beta): thread c forward-substitutes column c
-  if (s.variant == 1 && tid < C) {
-    const int c = tid;
-    float x[C];
-#pragma unroll
-    for (int r = 0; r < C; ++r) {
-      float acc = 0.f;
-#pragma unroll
-      for (int j = 0; j < r; ++j) acc += sL[r][j] * x[j];
-      x[r] = (r < c) ? 0.f : ((r == c) ? 1.f : -acc);
-    }
+  // ---- Tu = (I + L)^{-1} diag(beta) (GDN), blocked unit-lower inverse in fp32
+  if (s.variant == 1) {
+    unit_lower_inverse<C, 256>([&](int r, int c) { return sm.L[r][c]; }, &sm.u.inv.X[0][0],
+                               Sm::CP, &sm.u.inv.Y[0][0][0]);
     float* Tg = p.Tu + (size_t)ch * C * C;
-    const float bc = sbeta[c];
-#pragma unroll
-    for (int r = 0; r < C; ++r) Tg[r * C + c] = x[r] * bc;
+    for (int idx = tid; idx < C * C / 4; idx += 256) {
+      const int r = idx / (C / 4), c4 = 4 * (idx % (C / 4));
+      *(f32x4*)(Tg + r * C + c4) = *(const f32x4*)&sm.u.inv.X[r][c4] *
+                                   *(const f32x4*)&sm.beta[c4];
+    }
   }
 }
 
@@ -660,7 +734,14 @@ template <typename T, int E> constexpr int fwd_waves() { return E >= 16 ? 8 : 4;
 
 template <typename T, int KD, int C, int E>
 static hipError_t prep_inst(const Shape& s, const FwdIn& in, const PrepBufs& p, hipStream_t st) {
-  hipLaunchKernelGGL((k_prep<T, KD, C, E>), dim3(s.NH * s.Nc), dim3(256), 0, st, s, in, p);
+  const size_t smem = sizeof(PrepSmem<T, KD, C, E>);
+  static bool attr_set = false;
+  if (!attr_set) {
+    (void)hipFuncSetAttribute((const void*)k_prep<T, KD, C, E>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+    attr_set = true;
+  }
+  hipLaunchKernelGGL((k_prep<T, KD, C, E>), dim3(s.NH * s.Nc), dim3(256), smem, st, s, in, p);
   return hipGetLastError();
 }
 
@@ -715,7 +796,8 @@ hipError_t launch_fwd(const Shape& s, const FwdIn& in, const PrepBufs& p, void* 
 
 template <typename T, int KD, int C, int E>
 static bool fits_inst() {
-  return sizeof(FwdSmem<T, KD, C, E, fwd_waves<T, E>()>) <= 160 * 1024;
+  return sizeof(FwdSmem<T, KD, C, E, fwd_waves<T, E>()>) <= 160 * 1024 &&
+         sizeof(PrepSmem<T, KD, C, E>) <= 160 * 1024;
 }
 
 bool fits_lds(int K, int C, int E, bool bf16) {
