@@ -401,10 +401,7 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
       if (e >= E) continue;
       T* dst = (T*)bb.dSck + ((ch * E + e) * (size_t)(V / 16) + vt) * KD * 16;
 #pragma unroll
-      for (int kt = 0; kt < KT; ++kt)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          dst[(16 * kt + 4 * g + j) * 16 + n] = Elem<T>::from_f(dS[i][kt][j]);
+      for (int kt = 0; kt < KT; ++kt) store_tile16(dst + 256 * kt, dS[i][kt], g, n);
     }
 
     // ---- partial of sum_e diag(c_e) K dS'_e over the owned slices

@@ -350,6 +350,35 @@ __device__ __forceinline__ float group16_transpose_sum(const float (&v)[16], int
   return (b0 ? c[1] : c[0]) + dpp_f<0xB1>(send);        // quad_perm [1,0,3,2]
 }
 
+// Store a 16 x 16 accumulator tile (lane (g, n) holds rows 4 g + j, column n)
+// into a row-major 16 x 16 tile at dst (row r at dst + 16 r).  Two DPP
+// exchange rounds transpose 4 x 4 blocks within each quad of lanes, after
+// which lane n holds row 4 g + n % 4, columns 4 (n / 4) .. + 3 and writes
+// them with one 8-byte (bf16) or 16-byte (fp32) store instead of four
+// scalar ones.
+template <typename T>
+__device__ __forceinline__ void store_tile16(T* dst, f32x4 x, int g, int n) {
+  const int i = n & 3;
+  const bool b0 = i & 1, b1 = i & 2;
+  float t = dpp_f<0xB1>(b0 ? x[0] : x[1]);  // lanes differing in bit 0
+  x[0] = b0 ? t : x[0];
+  x[1] = b0 ? x[1] : t;
+  t = dpp_f<0xB1>(b0 ? x[2] : x[3]);
+  x[2] = b0 ? t : x[2];
+  x[3] = b0 ? x[3] : t;
+  t = dpp_f<0x4E>(b1 ? x[0] : x[2]);        // lanes differing in bit 1
+  x[0] = b1 ? t : x[0];
+  x[2] = b1 ? x[2] : t;
+  t = dpp_f<0x4E>(b1 ? x[1] : x[3]);
+  x[1] = b1 ? t : x[1];
+  x[3] = b1 ? x[3] : t;
+  T* p = dst + (4 * g + i) * 16 + 4 * (n >> 2);
+  if constexpr (sizeof(T) == 2)
+    *(uint2*)p = __builtin_bit_cast(uint2, cvt_frag<bf16_t>(x));
+  else
+    *(f32x4*)p = x;
+}
+
 // XCD-aware block mapping: the 8 accelerator dies each have their own L2 and
 // receive blocks round-robin by linear id.  Blocks that share a head (the
 // value tiles of one head read the same chunk inputs) are placed on one die.

@@ -497,10 +497,7 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
         if (e >= E) continue;
         T* dst = (T*)sv.Sck + ((ch * E + e) * (size_t)(V / 16) + vt) * KD * 16;
 #pragma unroll
-        for (int kt = 0; kt < KT; ++kt)
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-            dst[(16 * kt + 4 * g + j) * 16 + n] = Elem<T>::from_f(S[i][kt][j]);
+        for (int kt = 0; kt < KT; ++kt) store_tile16(dst + 256 * kt, S[i][kt], g, n);
       }
     }
 
