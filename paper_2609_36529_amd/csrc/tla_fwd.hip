@@ -304,13 +304,16 @@ struct FwdStage {
   // index past the end from the last element) and store() zeroes or skips
   // what is out of range: a per-lane branch around a load would make the
   // compiler wait for it at once, which defeats the prefetch.
+  // parts: 1 = the K, Q rows and the V tile; 2 = M, Tu and the vectors (the
+  // two halves are issued at different points of a chunk step)
   __device__ __forceinline__ void load(const Shape& s, const FwdIn& in, const PrepBufs& p,
                                        const T* Kg, const T* Qg, const T* Vg, int b, int h,
-                                       int ci) {
+                                       int ci, int parts = 3) {
     const int tid = threadIdx.x;
     const int t0 = ci * C;
     const size_t ch = (size_t)(b * s.H + h) * s.Nc + ci;
     const size_t krs = (size_t)s.H * KD, vrs = (size_t)s.H * s.V;
+    if (parts & 1) {
 #pragma unroll
     for (int i = 0; i < NKB; ++i) {
       const int blk = min(tid + i * NTHR, RB * CB - 1);
@@ -339,6 +342,8 @@ struct FwdStage {
         v[i][3] = x.w;
       }
     }
+    }
+    if (!(parts & 2)) return;
     const float* Mg = p.M + ch * C * C;
     const float* Tg = p.Tu + ch * C * C;
 #pragma unroll
@@ -480,8 +485,6 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
     // ---- stage the chunk from registers (loaded during the previous chunk)
     stage.store(sm, s.variant, ci * C, s.T);
     __syncthreads();
-    // next chunk's inputs are in flight while this chunk computes
-    if (ci + 1 < s.Nc) stage.load(s, in, p, Kg, Qg, Vg, b, h, ci + 1);
 
     // ---- operand copies of the chunk-start state
     F Sop[SPW][KT];
@@ -567,6 +570,8 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
       }
     }
     __syncthreads();
+    // the next chunk's rows are in flight while this chunk computes
+    if (ci + 1 < s.Nc) stage.load(s, in, p, Kg, Qg, Vg, b, h, ci + 1, 1);
 
     // ---- U = Tu (V - W) (GDN) or diag(beta) V (sGLA); every wave keeps all of U
     f32x4 U[NT];
@@ -658,6 +663,9 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
       }
     }
 
+    // (the next chunk's M, Tu and vectors: gamma^C and the coefficients are
+    // read from LDS below, so their registers are only refilled here)
+    if (ci + 1 < s.Nc) stage.load(s, in, p, Kg, Qg, Vg, b, h, ci + 1, 2);
     // ---- state update S_e <- gamma^C_e S_e + K^T diag(c_e) U
     F Uc[SPW][NT], Ucl[SPW][NT];
 #pragma unroll
