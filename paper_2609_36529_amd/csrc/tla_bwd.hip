@@ -126,11 +126,15 @@ struct RecStage {
   // block index past the end from the last block, and store() zeroes or
   // skips them.  (A per-lane branch around a load would make the compiler
   // wait for the load right away, which defeats the prefetch.)
+  // parts: 1 = the K, Q rows and the dO tile; 2 = M, Tu and the vectors (the
+  // two halves are issued at different points of a chunk step)
   __device__ __forceinline__ void load(const Shape& s, const PrepBufs& p, const T* Kg,
-                                       const T* Qg, const T* dOg, size_t ch, int ci) {
+                                       const T* Qg, const T* dOg, size_t ch, int ci,
+                                       int parts = 3) {
     const int tid = threadIdx.x;
     const int t0 = ci * C;
     const size_t krs = (size_t)s.H * KD, vrs = (size_t)s.H * s.V;
+    if (parts & 1) {
 #pragma unroll
     for (int i = 0; i < NKB; ++i) {
       const int blk = min(tid + i * NTHR, RB * KCB - 1);
@@ -152,6 +156,8 @@ struct RecStage {
         ld_words(d[i][rr], dOg + (size_t)t * vrs + 4 * c4);
       }
     }
+    }
+    if (!(parts & 2)) return;
     const float* Mg = p.M + ch * C * C;
     const float* Tg = p.Tu + ch * C * C;
 #pragma unroll
@@ -325,7 +331,6 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
     // ---- this chunk's inputs to LDS; the next chunk's loads go in flight
     if constexpr (PREFETCH) {
       stage.store(sm, s.variant, t0, s.T);
-      if (ci > 0) stage.load(s, p, Kg, Qg, dOg, ch - 1, ci - 1);
     } else {
       // ---- stage: K rows, K^T, Q^T, dO tile^T, M^T, Tu^T (split), coefficients
       constexpr int RB = C / 4, CB = KD / 8;
@@ -450,6 +455,9 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
     }
     __syncthreads();
 
+    // the next chunk's rows are in flight while this chunk computes
+    if constexpr (PREFETCH)
+      if (ci > 0) stage.load(s, p, Kg, Qg, dOg, ch - 1, ci - 1, 1);
     // ---- dU = M^T dO + sum of the partials; dW = -Tu^T dU (every wave keeps both)
     f32x4 dU[NT], dW[NT];
     F dUh[NT], dUl[NT];
@@ -495,6 +503,10 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
       }
     }
 
+    // (the next chunk's M, Tu and vectors; the update below reads its
+    // coefficients from LDS)
+    if constexpr (PREFETCH)
+      if (ci > 0) stage.load(s, p, Kg, Qg, dOg, ch - 1, ci - 1, 2);
     // ---- dS_e <- gamma^C_e dS'_e + Q^T diag(b_e) dO + K^T diag(a_e) dW
     // (B operands of a group of owned slices first; each Q^T / K^T fragment is
     // read once per group; four-wave instances take all owned slices at once)
