@@ -95,6 +95,8 @@ struct RecSmem {
   alignas(16) float coef[3][E][C];
   alignas(16) float gC[E4];
   alignas(16) f32x4 X[NW][NT][64];  // per-wave partials of sum_e diag(c_e) K dS'_e
+  alignas(16) typename Elem<T>::frag dUs[SPLIT ? 2 : 1][NT][64];  // dU as B operands (hi, lo)
+  alignas(16) f32x4 dWs[NT][64];
 };
 
 // Register staging of one chunk's inputs for the reverse recurrence: the
@@ -458,11 +460,10 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
     // the next chunk's rows are in flight while this chunk computes
     if constexpr (PREFETCH)
       if (ci > 0) stage.load(s, p, Kg, Qg, dOg, ch - 1, ci - 1, 1);
-    // ---- dU = M^T dO + sum of the partials; dW = -Tu^T dU (every wave keeps both)
-    f32x4 dU[NT], dW[NT];
-    F dUh[NT], dUl[NT];
-#pragma unroll
-    for (int rt = 0; rt < NT; ++rt) {
+    // ---- dU = M^T dO + sum of the partials, then dW = -Tu^T dU: wave w < NT
+    // forms row tile w of each, and the tiles are exchanged through LDS
+    if (w < NT) {
+      const int rt = w;
       f32x4 acc = zero4();
 #pragma unroll
       for (int ww = 0; ww < NW; ++ww) acc += sm.X[ww][rt][l];
@@ -471,36 +472,42 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
       bmma_k<C>(acc, [&](int kb) { return ld_frag(&sm.MT[r][16 * kb + 4 * g]); }, dof);
       if constexpr (Sm::SPLIT)
         bmma_k<C>(acc, [&](int kb) { return ld_frag(&sm.MTL[r][16 * kb + 4 * g]); }, dof);
-      dU[rt] = acc;
-      split_frag(acc, dUh[rt], dUl[rt]);
-    }
-    if (s.variant == 1) {
+      F hi, lo;
+      split_frag(acc, hi, lo);
+      sm.dUs[0][rt][l] = hi;
+      if constexpr (Sm::SPLIT) sm.dUs[1][rt][l] = lo;
+      float* du = bb.dU + ch * C * (size_t)V + (size_t)(16 * rt + 4 * g) * V + v0 + n;
 #pragma unroll
-      for (int rt = 0; rt < NT; ++rt) {
-        f32x4 acc = zero4();
-        const int r = 16 * rt + n;
-        auto th = [&](int kb) { return ld_frag(&sm.TuT[r][16 * kb + 4 * g]); };
-        bmma_k<C>(acc, th, [&](int kb) { return dUh[kb]; });
-        if constexpr (Sm::SPLIT) {
-          bmma_k<C>(acc, th, [&](int kb) { return dUl[kb]; });
-          bmma_k<C>(acc, [&](int kb) { return ld_frag(&sm.TuTL[r][16 * kb + 4 * g]); },
-                    [&](int kb) { return dUh[kb]; });
-        }
-        dW[rt] = -acc;
-      }
-    } else {
-#pragma unroll
-      for (int rt = 0; rt < NT; ++rt) dW[rt] = zero4();
+      for (int j = 0; j < 4; ++j) du[(size_t)j * V] = acc[j];
     }
+    __syncthreads();
     if (w < NT) {
       const int rt = w;
-      float* du = bb.dU + ch * C * (size_t)V + (size_t)(16 * rt + 4 * g) * V + v0 + n;
+      f32x4 acc = zero4();
+      if (s.variant == 1) {
+        const int r = 16 * rt + n;
+        auto th = [&](int kb) { return ld_frag(&sm.TuT[r][16 * kb + 4 * g]); };
+        bmma_k<C>(acc, th, [&](int kb) { return sm.dUs[0][kb][l]; });
+        if constexpr (Sm::SPLIT) {
+          bmma_k<C>(acc, th, [&](int kb) { return sm.dUs[1][kb][l]; });
+          bmma_k<C>(acc, [&](int kb) { return ld_frag(&sm.TuTL[r][16 * kb + 4 * g]); },
+                    [&](int kb) { return sm.dUs[0][kb][l]; });
+        }
+        acc = -acc;
+        sm.dWs[rt][l] = acc;
+      }
       float* dw = bb.dW + ch * C * (size_t)V + (size_t)(16 * rt + 4 * g) * V + v0 + n;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        du[(size_t)j * V] = dU[rt][j];
-        dw[(size_t)j * V] = dW[rt][j];
-      }
+      for (int j = 0; j < 4; ++j) dw[(size_t)j * V] = acc[j];
+    }
+    f32x4 dW[NT];
+    if (s.variant == 1) {
+      __syncthreads();
+#pragma unroll
+      for (int kb = 0; kb < NT; ++kb) dW[kb] = sm.dWs[kb][l];
+    } else {
+#pragma unroll
+      for (int kb = 0; kb < NT; ++kb) dW[kb] = zero4();
     }
 
     // (the next chunk's M, Tu and vectors; the update below reads its
