@@ -277,6 +277,7 @@ struct FwdSmem {
   alignas(16) float beta[C];
   alignas(16) f32x4 W[NW][NT][64];
   alignas(16) f32x4 O[NW][NT][64];
+  alignas(16) f32x4 Us[NT][64];  // U row tiles in the accumulator layout
 };
 
 // Register staging of one chunk's inputs for the recurrent forward: global
@@ -573,63 +574,71 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
     // the next chunk's rows are in flight while this chunk computes
     if (ci + 1 < s.Nc) stage.load(s, in, p, Kg, Qg, Vg, b, h, ci + 1, 1);
 
-    // ---- U = Tu (V - W) (GDN) or diag(beta) V (sGLA); every wave keeps all of U
-    f32x4 U[NT];
-    if (s.variant == 1) {
-      F Xh[NT], Xl[NT];
+    // ---- U = Tu (V - W) (GDN) or diag(beta) V (sGLA): wave w < NT forms row
+    // tile w (Tu is lower triangular: blocks kb <= w only) and the tiles are
+    // exchanged through LDS
+    if (w < NT) {
+      const int rt = w;
+      f32x4 u;
+      if (s.variant == 1) {
+        F Xh[NT], Xl[NT];
 #pragma unroll
-      for (int rt = 0; rt < NT; ++rt) {
-        f32x4 x = ld4_f(&sm.Vt[n][16 * rt + 4 * g]);
+        for (int kb = 0; kb < NT; ++kb) {
+          if (kb > rt) {
+            Xh[kb] = Xl[kb] = cvt_frag<T>(zero4());
+            continue;
+          }
+          f32x4 x = ld4_f(&sm.Vt[n][16 * kb + 4 * g]);
 #pragma unroll
-        for (int ww = 0; ww < NW; ++ww) x -= sm.W[ww][rt][l];
-        split_frag(x, Xh[rt], Xl[rt]);
-        if (train && rt == w) {
-          float* dst = sv.X + ch * C * (size_t)V + (size_t)(16 * rt + 4 * g) * V + v0 + n;
+          for (int ww = 0; ww < NW; ++ww) x -= sm.W[ww][kb][l];
+          split_frag(x, Xh[kb], Xl[kb]);
+          if (train && kb == rt) {
+            float* dst = sv.X + ch * C * (size_t)V + (size_t)(16 * rt + 4 * g) * V + v0 + n;
 #pragma unroll
-          for (int j = 0; j < 4; ++j) dst[(size_t)j * V] = x[j];
+            for (int j = 0; j < 4; ++j) dst[(size_t)j * V] = x[j];
+          }
         }
-      }
+        u = zero4();
+        const int r = 16 * rt + n;
 #pragma unroll
-      for (int rt = 0; rt < NT; ++rt) U[rt] = zero4();
-      // k-block outer: NT independent accumulators per step
-#pragma unroll
-      for (int kb = 0; kb < NT; kb += (NT > 1 ? 2 : 1)) {
-        if constexpr (NT > 1) {
-          F h0[NT], h1[NT], l0[NT], l1[NT];
-#pragma unroll
-          for (int rt = 0; rt < NT; ++rt) {
-            h0[rt] = ld_frag(&sm.Tu[16 * rt + n][16 * kb + 4 * g]);
-            h1[rt] = ld_frag(&sm.Tu[16 * rt + n][16 * kb + 16 + 4 * g]);
+        for (int kb = 0; kb < NT; kb += (NT > 1 ? 2 : 1)) {
+          if (kb > rt) continue;
+          if constexpr (NT > 1) {
+            const F h0 = ld_frag(&sm.Tu[r][16 * kb + 4 * g]);
+            const F h1 = ld_frag(&sm.Tu[r][16 * kb + 16 + 4 * g]);
+            mma32(u, h0, h1, Xh[kb], Xh[kb + 1]);
             if constexpr (Sm::SPLIT) {
-              l0[rt] = ld_frag(&sm.TuL[16 * rt + n][16 * kb + 4 * g]);
-              l1[rt] = ld_frag(&sm.TuL[16 * rt + n][16 * kb + 16 + 4 * g]);
+              mma32(u, h0, h1, Xl[kb], Xl[kb + 1]);
+              mma32(u, ld_frag(&sm.TuL[r][16 * kb + 4 * g]),
+                    ld_frag(&sm.TuL[r][16 * kb + 16 + 4 * g]), Xh[kb], Xh[kb + 1]);
+            }
+          } else {
+            const F hh = ld_frag(&sm.Tu[n][4 * g]);
+            mma16(u, hh, Xh[0]);
+            if constexpr (Sm::SPLIT) {
+              mma16(u, hh, Xl[0]);
+              mma16(u, ld_frag(&sm.TuL[n][4 * g]), Xh[0]);
             }
           }
-#pragma unroll
-          for (int rt = 0; rt < NT; ++rt) mma32(U[rt], h0[rt], h1[rt], Xh[kb], Xh[kb + 1]);
-          if constexpr (Sm::SPLIT) {
-#pragma unroll
-            for (int rt = 0; rt < NT; ++rt) mma32(U[rt], h0[rt], h1[rt], Xl[kb], Xl[kb + 1]);
-#pragma unroll
-            for (int rt = 0; rt < NT; ++rt) mma32(U[rt], l0[rt], l1[rt], Xh[kb], Xh[kb + 1]);
-          }
-        } else {
-          const F hh = ld_frag(&sm.Tu[n][4 * g]);
-          mma16(U[0], hh, Xh[0]);
-          if constexpr (Sm::SPLIT) {
-            mma16(U[0], hh, Xl[0]);
-            mma16(U[0], ld_frag(&sm.TuL[n][4 * g]), Xh[0]);
-          }
         }
+      } else {
+        u = ld4_f(&sm.Vt[n][16 * rt + 4 * g]) * *(const f32x4*)&sm.beta[16 * rt + 4 * g];
       }
-    } else {
+      sm.Us[rt][l] = u;
+      if (train) {
+        float* dst = sv.U + ch * C * (size_t)V + (size_t)(16 * rt + 4 * g) * V + v0 + n;
 #pragma unroll
-      for (int rt = 0; rt < NT; ++rt)
-        U[rt] = ld4_f(&sm.Vt[n][16 * rt + 4 * g]) * *(const f32x4*)&sm.beta[16 * rt + 4 * g];
+        for (int j = 0; j < 4; ++j) dst[(size_t)j * V] = u[j];
+      }
     }
+    __syncthreads();
+    f32x4 U[NT];
     F Uh[NT], Ul[NT];
 #pragma unroll
-    for (int rt = 0; rt < NT; ++rt) split_frag(U[rt], Uh[rt], Ul[rt]);
+    for (int rt = 0; rt < NT; ++rt) {
+      U[rt] = sm.Us[rt][l];
+      split_frag(U[rt], Uh[rt], Ul[rt]);
+    }
 
     // ---- O for row tile w: sum of the partials plus M U
     if (w < NT) {
@@ -655,11 +664,6 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
           else
             ((float*)out)[off] = acc[j];
         }
-      }
-      if (train) {
-        float* dst = sv.U + ch * C * (size_t)V + (size_t)(16 * rt + 4 * g) * V + v0 + n;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) dst[(size_t)j * V] = U[rt][j];
       }
     }
 
