@@ -281,6 +281,7 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
                                                      const float* dS_final, PrepBufs p,
                                                      BwdBufs bb, float* ds0) {
   constexpr int SPW = (E + NW - 1) / NW;
+  constexpr bool RAGGED = E % NW != 0;  // some waves own fewer slices
   constexpr int NT = C / 16;
   constexpr int KT = KD / 16;
   constexpr int NTHR = NW * 64;
@@ -405,7 +406,7 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
 #pragma unroll
     for (int i = 0; i < SPW; ++i) {
       const int e = w * SPW + i;
-      if (e >= E) continue;
+      if (RAGGED && e >= E) continue;
       T* dst = (T*)bb.dSck + ((ch * E + e) * (size_t)(V / 16) + vt) * KD * 16;
 #pragma unroll
       for (int kt = 0; kt < KT; ++kt) store_tile16(dst + 256 * kt, dS[i][kt], g, n);
@@ -438,20 +439,20 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
           const F k0 = kfrag(kb), k1 = kfrag(kb + 1);
 #pragma unroll
           for (int i = i0; i < i0 + GZ; ++i)
-            if (w * SPW + i < E) mma32(z[i], k0, k1, dSop[i][kb], dSop[i][kb + 1]);
+            if (!RAGGED || w * SPW + i < E) mma32(z[i], k0, k1, dSop[i][kb], dSop[i][kb + 1]);
         }
         if constexpr (KT & 1) {
           const F k0 = kfrag(KT - 1);
 #pragma unroll
           for (int i = i0; i < i0 + GZ; ++i)
-            if (w * SPW + i < E) mma16(z[i], k0, dSop[i][KT - 1]);
+            if (!RAGGED || w * SPW + i < E) mma16(z[i], k0, dSop[i][KT - 1]);
         }
       }
       f32x4 acc = zero4();
 #pragma unroll
       for (int i = 0; i < SPW; ++i) {
         const int e = w * SPW + i;
-        if (e < E) acc += *(const f32x4*)&sm.coef[2][e][16 * rt + 4 * g] * z[i];
+        if (!RAGGED || e < E) acc += *(const f32x4*)&sm.coef[2][e][16 * rt + 4 * g] * z[i];
       }
       sm.X[w][rt][l] = acc;
     }
@@ -526,7 +527,7 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
 #pragma unroll
       for (int ii = 0; ii < GS; ++ii) {
         const int e = w * SPW + i0 + ii;
-        if (e >= E) continue;
+        if (RAGGED && e >= E) continue;
         gcs[ii] = sm.gC[e];
 #pragma unroll
         for (int kb = 0; kb < NT; ++kb) {
@@ -553,7 +554,7 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
           }
 #pragma unroll
           for (int ii = 0; ii < GS; ++ii) {
-            if (w * SPW + i0 + ii >= E) continue;
+            if (RAGGED && w * SPW + i0 + ii >= E) continue;
             mma32(acc[ii], q0, q1, bh[ii][kb], bh[ii][kb + 1]);
             if constexpr (Sm::SPLIT) mma32(acc[ii], q0, q1, bl[ii][kb], bl[ii][kb + 1]);
             if (gdn) {
@@ -569,7 +570,7 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
           if (gdn) k0 = ld_frag(&sm.Kt[r][16 * kb + 4 * g]);
 #pragma unroll
           for (int ii = 0; ii < GS; ++ii) {
-            if (w * SPW + i0 + ii >= E) continue;
+            if (RAGGED && w * SPW + i0 + ii >= E) continue;
             mma16(acc[ii], q0, bh[ii][kb]);
             if constexpr (Sm::SPLIT) mma16(acc[ii], q0, bl[ii][kb]);
             if (gdn) {
@@ -580,7 +581,7 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
         }
 #pragma unroll
         for (int ii = 0; ii < GS; ++ii)
-          if (w * SPW + i0 + ii < E) dS[i0 + ii][kt] = acc[ii];
+          if (!RAGGED || w * SPW + i0 + ii < E) dS[i0 + ii][kt] = acc[ii];
       }
     }
   }
@@ -589,7 +590,7 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
 #pragma unroll
     for (int i = 0; i < SPW; ++i) {
       const int e = w * SPW + i;
-      if (e >= E) continue;
+      if (RAGGED && e >= E) continue;
 #pragma unroll
       for (int kt = 0; kt < KT; ++kt) {
         float* dst = ds0 + (((size_t)head * E + e) * KD + 16 * kt + 4 * g) * V + v0 + n;
@@ -637,7 +638,9 @@ __global__ __launch_bounds__(256) void k_bwd_state(Shape s, FwdIn in, const void
   extern __shared__ __align__(16) unsigned char smem_raw[];
   Sm& sm = *reinterpret_cast<Sm*>(smem_raw);
 
-  const int tid = threadIdx.x, w = wave_id(), l = lane_id(), g = l >> 4, n = l & 15;
+  // (the wave index is left unmarked here: with uniform branches the
+  // compiler hoists this kernel's loads further and spills registers)
+  const int tid = threadIdx.x, w = threadIdx.x >> 6, l = lane_id(), g = l >> 4, n = l & 15;
   const int V = s.V;
   const int VB = V / 16;
   const int NP = (VB + 1) / 2;

@@ -26,7 +26,9 @@ typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef uint16_t bf16_t;  // bf16 storage in global memory
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
-__device__ __forceinline__ int wave_id() { return threadIdx.x >> 6; }
+// The wave index, marked uniform (read from the first lane) so that branches
+// on it are scalar and do not split the wave's code into exec-masked blocks.
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 
 __device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
 

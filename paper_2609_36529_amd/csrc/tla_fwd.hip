@@ -438,6 +438,7 @@ template <typename T, int KD, int C, int E, int NW>
 __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, void* out,
                                                  float* s_final, SavedBufs sv, int train) {
   constexpr int SPW = (E + NW - 1) / NW;
+  constexpr bool RAGGED = E % NW != 0;  // some waves own fewer slices
   constexpr int NT = C / 16;
   constexpr int KT = KD / 16;
   constexpr int NTHR = NW * 64;
@@ -498,7 +499,7 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
 #pragma unroll
       for (int i = 0; i < SPW; ++i) {
         const int e = w * SPW + i;
-        if (e >= E) continue;
+        if (RAGGED && e >= E) continue;
         T* dst = (T*)sv.Sck + ((ch * E + e) * (size_t)(V / 16) + vt) * KD * 16;
 #pragma unroll
         for (int kt = 0; kt < KT; ++kt) store_tile16(dst + 256 * kt, S[i][kt], g, n);
@@ -539,7 +540,7 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
           }
 #pragma unroll
           for (int i = 0; i < SPW; ++i) {
-            if (w * SPW + i >= E) continue;
+            if (RAGGED && w * SPW + i >= E) continue;
 #pragma unroll
             for (int rt = 0; rt < NT; ++rt) mma32(P[i][rt], a0[rt], a1[rt], Sop[i][kb], Sop[i][kb + 1]);
           }
@@ -549,7 +550,7 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
           for (int rt = 0; rt < NT; ++rt) a[rt] = afrag(rt, 0);
 #pragma unroll
           for (int i = 0; i < SPW; ++i) {
-            if (w * SPW + i >= E) continue;
+            if (RAGGED && w * SPW + i >= E) continue;
 #pragma unroll
             for (int rt = 0; rt < NT; ++rt) mma16(P[i][rt], a[rt], Sop[i][0]);
           }
@@ -561,7 +562,7 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
 #pragma unroll
         for (int i = 0; i < SPW; ++i) {
           const int e = w * SPW + i;
-          if (e >= E) continue;
+          if (RAGGED && e >= E) continue;
           acc += *(const f32x4*)&sm.coef[pass][e][16 * rt + 4 * g] * P[i][rt];
         }
         if (pass == 0)
@@ -675,7 +676,7 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
 #pragma unroll
     for (int i = 0; i < SPW; ++i) {
       const int e = w * SPW + i;
-      if (e >= E) continue;
+      if (RAGGED && e >= E) continue;
       const float gc = sm.gC[e];
 #pragma unroll
       for (int kt = 0; kt < KT; ++kt) S[i][kt] *= gc;
@@ -695,7 +696,7 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
         }
 #pragma unroll
         for (int i = 0; i < SPW; ++i) {
-          if (w * SPW + i >= E) continue;
+          if (RAGGED && w * SPW + i >= E) continue;
 #pragma unroll
           for (int kt = 0; kt < KT; ++kt) mma32(S[i][kt], a0[kt], a1[kt], Uc[i][kb], Uc[i][kb + 1]);
           if constexpr (Sm::SPLIT) {
@@ -710,7 +711,7 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
         for (int kt = 0; kt < KT; ++kt) a[kt] = ld_frag(&sm.Kt[16 * kt + n][4 * g]);
 #pragma unroll
         for (int i = 0; i < SPW; ++i) {
-          if (w * SPW + i >= E) continue;
+          if (RAGGED && w * SPW + i >= E) continue;
 #pragma unroll
           for (int kt = 0; kt < KT; ++kt) {
             mma16(S[i][kt], a[kt], Uc[i][0]);
@@ -725,7 +726,7 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
 #pragma unroll
     for (int i = 0; i < SPW; ++i) {
       const int e = w * SPW + i;
-      if (e >= E) continue;
+      if (RAGGED && e >= E) continue;
 #pragma unroll
       for (int kt = 0; kt < KT; ++kt) {
         float* dst = s_final + (((size_t)head * E + e) * KD + 16 * kt + 4 * g) * V + v0 + n;
