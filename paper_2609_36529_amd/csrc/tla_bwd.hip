@@ -1001,8 +1001,13 @@ struct ChunkSmem {
   alignas(16) float dbeta[C];
 };
 
+// Eight waves (two per SIMD): every phase is latency-bound at this size, so
+// the second wave per SIMD hides LDS and memory latency of the first.
+constexpr int CHUNK_NW = 8;
+constexpr int CHUNK_NTHR = CHUNK_NW * 64;
+
 template <typename T, int KD, int C, int E>
-__global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void* dOv,
+__global__ __launch_bounds__(CHUNK_NTHR) void k_bwd_chunk(Shape s, FwdIn in, const void* dOv,
                                                    SavedBufs sv, BwdBufs bb, void* dqv, void* dkv,
                                                    void* dvv, void* dq2v, void* dk2v, float* dg,
                                                    float* dbeta) {
@@ -1010,6 +1015,7 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
   constexpr int KT = KD / 16;
   constexpr int E4 = (E + 3) & ~3;
   constexpr int NVPMAX = 4;  // pairs of 16-column value blocks, V <= 128
+  constexpr int NW = CHUNK_NW, NTHR = CHUNK_NTHR;
   typedef typename Elem<T>::frag F;
   typedef ChunkSmem<T, KD, C, E> Sm;
   constexpr bool STAGE_QK = Sm::STAGE_QK;
@@ -1038,23 +1044,23 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
   const bool gdn = s.variant == 1;
 
   // ---- phase 0: per-position vectors, Q and K rows, in-chunk cumulative log-gates
-  for (int idx = tid; idx < C * E; idx += 256) {
+  for (int idx = tid; idx < C * E; idx += NTHR) {
     const int r = idx / E, e = idx % E;
     const int t = t0 + r;
     const bool ok = t < s.T;
     sm.q2[r][e] = ok ? ld_f((const T*)in.q2 + eoff + (size_t)t * erow + e) : 0.f;
     sm.k2[r][e] = ok ? ld_f((const T*)in.k2 + eoff + (size_t)t * erow + e) : 0.f;
   }
-  for (int r = tid; r < C; r += 256) {
+  for (int r = tid; r < C; r += NTHR) {
     const int t = t0 + r;
     sm.beta[r] = (t < s.T) ? (in.beta ? in.beta[((size_t)b * s.T + t) * s.H + h] : 1.f) : 0.f;
   }
   if constexpr (STAGE_QK) {
-    constexpr int IT = (C * KD / 8 + 255) / 256;
+    constexpr int IT = (C * KD / 8 + NTHR - 1) / NTHR;
     Raw8<T> qv[IT], kv[IT];
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
-      const int idx = tid + 256 * it;
+      const int idx = tid + NTHR * it;
       const int r = idx / (KD / 8), c8 = idx % (KD / 8);
       const int t = t0 + r;
       qv[it] = zero_raw8<T>();
@@ -1066,7 +1072,7 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
     }
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
-      const int idx = tid + 256 * it;
+      const int idx = tid + NTHR * it;
       if (idx >= C * KD / 8) continue;
       const int r = idx / (KD / 8), c8 = idx % (KD / 8);
       *(Raw8<T>*)&sm.u1.qk.sQ[r][8 * c8] = qv[it];
@@ -1075,7 +1081,7 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
   }
   // G = inclusive cumulative sum of g over the chunk, in fp64: one wave per
   // slice, lane r holds row r
-  for (int e = w; e < E; e += 4) {
+  for (int e = w; e < E; e += NW) {
     const int t = t0 + l;
     double x = (l < C && t < s.T) ? (double)in.g[eoff + (size_t)t * erow + e] : 0.0;
 #pragma unroll
@@ -1104,7 +1110,7 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
   // then R', R and  dR' = dM o A_qk, dA_qk = dM o R'  element by element
   // tiles in the order: the NT (NT + 1) / 2 lower ones, then the upper ones,
   // dealt round-robin to the waves
-  for (int tile = w; tile < NT * NT; tile += 4) {
+  for (int tile = w; tile < NT * NT; tile += NW) {
     constexpr int NL = NT * (NT + 1) / 2;
     int rt = 0, st = 0;
     if (tile < NL) {
@@ -1211,14 +1217,14 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
 
   if (gdn) {
     // ---- (I + L)^{-1} with L = diag(beta)(A_kk o R), strictly lower
-    unit_lower_inverse<C, 256>(
+    unit_lower_inverse<C, NTHR>(
         [&](int r, int c) { return sm.beta[r] * sm.Akk[r][c] * sm.u2.r.R[r][c]; },
         &sm.u2.r.X1[0][0], Sm::CP, &sm.Y[0][0][0]);
     // ---- P = N^{-T} dTu on MFMA (fp32 operands); N^{-T} is upper triangular
-    f32x4 pt[(NT * NT + 3) / 4];
+    f32x4 pt[(NT * NT + NW - 1) / NW];
 #pragma unroll
-    for (int i = 0; i < (NT * NT + 3) / 4; ++i) {
-      const int tile = w + 4 * i;
+    for (int i = 0; i < (NT * NT + NW - 1) / NW; ++i) {
+      const int tile = w + NW * i;
       f32x4 acc = zero4();
       if (tile < NT * NT) {
         const int rt = tile / NT, ct = tile % NT;
@@ -1236,8 +1242,8 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
     }
     __syncthreads();
 #pragma unroll
-    for (int i = 0; i < (NT * NT + 3) / 4; ++i) {
-      const int tile = w + 4 * i;
+    for (int i = 0; i < (NT * NT + NW - 1) / NW; ++i) {
+      const int tile = w + NW * i;
       if (tile < NT * NT) {
         const int rt = tile / NT, ct = tile % NT;
 #pragma unroll
@@ -1248,8 +1254,8 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
     if (tid < C) sm.dbeta[tid] = sm.dT[tid][tid];  // diag(N^{-T} dTu)
     // ---- dL = tril(-P Tu^T, -1) with Tu = N^{-1} diag(beta)
 #pragma unroll
-    for (int i = 0; i < (NT * NT + 3) / 4; ++i) {
-      const int tile = w + 4 * i;
+    for (int i = 0; i < (NT * NT + NW - 1) / NW; ++i) {
+      const int tile = w + NW * i;
       f32x4 acc = zero4();
       if (tile < NT * NT) {
         const int rt = tile / NT, st = tile % NT;
@@ -1267,8 +1273,8 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
     __syncthreads();
     // element (4g+j, n) of tile (rt, st) is dL[16 rt + 4 g + j][16 st + n]
 #pragma unroll
-    for (int i = 0; i < (NT * NT + 3) / 4; ++i) {
-      const int tile = w + 4 * i;
+    for (int i = 0; i < (NT * NT + NW - 1) / NW; ++i) {
+      const int tile = w + NW * i;
       if (tile < NT * NT) {
         const int rt = tile / NT, st = tile % NT;
 #pragma unroll
@@ -1290,7 +1296,7 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
       sm.dbeta[tid] += acc;
     }
   } else {
-    for (int idx = tid; idx < C * C; idx += 256) {
+    for (int idx = tid; idx < C * C; idx += NTHR) {
       sm.Akk[idx / C][idx % C] = 0.f;  // dR
       sm.dT[idx / C][idx % C] = 0.f;   // dA_kk
     }
@@ -1319,7 +1325,7 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
   // then dA_qk^T and dA_kk + dA_kk^T (over the dead Q / K rows)
   if constexpr (STAGE_QK) {
     constexpr int NB = (C / 4) * (KD / 4);
-    for (int idx = tid; idx < 2 * NB; idx += 256) {
+    for (int idx = tid; idx < 2 * NB; idx += NTHR) {
       const int m = idx / NB, bi = idx % NB;
       const int rb = bi / (KD / 4), kb = bi % (KD / 4);
       const T* src = m ? &sm.u1.qk.sQ[0][0] : &sm.u1.qk.sK[0][0];
@@ -1341,7 +1347,7 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
   }
   {
     constexpr int NB = (C / 4) * (C / 4);
-    for (int idx = tid; idx < NB; idx += 256) {
+    for (int idx = tid; idx < NB; idx += NTHR) {
       const int rb = idx / (C / 4), cb4 = idx % (C / 4);
       f32x4 a[4], p[4], q[4];
 #pragma unroll
@@ -1392,7 +1398,7 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
   };
 
   // ---- dq = dq_s + dA_qk K;  dk = dk_s + dA_qk^T Q + (dA_kk + dA_kk^T) K
-  for (int tile = w; tile < NT * KT; tile += 4) {
+  for (int tile = w; tile < NT * KT; tile += NW) {
     const int rt = tile % NT, kt = tile / NT;
     float pq[4], pk[4];
 #pragma unroll
@@ -1434,12 +1440,12 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
 
   // ---- dv = Tu^T dU = -dW (GDN) or diag(beta) dU (sGLA), 8 values per item
   {
-    constexpr int IT = (C * 128 / 8 + 255) / 256;
+    constexpr int IT = (C * 128 / 8 + NTHR - 1) / NTHR;
     const int n8 = V / 8;
     f32x4 x[IT][2];
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
-      const int idx = tid + 256 * it;
+      const int idx = tid + NTHR * it;
       const int r = idx / n8, c = 8 * (idx % n8);
       x[it][0] = x[it][1] = zero4();
       if (idx < C * n8 && t0 + r < s.T) {
@@ -1450,7 +1456,7 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
     }
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
-      const int idx = tid + 256 * it;
+      const int idx = tid + NTHR * it;
       const int r = idx / n8, c = 8 * (idx % n8);
       const int t = t0 + r;
       if (idx >= C * n8 || t >= s.T) continue;
@@ -1468,7 +1474,7 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
   float* ak2s = aq2s + C * E;
   float* acols = ak2s + C * E;
   __syncthreads();
-  for (int e = w; e < E; e += 4) {
+  for (int e = w; e < E; e += NW) {
     float rowq[16], rowk[16], colacc[NT];
 #pragma unroll
     for (int i = 0; i < 16; ++i) rowq[i] = rowk[i] = 0.f;
@@ -1525,7 +1531,7 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
 
   // ---- per (r, e): Gram terms and the coefficient vectors
   //   a = k2 gamma, b = q2 gamma, c = k2 gamma^C / gamma
-  for (int idx = tid; idx < C * E; idx += 256) {
+  for (int idx = tid; idx < C * E; idx += NTHR) {
     const int r = idx / E, e = idx % E;
     const float aq2 = aq2s[idx], ak2 = ak2s[idx], acol = acols[idx];
     const float q2 = sm.q2[r][e], k2 = sm.k2[r][e];
@@ -1545,7 +1551,7 @@ __global__ __launch_bounds__(256) void k_bwd_chunk(Shape s, FwdIn in, const void
   __syncthreads();
   // dG at the chunk end gains sum_r dc c + gamma^C dgamma^C; then dg_j = sum_{r >= j} dG_r
   // (one wave per slice, lane r holds row r)
-  for (int e = w; e < E; e += 4) {
+  for (int e = w; e < E; e += NW) {
     const float tail = wave_sum(l < C ? acols[l * E + e] : 0.f);
     float x = (l < C) ? sm.dG[l][e] : 0.f;
     if (l == C - 1)
@@ -1608,7 +1614,7 @@ static hipError_t chunk_inst(const Shape& s, const FwdIn& in, const void* dO, co
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     attr = true;
   }
-  hipLaunchKernelGGL((k_bwd_chunk<T, KD, C, E>), dim3(s.NH * s.Nc), dim3(256), smem, st, s, in, dO,
+  hipLaunchKernelGGL((k_bwd_chunk<T, KD, C, E>), dim3(s.NH * s.Nc), dim3(CHUNK_NTHR), smem, st, s, in, dO,
                      sv, bb, dq, dk, dv, dq2, dk2, dg, dbeta);
   return hipGetLastError();
 }
