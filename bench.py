@@ -12,6 +12,9 @@ average HIP-event time with its algorithmic FLOP and byte rates, the
 roofline of the dominant kernel, and the fp64 CPU oracle timed on a bounded
 sample of the same workload.
 
+`--decode` times the recurrent decode step instead (N=256, H=16, E=16) and
+prints its own JSON line.
+
 Helper modes for the HBM-traffic measurement (run under rocprofv3 --pmc):
   --copy-calibration     a plain fp32 copy kernel of known size
   --pmc-summary F W CF CW  reduce four rocprofv3 counter directories (bench
@@ -192,6 +195,52 @@ def pmc_summary(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir):
               f"{r['fetch_bytes'] + r['write_bytes']:.4g} |")
 
 
+def decode_bench(steps, warmup):
+    """The recurrent decode step (tla_step) at N=256 sequences, H=16, E=16,
+    K=V=128, bf16 token inputs, fp32 state [N,H,E,K,V] (4 GiB) updated in
+    place; 8 pre-generated tokens are cycled so no input generation is timed.
+    HBM-bound: one read and one write of the state per step."""
+    import torch
+    import paper_2609_36529_amd as tla
+    from paper_2609_36529_amd import synth
+    N, H, E, K, V = 256, 16, 16, 128, 128
+    state = synth.make_decode_state(N, H, E, K, V).cuda()
+    toks = []
+    for i in range(8):
+        t = synth.make_decode_token(N, H, K, V, E, dtype="bf16", seed=900 + i)
+        toks.append({k: v.cuda() for k, v in t.items()})
+    o = torch.empty((N, H, V), dtype=torch.bfloat16, device="cuda")
+
+    def one(i):
+        t = toks[i % len(toks)]
+        tla.step(tla.GDN, t["q"], t["k"], t["v"], t["q2"], t["k2"], t["g"], t["beta"], state,
+                 out_dtype=torch.bfloat16, o=o)
+    for i in range(warmup):
+        one(i)
+    torch.cuda.synchronize()
+    tla.prof_enable(True)
+    t0 = time.perf_counter()
+    for i in range(steps):
+        one(i)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    tot, n = tla.prof_read()["step"]
+    tla.prof_enable(False)
+    avg_ms = tot / n
+    state_bytes = 2.0 * N * H * E * K * V * 4
+    gbs = state_bytes / (avg_ms * 1e-3) / 1e9
+    print(json.dumps({
+        "metric": "decode tokens/s, triadic GDN tla_step N=256 H=16 E=16 K=V=128",
+        "value": round(N / (elapsed / steps), 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": steps, "warmup": warmup, "ms_per_step": round(1e3 * elapsed / steps, 4),
+        "higher_is_better": True, "dtype": "f32 state, bf16 tokens", "data": "synthetic",
+        "config": {"workload": "GDN decode step", "N": N, "H": H, "E": E, "K": K, "V": V},
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
+                     "kernel": "step", "algorithmic_bytes_per_launch": state_bytes,
+                     "avg_ms": round(avg_ms, 4)}}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -200,6 +249,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true")
     ap.add_argument("--pmc-summary", nargs=4, metavar="DIR")
+    ap.add_argument("--decode", action="store_true",
+                    help="time the decode step instead (its own JSON line)")
     args = ap.parse_args()
     if args.pmc_summary:
         pmc_summary(*args.pmc_summary)
@@ -211,6 +262,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.decode:
+        decode_bench(args.steps, args.warmup)
         return
 
     import torch
