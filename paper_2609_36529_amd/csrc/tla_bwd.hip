@@ -602,13 +602,18 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
 }
 
 // ===================================================== state-gradient contractions
-// One workgroup per (head, chunk); wave w owns the key columns [16 CTW w,
-// 16 CTW (w + 1)).  The chunk's dO, dW and U rows (A operands; dW and U as
-// bf16 hi + lo pairs) are staged in LDS once; the chunk-start state S_e and
-// the chunk-end state gradient dS'_e stream from their tiled stores as B
-// operands of 32-deep MFMAs over pairs of 16-column value blocks, each pair
-// reloaded for the next slice as soon as this slice is done with it.  The
-// rows of Q and K that the row sums need live in registers.
+// One workgroup per (head, chunk) with eight waves (two per SIMD).  Wave w
+// owns the key columns of quarter q = w % 4 ([16 CTW q, 16 CTW (q + 1))) and
+// the row tiles of half w / 4.  The chunk's dO, dW and U rows (A operands;
+// dW and U as bf16 hi + lo pairs) are staged in LDS once; the chunk-start
+// state S_e and the chunk-end state gradient dS'_e stream from their tiled
+// stores as B operands of 32-deep MFMAs over pairs of 16-column value blocks,
+// each pair reloaded for the next slice as soon as this slice is done with it
+// (the two row halves load the same B data; the second request hits the
+// cache).  The rows of Q and K that the row sums need live in registers.
+constexpr int STATE_NW = 8;
+constexpr int STATE_NTHR = STATE_NW * 64;
+
 template <typename T, int KD, int C, int E>
 struct StateSmem {
   static constexpr bool SPLIT = sizeof(T) == 2;
@@ -620,27 +625,30 @@ struct StateSmem {
   alignas(16) T dWh[C][VS], Uh[C][VS];
   alignas(16) T dWl[SPLIT ? C : 1][VS], Ul[SPLIT ? C : 1][VS];
   alignas(16) float coef[3][E][C];
-  alignas(16) float red[2][4][3][C];  // per-wave row-sum partials, by slice parity
+  alignas(16) float red[2][4][3][C];  // per key quarter row-sum partials, by slice parity
   alignas(16) float dcf[3][E][C];
   alignas(16) float gred[4][E];
 };
 
 template <typename T, int KD, int C, int E>
-__global__ __launch_bounds__(256) void k_bwd_state(Shape s, FwdIn in, const void* dOv,
-                                                   PrepBufs p, SavedBufs sv, BwdBufs bb) {
+__global__ __launch_bounds__(STATE_NTHR) void k_bwd_state(Shape s, FwdIn in, const void* dOv,
+                                                          PrepBufs p, SavedBufs sv, BwdBufs bb) {
   constexpr int NT = C / 16;
   constexpr int KT = KD / 16;
   constexpr int CTW = (KT + 3) / 4;      // key column tiles per wave
+  constexpr int RTW = NT > 1 ? NT / 2 : 1;  // row tiles per wave
   constexpr int E4 = (E + 3) & ~3;
   constexpr int NPMAX = 4;               // pairs of value blocks, V <= 128
+  constexpr int NTHR = STATE_NTHR;
   typedef StateSmem<T, KD, C, E> Sm;
   constexpr bool SPLIT = Sm::SPLIT;
   extern __shared__ __align__(16) unsigned char smem_raw[];
   Sm& sm = *reinterpret_cast<Sm*>(smem_raw);
 
-  // (the wave index is left unmarked here: with uniform branches the
-  // compiler hoists this kernel's loads further and spills registers)
-  const int tid = threadIdx.x, w = threadIdx.x >> 6, l = lane_id(), g = l >> 4, n = l & 15;
+  const int tid = threadIdx.x, w = wave_id(), l = lane_id(), g = l >> 4, n = l & 15;
+  const int q = w & 3;                   // key quarter
+  const int rt0 = (w >> 2) * RTW;        // first owned row tile (>= NT: no rows)
+  const bool rows = rt0 < NT;
   const int V = s.V;
   const int VB = V / 16;
   const int NP = (VB + 1) / 2;
@@ -657,9 +665,8 @@ __global__ __launch_bounds__(256) void k_bwd_state(Shape s, FwdIn in, const void
 
   // Stage A-operand columns [c0, c0 + ncols) (ncols a multiple of 32) into LDS
   // columns [0, ncols); columns at or beyond V, and rows past T, are zero.
-  // Every load of the batch is issued before the first LDS write.
   auto stage = [&](int c0, int ncols) {
-    constexpr int IT = (C * Sm::NCOL / 8 + 255) / 256;
+    constexpr int IT = (C * Sm::NCOL / 8 + NTHR - 1) / NTHR;
     const int n8 = ncols / 8;
     Raw8<T> ro[IT];
     f32x4 rw[IT][2], ru[IT][2];
@@ -667,7 +674,7 @@ __global__ __launch_bounds__(256) void k_bwd_state(Shape s, FwdIn in, const void
     // every load of the batch is in flight before the first wait
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
-      const int idx = min(tid + 256 * it, C * n8 - 1);
+      const int idx = min(tid + NTHR * it, C * n8 - 1);
       const int r = idx / n8, col = min(c0 + 8 * (idx % n8), V - 8);
       ro[it] = load8(dOg + (size_t)min(t0 + r, s.T - 1) * vrs + col);
       const float* pw = dWg + (size_t)r * V + col;
@@ -679,7 +686,7 @@ __global__ __launch_bounds__(256) void k_bwd_state(Shape s, FwdIn in, const void
     }
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
-      const int idx = tid + 256 * it;
+      const int idx = tid + NTHR * it;
       if (idx >= C * n8) continue;
       const int r = idx / n8, c = 8 * (idx % n8);
       const bool cok = c0 + c < V;
@@ -707,39 +714,55 @@ __global__ __launch_bounds__(256) void k_bwd_state(Shape s, FwdIn in, const void
     }
   };
 
-  // rows of Q and K at the accumulator positions (row 16 rt + 4 g + j, key 16 ct + n)
-  float qv[NT][CTW][4], kv[NT][CTW][4];
+  // rows of Q and K at the accumulator positions (row 16 rt + 4 g + j, key
+  // 16 ct + n); bf16 values are kept as packed pairs
+  constexpr int QW = sizeof(T) == 2 ? 2 : 4;  // 32-bit words per 4 values
+  uint32_t qv[RTW][CTW][QW], kv[RTW][CTW][QW];
 #pragma unroll
-  for (int rt = 0; rt < NT; ++rt)
+  for (int i = 0; i < RTW; ++i)
 #pragma unroll
     for (int c = 0; c < CTW; ++c) {
-      const int ct = w * CTW + c;
+      const int ct = q * CTW + c, rt = min(rt0 + i, NT - 1);
+#pragma unroll
+      for (int j = 0; j < QW; ++j) qv[i][c][j] = kv[i][c][j] = 0u;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int t = t0 + 16 * rt + 4 * g + j;
-        const bool ok = ct < KT && t < s.T;
+        const bool ok = rows && ct < KT && t < s.T;
         const size_t off = (size_t)min(t, s.T - 1) * krs + 16 * min(ct, KT - 1) + n;
-        const float qx = Elem<T>::to_f(Qg[off]), kx = Elem<T>::to_f(Kg[off]);
-        qv[rt][c][j] = ok ? qx : 0.f;
-        kv[rt][c][j] = ok ? kx : 0.f;
+        if constexpr (sizeof(T) == 2) {
+          const uint32_t qx = (uint32_t)((const uint16_t*)Qg)[off] << (16 * (j & 1));
+          const uint32_t kx = (uint32_t)((const uint16_t*)Kg)[off] << (16 * (j & 1));
+          qv[i][c][j >> 1] |= ok ? qx : 0u;
+          kv[i][c][j >> 1] |= ok ? kx : 0u;
+        } else {
+          const uint32_t qx = __float_as_uint(((const float*)Qg)[off]);
+          const uint32_t kx = __float_as_uint(((const float*)Kg)[off]);
+          qv[i][c][j] = ok ? qx : 0u;
+          kv[i][c][j] = ok ? kx : 0u;
+        }
       }
     }
+  auto unpack = [&](const uint32_t (&x)[QW], int j) -> float {
+    if constexpr (sizeof(T) == 2) return __uint_as_float((j & 1) ? (x[j >> 1] & 0xffff0000u) : (x[j >> 1] << 16));
+    else return __uint_as_float(x[j]);
+  };
   {
     const float* cg = p.coef + (size_t)ch * 3 * E * C;
-    for (int idx = tid; idx < 3 * E * C; idx += 256) (&sm.coef[0][0][0])[idx] = cg[idx];
+    for (int idx = tid; idx < 3 * E * C; idx += NTHR) (&sm.coef[0][0][0])[idx] = cg[idx];
   }
   if constexpr (Sm::STAGE_ALL) stage(0, 32 * NP);
 
   // B operands: S_e^T and dS'_e^T for this wave's key columns; lane (g, n)
   // takes key row 16 ct + n of value block 2 pp + g / 2, columns 8 (g & 1) + 0..7
-  const T* Sck = (const T*)sv.Sck;
-  const T* dSck = (const T*)bb.dSck;
-  Raw8<T> sbuf[CTW][NPMAX], dbuf[CTW][NPMAX];
   // (loads from clamped tiles, never under a per-lane branch: a value block
   // past V meets zero A-operand columns, and the state-gradient dot product
   // below masks it)
+  const T* Sck = (const T*)sv.Sck;
+  const T* dSck = (const T*)bb.dSck;
+  Raw8<T> sbuf[CTW][NPMAX], dbuf[CTW][NPMAX];
   auto load_pair = [&](int e, int c, int pp) {
-    const int ct = min(w * CTW + c, KT - 1);
+    const int ct = min(q * CTW + c, KT - 1);
     const int vb = min(2 * pp + (g >> 1), VB - 1);
     const size_t off = ((((size_t)ch * E + e) * VB + vb) * KD + 16 * ct + n) * 16 + 8 * (g & 1);
     sbuf[c][pp] = load8(Sck + off);
@@ -752,25 +775,25 @@ __global__ __launch_bounds__(256) void k_bwd_state(Shape s, FwdIn in, const void
       if (pp < NP) load_pair(0, c, pp);
   __syncthreads();
 
-  f32x4 dq[NT][CTW], dk[NT][CTW];
+  f32x4 dq[RTW][CTW], dk[RTW][CTW];
 #pragma unroll
-  for (int rt = 0; rt < NT; ++rt)
+  for (int i = 0; i < RTW; ++i)
 #pragma unroll
     for (int c = 0; c < CTW; ++c) {
-      dq[rt][c] = zero4();
-      dk[rt][c] = zero4();
+      dq[i][c] = zero4();
+      dk[i][c] = zero4();
     }
 
   for (int e = 0; e < E; ++e) {
     float gpart = 0.f;
-    f32x4 X[NT][CTW], Y[NT][CTW], Vp[NT][CTW];
+    f32x4 X[RTW][CTW], Y[RTW][CTW], Vp[RTW][CTW];
 #pragma unroll
-    for (int rt = 0; rt < NT; ++rt)
+    for (int i = 0; i < RTW; ++i)
 #pragma unroll
       for (int c = 0; c < CTW; ++c) {
-        X[rt][c] = zero4();
-        Y[rt][c] = zero4();
-        Vp[rt][c] = zero4();
+        X[i][c] = zero4();
+        Y[i][c] = zero4();
+        Vp[i][c] = zero4();
       }
 #pragma unroll
     for (int pp = 0; pp < NPMAX; ++pp) {
@@ -782,37 +805,41 @@ __global__ __launch_bounds__(256) void k_bwd_state(Shape s, FwdIn in, const void
         __syncthreads();
         col = 0;
       }
-#pragma unroll
-      for (int c = 0; c < CTW; ++c) {
-        if (w * CTW + c >= KT) continue;
-        float a[8], d[8], part = 0.f;
-        raw8_to_f(sbuf[c][pp], a);
-        raw8_to_f(dbuf[c][pp], d);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) part += a[i] * d[i];
-        gpart += (2 * pp + (g >> 1) < VB) ? part : 0.f;
-      }
-#pragma unroll
-      for (int rt = 0; rt < NT; ++rt) {
-        const int r = 16 * rt + n;
-        const int cc = col + 8 * g;
-        const Raw8<T> ao = *(const Raw8<T>*)&sm.dO[r][cc];
-        const Raw8<T> awh = *(const Raw8<T>*)&sm.dWh[r][cc];
-        const Raw8<T> auh = *(const Raw8<T>*)&sm.Uh[r][cc];
-        Raw8<T> awl, aul;
-        if constexpr (SPLIT) {
-          awl = *(const Raw8<T>*)&sm.dWl[r][cc];
-          aul = *(const Raw8<T>*)&sm.Ul[r][cc];
-        }
+      if (w < 4) {  // the state-gradient dot product, once per key quarter
 #pragma unroll
         for (int c = 0; c < CTW; ++c) {
-          if (w * CTW + c >= KT) continue;
-          mma8(X[rt][c], ao, sbuf[c][pp]);
-          mma8(Y[rt][c], awh, sbuf[c][pp]);
-          mma8(Vp[rt][c], auh, dbuf[c][pp]);
+          if (q * CTW + c >= KT) continue;
+          float a[8], d[8], part = 0.f;
+          raw8_to_f(sbuf[c][pp], a);
+          raw8_to_f(dbuf[c][pp], d);
+#pragma unroll
+          for (int i = 0; i < 8; ++i) part += a[i] * d[i];
+          gpart += (2 * pp + (g >> 1) < VB) ? part : 0.f;
+        }
+      }
+      if (rows) {
+#pragma unroll
+        for (int i = 0; i < RTW; ++i) {
+          const int r = 16 * (rt0 + i) + n;
+          const int cc = col + 8 * g;
+          const Raw8<T> ao = *(const Raw8<T>*)&sm.dO[r][cc];
+          const Raw8<T> awh = *(const Raw8<T>*)&sm.dWh[r][cc];
+          const Raw8<T> auh = *(const Raw8<T>*)&sm.Uh[r][cc];
+          Raw8<T> awl, aul;
           if constexpr (SPLIT) {
-            mma8(Y[rt][c], awl, sbuf[c][pp]);
-            mma8(Vp[rt][c], aul, dbuf[c][pp]);
+            awl = *(const Raw8<T>*)&sm.dWl[r][cc];
+            aul = *(const Raw8<T>*)&sm.Ul[r][cc];
+          }
+#pragma unroll
+          for (int c = 0; c < CTW; ++c) {
+            if (q * CTW + c >= KT) continue;
+            mma8(X[i][c], ao, sbuf[c][pp]);
+            mma8(Y[i][c], awh, sbuf[c][pp]);
+            mma8(Vp[i][c], auh, dbuf[c][pp]);
+            if constexpr (SPLIT) {
+              mma8(Y[i][c], awl, sbuf[c][pp]);
+              mma8(Vp[i][c], aul, dbuf[c][pp]);
+            }
           }
         }
       }
@@ -826,62 +853,68 @@ __global__ __launch_bounds__(256) void k_bwd_state(Shape s, FwdIn in, const void
     const int par = e & 1;
     float rs[3][16];
 #pragma unroll
-    for (int rt = 0; rt < 4; ++rt) {
+    for (int i = 0; i < 4; ++i) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) rs[0][4 * rt + j] = rs[1][4 * rt + j] = rs[2][4 * rt + j] = 0.f;
-      if (rt >= NT) continue;
+      for (int j = 0; j < 4; ++j) rs[0][4 * i + j] = rs[1][4 * i + j] = rs[2][4 * i + j] = 0.f;
+      if (i >= RTW || !rows) continue;
+      const int rt = rt0 + i;
       const f32x4 ca = *(const f32x4*)&sm.coef[0][e][16 * rt + 4 * g];
       const f32x4 cb = *(const f32x4*)&sm.coef[1][e][16 * rt + 4 * g];
       const f32x4 cc = *(const f32x4*)&sm.coef[2][e][16 * rt + 4 * g];
 #pragma unroll
       for (int c = 0; c < CTW; ++c) {
-        if (w * CTW + c >= KT) continue;
-        dq[rt][c] += cb * X[rt][c];
-        dk[rt][c] += ca * Y[rt][c] + cc * Vp[rt][c];
+        if (q * CTW + c >= KT) continue;
+        dq[i][c] += cb * X[i][c];
+        dk[i][c] += ca * Y[i][c] + cc * Vp[i][c];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          rs[0][4 * rt + j] += kv[rt][c][j] * Y[rt][c][j];   // d a_e
-          rs[1][4 * rt + j] += qv[rt][c][j] * X[rt][c][j];   // d b_e
-          rs[2][4 * rt + j] += kv[rt][c][j] * Vp[rt][c][j];  // d c_e
+          const float kj = unpack(kv[i][c], j), qj = unpack(qv[i][c], j);
+          rs[0][4 * i + j] += kj * Y[i][c][j];   // d a_e
+          rs[1][4 * i + j] += qj * X[i][c][j];   // d b_e
+          rs[2][4 * i + j] += kj * Vp[i][c][j];  // d c_e
         }
       }
     }
-    // lane n of group g now receives the row sum of row 16 (n / 4) + 4 g + n % 4
-    const int rrow = 16 * (n >> 2) + 4 * g + (n & 3);
+    // lane n of group g now receives the row sum of row 16 (rt0 + n / 4) + 4 g + n % 4
+    const int rrow = 16 * (rt0 + (n >> 2)) + 4 * g + (n & 3);
 #pragma unroll
     for (int kind = 0; kind < 3; ++kind) {
       const float x = group16_transpose_sum(rs[kind], n);
-      if ((n >> 2) < NT) sm.red[par][w][kind][rrow] = x;
+      if (rows && (n >> 2) < RTW) sm.red[par][q][kind][rrow] = x;
     }
-    gpart = wave_sum(gpart);
-    if (l == 0) sm.gred[w][e] = gpart;
+    if (w < 4) {
+      gpart = wave_sum(gpart);
+      if (l == 0) sm.gred[q][e] = gpart;
+    }
     __syncthreads();
-    for (int idx = tid; idx < 3 * C; idx += 256) {  // fixed-order sum over the waves
+    for (int idx = tid; idx < 3 * C; idx += NTHR) {  // fixed-order sum over the key quarters
       const int kind = idx / C, r = idx % C;
       sm.dcf[kind][e][r] = ((sm.red[par][0][kind][r] + sm.red[par][1][kind][r]) +
                             sm.red[par][2][kind][r]) + sm.red[par][3][kind][r];
     }
   }
   __syncthreads();
-  for (int idx = tid; idx < 3 * E * C; idx += 256)
+  for (int idx = tid; idx < 3 * E * C; idx += NTHR)
     bb.dcoef[(size_t)ch * 3 * E * C + idx] = (&sm.dcf[0][0][0])[idx];
   if (tid < E4)
     bb.dgC[(size_t)ch * E4 + tid] =
         (tid < E) ? ((sm.gred[0][tid] + sm.gred[1][tid]) + sm.gred[2][tid]) + sm.gred[3][tid] : 0.f;
+  if (rows) {
 #pragma unroll
-  for (int rt = 0; rt < NT; ++rt)
+    for (int i = 0; i < RTW; ++i)
 #pragma unroll
-    for (int c = 0; c < CTW; ++c) {
-      const int ct = w * CTW + c;
-      if (ct >= KT) continue;
-      float* q = bb.dqs + (size_t)ch * C * KD + (size_t)(16 * rt + 4 * g) * KD + 16 * ct + n;
-      float* k = bb.dks + (size_t)ch * C * KD + (size_t)(16 * rt + 4 * g) * KD + 16 * ct + n;
+      for (int c = 0; c < CTW; ++c) {
+        const int ct = q * CTW + c, rt = rt0 + i;
+        if (ct >= KT) continue;
+        float* qo = bb.dqs + (size_t)ch * C * KD + (size_t)(16 * rt + 4 * g) * KD + 16 * ct + n;
+        float* ko = bb.dks + (size_t)ch * C * KD + (size_t)(16 * rt + 4 * g) * KD + 16 * ct + n;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        q[(size_t)j * KD] = dq[rt][c][j];
-        k[(size_t)j * KD] = dk[rt][c][j];
+        for (int j = 0; j < 4; ++j) {
+          qo[(size_t)j * KD] = dq[i][c][j];
+          ko[(size_t)j * KD] = dk[i][c][j];
+        }
       }
-    }
+  }
 }
 
 // ========================================================= per-chunk gradients
@@ -1598,7 +1631,7 @@ static hipError_t state_inst(const Shape& s, const FwdIn& in, const void* dO, co
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     attr = true;
   }
-  hipLaunchKernelGGL((k_bwd_state<T, KD, C, E>), dim3(s.NH * s.Nc), dim3(256), smem, st, s, in, dO,
+  hipLaunchKernelGGL((k_bwd_state<T, KD, C, E>), dim3(s.NH * s.Nc), dim3(STATE_NTHR), smem, st, s, in, dO,
                      p, sv, bb);
   return hipGetLastError();
 }
