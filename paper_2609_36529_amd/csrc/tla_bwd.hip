@@ -102,13 +102,13 @@ struct RecSmem {
 // Register staging of one chunk's inputs for the reverse recurrence: the
 // global loads for chunk ci - 1 are issued while chunk ci is computed, and
 // written to LDS (with the transposed copies) at the top of the next step.
-// K and Q are moved in blocks of 4 rows x KW columns, M and Tu in blocks of
-// 4 rows x MW columns; eight-wave workgroups use the narrower blocks so that
-// every thread holds a share and the registers per lane stay low.
+// K and Q are moved in blocks of 4 rows x KW columns (16-byte loads), M and
+// Tu in blocks of 4 rows x MW columns; in eight-wave workgroups the waves
+// past the last block skip the loads (fewer, wider load instructions).
 template <typename T, int KD, int C, int E, int NTHR>
 struct RecStage {
-  static constexpr int KW = NTHR >= 512 ? 4 : 8;
-  static constexpr int MW = NTHR >= 512 ? 2 : 4;
+  static constexpr int KW = 8;
+  static constexpr int MW = 4;
   static constexpr int RB = C / 4;
   static constexpr int KCB = KD / KW, MCB = C / MW;
   static constexpr int KWD = KW * (int)sizeof(T) / 4;          // words per block row
@@ -134,11 +134,14 @@ struct RecStage {
                                        const T* Qg, const T* dOg, size_t ch, int ci,
                                        int parts = 3) {
     const int tid = threadIdx.x;
+    const int w0 = 64 * wave_id();  // first thread of this wave (wave-uniform)
     const int t0 = ci * C;
     const size_t krs = (size_t)s.H * KD, vrs = (size_t)s.H * s.V;
+    // (waves with no block at all skip a loop step: a scalar branch)
     if (parts & 1) {
 #pragma unroll
     for (int i = 0; i < NKB; ++i) {
+      if (w0 + i * NTHR >= RB * KCB) continue;
       const int blk = min(tid + i * NTHR, RB * KCB - 1);
       const int rb = blk % RB, cb = blk / RB;
 #pragma unroll
@@ -150,6 +153,7 @@ struct RecStage {
     }
 #pragma unroll
     for (int i = 0; i < NDB; ++i) {
+      if (w0 + i * NTHR >= RB * 4) continue;
       const int blk = min(tid + i * NTHR, RB * 4 - 1);
       const int rb = blk % RB, c4 = blk / RB;
 #pragma unroll
@@ -164,6 +168,7 @@ struct RecStage {
     const float* Tg = p.Tu + ch * C * C;
 #pragma unroll
     for (int i = 0; i < NMB; ++i) {
+      if (w0 + i * NTHR >= RB * MCB) continue;
       const int blk = min(tid + i * NTHR, RB * MCB - 1);
       const int rb = blk % RB, cb = blk / RB;
 #pragma unroll
@@ -189,7 +194,9 @@ struct RecStage {
     }
     const float* cg = p.coef + ch * 3 * E * C;
 #pragma unroll
-    for (int i = 0; i < NCB; ++i) c[i] = *(const f32x4*)(cg + 4 * min(tid + i * NTHR, 3 * E * C / 4 - 1));
+    for (int i = 0; i < NCB; ++i)
+      if (w0 + i * NTHR < 3 * E * C / 4)
+        c[i] = *(const f32x4*)(cg + 4 * min(tid + i * NTHR, 3 * E * C / 4 - 1));
     gc = p.gC[ch * E4 + min(tid, E4 - 1)];
   }
 
