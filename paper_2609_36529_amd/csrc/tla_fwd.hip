@@ -311,12 +311,14 @@ struct FwdStage {
                                        const T* Kg, const T* Qg, const T* Vg, int b, int h,
                                        int ci, int parts = 3) {
     const int tid = threadIdx.x;
+    const int w0 = 64 * wave_id();  // first thread of this wave (wave-uniform)
     const int t0 = ci * C;
     const size_t ch = (size_t)(b * s.H + h) * s.Nc + ci;
     const size_t krs = (size_t)s.H * KD, vrs = (size_t)s.H * s.V;
     if (parts & 1) {
 #pragma unroll
     for (int i = 0; i < NKB; ++i) {
+      if (w0 + i * NTHR >= RB * CB) continue;  // (scalar branch: no block in this wave)
       const int blk = min(tid + i * NTHR, RB * CB - 1);
       const int rb = blk % RB, cb = blk / RB;
 #pragma unroll
@@ -328,6 +330,7 @@ struct FwdStage {
     }
 #pragma unroll
     for (int i = 0; i < NV4; ++i) {
+      if (w0 + i * NTHR >= C * 4) continue;
       const int idx = min(tid + i * NTHR, C * 4 - 1);
       const int r = idx >> 2, c4 = idx & 3;
       const int t = min(t0 + r, s.T - 1);
@@ -349,13 +352,16 @@ struct FwdStage {
     const float* Tg = p.Tu + ch * C * C;
 #pragma unroll
     for (int i = 0; i < NMB; ++i) {
+      if (w0 + i * NTHR >= C * C / 4) continue;
       const int idx = min(tid + i * NTHR, C * C / 4 - 1);
       m[i] = *(const f32x4*)(Mg + 4 * idx);
       tu[i] = *(const f32x4*)(Tg + 4 * idx);
     }
     const float* cg = p.coef + ch * 3 * E * C;
 #pragma unroll
-    for (int i = 0; i < NCB; ++i) c[i] = *(const f32x4*)(cg + 4 * min(tid + i * NTHR, 3 * E * C / 4 - 1));
+    for (int i = 0; i < NCB; ++i)
+      if (w0 + i * NTHR < 3 * E * C / 4)
+        c[i] = *(const f32x4*)(cg + 4 * min(tid + i * NTHR, 3 * E * C / 4 - 1));
     gc = p.gC[ch * E4 + min(tid, E4 - 1)];
     const int tb = min(t0 + min(tid, C - 1), s.T - 1);
     beta = in.beta ? in.beta[((size_t)b * s.T + tb) * s.H + h] : 1.f;
