@@ -95,7 +95,7 @@ size_t esize(const tla::Shape& s) { return s.in_bf16 ? 2 : 4; }
 // M, Tu) live in the forward workspace for inference; a training forward
 // writes them into `saved`, where the backward reads them again.
 struct Layout {
-  size_t p_coef, p_gC, p_M, p_Tu, p_size;  // prep region, relative offsets
+  size_t p_coef, p_gC, p_ops, p_size;  // prep region, relative offsets
   size_t bwd_dS, bwd_dU, bwd_dW, bwd_dqs, bwd_dks, bwd_dcoef, bwd_dgC, bwd_end;
   size_t sv_S, sv_U, sv_X, sv_prep, sv_end;
 };
@@ -108,8 +108,7 @@ Layout layout(const tla::Shape& s) {
   size_t o = 0;
   L.p_coef = o; o += align256(nch * 3 * s.E * s.C * 4);
   L.p_gC = o;   o += align256(nch * E4 * 4);
-  L.p_M = o;    o += align256(nch * s.C * s.C * 4);
-  L.p_Tu = o;   o += align256(nch * s.C * s.C * 4);
+  L.p_ops = o;  o += align256(nch * tla::op_tile_bytes(s.K, s.C, s.in_bf16));
   L.p_size = o;
   o = 0;
   L.bwd_dS = o;    o += align256(nch * s.E * s.K * s.V * es);
@@ -131,8 +130,7 @@ Layout layout(const tla::Shape& s) {
 
 tla::PrepBufs prep_bufs(const Layout& L, const void* base) {
   char* b = (char*)base;
-  return tla::PrepBufs{(float*)(b + L.p_coef), (float*)(b + L.p_gC), (float*)(b + L.p_M),
-                       (float*)(b + L.p_Tu)};
+  return tla::PrepBufs{(float*)(b + L.p_coef), (float*)(b + L.p_gC), (void*)(b + L.p_ops)};
 }
 tla::SavedBufs saved_bufs(const Layout& L, const void* saved) {
   char* b = (char*)saved;

@@ -101,35 +101,34 @@ struct RecSmem {
 
 // Register staging of one chunk's inputs for the reverse recurrence: the
 // global loads for chunk ci - 1 are issued while chunk ci is computed, and
-// written to LDS (with the transposed copies) at the top of the next step.
-// K and Q are moved in blocks of 4 rows x KW columns (16-byte loads), M and
-// Tu in blocks of 4 rows x MW columns; in eight-wave workgroups the waves
-// past the last block skip the loads (fewer, wider load instructions).
+// copied to shared memory at the top of the next step.  K^T, Q^T, M^T and
+// Tu^T arrive from the prep kernel already transposed and split, so only the
+// dO tile is transposed here.  Loads are unconditional (rows past T read a
+// clamped row and are zeroed when stored) and waves past the last piece of a
+// loop step skip it (a scalar branch).
 template <typename T, int KD, int C, int E, int NTHR>
 struct RecStage {
-  static constexpr int KW = 8;
-  static constexpr int MW = 4;
+  typedef OpTiles<T, KD, C> OT;
+  static constexpr int EC = 16 / (int)sizeof(T);        // elements per 16-byte chunk
+  static constexpr int NRC = C * KD / EC;                // chunks of the K rows
+  static constexpr int NTC = 2 * KD * C / EC;            // chunks of K^T and Q^T
+  static constexpr int NMC = 2 * OT::NS * C * C / EC;    // chunks of M^T and Tu^T (hi, lo)
   static constexpr int RB = C / 4;
-  static constexpr int KCB = KD / KW, MCB = C / MW;
-  static constexpr int KWD = KW * (int)sizeof(T) / 4;          // words per block row
-  static constexpr int NKB = (RB * KCB + NTHR - 1) / NTHR;
+  static constexpr int NR = (NRC + NTHR - 1) / NTHR;
+  static constexpr int NTT = (NTC + NTHR - 1) / NTHR;
+  static constexpr int NM = (NMC + NTHR - 1) / NTHR;
   static constexpr int NDB = (RB * 4 + NTHR - 1) / NTHR;       // 4 x 4 blocks of the dO tile
-  static constexpr int NMB = (RB * MCB + NTHR - 1) / NTHR;
   static constexpr int NCB = (3 * E * C / 4 + NTHR - 1) / NTHR;
   static constexpr int E4 = (E + 3) & ~3;
   static constexpr int DW = sizeof(T) == 2 ? 2 : 4;            // words per 4 elements
-  uint32_t k[NKB][4][KWD], q[NKB][4][KWD];
+  static constexpr bool ROWS = sizeof(T) == 2;                 // K rows staged (bf16 only)
+  uint4 k[ROWS ? NR : 1], tt[NTT], mt[NM];
   uint32_t d[NDB][4][DW];
-  float m[NMB][4][MW], tu[NMB][4][MW];
   f32x4 c[NCB];
   float gc;
 
-  // Every load is unconditional: a row past T is read from row T - 1 and a
-  // block index past the end from the last block, and store() zeroes or
-  // skips them.  (A per-lane branch around a load would make the compiler
-  // wait for the load right away, which defeats the prefetch.)
-  // parts: 1 = the K, Q rows and the dO tile; 2 = M, Tu and the vectors (the
-  // two halves are issued at different points of a chunk step)
+  // parts: 1 = the K rows, K^T, Q^T and the dO tile; 2 = M^T, Tu^T and the
+  // vectors (the two halves are issued at different points of a chunk step)
   __device__ __forceinline__ void load(const Shape& s, const PrepBufs& p, const T* Kg,
                                        const T* Qg, const T* dOg, size_t ch, int ci,
                                        int parts = 3) {
@@ -137,60 +136,39 @@ struct RecStage {
     const int w0 = 64 * wave_id();  // first thread of this wave (wave-uniform)
     const int t0 = ci * C;
     const size_t krs = (size_t)s.H * KD, vrs = (size_t)s.H * s.V;
-    // (waves with no block at all skip a loop step: a scalar branch)
+    const T* ops = (const T*)p.ops + ch * OT::STRIDE;
     if (parts & 1) {
+      if constexpr (ROWS) {
 #pragma unroll
-    for (int i = 0; i < NKB; ++i) {
-      if (w0 + i * NTHR >= RB * KCB) continue;
-      const int blk = min(tid + i * NTHR, RB * KCB - 1);
-      const int rb = blk % RB, cb = blk / RB;
-#pragma unroll
-      for (int rr = 0; rr < 4; ++rr) {
-        const int t = min(t0 + 4 * rb + rr, s.T - 1);
-        ld_words(k[i][rr], Kg + (size_t)t * krs + KW * cb);
-        ld_words(q[i][rr], Qg + (size_t)t * krs + KW * cb);
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < NDB; ++i) {
-      if (w0 + i * NTHR >= RB * 4) continue;
-      const int blk = min(tid + i * NTHR, RB * 4 - 1);
-      const int rb = blk % RB, c4 = blk / RB;
-#pragma unroll
-      for (int rr = 0; rr < 4; ++rr) {
-        const int t = min(t0 + 4 * rb + rr, s.T - 1);
-        ld_words(d[i][rr], dOg + (size_t)t * vrs + 4 * c4);
-      }
-    }
-    }
-    if (!(parts & 2)) return;
-    const float* Mg = p.M + ch * C * C;
-    const float* Tg = p.Tu + ch * C * C;
-#pragma unroll
-    for (int i = 0; i < NMB; ++i) {
-      if (w0 + i * NTHR >= RB * MCB) continue;
-      const int blk = min(tid + i * NTHR, RB * MCB - 1);
-      const int rb = blk % RB, cb = blk / RB;
-#pragma unroll
-      for (int rr = 0; rr < 4; ++rr) {
-        const size_t off = (size_t)(4 * rb + rr) * C + MW * cb;
-        if constexpr (MW == 4) {
-          const f32x4 x = *(const f32x4*)(Mg + off);
-          const f32x4 y = *(const f32x4*)(Tg + off);
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            m[i][rr][j] = x[j];
-            tu[i][rr][j] = y[j];
-          }
-        } else {
-          const float2 x = *(const float2*)(Mg + off);
-          const float2 y = *(const float2*)(Tg + off);
-          m[i][rr][0] = x.x;
-          m[i][rr][1] = x.y;
-          tu[i][rr][0] = y.x;
-          tu[i][rr][1] = y.y;
+        for (int i = 0; i < NR; ++i) {
+          if (w0 + i * NTHR >= NRC) continue;
+          const int idx = min(tid + i * NTHR, NRC - 1);
+          const int r = idx / (KD / EC), c0 = EC * (idx % (KD / EC));
+          k[i] = *(const uint4*)(Kg + (size_t)min(t0 + r, s.T - 1) * krs + c0);
         }
       }
+#pragma unroll
+      for (int i = 0; i < NTT; ++i) {
+        if (w0 + i * NTHR >= NTC) continue;
+        tt[i] = ((const uint4*)(ops + OT::Kt))[min(tid + i * NTHR, NTC - 1)];
+      }
+#pragma unroll
+      for (int i = 0; i < NDB; ++i) {
+        if (w0 + i * NTHR >= RB * 4) continue;
+        const int blk = min(tid + i * NTHR, RB * 4 - 1);
+        const int rb = blk % RB, c4 = blk / RB;
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) {
+          const int t = min(t0 + 4 * rb + rr, s.T - 1);
+          ld_words(d[i][rr], dOg + (size_t)t * vrs + 4 * c4);
+        }
+      }
+    }
+    if (!(parts & 2)) return;
+#pragma unroll
+    for (int i = 0; i < NM; ++i) {
+      if (w0 + i * NTHR >= NMC) continue;
+      mt[i] = ((const uint4*)(ops + OT::MT))[min(tid + i * NTHR, NMC - 1)];
     }
     const float* cg = p.coef + ch * 3 * E * C;
 #pragma unroll
@@ -201,40 +179,28 @@ struct RecStage {
   }
 
   template <typename Sm>
-  __device__ __forceinline__ void store(Sm& sm, int variant, int t0, int nT) const {
-    typedef typename Elem<T>::frag F;
+  __device__ __forceinline__ void store(Sm& sm, int variant, int t0, int nT,
+                                        int parts = 3) const {
     const int tid = threadIdx.x;
+    if (parts & 1) {
+    if constexpr (ROWS) {
 #pragma unroll
-    for (int i = 0; i < NKB; ++i) {
-      const int blk = tid + i * NTHR;
-      const int rb = blk % RB, cb = blk / RB;
-      if (blk < RB * KCB) {
-        uint32_t kk[4][KWD], qq[4][KWD];
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr) {
-          const bool ok = t0 + 4 * rb + rr < nT;
-#pragma unroll
-          for (int j = 0; j < KWD; ++j) {
-            kk[rr][j] = ok ? k[i][rr][j] : 0u;
-            qq[rr][j] = ok ? q[i][rr][j] : 0u;
-          }
-        }
-        if constexpr (Sm::STAGE_K) {
-#pragma unroll
-          for (int rr = 0; rr < 4; ++rr)
-#pragma unroll
-            for (int j = 0; j < KWD; j += 2)
-              *(uint2*)((uint32_t*)&sm.K[4 * rb + rr][KW * cb] + j) =
-                  make_uint2(kk[rr][j], kk[rr][j + 1]);
-        }
-#pragma unroll
-        for (int cc = 0; cc < KW; ++cc) {
-          lds_put4(&sm.Kt[KW * cb + cc][4 * rb], word_elem<T>(kk[0], cc), word_elem<T>(kk[1], cc),
-                   word_elem<T>(kk[2], cc), word_elem<T>(kk[3], cc));
-          lds_put4(&sm.Qt[KW * cb + cc][4 * rb], word_elem<T>(qq[0], cc), word_elem<T>(qq[1], cc),
-                   word_elem<T>(qq[2], cc), word_elem<T>(qq[3], cc));
-        }
+      for (int i = 0; i < NR; ++i) {
+        const int idx = tid + i * NTHR;
+        if (idx >= NRC) continue;
+        const int r = idx / (KD / EC), c0 = EC * (idx % (KD / EC));
+        lds_put16(&sm.K[r][c0], (t0 + r < nT) ? k[i] : make_uint4(0, 0, 0, 0));
       }
+    }
+    // K^T then Q^T (rows past T are already zero)
+    constexpr int PERT = KD * C / EC;
+#pragma unroll
+    for (int i = 0; i < NTT; ++i) {
+      const int idx = tid + i * NTHR;
+      if (idx >= NTC) continue;
+      const int mtx = idx / PERT, j = idx % PERT;
+      const int r = j / (C / EC), c0 = EC * (j % (C / EC));
+      lds_put16(mtx ? &sm.Qt[r][c0] : &sm.Kt[r][c0], tt[i]);
     }
 #pragma unroll
     for (int i = 0; i < NDB; ++i) {
@@ -254,24 +220,22 @@ struct RecStage {
                    word_elem<T>(dd[2], cc), word_elem<T>(dd[3], cc));
       }
     }
+    }
+    if (!(parts & 2)) return;
+    // M^T and Tu^T chunks: matrix m (M^T hi, lo, Tu^T hi, lo for bf16; M^T, Tu^T for fp32)
+    constexpr int PER = C * C / EC;
 #pragma unroll
-    for (int i = 0; i < NMB; ++i) {
-      const int blk = tid + i * NTHR;
-      const int rb = blk % RB, cb = blk / RB;
-      if (blk < RB * MCB) {
-#pragma unroll
-        for (int cc = 0; cc < MW; ++cc) {
-          F h, lw;
-          split_frag(f32x4{m[i][0][cc], m[i][1][cc], m[i][2][cc], m[i][3][cc]}, h, lw);
-          *(F*)&sm.MT[MW * cb + cc][4 * rb] = h;
-          if constexpr (Sm::SPLIT) *(F*)&sm.MTL[MW * cb + cc][4 * rb] = lw;
-          if (variant == 1) {
-            split_frag(f32x4{tu[i][0][cc], tu[i][1][cc], tu[i][2][cc], tu[i][3][cc]}, h, lw);
-            *(F*)&sm.TuT[MW * cb + cc][4 * rb] = h;
-            if constexpr (Sm::SPLIT) *(F*)&sm.TuTL[MW * cb + cc][4 * rb] = lw;
-          }
-        }
-      }
+    for (int i = 0; i < NM; ++i) {
+      const int idx = tid + i * NTHR;
+      if (idx >= NMC) continue;
+      const int mtx = idx / PER, j = idx % PER;
+      const int r = j / (C / EC), c0 = EC * (j % (C / EC));
+      T* dst;
+      if constexpr (OT::NS == 2)
+        dst = (mtx == 0) ? &sm.MT[r][c0] : (mtx == 1) ? &sm.MTL[r][c0] : (mtx == 2) ? &sm.TuT[r][c0] : &sm.TuTL[r][c0];
+      else
+        dst = (mtx == 0) ? &sm.MT[r][c0] : &sm.TuT[r][c0];
+      lds_put16(dst, mt[i]);
     }
     float* cs = &sm.coef[0][0][0];
 #pragma unroll
@@ -342,69 +306,11 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
     if constexpr (PREFETCH) {
       stage.store(sm, s.variant, t0, s.T);
     } else {
-      // ---- stage: K rows, K^T, Q^T, dO tile^T, M^T, Tu^T (split), coefficients
-      constexpr int RB = C / 4, CB = KD / 8;
-      for (int blk = tid; blk < RB * CB; blk += NTHR) {
-        const int rb = blk % RB, cb = blk / RB;
-        T kv[4][8], qv[4][8];
 #pragma unroll
-        for (int rr = 0; rr < 4; ++rr) {
-          const int t = t0 + 4 * rb + rr;
-          if (t < s.T) {
-            bcopy8(kv[rr], Kg + (size_t)t * krs + 8 * cb);
-            bcopy8(qv[rr], Qg + (size_t)t * krs + 8 * cb);
-          } else {
-            bzero8(kv[rr]);
-            bzero8(qv[rr]);
-          }
-        }
-        if constexpr (Sm::STAGE_K) {
-#pragma unroll
-          for (int rr = 0; rr < 4; ++rr) lds_put8(&sm.K[4 * rb + rr][8 * cb], kv[rr]);
-        }
-#pragma unroll
-        for (int cc = 0; cc < 8; ++cc) {
-          lds_put4(&sm.Kt[8 * cb + cc][4 * rb], kv[0][cc], kv[1][cc], kv[2][cc], kv[3][cc]);
-          lds_put4(&sm.Qt[8 * cb + cc][4 * rb], qv[0][cc], qv[1][cc], qv[2][cc], qv[3][cc]);
-        }
-      }
-      for (int idx = tid; idx < (C / 4) * 16; idx += NTHR) {  // 4 rows x 1 column per thread
-        const int rb = idx % (C / 4), col = idx / (C / 4);
-        T x[4];
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr) {
-          const int t = t0 + 4 * rb + rr;
-          x[rr] = (t < s.T) ? dOg[(size_t)t * vrs + col] : T(0);
-        }
-        lds_put4(&sm.dOt[col][4 * rb], x[0], x[1], x[2], x[3]);
-      }
-      {
-        // M^T and Tu^T (hi / lo) from 4x4 blocks: 4 row loads, 4 column stores
-        const float* Mg = p.M + ch * C * C;
-        const float* Tg = p.Tu + ch * C * C;
-        auto put_t = [&](const float* src, T (*hi)[Sm::CP], T (*lo)[Sm::CP], int rb, int cb) {
-          f32x4 x[4];
-#pragma unroll
-          for (int rr = 0; rr < 4; ++rr) x[rr] = *(const f32x4*)(src + (4 * rb + rr) * C + 4 * cb);
-#pragma unroll
-          for (int cc = 0; cc < 4; ++cc) {
-            const f32x4 col{x[0][cc], x[1][cc], x[2][cc], x[3][cc]};
-            F h, lw;
-            split_frag(col, h, lw);
-            *(F*)&hi[4 * cb + cc][4 * rb] = h;
-            if constexpr (Sm::SPLIT) *(F*)&lo[4 * cb + cc][4 * rb] = lw;
-          }
-        };
-        for (int idx = tid; idx < (C / 4) * (C / 4); idx += NTHR) {
-          const int rb = idx % (C / 4), cb = idx / (C / 4);
-          put_t(Mg, sm.MT, sm.MTL, rb, cb);
-          if (s.variant == 1) put_t(Tg, sm.TuT, sm.TuTL, rb, cb);
-        }
-        const float* cg = p.coef + ch * 3 * E * C;
-        float* cs = &sm.coef[0][0][0];
-        for (int idx = tid; idx < 3 * E * C / 4; idx += NTHR)
-          ((float4*)cs)[idx] = ((const float4*)cg)[idx];
-        if (tid < E4) sm.gC[tid] = p.gC[ch * E4 + tid];
+      for (int part = 1; part <= 2; ++part) {  // in halves: fewer live registers
+        RecStage<T, KD, C, E, NTHR> now;
+        now.load(s, p, Kg, Qg, dOg, ch, ci, part);
+        now.store(sm, s.variant, t0, s.T, part);
       }
     }
     __syncthreads();

@@ -352,14 +352,32 @@ __device__ __forceinline__ float group16_transpose_sum(const float (&v)[16], int
   return (b0 ? c[1] : c[0]) + dpp_f<0xB1>(send);        // quad_perm [1,0,3,2]
 }
 
+// A 16-byte chunk into shared memory at an 8-byte aligned address (padded
+// rows are not 16-byte aligned): two 8-byte writes.
+template <typename T>
+__device__ __forceinline__ void lds_put16(T* dst, uint4 x) {
+  ((uint2*)dst)[0] = make_uint2(x.x, x.y);
+  ((uint2*)dst)[1] = make_uint2(x.z, x.w);
+}
+
+// Four consecutive values to global memory in the element type (one 8-byte
+// store for bf16, one 16-byte store for fp32).
+template <typename T>
+__device__ __forceinline__ void put4(T* dst, f32x4 x) {
+  if constexpr (sizeof(T) == 2)
+    *(uint2*)dst = __builtin_bit_cast(uint2, cvt_frag<bf16_t>(x));
+  else
+    *(f32x4*)dst = x;
+}
+
 // Store a 16 x 16 accumulator tile (lane (g, n) holds rows 4 g + j, column n)
-// into a row-major 16 x 16 tile at dst (row r at dst + 16 r).  Two DPP
+// into a row-major tile at dst (row r at dst + ld r, ld = 16 by default).  Two DPP
 // exchange rounds transpose 4 x 4 blocks within each quad of lanes, after
 // which lane n holds row 4 g + n % 4, columns 4 (n / 4) .. + 3 and writes
 // them with one 8-byte (bf16) or 16-byte (fp32) store instead of four
 // scalar ones.
 template <typename T>
-__device__ __forceinline__ void store_tile16(T* dst, f32x4 x, int g, int n) {
+__device__ __forceinline__ void store_tile16(T* dst, f32x4 x, int g, int n, int ld = 16) {
   const int i = n & 3;
   const bool b0 = i & 1, b1 = i & 2;
   float t = dpp_f<0xB1>(b0 ? x[0] : x[1]);  // lanes differing in bit 0
@@ -374,7 +392,7 @@ __device__ __forceinline__ void store_tile16(T* dst, f32x4 x, int g, int n) {
   t = dpp_f<0x4E>(b1 ? x[1] : x[3]);
   x[1] = b1 ? t : x[1];
   x[3] = b1 ? x[3] : t;
-  T* p = dst + (4 * g + i) * 16 + 4 * (n >> 2);
+  T* p = dst + (4 * g + i) * ld + 4 * (n >> 2);
   if constexpr (sizeof(T) == 2)
     *(uint2*)p = __builtin_bit_cast(uint2, cvt_frag<bf16_t>(x));
   else

@@ -181,7 +181,24 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
       return (t0 + r < s.T) ? x : zero_raw8<T>();
     }
   };
-  float* Mg = p.M + (size_t)ch * C * C;
+  typedef OpTiles<T, KD, C> OT;
+  T* ops = (T*)p.ops + (size_t)ch * OT::STRIDE;
+  // M tile (rt, st) of the lane layout into the row-major and transposed
+  // copies, split into (hi, lo) for bf16 operands
+  auto put_m = [&](int rt, int st, f32x4 mv) {
+    f32x4 parts[2];
+    if constexpr (OT::NS == 2) {
+      parts[0] = bf16x4_to_f(cvt_frag<bf16_t>(mv));
+      parts[1] = mv - parts[0];
+    } else {
+      parts[0] = mv;
+    }
+#pragma unroll
+    for (int pt = 0; pt < OT::NS; ++pt) {
+      store_tile16(ops + OT::M + pt * OT::MAT + (size_t)(16 * rt) * C + 16 * st, parts[pt], g, n, C);
+      put4<T>(ops + OT::MT + pt * OT::MAT + (size_t)(16 * st + n) * C + 16 * rt + 4 * g, parts[pt]);
+    }
+  };
   for (int tile = w; tile < NT * NT; tile += 4) {
     constexpr int NL = NT * (NT + 1) / 2;  // lower tiles first, then the upper ones
     int rt = 0, st = 0;
@@ -199,11 +216,8 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
     const int c = 16 * st + n;
     if (st > rt) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int r = 16 * rt + 4 * g + j;
-        Mg[r * C + c] = 0.f;
-        sm.L[r][c] = 0.f;
-      }
+      for (int j = 0; j < 4; ++j) sm.L[16 * rt + 4 * g + j][c] = 0.f;
+      put_m(rt, st, zero4());
       continue;
     }
     f32x4 aq = zero4(), ak = zero4();
@@ -221,6 +235,7 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
       Gc[e] = sm.G[c][e];
       k2c[e] = sm.k2[c][e];
     }
+    f32x4 mv;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int r = 16 * rt + 4 * g + j;
@@ -233,8 +248,39 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
           rk += sm.k2[r][e] * d;
         }
       }
-      Mg[r * C + c] = (c <= r) ? aq[j] * rq : 0.f;
+      mv[j] = (c <= r) ? aq[j] * rq : 0.f;
       sm.L[r][c] = (c < r) ? sm.beta[r] * ak[j] * rk : 0.f;
+    }
+    put_m(rt, st, mv);
+  }
+  // ---- K^T and Q^T of the chunk (4 x 4 blocks; rows past T are zero)
+  {
+    constexpr int NB = (C / 4) * (KD / 4);
+    for (int idx = tid; idx < 2 * NB; idx += 256) {
+      const int mtx = idx / NB, bi = idx % NB;
+      const int rb = bi / (KD / 4), kb = bi % (KD / 4);
+      float x[4][4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = 4 * rb + i;
+        if constexpr (STAGE) {
+          const T* src = mtx ? &sm.u.qk.sQ[r][4 * kb] : &sm.u.qk.sK[r][4 * kb];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) x[i][j] = Elem<T>::to_f(src[j]);
+        } else {
+          const T* src = (mtx ? Qg : Kg) + (size_t)min(t0 + r, s.T - 1) * krs + 4 * kb;
+          const bool ok = t0 + r < s.T;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const float v = Elem<T>::to_f(src[j]);
+            x[i][j] = ok ? v : 0.f;
+          }
+        }
+      }
+      T* dst = ops + (mtx ? OT::Qt : OT::Kt);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        put4<T>(dst + (size_t)(4 * kb + j) * C + 4 * rb, f32x4{x[0][j], x[1][j], x[2][j], x[3][j]});
     }
   }
   __syncthreads();
@@ -243,11 +289,27 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
   if (s.variant == 1) {
     unit_lower_inverse<C, 256>([&](int r, int c) { return sm.L[r][c]; }, &sm.u.inv.X[0][0],
                                Sm::CP, &sm.u.inv.Y[0][0][0]);
-    float* Tg = p.Tu + (size_t)ch * C * C;
-    for (int idx = tid; idx < C * C / 4; idx += 256) {
-      const int r = idx / (C / 4), c4 = 4 * (idx % (C / 4));
-      *(f32x4*)(Tg + r * C + c4) = *(const f32x4*)&sm.u.inv.X[r][c4] *
-                                   *(const f32x4*)&sm.beta[c4];
+    // Tu row-major and transposed, from 4 x 4 blocks of the inverse
+    for (int idx = tid; idx < (C / 4) * (C / 4); idx += 256) {
+      const int rb = idx / (C / 4), cb = idx % (C / 4);
+      const f32x4 bc = *(const f32x4*)&sm.beta[4 * cb];
+      f32x4 x[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) x[i] = *(const f32x4*)&sm.u.inv.X[4 * rb + i][4 * cb] * bc;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const f32x4 col{x[0][i], x[1][i], x[2][i], x[3][i]};
+        if constexpr (OT::NS == 2) {
+          const f32x4 hr = bf16x4_to_f(cvt_frag<bf16_t>(x[i])), hc = bf16x4_to_f(cvt_frag<bf16_t>(col));
+          put4<T>(ops + OT::Tu + (size_t)(4 * rb + i) * C + 4 * cb, hr);
+          put4<T>(ops + OT::Tu + OT::MAT + (size_t)(4 * rb + i) * C + 4 * cb, x[i] - hr);
+          put4<T>(ops + OT::TuT + (size_t)(4 * cb + i) * C + 4 * rb, hc);
+          put4<T>(ops + OT::TuT + OT::MAT + (size_t)(4 * cb + i) * C + 4 * rb, col - hc);
+        } else {
+          put4<T>(ops + OT::Tu + (size_t)(4 * rb + i) * C + 4 * cb, x[i]);
+          put4<T>(ops + OT::TuT + (size_t)(4 * cb + i) * C + 4 * rb, col);
+        }
+      }
     }
   }
 }
@@ -281,32 +343,38 @@ struct FwdSmem {
 };
 
 // Register staging of one chunk's inputs for the recurrent forward: global
-// loads are issued one chunk ahead into registers and written to shared
-// memory (including the transposed copies) at the top of the next chunk.
+// loads are issued one chunk ahead into registers and copied to shared memory
+// at the top of the next chunk (K^T written from the same K registers).  M
+// and Tu arrive from the prep kernel already split, as plain 16-byte chunks.
+// Every load is unconditional (a row past T is read from row T - 1, an index
+// past the end from the last element) and store() zeroes or skips what is
+// out of range: a per-lane branch around a load would make the compiler wait
+// for it at once, which defeats the prefetch.  Waves past the last piece of
+// a loop step skip it (a scalar branch).
 template <typename T, int KD, int C, int E, int NTHR, bool STAGE_Q, bool SPLIT>
 struct FwdStage {
-  // K and Q move in blocks of 4 rows x KW columns (narrower for eight-wave
-  // workgroups, so that every thread holds a share)
+  typedef OpTiles<T, KD, C> OT;
+  static constexpr int EC = 16 / (int)sizeof(T);        // elements per 16-byte chunk
+  static constexpr int NMC = 2 * OT::NS * C * C / EC;    // chunks of M and Tu (hi, lo)
+  static constexpr int NM = (NMC + NTHR - 1) / NTHR;
+  // K and Q rows move in blocks of 4 rows x KW columns; K^T is written from
+  // the same registers (narrower blocks for eight-wave workgroups)
   static constexpr int KW = NTHR >= 512 ? 4 : 8;
   static constexpr int KWD = KW * (int)sizeof(T) / 4;  // words per block row
   static constexpr int RB = C / 4, CB = KD / KW;
   static constexpr int NKB = (RB * CB + NTHR - 1) / NTHR;
-  static constexpr int NV4 = (C * 4 + NTHR - 1) / NTHR;    // 4-element pieces of the V tile
-  static constexpr int NMB = (C * C / 4 + NTHR - 1) / NTHR;
+  static constexpr int NV4 = (C * 4 + NTHR - 1) / NTHR;  // 4-element pieces of the V tile
   static constexpr int NCB = (3 * E * C / 4 + NTHR - 1) / NTHR;
   static constexpr int E4 = (E + 3) & ~3;
   uint32_t k[NKB][4][KWD];
   uint32_t q[STAGE_Q ? NKB : 1][4][KWD];
+  uint4 mt[NM];
   uint32_t v[NV4][sizeof(T) == 2 ? 2 : 4];  // 4 elements as raw words
-  f32x4 m[NMB], tu[NMB], c[NCB];
+  f32x4 c[NCB];
   float gc, beta;
 
-  // Every load is unconditional (a row past T is read from row T - 1, an
-  // index past the end from the last element) and store() zeroes or skips
-  // what is out of range: a per-lane branch around a load would make the
-  // compiler wait for it at once, which defeats the prefetch.
-  // parts: 1 = the K, Q rows and the V tile; 2 = M, Tu and the vectors (the
-  // two halves are issued at different points of a chunk step)
+  // parts: 1 = the K, Q rows and the V tile; 2 = M, Tu and the vectors
+  // (the two halves are issued at different points of a chunk step)
   __device__ __forceinline__ void load(const Shape& s, const FwdIn& in, const PrepBufs& p,
                                        const T* Kg, const T* Qg, const T* Vg, int b, int h,
                                        int ci, int parts = 3) {
@@ -315,47 +383,44 @@ struct FwdStage {
     const int t0 = ci * C;
     const size_t ch = (size_t)(b * s.H + h) * s.Nc + ci;
     const size_t krs = (size_t)s.H * KD, vrs = (size_t)s.H * s.V;
+    const T* ops = (const T*)p.ops + ch * OT::STRIDE;
     if (parts & 1) {
 #pragma unroll
-    for (int i = 0; i < NKB; ++i) {
-      if (w0 + i * NTHR >= RB * CB) continue;  // (scalar branch: no block in this wave)
-      const int blk = min(tid + i * NTHR, RB * CB - 1);
-      const int rb = blk % RB, cb = blk / RB;
+      for (int i = 0; i < NKB; ++i) {
+        if (w0 + i * NTHR >= RB * CB) continue;
+        const int blk = min(tid + i * NTHR, RB * CB - 1);
+        const int rb = blk % RB, cb = blk / RB;
 #pragma unroll
-      for (int rr = 0; rr < 4; ++rr) {
-        const int t = min(t0 + 4 * rb + rr, s.T - 1);
-        ld_words(k[i][rr], Kg + (size_t)t * krs + KW * cb);
-        if constexpr (STAGE_Q) ld_words(q[i][rr], Qg + (size_t)t * krs + KW * cb);
+        for (int rr = 0; rr < 4; ++rr) {
+          const int t = min(t0 + 4 * rb + rr, s.T - 1);
+          ld_words(k[i][rr], Kg + (size_t)t * krs + KW * cb);
+          if constexpr (STAGE_Q) ld_words(q[i][rr], Qg + (size_t)t * krs + KW * cb);
+        }
       }
-    }
 #pragma unroll
-    for (int i = 0; i < NV4; ++i) {
-      if (w0 + i * NTHR >= C * 4) continue;
-      const int idx = min(tid + i * NTHR, C * 4 - 1);
-      const int r = idx >> 2, c4 = idx & 3;
-      const int t = min(t0 + r, s.T - 1);
-      if constexpr (sizeof(T) == 2) {
-        const uint2 x = *(const uint2*)(Vg + (size_t)t * vrs + 4 * c4);
-        v[i][0] = x.x;
-        v[i][1] = x.y;
-      } else {
-        const uint4 x = *(const uint4*)(Vg + (size_t)t * vrs + 4 * c4);
-        v[i][0] = x.x;
-        v[i][1] = x.y;
-        v[i][2] = x.z;
-        v[i][3] = x.w;
+      for (int i = 0; i < NV4; ++i) {
+        if (w0 + i * NTHR >= C * 4) continue;
+        const int idx = min(tid + i * NTHR, C * 4 - 1);
+        const int r = idx >> 2, c4 = idx & 3;
+        const int t = min(t0 + r, s.T - 1);
+        if constexpr (sizeof(T) == 2) {
+          const uint2 x = *(const uint2*)(Vg + (size_t)t * vrs + 4 * c4);
+          v[i][0] = x.x;
+          v[i][1] = x.y;
+        } else {
+          const uint4 x = *(const uint4*)(Vg + (size_t)t * vrs + 4 * c4);
+          v[i][0] = x.x;
+          v[i][1] = x.y;
+          v[i][2] = x.z;
+          v[i][3] = x.w;
+        }
       }
-    }
     }
     if (!(parts & 2)) return;
-    const float* Mg = p.M + ch * C * C;
-    const float* Tg = p.Tu + ch * C * C;
 #pragma unroll
-    for (int i = 0; i < NMB; ++i) {
-      if (w0 + i * NTHR >= C * C / 4) continue;
-      const int idx = min(tid + i * NTHR, C * C / 4 - 1);
-      m[i] = *(const f32x4*)(Mg + 4 * idx);
-      tu[i] = *(const f32x4*)(Tg + 4 * idx);
+    for (int i = 0; i < NM; ++i) {
+      if (w0 + i * NTHR >= NMC) continue;
+      mt[i] = ((const uint4*)(ops + OT::M))[min(tid + i * NTHR, NMC - 1)];
     }
     const float* cg = p.coef + ch * 3 * E * C;
 #pragma unroll
@@ -369,7 +434,6 @@ struct FwdStage {
 
   template <typename Sm>
   __device__ __forceinline__ void store(Sm& sm, int variant, int t0, int nT) const {
-    typedef typename Elem<T>::frag F;
     const int tid = threadIdx.x;
 #pragma unroll
     for (int i = 0; i < NKB; ++i) {
@@ -413,21 +477,20 @@ struct FwdStage {
         }
       }
     }
+    // M and Tu chunks: matrix m (M hi, M lo, Tu hi, Tu lo for bf16; M, Tu for fp32)
+    constexpr int PER = C * C / EC;
 #pragma unroll
-    for (int i = 0; i < NMB; ++i) {
+    for (int i = 0; i < NM; ++i) {
       const int idx = tid + i * NTHR;
-      if (idx < C * C / 4) {
-        const int r = idx / (C / 4), c4 = idx % (C / 4);
-        F hi, lo;
-        split_frag(m[i], hi, lo);
-        *(F*)&sm.M[r][4 * c4] = hi;
-        if constexpr (SPLIT) *(F*)&sm.ML[r][4 * c4] = lo;
-        if (variant == 1) {
-          split_frag(tu[i], hi, lo);
-          *(F*)&sm.Tu[r][4 * c4] = hi;
-          if constexpr (SPLIT) *(F*)&sm.TuL[r][4 * c4] = lo;
-        }
-      }
+      if (idx >= NMC) continue;
+      const int mtx = idx / PER, j = idx % PER;
+      const int r = j / (C / EC), c0 = EC * (j % (C / EC));
+      T* dst;
+      if constexpr (OT::NS == 2)
+        dst = (mtx == 0) ? &sm.M[r][c0] : (mtx == 1) ? &sm.ML[r][c0] : (mtx == 2) ? &sm.Tu[r][c0] : &sm.TuL[r][c0];
+      else
+        dst = (mtx == 0) ? &sm.M[r][c0] : &sm.Tu[r][c0];
+      lds_put16(dst, mt[i]);
     }
     float* cs = &sm.coef[0][0][0];
 #pragma unroll

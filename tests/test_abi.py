@@ -160,8 +160,9 @@ def test_size_queries():
     ws_f, ws_b, sv = (tla.workspace_bytes(d, tla.OP_FWD), tla.workspace_bytes(d, tla.OP_BWD),
                       tla.saved_bytes(d))
     nch = 4 * 8 * 64
-    # forward workspace: per-chunk coefficient vectors, gamma^C, M and Tu (fp32)
-    assert ws_f == nch * (3 * 8 * 64 * 4 + 8 * 4 + 2 * 64 * 64 * 4)
+    # forward workspace: per-chunk coefficient vectors, gamma^C and the bf16
+    # operand tiles (M, Tu as hi + lo pairs, row-major and transposed; K^T, Q^T)
+    assert ws_f == nch * (3 * 8 * 64 * 4 + 8 * 4 + (8 * 64 * 64 + 2 * 128 * 64) * 2)
     # saved: bf16 chunk-start states, fp32 U and V - W, and the same prep terms
     assert sv == nch * (8 * 128 * 128 * 2 + 2 * 64 * 128 * 4) + ws_f
     assert ws_b > ws_f > 0
