@@ -399,6 +399,76 @@ __device__ __forceinline__ void store_tile16(T* dst, f32x4 x, int g, int n, int 
     *(f32x4*)p = x;
 }
 
+// ------------------------------------------------ direct global -> LDS copies
+// gfx950 loads that write shared memory without a register round trip: every
+// active lane l of a wave copies SIZE (4 or 16) bytes from base + off (base
+// wave-uniform, off per lane) to LDS bytes [lds + SIZE l, lds + SIZE (l + 1))
+// (lds wave-uniform, passed in M0).  They count in vmcnt like other vector
+// loads (which complete in issue order for the counter), so a vmcnt wait
+// followed by a barrier makes the data visible to the whole workgroup.  They
+// are issued from inline assembly: the compiler then neither adds waits for
+// them at every barrier nor before unrelated shared-memory reads, and the
+// kernels wait for them explicitly with wait_vmcnt.  (A compiler wait for one
+// of its own loads stays correct: copies issued after that load only make it
+// wait longer.)
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)p);
+}
+// (M0 is written inside the assembly and declared clobbered; the compiler
+// warns that it reserves M0, which none of these kernels otherwise use)
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+template <int SIZE>
+__device__ __forceinline__ void lds_dma(const void* base, uint32_t off, uint32_t lds) {
+  static_assert(SIZE == 4 || SIZE == 16, "copy size");
+  if constexpr (SIZE == 16)
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+                 :: "v"(off), "s"(base), "s"(lds) : "memory", "m0");
+  else
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %0, %1"
+                 :: "v"(off), "s"(base), "s"(lds) : "memory", "m0");
+}
+#pragma clang diagnostic pop
+// Wait until at most N vector memory operations of this wave are in flight.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+// Copies issued per wave when the 64-lane blocks of an NB-block copy are
+// dealt round-robin to NW waves: the wave with the fewest (the last one).
+template <int NB, int NW>
+constexpr int dma_min_count() {
+  int c = 0;
+  for (int i = 0; i * NW + NW - 1 < NB; ++i) ++c;
+  return c;
+}
+
+// Unpadded LDS tile of R rows x COLS elements in 16-byte chunks.  Within row
+// r the chunk index is XOR-ed with sw(r), so that 16 consecutive rows read at
+// the same columns touch 16 distinct chunk positions (fragment reads of a
+// 16-row tile are free of bank conflicts) while whole 1 KiB blocks of the
+// tile can still be filled by the direct copies above.
+template <typename T, int R, int COLS>
+struct SwzTile {
+  static constexpr int EC = 16 / (int)sizeof(T);  // elements per chunk
+  static constexpr int NCH = COLS / EC;           // chunks per row (a power of two)
+  static constexpr int NCHK = R * NCH;            // chunks in the tile
+  static_assert(COLS % EC == 0 && (NCH & (NCH - 1)) == 0, "rows of 2^n whole chunks");
+  alignas(16) T d[R * COLS];
+  __device__ static __forceinline__ int sw(int r) {
+    return NCH >= 16 ? (r & 15) : ((r * NCH / 16) & (NCH - 1));
+  }
+  __device__ __forceinline__ const T* at(int r, int col) const {
+    return d + r * COLS + ((col / EC) ^ sw(r)) * EC + col % EC;
+  }
+  // the logical (row, chunk) held at physical chunk position p
+  __device__ static __forceinline__ void logical(int p, int& r, int& c) {
+    r = p / NCH;
+    c = (p % NCH) ^ sw(r);
+  }
+};
+
 // XCD-aware block mapping: the 8 accelerator dies each have their own L2 and
 // receive blocks round-robin by linear id.  Blocks that share a head (the
 // value tiles of one head read the same chunk inputs) are placed on one die.

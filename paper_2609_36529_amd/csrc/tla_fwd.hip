@@ -317,24 +317,23 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
 // ---------------------------------------------------------------- forward
 template <typename T, int KD, int C, int E, int NW>
 struct FwdSmem {
-  static constexpr int KP = KD + 4;  // padded row lengths (elements)
-  static constexpr int CP = C + 4;
+  static constexpr int CP = C + 4;  // padded row length of the V^T tile
   static constexpr int NT = C / 16;
   static constexpr int E4 = (E + 3) & ~3;
+  static constexpr int EC = 16 / (int)sizeof(T);
   // bf16 operands carry Tu and M as hi + lo pairs (SPLIT).  The largest
   // instances read the queries straight from global memory so that the plan
   // fits the 160 KiB of LDS.
   static constexpr bool SPLIT = sizeof(T) == 2;
   static constexpr bool STAGE_Q = sizeof(T) == 2 && E < 16;
-  alignas(16) T K[C][KP];
-  alignas(16) T Q[STAGE_Q ? C : 1][KP];
-  alignas(16) T Kt[KD][CP];
+  SwzTile<T, C, KD> K;
+  SwzTile<T, STAGE_Q ? C : 1, STAGE_Q ? KD : EC> Q;
+  SwzTile<T, KD, C> Kt;
+  SwzTile<T, C, C> Tu, M;
+  SwzTile<T, SPLIT ? C : 1, SPLIT ? C : EC> TuL, ML;
   alignas(16) T Vt[16][CP];
-  alignas(16) T Tu[C][CP];
-  alignas(16) T M[C][CP];
-  alignas(16) T TuL[SPLIT ? C : 1][CP];
-  alignas(16) T ML[SPLIT ? C : 1][CP];
-  alignas(16) float coef[3][E][C];
+  alignas(16) float coef01[2][E][C];  // a_e, b_e
+  alignas(16) float coef2[E][C];      // c_e
   alignas(16) float gC[E4];
   alignas(16) float beta[C];
   alignas(16) f32x4 W[NW][NT][64];
@@ -342,124 +341,153 @@ struct FwdSmem {
   alignas(16) f32x4 Us[NT][64];  // U row tiles in the accumulator layout
 };
 
-// Register staging of one chunk's inputs for the recurrent forward: global
-// loads are issued one chunk ahead into registers and copied to shared memory
-// at the top of the next chunk (K^T written from the same K registers).  M
-// and Tu arrive from the prep kernel already split, as plain 16-byte chunks.
-// Every load is unconditional (a row past T is read from row T - 1, an index
-// past the end from the last element) and store() zeroes or skips what is
-// out of range: a per-lane branch around a load would make the compiler wait
-// for it at once, which defeats the prefetch.  Waves past the last piece of
-// a loop step skip it (a scalar branch).
-template <typename T, int KD, int C, int E, int NTHR, bool STAGE_Q, bool SPLIT>
-struct FwdStage {
+// Direct copies of one chunk's operands into shared memory, in four groups
+// issued at different points of a chunk step (each right after the barrier
+// that frees its destination):
+//   KQ  the K (and Q) rows and the coefficients a_e, b_e   (for the next chunk)
+//   Tu  Tu (hi, lo)                                         (for the next chunk)
+//   M   M (hi, lo)                                          (for the next chunk)
+//   Kt  K^T and the coefficients c_e                        (for this chunk)
+// Wave w copies the 1 KiB blocks w, w + NW, ... of a tile.  K and Q rows past
+// T are read from row T - 1 (and zeroed after arrival in the last chunk);
+// M, Tu and K^T come from the prep kernel's operand tiles, whose rows and
+// columns past T are already zero.
+template <typename T, int KD, int C, int E, int NW>
+struct FwdDma {
+  typedef FwdSmem<T, KD, C, E, NW> Sm;
   typedef OpTiles<T, KD, C> OT;
-  static constexpr int EC = 16 / (int)sizeof(T);        // elements per 16-byte chunk
-  static constexpr int NMC = 2 * OT::NS * C * C / EC;    // chunks of M and Tu (hi, lo)
-  static constexpr int NM = (NMC + NTHR - 1) / NTHR;
-  // K and Q rows move in blocks of 4 rows x KW columns; K^T is written from
-  // the same registers (narrower blocks for eight-wave workgroups)
-  static constexpr int KW = NTHR >= 512 ? 4 : 8;
-  static constexpr int KWD = KW * (int)sizeof(T) / 4;  // words per block row
-  static constexpr int RB = C / 4, CB = KD / KW;
-  static constexpr int NKB = (RB * CB + NTHR - 1) / NTHR;
+  static constexpr int NCO01 = 2 * E * C * 4, NCO2 = E * C * 4;  // bytes
+  // a coefficient copy uses 16-byte lanes when its 1 KiB blocks split evenly
+  // over the waves, else 4-byte lanes when those do
+  template <int NBYTES>
+  static constexpr int co_size() {
+    return (NBYTES % (1024 * NW) == 0) ? 16 : (NBYTES % (256 * NW) == 0) ? 4 : 16;
+  }
+  template <int NBYTES>
+  static constexpr int co_count() {
+    constexpr int SZ = co_size<NBYTES>();
+    return dma_min_count<(NBYTES + 64 * SZ - 1) / (64 * SZ), NW>();
+  }
+  template <typename Tile>
+  static constexpr int tile_count() {
+    return dma_min_count<(Tile::NCHK + 63) / 64, NW>();
+  }
+  static constexpr int N_KQ = tile_count<decltype(Sm::K)>() +
+                              (Sm::STAGE_Q ? tile_count<decltype(Sm::Q)>() : 0) + co_count<NCO01>();
+  static constexpr int N_TU = tile_count<decltype(Sm::Tu)>() * (Sm::SPLIT ? 2 : 1);
+  static constexpr int N_M = tile_count<decltype(Sm::M)>() * (Sm::SPLIT ? 2 : 1);
+  static constexpr int N_KT = tile_count<decltype(Sm::Kt)>() + co_count<NCO2>();
+
+  // Fill a swizzled tile; off(r, c) is the byte offset from the wave-uniform
+  // base of logical chunk c of row r.
+  template <typename Tile, typename F>
+  static __device__ __forceinline__ void tile(Tile& t, const void* base, F off) {
+    constexpr int NB = (Tile::NCHK + 63) / 64;
+    const int w = wave_id(), l = lane_id();
+    const uint32_t lds = lds_addr(t.d);
+#pragma unroll
+    for (int i = 0; i * NW < NB; ++i) {
+      const int blk = i * NW + w;
+      if (NB % NW != 0 && blk >= NB) continue;  // wave-uniform
+      int r, c;
+      Tile::logical(64 * blk + l, r, c);
+      if (Tile::NCHK % 64 == 0 || 64 * blk + l < Tile::NCHK)
+        lds_dma<16>(base, off(r, c), lds + 1024 * blk);
+    }
+  }
+  // A plain copy of NBYTES contiguous bytes.
+  template <int NBYTES>
+  static __device__ __forceinline__ void copy(void* dst, const void* src) {
+    constexpr int SZ = co_size<NBYTES>(), NB = (NBYTES + 64 * SZ - 1) / (64 * SZ);
+    const int w = wave_id(), l = lane_id();
+    const uint32_t lds = lds_addr(dst);
+#pragma unroll
+    for (int i = 0; i * NW < NB; ++i) {
+      const int blk = i * NW + w;
+      if (NB % NW != 0 && blk >= NB) continue;
+      const uint32_t off = 64 * SZ * blk + SZ * l;
+      if (NBYTES % (64 * SZ) == 0 || off < (uint32_t)NBYTES)
+        lds_dma<SZ>(src, off, lds + 64 * SZ * blk);
+    }
+  }
+  // an operand tile of the prep kernel (row-major C-wide rows) at src
+  template <typename Tile>
+  static __device__ __forceinline__ void op_tile(Tile& t, const T* src) {
+    tile(t, src, [](int r, int c) { return (uint32_t)(sizeof(T) * (r * C + Tile::EC * c)); });
+  }
+
+  static __device__ __forceinline__ void kq(Sm& sm, const Shape& s, const PrepBufs& p, const T* Kg,
+                                            const T* Qg, size_t ch, int t0) {
+    const size_t krs = (size_t)s.H * KD;
+    const int last = s.T - 1 - t0;  // rows past it are read from row T - 1
+    auto off = [=](int r, int c) {
+      return (uint32_t)(sizeof(T) * ((size_t)min(r, last) * krs + Sm::EC * c));
+    };
+    tile(sm.K, Kg + (size_t)t0 * krs, off);
+    if constexpr (Sm::STAGE_Q) tile(sm.Q, Qg + (size_t)t0 * krs, off);
+    copy<NCO01>(&sm.coef01[0][0][0], p.coef + ch * 3 * E * C);
+  }
+  static __device__ __forceinline__ void tu(Sm& sm, const PrepBufs& p, size_t ch) {
+    const T* ops = (const T*)p.ops + ch * OT::STRIDE;
+    op_tile(sm.Tu, ops + OT::Tu);
+    if constexpr (Sm::SPLIT) op_tile(sm.TuL, ops + OT::Tu + OT::MAT);
+  }
+  static __device__ __forceinline__ void m(Sm& sm, const PrepBufs& p, size_t ch) {
+    const T* ops = (const T*)p.ops + ch * OT::STRIDE;
+    op_tile(sm.M, ops + OT::M);
+    if constexpr (Sm::SPLIT) op_tile(sm.ML, ops + OT::M + OT::MAT);
+  }
+  static __device__ __forceinline__ void kt(Sm& sm, const PrepBufs& p, size_t ch) {
+    const T* ops = (const T*)p.ops + ch * OT::STRIDE;
+    op_tile(sm.Kt, ops + OT::Kt);
+    copy<NCO2>(&sm.coef2[0][0], p.coef + ch * 3 * E * C + 2 * E * C);
+  }
+};
+
+// Register staging of the small per-chunk inputs (the V tile, gamma^C, beta),
+// loaded one chunk ahead and written to shared memory at the top of the
+// chunk step (V transposed).  Loads are unconditional (clamped indices) and
+// store() zeroes what is past T.
+template <typename T, int C, int E, int NTHR>
+struct FwdVStage {
   static constexpr int NV4 = (C * 4 + NTHR - 1) / NTHR;  // 4-element pieces of the V tile
-  static constexpr int NCB = (3 * E * C / 4 + NTHR - 1) / NTHR;
   static constexpr int E4 = (E + 3) & ~3;
-  uint32_t k[NKB][4][KWD];
-  uint32_t q[STAGE_Q ? NKB : 1][4][KWD];
-  uint4 mt[NM];
   uint32_t v[NV4][sizeof(T) == 2 ? 2 : 4];  // 4 elements as raw words
-  f32x4 c[NCB];
   float gc, beta;
 
-  // parts: 1 = the K, Q rows and the V tile; 2 = M, Tu and the vectors
-  // (the two halves are issued at different points of a chunk step)
   __device__ __forceinline__ void load(const Shape& s, const FwdIn& in, const PrepBufs& p,
-                                       const T* Kg, const T* Qg, const T* Vg, int b, int h,
-                                       int ci, int parts = 3) {
+                                       const T* Vg, int b, int h, int ci) {
     const int tid = threadIdx.x;
-    const int w0 = 64 * wave_id();  // first thread of this wave (wave-uniform)
+    const int w0 = 64 * wave_id();
     const int t0 = ci * C;
     const size_t ch = (size_t)(b * s.H + h) * s.Nc + ci;
-    const size_t krs = (size_t)s.H * KD, vrs = (size_t)s.H * s.V;
-    const T* ops = (const T*)p.ops + ch * OT::STRIDE;
-    if (parts & 1) {
+    const size_t vrs = (size_t)s.H * s.V;
 #pragma unroll
-      for (int i = 0; i < NKB; ++i) {
-        if (w0 + i * NTHR >= RB * CB) continue;
-        const int blk = min(tid + i * NTHR, RB * CB - 1);
-        const int rb = blk % RB, cb = blk / RB;
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr) {
-          const int t = min(t0 + 4 * rb + rr, s.T - 1);
-          ld_words(k[i][rr], Kg + (size_t)t * krs + KW * cb);
-          if constexpr (STAGE_Q) ld_words(q[i][rr], Qg + (size_t)t * krs + KW * cb);
-        }
-      }
-#pragma unroll
-      for (int i = 0; i < NV4; ++i) {
-        if (w0 + i * NTHR >= C * 4) continue;
-        const int idx = min(tid + i * NTHR, C * 4 - 1);
-        const int r = idx >> 2, c4 = idx & 3;
-        const int t = min(t0 + r, s.T - 1);
-        if constexpr (sizeof(T) == 2) {
-          const uint2 x = *(const uint2*)(Vg + (size_t)t * vrs + 4 * c4);
-          v[i][0] = x.x;
-          v[i][1] = x.y;
-        } else {
-          const uint4 x = *(const uint4*)(Vg + (size_t)t * vrs + 4 * c4);
-          v[i][0] = x.x;
-          v[i][1] = x.y;
-          v[i][2] = x.z;
-          v[i][3] = x.w;
-        }
+    for (int i = 0; i < NV4; ++i) {
+      if (w0 + i * NTHR >= C * 4) continue;
+      const int idx = min(tid + i * NTHR, C * 4 - 1);
+      const int r = idx >> 2, c4 = idx & 3;
+      const int t = min(t0 + r, s.T - 1);
+      if constexpr (sizeof(T) == 2) {
+        const uint2 x = *(const uint2*)(Vg + (size_t)t * vrs + 4 * c4);
+        v[i][0] = x.x;
+        v[i][1] = x.y;
+      } else {
+        const uint4 x = *(const uint4*)(Vg + (size_t)t * vrs + 4 * c4);
+        v[i][0] = x.x;
+        v[i][1] = x.y;
+        v[i][2] = x.z;
+        v[i][3] = x.w;
       }
     }
-    if (!(parts & 2)) return;
-#pragma unroll
-    for (int i = 0; i < NM; ++i) {
-      if (w0 + i * NTHR >= NMC) continue;
-      mt[i] = ((const uint4*)(ops + OT::M))[min(tid + i * NTHR, NMC - 1)];
-    }
-    const float* cg = p.coef + ch * 3 * E * C;
-#pragma unroll
-    for (int i = 0; i < NCB; ++i)
-      if (w0 + i * NTHR < 3 * E * C / 4)
-        c[i] = *(const f32x4*)(cg + 4 * min(tid + i * NTHR, 3 * E * C / 4 - 1));
     gc = p.gC[ch * E4 + min(tid, E4 - 1)];
     const int tb = min(t0 + min(tid, C - 1), s.T - 1);
     beta = in.beta ? in.beta[((size_t)b * s.T + tb) * s.H + h] : 1.f;
   }
 
   template <typename Sm>
-  __device__ __forceinline__ void store(Sm& sm, int variant, int t0, int nT) const {
+  __device__ __forceinline__ void store(Sm& sm, int t0, int nT) const {
     const int tid = threadIdx.x;
-#pragma unroll
-    for (int i = 0; i < NKB; ++i) {
-      const int blk = tid + i * NTHR;
-      const int rb = blk % RB, cb = blk / RB;
-      if (blk < RB * CB) {
-        uint32_t kk[4][KWD];
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr) {
-          const bool ok = t0 + 4 * rb + rr < nT;
-#pragma unroll
-          for (int j = 0; j < KWD; j += 2) {
-            kk[rr][j] = ok ? k[i][rr][j] : 0u;
-            kk[rr][j + 1] = ok ? k[i][rr][j + 1] : 0u;
-            *(uint2*)((uint32_t*)&sm.K[4 * rb + rr][KW * cb] + j) = make_uint2(kk[rr][j], kk[rr][j + 1]);
-            if constexpr (STAGE_Q)
-              *(uint2*)((uint32_t*)&sm.Q[4 * rb + rr][KW * cb] + j) =
-                  make_uint2(ok ? q[i][rr][j] : 0u, ok ? q[i][rr][j + 1] : 0u);
-          }
-        }
-#pragma unroll
-        for (int cc = 0; cc < KW; ++cc)
-          lds_put4(&sm.Kt[KW * cb + cc][4 * rb], word_elem<T>(kk[0], cc), word_elem<T>(kk[1], cc),
-                   word_elem<T>(kk[2], cc), word_elem<T>(kk[3], cc));
-      }
-    }
 #pragma unroll
     for (int i = 0; i < NV4; ++i) {
       const int idx = tid + i * NTHR;
@@ -477,31 +505,18 @@ struct FwdStage {
         }
       }
     }
-    // M and Tu chunks: matrix m (M hi, M lo, Tu hi, Tu lo for bf16; M, Tu for fp32)
-    constexpr int PER = C * C / EC;
-#pragma unroll
-    for (int i = 0; i < NM; ++i) {
-      const int idx = tid + i * NTHR;
-      if (idx >= NMC) continue;
-      const int mtx = idx / PER, j = idx % PER;
-      const int r = j / (C / EC), c0 = EC * (j % (C / EC));
-      T* dst;
-      if constexpr (OT::NS == 2)
-        dst = (mtx == 0) ? &sm.M[r][c0] : (mtx == 1) ? &sm.ML[r][c0] : (mtx == 2) ? &sm.Tu[r][c0] : &sm.TuL[r][c0];
-      else
-        dst = (mtx == 0) ? &sm.M[r][c0] : &sm.Tu[r][c0];
-      lds_put16(dst, mt[i]);
-    }
-    float* cs = &sm.coef[0][0][0];
-#pragma unroll
-    for (int i = 0; i < NCB; ++i) {
-      const int idx = tid + i * NTHR;
-      if (idx < 3 * E * C / 4) ((f32x4*)cs)[idx] = c[i];
-    }
     if (tid < E4) sm.gC[tid] = gc;
     if (tid < C) sm.beta[tid] = (t0 + tid < nT) ? beta : 0.f;
   }
 };
+
+// Rows past T of a row tile (the last, partial chunk): zero them after the
+// direct copies have landed.
+template <typename Tile>
+__device__ __forceinline__ void zero_rows_from(Tile& t, int r0, int nthr) {
+  for (int p = threadIdx.x; p < Tile::NCHK; p += nthr)
+    if (p / Tile::NCH >= r0) *(uint4*)((char*)t.d + 16 * p) = make_uint4(0, 0, 0, 0);
+}
 
 template <typename T, int KD, int C, int E, int NW>
 __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, void* out,
@@ -513,6 +528,7 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
   constexpr int NTHR = NW * 64;
   typedef typename Elem<T>::frag F;
   typedef FwdSmem<T, KD, C, E, NW> Sm;
+  typedef FwdDma<T, KD, C, E, NW> Dma;
   extern __shared__ __align__(16) unsigned char smem_raw[];
   Sm& sm = *reinterpret_cast<Sm*>(smem_raw);
 
@@ -544,17 +560,34 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
   const T* Qg = (const T*)in.q + (((size_t)b * s.T) * s.H + h) * KD;
   const T* Vg = (const T*)in.v + (((size_t)b * s.T) * s.H + h) * (size_t)V + v0;
   const size_t krs = (size_t)s.H * KD;  // row stride between positions
+  const size_t ch0 = (size_t)head * s.Nc;
 
-  FwdStage<T, KD, C, E, NTHR, Sm::STAGE_Q, Sm::SPLIT> stage;
-  if (s.Nc > 0) stage.load(s, in, p, Kg, Qg, Vg, b, h, 0);
+  FwdVStage<T, C, E, NTHR> vst;
+  if (s.Nc > 0) {
+    Dma::kq(sm, s, p, Kg, Qg, ch0, 0);
+    vst.load(s, in, p, Vg, b, h, 0);
+    Dma::tu(sm, p, ch0);
+    Dma::m(sm, p, ch0);
+  }
 
   for (int ci = 0; ci < s.Nc; ++ci) {
     const int t0 = ci * C;
-    const size_t ch = (size_t)head * s.Nc + ci;
-    __syncthreads();  // the previous chunk is done with shared memory
+    const size_t ch = ch0 + ci;
+    const bool more = ci + 1 < s.Nc;
+    __syncthreads();  // the previous chunk is done with K^T and c_e
 
-    // ---- stage the chunk from registers (loaded during the previous chunk)
-    stage.store(sm, s.variant, ci * C, s.T);
+    // (the V tile first: the compiler's wait for its loads then covers only
+    // copies that were issued before it)
+    vst.store(sm, ci * C, s.T);
+    Dma::kt(sm, p, ch);
+    // the K, Q rows, a_e, b_e, Tu and M of this chunk have landed (only the
+    // K^T copies just issued may still be in flight)
+    wait_vmcnt<Dma::N_KT>();
+    if (t0 + C > s.T) {  // every wave's copies must have landed before the zeroing
+      __syncthreads();
+      zero_rows_from(sm.K, s.T - t0, NTHR);
+      if constexpr (Sm::STAGE_Q) zero_rows_from(sm.Q, s.T - t0, NTHR);
+    }
     __syncthreads();
 
     // ---- operand copies of the chunk-start state
@@ -578,71 +611,133 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
     // ---- P^K_e = K S_e, then P^Q_e = Q S_e for the owned slices, each folded
     // straight into this wave's partial of W = sum_e diag(a_e) P^K_e and of
     // sum_e diag(b_e) P^Q_e (the two passes keep one set of accumulators live)
-#pragma unroll
-    for (int pass = 0; pass < 2; ++pass) {
-      f32x4 P[SPW][NT];
-#pragma unroll
-      for (int rt = 0; rt < NT; ++rt)
-#pragma unroll
-        for (int i = 0; i < SPW; ++i) P[i][rt] = zero4();
+    {
       // A fragment of K (pass 0) or Q (pass 1) rows for row tile rt, block kb
-      auto afrag = [&](int rt, int kb) -> F {
+      auto afrag = [&](int pass, int rt, int kb) -> F {
         const int r = 16 * rt + n;
-        if (pass == 0) return ld_frag(&sm.K[r][16 * kb + 4 * g]);
+        if (pass == 0) return ld_frag(sm.K.at(r, 16 * kb + 4 * g));
         if constexpr (Sm::STAGE_Q) {
-          return ld_frag(&sm.Q[r][16 * kb + 4 * g]);
+          return ld_frag(sm.Q.at(r, 16 * kb + 4 * g));
         } else {
           const bool qok = t0 + r < s.T;
           return qok ? ld_frag(Qg + (size_t)(t0 + r) * krs + 16 * kb + 4 * g) : cvt_frag<T>(zero4());
         }
       };
-      // k-block outer: the fragments of all row tiles are loaded together and
-      // NT x SPW independent accumulators advance per step
+      // fold the accumulators of a pass into this wave's partial
+      auto fold = [&](int pass, f32x4(&P)[SPW][NT]) {
 #pragma unroll
-      for (int kb = 0; kb < KT; kb += (KT > 1 ? 2 : 1)) {
-        if constexpr (KT > 1) {
-          F a0[NT], a1[NT];
+        for (int rt = 0; rt < NT; ++rt) {
+          f32x4 acc = zero4();
+#pragma unroll
+          for (int i = 0; i < SPW; ++i) {
+            const int e = w * SPW + i;
+            if (RAGGED && e >= E) continue;
+            acc += *(const f32x4*)&sm.coef01[pass][e][16 * rt + 4 * g] * P[i][rt];
+          }
+          if (pass == 0)
+            sm.W[w][rt][l] = acc;
+          else
+            sm.O[w][rt][l] = acc;
+        }
+      };
+      constexpr bool PIPE = KT > 1 && NW <= 4;
+      if constexpr (PIPE) {
+        // steps j = 0 .. 2 NS - 1 over (pass, k-block pair); the fragments of
+        // step j + 1 are loaded before the MFMAs of step j, so the shared
+        // memory latency hides behind them (with one wave per SIMD nothing
+        // else would; two waves per SIMD hide it for each other and have no
+        // registers to spare).  NT x SPW independent accumulators advance per
+        // step.
+        constexpr int NS = KT / 2;
+        auto load_step = [&](int j, F(&x0)[NT], F(&x1)[NT]) {
+          const int ps = j / NS, kb = 2 * (j % NS);
 #pragma unroll
           for (int rt = 0; rt < NT; ++rt) {
-            a0[rt] = afrag(rt, kb);
-            a1[rt] = afrag(rt, kb + 1);
+            x0[rt] = afrag(ps, rt, kb);
+            x1[rt] = afrag(ps, rt, kb + 1);
           }
+        };
+        f32x4 P[SPW][NT];
+#pragma unroll
+        for (int rt = 0; rt < NT; ++rt)
+#pragma unroll
+          for (int i = 0; i < SPW; ++i) P[i][rt] = zero4();
+        F a0[NT], a1[NT];
+        load_step(0, a0, a1);
+#pragma unroll
+        for (int j = 0; j < 2 * NS; ++j) {
+          F b0[NT], b1[NT];
+          if (j + 1 < 2 * NS) load_step(j + 1, b0, b1);
+          const int kb = 2 * (j % NS);
 #pragma unroll
           for (int i = 0; i < SPW; ++i) {
             if (RAGGED && w * SPW + i >= E) continue;
 #pragma unroll
             for (int rt = 0; rt < NT; ++rt) mma32(P[i][rt], a0[rt], a1[rt], Sop[i][kb], Sop[i][kb + 1]);
           }
-        } else {
-          F a[NT];
+          if (j % NS == NS - 1) {
+            fold(j / NS, P);
 #pragma unroll
-          for (int rt = 0; rt < NT; ++rt) a[rt] = afrag(rt, 0);
+            for (int rt = 0; rt < NT; ++rt)
 #pragma unroll
-          for (int i = 0; i < SPW; ++i) {
-            if (RAGGED && w * SPW + i >= E) continue;
+              for (int i = 0; i < SPW; ++i) P[i][rt] = zero4();
+          }
+          if (j + 1 < 2 * NS) {
 #pragma unroll
-            for (int rt = 0; rt < NT; ++rt) mma16(P[i][rt], a[rt], Sop[i][0]);
+            for (int rt = 0; rt < NT; ++rt) {
+              a0[rt] = b0[rt];
+              a1[rt] = b1[rt];
+            }
           }
         }
-      }
+      } else {
+        // k-block outer: the fragments of all row tiles are loaded together
+        // and NT x SPW independent accumulators advance per step
 #pragma unroll
-      for (int rt = 0; rt < NT; ++rt) {
-        f32x4 acc = zero4();
+        for (int pass = 0; pass < 2; ++pass) {
+          f32x4 P[SPW][NT];
 #pragma unroll
-        for (int i = 0; i < SPW; ++i) {
-          const int e = w * SPW + i;
-          if (RAGGED && e >= E) continue;
-          acc += *(const f32x4*)&sm.coef[pass][e][16 * rt + 4 * g] * P[i][rt];
+          for (int rt = 0; rt < NT; ++rt)
+#pragma unroll
+            for (int i = 0; i < SPW; ++i) P[i][rt] = zero4();
+#pragma unroll
+          for (int kb = 0; kb < KT; kb += (KT > 1 ? 2 : 1)) {
+            if constexpr (KT > 1) {
+              F a0[NT], a1[NT];
+#pragma unroll
+              for (int rt = 0; rt < NT; ++rt) {
+                a0[rt] = afrag(pass, rt, kb);
+                a1[rt] = afrag(pass, rt, kb + 1);
+              }
+#pragma unroll
+              for (int i = 0; i < SPW; ++i) {
+                if (RAGGED && w * SPW + i >= E) continue;
+#pragma unroll
+                for (int rt = 0; rt < NT; ++rt) mma32(P[i][rt], a0[rt], a1[rt], Sop[i][kb], Sop[i][kb + 1]);
+              }
+            } else {
+              F a[NT];
+#pragma unroll
+              for (int rt = 0; rt < NT; ++rt) a[rt] = afrag(pass, rt, 0);
+#pragma unroll
+              for (int i = 0; i < SPW; ++i) {
+                if (RAGGED && w * SPW + i >= E) continue;
+#pragma unroll
+                for (int rt = 0; rt < NT; ++rt) mma16(P[i][rt], a[rt], Sop[i][0]);
+              }
+            }
+          }
+          fold(pass, P);
         }
-        if (pass == 0)
-          sm.W[w][rt][l] = acc;
-        else
-          sm.O[w][rt][l] = acc;
       }
     }
     __syncthreads();
-    // the next chunk's rows are in flight while this chunk computes
-    if (ci + 1 < s.Nc) stage.load(s, in, p, Kg, Qg, Vg, b, h, ci + 1, 1);
+    // K, Q rows and a_e, b_e are free: the next chunk's are copied while this
+    // chunk computes
+    if (more) {
+      Dma::kq(sm, s, p, Kg, Qg, ch + 1, t0 + C);
+      vst.load(s, in, p, Vg, b, h, ci + 1);
+    }
 
     // ---- U = Tu (V - W) (GDN) or diag(beta) V (sGLA): wave w < NT forms row
     // tile w (Tu is lower triangular: blocks kb <= w only) and the tiles are
@@ -674,20 +769,20 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
         for (int kb = 0; kb < NT; kb += (NT > 1 ? 2 : 1)) {
           if (kb > rt) continue;
           if constexpr (NT > 1) {
-            const F h0 = ld_frag(&sm.Tu[r][16 * kb + 4 * g]);
-            const F h1 = ld_frag(&sm.Tu[r][16 * kb + 16 + 4 * g]);
+            const F h0 = ld_frag(sm.Tu.at(r, 16 * kb + 4 * g));
+            const F h1 = ld_frag(sm.Tu.at(r, 16 * kb + 16 + 4 * g));
             mma32(u, h0, h1, Xh[kb], Xh[kb + 1]);
             if constexpr (Sm::SPLIT) {
               mma32(u, h0, h1, Xl[kb], Xl[kb + 1]);
-              mma32(u, ld_frag(&sm.TuL[r][16 * kb + 4 * g]),
-                    ld_frag(&sm.TuL[r][16 * kb + 16 + 4 * g]), Xh[kb], Xh[kb + 1]);
+              mma32(u, ld_frag(sm.TuL.at(r, 16 * kb + 4 * g)),
+                    ld_frag(sm.TuL.at(r, 16 * kb + 16 + 4 * g)), Xh[kb], Xh[kb + 1]);
             }
           } else {
-            const F hh = ld_frag(&sm.Tu[n][4 * g]);
+            const F hh = ld_frag(sm.Tu.at(n, 4 * g));
             mma16(u, hh, Xh[0]);
             if constexpr (Sm::SPLIT) {
               mma16(u, hh, Xl[0]);
-              mma16(u, ld_frag(&sm.TuL[n][4 * g]), Xh[0]);
+              mma16(u, ld_frag(sm.TuL.at(n, 4 * g)), Xh[0]);
             }
           }
         }
@@ -702,6 +797,7 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
       }
     }
     __syncthreads();
+    if (more) Dma::tu(sm, p, ch + 1);  // Tu is free
     f32x4 U[NT];
     F Uh[NT], Ul[NT];
 #pragma unroll
@@ -711,35 +807,43 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
     }
 
     // ---- O for row tile w: sum of the partials plus M U
+    f32x4 oacc = zero4();
     if (w < NT) {
       const int rt = w;
-      f32x4 acc = zero4();
 #pragma unroll
-      for (int ww = 0; ww < NW; ++ww) acc += sm.O[ww][rt][l];
+      for (int ww = 0; ww < NW; ++ww) oacc += sm.O[ww][rt][l];
       const int r = 16 * rt + n;
-      auto mh = [&](int kb) { return ld_frag(&sm.M[r][16 * kb + 4 * g]); };
-      mma_k<C>(acc, mh, [&](int kb) { return Uh[kb]; });
+      auto mh = [&](int kb) { return ld_frag(sm.M.at(r, 16 * kb + 4 * g)); };
+      mma_k<C>(oacc, mh, [&](int kb) { return Uh[kb]; });
       if constexpr (Sm::SPLIT) {
-        mma_k<C>(acc, mh, [&](int kb) { return Ul[kb]; });
-        mma_k<C>(acc, [&](int kb) { return ld_frag(&sm.ML[r][16 * kb + 4 * g]); },
+        mma_k<C>(oacc, mh, [&](int kb) { return Ul[kb]; });
+        mma_k<C>(oacc, [&](int kb) { return ld_frag(sm.ML.at(r, 16 * kb + 4 * g)); },
                  [&](int kb) { return Uh[kb]; });
       }
+    }
+    // K^T and c_e of this chunk have landed (what was issued after them: the
+    // next chunk's rows and Tu); every wave is done with M after the barrier
+    if (more)
+      wait_vmcnt<Dma::N_KQ + Dma::N_TU>();
+    else
+      wait_vmcnt<0>();
+    __syncthreads();
+    if (more) Dma::m(sm, p, ch + 1);
+    if (w < NT) {
+      const int rt = w;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int t = t0 + 16 * rt + 4 * g + j;
         if (t < s.T) {
           const size_t off = (((size_t)b * s.T + t) * s.H + h) * (size_t)V + v0 + n;
           if (s.out_bf16)
-            ((bf16_t*)out)[off] = Elem<bf16_t>::from_f(acc[j]);
+            ((bf16_t*)out)[off] = Elem<bf16_t>::from_f(oacc[j]);
           else
-            ((float*)out)[off] = acc[j];
+            ((float*)out)[off] = oacc[j];
         }
       }
     }
 
-    // (the next chunk's M, Tu and vectors: gamma^C and the coefficients are
-    // read from LDS below, so their registers are only refilled here)
-    if (ci + 1 < s.Nc) stage.load(s, in, p, Kg, Qg, Vg, b, h, ci + 1, 2);
     // ---- state update S_e <- gamma^C_e S_e + K^T diag(c_e) U
     F Uc[SPW][NT], Ucl[SPW][NT];
 #pragma unroll
@@ -751,7 +855,7 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
       for (int kt = 0; kt < KT; ++kt) S[i][kt] *= gc;
 #pragma unroll
       for (int kb = 0; kb < NT; ++kb)
-        split_frag(U[kb] * *(const f32x4*)&sm.coef[2][e][16 * kb + 4 * g], Uc[i][kb], Ucl[i][kb]);
+        split_frag(U[kb] * *(const f32x4*)&sm.coef2[e][16 * kb + 4 * g], Uc[i][kb], Ucl[i][kb]);
     }
     // k-block outer: KT x SPW independent accumulators per step
 #pragma unroll
@@ -760,8 +864,8 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
         F a0[KT], a1[KT];
 #pragma unroll
         for (int kt = 0; kt < KT; ++kt) {
-          a0[kt] = ld_frag(&sm.Kt[16 * kt + n][16 * kb + 4 * g]);
-          a1[kt] = ld_frag(&sm.Kt[16 * kt + n][16 * kb + 16 + 4 * g]);
+          a0[kt] = ld_frag(sm.Kt.at(16 * kt + n, 16 * kb + 4 * g));
+          a1[kt] = ld_frag(sm.Kt.at(16 * kt + n, 16 * kb + 16 + 4 * g));
         }
 #pragma unroll
         for (int i = 0; i < SPW; ++i) {
@@ -777,7 +881,7 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
       } else {
         F a[KT];
 #pragma unroll
-        for (int kt = 0; kt < KT; ++kt) a[kt] = ld_frag(&sm.Kt[16 * kt + n][4 * g]);
+        for (int kt = 0; kt < KT; ++kt) a[kt] = ld_frag(sm.Kt.at(16 * kt + n, 4 * g));
 #pragma unroll
         for (int i = 0; i < SPW; ++i) {
           if (RAGGED && w * SPW + i >= E) continue;
