@@ -296,6 +296,7 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
   const size_t krs = (size_t)s.H * KD;
   const size_t vrs = (size_t)s.H * V;
 
+  const bf16x4 idf = identity_frag();  // for the transposing dS' stores
   RecStage<T, KD, C, E, NTHR> stage;
   if constexpr (PREFETCH) stage.load(s, p, Kg, Qg, dOg, (size_t)head * s.Nc + s.Nc - 1, s.Nc - 1);
   for (int ci = s.Nc - 1; ci >= 0; --ci) {
@@ -315,22 +316,28 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
     }
     __syncthreads();
 
-    // ---- store dS' (gradient of the chunk-end state) for the chunk-parallel kernel
+    // ---- operand copies of dS' (gradient of the chunk-end state), stored for
+    // the chunk-parallel kernel
+    F dSop[SPW][KT];
+#pragma unroll
+    for (int i = 0; i < SPW; ++i)
+#pragma unroll
+      for (int kt = 0; kt < KT; ++kt) dSop[i][kt] = cvt_frag<T>(dS[i][kt]);
 #pragma unroll
     for (int i = 0; i < SPW; ++i) {
       const int e = w * SPW + i;
       if (RAGGED && e >= E) continue;
       T* dst = (T*)bb.dSck + ((ch * E + e) * (size_t)(V / 16) + vt) * KD * 16;
 #pragma unroll
-      for (int kt = 0; kt < KT; ++kt) store_tile16(dst + 256 * kt, dS[i][kt], g, n);
+      for (int kt = 0; kt < KT; ++kt) {
+        if constexpr (sizeof(T) == 2)
+          store_tile16_frag(dst + 256 * kt, dSop[i][kt], idf, g, n);
+        else
+          store_tile16(dst + 256 * kt, dS[i][kt], g, n);
+      }
     }
 
     // ---- partial of sum_e diag(c_e) K dS'_e over the owned slices
-    F dSop[SPW][KT];
-#pragma unroll
-    for (int i = 0; i < SPW; ++i)
-#pragma unroll
-      for (int kt = 0; kt < KT; ++kt) dSop[i][kt] = cvt_frag<T>(dS[i][kt]);
     // (K fragments are read once per key block and reused for every owned slice)
 #pragma unroll
     for (int rt = 0; rt < NT; ++rt) {

@@ -370,12 +370,30 @@ __device__ __forceinline__ void put4(T* dst, f32x4 x) {
     *(f32x4*)dst = x;
 }
 
+// Vector stores issued from inline assembly: exactly one instruction each, so
+// a kernel can count them in an explicit vmcnt wait (on gfx9 a store counts
+// in vmcnt until the write is acknowledged, in issue order with the loads).
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ void gstore_b32(void* p, uint32_t x) {
+  asm volatile("global_store_dword %0, %1, off" ::"v"(p), "v"(x) : "memory");
+}
+__device__ __forceinline__ void gstore_b64(void* p, u32x2 x) {
+  asm volatile("global_store_dwordx2 %0, %1, off" ::"v"(p), "v"(x) : "memory");
+}
+// (a VALU write to the data registers of a store of more than 8 bytes needs
+// one wait state after it; the compiler cannot see that inside the assembly,
+// so the nop is part of it)
+__device__ __forceinline__ void gstore_b128(void* p, u32x4 x) {
+  asm volatile("global_store_dwordx4 %0, %1, off\n\ts_nop 1" ::"v"(p), "v"(x) : "memory");
+}
+
 // Store a 16 x 16 accumulator tile (lane (g, n) holds rows 4 g + j, column n)
 // into a row-major tile at dst (row r at dst + ld r, ld = 16 by default).  Two DPP
 // exchange rounds transpose 4 x 4 blocks within each quad of lanes, after
 // which lane n holds row 4 g + n % 4, columns 4 (n / 4) .. + 3 and writes
 // them with one 8-byte (bf16) or 16-byte (fp32) store instead of four
-// scalar ones.
+// scalar ones (one store instruction per tile, countable in a vmcnt wait).
 template <typename T>
 __device__ __forceinline__ void store_tile16(T* dst, f32x4 x, int g, int n, int ld = 16) {
   const int i = n & 3;
@@ -394,9 +412,33 @@ __device__ __forceinline__ void store_tile16(T* dst, f32x4 x, int g, int n, int 
   x[3] = b1 ? x[3] : t;
   T* p = dst + (4 * g + i) * ld + 4 * (n >> 2);
   if constexpr (sizeof(T) == 2)
-    *(uint2*)p = __builtin_bit_cast(uint2, cvt_frag<bf16_t>(x));
+    gstore_b64(p, __builtin_bit_cast(u32x2, cvt_frag<bf16_t>(x)));
   else
-    *(f32x4*)p = x;
+    gstore_b128(p, __builtin_bit_cast(u32x4, x));
+}
+
+// The identity as a 16-deep bf16 B fragment: lane (g, n) holds I[4 g + j][n].
+__device__ __forceinline__ bf16x4 identity_frag() {
+  const int l = lane_id(), g = l >> 4, n = l & 15;
+  bf16x4 r;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) r[j] = (__bf16)((4 * g + j == n) ? 1.f : 0.f);
+  return r;
+}
+
+// Store a 16 x 16 tile given as a bf16 operand fragment x (lane (g, n) holds
+// T[4 g + j][n], the layout of an accumulator converted to bf16) row-major at
+// dst (row stride 16).  Fed as the A operand the fragment is T^T, so one
+// 16x16x16 MFMA against the identity (id = identity_frag()) leaves T^T I in
+// the accumulator layout: lane (g, n) then holds T[n][4 g + j], four
+// consecutive elements of row n, written with one 8-byte store.  Every
+// product is a bf16 value times one or zero, so the stored values are exact
+// copies of the fragment's.  The matrix cores do the lane exchange that would
+// otherwise take a dozen VALU instructions per tile.
+__device__ __forceinline__ void store_tile16_frag(bf16_t* dst, bf16x4 x, bf16x4 id, int g, int n) {
+  f32x4 t = zero4();
+  mma16(t, x, id);
+  gstore_b64(dst + 16 * n + 4 * g, __builtin_bit_cast(u32x2, cvt_frag<bf16_t>(t)));
 }
 
 // ------------------------------------------------ direct global -> LDS copies
@@ -435,6 +477,23 @@ __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
+// Wait with a count known only at run time (wave-uniform n; counts above 63
+// wait for 63, which is stricter).  A chain of scalar branches selects the
+// immediate.
+template <int LO, int HI>
+__device__ __forceinline__ void wait_vmcnt_rt(int n) {
+  if constexpr (LO == HI) {
+    wait_vmcnt<LO>();
+  } else {
+    constexpr int MID = (LO + HI) / 2;
+    if (n <= MID)
+      wait_vmcnt_rt<LO, MID>(n);
+    else
+      wait_vmcnt_rt<MID + 1, HI>(n);
+  }
+}
+__device__ __forceinline__ void wait_vmcnt_rt(int n) { wait_vmcnt_rt<0, 63>(n < 63 ? n : 63); }
+
 // Copies issued per wave when the 64-lane blocks of an NB-block copy are
 // dealt round-robin to NW waves: the wave with the fewest (the last one).
 template <int NB, int NW>

@@ -317,7 +317,6 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
 // ---------------------------------------------------------------- forward
 template <typename T, int KD, int C, int E, int NW>
 struct FwdSmem {
-  static constexpr int CP = C + 4;  // padded row length of the V^T tile
   static constexpr int NT = C / 16;
   static constexpr int E4 = (E + 3) & ~3;
   static constexpr int EC = 16 / (int)sizeof(T);
@@ -331,7 +330,10 @@ struct FwdSmem {
   SwzTile<T, KD, C> Kt;
   SwzTile<T, C, C> Tu, M;
   SwzTile<T, SPLIT ? C : 1, SPLIT ? C : EC> TuL, ML;
-  alignas(16) T Vt[16][CP];
+  // V tile rows, permuted within each 16-row block: position 16 b + 4 j + i
+  // holds row 16 b + 4 i + j, so that the four rows 4 i + j (i = 0..3) a
+  // lane group reads together are adjacent (no bank conflicts)
+  alignas(16) T Vr[C][16];
   alignas(16) float coef01[2][E][C];  // a_e, b_e
   alignas(16) float coef2[E][C];      // c_e
   alignas(16) float gC[E4];
@@ -442,71 +444,34 @@ struct FwdDma {
     op_tile(sm.Kt, ops + OT::Kt);
     copy<NCO2>(&sm.coef2[0][0], p.coef + ch * 3 * E * C + 2 * E * C);
   }
-};
 
-// Register staging of the small per-chunk inputs (the V tile, gamma^C, beta),
-// loaded one chunk ahead and written to shared memory at the top of the
-// chunk step (V transposed).  Loads are unconditional (clamped indices) and
-// store() zeroes what is past T.
-template <typename T, int C, int E, int NTHR>
-struct FwdVStage {
-  static constexpr int NV4 = (C * 4 + NTHR - 1) / NTHR;  // 4-element pieces of the V tile
-  static constexpr int E4 = (E + 3) & ~3;
-  uint32_t v[NV4][sizeof(T) == 2 ? 2 : 4];  // 4 elements as raw words
-  float gc, beta;
-
-  __device__ __forceinline__ void load(const Shape& s, const FwdIn& in, const PrepBufs& p,
-                                       const T* Vg, int b, int h, int ci) {
-    const int tid = threadIdx.x;
-    const int w0 = 64 * wave_id();
-    const int t0 = ci * C;
-    const size_t ch = (size_t)(b * s.H + h) * s.Nc + ci;
-    const size_t vrs = (size_t)s.H * s.V;
-#pragma unroll
-    for (int i = 0; i < NV4; ++i) {
-      if (w0 + i * NTHR >= C * 4) continue;
-      const int idx = min(tid + i * NTHR, C * 4 - 1);
-      const int r = idx >> 2, c4 = idx & 3;
-      const int t = min(t0 + r, s.T - 1);
-      if constexpr (sizeof(T) == 2) {
-        const uint2 x = *(const uint2*)(Vg + (size_t)t * vrs + 4 * c4);
-        v[i][0] = x.x;
-        v[i][1] = x.y;
-      } else {
-        const uint4 x = *(const uint4*)(Vg + (size_t)t * vrs + 4 * c4);
-        v[i][0] = x.x;
-        v[i][1] = x.y;
-        v[i][2] = x.z;
-        v[i][3] = x.w;
-      }
-    }
-    gc = p.gC[ch * E4 + min(tid, E4 - 1)];
-    const int tb = min(t0 + min(tid, C - 1), s.T - 1);
-    beta = in.beta ? in.beta[((size_t)b * s.T + tb) * s.H + h] : 1.f;
+  // The copies below are exactly one instruction per wave, so that every
+  // wave's vmcnt waits can count them.
+  // gamma^C of the chunk (every wave copies the same E4 values)
+  static __device__ __forceinline__ void gc(Sm& sm, const PrepBufs& p, size_t ch) {
+    if (lane_id() < Sm::E4) lds_dma<4>(p.gC + ch * Sm::E4, 4 * lane_id(), lds_addr(&sm.gC[0]));
   }
-
-  template <typename Sm>
-  __device__ __forceinline__ void store(Sm& sm, int t0, int nT) const {
-    const int tid = threadIdx.x;
-#pragma unroll
-    for (int i = 0; i < NV4; ++i) {
-      const int idx = tid + i * NTHR;
-      const int r = idx >> 2, c4 = idx & 3;
-      if (idx < C * 4) {
-        const bool ok = t0 + r < nT;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          T x;
-          if constexpr (sizeof(T) == 2)
-            x = (T)((j & 1) ? (v[i][j >> 1] >> 16) : (v[i][j >> 1] & 0xffffu));
-          else
-            x = __uint_as_float(v[i][j]);
-          sm.Vt[4 * c4 + j][r] = ok ? x : T(0);
-        }
-      }
-    }
-    if (tid < E4) sm.gC[tid] = gc;
-    if (tid < C) sm.beta[tid] = (t0 + tid < nT) ? beta : 0.f;
+  // The V tile (rows t0 .. t0 + C - 1, the workgroup's 16 columns) in the
+  // permuted row order of Sm::Vr; wave w copies 16-byte pieces
+  // [w VL, (w + 1) VL) of the tile.  Rows past T read row T - 1 (zeroed after
+  // arrival in the last chunk).  Vg points at the columns' start in row t0.
+  static constexpr int PPR = 16 * (int)sizeof(T) / 16;  // 16-byte pieces per row
+  static constexpr int VL = C * PPR / NW;                // lanes per wave
+  static_assert(C * PPR % NW == 0 && VL <= 64, "V tile split over the waves");
+  static __device__ __forceinline__ void v(Sm& sm, const T* Vg, size_t vrs, int last) {
+    const int w = wave_id(), l = lane_id();
+    const int q = w * VL + l, pos = q / PPR, part = q % PPR;
+    const int r = (pos & ~15) + 4 * (pos & 3) + ((pos >> 2) & 3);  // row held at position pos
+    const uint32_t off = (uint32_t)(sizeof(T) * (size_t)min(r, last) * vrs) + 16 * part;
+    if (l < VL) lds_dma<16>(Vg, off, lds_addr(&sm.Vr[0][0]) + 16 * w * VL);
+  }
+  // beta of the chunk's rows (sGLA with beta), rows past T read row T - 1;
+  // bg points at the beta of row t0 (row stride H)
+  static constexpr int BL = C / NW;
+  static __device__ __forceinline__ void beta(Sm& sm, const float* bg, int H, int last) {
+    const int w = wave_id(), l = lane_id();
+    const uint32_t off = (uint32_t)(4 * (size_t)min(w * BL + l, last) * H);
+    if (l < BL) lds_dma<4>(bg, off, lds_addr(&sm.beta[0]) + 4 * w * BL);
   }
 };
 
@@ -562,31 +527,50 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
   const size_t krs = (size_t)s.H * KD;  // row stride between positions
   const size_t ch0 = (size_t)head * s.Nc;
 
-  FwdVStage<T, C, E, NTHR> vst;
+  const bf16x4 idf = identity_frag();  // for the transposing checkpoint stores
+  const size_t vrs = (size_t)s.H * V;
+  const bool sbeta = s.variant == 0 && in.beta != nullptr;  // beta copied per chunk
+  const float* bg = in.beta ? in.beta + (size_t)b * s.T * s.H + h : nullptr;
+  if (s.variant == 0 && !in.beta)
+    for (int r = threadIdx.x; r < C; r += NTHR) sm.beta[r] = 1.f;
   if (s.Nc > 0) {
     Dma::kq(sm, s, p, Kg, Qg, ch0, 0);
-    vst.load(s, in, p, Vg, b, h, 0);
+    Dma::v(sm, Vg, vrs, s.T - 1);
+    if (sbeta) Dma::beta(sm, bg, s.H, s.T - 1);
     Dma::tu(sm, p, ch0);
     Dma::m(sm, p, ch0);
   }
+  // Vector memory operations this wave issues after the gamma^C copy and
+  // before the wait that precedes the state update (all of them exactly
+  // counted): checkpoint tile stores, the next chunk's K, Q rows and a_e,
+  // b_e, the X and U stores, the next chunk's Tu, V tile and beta.  The wait
+  // then covers the K^T, c_e and gamma^C copies without waiting for the
+  // stores.  (A compiler-issued load among them would only make it stricter.)
+  const int owned = RAGGED ? max(0, min(SPW, E - w * SPW)) : SPW;
+  const int n_st = (train ? owned * KT : 0) + ((train && w < NT) ? (s.variant == 1 ? 8 : 4) : 0);
+  const int n_more = n_st + Dma::N_KQ + Dma::N_TU + 1 + (sbeta ? 1 : 0);
 
   for (int ci = 0; ci < s.Nc; ++ci) {
     const int t0 = ci * C;
     const size_t ch = ch0 + ci;
     const bool more = ci + 1 < s.Nc;
-    __syncthreads();  // the previous chunk is done with K^T and c_e
+    __syncthreads();  // the previous chunk is done with K^T, c_e and gamma^C
 
-    // (the V tile first: the compiler's wait for its loads then covers only
-    // copies that were issued before it)
-    vst.store(sm, ci * C, s.T);
     Dma::kt(sm, p, ch);
-    // the K, Q rows, a_e, b_e, Tu and M of this chunk have landed (only the
-    // K^T copies just issued may still be in flight)
-    wait_vmcnt<Dma::N_KT>();
+    Dma::gc(sm, p, ch);
+    // the K, Q rows, a_e, b_e, Tu, M, V tile and beta of this chunk have
+    // landed (only the K^T, c_e and gamma^C copies just issued may still be
+    // in flight)
+    wait_vmcnt<Dma::N_KT + 1>();
     if (t0 + C > s.T) {  // every wave's copies must have landed before the zeroing
       __syncthreads();
       zero_rows_from(sm.K, s.T - t0, NTHR);
       if constexpr (Sm::STAGE_Q) zero_rows_from(sm.Q, s.T - t0, NTHR);
+      for (int pos = threadIdx.x; pos < C; pos += NTHR) {
+        const int r = (pos & ~15) + 4 * (pos & 3) + ((pos >> 2) & 3);
+        if (t0 + r >= s.T)
+          for (int c = 0; c < 16; ++c) sm.Vr[pos][c] = T(0);
+      }
     }
     __syncthreads();
 
@@ -604,7 +588,12 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
         if (RAGGED && e >= E) continue;
         T* dst = (T*)sv.Sck + ((ch * E + e) * (size_t)(V / 16) + vt) * KD * 16;
 #pragma unroll
-        for (int kt = 0; kt < KT; ++kt) store_tile16(dst + 256 * kt, S[i][kt], g, n);
+        for (int kt = 0; kt < KT; ++kt) {
+          if constexpr (sizeof(T) == 2)
+            store_tile16_frag(dst + 256 * kt, Sop[i][kt], idf, g, n);
+          else
+            store_tile16(dst + 256 * kt, S[i][kt], g, n);
+        }
       }
     }
 
@@ -734,70 +723,92 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
     __syncthreads();
     // K, Q rows and a_e, b_e are free: the next chunk's are copied while this
     // chunk computes
-    if (more) {
-      Dma::kq(sm, s, p, Kg, Qg, ch + 1, t0 + C);
-      vst.load(s, in, p, Vg, b, h, ci + 1);
-    }
+    if (more) Dma::kq(sm, s, p, Kg, Qg, ch + 1, t0 + C);
 
     // ---- U = Tu (V - W) (GDN) or diag(beta) V (sGLA): wave w < NT forms row
-    // tile w (Tu is lower triangular: blocks kb <= w only) and the tiles are
-    // exchanged through LDS
+    // tile w and the tiles are exchanged through LDS.  Every block kb of the
+    // row is formed, also those right of the diagonal (Tu is zero there, so
+    // they add exact zeros): no branch separates the shared-memory reads, so
+    // they are all in flight before the first one is used.
+    // rows 16 kb + 4 g + j of the lane's value column, j = 0..3
+    auto vrows = [&](int kb) {
+      f32x4 x;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) x[j] = Elem<T>::to_f(sm.Vr[16 * kb + 4 * j + g][n]);
+      return x;
+    };
     if (w < NT) {
       const int rt = w;
       f32x4 u;
       if (s.variant == 1) {
-        F Xh[NT], Xl[NT];
+        const int r = 16 * rt + n;
+        f32x4 xr[NT], wq[NW][NT];
+        F th[NT], tl[NT];
+        T vr[NT][4];  // raw V elements (converted after the reads are issued)
 #pragma unroll
         for (int kb = 0; kb < NT; ++kb) {
-          if (kb > rt) {
-            Xh[kb] = Xl[kb] = cvt_frag<T>(zero4());
-            continue;
-          }
-          f32x4 x = ld4_f(&sm.Vt[n][16 * kb + 4 * g]);
 #pragma unroll
-          for (int ww = 0; ww < NW; ++ww) x -= sm.W[ww][kb][l];
-          split_frag(x, Xh[kb], Xl[kb]);
-          if (train && kb == rt) {
-            float* dst = sv.X + ch * C * (size_t)V + (size_t)(16 * rt + 4 * g) * V + v0 + n;
+          for (int j = 0; j < 4; ++j) vr[kb][j] = sm.Vr[16 * kb + 4 * j + g][n];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) dst[(size_t)j * V] = x[j];
-          }
+          for (int ww = 0; ww < NW; ++ww) wq[ww][kb] = sm.W[ww][kb][l];
+          th[kb] = ld_frag(sm.Tu.at(r, 16 * kb + 4 * g));
+          if constexpr (Sm::SPLIT) tl[kb] = ld_frag(sm.TuL.at(r, 16 * kb + 4 * g));
+        }
+        // (keeps the reads above together: the scheduler would otherwise
+        // interleave each with its use and wait for every one in turn)
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int kb = 0; kb < NT; ++kb) {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) xr[kb][j] = Elem<T>::to_f(vr[kb][j]);
+#pragma unroll
+          for (int ww = 0; ww < NW; ++ww) xr[kb] -= wq[ww][kb];
+        }
+        F Xh[NT], Xl[NT];
+        f32x4 xd = xr[0];  // the diagonal block, saved for the backward
+#pragma unroll
+        for (int kb = 0; kb < NT; ++kb) {
+          split_frag(xr[kb], Xh[kb], Xl[kb]);
+          if (kb > 0 && kb == rt) xd = xr[kb];
+        }
+        if (train) {
+          float* dst = sv.X + ch * C * (size_t)V + (size_t)(16 * rt + 4 * g) * V + v0 + n;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) gstore_b32(dst + (size_t)j * V, __float_as_uint(xd[j]));
         }
         u = zero4();
-        const int r = 16 * rt + n;
 #pragma unroll
         for (int kb = 0; kb < NT; kb += (NT > 1 ? 2 : 1)) {
-          if (kb > rt) continue;
           if constexpr (NT > 1) {
-            const F h0 = ld_frag(sm.Tu.at(r, 16 * kb + 4 * g));
-            const F h1 = ld_frag(sm.Tu.at(r, 16 * kb + 16 + 4 * g));
-            mma32(u, h0, h1, Xh[kb], Xh[kb + 1]);
+            mma32(u, th[kb], th[kb + 1], Xh[kb], Xh[kb + 1]);
             if constexpr (Sm::SPLIT) {
-              mma32(u, h0, h1, Xl[kb], Xl[kb + 1]);
-              mma32(u, ld_frag(sm.TuL.at(r, 16 * kb + 4 * g)),
-                    ld_frag(sm.TuL.at(r, 16 * kb + 16 + 4 * g)), Xh[kb], Xh[kb + 1]);
+              mma32(u, th[kb], th[kb + 1], Xl[kb], Xl[kb + 1]);
+              mma32(u, tl[kb], tl[kb + 1], Xh[kb], Xh[kb + 1]);
             }
           } else {
-            const F hh = ld_frag(sm.Tu.at(n, 4 * g));
-            mma16(u, hh, Xh[0]);
+            mma16(u, th[0], Xh[0]);
             if constexpr (Sm::SPLIT) {
-              mma16(u, hh, Xl[0]);
-              mma16(u, ld_frag(sm.TuL.at(n, 4 * g)), Xh[0]);
+              mma16(u, th[0], Xl[0]);
+              mma16(u, tl[0], Xh[0]);
             }
           }
         }
       } else {
-        u = ld4_f(&sm.Vt[n][16 * rt + 4 * g]) * *(const f32x4*)&sm.beta[16 * rt + 4 * g];
+        u = vrows(rt) * *(const f32x4*)&sm.beta[16 * rt + 4 * g];
       }
       sm.Us[rt][l] = u;
       if (train) {
         float* dst = sv.U + ch * C * (size_t)V + (size_t)(16 * rt + 4 * g) * V + v0 + n;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) dst[(size_t)j * V] = u[j];
+        for (int j = 0; j < 4; ++j) gstore_b32(dst + (size_t)j * V, __float_as_uint(u[j]));
       }
     }
     __syncthreads();
-    if (more) Dma::tu(sm, p, ch + 1);  // Tu is free
+    if (more) {  // Tu, the V tile and beta are free
+      Dma::tu(sm, p, ch + 1);
+      Dma::v(sm, Vg + (size_t)(t0 + C) * vrs, vrs, s.T - 1 - (t0 + C));
+      if (sbeta) Dma::beta(sm, bg + (size_t)(t0 + C) * s.H, s.H, s.T - 1 - (t0 + C));
+    }
     f32x4 U[NT];
     F Uh[NT], Ul[NT];
 #pragma unroll
@@ -810,23 +821,28 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
     f32x4 oacc = zero4();
     if (w < NT) {
       const int rt = w;
-#pragma unroll
-      for (int ww = 0; ww < NW; ++ww) oacc += sm.O[ww][rt][l];
       const int r = 16 * rt + n;
-      auto mh = [&](int kb) { return ld_frag(sm.M.at(r, 16 * kb + 4 * g)); };
-      mma_k<C>(oacc, mh, [&](int kb) { return Uh[kb]; });
+      F mf[NT], ml[NT];  // all fragment reads first
+#pragma unroll
+      for (int kb = 0; kb < NT; ++kb) {
+        mf[kb] = ld_frag(sm.M.at(r, 16 * kb + 4 * g));
+        if constexpr (Sm::SPLIT) ml[kb] = ld_frag(sm.ML.at(r, 16 * kb + 4 * g));
+      }
+      f32x4 op[NW];
+#pragma unroll
+      for (int ww = 0; ww < NW; ++ww) op[ww] = sm.O[ww][rt][l];
+      __builtin_amdgcn_sched_barrier(0);  // the reads above stay together
+#pragma unroll
+      for (int ww = 0; ww < NW; ++ww) oacc += op[ww];
+      mma_k<C>(oacc, [&](int kb) { return mf[kb]; }, [&](int kb) { return Uh[kb]; });
       if constexpr (Sm::SPLIT) {
-        mma_k<C>(oacc, mh, [&](int kb) { return Ul[kb]; });
-        mma_k<C>(oacc, [&](int kb) { return ld_frag(sm.ML.at(r, 16 * kb + 4 * g)); },
-                 [&](int kb) { return Uh[kb]; });
+        mma_k<C>(oacc, [&](int kb) { return mf[kb]; }, [&](int kb) { return Ul[kb]; });
+        mma_k<C>(oacc, [&](int kb) { return ml[kb]; }, [&](int kb) { return Uh[kb]; });
       }
     }
-    // K^T and c_e of this chunk have landed (what was issued after them: the
-    // next chunk's rows and Tu); every wave is done with M after the barrier
-    if (more)
-      wait_vmcnt<Dma::N_KQ + Dma::N_TU>();
-    else
-      wait_vmcnt<0>();
+    // K^T, c_e and gamma^C of this chunk have landed (n_more / n_st count
+    // what was issued after them); every wave is done with M after the barrier
+    wait_vmcnt_rt(more ? n_more : n_st);
     __syncthreads();
     if (more) Dma::m(sm, p, ch + 1);
     if (w < NT) {
