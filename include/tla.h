@@ -97,7 +97,8 @@ size_t tla_workspace_bytes(const tla_desc* desc, int op);
  * the start of every chunk so the backward need not recompute it), the
  * delta-corrected values U and the residual V - W of every chunk, and the
  * per-chunk terms of Eq. joint-gram / joint-solve (coefficient vectors, M,
- * Tu), in an opaque layout.  0 if desc is invalid. */
+ * Tu, and for GDN the fp32 inverse (I + L)^{-1} that the backward of the
+ * solve reuses), in an opaque layout.  0 if desc is invalid. */
 size_t tla_saved_bytes(const tla_desc* desc);
 
 /*

@@ -95,7 +95,7 @@ size_t esize(const tla::Shape& s) { return s.in_bf16 ? 2 : 4; }
 // M, Tu) live in the forward workspace for inference; a training forward
 // writes them into `saved`, where the backward reads them again.
 struct Layout {
-  size_t p_coef, p_gC, p_ops, p_size;  // prep region, relative offsets
+  size_t p_coef, p_gC, p_ops, p_ninv, p_size;  // prep region, relative offsets
   size_t bwd_dS, bwd_dU, bwd_dW, bwd_dqs, bwd_dks, bwd_dcoef, bwd_dgC, bwd_end;
   size_t sv_S, sv_U, sv_X, sv_prep, sv_end;
 };
@@ -109,6 +109,7 @@ Layout layout(const tla::Shape& s) {
   L.p_coef = o; o += align256(nch * 3 * s.E * s.C * 4);
   L.p_gC = o;   o += align256(nch * E4 * 4);
   L.p_ops = o;  o += align256(nch * tla::op_tile_bytes(s.K, s.C, s.in_bf16));
+  L.p_ninv = o; o += s.variant == TLA_GDN ? align256(nch * s.C * s.C * 4) : 0;
   L.p_size = o;
   o = 0;
   L.bwd_dS = o;    o += align256(nch * s.E * s.K * s.V * es);
@@ -128,9 +129,11 @@ Layout layout(const tla::Shape& s) {
   return L;
 }
 
-tla::PrepBufs prep_bufs(const Layout& L, const void* base) {
+// `ninv`: whether the prep kernel also keeps (I + L)^{-1} for the backward
+tla::PrepBufs prep_bufs(const Layout& L, const void* base, bool ninv) {
   char* b = (char*)base;
-  return tla::PrepBufs{(float*)(b + L.p_coef), (float*)(b + L.p_gC), (void*)(b + L.p_ops)};
+  return tla::PrepBufs{(float*)(b + L.p_coef), (float*)(b + L.p_gC), (void*)(b + L.p_ops),
+                       (ninv && L.p_ninv < L.p_size) ? (float*)(b + L.p_ninv) : nullptr};
 }
 tla::SavedBufs saved_bufs(const Layout& L, const void* saved) {
   char* b = (char*)saved;
@@ -231,7 +234,7 @@ size_t tla_workspace_bytes(const tla_desc* d, int op) {
   tla::Shape s;
   if (check_desc(d, &s, false) != TLA_OK) return 0;
   const Layout L = layout(s);
-  if (op == TLA_OP_FWD) return L.p_size;
+  if (op == TLA_OP_FWD) return L.p_ninv;  // an inference forward keeps no inverse
   if (op == TLA_OP_BWD) return L.bwd_end;
   return 0;
 }
@@ -258,15 +261,15 @@ int tla_fwd(const tla_desc* d, const void* q, const void* k, const void* v, cons
     if (misaligned(p)) return fail(TLA_E_ALIGN, "pointer %p is not 16-byte aligned", p);
   const Layout L = layout(s);
   const bool use_ws = s.T > 0 && !saved;  // a training forward keeps its prep results in saved
-  if (use_ws && (!ws || ws_bytes < L.p_size))
-    return fail(TLA_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, L.p_size);
+  if (use_ws && (!ws || ws_bytes < L.p_ninv))
+    return fail(TLA_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, L.p_ninv);
   const size_t es = esize(s), os = s.out_bf16 ? 2 : 4;
   const size_t sbytes = (size_t)s.NH * s.E * s.K * s.V * 4;
   const Range ins[] = {{q, ntok * s.K * es}, {k, ntok * s.K * es}, {v, ntok * s.V * es},
                        {q2, ntok * s.E * es}, {k2, ntok * s.E * es}, {g, ntok * s.E * 4},
                        {beta, beta ? ntok * 4 : 0}, {s0, s0 ? sbytes : 0}};
   const Range outs[] = {{o, ntok * s.V * os}, {saved, saved ? L.sv_end : 0},
-                        {ws, use_ws ? L.p_size : 0}};
+                        {ws, use_ws ? L.p_ninv : 0}};
   for (const Range& a : outs)
     for (const Range& b : ins)
       if (overlap(a, b)) return fail(TLA_E_ALIAS, "an output or buffer overlaps an input");
@@ -286,7 +289,8 @@ int tla_fwd(const tla_desc* d, const void* q, const void* k, const void* v, cons
   hipStream_t st = (hipStream_t)stream;
   s.has_beta = beta != nullptr;
   tla::FwdIn in{q, k, v, q2, k2, g, beta, s0};
-  const tla::PrepBufs pb = saved ? prep_bufs(L, (char*)saved + L.sv_prep) : prep_bufs(L, ws);
+  const tla::PrepBufs pb =
+      saved ? prep_bufs(L, (char*)saved + L.sv_prep, true) : prep_bufs(L, ws, false);
   hipError_t e;
   if (s.T > 0) {
     e = timed(PROF_PREP, st, [&] { return tla::launch_prep(s, in, pb, st); });
@@ -348,7 +352,7 @@ int tla_bwd(const tla_desc* d, const void* q, const void* k, const void* v, cons
   hipStream_t st = (hipStream_t)stream;
   s.has_beta = beta != nullptr;
   tla::FwdIn in{q, k, v, q2, k2, g, beta, s0};
-  const tla::PrepBufs pb = prep_bufs(L, (const char*)saved + L.sv_prep);  // from the forward
+  const tla::PrepBufs pb = prep_bufs(L, (const char*)saved + L.sv_prep, true);  // from the forward
   char* wb = (char*)ws;
   const tla::BwdBufs bb{wb + L.bwd_dS, (float*)(wb + L.bwd_dU), (float*)(wb + L.bwd_dW),
                         (float*)(wb + L.bwd_dqs), (float*)(wb + L.bwd_dks),
@@ -360,7 +364,7 @@ int tla_bwd(const tla_desc* d, const void* q, const void* k, const void* v, cons
   e = timed(PROF_BWD_STATE, st, [&] { return tla::launch_bwd_state(s, in, dO, pb, sv, bb, st); });
   if (e != hipSuccess) return device_fail(e, "backward state-gradient kernel");
   e = timed(PROF_BWD_CHUNK, st, [&] {
-    return tla::launch_bwd_chunk(s, in, dO, sv, bb, dq, dk, dv, dq2, dk2, dg, dbeta, st);
+    return tla::launch_bwd_chunk(s, in, dO, pb, sv, bb, dq, dk, dv, dq2, dk2, dg, dbeta, st);
   });
   if (e != hipSuccess) return device_fail(e, "backward chunk kernel");
   return TLA_OK;

@@ -31,6 +31,8 @@
 //     coefficient vectors: dk2 += da o gamma + dc o gamma^C/gamma;  dq2 += db o gamma
 //          dG += da o a + db o b - dc o c;  dG_C += sum_r dc c + gamma^C dgamma^C
 //     dg_j = sum_{r >= j in the chunk} dG_r   (G is the in-chunk cumulative log-gate)
+#include <type_traits>
+
 #include "tla_common.hpp"
 #include "tla_internal.hpp"
 
@@ -437,73 +439,84 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
       if (ci > 0) stage.load(s, p, Kg, Qg, dOg, ch - 1, ci - 1, 2);
     // ---- dS_e <- gamma^C_e dS'_e + Q^T diag(b_e) dO + K^T diag(a_e) dW
     // (B operands of a group of owned slices first; each Q^T / K^T fragment is
-    // read once per group; four-wave instances take all owned slices at once)
+    // read once per group, one key tile ahead of its MFMAs; four-wave
+    // instances take all owned slices at once).  The variant is a constant
+    // inside: no branch splits the loop.
     constexpr int GS = PREFETCH ? SPW : 1;
-    const bool gdn = s.variant == 1;
+    auto update = [&](auto gdn_c) {
+      constexpr bool GDN = decltype(gdn_c)::value;
 #pragma unroll
-    for (int i0 = 0; i0 < SPW; i0 += GS) {
-      F bh[GS][NT], bl[GS][NT], ah[GS][NT], al[GS][NT];
-      float gcs[GS];
+      for (int i0 = 0; i0 < SPW; i0 += GS) {
+        F bh[GS][NT], bl[GS][NT], ah[GS][NT], al[GS][NT];
+        float gcs[GS];
 #pragma unroll
-      for (int ii = 0; ii < GS; ++ii) {
-        const int e = w * SPW + i0 + ii;
-        if (RAGGED && e >= E) continue;
-        gcs[ii] = sm.gC[e];
+        for (int ii = 0; ii < GS; ++ii) {
+          const int e = w * SPW + i0 + ii;
+          if (RAGGED && e >= E) continue;
+          gcs[ii] = sm.gC[e];
 #pragma unroll
-        for (int kb = 0; kb < NT; ++kb) {
-          const f32x4 dov = ld4_f(&sm.dOt[n][16 * kb + 4 * g]);
-          split_frag(dov * *(const f32x4*)&sm.coef[1][e][16 * kb + 4 * g], bh[ii][kb], bl[ii][kb]);
-          split_frag(dW[kb] * *(const f32x4*)&sm.coef[0][e][16 * kb + 4 * g], ah[ii][kb],
-                     al[ii][kb]);
-        }
-      }
-#pragma unroll
-      for (int kt = 0; kt < KT; ++kt) {
-        const int r = 16 * kt + n;
-        f32x4 acc[GS];
-#pragma unroll
-        for (int ii = 0; ii < GS; ++ii) acc[ii] = dS[i0 + ii][kt] * gcs[ii];
-#pragma unroll
-        for (int kb = 0; kb + 1 < NT; kb += 2) {
-          const F q0 = ld_frag(&sm.Qt[r][16 * kb + 4 * g]);
-          const F q1 = ld_frag(&sm.Qt[r][16 * kb + 16 + 4 * g]);
-          F k0, k1;
-          if (gdn) {
-            k0 = ld_frag(&sm.Kt[r][16 * kb + 4 * g]);
-            k1 = ld_frag(&sm.Kt[r][16 * kb + 16 + 4 * g]);
+          for (int kb = 0; kb < NT; ++kb) {
+            const f32x4 dov = ld4_f(&sm.dOt[n][16 * kb + 4 * g]);
+            split_frag(dov * *(const f32x4*)&sm.coef[1][e][16 * kb + 4 * g], bh[ii][kb], bl[ii][kb]);
+            if constexpr (GDN)
+              split_frag(dW[kb] * *(const f32x4*)&sm.coef[0][e][16 * kb + 4 * g], ah[ii][kb],
+                         al[ii][kb]);
           }
+        }
+        F qf[2][NT], kf[2][NT];
+        auto load_kt = [&](int kt, F(&q)[NT], F(&k)[NT]) {
+          const int r = 16 * kt + n;
 #pragma unroll
-          for (int ii = 0; ii < GS; ++ii) {
-            if (RAGGED && w * SPW + i0 + ii >= E) continue;
-            mma32(acc[ii], q0, q1, bh[ii][kb], bh[ii][kb + 1]);
-            if constexpr (Sm::SPLIT) mma32(acc[ii], q0, q1, bl[ii][kb], bl[ii][kb + 1]);
-            if (gdn) {
-              mma32(acc[ii], k0, k1, ah[ii][kb], ah[ii][kb + 1]);
-              if constexpr (Sm::SPLIT) mma32(acc[ii], k0, k1, al[ii][kb], al[ii][kb + 1]);
+          for (int kb = 0; kb < NT; ++kb) {
+            q[kb] = ld_frag(&sm.Qt[r][16 * kb + 4 * g]);
+            if constexpr (GDN) k[kb] = ld_frag(&sm.Kt[r][16 * kb + 4 * g]);
+          }
+        };
+        load_kt(0, qf[0], kf[0]);
+#pragma unroll
+        for (int kt = 0; kt < KT; ++kt) {
+          if (kt + 1 < KT) load_kt(kt + 1, qf[(kt + 1) & 1], kf[(kt + 1) & 1]);
+          const F* q = qf[kt & 1];
+          const F* k = kf[kt & 1];
+          f32x4 acc[GS];
+#pragma unroll
+          for (int ii = 0; ii < GS; ++ii) acc[ii] = dS[i0 + ii][kt] * gcs[ii];
+#pragma unroll
+          for (int kb = 0; kb + 1 < NT; kb += 2) {
+#pragma unroll
+            for (int ii = 0; ii < GS; ++ii) {
+              if (RAGGED && w * SPW + i0 + ii >= E) continue;
+              mma32(acc[ii], q[kb], q[kb + 1], bh[ii][kb], bh[ii][kb + 1]);
+              if constexpr (Sm::SPLIT) mma32(acc[ii], q[kb], q[kb + 1], bl[ii][kb], bl[ii][kb + 1]);
+              if constexpr (GDN) {
+                mma32(acc[ii], k[kb], k[kb + 1], ah[ii][kb], ah[ii][kb + 1]);
+                if constexpr (Sm::SPLIT) mma32(acc[ii], k[kb], k[kb + 1], al[ii][kb], al[ii][kb + 1]);
+              }
             }
           }
-        }
-        if constexpr (NT & 1) {
-          const int kb = NT - 1;
-          const F q0 = ld_frag(&sm.Qt[r][16 * kb + 4 * g]);
-          F k0;
-          if (gdn) k0 = ld_frag(&sm.Kt[r][16 * kb + 4 * g]);
+          if constexpr (NT & 1) {
+            const int kb = NT - 1;
 #pragma unroll
-          for (int ii = 0; ii < GS; ++ii) {
-            if (RAGGED && w * SPW + i0 + ii >= E) continue;
-            mma16(acc[ii], q0, bh[ii][kb]);
-            if constexpr (Sm::SPLIT) mma16(acc[ii], q0, bl[ii][kb]);
-            if (gdn) {
-              mma16(acc[ii], k0, ah[ii][kb]);
-              if constexpr (Sm::SPLIT) mma16(acc[ii], k0, al[ii][kb]);
+            for (int ii = 0; ii < GS; ++ii) {
+              if (RAGGED && w * SPW + i0 + ii >= E) continue;
+              mma16(acc[ii], q[kb], bh[ii][kb]);
+              if constexpr (Sm::SPLIT) mma16(acc[ii], q[kb], bl[ii][kb]);
+              if constexpr (GDN) {
+                mma16(acc[ii], k[kb], ah[ii][kb]);
+                if constexpr (Sm::SPLIT) mma16(acc[ii], k[kb], al[ii][kb]);
+              }
             }
           }
-        }
 #pragma unroll
-        for (int ii = 0; ii < GS; ++ii)
-          if (!RAGGED || w * SPW + i0 + ii < E) dS[i0 + ii][kt] = acc[ii];
+          for (int ii = 0; ii < GS; ++ii)
+            if (!RAGGED || w * SPW + i0 + ii < E) dS[i0 + ii][kt] = acc[ii];
+        }
       }
-    }
+    };
+    if (s.variant == 1)
+      update(std::integral_constant<bool, true>{});
+    else
+      update(std::integral_constant<bool, false>{});
   }
 
   if (ds0) {
@@ -961,7 +974,7 @@ constexpr int CHUNK_NTHR = CHUNK_NW * 64;
 
 template <typename T, int KD, int C, int E>
 __global__ __launch_bounds__(CHUNK_NTHR) void k_bwd_chunk(Shape s, FwdIn in, const void* dOv,
-                                                   SavedBufs sv, BwdBufs bb, void* dqv, void* dkv,
+                                                   PrepBufs p, SavedBufs sv, BwdBufs bb, void* dqv, void* dkv,
                                                    void* dvv, void* dq2v, void* dk2v, float* dg,
                                                    float* dbeta) {
   constexpr int NT = C / 16;
@@ -1030,6 +1043,16 @@ __global__ __launch_bounds__(CHUNK_NTHR) void k_bwd_chunk(Shape s, FwdIn in, con
       const int r = idx / (KD / 8), c8 = idx % (KD / 8);
       *(Raw8<T>*)&sm.u1.qk.sQ[r][8 * c8] = qv[it];
       *(Raw8<T>*)&sm.u1.qk.sK[r][8 * c8] = kv[it];
+    }
+  }
+  // (I + L)^{-1} as the forward's prep kernel formed it (GDN): into its LDS
+  // region, which stays free until the solve backward
+  const bool have_ninv = gdn && p.ninv != nullptr;
+  if (have_ninv) {
+    const float* src = p.ninv + (size_t)ch * C * C;
+    for (int idx = tid; idx < C * C / 4; idx += NTHR) {
+      const int r = idx / (C / 4), c4 = idx % (C / 4);
+      *(f32x4*)&sm.u2.r.X1[r][4 * c4] = *(const f32x4*)(src + r * C + 4 * c4);
     }
   }
   // G = inclusive cumulative sum of g over the chunk, in fp64: one wave per
@@ -1113,29 +1136,33 @@ __global__ __launch_bounds__(CHUNK_NTHR) void k_bwd_chunk(Shape s, FwdIn in, con
         mma8(ak, krow8(ra, col), kb);
       }
     }
-    // decayed Grams of the lane's four (r, c) pairs
-    float rq[4], rk[4];
-    {
+    // decayed Grams of the lane's four (r, c) pairs (formed for every pair of
+    // a lower tile and masked afterwards: no per-lane branch around the
+    // shared-memory reads, which are whole-row vector reads)
+    float rq[4] = {0.f, 0.f, 0.f, 0.f}, rk[4] = {0.f, 0.f, 0.f, 0.f};
+    if (lower) {
       const int c = 16 * st + n;
       double Gc[E];
       float k2c[E];
-#pragma unroll
-      for (int e = 0; e < E; ++e) {
-        Gc[e] = sm.G[c][e];
-        k2c[e] = sm.k2[c][e];
-      }
+      lds_row<E>(Gc, &sm.G[c][0]);
+      lds_row<E>(k2c, &sm.k2[c][0]);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int r = 16 * rt + 4 * g + j;
-        rq[j] = rk[j] = 0.f;
-        if (lower && c <= r) {
+        double Gr[E];
+        float q2r[E], k2r[E];
+        lds_row<E>(Gr, &sm.G[r][0]);
+        lds_row<E>(q2r, &sm.q2[r][0]);
+        lds_row<E>(k2r, &sm.k2[r][0]);
+        float aq = 0.f, ak = 0.f;
 #pragma unroll
-          for (int e = 0; e < E; ++e) {
-            const float d = exp_nonpos((float)(sm.G[r][e] - Gc[e])) * k2c[e];
-            rq[j] += sm.q2[r][e] * d;
-            rk[j] += sm.k2[r][e] * d;
-          }
+        for (int e = 0; e < E; ++e) {
+          const float d = exp_nonpos((float)(Gr[e] - Gc[e])) * k2c[e];
+          aq += q2r[e] * d;
+          ak += k2r[e] * d;
         }
+        rq[j] = (c <= r) ? aq : 0.f;
+        rk[j] = (c <= r) ? ak : 0.f;
       }
     }
     if (lower) {
@@ -1169,10 +1196,12 @@ __global__ __launch_bounds__(CHUNK_NTHR) void k_bwd_chunk(Shape s, FwdIn in, con
   __syncthreads();
 
   if (gdn) {
-    // ---- (I + L)^{-1} with L = diag(beta)(A_kk o R), strictly lower
-    unit_lower_inverse<C, NTHR>(
-        [&](int r, int c) { return sm.beta[r] * sm.Akk[r][c] * sm.u2.r.R[r][c]; },
-        &sm.u2.r.X1[0][0], Sm::CP, &sm.Y[0][0][0]);
+    // ---- (I + L)^{-1} with L = diag(beta)(A_kk o R), strictly lower: the
+    // forward's, staged in phase 0 (formed here only without it)
+    if (!have_ninv)
+      unit_lower_inverse<C, NTHR>(
+          [&](int r, int c) { return sm.beta[r] * sm.Akk[r][c] * sm.u2.r.R[r][c]; },
+          &sm.u2.r.X1[0][0], Sm::CP, &sm.Y[0][0][0]);
     // ---- P = N^{-T} dTu on MFMA (fp32 operands); N^{-T} is upper triangular
     f32x4 pt[(NT * NT + NW - 1) / NW];
 #pragma unroll
@@ -1351,15 +1380,28 @@ __global__ __launch_bounds__(CHUNK_NTHR) void k_bwd_chunk(Shape s, FwdIn in, con
   };
 
   // ---- dq = dq_s + dA_qk K;  dk = dk_s + dA_qk^T Q + (dA_kk + dA_kk^T) K
-  for (int tile = w; tile < NT * KT; tile += NW) {
+  // (the state-contraction partials dq_s, dk_s of all the wave's tiles are
+  // loaded first: one memory latency instead of one per tile)
+  constexpr int TPW = (NT * KT + NW - 1) / NW;  // tiles per wave
+  float pqa[TPW][4], pka[TPW][4];
+#pragma unroll
+  for (int i = 0; i < TPW; ++i) {
+    const int tile = min(w + NW * i, NT * KT - 1);
     const int rt = tile % NT, kt = tile / NT;
-    float pq[4], pk[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const size_t wo = (size_t)ch * C * KD + (size_t)(16 * rt + 4 * g + j) * KD + 16 * kt + n;
-      pq[j] = bb.dqs[wo];
-      pk[j] = bb.dks[wo];
+      pqa[i][j] = bb.dqs[wo];
+      pka[i][j] = bb.dks[wo];
     }
+  }
+#pragma unroll
+  for (int i = 0; i < TPW; ++i) {
+    const int tile = w + NW * i;
+    if (tile >= NT * KT) continue;  // wave-uniform
+    const int rt = tile % NT, kt = tile / NT;
+    const float* pq = pqa[i];
+    const float* pk = pka[i];
     f32x4 aq = zero4(), ak = zero4();
     const int r = 16 * rt + n;
 #pragma unroll
@@ -1435,8 +1477,11 @@ __global__ __launch_bounds__(CHUNK_NTHR) void k_bwd_chunk(Shape s, FwdIn in, con
     for (int ct = 0; ct < NT; ++ct) colacc[ct] = 0.f;
 #pragma unroll
     for (int rt = 0; rt < NT; ++rt) {
-      double Gr[4];
-      float q2r[4], k2r[4];
+      // every shared-memory read of this row tile first (no per-lane
+      // branch), then the arithmetic; pairs above the diagonal are masked by
+      // selects (their exponent is positive)
+      double Gr[4], Gc[NT];
+      float q2r[4], k2r[4], k2c[NT], aqv[NT][4], akv[NT][4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int r = 16 * rt + 4 * g + j;
@@ -1447,19 +1492,29 @@ __global__ __launch_bounds__(CHUNK_NTHR) void k_bwd_chunk(Shape s, FwdIn in, con
 #pragma unroll
       for (int ct = 0; ct <= rt; ++ct) {
         const int c = 16 * ct + n;
-        const double Gc = sm.G[c][e];
-        const float k2c = sm.k2[c][e];
+        Gc[ct] = sm.G[c][e];
+        k2c[ct] = sm.k2[c][e];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int r = 16 * rt + 4 * g + j;
-          if (c <= r) {
-            const float d = exp_nonpos((float)(Gr[j] - Gc));
-            const float drq = sm.Aqk[r][c] * d;
-            const float drk = (c < r) ? sm.Akk[r][c] * d : 0.f;
-            rowq[4 * rt + j] += drq * k2c;
-            rowk[4 * rt + j] += drk * k2c;
-            colacc[ct] += drq * q2r[j] + drk * k2r[j];
-          }
+          aqv[ct][j] = sm.Aqk[r][c];
+          akv[ct][j] = sm.Akk[r][c];
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int ct = 0; ct <= rt; ++ct) {
+        const int c = 16 * ct + n;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int r = 16 * rt + 4 * g + j;
+          const float ex = exp_nonpos((float)(Gr[j] - Gc[ct]));
+          const float d = (c <= r) ? ex : 0.f;
+          const float drq = aqv[ct][j] * d;
+          const float drk = (c < r) ? akv[ct][j] * d : 0.f;
+          rowq[4 * rt + j] += drq * k2c[ct];
+          rowk[4 * rt + j] += drk * k2c[ct];
+          colacc[ct] += drq * q2r[j] + drk * k2r[j];
         }
       }
     }
@@ -1557,7 +1612,8 @@ static hipError_t state_inst(const Shape& s, const FwdIn& in, const void* dO, co
 }
 
 template <typename T, int KD, int C, int E>
-static hipError_t chunk_inst(const Shape& s, const FwdIn& in, const void* dO, const SavedBufs& sv,
+static hipError_t chunk_inst(const Shape& s, const FwdIn& in, const void* dO, const PrepBufs& p,
+                             const SavedBufs& sv,
                              const BwdBufs& bb, void* dq, void* dk, void* dv, void* dq2, void* dk2,
                              float* dg, float* dbeta, hipStream_t st) {
   const size_t smem = sizeof(ChunkSmem<T, KD, C, E>);
@@ -1568,7 +1624,7 @@ static hipError_t chunk_inst(const Shape& s, const FwdIn& in, const void* dO, co
     attr = true;
   }
   hipLaunchKernelGGL((k_bwd_chunk<T, KD, C, E>), dim3(s.NH * s.Nc), dim3(CHUNK_NTHR), smem, st, s, in, dO,
-                     sv, bb, dq, dk, dv, dq2, dk2, dg, dbeta);
+                     p, sv, bb, dq, dk, dv, dq2, dk2, dg, dbeta);
   return hipGetLastError();
 }
 
@@ -1618,11 +1674,11 @@ hipError_t launch_bwd_state(const Shape& s, const FwdIn& in, const void* dO, con
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_bwd_chunk(const Shape& s, const FwdIn& in, const void* dO, const SavedBufs& sv,
-                            const BwdBufs& bb, void* dq, void* dk, void* dv, void* dq2, void* dk2,
-                            float* dg, float* dbeta, hipStream_t st) {
+hipError_t launch_bwd_chunk(const Shape& s, const FwdIn& in, const void* dO, const PrepBufs& p,
+                            const SavedBufs& sv, const BwdBufs& bb, void* dq, void* dk, void* dv,
+                            void* dq2, void* dk2, float* dg, float* dbeta, hipStream_t st) {
 #define CALL_CH(T_, KD_, C_, E_) \
-  chunk_inst<T_, KD_, C_, E_>(s, in, dO, sv, bb, dq, dk, dv, dq2, dk2, dg, dbeta, st)
+  chunk_inst<T_, KD_, C_, E_>(s, in, dO, p, sv, bb, dq, dk, dv, dq2, dk2, dg, dbeta, st)
   TLA_BWD_FOR_EACH(CALL_CH)
 #undef CALL_CH
   return hipErrorInvalidValue;

@@ -141,6 +141,26 @@ __device__ __forceinline__ typename Elem<T>::frag ld_frag_strided(const T* p, in
   return cvt_frag<T>(x);
 }
 
+// A row of N consecutive values from shared memory (16-byte aligned when N
+// fills whole 16-byte words) with the widest reads the length allows.
+template <int N, typename V>
+__device__ __forceinline__ void lds_row(V (&x)[N], const V* src) {
+  constexpr int PER = 16 / (int)sizeof(V);  // values per 16-byte read
+  if constexpr (N % PER == 0) {
+#pragma unroll
+    for (int i = 0; i < N / PER; ++i) {
+      const uint4 w = ((const uint4*)src)[i];
+      V t[PER];
+      __builtin_memcpy(t, &w, 16);
+#pragma unroll
+      for (int k = 0; k < PER; ++k) x[PER * i + k] = t[k];
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < N; ++i) x[i] = src[i];
+  }
+}
+
 // ------------------------------------------------------------------ MFMA
 __device__ __forceinline__ void mma16(f32x4& acc, f32x4 a, f32x4 b) {
   acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[0], b[0], acc, 0, 0, 0);

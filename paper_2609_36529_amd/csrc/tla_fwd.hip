@@ -289,6 +289,13 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
   if (s.variant == 1) {
     unit_lower_inverse<C, 256>([&](int r, int c) { return sm.L[r][c]; }, &sm.u.inv.X[0][0],
                                Sm::CP, &sm.u.inv.Y[0][0][0]);
+    if (p.ninv) {  // kept in fp32 for the backward of the solve
+      float* dst = p.ninv + (size_t)ch * C * C;
+      for (int idx = tid; idx < C * C / 4; idx += 256) {
+        const int r = idx / (C / 4), c4 = idx % (C / 4);
+        *(f32x4*)(dst + r * C + 4 * c4) = *(const f32x4*)&sm.u.inv.X[r][4 * c4];
+      }
+    }
     // Tu row-major and transposed, from 4 x 4 blocks of the inverse
     for (int idx = tid; idx < (C / 4) * (C / 4); idx += 256) {
       const int rb = idx / (C / 4), cb = idx % (C / 4);

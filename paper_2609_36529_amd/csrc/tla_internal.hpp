@@ -23,6 +23,7 @@ struct PrepBufs {
   float* coef;   // [ch][3][E][C]  a = k2*gamma, b = q2*gamma, c = k2*gamma^C/gamma
   float* gC;     // [ch][E4]       gamma^C (E4 = E rounded up to 4)
   void* ops;     // [ch][op_tile_elems] operand tiles, see OpTiles
+  float* ninv;   // [ch][C][C]     (I + L)^{-1} in fp32 (GDN training forward), or NULL
 };
 
 // Operand tiles of one chunk, in the operand type T and in the layouts the
@@ -78,7 +79,8 @@ hipError_t launch_bwd_rec(const Shape& s, const FwdIn& in, const void* dO, const
                           const PrepBufs& p, const BwdBufs& bb, float* ds0, hipStream_t st);
 hipError_t launch_bwd_state(const Shape& s, const FwdIn& in, const void* dO, const PrepBufs& p,
                             const SavedBufs& sv, const BwdBufs& bb, hipStream_t st);
-hipError_t launch_bwd_chunk(const Shape& s, const FwdIn& in, const void* dO, const SavedBufs& sv,
+hipError_t launch_bwd_chunk(const Shape& s, const FwdIn& in, const void* dO, const PrepBufs& p,
+                            const SavedBufs& sv,
                             const BwdBufs& bb, void* dq, void* dk, void* dv, void* dq2,
                             void* dk2, float* dg, float* dbeta, hipStream_t st);
 hipError_t launch_step(const Shape& s, const FwdIn& in, float* state, void* o, hipStream_t st);
