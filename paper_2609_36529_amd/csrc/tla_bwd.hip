@@ -78,7 +78,7 @@ template <int E> constexpr int bwd_waves() { return E >= 8 ? 8 : 4; }
 // ============================================================ reverse recurrence
 template <typename T, int KD, int C, int E, int NW>
 struct RecSmem {
-  static constexpr int KP = KD + 4;
+  static constexpr int KP = KD + 8;  // 16-byte rows: 32-deep A operands are one 16-byte read
   static constexpr int CP = C + 4;
   static constexpr int NT = C / 16;
   static constexpr int E4 = (E + 3) & ~3;
@@ -284,7 +284,7 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
     for (int kt = 0; kt < KT; ++kt) {
       f32x4 x = zero4();
       if (dS_final && e < E) {
-        const float* src = dS_final + (((size_t)head * E + e) * KD + 16 * kt + 4 * g) * V + v0 + n;
+        const float* src = dS_final + (((size_t)head * E + e) * KD + key_col<KD>(kt, g)) * V + v0 + n;
 #pragma unroll
         for (int j = 0; j < 4; ++j) x[j] = src[(size_t)j * V];
       }
@@ -347,8 +347,26 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
       const bool kok = t0 + r < s.T;
       const T* krow = Kg + (size_t)(kok ? t0 + r : 0) * krs;
       auto kfrag = [&](int kb) -> F {
-        if constexpr (Sm::STAGE_K) return ld_frag(&sm.K[r][16 * kb + 4 * g]);
-        else return kok ? ld_frag(krow + 16 * kb + 4 * g) : cvt_frag<T>(zero4());
+        if constexpr (Sm::STAGE_K) return ld_frag(&sm.K[r][key_col<KD>(kb, g)]);
+        else return kok ? ld_frag(krow + key_col<KD>(kb, g)) : cvt_frag<T>(zero4());
+      };
+      // keys key_col(kb, g) .. + 7 of the row (kb even): one 32-deep A operand
+      auto kfrag8 = [&](int kb) -> Frag8<T> {
+        const int c = key_col<KD>(kb, g);
+        Frag8<T> f;
+        if constexpr (sizeof(T) == 2) {
+          if constexpr (Sm::STAGE_K) {
+            f.v = *(const bf16x8*)&sm.K[r][c];
+          } else {
+            const uint4 x = kok ? *(const uint4*)(krow + c) : make_uint4(0, 0, 0, 0);
+            f.v = __builtin_bit_cast(bf16x8, x);
+          }
+        } else {
+          f.lo = frag_to_f(kfrag(kb));
+          f.hi = kok ? ld_frag(krow + c + 4) : zero4();
+          if constexpr (Sm::STAGE_K) f.hi = ld_frag(&sm.K[r][c + 4]);
+        }
+        return f;
       };
       constexpr int GZ = PREFETCH ? SPW : 1;  // slices per pass over the K fragments
       f32x4 z[SPW];
@@ -358,10 +376,10 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
       for (int i0 = 0; i0 < SPW; i0 += GZ) {
 #pragma unroll
         for (int kb = 0; kb + 1 < KT; kb += 2) {
-          const F k0 = kfrag(kb), k1 = kfrag(kb + 1);
+          const Frag8<T> kk = kfrag8(kb);
 #pragma unroll
           for (int i = i0; i < i0 + GZ; ++i)
-            if (!RAGGED || w * SPW + i < E) mma32(z[i], k0, k1, dSop[i][kb], dSop[i][kb + 1]);
+            if (!RAGGED || w * SPW + i < E) mma32(z[i], kk, dSop[i][kb], dSop[i][kb + 1]);
         }
         if constexpr (KT & 1) {
           const F k0 = kfrag(KT - 1);
@@ -526,7 +544,7 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
       if (RAGGED && e >= E) continue;
 #pragma unroll
       for (int kt = 0; kt < KT; ++kt) {
-        float* dst = ds0 + (((size_t)head * E + e) * KD + 16 * kt + 4 * g) * V + v0 + n;
+        float* dst = ds0 + (((size_t)head * E + e) * KD + key_col<KD>(kt, g)) * V + v0 + n;
 #pragma unroll
         for (int j = 0; j < 4; ++j) dst[(size_t)j * V] = dS[i][kt][j];
       }
@@ -662,7 +680,7 @@ __global__ __launch_bounds__(STATE_NTHR) void k_bwd_state(Shape s, FwdIn in, con
       for (int j = 0; j < 4; ++j) {
         const int t = t0 + 16 * rt + 4 * g + j;
         const bool ok = rows && ct < KT && t < s.T;
-        const size_t off = (size_t)min(t, s.T - 1) * krs + 16 * min(ct, KT - 1) + n;
+        const size_t off = (size_t)min(t, s.T - 1) * krs + key_of_row<KD>(16 * min(ct, KT - 1) + n);
         if constexpr (sizeof(T) == 2) {
           const uint32_t qx = (uint32_t)((const uint16_t*)Qg)[off] << (16 * (j & 1));
           const uint32_t kx = (uint32_t)((const uint16_t*)Kg)[off] << (16 * (j & 1));
@@ -839,8 +857,9 @@ __global__ __launch_bounds__(STATE_NTHR) void k_bwd_state(Shape s, FwdIn in, con
       for (int c = 0; c < CTW; ++c) {
         const int ct = q * CTW + c, rt = rt0 + i;
         if (ct >= KT) continue;
-        float* qo = bb.dqs + (size_t)ch * C * KD + (size_t)(16 * rt + 4 * g) * KD + 16 * ct + n;
-        float* ko = bb.dks + (size_t)ch * C * KD + (size_t)(16 * rt + 4 * g) * KD + 16 * ct + n;
+        const int key = key_of_row<KD>(16 * ct + n);  // the key of tile row 16 ct + n
+        float* qo = bb.dqs + (size_t)ch * C * KD + (size_t)(16 * rt + 4 * g) * KD + key;
+        float* ko = bb.dks + (size_t)ch * C * KD + (size_t)(16 * rt + 4 * g) * KD + key;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           qo[(size_t)j * KD] = dq[i][c][j];

@@ -183,6 +183,20 @@ __device__ __forceinline__ void mma32(f32x4& acc, bf16x4 a0, bf16x4 a1, bf16x4 b
   acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc, 0, 0, 0);
 }
 
+// A 32-deep A operand held as one piece: lane group g's eight consecutive
+// contraction indices (a 16-byte read for bf16, two fp32 fragments).
+template <typename T> struct Frag8;
+template <> struct Frag8<bf16_t> { bf16x8 v; };
+template <> struct Frag8<float> { f32x4 lo, hi; };
+__device__ __forceinline__ void mma32(f32x4& acc, const Frag8<bf16_t>& a, bf16x4 b0, bf16x4 b1) {
+  const bf16x8 b = __builtin_shufflevector(b0, b1, 0, 1, 2, 3, 4, 5, 6, 7);
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v, b, acc, 0, 0, 0);
+}
+__device__ __forceinline__ void mma32(f32x4& acc, const Frag8<float>& a, f32x4 b0, f32x4 b1) {
+  mma16(acc, a.lo, b0);
+  mma16(acc, a.hi, b1);
+}
+
 // Fast exp of a non-positive argument (every decay factor here is exp of a
 // difference of accumulated log-gates that is <= 0).
 __device__ __forceinline__ float exp_nonpos(float x) { return __expf(x); }
@@ -436,6 +450,25 @@ __device__ __forceinline__ void store_tile16(T* dst, f32x4 x, int g, int n, int 
   else
     gstore_b128(p, __builtin_bit_cast(u32x4, x));
 }
+
+// Key order of the state tiles of the recurrent kernels.  Row i of a state
+// tile set (16 i-rows per accumulator tile) holds key key_of_row(i): within
+// each 32-key block, rows 16 h + 4 g + j hold keys 8 g + 4 h + j.  The two
+// accumulator tiles of a block then give lane group g the eight consecutive
+// keys 8 g .. 8 g + 7 as one 32-deep B operand, and the matching A operand
+// (a row of K or Q) is one 16-byte read.  Identity for fewer than 32 keys.
+template <int KD>
+__host__ __device__ constexpr int key_of_row(int i) {
+  return KD < 32 ? i : ((i & ~31) | (((i >> 2) & 3) << 3) | (((i >> 4) & 1) << 2) | (i & 3));
+}
+template <int KD>
+__host__ __device__ constexpr int row_of_key(int k) {
+  return KD < 32 ? k : ((k & ~31) | (((k >> 2) & 1) << 4) | (((k >> 3) & 3) << 2) | (k & 3));
+}
+// First key of the four that lane group g holds in 16-row block kb (the
+// others follow consecutively).
+template <int KD>
+__device__ __forceinline__ int key_col(int kb, int g) { return key_of_row<KD>(16 * kb + 4 * g); }
 
 // The identity as a 16-deep bf16 B fragment: lane (g, n) holds I[4 g + j][n].
 __device__ __forceinline__ bf16x4 identity_frag() {

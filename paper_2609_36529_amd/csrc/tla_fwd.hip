@@ -277,10 +277,13 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
           }
         }
       }
+      // (rows in the key order of the recurrent kernels' state tiles: key k
+      // at row row_of_key(k), which keeps each group of four keys together)
       T* dst = ops + (mtx ? OT::Qt : OT::Kt);
+      const int row4 = row_of_key<KD>(4 * kb);
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        put4<T>(dst + (size_t)(4 * kb + j) * C + 4 * rb, f32x4{x[0][j], x[1][j], x[2][j], x[3][j]});
+        put4<T>(dst + (size_t)(row4 + j) * C + 4 * rb, f32x4{x[0][j], x[1][j], x[2][j], x[3][j]});
     }
   }
   __syncthreads();
@@ -520,7 +523,7 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
     for (int kt = 0; kt < KT; ++kt) {
       f32x4 x = zero4();
       if (in.s0 && e < E) {
-        const float* src = in.s0 + (((size_t)head * E + e) * KD + 16 * kt + 4 * g) * V + v0 + n;
+        const float* src = in.s0 + (((size_t)head * E + e) * KD + key_col<KD>(kt, g)) * V + v0 + n;
 #pragma unroll
         for (int j = 0; j < 4; ++j) x[j] = src[(size_t)j * V];
       }
@@ -608,15 +611,47 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
     // straight into this wave's partial of W = sum_e diag(a_e) P^K_e and of
     // sum_e diag(b_e) P^Q_e (the two passes keep one set of accumulators live)
     {
+      // The 32-deep A operand of K (pass 0) or Q (pass 1) rows for row tile
+      // rt and the key blocks kb, kb + 1 (kb even): keys key_col(kb, g) ..
+      // + 7, one 16-byte piece of the row in the key order of the state tiles
+      auto afrag8 = [&](int pass, int rt, int kb) -> Frag8<T> {
+        const int r = 16 * rt + n, c = key_col<KD>(kb, g);
+        Frag8<T> f;
+        if constexpr (sizeof(T) == 2) {
+          if (pass == 0) {
+            f.v = *(const bf16x8*)sm.K.at(r, c);
+          } else if constexpr (Sm::STAGE_Q) {
+            f.v = *(const bf16x8*)sm.Q.at(r, c);
+          } else {
+            const bool qok = t0 + r < s.T;
+            const uint4 x = qok ? *(const uint4*)(Qg + (size_t)(t0 + r) * krs + c) : make_uint4(0, 0, 0, 0);
+            f.v = __builtin_bit_cast(bf16x8, x);
+          }
+        } else {
+          if (pass == 0) {
+            f.lo = ld_frag(sm.K.at(r, c));
+            f.hi = ld_frag(sm.K.at(r, c + 4));
+          } else if constexpr (Sm::STAGE_Q) {
+            f.lo = ld_frag(sm.Q.at(r, c));
+            f.hi = ld_frag(sm.Q.at(r, c + 4));
+          } else {
+            const bool qok = t0 + r < s.T;
+            f.lo = qok ? ld_frag(Qg + (size_t)(t0 + r) * krs + c) : zero4();
+            f.hi = qok ? ld_frag(Qg + (size_t)(t0 + r) * krs + c + 4) : zero4();
+          }
+        }
+        return f;
+      };
       // A fragment of K (pass 0) or Q (pass 1) rows for row tile rt, block kb
+      // (16-deep, for a single key block)
       auto afrag = [&](int pass, int rt, int kb) -> F {
         const int r = 16 * rt + n;
-        if (pass == 0) return ld_frag(sm.K.at(r, 16 * kb + 4 * g));
+        if (pass == 0) return ld_frag(sm.K.at(r, key_col<KD>(kb, g)));
         if constexpr (Sm::STAGE_Q) {
-          return ld_frag(sm.Q.at(r, 16 * kb + 4 * g));
+          return ld_frag(sm.Q.at(r, key_col<KD>(kb, g)));
         } else {
           const bool qok = t0 + r < s.T;
-          return qok ? ld_frag(Qg + (size_t)(t0 + r) * krs + 16 * kb + 4 * g) : cvt_frag<T>(zero4());
+          return qok ? ld_frag(Qg + (size_t)(t0 + r) * krs + key_col<KD>(kb, g)) : cvt_frag<T>(zero4());
         }
       };
       // fold the accumulators of a pass into this wave's partial
@@ -645,31 +680,28 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
         // registers to spare).  NT x SPW independent accumulators advance per
         // step.
         constexpr int NS = KT / 2;
-        auto load_step = [&](int j, F(&x0)[NT], F(&x1)[NT]) {
+        auto load_step = [&](int j, Frag8<T>(&x)[NT]) {
           const int ps = j / NS, kb = 2 * (j % NS);
 #pragma unroll
-          for (int rt = 0; rt < NT; ++rt) {
-            x0[rt] = afrag(ps, rt, kb);
-            x1[rt] = afrag(ps, rt, kb + 1);
-          }
+          for (int rt = 0; rt < NT; ++rt) x[rt] = afrag8(ps, rt, kb);
         };
         f32x4 P[SPW][NT];
 #pragma unroll
         for (int rt = 0; rt < NT; ++rt)
 #pragma unroll
           for (int i = 0; i < SPW; ++i) P[i][rt] = zero4();
-        F a0[NT], a1[NT];
-        load_step(0, a0, a1);
+        Frag8<T> a[NT];
+        load_step(0, a);
 #pragma unroll
         for (int j = 0; j < 2 * NS; ++j) {
-          F b0[NT], b1[NT];
-          if (j + 1 < 2 * NS) load_step(j + 1, b0, b1);
+          Frag8<T> bn[NT];
+          if (j + 1 < 2 * NS) load_step(j + 1, bn);
           const int kb = 2 * (j % NS);
 #pragma unroll
           for (int i = 0; i < SPW; ++i) {
             if (RAGGED && w * SPW + i >= E) continue;
 #pragma unroll
-            for (int rt = 0; rt < NT; ++rt) mma32(P[i][rt], a0[rt], a1[rt], Sop[i][kb], Sop[i][kb + 1]);
+            for (int rt = 0; rt < NT; ++rt) mma32(P[i][rt], a[rt], Sop[i][kb], Sop[i][kb + 1]);
           }
           if (j % NS == NS - 1) {
             fold(j / NS, P);
@@ -680,10 +712,7 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
           }
           if (j + 1 < 2 * NS) {
 #pragma unroll
-            for (int rt = 0; rt < NT; ++rt) {
-              a0[rt] = b0[rt];
-              a1[rt] = b1[rt];
-            }
+            for (int rt = 0; rt < NT; ++rt) a[rt] = bn[rt];
           }
         }
       } else {
@@ -699,17 +728,14 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
 #pragma unroll
           for (int kb = 0; kb < KT; kb += (KT > 1 ? 2 : 1)) {
             if constexpr (KT > 1) {
-              F a0[NT], a1[NT];
+              Frag8<T> a[NT];
 #pragma unroll
-              for (int rt = 0; rt < NT; ++rt) {
-                a0[rt] = afrag(pass, rt, kb);
-                a1[rt] = afrag(pass, rt, kb + 1);
-              }
+              for (int rt = 0; rt < NT; ++rt) a[rt] = afrag8(pass, rt, kb);
 #pragma unroll
               for (int i = 0; i < SPW; ++i) {
                 if (RAGGED && w * SPW + i >= E) continue;
 #pragma unroll
-                for (int rt = 0; rt < NT; ++rt) mma32(P[i][rt], a0[rt], a1[rt], Sop[i][kb], Sop[i][kb + 1]);
+                for (int rt = 0; rt < NT; ++rt) mma32(P[i][rt], a[rt], Sop[i][kb], Sop[i][kb + 1]);
               }
             } else {
               F a[NT];
@@ -925,7 +951,7 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
       if (RAGGED && e >= E) continue;
 #pragma unroll
       for (int kt = 0; kt < KT; ++kt) {
-        float* dst = s_final + (((size_t)head * E + e) * KD + 16 * kt + 4 * g) * V + v0 + n;
+        float* dst = s_final + (((size_t)head * E + e) * KD + key_col<KD>(kt, g)) * V + v0 + n;
 #pragma unroll
         for (int j = 0; j < 4; ++j) dst[(size_t)j * V] = S[i][kt][j];
       }

@@ -30,7 +30,8 @@ struct PrepBufs {
 // recurrent kernels copy into shared memory: M = (Q K^T) o R' (lower incl.
 // diagonal) and Tu = (I + L)^{-1} diag(beta) (GDN), each row-major and
 // transposed, as bf16 (hi, lo) pairs for bf16 operands (one fp32 copy for
-// fp32 operands), then K^T and Q^T of the chunk (rows past T are zero).
+// fp32 operands), then K^T and Q^T of the chunk (rows past T are zero; key k
+// in row row_of_key(k), the key order of the recurrent kernels' state tiles).
 // Element offsets within a chunk's block; part p (0 = hi, 1 = lo) of a
 // matrix X starts at X + p * MAT.
 template <typename T, int KD, int C>
@@ -49,13 +50,15 @@ inline size_t op_tile_bytes(int K, int C, bool bf16) {
 
 // Buffers the training forward stores for the backward (opaque layout).
 struct SavedBufs {
-  void* Sck;     // [ch][E][V/16][K][16] chunk-start states, operand type
+  void* Sck;     // [ch][E][V/16][K][16] chunk-start states, operand type; row i of a
+                 // tile holds key key_of_row(i), the recurrent kernels' register order
   float* U;      // [ch][C][V] delta-corrected values U
   float* X;      // [ch][C][V] residual V - W (GDN)
 };
 
 struct BwdBufs {
   void* dSck;    // [ch][E][V/16][K][16] state gradients at chunk ends, operand type
+                 // (rows in the same key order as Sck)
   float* dU;     // [ch][C][V]
   float* dW;     // [ch][C][V]
   float* dqs;    // [ch][C][K] state contributions to dq
