@@ -481,13 +481,18 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
                          al[ii][kb]);
           }
         }
+        // Q^T / K^T rows: positions 4 g + j and 16 + 4 g + j of a block pair
+        // are adjacent in the operand tiles (position r at column
+        // key_of_row(r)); element kb of a row's fragments is the 16-deep half
+        // kb % 2 of the pair kb / 2
         F qf[2][NT], kf[2][NT];
         auto load_kt = [&](int kt, F(&q)[NT], F(&k)[NT]) {
           const int r = 16 * kt + n;
 #pragma unroll
           for (int kb = 0; kb < NT; ++kb) {
-            q[kb] = ld_frag(&sm.Qt[r][16 * kb + 4 * g]);
-            if constexpr (GDN) k[kb] = ld_frag(&sm.Kt[r][16 * kb + 4 * g]);
+            const int c = key_of_row<C>(16 * (kb & ~1) + 4 * g) + (NT > 1 ? 4 * (kb & 1) : 0);
+            q[kb] = ld_frag(&sm.Qt[r][c]);
+            if constexpr (GDN) k[kb] = ld_frag(&sm.Kt[r][c]);
           }
         };
         load_kt(0, qf[0], kf[0]);

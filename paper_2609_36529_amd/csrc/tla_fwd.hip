@@ -278,12 +278,15 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
         }
       }
       // (rows in the key order of the recurrent kernels' state tiles: key k
-      // at row row_of_key(k), which keeps each group of four keys together)
+      // at row row_of_key(k); positions in the same order within 32-blocks,
+      // position r at column key_of_row(r), so that the eight positions of a
+      // lane group's 32-deep operand (4 g + j and 16 + 4 g + j) are adjacent;
+      // both keep each group of four together)
       T* dst = ops + (mtx ? OT::Qt : OT::Kt);
-      const int row4 = row_of_key<KD>(4 * kb);
+      const int row4 = row_of_key<KD>(4 * kb), col4 = key_of_row<C>(4 * rb);
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        put4<T>(dst + (size_t)(row4 + j) * C + 4 * rb, f32x4{x[0][j], x[1][j], x[2][j], x[3][j]});
+        put4<T>(dst + (size_t)(row4 + j) * C + col4, f32x4{x[0][j], x[1][j], x[2][j], x[3][j]});
     }
   }
   __syncthreads();
@@ -910,21 +913,27 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
 #pragma unroll
     for (int kb = 0; kb < NT; kb += (NT > 1 ? 2 : 1)) {
       if constexpr (NT > 1) {
-        F a0[KT], a1[KT];
+        // K^T rows: positions 4 g + j and 16 + 4 g + j of the block pair are
+        // adjacent in the operand tile (one 16-byte read per lane)
+        Frag8<T> a[KT];
+        const int c = key_of_row<C>(16 * kb + 4 * g);
 #pragma unroll
         for (int kt = 0; kt < KT; ++kt) {
-          a0[kt] = ld_frag(sm.Kt.at(16 * kt + n, 16 * kb + 4 * g));
-          a1[kt] = ld_frag(sm.Kt.at(16 * kt + n, 16 * kb + 16 + 4 * g));
+          if constexpr (sizeof(T) == 2) {
+            a[kt].v = *(const bf16x8*)sm.Kt.at(16 * kt + n, c);
+          } else {
+            a[kt].lo = ld_frag(sm.Kt.at(16 * kt + n, c));
+            a[kt].hi = ld_frag(sm.Kt.at(16 * kt + n, c + 4));
+          }
         }
 #pragma unroll
         for (int i = 0; i < SPW; ++i) {
           if (RAGGED && w * SPW + i >= E) continue;
 #pragma unroll
-          for (int kt = 0; kt < KT; ++kt) mma32(S[i][kt], a0[kt], a1[kt], Uc[i][kb], Uc[i][kb + 1]);
+          for (int kt = 0; kt < KT; ++kt) mma32(S[i][kt], a[kt], Uc[i][kb], Uc[i][kb + 1]);
           if constexpr (Sm::SPLIT) {
 #pragma unroll
-            for (int kt = 0; kt < KT; ++kt)
-              mma32(S[i][kt], a0[kt], a1[kt], Ucl[i][kb], Ucl[i][kb + 1]);
+            for (int kt = 0; kt < KT; ++kt) mma32(S[i][kt], a[kt], Ucl[i][kb], Ucl[i][kb + 1]);
           }
         }
       } else {
