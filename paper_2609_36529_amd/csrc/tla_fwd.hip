@@ -228,25 +228,27 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
       mma8(aq, qrow8(16 * rt + n, col), kb);
       mma8(ak, krow8(16 * rt + n, col), kb);
     }
+    // (every pair of the tile is formed and masked afterwards: no per-lane
+    // branch around the shared-memory reads, which are whole-row vector reads)
     double Gc[E];
     float k2c[E];
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-      Gc[e] = sm.G[c][e];
-      k2c[e] = sm.k2[c][e];
-    }
+    lds_row<E>(Gc, &sm.G[c][0]);
+    lds_row<E>(k2c, &sm.k2[c][0]);
     f32x4 mv;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int r = 16 * rt + 4 * g + j;
+      double Gr[E];
+      float q2r[E], k2r[E];
+      lds_row<E>(Gr, &sm.G[r][0]);
+      lds_row<E>(q2r, &sm.q2[r][0]);
+      lds_row<E>(k2r, &sm.k2[r][0]);
       float rq = 0.f, rk = 0.f;
-      if (c <= r) {
 #pragma unroll
-        for (int e = 0; e < E; ++e) {
-          const float d = exp_nonpos((float)(sm.G[r][e] - Gc[e])) * k2c[e];
-          rq += sm.q2[r][e] * d;
-          rk += sm.k2[r][e] * d;
-        }
+      for (int e = 0; e < E; ++e) {
+        const float d = exp_nonpos((float)(Gr[e] - Gc[e])) * k2c[e];
+        rq += q2r[e] * d;
+        rk += k2r[e] * d;
       }
       mv[j] = (c <= r) ? aq[j] * rq : 0.f;
       sm.L[r][c] = (c < r) ? sm.beta[r] * ak[j] * rk : 0.f;
