@@ -137,6 +137,43 @@ int tla_bwd(const tla_desc* desc, const void* q, const void* k, const void* v,
             size_t ws_bytes, void* stream);
 
 /*
+ * Packed variable-length batches: the forward and backward above for B =
+ * desc->B sequences of different lengths stored back to back.  Sequence b
+ * is tokens [cu_seqlens[b], cu_seqlens[b + 1]) of q, k, v, q2, k2, g, beta,
+ * o, dO and of the token gradients, which are laid out [1][total_tokens][H][.]
+ * (packed, no padding); each sequence runs its own recurrence from its own
+ * initial state s0[b] (or zero) to its own final state s_final[b], exactly
+ * as if it were called alone (Section 2: the state restarts with every
+ * sequence).  States and state gradients stay [B][H][E][K][V].
+ *   cu_seqlens  : device array of B + 1 int32 offsets, cu_seqlens[0] = 0,
+ *                 non-decreasing, cu_seqlens[B] = total_tokens; it is read
+ *                 by the kernels, never by the host.  Offsets outside that
+ *                 contract give wrong results but no access outside the
+ *                 tensors (every offset is clamped to [0, total_tokens] and
+ *                 every length to [0, desc->T]).
+ *   total_tokens: packed length, at most desc->B * desc->T.  With no tokens
+ *                 the token pointers may be NULL (states pass through).
+ *   desc->T     : the longest sequence; tla_workspace_bytes and
+ *                 tla_saved_bytes of desc size the buffers (as for B padded
+ *                 sequences of length T).
+ * Other arguments, ownership and errors as for tla_fwd / tla_bwd.
+ */
+int tla_fwd_varlen(const tla_desc* desc, const int32_t* cu_seqlens,
+                   long long total_tokens, const void* q, const void* k,
+                   const void* v, const void* q2, const void* k2,
+                   const float* g, const float* beta, const float* s0,
+                   void* o, float* s_final, void* saved, void* ws,
+                   size_t ws_bytes, void* stream);
+int tla_bwd_varlen(const tla_desc* desc, const int32_t* cu_seqlens,
+                   long long total_tokens, const void* q, const void* k,
+                   const void* v, const void* q2, const void* k2,
+                   const float* g, const float* beta, const float* s0,
+                   const void* dO, const float* dS_final, const void* saved,
+                   void* dq, void* dk, void* dv, void* dq2, void* dk2,
+                   float* dg, float* dbeta, float* ds0, void* ws,
+                   size_t ws_bytes, void* stream);
+
+/*
  * Recurrent single-token decode step (Eq. forget3 / gdn3 and the read of
  * Eq. la3, one token): for each of N = desc->B sequences and each head,
  * decays, (GDN) erases, writes and reads the state in one pass, updating

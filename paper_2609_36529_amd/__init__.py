@@ -59,6 +59,11 @@ def lib():
     L.tla_fwd.restype = I
     L.tla_bwd.argtypes = [DP] + [P] * 20 + [S, P]
     L.tla_bwd.restype = I
+    LL = ctypes.c_longlong
+    L.tla_fwd_varlen.argtypes = [DP, P, LL] + [P] * 12 + [S, P]
+    L.tla_fwd_varlen.restype = I
+    L.tla_bwd_varlen.argtypes = [DP, P, LL] + [P] * 20 + [S, P]
+    L.tla_bwd_varlen.restype = I
     L.tla_step.argtypes = [DP] + [P] * 9 + [P]
     L.tla_step.restype = I
     L.tla_prof_enable.argtypes = [I]
@@ -115,10 +120,23 @@ def _need(t, name, dtype=None, device=None):
     return t
 
 
-def describe(variant, q, v, q2, chunk, out_dtype=None):
+def describe(variant, q, v, q2, chunk, out_dtype=None, cu_seqlens=None, max_seqlen=None):
+    """Descriptor of a call; with cu_seqlens (packed sequences, q is
+    [1, total, H, K]) B is the number of sequences and T = max_seqlen."""
     B, T, H, K = q.shape
+    if cu_seqlens is not None:
+        if B != 1 or max_seqlen is None:
+            raise ValueError("packed sequences need q of shape [1, total, H, K] and max_seqlen")
+        B, T = cu_seqlens.numel() - 1, int(max_seqlen)
     return make_desc(variant, B, T, H, K, v.shape[-1], q2.shape[-1], chunk, _dtype_code(q.dtype),
                      _dtype_code(out_dtype if out_dtype is not None else q.dtype))
+
+
+def _cu(cu_seqlens, dev):
+    if cu_seqlens is None:
+        return None
+    _need(cu_seqlens, "cu_seqlens", torch.int32, dev)
+    return cu_seqlens
 
 
 def supported(desc):
@@ -134,8 +152,12 @@ def saved_bytes(desc):
 
 
 def fwd(variant, q, k, v, q2, k2, g, beta=None, s0=None, chunk=64, out_dtype=None,
-        want_final=True, training=False, o=None, s_final=None, ws=None, saved=None):
-    """Chunkwise forward.  Returns (o, s_final or None, saved or None)."""
+        want_final=True, training=False, o=None, s_final=None, ws=None, saved=None,
+        cu_seqlens=None, max_seqlen=None):
+    """Chunkwise forward.  Returns (o, s_final or None, saved or None).
+    With cu_seqlens (int32 device tensor of N + 1 offsets) the inputs hold N
+    packed sequences, [1, total, H, .], each with its own state (s0 and
+    s_final [N, H, E, K, V]); max_seqlen is the longest length."""
     dev = q.device
     dt = q.dtype
     for name, t in (("q", q), ("k", k), ("v", v), ("q2", q2), ("k2", k2)):
@@ -143,34 +165,42 @@ def fwd(variant, q, k, v, q2, k2, g, beta=None, s0=None, chunk=64, out_dtype=Non
     _need(g, "g", torch.float32, dev)
     _need(beta, "beta", torch.float32, dev)
     _need(s0, "s0", torch.float32, dev)
-    desc = describe(variant, q, v, q2, chunk, out_dtype)
-    B, T, H, K = q.shape
+    cu = _cu(cu_seqlens, dev)
+    desc = describe(variant, q, v, q2, chunk, out_dtype, cu, max_seqlen)
+    B, T = desc.B, desc.T
+    H, K = q.shape[2], q.shape[3]
     V, E = v.shape[-1], q2.shape[-1]
     if o is None:
-        o = torch.empty((B, T, H, V), dtype=out_dtype or dt, device=dev)
+        o = torch.empty(q.shape[:3] + (V,), dtype=out_dtype or dt, device=dev)
     if want_final and s_final is None:
         s_final = torch.empty((B, H, E, K, V), dtype=torch.float32, device=dev)
     if ws is None:
         ws = torch.empty(max(workspace_bytes(desc, OP_FWD), 1), dtype=torch.uint8, device=dev)
     if training and saved is None:
         saved = torch.empty(max(saved_bytes(desc), 1), dtype=torch.uint8, device=dev)
-    rc = lib().tla_fwd(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(q2), _ptr(k2), _ptr(g),
-                       _ptr(beta), _ptr(s0), _ptr(o), _ptr(s_final if want_final else None),
-                       _ptr(saved if training else None), _ptr(ws), ws.numel(), _stream(dev))
+    args = (_ptr(q), _ptr(k), _ptr(v), _ptr(q2), _ptr(k2), _ptr(g), _ptr(beta), _ptr(s0), _ptr(o),
+            _ptr(s_final if want_final else None), _ptr(saved if training else None), _ptr(ws),
+            ws.numel(), _stream(dev))
+    if cu is None:
+        rc = lib().tla_fwd(ctypes.byref(desc), *args)
+    else:
+        rc = lib().tla_fwd_varlen(ctypes.byref(desc), _ptr(cu), q.shape[1], *args)
     _check(rc)
     return o, (s_final if want_final else None), (saved if training else None)
 
 
 def bwd(variant, q, k, v, q2, k2, g, beta, s0, dO, saved, dS_final=None, chunk=64,
-        out_dtype=None, want_ds0=True, ws=None, grads=None):
+        out_dtype=None, want_ds0=True, ws=None, grads=None, cu_seqlens=None, max_seqlen=None):
     """Backward of a training forward.  Returns a dict of gradients
     (dq, dk, dv, dq2, dk2 in out_dtype (default: the input dtype); dg, dbeta or
-    None, ds0 or None in fp32)."""
+    None, ds0 or None in fp32).  cu_seqlens / max_seqlen as for fwd."""
     dev = q.device
     dt = q.dtype
     gt = out_dtype or dt
-    desc = describe(variant, q, v, q2, chunk, gt)
-    B, T, H, K = q.shape
+    cu = _cu(cu_seqlens, dev)
+    desc = describe(variant, q, v, q2, chunk, gt, cu, max_seqlen)
+    B = desc.B
+    H, K = q.shape[2], q.shape[3]
     V, E = v.shape[-1], q2.shape[-1]
     _need(dO, "dO", dt, dev)
     _need(dS_final, "dS_final", torch.float32, dev)
@@ -179,17 +209,20 @@ def bwd(variant, q, k, v, q2, k2, g, beta, s0, dO, saved, dS_final=None, chunk=6
             "dq": torch.empty_like(q, dtype=gt), "dk": torch.empty_like(k, dtype=gt),
             "dv": torch.empty_like(v, dtype=gt), "dq2": torch.empty_like(q2, dtype=gt),
             "dk2": torch.empty_like(k2, dtype=gt),
-            "dg": torch.empty((B, T, H, E), dtype=torch.float32, device=dev),
-            "dbeta": None if beta is None else torch.empty((B, T, H), dtype=torch.float32, device=dev),
+            "dg": torch.empty(q.shape[:3] + (E,), dtype=torch.float32, device=dev),
+            "dbeta": None if beta is None else torch.empty(q.shape[:3], dtype=torch.float32, device=dev),
             "ds0": torch.empty((B, H, E, K, V), dtype=torch.float32, device=dev) if want_ds0 else None,
         }
     if ws is None:
         ws = torch.empty(max(workspace_bytes(desc, OP_BWD), 1), dtype=torch.uint8, device=dev)
-    rc = lib().tla_bwd(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(q2), _ptr(k2), _ptr(g),
-                       _ptr(beta), _ptr(s0), _ptr(dO), _ptr(dS_final), _ptr(saved),
-                       _ptr(grads["dq"]), _ptr(grads["dk"]), _ptr(grads["dv"]), _ptr(grads["dq2"]),
-                       _ptr(grads["dk2"]), _ptr(grads["dg"]), _ptr(grads["dbeta"]),
-                       _ptr(grads["ds0"]), _ptr(ws), ws.numel(), _stream(dev))
+    args = (_ptr(q), _ptr(k), _ptr(v), _ptr(q2), _ptr(k2), _ptr(g), _ptr(beta), _ptr(s0), _ptr(dO),
+            _ptr(dS_final), _ptr(saved), _ptr(grads["dq"]), _ptr(grads["dk"]), _ptr(grads["dv"]),
+            _ptr(grads["dq2"]), _ptr(grads["dk2"]), _ptr(grads["dg"]), _ptr(grads["dbeta"]),
+            _ptr(grads["ds0"]), _ptr(ws), ws.numel(), _stream(dev))
+    if cu is None:
+        rc = lib().tla_bwd(ctypes.byref(desc), *args)
+    else:
+        rc = lib().tla_bwd_varlen(ctypes.byref(desc), _ptr(cu), q.shape[1], *args)
     _check(rc)
     return grads
 

@@ -86,6 +86,22 @@ int check_desc(const tla_desc* d, tla::Shape* s, bool for_step) {
   s->in_bf16 = d->in_dtype == TLA_BF16;
   s->out_bf16 = d->out_dtype == TLA_BF16;
   s->has_beta = 0;
+  s->cu = nullptr;
+  s->total = 0;
+  return TLA_OK;
+}
+
+// Packed variable-length batches: checks the host-side arguments and fills
+// the packed fields of the shape (offsets stay on the device).
+int check_varlen(const int32_t* cu_seqlens, long long total_tokens, tla::Shape* s) {
+  if (!cu_seqlens) return fail(TLA_E_NULL, "cu_seqlens is NULL");
+  if (((uintptr_t)cu_seqlens & 3u) != 0) return fail(TLA_E_ALIGN, "cu_seqlens is not 4-byte aligned");
+  if (total_tokens < 0) return fail(TLA_E_SHAPE, "total_tokens=%lld must be >= 0", total_tokens);
+  if (total_tokens > (long long)s->B * s->T)
+    return fail(TLA_E_SHAPE, "total_tokens=%lld exceeds B * T = %lld (T is the longest sequence)",
+                total_tokens, (long long)s->B * s->T);
+  s->cu = cu_seqlens;
+  s->total = total_tokens;
   return TLA_OK;
 }
 
@@ -245,22 +261,24 @@ size_t tla_saved_bytes(const tla_desc* d) {
   return layout(s).sv_end;
 }
 
-int tla_fwd(const tla_desc* d, const void* q, const void* k, const void* v, const void* q2,
-            const void* k2, const float* g, const float* beta, const float* s0, void* o,
-            float* s_final, void* saved, void* ws, size_t ws_bytes, void* stream) {
+static int fwd_impl(const tla_desc* d, const int32_t* cu, long long total, const void* q,
+                    const void* k, const void* v, const void* q2, const void* k2, const float* g,
+                    const float* beta, const float* s0, void* o, float* s_final, void* saved,
+                    void* ws, size_t ws_bytes, void* stream) {
   g_err[0] = 0;
   tla::Shape s;
   int rc = check_desc(d, &s, false);
   if (rc) return rc;
-  const size_t ntok = (size_t)s.B * s.T * s.H;
-  if (s.T > 0 && (!q || !k || !v || !q2 || !k2 || !g || !o))
+  if (cu && (rc = check_varlen(cu, total, &s))) return rc;
+  const size_t ntok = (cu ? (size_t)total : (size_t)s.B * s.T) * s.H;
+  if (ntok > 0 && (!q || !k || !v || !q2 || !k2 || !g || !o))
     return fail(TLA_E_NULL, "q, k, v, q2, k2, g and o are required");
-  if (s.variant == TLA_GDN && s.T > 0 && !beta) return fail(TLA_E_NULL, "GDN needs beta");
+  if (s.variant == TLA_GDN && ntok > 0 && !beta) return fail(TLA_E_NULL, "GDN needs beta");
   const void* ptrs[] = {q, k, v, q2, k2, g, beta, s0, o, s_final, saved, ws};
   for (const void* p : ptrs)
     if (misaligned(p)) return fail(TLA_E_ALIGN, "pointer %p is not 16-byte aligned", p);
   const Layout L = layout(s);
-  const bool use_ws = s.T > 0 && !saved;  // a training forward keeps its prep results in saved
+  const bool use_ws = ntok > 0 && !saved;  // a training forward keeps its prep results in saved
   if (use_ws && (!ws || ws_bytes < L.p_ninv))
     return fail(TLA_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, L.p_ninv);
   const size_t es = esize(s), os = s.out_bf16 ? 2 : 4;
@@ -292,11 +310,11 @@ int tla_fwd(const tla_desc* d, const void* q, const void* k, const void* v, cons
   const tla::PrepBufs pb =
       saved ? prep_bufs(L, (char*)saved + L.sv_prep, true) : prep_bufs(L, ws, false);
   hipError_t e;
-  if (s.T > 0) {
+  if (ntok > 0) {
     e = timed(PROF_PREP, st, [&] { return tla::launch_prep(s, in, pb, st); });
     if (e != hipSuccess) return device_fail(e, "prep kernel");
   }
-  if (s.T > 0 || s_final) {
+  if (ntok > 0 || s_final) {
     tla::SavedBufs sv = saved_bufs(L, saved);
     e = timed(PROF_FWD, st, [&] {
       return tla::launch_fwd(s, in, pb, o, s_final, saved ? &sv : nullptr, st);
@@ -306,21 +324,39 @@ int tla_fwd(const tla_desc* d, const void* q, const void* k, const void* v, cons
   return TLA_OK;
 }
 
-int tla_bwd(const tla_desc* d, const void* q, const void* k, const void* v, const void* q2,
-            const void* k2, const float* g, const float* beta, const float* s0, const void* dO,
-            const float* dS_final, const void* saved, void* dq, void* dk, void* dv, void* dq2,
-            void* dk2, float* dg, float* dbeta, float* ds0, void* ws, size_t ws_bytes,
-            void* stream) {
+int tla_fwd(const tla_desc* d, const void* q, const void* k, const void* v, const void* q2,
+            const void* k2, const float* g, const float* beta, const float* s0, void* o,
+            float* s_final, void* saved, void* ws, size_t ws_bytes, void* stream) {
+  return fwd_impl(d, nullptr, 0, q, k, v, q2, k2, g, beta, s0, o, s_final, saved, ws, ws_bytes,
+                  stream);
+}
+
+int tla_fwd_varlen(const tla_desc* d, const int32_t* cu_seqlens, long long total_tokens,
+                   const void* q, const void* k, const void* v, const void* q2, const void* k2,
+                   const float* g, const float* beta, const float* s0, void* o, float* s_final,
+                   void* saved, void* ws, size_t ws_bytes, void* stream) {
+  if (!cu_seqlens) return fail(TLA_E_NULL, "cu_seqlens is NULL");
+  return fwd_impl(d, cu_seqlens, total_tokens, q, k, v, q2, k2, g, beta, s0, o, s_final, saved,
+                  ws, ws_bytes, stream);
+}
+
+static int bwd_impl(const tla_desc* d, const int32_t* cu, long long total, const void* q,
+                    const void* k, const void* v, const void* q2, const void* k2, const float* g,
+                    const float* beta, const float* s0, const void* dO, const float* dS_final,
+                    const void* saved, void* dq, void* dk, void* dv, void* dq2, void* dk2,
+                    float* dg, float* dbeta, float* ds0, void* ws, size_t ws_bytes, void* stream) {
   g_err[0] = 0;
   tla::Shape s;
   int rc = check_desc(d, &s, false);
   if (rc) return rc;
   if (s.T < 1) return fail(TLA_E_SHAPE, "the backward needs T >= 1");
+  if (cu && (rc = check_varlen(cu, total, &s))) return rc;
   if (s.V > 128) return fail(TLA_E_UNSUPPORTED, "the backward supports V <= 128 (V=%d)", s.V);
-  if (!q || !k || !v || !q2 || !k2 || !g || !dO || !saved || !dq || !dk || !dv || !dq2 || !dk2 ||
-      !dg || !ws)
+  const size_t ntok = (cu ? (size_t)total : (size_t)s.B * s.T) * s.H;
+  if (!saved || !ws || (ntok > 0 && (!q || !k || !v || !q2 || !k2 || !g || !dO || !dq || !dk ||
+                                     !dv || !dq2 || !dk2 || !dg)))
     return fail(TLA_E_NULL, "a required pointer is NULL");
-  if (s.variant == TLA_GDN && !beta) return fail(TLA_E_NULL, "GDN needs beta");
+  if (s.variant == TLA_GDN && ntok > 0 && !beta) return fail(TLA_E_NULL, "GDN needs beta");
   if ((beta == nullptr) != (dbeta == nullptr))
     return fail(TLA_E_NULL, "dbeta must be given exactly when beta is");
   const void* ptrs[] = {q, k, v, q2, k2, g, beta, s0, dO, dS_final, saved, dq,
@@ -329,7 +365,6 @@ int tla_bwd(const tla_desc* d, const void* q, const void* k, const void* v, cons
     if (misaligned(p)) return fail(TLA_E_ALIGN, "pointer %p is not 16-byte aligned", p);
   const Layout L = layout(s);
   if (ws_bytes < L.bwd_end) return fail(TLA_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, L.bwd_end);
-  const size_t ntok = (size_t)s.B * s.T * s.H;
   const size_t es = esize(s), os = s.out_bf16 ? 2 : 4;
   const size_t sbytes = (size_t)s.NH * s.E * s.K * s.V * 4;
   const Range ins[] = {{q, ntok * s.K * es}, {k, ntok * s.K * es}, {v, ntok * s.V * es},
@@ -368,6 +403,26 @@ int tla_bwd(const tla_desc* d, const void* q, const void* k, const void* v, cons
   });
   if (e != hipSuccess) return device_fail(e, "backward chunk kernel");
   return TLA_OK;
+}
+
+int tla_bwd(const tla_desc* d, const void* q, const void* k, const void* v, const void* q2,
+            const void* k2, const float* g, const float* beta, const float* s0, const void* dO,
+            const float* dS_final, const void* saved, void* dq, void* dk, void* dv, void* dq2,
+            void* dk2, float* dg, float* dbeta, float* ds0, void* ws, size_t ws_bytes,
+            void* stream) {
+  return bwd_impl(d, nullptr, 0, q, k, v, q2, k2, g, beta, s0, dO, dS_final, saved, dq, dk, dv,
+                  dq2, dk2, dg, dbeta, ds0, ws, ws_bytes, stream);
+}
+
+int tla_bwd_varlen(const tla_desc* d, const int32_t* cu_seqlens, long long total_tokens,
+                   const void* q, const void* k, const void* v, const void* q2, const void* k2,
+                   const float* g, const float* beta, const float* s0, const void* dO,
+                   const float* dS_final, const void* saved, void* dq, void* dk, void* dv,
+                   void* dq2, void* dk2, float* dg, float* dbeta, float* ds0, void* ws,
+                   size_t ws_bytes, void* stream) {
+  if (!cu_seqlens) return fail(TLA_E_NULL, "cu_seqlens is NULL");
+  return bwd_impl(d, cu_seqlens, total_tokens, q, k, v, q2, k2, g, beta, s0, dO, dS_final, saved,
+                  dq, dk, dv, dq2, dk2, dg, dbeta, ds0, ws, ws_bytes, stream);
 }
 
 int tla_step(const tla_desc* d, const void* q, const void* k, const void* v, const void* q2,

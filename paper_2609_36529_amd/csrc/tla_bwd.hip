@@ -274,6 +274,9 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
   xcd_map(blockIdx.x, s.NH, V / 16, head, vt);
   const int b = head / s.H, h = head % s.H;
   const int v0 = vt * 16;
+  const size_t tok0 = seq_begin(s, b);
+  s.T = seq_len(s, b);                 // this sequence's length from here on
+  const int nc = (s.T + C - 1) / C;    // its chunks (s.Nc: the per-head stride)
 
   // dS[i][kt] = dS_e[16 kt + 4 g + j][v0 + n], e = w * SPW + i
   f32x4 dS[SPW][KT];
@@ -292,16 +295,17 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
     }
   }
 
-  const T* Kg = (const T*)in.k + (((size_t)b * s.T) * s.H + h) * KD;
-  const T* Qg = (const T*)in.q + (((size_t)b * s.T) * s.H + h) * KD;
-  const T* dOg = (const T*)dOv + (((size_t)b * s.T) * s.H + h) * (size_t)V + v0;
+  const T* Kg = (const T*)in.k + (tok0 * s.H + h) * KD;
+  const T* Qg = (const T*)in.q + (tok0 * s.H + h) * KD;
+  const T* dOg = (const T*)dOv + (tok0 * s.H + h) * (size_t)V + v0;
   const size_t krs = (size_t)s.H * KD;
   const size_t vrs = (size_t)s.H * V;
 
   const bf16x4 idf = identity_frag();  // for the transposing dS' stores
   RecStage<T, KD, C, E, NTHR> stage;
-  if constexpr (PREFETCH) stage.load(s, p, Kg, Qg, dOg, (size_t)head * s.Nc + s.Nc - 1, s.Nc - 1);
-  for (int ci = s.Nc - 1; ci >= 0; --ci) {
+  if constexpr (PREFETCH)
+    if (nc > 0) stage.load(s, p, Kg, Qg, dOg, (size_t)head * s.Nc + nc - 1, nc - 1);
+  for (int ci = nc - 1; ci >= 0; --ci) {
     const int t0 = ci * C;
     const size_t ch = (size_t)head * s.Nc + ci;
     __syncthreads();
@@ -612,10 +616,13 @@ __global__ __launch_bounds__(STATE_NTHR) void k_bwd_state(Shape s, FwdIn in, con
   const int head = ch / s.Nc, ci = ch % s.Nc;
   const int b = head / s.H, h = head % s.H;
   const int t0 = ci * C;
+  const size_t tok0 = seq_begin(s, b);
+  s.T = seq_len(s, b);  // this sequence's length from here on
+  if (t0 >= s.T) return;  // past the end of a shorter packed sequence
   const size_t krs = (size_t)s.H * KD, vrs = (size_t)s.H * V;
-  const T* Kg = (const T*)in.k + (((size_t)b * s.T) * s.H + h) * KD;
-  const T* Qg = (const T*)in.q + (((size_t)b * s.T) * s.H + h) * KD;
-  const T* dOg = (const T*)dOv + (((size_t)b * s.T) * s.H + h) * (size_t)V;
+  const T* Kg = (const T*)in.k + (tok0 * s.H + h) * KD;
+  const T* Qg = (const T*)in.q + (tok0 * s.H + h) * KD;
+  const T* dOg = (const T*)dOv + (tok0 * s.H + h) * (size_t)V;
   const float* dWg = bb.dW + (size_t)ch * C * V;
   const float* Ug = sv.U + (size_t)ch * C * V;
 
@@ -1019,17 +1026,20 @@ __global__ __launch_bounds__(CHUNK_NTHR) void k_bwd_chunk(Shape s, FwdIn in, con
   const int head = ch / s.Nc, ci = ch % s.Nc;
   const int b = head / s.H, h = head % s.H;
   const int t0 = ci * C;
+  const size_t tok0 = seq_begin(s, b);
+  s.T = seq_len(s, b);  // this sequence's length from here on
+  if (t0 >= s.T) return;  // past the end of a shorter packed sequence
   const size_t krs = (size_t)s.H * KD, vrs = (size_t)s.H * V;
-  const T* Kg = (const T*)in.k + (((size_t)b * s.T) * s.H + h) * KD;
-  const T* Qg = (const T*)in.q + (((size_t)b * s.T) * s.H + h) * KD;
-  const T* Vg = (const T*)in.v + (((size_t)b * s.T) * s.H + h) * (size_t)V;
-  const T* dOg = (const T*)dOv + (((size_t)b * s.T) * s.H + h) * (size_t)V;
+  const T* Kg = (const T*)in.k + (tok0 * s.H + h) * KD;
+  const T* Qg = (const T*)in.q + (tok0 * s.H + h) * KD;
+  const T* Vg = (const T*)in.v + (tok0 * s.H + h) * (size_t)V;
+  const T* dOg = (const T*)dOv + (tok0 * s.H + h) * (size_t)V;
   const float* Ug = sv.U + (size_t)ch * C * V;
   const float* Xg = sv.X + (size_t)ch * C * V;
   const float* dUg = bb.dU + (size_t)ch * C * V;
   const float* dWg = bb.dW + (size_t)ch * C * V;
   const float* dcf = bb.dcoef + (size_t)ch * 3 * E * C;
-  const size_t eoff = (((size_t)b * s.T) * s.H + h) * E;
+  const size_t eoff = (tok0 * s.H + h) * E;
   const size_t erow = (size_t)s.H * E;
   const bool gdn = s.variant == 1;
 
@@ -1043,7 +1053,7 @@ __global__ __launch_bounds__(CHUNK_NTHR) void k_bwd_chunk(Shape s, FwdIn in, con
   }
   for (int r = tid; r < C; r += NTHR) {
     const int t = t0 + r;
-    sm.beta[r] = (t < s.T) ? (in.beta ? in.beta[((size_t)b * s.T + t) * s.H + h] : 1.f) : 0.f;
+    sm.beta[r] = (t < s.T) ? (in.beta ? in.beta[(tok0 + t) * s.H + h] : 1.f) : 0.f;
   }
   if constexpr (STAGE_QK) {
     constexpr int IT = (C * KD / 8 + NTHR - 1) / NTHR;
@@ -1450,7 +1460,7 @@ __global__ __launch_bounds__(CHUNK_NTHR) void k_bwd_chunk(Shape s, FwdIn in, con
     for (int j = 0; j < 4; ++j) {
       const int t = t0 + 16 * rt + 4 * g + j;
       if (t < s.T) {
-        const size_t o = (((size_t)b * s.T + t) * s.H + h) * KD + 16 * kt + n;
+        const size_t o = ((tok0 + t) * s.H + h) * KD + 16 * kt + n;
         store_out(dqv, o, aq[j] + pq[j], s.out_bf16);
         store_out(dkv, o, ak[j] + pk[j], s.out_bf16);
       }
@@ -1480,7 +1490,7 @@ __global__ __launch_bounds__(CHUNK_NTHR) void k_bwd_chunk(Shape s, FwdIn in, con
       const int t = t0 + r;
       if (idx >= C * n8 || t >= s.T) continue;
       const float sc = gdn ? -1.f : sm.beta[r];
-      store8_out(dvv, (((size_t)b * s.T + t) * s.H + h) * (size_t)V + c, sc * x[it][0],
+      store8_out(dvv, ((tok0 + t) * s.H + h) * (size_t)V + c, sc * x[it][0],
                  sc * x[it][1], s.out_bf16);
     }
   }
@@ -1598,7 +1608,7 @@ __global__ __launch_bounds__(CHUNK_NTHR) void k_bwd_chunk(Shape s, FwdIn in, con
   }
   if (dbeta && tid < C) {
     const int t = t0 + tid;
-    if (t < s.T) dbeta[((size_t)b * s.T + t) * s.H + h] = sm.dbeta[tid];
+    if (t < s.T) dbeta[(tok0 + t) * s.H + h] = sm.dbeta[tid];
   }
 }
 

@@ -92,11 +92,14 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
   const int b = head / s.H, h = head % s.H;
   const int t0 = ci * C;
   const int tid = threadIdx.x;
+  const size_t tok0 = seq_begin(s, b);
+  s.T = seq_len(s, b);  // this sequence's length from here on
+  if (t0 >= s.T) return;  // past the end of a shorter packed sequence
   const int w = wave_id(), l = lane_id(), g = l >> 4, n = l & 15;
   const size_t krs = (size_t)s.H * KD;
-  const T* Qg = (const T*)in.q + (((size_t)b * s.T) * s.H + h) * KD;
-  const T* Kg = (const T*)in.k + (((size_t)b * s.T) * s.H + h) * KD;
-  const size_t eoff = (((size_t)b * s.T) * s.H + h) * E, erow = (size_t)s.H * E;
+  const T* Qg = (const T*)in.q + (tok0 * s.H + h) * KD;
+  const T* Kg = (const T*)in.k + (tok0 * s.H + h) * KD;
+  const size_t eoff = (tok0 * s.H + h) * E, erow = (size_t)s.H * E;
 
   // ---- per-position vectors; Q and K rows (rows past T read clamped, then zeroed)
   for (int idx = tid; idx < C * E; idx += 256) {
@@ -109,7 +112,7 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
   }
   if (tid < C) {
     const int t = min(t0 + tid, s.T - 1);
-    const float bv = in.beta ? in.beta[((size_t)b * s.T + t) * s.H + h] : 1.f;
+    const float bv = in.beta ? in.beta[(tok0 + t) * s.H + h] : 1.f;
     sm.beta[tid] = (t0 + tid < s.T) ? bv : 0.f;
   }
   if constexpr (STAGE) {
@@ -518,6 +521,9 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
   xcd_map(blockIdx.x, s.NH, V / 16, head, vt);
   const int b = head / s.H, h = head % s.H;
   const int v0 = vt * 16;
+  const size_t tok0 = seq_begin(s, b);
+  s.T = seq_len(s, b);                 // this sequence's length from here on
+  const int nc = (s.T + C - 1) / C;    // its chunks (s.Nc: the per-head stride)
 
   // state tiles S[i][kt] = S_e[16 kt + 4 g + j][v0 + n], e = w * SPW + i
   f32x4 S[SPW][KT];
@@ -536,19 +542,19 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
     }
   }
 
-  const T* Kg = (const T*)in.k + (((size_t)b * s.T) * s.H + h) * KD;
-  const T* Qg = (const T*)in.q + (((size_t)b * s.T) * s.H + h) * KD;
-  const T* Vg = (const T*)in.v + (((size_t)b * s.T) * s.H + h) * (size_t)V + v0;
+  const T* Kg = (const T*)in.k + (tok0 * s.H + h) * KD;
+  const T* Qg = (const T*)in.q + (tok0 * s.H + h) * KD;
+  const T* Vg = (const T*)in.v + (tok0 * s.H + h) * (size_t)V + v0;
   const size_t krs = (size_t)s.H * KD;  // row stride between positions
   const size_t ch0 = (size_t)head * s.Nc;
 
   const bf16x4 idf = identity_frag();  // for the transposing checkpoint stores
   const size_t vrs = (size_t)s.H * V;
   const bool sbeta = s.variant == 0 && in.beta != nullptr;  // beta copied per chunk
-  const float* bg = in.beta ? in.beta + (size_t)b * s.T * s.H + h : nullptr;
+  const float* bg = in.beta ? in.beta + tok0 * s.H + h : nullptr;
   if (s.variant == 0 && !in.beta)
     for (int r = threadIdx.x; r < C; r += NTHR) sm.beta[r] = 1.f;
-  if (s.Nc > 0) {
+  if (nc > 0) {
     Dma::kq(sm, s, p, Kg, Qg, ch0, 0);
     Dma::v(sm, Vg, vrs, s.T - 1);
     if (sbeta) Dma::beta(sm, bg, s.H, s.T - 1);
@@ -565,10 +571,10 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
   const int n_st = (train ? owned * KT : 0) + ((train && w < NT) ? (s.variant == 1 ? 8 : 4) : 0);
   const int n_more = n_st + Dma::N_KQ + Dma::N_TU + 1 + (sbeta ? 1 : 0);
 
-  for (int ci = 0; ci < s.Nc; ++ci) {
+  for (int ci = 0; ci < nc; ++ci) {
     const int t0 = ci * C;
     const size_t ch = ch0 + ci;
-    const bool more = ci + 1 < s.Nc;
+    const bool more = ci + 1 < nc;
     __syncthreads();  // the previous chunk is done with K^T, c_e and gamma^C
 
     Dma::kt(sm, p, ch);
@@ -889,7 +895,7 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
       for (int j = 0; j < 4; ++j) {
         const int t = t0 + 16 * rt + 4 * g + j;
         if (t < s.T) {
-          const size_t off = (((size_t)b * s.T + t) * s.H + h) * (size_t)V + v0 + n;
+          const size_t off = ((tok0 + t) * s.H + h) * (size_t)V + v0 + n;
           if (s.out_bf16)
             ((bf16_t*)out)[off] = Elem<bf16_t>::from_f(oacc[j]);
           else

@@ -15,7 +15,30 @@ struct Shape {
   int in_bf16;   // operand type of q, k, v, q2, k2, dO and gradients
   int out_bf16;  // type of o
   int has_beta;
+  // Packed variable-length sequences: with cu != nullptr, sequence b is
+  // tokens [cu[b], cu[b + 1]) of one packed batch of `total` tokens, T is
+  // the longest length (it sizes the per-chunk buffers) and B the number
+  // of sequences.  cu is a device array of B + 1 offsets.
+  const int* cu;
+  long long total;
 };
+
+// First token and length of sequence b.  Packed offsets are clamped to the
+// packed batch and lengths to [0, T], so malformed offsets give wrong
+// results but never address memory outside the tensors.
+__device__ __forceinline__ size_t seq_begin(const Shape& s, int b) {
+  if (!s.cu) return (size_t)b * s.T;
+  const long long x = s.cu[b];
+  return (size_t)(x < 0 ? 0 : (x > s.total ? s.total : x));
+}
+__device__ __forceinline__ int seq_len(const Shape& s, int b) {
+  if (!s.cu) return s.T;
+  const long long b0 = (long long)seq_begin(s, b);
+  long long e = s.cu[b + 1];
+  e = e > s.total ? s.total : e;
+  const long long n = e - b0;
+  return (int)(n < 0 ? 0 : (n > s.T ? s.T : n));
+}
 
 // Per-chunk quantities written by the prep kernel.  All arrays are indexed by
 // ch = (b * H + h) * Nc + chunk.

@@ -169,3 +169,25 @@ def test_size_queries():
     assert ws_b > ws_f > 0
     assert tla.supported(d)
     assert not tla.supported(desc(K=48))
+
+
+def test_varlen_validation():
+    """Packed-sequence entry points: offsets are required, 4-byte aligned, and
+    the packed length may not exceed B * T (T is the longest sequence)."""
+    L = tla.lib()
+    P = ctypes.c_void_p
+    d = desc(B=3, T=100)
+    ptrs = [P(FAKE + i * 0x1000000) for i in range(12)]
+
+    def fcall(cu, total):
+        return L.tla_fwd_varlen(ctypes.byref(d), cu, total, *ptrs, 1 << 40, None)
+
+    def bcall(cu, total):
+        return L.tla_bwd_varlen(ctypes.byref(d), cu, total, *[P(FAKE + i * 0x1000000)
+                                                             for i in range(20)], 1 << 40, None)
+    assert fcall(None, 10) == E_NULL
+    assert bcall(None, 10) == E_NULL
+    assert fcall(P(FAKE + 0x70000002), 10) == E_ALIGN
+    assert fcall(P(FAKE + 0x70000000), 301) == E_SHAPE
+    assert fcall(P(FAKE + 0x70000000), -1) == E_SHAPE
+    assert bcall(P(FAKE + 0x70000000), 301) == E_SHAPE
