@@ -13,7 +13,9 @@ roofline of the dominant kernel, and the fp64 CPU oracle timed on a bounded
 sample of the same workload.
 
 `--decode` times the recurrent decode step instead (N=256, H=16, E=16) and
-prints its own JSON line.
+prints its own JSON line; `--forward NAME` times the inference forward of
+one of the other workloads (sgla_bf16: sGLA B4 H8 T4096 E8; gdn_bf16: GDN,
+same shape; gdn_long_bf16: GDN B1 H16 T65536 E16) with its own JSON line.
 
 Helper modes for the HBM-traffic measurement (run under rocprofv3 --pmc):
   --copy-calibration     a plain fp32 copy kernel of known size
@@ -241,6 +243,58 @@ def decode_bench(steps, warmup):
                      "avg_ms": round(avg_ms, 4)}}), flush=True)
 
 
+def forward_bench(name, steps, warmup):
+    """Inference forward (tla_fwd without `saved`) of a named workload: prep +
+    recurrent forward, bf16 operands, bf16 output, final state returned.
+    MFMA-bound by its algorithmic counts (inputs and outputs only move about
+    1.2-1.6 KB per token-head against 0.56-1.6 MFLOP)."""
+    import torch
+    import paper_2609_36529_amd as tla
+    from paper_2609_36529_amd import synth
+    cfg = synth.CONFIGS[name]
+    inp = synth.make_inputs(cfg)
+    d = {k: (None if v is None else v.cuda()) for k, v in inp.items()}
+    del inp
+    B, T, H, K, V, E, C = cfg.B, cfg.T, cfg.H, cfg.K, cfg.V, cfg.E, cfg.chunk
+    desc = tla.describe(cfg.variant, d["q"], d["v"], d["q2"], C, torch.bfloat16)
+    ws = torch.empty(tla.workspace_bytes(desc, tla.OP_FWD), dtype=torch.uint8, device="cuda")
+    o = torch.empty((B, T, H, V), dtype=torch.bfloat16, device="cuda")
+    sf = torch.empty((B, H, E, K, V), dtype=torch.float32, device="cuda")
+
+    def one():
+        tla.fwd(cfg.variant, d["q"], d["k"], d["v"], d["q2"], d["k2"], d["g"], d["beta"], d["s0"],
+                chunk=C, out_dtype=torch.bfloat16, o=o, s_final=sf, ws=ws)
+    for _ in range(warmup):
+        one()
+    torch.cuda.synchronize()
+    tla.prof_enable(True)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        one()
+    torch.cuda.synchronize()
+    elapsed = (time.perf_counter() - t0) / steps
+    prof = tla.prof_read()
+    tla.prof_enable(False)
+    if cfg.variant == 1:   # GDN: 6KVE + 4CK + 4CV + C^2/3 per token-head
+        flops = 6 * K * V * E + 4 * C * K + 4 * C * V + C * C / 3.0
+    else:                  # sGLA: 4KVE + 2CK + 2CV
+        flops = 4 * K * V * E + 2 * C * K + 2 * C * V
+    th = B * T * H
+    tflops = flops * th / elapsed / 1e12
+    kern = {k: round(v[0] / v[1], 4) for k, v in prof.items() if v[1]}
+    print(json.dumps({
+        "metric": f"forward tokens/s, {name}", "value": round(B * T / elapsed, 1),
+        "unit": "tokens/s", "n_gpus": 1, "steps": steps, "warmup": warmup,
+        "ms_per_step": round(1e3 * elapsed, 4), "higher_is_better": True, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{'GDN' if cfg.variant == 1 else 'sGLA'} inference forward",
+                   "B": B, "T": T, "H": H, "K": K, "V": V, "E": E, "chunk": C, "seed": cfg.seed},
+        "kernels_ms": kern,
+        "roofline": {"bound": "mfma", "achieved": round(tflops, 2), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
+                     "kernel": "prep + fwd_recurrent"}}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -251,6 +305,8 @@ def main():
     ap.add_argument("--pmc-summary", nargs=4, metavar="DIR")
     ap.add_argument("--decode", action="store_true",
                     help="time the decode step instead (its own JSON line)")
+    ap.add_argument("--forward", metavar="NAME",
+                    help="time the inference forward of sgla_bf16, gdn_bf16 or gdn_long_bf16")
     args = ap.parse_args()
     if args.pmc_summary:
         pmc_summary(*args.pmc_summary)
@@ -265,6 +321,9 @@ def main():
         return
     if args.decode:
         decode_bench(args.steps, args.warmup)
+        return
+    if args.forward:
+        forward_bench(args.forward, args.steps, args.warmup)
         return
 
     import torch

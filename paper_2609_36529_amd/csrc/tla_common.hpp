@@ -24,6 +24,8 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef uint16_t bf16_t;  // bf16 storage in global memory
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
 // The wave index, marked uniform (read from the first lane) so that branches
@@ -407,8 +409,6 @@ __device__ __forceinline__ void put4(T* dst, f32x4 x) {
 // Vector stores issued from inline assembly: exactly one instruction each, so
 // a kernel can count them in an explicit vmcnt wait (on gfx9 a store counts
 // in vmcnt until the write is acknowledged, in issue order with the loads).
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ void gstore_b32(void* p, uint32_t x) {
   asm volatile("global_store_dword %0, %1, off" ::"v"(p), "v"(x) : "memory");
 }

@@ -8,7 +8,8 @@
 // registers.  After a fixed-order workgroup reduction it forms
 //   w = beta (v - r)   (GDN)   or   beta v   (sGLA)
 //   o = rho^T Sbar + (q2 . k2)(q . k) w        (= rho^T S_t)
-// and writes S_t = Sbar + kappa w^T back: one read and one write of the state.
+// and writes S_t = Sbar + kappa w^T back: one read and one write of the state,
+// both nontemporal (the state streams through once per step).
 #include "tla_common.hpp"
 #include "tla_internal.hpp"
 
@@ -73,7 +74,7 @@ __global__ __launch_bounds__(NTHR) void k_step(Shape s, FwdIn in, float* state, 
 #pragma unroll
   for (int i = 0; i < RPT; ++i) {
     const int row = rg + NRG * i;
-    st[i] = *(const f32x4*)(base + (size_t)row * V);
+    st[i] = __builtin_nontemporal_load((const f32x4*)(base + (size_t)row * V));
   }
 #pragma unroll
   for (int i = 0; i < RPT; ++i) {
