@@ -409,17 +409,20 @@ __device__ __forceinline__ void put4(T* dst, f32x4 x) {
 // Vector stores issued from inline assembly: exactly one instruction each, so
 // a kernel can count them in an explicit vmcnt wait (on gfx9 a store counts
 // in vmcnt until the write is acknowledged, in issue order with the loads).
+// They carry the nontemporal hint: every use here writes data that only a
+// later kernel reads (checkpoints, saved U and V - W, state gradients), so it
+// should not displace the operands the workgroups of a head share in L2.
 __device__ __forceinline__ void gstore_b32(void* p, uint32_t x) {
-  asm volatile("global_store_dword %0, %1, off" ::"v"(p), "v"(x) : "memory");
+  asm volatile("global_store_dword %0, %1, off nt" ::"v"(p), "v"(x) : "memory");
 }
 __device__ __forceinline__ void gstore_b64(void* p, u32x2 x) {
-  asm volatile("global_store_dwordx2 %0, %1, off" ::"v"(p), "v"(x) : "memory");
+  asm volatile("global_store_dwordx2 %0, %1, off nt" ::"v"(p), "v"(x) : "memory");
 }
 // (a VALU write to the data registers of a store of more than 8 bytes needs
 // one wait state after it; the compiler cannot see that inside the assembly,
 // so the nop is part of it)
 __device__ __forceinline__ void gstore_b128(void* p, u32x4 x) {
-  asm volatile("global_store_dwordx4 %0, %1, off\n\ts_nop 1" ::"v"(p), "v"(x) : "memory");
+  asm volatile("global_store_dwordx4 %0, %1, off nt\n\ts_nop 1" ::"v"(p), "v"(x) : "memory");
 }
 
 // Store a 16 x 16 accumulator tile (lane (g, n) holds rows 4 g + j, column n)
