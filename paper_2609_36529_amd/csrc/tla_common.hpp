@@ -425,14 +425,22 @@ __device__ __forceinline__ void gstore_b128(void* p, u32x4 x) {
   asm volatile("global_store_dwordx4 %0, %1, off nt\n\ts_nop 1" ::"v"(p), "v"(x) : "memory");
 }
 
-// Store a 16 x 16 accumulator tile (lane (g, n) holds rows 4 g + j, column n)
-// into a row-major tile at dst (row r at dst + ld r, ld = 16 by default).  Two DPP
-// exchange rounds transpose 4 x 4 blocks within each quad of lanes, after
-// which lane n holds row 4 g + n % 4, columns 4 (n / 4) .. + 3 and writes
-// them with one 8-byte (bf16) or 16-byte (fp32) store instead of four
-// scalar ones (one store instruction per tile, countable in a vmcnt wait).
-template <typename T>
-__device__ __forceinline__ void store_tile16(T* dst, f32x4 x, int g, int n, int ld = 16) {
+// gfx950 transposing shared-memory read (ds_read_b64_tr_b16).  Within each
+// group of 16 lanes, let row s of a 16 x 4 matrix IN be the four 16-bit
+// elements that lane s of the group reads at its own address p; lane o of the
+// group receives IN[4 j + o / 4][o % 4] as its element j (j = 0..3).  (The
+// lane layout was established on the device with an in-bounds test.)
+__device__ __forceinline__ bf16x4 lds_read_tr16(const void* p) {
+  typedef short v4i16 __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+  const v4i16 r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)const_cast<void*>(p));
+  return __builtin_bit_cast(bf16x4, r);
+}
+
+// 4 x 4 transposes within each quad of lanes by two DPP exchange rounds: a
+// lane (g, n) that holds rows 4 g + j (j = 0..3) of column n of a 16 x 16
+// accumulator tile afterwards holds row 4 g + n % 4, columns 4 (n / 4) + j.
+__device__ __forceinline__ f32x4 quad_transpose(f32x4 x, int n) {
   const int i = n & 3;
   const bool b0 = i & 1, b1 = i & 2;
   float t = dpp_f<0xB1>(b0 ? x[0] : x[1]);  // lanes differing in bit 0
@@ -447,7 +455,18 @@ __device__ __forceinline__ void store_tile16(T* dst, f32x4 x, int g, int n, int 
   t = dpp_f<0x4E>(b1 ? x[1] : x[3]);
   x[1] = b1 ? t : x[1];
   x[3] = b1 ? x[3] : t;
-  T* p = dst + (4 * g + i) * ld + 4 * (n >> 2);
+  return x;
+}
+
+// Store a 16 x 16 accumulator tile (lane (g, n) holds rows 4 g + j, column n)
+// into a row-major tile at dst (row r at dst + ld r, ld = 16 by default) after
+// quad_transpose: one 8-byte (bf16) or 16-byte (fp32) store per lane instead
+// of four scalar ones (one store instruction per tile, countable in a vmcnt
+// wait).
+template <typename T>
+__device__ __forceinline__ void store_tile16(T* dst, f32x4 x, int g, int n, int ld = 16) {
+  x = quad_transpose(x, n);
+  T* p = dst + (4 * g + (n & 3)) * ld + 4 * (n >> 2);
   if constexpr (sizeof(T) == 2)
     gstore_b64(p, __builtin_bit_cast(u32x2, cvt_frag<bf16_t>(x)));
   else

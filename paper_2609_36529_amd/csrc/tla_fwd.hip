@@ -368,7 +368,10 @@ struct FwdSmem {
 //   Tu  Tu (hi, lo)                                         (for the next chunk)
 //   M   M (hi, lo)                                          (for the next chunk)
 //   Kt  K^T and the coefficients c_e                        (for this chunk)
-// Wave w copies the 1 KiB blocks w, w + NW, ... of a tile.  K and Q rows past
+// Wave w copies the 1 KiB blocks w, w + NW, ... of a tile, where w is the
+// wave's index within its group of NW waves (the forward with separate state
+// and output waves has two groups of four, each issuing its own copies).  K
+// and Q rows past
 // T are read from row T - 1 (and zeroed after arrival in the last chunk);
 // M, Tu and K^T come from the prep kernel's operand tiles, whose rows and
 // columns past T are already zero.
@@ -397,13 +400,18 @@ struct FwdDma {
   static constexpr int N_TU = tile_count<decltype(Sm::Tu)>() * (Sm::SPLIT ? 2 : 1);
   static constexpr int N_M = tile_count<decltype(Sm::M)>() * (Sm::SPLIT ? 2 : 1);
   static constexpr int N_KT = tile_count<decltype(Sm::Kt)>() + co_count<NCO2>();
+  static constexpr int N_KC = tile_count<decltype(Sm::K)>() + co_count<NCO01>();
+  static constexpr int N_Q = tile_count<decltype(Sm::Q)>();
+  static_assert((NW & (NW - 1)) == 0, "wave groups of 2^n waves");
+  // index of the calling wave within its group
+  static __device__ __forceinline__ int wid() { return wave_id() & (NW - 1); }
 
   // Fill a swizzled tile; off(r, c) is the byte offset from the wave-uniform
   // base of logical chunk c of row r.
   template <typename Tile, typename F>
   static __device__ __forceinline__ void tile(Tile& t, const void* base, F off) {
     constexpr int NB = (Tile::NCHK + 63) / 64;
-    const int w = wave_id(), l = lane_id();
+    const int w = wid(), l = lane_id();
     const uint32_t lds = lds_addr(t.d);
 #pragma unroll
     for (int i = 0; i * NW < NB; ++i) {
@@ -419,7 +427,7 @@ struct FwdDma {
   template <int NBYTES>
   static __device__ __forceinline__ void copy(void* dst, const void* src) {
     constexpr int SZ = co_size<NBYTES>(), NB = (NBYTES + 64 * SZ - 1) / (64 * SZ);
-    const int w = wave_id(), l = lane_id();
+    const int w = wid(), l = lane_id();
     const uint32_t lds = lds_addr(dst);
 #pragma unroll
     for (int i = 0; i * NW < NB; ++i) {
@@ -446,6 +454,23 @@ struct FwdDma {
     tile(sm.K, Kg + (size_t)t0 * krs, off);
     if constexpr (Sm::STAGE_Q) tile(sm.Q, Qg + (size_t)t0 * krs, off);
     copy<NCO01>(&sm.coef01[0][0][0], p.coef + ch * 3 * E * C);
+  }
+  // K rows with a_e, b_e (N_KC copies) and Q rows (N_Q copies) separately
+  static __device__ __forceinline__ void kc(Sm& sm, const Shape& s, const PrepBufs& p, const T* Kg,
+                                            size_t ch, int t0) {
+    const size_t krs = (size_t)s.H * KD;
+    const int last = s.T - 1 - t0;
+    tile(sm.K, Kg + (size_t)t0 * krs, [=](int r, int c) {
+      return (uint32_t)(sizeof(T) * ((size_t)min(r, last) * krs + Sm::EC * c));
+    });
+    copy<NCO01>(&sm.coef01[0][0][0], p.coef + ch * 3 * E * C);
+  }
+  static __device__ __forceinline__ void q(Sm& sm, const Shape& s, const T* Qg, int t0) {
+    const size_t krs = (size_t)s.H * KD;
+    const int last = s.T - 1 - t0;
+    tile(sm.Q, Qg + (size_t)t0 * krs, [=](int r, int c) {
+      return (uint32_t)(sizeof(T) * ((size_t)min(r, last) * krs + Sm::EC * c));
+    });
   }
   static __device__ __forceinline__ void tu(Sm& sm, const PrepBufs& p, size_t ch) {
     const T* ops = (const T*)p.ops + ch * OT::STRIDE;
@@ -477,7 +502,7 @@ struct FwdDma {
   static constexpr int VL = C * PPR / NW;                // lanes per wave
   static_assert(C * PPR % NW == 0 && VL <= 64, "V tile split over the waves");
   static __device__ __forceinline__ void v(Sm& sm, const T* Vg, size_t vrs, int last) {
-    const int w = wave_id(), l = lane_id();
+    const int w = wid(), l = lane_id();
     const int q = w * VL + l, pos = q / PPR, part = q % PPR;
     const int r = (pos & ~15) + 4 * (pos & 3) + ((pos >> 2) & 3);  // row held at position pos
     const uint32_t off = (uint32_t)(sizeof(T) * (size_t)min(r, last) * vrs) + 16 * part;
@@ -487,7 +512,7 @@ struct FwdDma {
   // bg points at the beta of row t0 (row stride H)
   static constexpr int BL = C / NW;
   static __device__ __forceinline__ void beta(Sm& sm, const float* bg, int H, int last) {
-    const int w = wave_id(), l = lane_id();
+    const int w = wid(), l = lane_id();
     const uint32_t off = (uint32_t)(4 * (size_t)min(w * BL + l, last) * H);
     if (l < BL) lds_dma<4>(bg, off, lds_addr(&sm.beta[0]) + 4 * w * BL);
   }
@@ -976,6 +1001,454 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
   }
 }
 
+// ------------------------------------------- forward with state and output waves
+// The same chunk step on eight waves in two roles.  Waves 0..3 (state waves)
+// own E/4 slices of the state each, in fp32 registers, and run only what the
+// next chunk waits for: their partial of W = sum_e diag(a_e) K S_e, U
+// (Tu (V - W) for GDN, diag(beta) V for sGLA) and the update
+// S_e <- gamma^C_e S_e + K^T diag(c_e) U of the chunkwise form (Section 3).
+// After each update they leave the bf16 operand copy of the new state in
+// shared memory.  Waves 4..7 (output waves; wave 4 + i shares a SIMD with
+// state wave i) take it from there and form the chunk's output rows,
+// sum_e diag(b_e) Q S_e + M U, and its checkpoint, in the shadow of the
+// state waves' work.  Three barriers divide a chunk step:
+//   B0 .. B1  state: K S_e, W partials          output: Q S_e partials
+//   B1 .. B2  state: U, one row tile per wave   output: rows of V - W
+//   B2 .. B0  state: the update                 output: O rows (partials + M U)
+// The output waves issue every global store (checkpoint, U, V - W, O).
+// The state waves issue and await every copy into shared memory (also Q and
+// M, which only the output waves read), and the output waves never wait for
+// memory: a wave's vmcnt wait for a copy also waits for the stores it issued
+// before the copy, which under the write traffic of all workgroups take
+// thousands of cycles to be acknowledged.
+template <typename T, int KD, int C, int E>
+struct DualSmem {
+  FwdSmem<T, KD, C, E, 4> f;
+  // bf16 operand copy of the chunk-start state: [slice][key tile][lane], each
+  // lane's entry as the state wave's lane holds it in registers
+  alignas(16) typename Elem<T>::frag sop[E][KD / 16][64];
+};
+
+template <typename T, int KD, int C, int E>
+__global__ __launch_bounds__(512) void k_fwd_dual(Shape s, FwdIn in, PrepBufs p, void* out,
+                                                  float* s_final, SavedBufs sv, int train) {
+  constexpr int NG = 4;  // waves per role
+  constexpr int SPW = E / NG;
+  constexpr int NT = C / 16;
+  constexpr int KT = KD / 16;
+  constexpr int NTHR = 2 * NG * 64;
+  static_assert(E % NG == 0 && sizeof(T) == 2, "bf16 operands, whole slices per wave");
+  typedef typename Elem<T>::frag F;
+  typedef FwdSmem<T, KD, C, E, NG> Sm;
+  typedef FwdDma<T, KD, C, E, NG> Dma;
+  static_assert(Sm::STAGE_Q && Sm::SPLIT, "queries staged, Tu and M as hi + lo pairs");
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  DualSmem<T, KD, C, E>& smd = *reinterpret_cast<DualSmem<T, KD, C, E>*>(smem_raw);
+  Sm& sm = smd.f;
+
+  const int wv = wave_id(), w = wv & (NG - 1), l = lane_id(), g = l >> 4, n = l & 15;
+  const int V = s.V;
+  int head, vt;
+  xcd_map(blockIdx.x, s.NH, V / 16, head, vt);
+  const int b = head / s.H, h = head % s.H;
+  const int v0 = vt * 16;
+  const size_t tok0 = seq_begin(s, b);
+  s.T = seq_len(s, b);                 // this sequence's length from here on
+  const int nc = (s.T + C - 1) / C;    // its chunks (s.Nc: the per-head stride)
+
+  const T* Kg = (const T*)in.k + (tok0 * s.H + h) * KD;
+  const T* Qg = (const T*)in.q + (tok0 * s.H + h) * KD;
+  const T* Vg = (const T*)in.v + (tok0 * s.H + h) * (size_t)V + v0;
+  const size_t ch0 = (size_t)head * s.Nc;
+  const size_t vrs = (size_t)s.H * V;
+  const bool sbeta = s.variant == 0 && in.beta != nullptr;  // beta copied per chunk
+  const float* bg = in.beta ? in.beta + tok0 * s.H + h : nullptr;
+  if (s.variant == 0 && !in.beta)
+    for (int r = threadIdx.x; r < C; r += NTHR) sm.beta[r] = 1.f;
+
+  // Rows past T of the last, partial chunk: every copy of both roles has
+  // landed, then the K, Q and V rows are zeroed (run by all waves).
+  auto zero_tail = [&](int t0) {
+    wait_vmcnt<0>();
+    __syncthreads();
+    zero_rows_from(sm.K, s.T - t0, NTHR);
+    zero_rows_from(sm.Q, s.T - t0, NTHR);
+    for (int pos = threadIdx.x; pos < C; pos += NTHR) {
+      const int r = (pos & ~15) + 4 * (pos & 3) + ((pos >> 2) & 3);
+      if (t0 + r >= s.T)
+        for (int c = 0; c < 16; ++c) sm.Vr[pos][c] = T(0);
+    }
+    __syncthreads();
+  };
+
+  // X S_e for the wave's slices (X: the chunk's K or Q rows), folded with the
+  // coefficient vectors cf[e] (a_e or b_e) into the wave's partial dst[rt][l].
+  // The fragments of the next k-block pair are read before the MFMAs of the
+  // current one.
+  auto state_pass = [&](const decltype(sm.K)& X, const F(&So)[SPW][KT], const float(*cf)[C],
+                        f32x4(*dst)[64]) {
+    f32x4 P[SPW][NT];
+#pragma unroll
+    for (int i = 0; i < SPW; ++i)
+#pragma unroll
+      for (int rt = 0; rt < NT; ++rt) P[i][rt] = zero4();
+    if constexpr (KT > 1) {
+      constexpr int NS = KT / 2;
+      auto load = [&](int j, Frag8<T>(&a)[NT]) {
+#pragma unroll
+        for (int rt = 0; rt < NT; ++rt) a[rt].v = *(const bf16x8*)X.at(16 * rt + n, key_col<KD>(2 * j, g));
+      };
+      Frag8<T> a[NT];
+      load(0, a);
+#pragma unroll
+      for (int j = 0; j < NS; ++j) {
+        Frag8<T> bn[NT];
+        if (j + 1 < NS) load(j + 1, bn);
+#pragma unroll
+        for (int i = 0; i < SPW; ++i)
+#pragma unroll
+          for (int rt = 0; rt < NT; ++rt) mma32(P[i][rt], a[rt], So[i][2 * j], So[i][2 * j + 1]);
+        if (j + 1 < NS) {
+#pragma unroll
+          for (int rt = 0; rt < NT; ++rt) a[rt] = bn[rt];
+        }
+      }
+    } else {
+      F a[NT];
+#pragma unroll
+      for (int rt = 0; rt < NT; ++rt) a[rt] = ld_frag(X.at(16 * rt + n, 4 * g));
+#pragma unroll
+      for (int i = 0; i < SPW; ++i)
+#pragma unroll
+        for (int rt = 0; rt < NT; ++rt) mma16(P[i][rt], a[rt], So[i][0]);
+    }
+#pragma unroll
+    for (int rt = 0; rt < NT; ++rt) {
+      f32x4 acc = zero4();
+#pragma unroll
+      for (int i = 0; i < SPW; ++i) acc += *(const f32x4*)&cf[w * SPW + i][16 * rt + 4 * g] * P[i][rt];
+      dst[rt][l] = acc;
+    }
+  };
+
+  // The checkpoint (the chunk-start state for the backward,
+  // [ch][E][V/16][K][16]) of the slices of wave w goes out in NPC pieces of
+  // one 16-byte store per lane.  A piece is a pair of key tiles (1 KiB): lane
+  // o = 16 grp + 4 q + r writes row 4 grp + r of tile q / 2 of the pair,
+  // columns 8 (q & 1) .. + 7, which two transposing reads of the
+  // register-order copy give it (as source, lane 16 grp + 4 j + q reads
+  // state-wave lane 16 grp + 8 (q & 1) + j, and + 4, of tile q / 2).  With an
+  // odd number of key tiles a piece is one tile, transposed on the matrix
+  // cores.
+  constexpr bool PAIRS = KT % 2 == 0;
+  constexpr int NPC = PAIRS ? SPW * KT / 2 : SPW * KT;
+  constexpr int KH = PAIRS ? KT / 2 : 1;  // key tile pairs
+  // data of piece pc, read from the copy of the chunk-start state
+  auto piece_read = [&](int pc) -> u32x4 {
+    const int sq = l & 3, e = w * SPW + pc / KH, kt = 2 * (pc % KH) + (sq >> 1);
+    const F* src = &smd.sop[e][kt][16 * (l >> 4) + 8 * (sq & 1) + ((l & 15) >> 2)];
+    const bf16x4 a = lds_read_tr16(src), b = lds_read_tr16(src + 4);
+    return __builtin_bit_cast(u32x4, __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7));
+  };
+  auto piece_store = [&](size_t ch, int pc, u32x4 d) {
+    const int oq = (l & 15) >> 2, i = pc / KH, kt = 2 * (pc % KH) + (oq >> 1);
+    T* dst = (T*)sv.Sck + ((ch * E + w * SPW + i) * (size_t)(V / 16) + vt) * KD * 16;
+    gstore_b128(dst + 256 * kt + 16 * (4 * (l >> 4) + (l & 3)) + 8 * (oq & 1), d);
+  };
+
+  if (wv < NG) {
+    // ================================================= state waves
+    // S[i][kt] = S_e[key_col(kt, g) + j][v0 + n], e = w SPW + i
+    f32x4 S[SPW][KT];
+    F Sop[SPW][KT];
+#pragma unroll
+    for (int i = 0; i < SPW; ++i) {
+      const int e = w * SPW + i;
+#pragma unroll
+      for (int kt = 0; kt < KT; ++kt) {
+        f32x4 x = zero4();
+        if (in.s0) {
+          const float* src = in.s0 + (((size_t)head * E + e) * KD + key_col<KD>(kt, g)) * V + v0 + n;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) x[j] = src[(size_t)j * V];
+        }
+        S[i][kt] = x;
+        Sop[i][kt] = cvt_frag<T>(x);
+        smd.sop[e][kt][l] = Sop[i][kt];
+      }
+    }
+    if (nc > 0) {
+      Dma::kc(sm, s, p, Kg, ch0, 0);
+      Dma::q(sm, s, Qg, 0);
+      Dma::tu(sm, p, ch0);
+      Dma::v(sm, Vg, vrs, s.T - 1);
+      if (sbeta) Dma::beta(sm, bg, s.H, s.T - 1);
+      wait_vmcnt_rt(Dma::N_TU + 1 + (sbeta ? 1 : 0));  // K, Q, a_e, b_e have landed
+    }
+
+    for (int ci = 0; ci < nc; ++ci) {
+      const int t0 = ci * C;
+      const size_t ch = ch0 + ci;
+      const bool more = ci + 1 < nc;
+      __syncthreads();  // B0
+      if (t0 + C > s.T) zero_tail(t0);
+      Dma::kt(sm, p, ch);
+      Dma::gc(sm, p, ch);
+      Dma::m(sm, p, ch);
+
+      // ---- W partial: sum over the wave's slices of diag(a_e) K S_e
+      state_pass(sm.K, Sop, sm.coef01[0], sm.W[w]);
+      wait_vmcnt<Dma::N_KT + 1 + Dma::N_M>();  // this chunk's Tu, V and beta have landed
+      __syncthreads();  // B1
+      if (more) {  // K, Q, a_e and b_e are free
+        Dma::kc(sm, s, p, Kg, ch + 1, t0 + C);
+        Dma::q(sm, s, Qg, t0 + C);
+      }
+
+      // ---- U for row tile w: Tu (V - W) (GDN) or diag(beta) V (sGLA).  Every
+      // block kb of the row is formed (Tu is zero right of the diagonal), so no
+      // branch separates the shared-memory reads.
+      if (w < NT) {
+        const int rt = w;
+        f32x4 u;
+        if (s.variant == 1) {
+          const int r = 16 * rt + n;
+          f32x4 xr[NT], wq[NG][NT];
+          F th[NT], tl[NT];
+          T vr[NT][4];
+#pragma unroll
+          for (int kb = 0; kb < NT; ++kb) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) vr[kb][j] = sm.Vr[16 * kb + 4 * j + g][n];
+#pragma unroll
+            for (int ww = 0; ww < NG; ++ww) wq[ww][kb] = sm.W[ww][kb][l];
+            th[kb] = ld_frag(sm.Tu.at(r, 16 * kb + 4 * g));
+            tl[kb] = ld_frag(sm.TuL.at(r, 16 * kb + 4 * g));
+          }
+          __builtin_amdgcn_sched_barrier(0);  // the reads above stay together
+#pragma unroll
+          for (int kb = 0; kb < NT; ++kb) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) xr[kb][j] = Elem<T>::to_f(vr[kb][j]);
+#pragma unroll
+            for (int ww = 0; ww < NG; ++ww) xr[kb] -= wq[ww][kb];
+          }
+          F Xh[NT], Xl[NT];
+#pragma unroll
+          for (int kb = 0; kb < NT; ++kb) split_frag(xr[kb], Xh[kb], Xl[kb]);
+          u = zero4();
+#pragma unroll
+          for (int kb = 0; kb < NT; kb += (NT > 1 ? 2 : 1)) {
+            if constexpr (NT > 1) {
+              mma32(u, th[kb], th[kb + 1], Xh[kb], Xh[kb + 1]);
+              mma32(u, th[kb], th[kb + 1], Xl[kb], Xl[kb + 1]);
+              mma32(u, tl[kb], tl[kb + 1], Xh[kb], Xh[kb + 1]);
+            } else {
+              mma16(u, th[0], Xh[0]);
+              mma16(u, th[0], Xl[0]);
+              mma16(u, tl[0], Xh[0]);
+            }
+          }
+        } else {
+          f32x4 x;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) x[j] = Elem<T>::to_f(sm.Vr[16 * rt + 4 * j + g][n]);
+          u = x * *(const f32x4*)&sm.beta[16 * rt + 4 * g];
+        }
+        sm.Us[rt][l] = u;
+      }
+      wait_vmcnt_rt(more ? Dma::N_KC + Dma::N_Q : 0);  // K^T, c_e, gamma^C and M have landed
+      __syncthreads();  // B2
+      if (more) {  // Tu, the V tile and beta are free
+        Dma::tu(sm, p, ch + 1);
+        Dma::v(sm, Vg + (size_t)(t0 + C) * vrs, vrs, s.T - 1 - (t0 + C));
+        if (sbeta) Dma::beta(sm, bg + (size_t)(t0 + C) * s.H, s.H, s.T - 1 - (t0 + C));
+      }
+
+      // ---- update S_e <- gamma^C_e S_e + K^T diag(c_e) U
+      f32x4 U[NT];
+#pragma unroll
+      for (int rt = 0; rt < NT; ++rt) U[rt] = sm.Us[rt][l];
+      F Uc[SPW][NT], Ucl[SPW][NT];
+#pragma unroll
+      for (int i = 0; i < SPW; ++i) {
+        const int e = w * SPW + i;
+        const float gc = sm.gC[e];
+#pragma unroll
+        for (int kt = 0; kt < KT; ++kt) S[i][kt] *= gc;
+#pragma unroll
+        for (int kb = 0; kb < NT; ++kb)
+          split_frag(U[kb] * *(const f32x4*)&sm.coef2[e][16 * kb + 4 * g], Uc[i][kb], Ucl[i][kb]);
+      }
+#pragma unroll
+      for (int kb = 0; kb < NT; kb += (NT > 1 ? 2 : 1)) {
+        if constexpr (NT > 1) {
+          // K^T rows: positions 4 g + j and 16 + 4 g + j of the block pair are
+          // adjacent in the operand tile (one 16-byte read per lane)
+          Frag8<T> a[KT];
+          const int c = key_of_row<C>(16 * kb + 4 * g);
+#pragma unroll
+          for (int kt = 0; kt < KT; ++kt) a[kt].v = *(const bf16x8*)sm.Kt.at(16 * kt + n, c);
+#pragma unroll
+          for (int i = 0; i < SPW; ++i) {
+#pragma unroll
+            for (int kt = 0; kt < KT; ++kt) mma32(S[i][kt], a[kt], Uc[i][kb], Uc[i][kb + 1]);
+#pragma unroll
+            for (int kt = 0; kt < KT; ++kt) mma32(S[i][kt], a[kt], Ucl[i][kb], Ucl[i][kb + 1]);
+          }
+        } else {
+          F a[KT];
+#pragma unroll
+          for (int kt = 0; kt < KT; ++kt) a[kt] = ld_frag(sm.Kt.at(16 * kt + n, 4 * g));
+#pragma unroll
+          for (int i = 0; i < SPW; ++i)
+#pragma unroll
+            for (int kt = 0; kt < KT; ++kt) {
+              mma16(S[i][kt], a[kt], Uc[i][0]);
+              mma16(S[i][kt], a[kt], Ucl[i][0]);
+            }
+        }
+      }
+      // the next chunk-start state's operand copy, kept in registers for the
+      // next W partial and left in shared memory for the output waves
+#pragma unroll
+      for (int i = 0; i < SPW; ++i)
+#pragma unroll
+        for (int kt = 0; kt < KT; ++kt) {
+          Sop[i][kt] = cvt_frag<T>(S[i][kt]);
+          smd.sop[w * SPW + i][kt][l] = Sop[i][kt];
+        }
+      // K, Q, a_e and b_e of the next chunk have landed (the Tu, V and beta
+      // copies were issued after them)
+      if (more) wait_vmcnt_rt(Dma::N_TU + 1 + (sbeta ? 1 : 0));
+    }
+
+    if (s_final) {
+#pragma unroll
+      for (int i = 0; i < SPW; ++i) {
+        const int e = w * SPW + i;
+#pragma unroll
+        for (int kt = 0; kt < KT; ++kt) {
+          float* dst = s_final + (((size_t)head * E + e) * KD + key_col<KD>(kt, g)) * V + v0 + n;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) dst[(size_t)j * V] = S[i][kt][j];
+        }
+      }
+    }
+  } else {
+    // ================================================= output waves
+    const bf16x4 idf = identity_frag();  // for the transposing checkpoint stores
+    // Every global store of the forward is issued here.  Under the write
+    // traffic of all workgroups a store instruction holds up the wave that
+    // issues it for some hundreds of cycles, whatever its size (measured;
+    // the state waves would lose the same time), so the stores are 16-byte
+    // ones and few (11 per chunk step at E = 8), none in the Q pass (which
+    // the state waves wait for at B1), and most between B1 and B2, where the
+    // output waves have no other work: checkpoint pieces [0, NB) and the rows
+    // of V - W (GDN, while V and the W partials are in shared memory); the
+    // other pieces, U and the output rows after B2.
+    constexpr int NB = (5 * NPC + 4) / 8;
+    const bool rows = w < NT;  // the wave owns row tile w
+    for (int ci = 0; ci < nc; ++ci) {
+      const int t0 = ci * C;
+      const size_t ch = ch0 + ci;
+      const bool more = ci + 1 < nc;
+      __syncthreads();  // B0
+      if (t0 + C > s.T) zero_tail(t0);
+
+      // ---- the chunk-start state of the wave's slices, then the O partial
+      // sum over them of diag(b_e) Q S_e
+      F So[SPW][KT];
+#pragma unroll
+      for (int i = 0; i < SPW; ++i)
+#pragma unroll
+        for (int kt = 0; kt < KT; ++kt) So[i][kt] = smd.sop[w * SPW + i][kt][l];
+      u32x4 ckd[PAIRS ? NPC : 1];  // the pieces' data (filled after B1)
+      auto ck_store = [&](int pc) {
+        if constexpr (PAIRS) {
+          piece_store(ch, pc, ckd[pc]);
+        } else {
+          const int i = pc / KT, kt = pc % KT;
+          T* dst = (T*)sv.Sck + ((ch * E + w * SPW + i) * (size_t)(V / 16) + vt) * KD * 16;
+          store_tile16_frag(dst + 256 * kt, So[i][kt], idf, g, n);
+        }
+      };
+      state_pass(sm.Q, So, sm.coef01[1], sm.O[w]);
+      __syncthreads();  // B1
+      // the checkpoint pieces, read before the state waves replace the copy
+      // after B2
+      if (PAIRS && train) {
+#pragma unroll
+        for (int pc = 0; pc < NPC; ++pc) ckd[pc] = piece_read(pc);
+      }
+      if (train && rows && s.variant == 1) {  // rows of V - W of row tile w, as the state waves form them
+        const int rt = w;
+        T vr[4];
+        f32x4 wq[NG];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) vr[j] = sm.Vr[16 * rt + 4 * j + g][n];
+#pragma unroll
+        for (int ww = 0; ww < NG; ++ww) wq[ww] = sm.W[ww][rt][l];
+        f32x4 x;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) x[j] = Elem<T>::to_f(vr[j]);
+#pragma unroll
+        for (int ww = 0; ww < NG; ++ww) x -= wq[ww];
+        store_tile16(sv.X + ch * C * (size_t)V + (size_t)(16 * rt) * V + v0, x, g, n, V);
+      }
+      if (train) {
+#pragma unroll
+        for (int pc = 0; pc < NB; ++pc) ck_store(pc);
+      }
+      __syncthreads();  // B2
+
+      // ---- O for row tile w: the partials plus M U
+      if (w < NT) {
+        const int rt = w;
+        const int r = 16 * rt + n;
+        F mf[NT], ml[NT], Uh[NT], Ul[NT];
+        f32x4 U[NT], op[NG];
+#pragma unroll
+        for (int kb = 0; kb < NT; ++kb) {
+          mf[kb] = ld_frag(sm.M.at(r, 16 * kb + 4 * g));
+          ml[kb] = ld_frag(sm.ML.at(r, 16 * kb + 4 * g));
+          U[kb] = sm.Us[kb][l];
+        }
+#pragma unroll
+        for (int ww = 0; ww < NG; ++ww) op[ww] = sm.O[ww][rt][l];
+        __builtin_amdgcn_sched_barrier(0);  // the reads above stay together
+#pragma unroll
+        for (int kb = 0; kb < NT; ++kb) split_frag(U[kb], Uh[kb], Ul[kb]);
+        f32x4 oacc = zero4();
+#pragma unroll
+        for (int ww = 0; ww < NG; ++ww) oacc += op[ww];
+        mma_k<C>(oacc, [&](int kb) { return mf[kb]; }, [&](int kb) { return Uh[kb]; });
+        mma_k<C>(oacc, [&](int kb) { return mf[kb]; }, [&](int kb) { return Ul[kb]; });
+        mma_k<C>(oacc, [&](int kb) { return ml[kb]; }, [&](int kb) { return Uh[kb]; });
+        if (train) {
+#pragma unroll
+          for (int pc = NB; pc < NPC; ++pc) ck_store(pc);
+          store_tile16(sv.U + ch * C * (size_t)V + (size_t)(16 * rt) * V + v0, U[rt], g, n, V);
+        }
+        // output rows: lane (g, n) writes row 16 rt + 4 g + n % 4, columns
+        // 4 (n / 4) .. + 3
+        const f32x4 y = quad_transpose(oacc, n);
+        const int t = t0 + 16 * rt + 4 * g + (n & 3);
+        if (t < s.T) {
+          const size_t off = ((tok0 + t) * s.H + h) * (size_t)V + v0 + 4 * (n >> 2);
+          if (s.out_bf16)
+            *(bf16x4*)((bf16_t*)out + off) = cvt_frag<bf16_t>(y);
+          else
+            *(f32x4*)((float*)out + off) = y;
+        }
+      } else if (train) {
+#pragma unroll
+        for (int pc = NB; pc < NPC; ++pc) ck_store(pc);
+      }
+    }
+  }
+}
+
 // ---------------------------------------------------------------- launchers
 // Eight waves (two per SIMD) for E = 16, whose state does not fit four waves'
 // registers; four waves otherwise (measured faster at E = 8).
@@ -994,9 +1467,32 @@ static hipError_t prep_inst(const Shape& s, const FwdIn& in, const PrepBufs& p, 
   return hipGetLastError();
 }
 
+// The forward with separate state and output waves serves bf16 operands with
+// E = 4 or 8 slices; E = 16 (whose state would not fit the registers of four
+// waves that share their SIMDs with four more) and fp32 operands (whose tiles
+// would not fit the shared memory) keep the single-role kernel.
+template <typename T, int KD, int C, int E>
+constexpr bool fwd_dual() {
+  return sizeof(T) == 2 && E % 4 == 0 && E <= 8 && FwdSmem<T, KD, C, E, 4>::STAGE_Q &&
+         sizeof(DualSmem<T, KD, C, E>) <= 160 * 1024;
+}
+
 template <typename T, int KD, int C, int E>
 static hipError_t fwd_inst(const Shape& s, const FwdIn& in, const PrepBufs& p, void* o,
                            float* s_final, const SavedBufs* sv, hipStream_t st) {
+  SavedBufs none{nullptr, nullptr, nullptr};
+  if constexpr (fwd_dual<T, KD, C, E>()) {
+    const size_t smem = sizeof(DualSmem<T, KD, C, E>);
+    static bool attr_set = false;
+    if (!attr_set) {
+      (void)hipFuncSetAttribute((const void*)k_fwd_dual<T, KD, C, E>,
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+      attr_set = true;
+    }
+    hipLaunchKernelGGL((k_fwd_dual<T, KD, C, E>), dim3(s.NH * (s.V / 16)), dim3(512), smem, st, s,
+                       in, p, o, s_final, sv ? *sv : none, sv ? 1 : 0);
+    return hipGetLastError();
+  }
   constexpr int NW = fwd_waves<T, E>();
   typedef FwdSmem<T, KD, C, E, NW> Sm;
   const size_t smem = sizeof(Sm);
@@ -1006,7 +1502,6 @@ static hipError_t fwd_inst(const Shape& s, const FwdIn& in, const PrepBufs& p, v
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     attr_set = true;
   }
-  SavedBufs none{nullptr, nullptr, nullptr};
   hipLaunchKernelGGL((k_fwd<T, KD, C, E, NW>), dim3(s.NH * (s.V / 16)), dim3(NW * 64), smem, st,
                      s, in, p, o, s_final, sv ? *sv : none, sv ? 1 : 0);
   return hipGetLastError();
