@@ -421,9 +421,9 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
       split_frag(acc, hi, lo);
       sm.dUs[0][rt][l] = hi;
       if constexpr (Sm::SPLIT) sm.dUs[1][rt][l] = lo;
-      float* du = bb.dU + ch * C * (size_t)V + (size_t)(16 * rt + 4 * g) * V + v0 + n;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) du[(size_t)j * V] = acc[j];
+      // (one 16-byte store per lane: a store instruction holds up the wave
+      // for hundreds of cycles under the write traffic of all workgroups)
+      store_tile16(bb.dU + ch * C * (size_t)V + (size_t)(16 * rt) * V + v0, acc, g, n, V);
     }
     __syncthreads();
     if (w < NT) {
@@ -441,9 +441,7 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
         acc = -acc;
         sm.dWs[rt][l] = acc;
       }
-      float* dw = bb.dW + ch * C * (size_t)V + (size_t)(16 * rt + 4 * g) * V + v0 + n;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) dw[(size_t)j * V] = acc[j];
+      store_tile16(bb.dW + ch * C * (size_t)V + (size_t)(16 * rt) * V + v0, acc, g, n, V);
     }
     f32x4 dW[NT];
     if (s.variant == 1) {
