@@ -531,6 +531,16 @@ __device__ __forceinline__ void store_tile16_frag(bf16_t* dst, bf16x4 x, bf16x4 
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)p);
 }
+// A pointer that the caller knows to be the same in every lane, moved to
+// scalar registers (the base of a direct copy must be there; the compiler
+// cannot always prove that a pointer built from loaded values is uniform).
+template <typename P>
+__device__ __forceinline__ P* uniform_ptr(P* p) {
+  const uint64_t x = (uint64_t)(uintptr_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(x >> 32));
+  return (P*)(uintptr_t)(((uint64_t)hi << 32) | lo);
+}
 // (M0 is written inside the assembly and declared clobbered; the compiler
 // warns that it reserves M0, which none of these kernels otherwise use)
 #pragma clang diagnostic push
@@ -578,6 +588,81 @@ constexpr int dma_min_count() {
   return c;
 }
 
+// Direct copies of whole tiles and byte ranges into shared memory by a group
+// of NW waves: wave w of the group copies the 64-lane blocks w, w + NW, ...
+// (1 KiB for tiles).  The *_count functions give the copies each wave issues
+// at least (for vmcnt waits: a wave that issues more only waits longer).
+template <int NW>
+struct GroupDma {
+  // The lane index, recomputed at every use: the per-lane offsets of the
+  // copies are the same in every chunk step, and hoisted out of a kernel's
+  // chunk loop they would hold dozens of registers for its whole length.
+  static __device__ __forceinline__ int lane() {
+    int x;
+    asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(x));
+    return x;
+  }
+  // a coefficient copy uses 16-byte lanes when its 1 KiB blocks split evenly
+  // over the waves, else 4-byte lanes when those do
+  template <int NBYTES>
+  static constexpr int co_size() {
+    return (NBYTES % (1024 * NW) == 0) ? 16 : (NBYTES % (256 * NW) == 0) ? 4 : 16;
+  }
+  template <int NBYTES>
+  static constexpr int co_count() {
+    constexpr int SZ = co_size<NBYTES>();
+    return dma_min_count<(NBYTES + 64 * SZ - 1) / (64 * SZ), NW>();
+  }
+  template <typename Tile>
+  static constexpr int tile_count() {
+    return dma_min_count<(Tile::NCHK + 63) / 64, NW>();
+  }
+  static_assert((NW & (NW - 1)) == 0, "wave groups of 2^n waves");
+  // index of the calling wave within its group
+  static __device__ __forceinline__ int wid() { return wave_id() & (NW - 1); }
+
+  // Fill a swizzled tile; off(r, c) is the byte offset from the wave-uniform
+  // base of logical chunk c of row r.
+  template <typename Tile, typename F>
+  static __device__ __forceinline__ void tile(Tile& t, const void* base_, F off) {
+    constexpr int NB = (Tile::NCHK + 63) / 64;
+    const int w = wid(), l = lane();
+    const uint32_t lds = lds_addr(t.d);
+    const void* base = uniform_ptr(base_);
+#pragma unroll
+    for (int i = 0; i * NW < NB; ++i) {
+      const int blk = i * NW + w;
+      if (NB % NW != 0 && blk >= NB) continue;  // wave-uniform
+      int r, c;
+      Tile::logical(64 * blk + l, r, c);
+      if (Tile::NCHK % 64 == 0 || 64 * blk + l < Tile::NCHK)
+        lds_dma<16>(base, off(r, c), lds + 1024 * blk);
+    }
+  }
+  // A plain copy of NBYTES contiguous bytes.
+  template <int NBYTES>
+  static __device__ __forceinline__ void copy(void* dst, const void* src_) {
+    constexpr int SZ = co_size<NBYTES>(), NB = (NBYTES + 64 * SZ - 1) / (64 * SZ);
+    const int w = wid(), l = lane();
+    const uint32_t lds = lds_addr(dst);
+    const void* src = uniform_ptr(src_);
+#pragma unroll
+    for (int i = 0; i * NW < NB; ++i) {
+      const int blk = i * NW + w;
+      if (NB % NW != 0 && blk >= NB) continue;
+      const uint32_t off = 64 * SZ * blk + SZ * l;
+      if (NBYTES % (64 * SZ) == 0 || off < (uint32_t)NBYTES)
+        lds_dma<SZ>(src, off, lds + 64 * SZ * blk);
+    }
+  }
+  // a tile whose rows are stored row-major, RW elements apart, at src
+  template <int RW, typename Tile, typename T>
+  static __device__ __forceinline__ void op_tile(Tile& t, const T* src) {
+    tile(t, src, [](int r, int c) { return (uint32_t)(sizeof(T) * (r * RW + Tile::EC * c)); });
+  }
+
+};
+
 // Unpadded LDS tile of R rows x COLS elements in 16-byte chunks.  Within row
 // r the chunk index is XOR-ed with sw(r), so that 16 consecutive rows read at
 // the same columns touch 16 distinct chunk positions (fragment reads of a
@@ -602,6 +687,14 @@ struct SwzTile {
     c = (p % NCH) ^ sw(r);
   }
 };
+
+// Rows past T of a row tile (the last, partial chunk): zero them after the
+// direct copies have landed.
+template <typename Tile>
+__device__ __forceinline__ void zero_rows_from(Tile& t, int r0, int nthr) {
+  for (int p = threadIdx.x; p < Tile::NCHK; p += nthr)
+    if (p / Tile::NCH >= r0) *(uint4*)((char*)t.d + 16 * p) = make_uint4(0, 0, 0, 0);
+}
 
 // XCD-aware block mapping: the 8 accelerator dies each have their own L2 and
 // receive blocks round-robin by linear id.  Blocks that share a head (the

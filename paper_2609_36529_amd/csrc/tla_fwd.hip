@@ -376,25 +376,25 @@ struct FwdSmem {
 // M, Tu and K^T come from the prep kernel's operand tiles, whose rows and
 // columns past T are already zero.
 template <typename T, int KD, int C, int E, int NW>
-struct FwdDma {
+struct FwdDma : GroupDma<NW> {
+  typedef GroupDma<NW> G;
   typedef FwdSmem<T, KD, C, E, NW> Sm;
   typedef OpTiles<T, KD, C> OT;
-  static constexpr int NCO01 = 2 * E * C * 4, NCO2 = E * C * 4;  // bytes
-  // a coefficient copy uses 16-byte lanes when its 1 KiB blocks split evenly
-  // over the waves, else 4-byte lanes when those do
+  using G::tile;
+  using G::wid;
+  template <typename Tile>
+  static constexpr int tile_count() { return G::template tile_count<Tile>(); }
   template <int NBYTES>
-  static constexpr int co_size() {
-    return (NBYTES % (1024 * NW) == 0) ? 16 : (NBYTES % (256 * NW) == 0) ? 4 : 16;
-  }
+  static constexpr int co_count() { return G::template co_count<NBYTES>(); }
   template <int NBYTES>
-  static constexpr int co_count() {
-    constexpr int SZ = co_size<NBYTES>();
-    return dma_min_count<(NBYTES + 64 * SZ - 1) / (64 * SZ), NW>();
+  static __device__ __forceinline__ void copy(void* dst, const void* src) {
+    G::template copy<NBYTES>(dst, src);
   }
   template <typename Tile>
-  static constexpr int tile_count() {
-    return dma_min_count<(Tile::NCHK + 63) / 64, NW>();
+  static __device__ __forceinline__ void op_tile(Tile& t, const T* src) {
+    G::template op_tile<C>(t, src);
   }
+  static constexpr int NCO01 = 2 * E * C * 4, NCO2 = E * C * 4;  // bytes
   static constexpr int N_KQ = tile_count<decltype(Sm::K)>() +
                               (Sm::STAGE_Q ? tile_count<decltype(Sm::Q)>() : 0) + co_count<NCO01>();
   static constexpr int N_TU = tile_count<decltype(Sm::Tu)>() * (Sm::SPLIT ? 2 : 1);
@@ -402,48 +402,6 @@ struct FwdDma {
   static constexpr int N_KT = tile_count<decltype(Sm::Kt)>() + co_count<NCO2>();
   static constexpr int N_KC = tile_count<decltype(Sm::K)>() + co_count<NCO01>();
   static constexpr int N_Q = tile_count<decltype(Sm::Q)>();
-  static_assert((NW & (NW - 1)) == 0, "wave groups of 2^n waves");
-  // index of the calling wave within its group
-  static __device__ __forceinline__ int wid() { return wave_id() & (NW - 1); }
-
-  // Fill a swizzled tile; off(r, c) is the byte offset from the wave-uniform
-  // base of logical chunk c of row r.
-  template <typename Tile, typename F>
-  static __device__ __forceinline__ void tile(Tile& t, const void* base, F off) {
-    constexpr int NB = (Tile::NCHK + 63) / 64;
-    const int w = wid(), l = lane_id();
-    const uint32_t lds = lds_addr(t.d);
-#pragma unroll
-    for (int i = 0; i * NW < NB; ++i) {
-      const int blk = i * NW + w;
-      if (NB % NW != 0 && blk >= NB) continue;  // wave-uniform
-      int r, c;
-      Tile::logical(64 * blk + l, r, c);
-      if (Tile::NCHK % 64 == 0 || 64 * blk + l < Tile::NCHK)
-        lds_dma<16>(base, off(r, c), lds + 1024 * blk);
-    }
-  }
-  // A plain copy of NBYTES contiguous bytes.
-  template <int NBYTES>
-  static __device__ __forceinline__ void copy(void* dst, const void* src) {
-    constexpr int SZ = co_size<NBYTES>(), NB = (NBYTES + 64 * SZ - 1) / (64 * SZ);
-    const int w = wid(), l = lane_id();
-    const uint32_t lds = lds_addr(dst);
-#pragma unroll
-    for (int i = 0; i * NW < NB; ++i) {
-      const int blk = i * NW + w;
-      if (NB % NW != 0 && blk >= NB) continue;
-      const uint32_t off = 64 * SZ * blk + SZ * l;
-      if (NBYTES % (64 * SZ) == 0 || off < (uint32_t)NBYTES)
-        lds_dma<SZ>(src, off, lds + 64 * SZ * blk);
-    }
-  }
-  // an operand tile of the prep kernel (row-major C-wide rows) at src
-  template <typename Tile>
-  static __device__ __forceinline__ void op_tile(Tile& t, const T* src) {
-    tile(t, src, [](int r, int c) { return (uint32_t)(sizeof(T) * (r * C + Tile::EC * c)); });
-  }
-
   static __device__ __forceinline__ void kq(Sm& sm, const Shape& s, const PrepBufs& p, const T* Kg,
                                             const T* Qg, size_t ch, int t0) {
     const size_t krs = (size_t)s.H * KD;
@@ -517,14 +475,6 @@ struct FwdDma {
     if (l < BL) lds_dma<4>(bg, off, lds_addr(&sm.beta[0]) + 4 * w * BL);
   }
 };
-
-// Rows past T of a row tile (the last, partial chunk): zero them after the
-// direct copies have landed.
-template <typename Tile>
-__device__ __forceinline__ void zero_rows_from(Tile& t, int r0, int nthr) {
-  for (int p = threadIdx.x; p < Tile::NCHK; p += nthr)
-    if (p / Tile::NCH >= r0) *(uint4*)((char*)t.d + 16 * p) = make_uint4(0, 0, 0, 0);
-}
 
 template <typename T, int KD, int C, int E, int NW>
 __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, void* out,
