@@ -47,7 +47,8 @@ KERNEL_SOURCES = {
     "bwd_state": "tla_bwd.hip", "bwd_chunk": "tla_bwd.hip", "step": "tla_step.hip",
 }
 KERNEL_SYMBOLS = {  # rocprofv3 kernel-name prefix -> timing slot
-    "tla::k_prep<": "prep", "tla::k_fwd<": "fwd_recurrent", "tla::k_bwd_rec<": "bwd_recurrent",
+    "tla::k_prep<": "prep", "tla::k_fwd<": "fwd_recurrent", "tla::k_fwd_dual<": "fwd_recurrent",
+    "tla::k_bwd_rec<": "bwd_recurrent",
     "tla::k_bwd_state<": "bwd_state", "tla::k_bwd_chunk<": "bwd_chunk", "tla::k_step<": "step",
 }
 COPY_BYTES = 1 << 28         # copy-calibration buffer (fp32)
