@@ -1151,7 +1151,7 @@ __global__ __launch_bounds__(CHUNK_NTHR) void k_bwd_chunk(Shape s, FwdIn in, con
         Ub[vp][0] = *(const f32x4*)(Ug + (size_t)cb * V + col);
         Ub[vp][1] = *(const f32x4*)(Ug + (size_t)cb * V + col + 4);
       }
-      if (gdn) {
+      if (gdn && lower) {
         dUa[vp][0] = *(const f32x4*)(dUg + (size_t)ra * V + col);
         dUa[vp][1] = *(const f32x4*)(dUg + (size_t)ra * V + col + 4);
         Xb[vp][0] = *(const f32x4*)(Xg + (size_t)cb * V + col);
@@ -1205,7 +1205,10 @@ __global__ __launch_bounds__(CHUNK_NTHR) void k_bwd_chunk(Shape s, FwdIn in, con
         mma8_xs(dm, (cok && raok) ? dOa[vp] : zero_raw8<T>(), Ub[vp][0], Ub[vp][1]);
       }
     }
-    if (gdn) {
+    // dTu only on and below the diagonal: Tu is lower triangular, and of
+    // P = N^{-T} dTu the solve below uses the diagonal (dbeta) and the
+    // strictly lower part (dL), which read only those tiles of dTu
+    if (gdn && lower) {
 #pragma unroll
       for (int vp = 0; vp < NVPMAX; ++vp) {
         if (vp >= NVP) continue;
@@ -1234,13 +1237,15 @@ __global__ __launch_bounds__(CHUNK_NTHR) void k_bwd_chunk(Shape s, FwdIn in, con
       unit_lower_inverse<C, NTHR>(
           [&](int r, int c) { return sm.beta[r] * sm.Akk[r][c] * sm.u2.r.R[r][c]; },
           &sm.u2.r.X1[0][0], Sm::CP, &sm.Y[0][0][0]);
-    // ---- P = N^{-T} dTu on MFMA (fp32 operands); N^{-T} is upper triangular
+    // ---- P = N^{-T} dTu on MFMA (fp32 operands); N^{-T} is upper triangular.
+    // Only the tiles on and below the diagonal are formed: dbeta takes the
+    // diagonal and dL the strictly lower part (the others would stay unused)
     f32x4 pt[(NT * NT + NW - 1) / NW];
 #pragma unroll
     for (int i = 0; i < (NT * NT + NW - 1) / NW; ++i) {
       const int tile = w + NW * i;
       f32x4 acc = zero4();
-      if (tile < NT * NT) {
+      if (tile < NT * NT && tile % NT <= tile / NT) {
         const int rt = tile / NT, ct = tile % NT;
         for (int kb = rt; kb < NT; ++kb) {
           f32x4 a, bv;
