@@ -959,6 +959,14 @@ __device__ __forceinline__ void store8_out(void* base, size_t off, f32x4 a, f32x
   }
 }
 
+// 4 gradient values (consecutive columns of one row) to an out_dtype row
+__device__ __forceinline__ void store4_out(void* base, size_t off, f32x4 a, int out_bf16) {
+  if (out_bf16)
+    *(bf16x4*)((bf16_t*)base + off) = cvt_frag<bf16_t>(a);
+  else
+    *(f32x4*)((float*)base + off) = a;
+}
+
 // LDS plan of the per-chunk kernel.  C x C fp32 matrices use a row stride of
 // C + 4 floats (16-byte rows, conflict-free fragment reads).  Two regions are
 // reused once their first contents are dead: the Q / K rows become dM^T and
@@ -1432,8 +1440,56 @@ __global__ __launch_bounds__(CHUNK_NTHR) void k_bwd_chunk(Shape s, FwdIn in, con
       pka[i][j] = bb.dks[wo];
     }
   }
+  // bf16 operands with an even number of row tiles: every tile of the wave
+  // has row tile w % NT, so the (hi, lo) splits of its dM, dA_qk^T and
+  // dA_kk + dA_kk^T rows are formed once, and the results leave as one
+  // quad-transposed store per lane (row 16 rt + 4 g + n % 4, four columns)
+  constexpr bool HOIST = sizeof(T) == 2 && NT % 2 == 0 && NW % NT == 0;
+  if constexpr (HOIST) {
+    const int rt = w % NT, r = 16 * rt + n;
+    bf16x4 mh[NT], ml[NT], th[NT], tl[NT], yh[NT], yl[NT];
+#pragma unroll
+    for (int sb = 0; sb < NT; ++sb) {
+      const int c = 16 * sb + 4 * g;
+      split_frag(*(const f32x4*)&sm.dM[r][c], mh[sb], ml[sb]);
+      split_frag(*(const f32x4*)&sm.u1.tr.dMT[r][c], th[sb], tl[sb]);
+      split_frag(*(const f32x4*)&sm.u1.tr.Dsym[r][c], yh[sb], yl[sb]);
+    }
+#pragma unroll
+    for (int i = 0; i < TPW; ++i) {
+      const int tile = w + NW * i;
+      if (tile >= NT * KT) continue;  // wave-uniform
+      const int kt = tile / NT;
+      f32x4 aq = zero4(), ak = zero4();
+#pragma unroll
+      for (int sb = 0; sb < NT; sb += 2) {
+        const F bk0 = ktf(kt, sb), bk1 = ktf(kt, sb + 1);
+        const F bq0 = qtf(kt, sb), bq1 = qtf(kt, sb + 1);
+        mma32(aq, mh[sb], mh[sb + 1], bk0, bk1);
+        mma32(aq, ml[sb], ml[sb + 1], bk0, bk1);
+        mma32(ak, th[sb], th[sb + 1], bq0, bq1);
+        mma32(ak, tl[sb], tl[sb + 1], bq0, bq1);
+        mma32(ak, yh[sb], yh[sb + 1], bk0, bk1);
+        mma32(ak, yl[sb], yl[sb + 1], bk0, bk1);
+      }
+      f32x4 pq, pk;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        pq[j] = pqa[i][j];
+        pk[j] = pka[i][j];
+      }
+      const f32x4 yq = quad_transpose(aq + pq, n), yk = quad_transpose(ak + pk, n);
+      const int t = t0 + 16 * rt + 4 * g + (n & 3);
+      if (t < s.T) {
+        const size_t o = ((tok0 + t) * s.H + h) * KD + 16 * kt + 4 * (n >> 2);
+        store4_out(dqv, o, yq, s.out_bf16);
+        store4_out(dkv, o, yk, s.out_bf16);
+      }
+    }
+  }
 #pragma unroll
   for (int i = 0; i < TPW; ++i) {
+    if constexpr (HOIST) break;
     const int tile = w + NW * i;
     if (tile >= NT * KT) continue;  // wave-uniform
     const int rt = tile % NT, kt = tile / NT;
