@@ -1049,21 +1049,30 @@ __global__ __launch_bounds__(CHUNK_NTHR) void k_bwd_chunk(Shape s, FwdIn in, con
   const size_t erow = (size_t)s.H * E;
   const bool gdn = s.variant == 1;
 
-  // ---- phase 0: per-position vectors, Q and K rows, in-chunk cumulative log-gates
-  for (int idx = tid; idx < C * E; idx += NTHR) {
-    const int r = idx / E, e = idx % E;
-    const int t = t0 + r;
-    const bool ok = t < s.T;
-    sm.q2[r][e] = ok ? ld_f((const T*)in.q2 + eoff + (size_t)t * erow + e) : 0.f;
-    sm.k2[r][e] = ok ? ld_f((const T*)in.k2 + eoff + (size_t)t * erow + e) : 0.f;
+  // ---- phase 0: per-position vectors, Q and K rows, in-chunk cumulative
+  // log-gates.  Every global load of the phase is issued before the first of
+  // their results is stored (one memory latency instead of one per array).
+  constexpr int NQE = (C * E + NTHR - 1) / NTHR;             // q2, k2 entries per thread
+  constexpr int IT = STAGE_QK ? (C * KD / 8 + NTHR - 1) / NTHR : 1;  // Q, K pieces
+  constexpr int NNV = (C * C / 4 + NTHR - 1) / NTHR;        // (I + L)^{-1} pieces
+  constexpr int NGE = (E + NW - 1) / NW;                     // slices per wave (g)
+  const bool have_ninv = gdn && p.ninv != nullptr;
+  float q2v[NQE], k2v[NQE], bv = 0.f;
+  Raw8<T> qv[IT], kv[IT];
+  f32x4 nv[NNV];
+  double gv[NGE];
+#pragma unroll
+  for (int i = 0; i < NQE; ++i) {
+    const int idx = tid + NTHR * i, r = idx / E, e = idx % E, t = t0 + r;
+    const bool ok = idx < C * E && t < s.T;
+    q2v[i] = ok ? ld_f((const T*)in.q2 + eoff + (size_t)t * erow + e) : 0.f;
+    k2v[i] = ok ? ld_f((const T*)in.k2 + eoff + (size_t)t * erow + e) : 0.f;
   }
-  for (int r = tid; r < C; r += NTHR) {
-    const int t = t0 + r;
-    sm.beta[r] = (t < s.T) ? (in.beta ? in.beta[(tok0 + t) * s.H + h] : 1.f) : 0.f;
+  if (tid < C) {
+    const int t = t0 + tid;
+    bv = (t < s.T) ? (in.beta ? in.beta[(tok0 + t) * s.H + h] : 1.f) : 0.f;
   }
   if constexpr (STAGE_QK) {
-    constexpr int IT = (C * KD / 8 + NTHR - 1) / NTHR;
-    Raw8<T> qv[IT], kv[IT];
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
       const int idx = tid + NTHR * it;
@@ -1076,6 +1085,33 @@ __global__ __launch_bounds__(CHUNK_NTHR) void k_bwd_chunk(Shape s, FwdIn in, con
         kv[it] = load8(Kg + (size_t)t * krs + 8 * c8);
       }
     }
+  }
+  // (I + L)^{-1} as the forward's prep kernel formed it (GDN): into its LDS
+  // region, which stays free until the solve backward
+  if (have_ninv) {
+    const float* src = p.ninv + (size_t)ch * C * C;
+#pragma unroll
+    for (int i = 0; i < NNV; ++i) {
+      const int idx = tid + NTHR * i;
+      nv[i] = idx < C * C / 4 ? *(const f32x4*)(src + 4 * idx) : zero4();
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < NGE; ++i) {
+    const int e = w + NW * i, t = t0 + l;
+    gv[i] = (e < E && l < C && t < s.T) ? (double)in.g[eoff + (size_t)t * erow + e] : 0.0;
+  }
+  // ---- the stores
+#pragma unroll
+  for (int i = 0; i < NQE; ++i) {
+    const int idx = tid + NTHR * i;
+    if (idx < C * E) {
+      sm.q2[idx / E][idx % E] = q2v[i];
+      sm.k2[idx / E][idx % E] = k2v[i];
+    }
+  }
+  if (tid < C) sm.beta[tid] = bv;
+  if constexpr (STAGE_QK) {
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
       const int idx = tid + NTHR * it;
@@ -1085,21 +1121,20 @@ __global__ __launch_bounds__(CHUNK_NTHR) void k_bwd_chunk(Shape s, FwdIn in, con
       *(Raw8<T>*)&sm.u1.qk.sK[r][8 * c8] = kv[it];
     }
   }
-  // (I + L)^{-1} as the forward's prep kernel formed it (GDN): into its LDS
-  // region, which stays free until the solve backward
-  const bool have_ninv = gdn && p.ninv != nullptr;
   if (have_ninv) {
-    const float* src = p.ninv + (size_t)ch * C * C;
-    for (int idx = tid; idx < C * C / 4; idx += NTHR) {
-      const int r = idx / (C / 4), c4 = idx % (C / 4);
-      *(f32x4*)&sm.u2.r.X1[r][4 * c4] = *(const f32x4*)(src + r * C + 4 * c4);
+#pragma unroll
+    for (int i = 0; i < NNV; ++i) {
+      const int idx = tid + NTHR * i;
+      if (idx < C * C / 4) *(f32x4*)&sm.u2.r.X1[idx / (C / 4)][4 * (idx % (C / 4))] = nv[i];
     }
   }
   // G = inclusive cumulative sum of g over the chunk, in fp64: one wave per
   // slice, lane r holds row r
-  for (int e = w; e < E; e += NW) {
-    const int t = t0 + l;
-    double x = (l < C && t < s.T) ? (double)in.g[eoff + (size_t)t * erow + e] : 0.0;
+#pragma unroll
+  for (int i = 0; i < NGE; ++i) {
+    const int e = w + NW * i;
+    if (e >= E) continue;  // wave-uniform
+    double x = gv[i];
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
       const double y = __shfl_up(x, off, 64);
