@@ -101,23 +101,27 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
   const T* Kg = (const T*)in.k + (tok0 * s.H + h) * KD;
   const size_t eoff = (tok0 * s.H + h) * E, erow = (size_t)s.H * E;
 
-  // ---- per-position vectors; Q and K rows (rows past T read clamped, then zeroed)
-  for (int idx = tid; idx < C * E; idx += 256) {
-    const int r = idx / E, e = idx % E;
+  // ---- per-position vectors; Q and K rows (rows past T read clamped, then
+  // zeroed).  Every global load of the phase is issued before the first of
+  // their results is stored (one memory latency instead of one per array).
+  constexpr int NQE = (C * E + 255) / 256;  // q2, k2 entries per thread
+  constexpr int IT = STAGE ? (C * KD / 8 + 255) / 256 : 1;
+  constexpr int NGE = (E + 3) / 4;          // slices per wave (g)
+  float q2v[NQE], k2v[NQE], bv = 0.f;
+  Raw8<T> qv[IT], kv[IT];
+  double gv[NGE];
+#pragma unroll
+  for (int i = 0; i < NQE; ++i) {
+    const int idx = min(tid + 256 * i, C * E - 1), r = idx / E, e = idx % E;
     const size_t off = eoff + (size_t)min(t0 + r, s.T - 1) * erow + e;
-    const float x2 = ld_f((const T*)in.q2 + off), y2 = ld_f((const T*)in.k2 + off);
-    const bool ok = t0 + r < s.T;
-    sm.q2[r][e] = ok ? x2 : 0.f;
-    sm.k2[r][e] = ok ? y2 : 0.f;
+    q2v[i] = ld_f((const T*)in.q2 + off);
+    k2v[i] = ld_f((const T*)in.k2 + off);
   }
   if (tid < C) {
     const int t = min(t0 + tid, s.T - 1);
-    const float bv = in.beta ? in.beta[(tok0 + t) * s.H + h] : 1.f;
-    sm.beta[tid] = (t0 + tid < s.T) ? bv : 0.f;
+    bv = in.beta ? in.beta[(tok0 + t) * s.H + h] : 1.f;
   }
   if constexpr (STAGE) {
-    constexpr int IT = (C * KD / 8 + 255) / 256;
-    Raw8<T> qv[IT], kv[IT];
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
       const int idx = min(tid + 256 * it, C * KD / 8 - 1);
@@ -126,6 +130,23 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
       qv[it] = load8(Qg + off);
       kv[it] = load8(Kg + off);
     }
+  }
+#pragma unroll
+  for (int i = 0; i < NGE; ++i) {
+    const int e = min(w + 4 * i, E - 1);
+    gv[i] = (double)in.g[eoff + (size_t)min(t0 + l, s.T - 1) * erow + e];
+  }
+  // ---- the stores
+#pragma unroll
+  for (int i = 0; i < NQE; ++i) {
+    const int idx = tid + 256 * i, r = idx / E, e = idx % E;
+    if (idx >= C * E) continue;
+    const bool ok = t0 + r < s.T;
+    sm.q2[r][e] = ok ? q2v[i] : 0.f;
+    sm.k2[r][e] = ok ? k2v[i] : 0.f;
+  }
+  if (tid < C) sm.beta[tid] = (t0 + tid < s.T) ? bv : 0.f;
+  if constexpr (STAGE) {
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
       const int idx = tid + 256 * it;
@@ -139,9 +160,11 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
   // G: inclusive cumulative sum over the chunk in fp64 (one wave per slice,
   // lane r holds row r); after a very negative gate the running sum is large
   // and fp32 would lose the small gates that follow it
-  for (int e = w; e < E; e += 4) {
-    const double gx = (double)in.g[eoff + (size_t)min(t0 + l, s.T - 1) * erow + e];
-    double x = (l < C && t0 + l < s.T) ? gx : 0.0;
+#pragma unroll
+  for (int i = 0; i < NGE; ++i) {
+    const int e = w + 4 * i;
+    if (e >= E) continue;  // wave-uniform
+    double x = (l < C && t0 + l < s.T) ? gv[i] : 0.0;
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
       const double y = __shfl_up(x, off, 64);
