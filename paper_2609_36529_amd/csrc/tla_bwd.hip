@@ -708,11 +708,20 @@ __global__ __launch_bounds__(STATE_NTHR) void k_bwd_state(Shape s, FwdIn in, con
     if constexpr (sizeof(T) == 2) return __uint_as_float((j & 1) ? (x[j >> 1] & 0xffff0000u) : (x[j >> 1] << 16));
     else return __uint_as_float(x[j]);
   };
+  // coefficient vectors: loaded with the staged rows (one memory latency for
+  // both), stored to LDS after the staging has waited for them
+  constexpr int NCF = (3 * E * C / 4 + NTHR - 1) / NTHR;
+  f32x4 cf[NCF];
   {
     const float* cg = p.coef + (size_t)ch * 3 * E * C;
-    for (int idx = tid; idx < 3 * E * C; idx += NTHR) (&sm.coef[0][0][0])[idx] = cg[idx];
+#pragma unroll
+    for (int i = 0; i < NCF; ++i)
+      cf[i] = *(const f32x4*)(cg + 4 * min(tid + NTHR * i, 3 * E * C / 4 - 1));
   }
   if constexpr (Sm::STAGE_ALL) stage(0, 32 * NP);
+#pragma unroll
+  for (int i = 0; i < NCF; ++i)
+    if (tid + NTHR * i < 3 * E * C / 4) *(f32x4*)(&sm.coef[0][0][0] + 4 * (tid + NTHR * i)) = cf[i];
 
   // B operands: S_e^T and dS'_e^T for this wave's key columns; lane (g, n)
   // takes key row 16 ct + n of value block 2 pp + g / 2, columns 8 (g & 1) + 0..7
