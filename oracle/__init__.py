@@ -8,7 +8,8 @@ shares no code with it.
 ``tla_oracle.c`` (the plain definition of the operator: Eq. forget3, Eq. gdn3,
 Eq. la3 and the mixer of Alg. 2).  ``forms`` holds independent numpy
 formulations used to pin it (flattened joint key, dyadic special case,
-quadratic form, chunkwise form).
+quadratic form, chunkwise form).  ``gate`` is the mixer's output side
+(RMSNorm times a sigmoid gate) in numpy.
 """
 import ctypes
 import os
@@ -16,6 +17,7 @@ import os
 import numpy as np
 
 from . import build as _build
+from .gate import out_gate_bwd, out_gate_fwd  # noqa: F401
 
 SGLA, GDN = 0, 1
 _HERE = os.path.dirname(os.path.abspath(__file__))
