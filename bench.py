@@ -296,6 +296,55 @@ def forward_bench(name, steps, warmup):
                      "kernel": "prep + fwd_recurrent"}}), flush=True)
 
 
+def gate_bench(steps, warmup):
+    """The mixer's output side (RMSNorm times a sigmoid gate) forward and
+    backward on the forward's output at the metric shape: B4 T4096 H8 V128
+    rows, bf16.  HBM-bound; algorithmic bytes per element: forward 3 x 2 (o,
+    z read, y written), backward 5 x 2 (o, z, dy read, d_o, dz written), plus
+    the fp32 gain-gradient partials (1024 workgroups x V floats, written and
+    read once)."""
+    import torch
+    import paper_2609_36529_amd as tla
+    B, T, H, V = 4, 4096, 8, 128
+    rows = B * T * H
+    g = torch.Generator().manual_seed(17)
+    o = torch.randn(rows, V, generator=g).to(torch.bfloat16).cuda()
+    z = (2.0 * torch.randn(rows, V, generator=g)).to(torch.bfloat16).cuda()
+    dy = torch.randn(rows, V, generator=g).to(torch.bfloat16).cuda()
+    w = (1.0 + 0.5 * torch.randn(V, generator=g)).float().cuda()
+
+    def one():
+        tla.out_gate_fwd(o, z, w)
+        tla.out_gate_bwd(o, z, w, dy)
+    for _ in range(warmup):
+        one()
+    torch.cuda.synchronize()
+    tla.prof_enable(True)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        one()
+    torch.cuda.synchronize()
+    elapsed = (time.perf_counter() - t0) / steps
+    prof = tla.prof_read()
+    tla.prof_enable(False)
+    kern = {k: round(v[0] / v[1], 4) for k, v in prof.items() if v[1]}
+    part = 1024 * V * 4
+    bytes_fwd, bytes_bwd = 6 * rows * V, 10 * rows * V + part
+    gbs_f = bytes_fwd / (kern["out_gate_fwd"] * 1e-3) / 1e9
+    gbs_b = bytes_bwd / (kern["out_gate_bwd"] * 1e-3) / 1e9
+    print(json.dumps({
+        "metric": "output gate fwd+bwd tokens/s, B4 T4096 H8 V128", "value": round(B * T / elapsed, 1),
+        "unit": "tokens/s", "n_gpus": 1, "steps": steps, "warmup": warmup,
+        "ms_per_step": round(1e3 * elapsed, 4), "higher_is_better": True, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "RMSNorm x sigmoid gate, forward and backward", "rows": rows, "V": V},
+        "kernels_ms": kern,
+        "roofline": {"bound": "hbm", "achieved": round(gbs_b, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(gbs_b / PEAK_HBM_GBS, 4), "kernel": "out_gate_bwd",
+                     "forward_gbs": round(gbs_f, 1), "forward_frac": round(gbs_f / PEAK_HBM_GBS, 4)}}),
+          flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -306,6 +355,8 @@ def main():
     ap.add_argument("--pmc-summary", nargs=4, metavar="DIR")
     ap.add_argument("--decode", action="store_true",
                     help="time the decode step instead (its own JSON line)")
+    ap.add_argument("--gate", action="store_true",
+                    help="time the output gate (RMSNorm x sigmoid) forward and backward")
     ap.add_argument("--forward", metavar="NAME",
                     help="time the inference forward of sgla_bf16, gdn_bf16 or gdn_long_bf16")
     args = ap.parse_args()
@@ -322,6 +373,9 @@ def main():
         return
     if args.decode:
         decode_bench(args.steps, args.warmup)
+        return
+    if args.gate:
+        gate_bench(args.steps, args.warmup)
         return
     if args.forward:
         forward_bench(args.forward, args.steps, args.warmup)

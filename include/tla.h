@@ -186,15 +186,43 @@ int tla_step(const tla_desc* desc, const void* q, const void* k, const void* v,
              float* state, void* o, void* stream);
 
 /*
+ * The output side of the mixer (Alg. 2, the mixer's last line): per row of
+ * V values (one head of one token),
+ *   y[v] = o[v] / sqrt(mean_v(o^2) + eps) * w[v] * sigmoid(z[v]),
+ * an RMS normalisation with gain w times a sigmoid gate whose pre-activation
+ * z the caller forms (the gate projections are not part of this op).
+ * o, z, y (and dy, d_o, dz of the backward) are row-major [rows][V] arrays of
+ * element type dtype (TLA_F32 or TLA_BF16), w and dw fp32 [V] (one gain
+ * shared by every row, i.e. every head); rows >= 0 (e.g. B * T * H), V one of
+ * 16, 32, 64, 128, 256 (TLA_E_UNSUPPORTED otherwise), eps >= 0 finite.
+ * Device pointers, 16-byte aligned, outputs not overlapping any input;
+ * arrays of zero size may be NULL.  Both calls are asynchronous on `stream`.
+ *
+ * tla_out_gate_bwd: given dy = dL/dy, writes d_o = dL/do, dz = dL/dz and
+ * dw = dL/dw (dw summed over all rows, in a fixed order: bitwise
+ * reproducible).  It needs a device workspace of
+ * tla_out_gate_workspace_bytes(rows, V) bytes (per-workgroup partials of dw;
+ * TLA_E_WORKSPACE if smaller), owned by the caller, free again when the call's
+ * work on `stream` is done.
+ */
+int tla_out_gate_fwd(int dtype, long long rows, int V, const void* o, const void* z,
+                     const float* w, float eps, void* y, void* stream);
+size_t tla_out_gate_workspace_bytes(long long rows, int V);
+int tla_out_gate_bwd(int dtype, long long rows, int V, const void* o, const void* z,
+                     const float* w, float eps, const void* dy, void* d_o, void* dz,
+                     float* dw, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * Per-kernel timing, for diagnostics and benchmarks (not needed otherwise).
  * tla_prof_enable(1) clears previous records and starts bracketing every
  * kernel launch of the library with a pair of HIP events on the launch
  * stream (events are created once and pooled); tla_prof_enable(0) stops and
  * clears.  tla_prof_read() waits for the recorded events and fills, for each
- * of the 6 kernel kinds named by tla_prof_name(0..5) ("prep",
- * "fwd_recurrent", "bwd_recurrent", "bwd_state", "bwd_chunk", "step"), the
- * summed event time in milliseconds and the number of launches; n must be
- * at least 6.  Not meant for use while another thread launches.
+ * of the 9 kernel kinds named by tla_prof_name(0..8) ("prep",
+ * "fwd_recurrent", "bwd_recurrent", "bwd_state", "bwd_chunk", "step",
+ * "out_gate_fwd", "out_gate_bwd", "out_gate_dw"), the summed event time in
+ * milliseconds and the number of launches; n must be at least 9.  Not meant
+ * for use while another thread launches.
  */
 int tla_prof_enable(int on);
 int tla_prof_read(double* total_ms, int* launches, int n);

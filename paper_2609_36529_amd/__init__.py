@@ -34,6 +34,9 @@ class TLAError(RuntimeError):
     pass
 
 
+PROF_SLOTS = 9  # kernel kinds of tla_prof_read
+
+
 def lib():
     """Loads the built HIP library (raises if it has not been built)."""
     global _lib
@@ -66,6 +69,12 @@ def lib():
     L.tla_bwd_varlen.restype = I
     L.tla_step.argtypes = [DP] + [P] * 9 + [P]
     L.tla_step.restype = I
+    L.tla_out_gate_fwd.argtypes = [I, LL, I, P, P, P, ctypes.c_float, P, P]
+    L.tla_out_gate_fwd.restype = I
+    L.tla_out_gate_workspace_bytes.argtypes = [LL, I]
+    L.tla_out_gate_workspace_bytes.restype = S
+    L.tla_out_gate_bwd.argtypes = [I, LL, I, P, P, P, ctypes.c_float, P, P, P, P, P, S, P]
+    L.tla_out_gate_bwd.restype = I
     L.tla_prof_enable.argtypes = [I]
     L.tla_prof_enable.restype = I
     L.tla_prof_read.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I), I]
@@ -248,6 +257,46 @@ def step(variant, q, k, v, q2, k2, g, beta, state, out_dtype=None, o=None):
     return o
 
 
+def out_gate_fwd(o, z, w, eps=1e-6, y=None):
+    """The mixer's output side (Alg. 2): y = o / sqrt(mean(o^2) + eps) * w * sigmoid(z)
+    over the last axis (V values of one head), for o, z of any leading shape
+    (bf16 or fp32, contiguous), gain w fp32 [V].  Runs tla_out_gate_fwd."""
+    _need(o, "o")
+    V = o.shape[-1]
+    dev = o.device
+    dt = _dtype_code(o.dtype)
+    _need(z, "z", o.dtype, dev)
+    _need(w, "w", torch.float32, dev)
+    if tuple(z.shape) != tuple(o.shape) or tuple(w.shape) != (V,):
+        raise ValueError("z must match o, w must be [V]")
+    if y is None:
+        y = torch.empty_like(o)
+    rows = o.numel() // V if V else 0
+    _check(lib().tla_out_gate_fwd(dt, rows, V, _ptr(o), _ptr(z), _ptr(w), float(eps), _ptr(y),
+                                  _stream(dev)))
+    return y
+
+
+def out_gate_bwd(o, z, w, dy, eps=1e-6):
+    """Gradients (d_o, dz, dw) of the output gate for upstream dy (tla_out_gate_bwd;
+    dw summed over all rows in a fixed order)."""
+    _need(o, "o")
+    V = o.shape[-1]
+    dev = o.device
+    dt = _dtype_code(o.dtype)
+    for t, nm in ((z, "z"), (dy, "dy")):
+        _need(t, nm, o.dtype, dev)
+    _need(w, "w", torch.float32, dev)
+    rows = o.numel() // V if V else 0
+    d_o, dz = torch.empty_like(o), torch.empty_like(o)
+    dw = torch.empty(V, dtype=torch.float32, device=dev)
+    L = lib()
+    ws = torch.empty(max(L.tla_out_gate_workspace_bytes(rows, V), 256), dtype=torch.uint8, device=dev)
+    _check(L.tla_out_gate_bwd(dt, rows, V, _ptr(o), _ptr(z), _ptr(w), float(eps), _ptr(dy), _ptr(d_o),
+                              _ptr(dz), _ptr(dw), _ptr(ws), ws.numel(), _stream(dev)))
+    return d_o, dz, dw
+
+
 def prof_enable(on=True):
     """Start (clearing old records) or stop per-kernel HIP-event timing."""
     _check(lib().tla_prof_enable(1 if on else 0))
@@ -256,7 +305,7 @@ def prof_enable(on=True):
 def prof_read():
     """{kernel name: (total ms, launches)} for the launches since prof_enable()."""
     L = lib()
-    tot = (ctypes.c_double * 6)()
-    cnt = (ctypes.c_int * 6)()
-    _check(L.tla_prof_read(tot, cnt, 6))
-    return {L.tla_prof_name(i).decode(): (tot[i], cnt[i]) for i in range(6)}
+    tot = (ctypes.c_double * PROF_SLOTS)()
+    cnt = (ctypes.c_int * PROF_SLOTS)()
+    _check(L.tla_prof_read(tot, cnt, PROF_SLOTS))
+    return {L.tla_prof_name(i).decode(): (tot[i], cnt[i]) for i in range(PROF_SLOTS)}

@@ -175,9 +175,11 @@ int device_fail(hipError_t e, const char* what) {
 // Diagnostics only: while enabled, every kernel launch of the library is
 // bracketed by a pair of HIP events recorded on the launch stream.  Events are
 // pooled and reused; nothing is recorded when timing is off.
-enum { PROF_PREP, PROF_FWD, PROF_BWD_REC, PROF_BWD_STATE, PROF_BWD_CHUNK, PROF_STEP, PROF_N };
-const char* const kProfNames[PROF_N] = {"prep", "fwd_recurrent", "bwd_recurrent",
-                                        "bwd_state", "bwd_chunk", "step"};
+enum { PROF_PREP, PROF_FWD, PROF_BWD_REC, PROF_BWD_STATE, PROF_BWD_CHUNK, PROF_STEP,
+       PROF_GATE_FWD, PROF_GATE_BWD, PROF_GATE_DW, PROF_N };
+const char* const kProfNames[PROF_N] = {"prep",      "fwd_recurrent", "bwd_recurrent",
+                                        "bwd_state", "bwd_chunk",     "step",
+                                        "out_gate_fwd", "out_gate_bwd", "out_gate_dw"};
 struct ProfRec {
   int kind;
   hipEvent_t a, b;
@@ -455,6 +457,76 @@ int tla_step(const tla_desc* d, const void* q, const void* k, const void* v, con
   return TLA_OK;
 }
 
+// ------------------------------------------------------- output side of the mixer
+static int gate_check(int dtype, long long rows, int V, float eps) {
+  if (dtype != TLA_F32 && dtype != TLA_BF16) return fail(TLA_E_SHAPE, "dtype %d", dtype);
+  if (rows < 0) return fail(TLA_E_SHAPE, "rows = %lld", rows);
+  if (V != 16 && V != 32 && V != 64 && V != 128 && V != 256)
+    return fail(TLA_E_UNSUPPORTED, "V = %d (16, 32, 64, 128 or 256)", V);
+  if (!(eps >= 0.f) || eps > 3.4e38f) return fail(TLA_E_SHAPE, "eps must be finite and >= 0");
+  return TLA_OK;
+}
+
+size_t tla_out_gate_workspace_bytes(long long rows, int V) {
+  if (rows < 0 || V < 16 || V > 256 || (V & (V - 1))) return 0;
+  return align256((size_t)tla::gate_blocks(rows, V) * V * sizeof(float));
+}
+
+int tla_out_gate_fwd(int dtype, long long rows, int V, const void* o, const void* z,
+                     const float* w, float eps, void* y, void* stream) {
+  g_err[0] = 0;
+  int rc = gate_check(dtype, rows, V, eps);
+  if (rc) return rc;
+  if (!w || (rows > 0 && (!o || !z || !y))) return fail(TLA_E_NULL, "o, z, w and y are required");
+  const void* ptrs[] = {o, z, w, y};
+  for (const void* p : ptrs)
+    if (misaligned(p)) return fail(TLA_E_ALIGN, "pointer %p is not 16-byte aligned", p);
+  const size_t nb = (size_t)rows * V * (dtype == TLA_BF16 ? 2 : 4);
+  const Range out{y, nb};
+  if (overlap(out, {o, nb}) || overlap(out, {z, nb}) || overlap(out, {w, (size_t)V * 4}))
+    return fail(TLA_E_ALIAS, "y overlaps an input");
+  if (rows == 0) return TLA_OK;
+  hipError_t e = timed(PROF_GATE_FWD, (hipStream_t)stream, [&] {
+    return tla::launch_gate_fwd(dtype == TLA_BF16, rows, V, o, z, w, eps, y, (hipStream_t)stream);
+  });
+  if (e != hipSuccess) return device_fail(e, "output gate kernel");
+  return TLA_OK;
+}
+
+int tla_out_gate_bwd(int dtype, long long rows, int V, const void* o, const void* z,
+                     const float* w, float eps, const void* dy, void* d_o, void* dz, float* dw,
+                     void* workspace, size_t workspace_bytes, void* stream) {
+  g_err[0] = 0;
+  int rc = gate_check(dtype, rows, V, eps);
+  if (rc) return rc;
+  if (!w || !dw || (rows > 0 && (!o || !z || !dy || !d_o || !dz)))
+    return fail(TLA_E_NULL, "o, z, w, dy, d_o, dz and dw are required");
+  const void* ptrs[] = {o, z, w, dy, d_o, dz, dw, workspace};
+  for (const void* p : ptrs)
+    if (misaligned(p)) return fail(TLA_E_ALIGN, "pointer %p is not 16-byte aligned", p);
+  const size_t need = tla_out_gate_workspace_bytes(rows, V);
+  if (!workspace || workspace_bytes < need)
+    return fail(TLA_E_WORKSPACE, "workspace of %zu bytes needed", need);
+  const size_t nb = (size_t)rows * V * (dtype == TLA_BF16 ? 2 : 4);
+  const Range ins[] = {{o, nb}, {z, nb}, {w, (size_t)V * 4}, {dy, nb}};
+  const Range outs[] = {{d_o, nb}, {dz, nb}, {dw, (size_t)V * 4}, {workspace, need}};
+  for (const Range& a : outs)
+    for (const Range& b : ins)
+      if (overlap(a, b)) return fail(TLA_E_ALIAS, "an output or the workspace overlaps an input");
+  for (int i = 0; i < 4; ++i)
+    for (int j = i + 1; j < 4; ++j)
+      if (overlap(outs[i], outs[j])) return fail(TLA_E_ALIAS, "two outputs overlap");
+  hipStream_t st = (hipStream_t)stream;
+  float* part = (float*)workspace;
+  hipError_t e = timed(PROF_GATE_BWD, st, [&] {
+    return tla::launch_gate_bwd(dtype == TLA_BF16, rows, V, o, z, w, eps, dy, d_o, dz, part, st);
+  });
+  if (e != hipSuccess) return device_fail(e, "output gate backward kernel");
+  e = timed(PROF_GATE_DW, st, [&] { return tla::launch_gate_dw(rows, V, part, dw, st); });
+  if (e != hipSuccess) return device_fail(e, "output gate dw kernel");
+  return TLA_OK;
+}
+
 int tla_prof_enable(int on) {
   std::lock_guard<std::mutex> lk(g_prof_mu);
   for (ProfRec& r : g_prof) {
@@ -467,7 +539,7 @@ int tla_prof_enable(int on) {
 }
 
 int tla_prof_read(double* total_ms, int* launches, int n) {
-  if (!total_ms || !launches || n < 6) return fail(TLA_E_NULL, "tla_prof_read needs 6 slots");
+  if (!total_ms || !launches || n < PROF_N) return fail(TLA_E_NULL, "tla_prof_read needs %d slots", PROF_N);
   std::lock_guard<std::mutex> lk(g_prof_mu);
   for (int i = 0; i < n; ++i) {
     total_ms[i] = 0.0;

@@ -1,0 +1,225 @@
+// The output side of the mixer (Alg. 2, the mixer's last line): per row of
+// a head's V values,
+//   y = o / sqrt(mean(o^2) + eps) * w * sigmoid(z),
+// and its backward.  HBM-bound row kernels: V / 8 lanes per row, each lane
+// holding eight consecutive values (one 16-byte access per bf16 operand),
+// the mean square reduced within the row's lane group.  The gain gradient dw
+// (a sum over all rows) is reduced in a fixed order: per lane over its rows
+// (a fixed grid-stride set), per workgroup over its lanes, then over the
+// workgroups by a second kernel, so it is bitwise reproducible.
+#include <hip/hip_runtime.h>
+
+#include "tla_common.hpp"
+#include "tla_internal.hpp"
+
+namespace tla {
+
+constexpr int GATE_NTHR = 256;  // four waves
+
+// eight values of a row: bf16 (one 16-byte access) or fp32 (two)
+template <typename T>
+__device__ __forceinline__ void gate_load8(const T* p, float (&x)[8]) {
+  if constexpr (sizeof(T) == 2) {
+    const uint4 u = *(const uint4*)p;
+    const bf16x8 b = __builtin_bit_cast(bf16x8, u);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] = (float)b[i];
+  } else {
+    const f32x4 a = *(const f32x4*)p, c = *(const f32x4*)(p + 4);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      x[i] = a[i];
+      x[4 + i] = c[i];
+    }
+  }
+}
+template <typename T>
+__device__ __forceinline__ void gate_store8(T* p, const float (&x)[8]) {
+  if constexpr (sizeof(T) == 2) {
+    bf16x8 b;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) b[i] = (__bf16)x[i];
+    *(uint4*)p = __builtin_bit_cast(uint4, b);
+  } else {
+    *(f32x4*)p = f32x4{x[0], x[1], x[2], x[3]};
+    *(f32x4*)(p + 4) = f32x4{x[4], x[5], x[6], x[7]};
+  }
+}
+// sum over the LPR lanes of a row's group (aligned, a power of two)
+template <int LPR>
+__device__ __forceinline__ float group_sum(float x) {
+#pragma unroll
+  for (int m = 1; m < LPR; m <<= 1) x += __shfl_xor(x, m, 64);
+  return x;
+}
+__device__ __forceinline__ float sigmoidf_(float z) { return 1.f / (1.f + __expf(-z)); }
+
+// rows handled by one workgroup per grid-stride step
+template <int V> constexpr int gate_rows_per_block() { return (GATE_NTHR / 64) * (64 / (V / 8)); }
+
+template <typename T, int V>
+__global__ __launch_bounds__(GATE_NTHR) void k_gate_fwd(long long rows, const T* o, const T* z,
+                                                        const float* w, float eps, T* y) {
+  constexpr int LPR = V / 8, RPW = 64 / LPR, RPB = gate_rows_per_block<V>();
+  const int l = lane_id(), wv = threadIdx.x >> 6;
+  const int c0 = 8 * (l % LPR);
+  float wg[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) wg[i] = w[c0 + i];
+  for (long long r0 = (long long)blockIdx.x * RPB; r0 < rows; r0 += (long long)gridDim.x * RPB) {
+    const long long r = r0 + wv * RPW + l / LPR;
+    const bool ok = r < rows;
+    const size_t off = (size_t)(ok ? r : 0) * V + c0;
+    float x[8], g[8];
+    gate_load8(o + off, x);
+    gate_load8(z + off, g);
+    float ss = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) ss += x[i] * x[i];
+    const float inv = 1.f / sqrtf(group_sum<LPR>(ss) / V + eps);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] = x[i] * inv * wg[i] * sigmoidf_(g[i]);
+    if (ok) gate_store8(y + off, x);
+  }
+}
+
+template <typename T, int V>
+__global__ __launch_bounds__(GATE_NTHR) void k_gate_bwd(long long rows, const T* o, const T* z,
+                                                        const float* w, float eps, const T* dy, T* d_o,
+                                                        T* dz, float* dw_part) {
+  constexpr int LPR = V / 8, RPW = 64 / LPR, RPB = gate_rows_per_block<V>();
+  __shared__ float red[GATE_NTHR][8];
+  const int l = lane_id(), wv = threadIdx.x >> 6;
+  const int c0 = 8 * (l % LPR);
+  float wg[8], dwp[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    wg[i] = w[c0 + i];
+    dwp[i] = 0.f;
+  }
+  for (long long r0 = (long long)blockIdx.x * RPB; r0 < rows; r0 += (long long)gridDim.x * RPB) {
+    const long long r = r0 + wv * RPW + l / LPR;
+    const bool ok = r < rows;
+    const size_t off = (size_t)(ok ? r : 0) * V + c0;
+    float x[8], g[8], d[8];
+    gate_load8(o + off, x);
+    gate_load8(z + off, g);
+    gate_load8(dy + off, d);
+    float ss = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) ss += x[i] * x[i];
+    const float inv = 1.f / sqrtf(group_sum<LPR>(ss) / V + eps);
+    float dn[8], nn[8], dzv[8], dot = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float s = sigmoidf_(g[i]);
+      nn[i] = x[i] * inv;
+      dzv[i] = d[i] * wg[i] * nn[i] * s * (1.f - s);
+      dn[i] = d[i] * wg[i] * s;
+      dot += dn[i] * nn[i];
+      if (ok) dwp[i] += d[i] * nn[i] * s;
+    }
+    const float mdot = group_sum<LPR>(dot) / V;
+    float dov[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) dov[i] = inv * (dn[i] - nn[i] * mdot);
+    if (ok) {
+      gate_store8(d_o + off, dov);
+      gate_store8(dz + off, dzv);
+    }
+  }
+  // workgroup partial of dw: column c sums, in a fixed order, the lanes that
+  // hold it (lane l holds columns 8 (l % LPR) .. + 7 in every wave)
+#pragma unroll
+  for (int i = 0; i < 8; ++i) red[threadIdx.x][i] = dwp[i];
+  __syncthreads();
+  for (int c = threadIdx.x; c < V; c += GATE_NTHR) {
+    float acc = 0.f;
+    for (int t = c / 8; t < GATE_NTHR; t += LPR) acc += red[t][c % 8];
+    dw_part[(size_t)blockIdx.x * V + c] = acc;
+  }
+}
+
+// dw[c] = sum over the workgroups' partials (one workgroup per column c):
+// thread t sums partials t, t + 256, ... in order, then a fixed binary tree
+// over the threads (the same order on every call)
+__global__ __launch_bounds__(GATE_NTHR) void k_gate_dw(int nblocks, int V, const float* dw_part,
+                                                       float* dw) {
+  __shared__ float red[GATE_NTHR];
+  const int c = blockIdx.x, t = threadIdx.x;
+  float acc = 0.f;
+  for (int b = t; b < nblocks; b += GATE_NTHR) acc += dw_part[(size_t)b * V + c];
+  red[t] = acc;
+  __syncthreads();
+#pragma unroll
+  for (int m = GATE_NTHR / 2; m > 0; m >>= 1) {
+    if (t < m) red[t] += red[t + m];
+    __syncthreads();
+  }
+  if (t == 0) dw[c] = red[0];
+}
+
+// workgroups of the row kernels: enough to keep several per CU in flight;
+// the backward's count is also the number of dw partials per column
+static int gate_grid(long long rows, int V, long long cap) {
+  const long long rpb = (GATE_NTHR / 64) * (64 / (V / 8));
+  long long nb = (rows + rpb - 1) / rpb;
+  if (nb > cap) nb = cap;
+  return nb < 1 ? 1 : (int)nb;
+}
+int gate_blocks(long long rows, int V) { return gate_grid(rows, V, 1024); }
+
+template <typename T>
+static hipError_t gate_fwd_t(long long rows, int V, const void* o, const void* z, const float* w,
+                             float eps, void* y, hipStream_t st) {
+  const int nb = gate_grid(rows, V, 4096);
+#define GATE_F(V_)                                                                                  \
+  case V_:                                                                                          \
+    hipLaunchKernelGGL((k_gate_fwd<T, V_>), dim3(nb), dim3(GATE_NTHR), 0, st, rows, (const T*)o,    \
+                       (const T*)z, w, eps, (T*)y);                                                 \
+    break;
+  switch (V) {
+    GATE_F(16) GATE_F(32) GATE_F(64) GATE_F(128) GATE_F(256)
+    default: return hipErrorInvalidValue;
+  }
+#undef GATE_F
+  return hipGetLastError();
+}
+
+template <typename T>
+static hipError_t gate_bwd_t(long long rows, int V, const void* o, const void* z, const float* w,
+                             float eps, const void* dy, void* d_o, void* dz, float* dw_part,
+                             hipStream_t st) {
+  const int nb = gate_blocks(rows, V);
+#define GATE_B(V_)                                                                                  \
+  case V_:                                                                                          \
+    hipLaunchKernelGGL((k_gate_bwd<T, V_>), dim3(nb), dim3(GATE_NTHR), 0, st, rows, (const T*)o,    \
+                       (const T*)z, w, eps, (const T*)dy, (T*)d_o, (T*)dz, dw_part);                \
+    break;
+  switch (V) {
+    GATE_B(16) GATE_B(32) GATE_B(64) GATE_B(128) GATE_B(256)
+    default: return hipErrorInvalidValue;
+  }
+#undef GATE_B
+  return hipGetLastError();
+}
+
+hipError_t launch_gate_fwd(bool bf16, long long rows, int V, const void* o, const void* z,
+                           const float* w, float eps, void* y, hipStream_t st) {
+  return bf16 ? gate_fwd_t<bf16_t>(rows, V, o, z, w, eps, y, st)
+              : gate_fwd_t<float>(rows, V, o, z, w, eps, y, st);
+}
+
+hipError_t launch_gate_bwd(bool bf16, long long rows, int V, const void* o, const void* z,
+                           const float* w, float eps, const void* dy, void* d_o, void* dz,
+                           float* dw_part, hipStream_t st) {
+  return bf16 ? gate_bwd_t<bf16_t>(rows, V, o, z, w, eps, dy, d_o, dz, dw_part, st)
+              : gate_bwd_t<float>(rows, V, o, z, w, eps, dy, d_o, dz, dw_part, st);
+}
+
+hipError_t launch_gate_dw(long long rows, int V, const float* dw_part, float* dw, hipStream_t st) {
+  hipLaunchKernelGGL(k_gate_dw, dim3(V), dim3(GATE_NTHR), 0, st, gate_blocks(rows, V), V, dw_part, dw);
+  return hipGetLastError();
+}
+
+}  // namespace tla

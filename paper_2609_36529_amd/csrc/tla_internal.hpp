@@ -110,6 +110,14 @@ hipError_t launch_bwd_chunk(const Shape& s, const FwdIn& in, const void* dO, con
                             const BwdBufs& bb, void* dq, void* dk, void* dv, void* dq2,
                             void* dk2, float* dg, float* dbeta, hipStream_t st);
 hipError_t launch_step(const Shape& s, const FwdIn& in, float* state, void* o, hipStream_t st);
+// The mixer's output side (RMSNorm times a sigmoid gate), rows of V values.
+int gate_blocks(long long rows, int V);  // workgroups of the row kernels (dw partials)
+hipError_t launch_gate_fwd(bool bf16, long long rows, int V, const void* o, const void* z,
+                           const float* w, float eps, void* y, hipStream_t st);
+hipError_t launch_gate_bwd(bool bf16, long long rows, int V, const void* o, const void* z,
+                           const float* w, float eps, const void* dy, void* d_o, void* dz,
+                           float* dw_part, hipStream_t st);
+hipError_t launch_gate_dw(long long rows, int V, const float* dw_part, float* dw, hipStream_t st);
 
 // Which (K, C, E) combinations have kernel instances, and whether the
 // forward/backward shared-memory plan of an instance fits 160 KiB.

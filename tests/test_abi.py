@@ -191,3 +191,43 @@ def test_varlen_validation():
     assert fcall(P(FAKE + 0x70000000), 301) == E_SHAPE
     assert fcall(P(FAKE + 0x70000000), -1) == E_SHAPE
     assert bcall(P(FAKE + 0x70000000), 301) == E_SHAPE
+
+
+def test_out_gate_validation():
+    """Output gate: dtype, V, eps, required pointers, alignment, aliasing and
+    workspace are checked on the host (fake addresses, nothing launched)."""
+    L = tla.lib()
+    P = ctypes.c_void_p
+    o, z, w, y = (P(FAKE + i * 0x1000000) for i in range(4))
+    rows, V = 1000, 128
+
+    def fwd(dtype=tla.BF16, rows_=rows, V_=V, eps=1e-6, **kw):
+        a = dict(o=o, z=z, w=w, y=y)
+        a.update(kw)
+        return L.tla_out_gate_fwd(dtype, rows_, V_, a["o"], a["z"], a["w"], eps, a["y"], None)
+    assert fwd(dtype=7) == E_SHAPE
+    assert fwd(rows_=-1) == E_SHAPE
+    assert fwd(V_=96) == E_UNSUP
+    assert fwd(V_=512) == E_UNSUP
+    assert fwd(eps=-1.0) == E_SHAPE
+    assert fwd(eps=float("nan")) == E_SHAPE
+    assert fwd(z=None) == E_NULL
+    assert fwd(w=None) == E_NULL
+    assert fwd(y=P(FAKE + 8)) == E_ALIGN
+    assert fwd(y=o) == E_ALIAS
+    need = L.tla_out_gate_workspace_bytes(rows, V)
+    assert need >= 128 * 4 and need % 256 == 0
+    assert L.tla_out_gate_workspace_bytes(rows, 100) == 0
+    ws = P(FAKE + 0x8000000)
+    dy, do_, dz, dw = (P(FAKE + 0x4000000 + i * 0x1000000) for i in range(4))
+
+    def bwd(ws_bytes=need, **kw):
+        a = dict(dy=dy, do_=do_, dz=dz, dw=dw, ws=ws)
+        a.update(kw)
+        return L.tla_out_gate_bwd(tla.F32, rows, V, o, z, w, 1e-6, a["dy"], a["do_"], a["dz"], a["dw"],
+                                  a["ws"], ws_bytes, None)
+    assert bwd(ws_bytes=need - 1) == E_WS
+    assert bwd(ws=None) == E_WS
+    assert bwd(dw=None) == E_NULL
+    assert bwd(dz=dy) == E_ALIAS
+    assert bwd(dz=do_) == E_ALIAS
