@@ -9,7 +9,8 @@ shares no code with it.
 Eq. la3 and the mixer of Alg. 2).  ``forms`` holds independent numpy
 formulations used to pin it (flattened joint key, dyadic special case,
 quadratic form, chunkwise form).  ``gate`` is the mixer's output side
-(RMSNorm times a sigmoid gate) in numpy.
+(RMSNorm times a sigmoid gate) and ``heads`` its gate heads (forget gate and
+write strength), both in numpy.
 """
 import ctypes
 import os
@@ -18,6 +19,7 @@ import numpy as np
 
 from . import build as _build
 from .gate import out_gate_bwd, out_gate_fwd  # noqa: F401
+from .heads import gate_heads_bwd, gate_heads_fwd  # noqa: F401
 
 SGLA, GDN = 0, 1
 _HERE = os.path.dirname(os.path.abspath(__file__))
