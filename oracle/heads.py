@@ -37,5 +37,5 @@ def gate_heads_bwd(x, xb, A, b, dg, dbeta):
     dx = dg * (-np.exp(A)) * _sigmoid(x + b)
     db = np.sum(dx.reshape(-1, H, E), axis=0)
     dA = np.sum((dg * g).reshape(-1, H, E), axis=0)
-    be = _sigmoid(xb)
-    return dx, dbeta * be * (1.0 - be), dA, db
+    # sigmoid' = sigmoid(x) sigmoid(-x) (= beta (1 - beta), without 1 - beta rounding to 0)
+    return dx, dbeta * _sigmoid(xb) * _sigmoid(-xb), dA, db

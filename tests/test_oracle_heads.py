@@ -56,3 +56,15 @@ def test_gradients_match_finite_differences():
             am[name][idx] -= h
             fd[idx] = (loss(ap) - loss(am)) / (2 * h)
         np.testing.assert_allclose(grads[name], fd, rtol=1e-6, atol=1e-9, err_msg=name)
+
+
+def test_write_strength_slope_in_the_tails():
+    """d sigmoid / dx = e^-|x| / (1 + e^-|x|)^2 exactly; in the tails this is
+    tiny but still owed to full relative precision (1 - sigmoid(x) would round
+    to 0 in fp64 beyond |x| ~ 37)."""
+    xb = np.array([[-60.0, -40.0, -5.0, 0.0, 5.0, 40.0, 60.0]])
+    _, dxb, _, _ = oracle.gate_heads_bwd(np.zeros((1, 7, 1)), xb, np.zeros((7, 1)), np.zeros((7, 1)),
+                                         np.zeros((1, 7, 1)), np.ones((1, 7)))
+    a = np.exp(-np.abs(xb))
+    np.testing.assert_allclose(dxb, a / (1.0 + a) ** 2, rtol=1e-13, atol=0)
+
