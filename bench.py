@@ -345,6 +345,60 @@ def gate_bench(steps, warmup):
           flush=True)
 
 
+def heads_bench(steps, warmup):
+    """The mixer's gate heads (log forget gate g = -exp(A) softplus(x + b) per
+    key slice, write strength beta = sigmoid(x_beta)) forward and backward at
+    the metric shape: B4 T4096 H8 E8, bf16 pre-activations.  HBM-bound;
+    algorithmic bytes per (token, head, slice): forward 2 + 4 (x read, g
+    written), backward 2 + 4 + 2 (x, dg read, dx written); per (token, head):
+    forward 2 + 4, backward 2 + 4 + 2; plus the backward's fp32 partials of
+    dA, db (2 per column per 64 tokens, written and read once)."""
+    import torch
+    import paper_2609_36529_amd as tla
+    B, T, H, E = 4, 4096, 8, 8
+    n = B * T
+    gen = torch.Generator().manual_seed(19)
+    x = torch.randn(n, H, E, generator=gen).to(torch.bfloat16).cuda()
+    xb = torch.randn(n, H, generator=gen).to(torch.bfloat16).cuda()
+    A = torch.log(1.0 + 15.0 * torch.rand(H, E, generator=gen)).float().cuda()
+    b = (-4.0 + torch.rand(H, E, generator=gen)).float().cuda()
+    dg = torch.randn(n, H, E, generator=gen).float().cuda()
+    dbeta = torch.randn(n, H, generator=gen).float().cuda()
+
+    def one():
+        tla.gate_heads_fwd(x, xb, A, b)
+        tla.gate_heads_bwd(x, xb, A, b, dg, dbeta)
+    for _ in range(warmup):
+        one()
+    torch.cuda.synchronize()
+    tla.prof_enable(True)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        one()
+    torch.cuda.synchronize()
+    elapsed = (time.perf_counter() - t0) / steps
+    prof = tla.prof_read()
+    tla.prof_enable(False)
+    kern = {k: round(v[0] / v[1], 4) for k, v in prof.items() if v[1]}
+    part = 2 * 2 * ((n + 63) // 64) * H * E * 4
+    bytes_fwd = 6 * n * H * E + 6 * n * H
+    bytes_bwd = 8 * n * H * E + 8 * n * H + part
+    gbs_f = bytes_fwd / (kern["gate_heads_fwd"] * 1e-3) / 1e9
+    gbs_b = bytes_bwd / (kern["gate_heads_bwd"] * 1e-3) / 1e9
+    print(json.dumps({
+        "metric": "gate heads fwd+bwd tokens/s, B4 T4096 H8 E8", "value": round(n / elapsed, 1),
+        "unit": "tokens/s", "n_gpus": 1, "steps": steps, "warmup": warmup,
+        "ms_per_step": round(1e3 * elapsed, 4), "higher_is_better": True, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "forget gate and write strength heads, forward and backward",
+                   "tokens": n, "H": H, "E": E},
+        "kernels_ms": kern,
+        "roofline": {"bound": "hbm", "achieved": round(gbs_b, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(gbs_b / PEAK_HBM_GBS, 4), "kernel": "gate_heads_bwd",
+                     "forward_gbs": round(gbs_f, 1), "forward_frac": round(gbs_f / PEAK_HBM_GBS, 4)}}),
+          flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -357,6 +411,8 @@ def main():
                     help="time the decode step instead (its own JSON line)")
     ap.add_argument("--gate", action="store_true",
                     help="time the output gate (RMSNorm x sigmoid) forward and backward")
+    ap.add_argument("--heads", action="store_true",
+                    help="time the gate heads (forget gate, write strength) forward and backward")
     ap.add_argument("--forward", metavar="NAME",
                     help="time the inference forward of sgla_bf16, gdn_bf16 or gdn_long_bf16")
     args = ap.parse_args()
@@ -376,6 +432,9 @@ def main():
         return
     if args.gate:
         gate_bench(args.steps, args.warmup)
+        return
+    if args.heads:
+        heads_bench(args.steps, args.warmup)
         return
     if args.forward:
         forward_bench(args.forward, args.steps, args.warmup)

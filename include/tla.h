@@ -213,15 +213,45 @@ int tla_out_gate_bwd(int dtype, long long rows, int V, const void* o, const void
                      float* dw, void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * The gate heads of the mixer (Alg. 2): from pre-activations x (the forget
+ * gate's projection, per token, head h and slice e) and x_beta (the write
+ * strength's, per token and head), with per-(h, e) parameters A and b,
+ *   g[n][h][e]  = -exp(A[h][e]) * softplus(x[n][h][e] + b[h][e])   (log alpha, <= 0)
+ *   beta[n][h]  = sigmoid(x_beta[n][h]).
+ * g and beta are what tla_fwd / tla_step take.  x [tokens][H][E] and xb
+ * [tokens][H] have element type dtype (TLA_F32 or TLA_BF16); A, b, g, beta are
+ * fp32, A and b [H][E].  xb and beta (and dbeta, dxb of the backward) are
+ * NULL together (sGLA has no beta).  tokens >= 0 (e.g. B * T), H, E >= 1,
+ * H * E <= 2^20 (TLA_E_SHAPE otherwise).  Device pointers, 16-byte aligned,
+ * outputs not overlapping any input; arrays of zero size may be NULL.  Both
+ * calls are asynchronous on `stream`.
+ *
+ * tla_gate_heads_bwd: given dg = dL/dg and dbeta = dL/dbeta (fp32), writes
+ * dx, dxb (type dtype) and dA, db ([H][E] fp32, summed over all tokens in a
+ * fixed order: bitwise reproducible).  It needs a device workspace of
+ * tla_gate_heads_workspace_bytes(tokens, H, E) bytes (per-workgroup partials;
+ * TLA_E_WORKSPACE if smaller), owned by the caller, free again when the call's
+ * work on `stream` is done.
+ */
+int tla_gate_heads_fwd(int dtype, long long tokens, int H, int E, const void* x, const void* xb,
+                       const float* A, const float* b, float* g, float* beta, void* stream);
+size_t tla_gate_heads_workspace_bytes(long long tokens, int H, int E);
+int tla_gate_heads_bwd(int dtype, long long tokens, int H, int E, const void* x, const void* xb,
+                       const float* A, const float* b, const float* dg, const float* dbeta,
+                       void* dx, void* dxb, float* dA, float* db, void* workspace,
+                       size_t workspace_bytes, void* stream);
+
+/*
  * Per-kernel timing, for diagnostics and benchmarks (not needed otherwise).
  * tla_prof_enable(1) clears previous records and starts bracketing every
  * kernel launch of the library with a pair of HIP events on the launch
  * stream (events are created once and pooled); tla_prof_enable(0) stops and
  * clears.  tla_prof_read() waits for the recorded events and fills, for each
- * of the 9 kernel kinds named by tla_prof_name(0..8) ("prep",
+ * of the 11 kernel kinds named by tla_prof_name(0..10) ("prep",
  * "fwd_recurrent", "bwd_recurrent", "bwd_state", "bwd_chunk", "step",
- * "out_gate_fwd", "out_gate_bwd", "out_gate_dw"), the summed event time in
- * milliseconds and the number of launches; n must be at least 9.  Not meant
+ * "out_gate_fwd", "out_gate_bwd", "out_gate_dw", "gate_heads_fwd",
+ * "gate_heads_bwd"), the summed event time in milliseconds and the number of
+ * launches; n must be at least 11.  Not meant
  * for use while another thread launches.
  */
 int tla_prof_enable(int on);

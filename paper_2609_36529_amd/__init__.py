@@ -34,7 +34,7 @@ class TLAError(RuntimeError):
     pass
 
 
-PROF_SLOTS = 9  # kernel kinds of tla_prof_read
+PROF_SLOTS = 11  # kernel kinds of tla_prof_read
 
 
 def lib():
@@ -75,6 +75,12 @@ def lib():
     L.tla_out_gate_workspace_bytes.restype = S
     L.tla_out_gate_bwd.argtypes = [I, LL, I, P, P, P, ctypes.c_float, P, P, P, P, P, S, P]
     L.tla_out_gate_bwd.restype = I
+    L.tla_gate_heads_fwd.argtypes = [I, LL, I, I, P, P, P, P, P, P, P]
+    L.tla_gate_heads_fwd.restype = I
+    L.tla_gate_heads_workspace_bytes.argtypes = [LL, I, I]
+    L.tla_gate_heads_workspace_bytes.restype = S
+    L.tla_gate_heads_bwd.argtypes = [I, LL, I, I] + [P] * 11 + [S, P]
+    L.tla_gate_heads_bwd.restype = I
     L.tla_prof_enable.argtypes = [I]
     L.tla_prof_enable.restype = I
     L.tla_prof_read.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I), I]
@@ -295,6 +301,60 @@ def out_gate_bwd(o, z, w, dy, eps=1e-6):
     _check(L.tla_out_gate_bwd(dt, rows, V, _ptr(o), _ptr(z), _ptr(w), float(eps), _ptr(dy), _ptr(d_o),
                               _ptr(dz), _ptr(dw), _ptr(ws), ws.numel(), _stream(dev)))
     return d_o, dz, dw
+
+
+def gate_heads_fwd(x, xb, A, b):
+    """The mixer's gate heads (Alg. 2): g = -exp(A) softplus(x + b) (the log
+    forget gate, fp32) and beta = sigmoid(xb) (fp32, None if xb is None), for
+    x [..., H, E], xb [..., H] (bf16 or fp32, contiguous), A, b fp32 [H, E].
+    Runs tla_gate_heads_fwd."""
+    _need(x, "x")
+    dev = x.device
+    dt = _dtype_code(x.dtype)
+    H, E = A.shape
+    _need(A, "A", torch.float32, dev)
+    _need(b, "b", torch.float32, dev)
+    _need(xb, "xb", x.dtype, dev)
+    if tuple(x.shape[-2:]) != (H, E) or tuple(b.shape) != (H, E):
+        raise ValueError("x must end in [H, E] and b must be [H, E] like A")
+    if xb is not None and tuple(xb.shape) != tuple(x.shape[:-1]):
+        raise ValueError("xb must be x's shape without the last axis")
+    tokens = x.numel() // (H * E)
+    g = torch.empty(x.shape, dtype=torch.float32, device=dev)
+    beta = None if xb is None else torch.empty(xb.shape, dtype=torch.float32, device=dev)
+    _check(lib().tla_gate_heads_fwd(dt, tokens, H, E, _ptr(x), _ptr(xb), _ptr(A), _ptr(b), _ptr(g),
+                                    _ptr(beta), _stream(dev)))
+    return g, beta
+
+
+def gate_heads_bwd(x, xb, A, b, dg, dbeta):
+    """Gradients (dx, dxb, dA, db) of the gate heads for upstream dg, dbeta
+    (fp32; dbeta and dxb None when xb is None); dA, db are summed over all
+    tokens in a fixed order.  Runs tla_gate_heads_bwd."""
+    _need(x, "x")
+    dev = x.device
+    dt = _dtype_code(x.dtype)
+    H, E = A.shape
+    _need(A, "A", torch.float32, dev)
+    _need(b, "b", torch.float32, dev)
+    _need(xb, "xb", x.dtype, dev)
+    _need(dg, "dg", torch.float32, dev)
+    _need(dbeta, "dbeta", torch.float32, dev)
+    if tuple(dg.shape) != tuple(x.shape) or (xb is not None and dbeta is not None
+                                            and tuple(dbeta.shape) != tuple(xb.shape)):
+        raise ValueError("dg must match x and dbeta must match xb")
+    tokens = x.numel() // (H * E)
+    dx = torch.empty_like(x)
+    dxb = None if xb is None else torch.empty_like(xb)
+    dA = torch.empty((H, E), dtype=torch.float32, device=dev)
+    db = torch.empty((H, E), dtype=torch.float32, device=dev)
+    L = lib()
+    ws = torch.empty(max(L.tla_gate_heads_workspace_bytes(tokens, H, E), 256), dtype=torch.uint8,
+                     device=dev)
+    _check(L.tla_gate_heads_bwd(dt, tokens, H, E, _ptr(x), _ptr(xb), _ptr(A), _ptr(b), _ptr(dg),
+                                _ptr(dbeta), _ptr(dx), _ptr(dxb), _ptr(dA), _ptr(db), _ptr(ws),
+                                ws.numel(), _stream(dev)))
+    return dx, dxb, dA, db
 
 
 def prof_enable(on=True):

@@ -176,10 +176,11 @@ int device_fail(hipError_t e, const char* what) {
 // bracketed by a pair of HIP events recorded on the launch stream.  Events are
 // pooled and reused; nothing is recorded when timing is off.
 enum { PROF_PREP, PROF_FWD, PROF_BWD_REC, PROF_BWD_STATE, PROF_BWD_CHUNK, PROF_STEP,
-       PROF_GATE_FWD, PROF_GATE_BWD, PROF_GATE_DW, PROF_N };
-const char* const kProfNames[PROF_N] = {"prep",      "fwd_recurrent", "bwd_recurrent",
-                                        "bwd_state", "bwd_chunk",     "step",
-                                        "out_gate_fwd", "out_gate_bwd", "out_gate_dw"};
+       PROF_GATE_FWD, PROF_GATE_BWD, PROF_GATE_DW, PROF_HEADS_FWD, PROF_HEADS_BWD, PROF_N };
+const char* const kProfNames[PROF_N] = {"prep",         "fwd_recurrent",  "bwd_recurrent",
+                                        "bwd_state",    "bwd_chunk",      "step",
+                                        "out_gate_fwd", "out_gate_bwd",   "out_gate_dw",
+                                        "gate_heads_fwd", "gate_heads_bwd"};
 struct ProfRec {
   int kind;
   hipEvent_t a, b;
@@ -524,6 +525,83 @@ int tla_out_gate_bwd(int dtype, long long rows, int V, const void* o, const void
   if (e != hipSuccess) return device_fail(e, "output gate backward kernel");
   e = timed(PROF_GATE_DW, st, [&] { return tla::launch_gate_dw(rows, V, part, dw, st); });
   if (e != hipSuccess) return device_fail(e, "output gate dw kernel");
+  return TLA_OK;
+}
+
+// ------------------------------------------------------------- gate heads
+static int heads_check(int dtype, long long tokens, int H, int E) {
+  if (dtype != TLA_F32 && dtype != TLA_BF16) return fail(TLA_E_SHAPE, "dtype %d", dtype);
+  if (tokens < 0) return fail(TLA_E_SHAPE, "tokens = %lld", tokens);
+  if (H < 1 || E < 1 || (long long)H * E > (1 << 20))
+    return fail(TLA_E_SHAPE, "H = %d, E = %d (H, E >= 1, H * E <= 2^20)", H, E);
+  return TLA_OK;
+}
+
+size_t tla_gate_heads_workspace_bytes(long long tokens, int H, int E) {
+  if (tokens < 0 || H < 1 || E < 1 || (long long)H * E > (1 << 20)) return 0;
+  return align256((size_t)tla::heads_map(tokens, H, E).nbg * 2 * H * E * sizeof(float));
+}
+
+int tla_gate_heads_fwd(int dtype, long long tokens, int H, int E, const void* x, const void* xb,
+                       const float* A, const float* b, float* g, float* beta, void* stream) {
+  g_err[0] = 0;
+  int rc = heads_check(dtype, tokens, H, E);
+  if (rc) return rc;
+  if (!A || !b || (tokens > 0 && (!x || !g))) return fail(TLA_E_NULL, "x, A, b and g are required");
+  if ((xb == nullptr) != (beta == nullptr)) return fail(TLA_E_NULL, "xb and beta go together");
+  const void* ptrs[] = {x, xb, A, b, g, beta};
+  for (const void* p : ptrs)
+    if (misaligned(p)) return fail(TLA_E_ALIGN, "pointer %p is not 16-byte aligned", p);
+  const size_t es = dtype == TLA_BF16 ? 2 : 4, nx = (size_t)tokens * H * E, nb = (size_t)tokens * H;
+  const Range ins[] = {{x, nx * es}, {xb, xb ? nb * es : 0}, {A, (size_t)H * E * 4},
+                       {b, (size_t)H * E * 4}};
+  const Range outs[] = {{g, nx * 4}, {beta, beta ? nb * 4 : 0}};
+  for (const Range& a : outs)
+    for (const Range& c : ins)
+      if (overlap(a, c)) return fail(TLA_E_ALIAS, "g or beta overlaps an input");
+  if (overlap(outs[0], outs[1])) return fail(TLA_E_ALIAS, "g and beta overlap");
+  if (tokens == 0) return TLA_OK;
+  hipError_t e = timed(PROF_HEADS_FWD, (hipStream_t)stream, [&] {
+    return tla::launch_heads_fwd(dtype == TLA_BF16, tokens, H, E, x, xb, A, b, g, beta,
+                                 (hipStream_t)stream);
+  });
+  if (e != hipSuccess) return device_fail(e, "gate heads kernel");
+  return TLA_OK;
+}
+
+int tla_gate_heads_bwd(int dtype, long long tokens, int H, int E, const void* x, const void* xb,
+                       const float* A, const float* b, const float* dg, const float* dbeta,
+                       void* dx, void* dxb, float* dA, float* db, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+  g_err[0] = 0;
+  int rc = heads_check(dtype, tokens, H, E);
+  if (rc) return rc;
+  if (!A || !b || !dA || !db || (tokens > 0 && (!x || !dg || !dx)))
+    return fail(TLA_E_NULL, "x, A, b, dg, dx, dA and db are required");
+  if ((xb == nullptr) != (dbeta == nullptr) || (xb == nullptr) != (dxb == nullptr))
+    return fail(TLA_E_NULL, "xb, dbeta and dxb go together");
+  const void* ptrs[] = {x, xb, A, b, dg, dbeta, dx, dxb, dA, db, workspace};
+  for (const void* p : ptrs)
+    if (misaligned(p)) return fail(TLA_E_ALIGN, "pointer %p is not 16-byte aligned", p);
+  const size_t need = tla_gate_heads_workspace_bytes(tokens, H, E);
+  if (!workspace || workspace_bytes < need)
+    return fail(TLA_E_WORKSPACE, "workspace of %zu bytes needed", need);
+  const size_t es = dtype == TLA_BF16 ? 2 : 4, nx = (size_t)tokens * H * E, nb = (size_t)tokens * H;
+  const size_t np = (size_t)H * E * 4, nbb = xb ? nb : 0;
+  const Range ins[] = {{x, nx * es}, {xb, nbb * es}, {A, np}, {b, np}, {dg, nx * 4}, {dbeta, nbb * 4}};
+  const Range outs[] = {{dx, nx * es}, {dxb, nbb * es}, {dA, np}, {db, np}, {workspace, need}};
+  for (const Range& a : outs)
+    for (const Range& c : ins)
+      if (overlap(a, c)) return fail(TLA_E_ALIAS, "an output or the workspace overlaps an input");
+  for (int i = 0; i < 5; ++i)
+    for (int j = i + 1; j < 5; ++j)
+      if (overlap(outs[i], outs[j])) return fail(TLA_E_ALIAS, "two outputs overlap");
+  hipStream_t st = (hipStream_t)stream;
+  hipError_t e = timed(PROF_HEADS_BWD, st, [&] {
+    return tla::launch_heads_bwd(dtype == TLA_BF16, tokens, H, E, x, xb, A, b, dg, dbeta, dx, dxb,
+                                 dA, db, (float*)workspace, st);
+  });
+  if (e != hipSuccess) return device_fail(e, "gate heads backward kernel");
   return TLA_OK;
 }
 

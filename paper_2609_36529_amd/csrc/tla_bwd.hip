@@ -258,7 +258,6 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
   constexpr int NT = C / 16;
   constexpr int KT = KD / 16;
   constexpr int NTHR = NW * 64;
-  constexpr int E4 = (E + 3) & ~3;
   typedef typename Elem<T>::frag F;
   typedef RecSmem<T, KD, C, E, NW> Sm;
   // eight-wave instances (E = 16) have half the registers per lane: they load
@@ -268,7 +267,7 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
   extern __shared__ __align__(16) unsigned char smem_raw[];
   Sm& sm = *reinterpret_cast<Sm*>(smem_raw);
 
-  const int tid = threadIdx.x, w = wave_id(), l = lane_id(), g = l >> 4, n = l & 15;
+  const int w = wave_id(), l = lane_id(), g = l >> 4, n = l & 15;
   const int V = s.V;
   int head, vt;
   xcd_map(blockIdx.x, s.NH, V / 16, head, vt);
@@ -299,7 +298,6 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
   const T* Qg = (const T*)in.q + (tok0 * s.H + h) * KD;
   const T* dOg = (const T*)dOv + (tok0 * s.H + h) * (size_t)V + v0;
   const size_t krs = (size_t)s.H * KD;
-  const size_t vrs = (size_t)s.H * V;
 
   const bf16x4 idf = identity_frag();  // for the transposing dS' stores
   RecStage<T, KD, C, E, NTHR> stage;

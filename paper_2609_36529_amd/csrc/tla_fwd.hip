@@ -1325,7 +1325,6 @@ __global__ __launch_bounds__(512) void k_fwd_dual(Shape s, FwdIn in, PrepBufs p,
     for (int ci = 0; ci < nc; ++ci) {
       const int t0 = ci * C;
       const size_t ch = ch0 + ci;
-      const bool more = ci + 1 < nc;
       __syncthreads();  // B0
       if (t0 + C > s.T) zero_tail(t0);
 

@@ -169,6 +169,201 @@ static int gate_grid(long long rows, int V, long long cap) {
 }
 int gate_blocks(long long rows, int V) { return gate_grid(rows, V, 1024); }
 
+// ------------------------------------------------------------ gate heads
+// Alg. 2's forget gate and write strength from their pre-activations:
+//   g[n, h, e] = -exp(A[h, e]) softplus(x[n, h, e] + b[h, e])   (= log alpha <= 0)
+//   beta[n, h] = sigmoid(xb[n, h])
+// x is [tokens][HE] (HE = H * E columns).  Thread t of a g workgroup owns
+// column c = t % HE and token row r = t / HE of each run of R = 256 / HE
+// consecutive tokens (HE >= 256: R = 1, columns t, t + 256, ...); a workgroup
+// covers U runs, R U tokens, and issues all U loads of a thread before any
+// arithmetic.  The backward's per-column sums (dA, db) are therefore formed in
+// a fixed order: each thread over its U tokens, then over the R rows of the
+// workgroup, then one workgroup per column over the workgroups.  Workgroups
+// past the g ones handle beta, HEAD_BPT consecutive (token, head) values per
+// thread.
+constexpr int HEAD_UMAX = 8;  // token runs per workgroup, at most
+constexpr int HEAD_BPT = 4;   // beta values per thread
+
+__device__ __forceinline__ float softplusf_(float y) { return y > 20.f ? y : log1pf(__expf(y)); }
+
+HeadsMap heads_map(long long tokens, int H, int E) {
+  HeadsMap m;
+  const long long HE = (long long)H * E;
+  m.R = HE >= GATE_NTHR ? 1 : GATE_NTHR / (int)HE;
+  m.U = HEAD_UMAX;  // fewer runs per workgroup while that leaves under 1024 workgroups
+  while (m.U > 1 && (tokens + (long long)m.R * m.U - 1) / ((long long)m.R * m.U) < 1024) m.U /= 2;
+  const long long nbg = (tokens + (long long)m.R * m.U - 1) / ((long long)m.R * m.U);
+  m.nbg = nbg < 1 ? 1 : nbg;
+  m.nbb = (tokens * H + GATE_NTHR * HEAD_BPT - 1) / (GATE_NTHR * HEAD_BPT);
+  return m;
+}
+
+template <typename T>
+__global__ __launch_bounds__(GATE_NTHR) void k_heads_fwd(long long tokens, int H, int HE, int R, int U,
+                                                         int nbg, const T* x, const T* xb, const float* A,
+                                                         const float* b, float* g, float* beta) {
+  const int t = threadIdx.x;
+  if ((int)blockIdx.x >= nbg) {  // write strength
+    const long long NB = tokens * H;
+    const long long j0 = ((long long)(blockIdx.x - nbg) * GATE_NTHR + t) * HEAD_BPT;
+#pragma unroll
+    for (int k = 0; k < HEAD_BPT; ++k)
+      if (j0 + k < NB) beta[j0 + k] = sigmoidf_(Elem<T>::to_f(xb[j0 + k]));
+    return;
+  }
+  const bool wide = HE >= GATE_NTHR;
+  const int r = wide ? 0 : t / HE;
+  if (r >= R) return;
+  const long long n0 = (long long)blockIdx.x * R * U + r;
+  for (int c = wide ? t : t % HE; c < HE; c += GATE_NTHR) {
+    const float ea = __expf(A[c]), bc = b[c];
+    float xv[HEAD_UMAX];
+#pragma unroll
+    for (int u = 0; u < HEAD_UMAX; ++u) {
+      const long long n = n0 + (long long)u * R;
+      xv[u] = (u < U && n < tokens) ? Elem<T>::to_f(x[n * HE + c]) : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < HEAD_UMAX; ++u) {
+      const long long n = n0 + (long long)u * R;
+      if (u < U && n < tokens) g[n * HE + c] = -ea * softplusf_(xv[u] + bc);
+    }
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(GATE_NTHR) void k_heads_bwd(long long tokens, int H, int HE, int R, int U,
+                                                         int nbg, const T* x, const T* xb, const float* A,
+                                                         const float* b, const float* dg,
+                                                         const float* dbeta, T* dx, T* dxb,
+                                                         float* part) {
+  const int t = threadIdx.x;
+  if ((int)blockIdx.x >= nbg) {  // write strength: dxb = dbeta sigmoid'(xb)
+    const long long NB = tokens * H;
+    const long long j0 = ((long long)(blockIdx.x - nbg) * GATE_NTHR + t) * HEAD_BPT;
+#pragma unroll
+    for (int k = 0; k < HEAD_BPT; ++k)
+      if (j0 + k < NB) {
+        // beta (1 - beta) as sigmoid(x) sigmoid(-x): no cancellation once beta rounds to 1
+        const float xv = Elem<T>::to_f(xb[j0 + k]);
+        dxb[j0 + k] = Elem<T>::from_f(dbeta[j0 + k] * sigmoidf_(xv) * sigmoidf_(-xv));
+      }
+    return;
+  }
+  __shared__ float red[2][GATE_NTHR];
+  const bool wide = HE >= GATE_NTHR;
+  const int r = wide ? 0 : t / HE;
+  const long long n0 = (long long)blockIdx.x * R * U + r;
+  float* pa = part + (size_t)blockIdx.x * 2 * HE;  // this workgroup's partials of dA, then db
+  for (int c = wide ? t : t % HE; c < HE; c += GATE_NTHR) {
+    float sa = 0.f, sb = 0.f;
+    if (r < R) {
+      const float ea = __expf(A[c]), bc = b[c];
+      float xv[HEAD_UMAX], dv[HEAD_UMAX];
+#pragma unroll
+      for (int u = 0; u < HEAD_UMAX; ++u) {
+        const long long n = n0 + (long long)u * R;
+        const bool ok = u < U && n < tokens;
+        xv[u] = ok ? Elem<T>::to_f(x[n * HE + c]) : 0.f;
+        dv[u] = ok ? dg[n * HE + c] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < HEAD_UMAX; ++u) {
+        const long long n = n0 + (long long)u * R;
+        if (u < U && n < tokens) {
+          const float y = xv[u] + bc;
+          const float dxx = -dv[u] * ea * sigmoidf_(y);
+          dx[n * HE + c] = Elem<T>::from_f(dxx);
+          sa += dv[u] * (-ea * softplusf_(y));
+          sb += dxx;
+        }
+      }
+    }
+    if (wide) {  // one row: the thread's sums are the workgroup's
+      pa[c] = sa;
+      pa[HE + c] = sb;
+    } else {  // sum the R rows of column c in row order
+      red[0][t] = sa;
+      red[1][t] = sb;
+      __syncthreads();
+      if (t < HE) {
+        float a = 0.f, bb = 0.f;
+        for (int q = 0; q < R; ++q) {
+          a += red[0][q * HE + t];
+          bb += red[1][q * HE + t];
+        }
+        pa[t] = a;
+        pa[HE + t] = bb;
+      }
+    }
+  }
+}
+
+// dA[c], db[c]: one workgroup per column, fixed-order sums of the partials
+__global__ __launch_bounds__(GATE_NTHR) void k_heads_sum(int nblocks, int HE, const float* part,
+                                                         float* dA, float* db) {
+  __shared__ float red[2][GATE_NTHR];
+  const int c = blockIdx.x, t = threadIdx.x;
+  float a = 0.f, bb = 0.f;
+  for (int k = t; k < nblocks; k += GATE_NTHR) {
+    a += part[((size_t)k * 2 + 0) * HE + c];
+    bb += part[((size_t)k * 2 + 1) * HE + c];
+  }
+  red[0][t] = a;
+  red[1][t] = bb;
+  __syncthreads();
+#pragma unroll
+  for (int m = GATE_NTHR / 2; m > 0; m >>= 1) {
+    if (t < m) {
+      red[0][t] += red[0][t + m];
+      red[1][t] += red[1][t + m];
+    }
+    __syncthreads();
+  }
+  if (t == 0) {
+    dA[c] = red[0][0];
+    db[c] = red[1][0];
+  }
+}
+
+hipError_t launch_heads_fwd(bool bf16, long long tokens, int H, int E, const void* x, const void* xb,
+                            const float* A, const float* b, float* g, float* beta, hipStream_t st) {
+  const HeadsMap m = heads_map(tokens, H, E);
+  const long long nbb = xb ? m.nbb : 0;
+  if (m.nbg + nbb > 0x7fffffffLL) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)(m.nbg + nbb));
+  if (bf16)
+    hipLaunchKernelGGL(k_heads_fwd<bf16_t>, grid, dim3(GATE_NTHR), 0, st, tokens, H, H * E, m.R, m.U,
+                       (int)m.nbg, (const bf16_t*)x, (const bf16_t*)xb, A, b, g, beta);
+  else
+    hipLaunchKernelGGL(k_heads_fwd<float>, grid, dim3(GATE_NTHR), 0, st, tokens, H, H * E, m.R, m.U,
+                       (int)m.nbg, (const float*)x, (const float*)xb, A, b, g, beta);
+  return hipGetLastError();
+}
+
+hipError_t launch_heads_bwd(bool bf16, long long tokens, int H, int E, const void* x, const void* xb,
+                            const float* A, const float* b, const float* dg, const float* dbeta,
+                            void* dx, void* dxb, float* dA, float* db, float* part, hipStream_t st) {
+  const HeadsMap m = heads_map(tokens, H, E);
+  const long long nbb = xb ? m.nbb : 0;
+  if (m.nbg + nbb > 0x7fffffffLL) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)(m.nbg + nbb));
+  if (bf16)
+    hipLaunchKernelGGL(k_heads_bwd<bf16_t>, grid, dim3(GATE_NTHR), 0, st, tokens, H, H * E, m.R, m.U,
+                       (int)m.nbg, (const bf16_t*)x, (const bf16_t*)xb, A, b, dg, dbeta, (bf16_t*)dx,
+                       (bf16_t*)dxb, part);
+  else
+    hipLaunchKernelGGL(k_heads_bwd<float>, grid, dim3(GATE_NTHR), 0, st, tokens, H, H * E, m.R, m.U,
+                       (int)m.nbg, (const float*)x, (const float*)xb, A, b, dg, dbeta, (float*)dx,
+                       (float*)dxb, part);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_heads_sum, dim3(H * E), dim3(GATE_NTHR), 0, st, (int)m.nbg, H * E, part, dA, db);
+  return hipGetLastError();
+}
+
+
 template <typename T>
 static hipError_t gate_fwd_t(long long rows, int V, const void* o, const void* z, const float* w,
                              float eps, void* y, hipStream_t st) {

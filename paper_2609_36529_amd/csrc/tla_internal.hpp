@@ -118,6 +118,18 @@ hipError_t launch_gate_bwd(bool bf16, long long rows, int V, const void* o, cons
                            const float* w, float eps, const void* dy, void* d_o, void* dz,
                            float* dw_part, hipStream_t st);
 hipError_t launch_gate_dw(long long rows, int V, const float* dw_part, float* dw, hipStream_t st);
+// The gate heads (log forget gate, write strength) from their pre-activations.
+struct HeadsMap {
+  int R, U;       // token rows side by side, runs per workgroup
+  long long nbg;  // workgroups for g (= sets of dA, db partials)
+  long long nbb;  // workgroups for beta
+};
+HeadsMap heads_map(long long tokens, int H, int E);
+hipError_t launch_heads_fwd(bool bf16, long long tokens, int H, int E, const void* x, const void* xb,
+                            const float* A, const float* b, float* g, float* beta, hipStream_t st);
+hipError_t launch_heads_bwd(bool bf16, long long tokens, int H, int E, const void* x, const void* xb,
+                            const float* A, const float* b, const float* dg, const float* dbeta,
+                            void* dx, void* dxb, float* dA, float* db, float* part, hipStream_t st);
 
 // Which (K, C, E) combinations have kernel instances, and whether the
 // forward/backward shared-memory plan of an instance fits 160 KiB.

@@ -231,3 +231,49 @@ def test_out_gate_validation():
     assert bwd(dw=None) == E_NULL
     assert bwd(dz=dy) == E_ALIAS
     assert bwd(dz=do_) == E_ALIAS
+
+
+def test_gate_heads_validation():
+    """Gate heads: dtype, shape, required and paired pointers, alignment,
+    aliasing and workspace are checked on the host (fake addresses, nothing
+    launched)."""
+    L = tla.lib()
+    P = ctypes.c_void_p
+    x, xb, A, b, g, beta = (P(FAKE + i * 0x1000000) for i in range(6))
+    n, H, E = 1000, 8, 8
+
+    def fwd(dtype=tla.BF16, n_=n, H_=H, E_=E, **kw):
+        a = dict(x=x, xb=xb, A=A, b=b, g=g, beta=beta)
+        a.update(kw)
+        return L.tla_gate_heads_fwd(dtype, n_, H_, E_, a["x"], a["xb"], a["A"], a["b"], a["g"], a["beta"],
+                                    None)
+    assert fwd(dtype=7) == E_SHAPE
+    assert fwd(n_=-1) == E_SHAPE
+    assert fwd(H_=0) == E_SHAPE
+    assert fwd(E_=0) == E_SHAPE
+    assert fwd(H_=2048, E_=1024) == E_SHAPE
+    assert fwd(A=None) == E_NULL
+    assert fwd(g=None) == E_NULL
+    assert fwd(beta=None) == E_NULL      # xb without beta
+    assert fwd(xb=None) == E_NULL        # beta without xb
+    assert fwd(g=P(FAKE + 4)) == E_ALIGN
+    assert fwd(g=x) == E_ALIAS
+    assert fwd(beta=g) == E_ALIAS
+    need = L.tla_gate_heads_workspace_bytes(n, H, E)
+    assert need >= 2 * H * E * 4 and need % 256 == 0
+    assert L.tla_gate_heads_workspace_bytes(n, 0, E) == 0
+    dg, dbeta, dx, dxb, dA, db = (P(FAKE + 0x8000000 + i * 0x1000000) for i in range(6))
+    ws = P(FAKE + 0x10000000)
+
+    def bwd(ws_bytes=need, **kw):
+        a = dict(xb=xb, dg=dg, dbeta=dbeta, dx=dx, dxb=dxb, dA=dA, db=db, ws=ws)
+        a.update(kw)
+        return L.tla_gate_heads_bwd(tla.F32, n, H, E, x, a["xb"], A, b, a["dg"], a["dbeta"], a["dx"],
+                                    a["dxb"], a["dA"], a["db"], a["ws"], ws_bytes, None)
+    assert bwd(ws_bytes=need - 1) == E_WS
+    assert bwd(ws=None) == E_WS
+    assert bwd(dA=None) == E_NULL
+    assert bwd(dxb=None) == E_NULL
+    assert bwd(dx=dg) == E_ALIAS
+    assert bwd(db=dA) == E_ALIAS
+    assert bwd(ws=dx) == E_ALIAS
