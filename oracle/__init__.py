@@ -9,8 +9,9 @@ shares no code with it.
 Eq. la3 and the mixer of Alg. 2).  ``forms`` holds independent numpy
 formulations used to pin it (flattened joint key, dyadic special case,
 quadratic form, chunkwise form).  ``gate`` is the mixer's output side
-(RMSNorm times a sigmoid gate) and ``heads`` its gate heads (forget gate and
-write strength), both in numpy.
+(RMSNorm times a sigmoid gate), ``heads`` its gate heads (forget gate and
+write strength) and ``conv_in`` its input side after the projection GEMM
+(causal depthwise convolution, activations, L2 normalisation), all in numpy.
 """
 import ctypes
 import os
@@ -20,6 +21,7 @@ import numpy as np
 from . import build as _build
 from .gate import out_gate_bwd, out_gate_fwd  # noqa: F401
 from .heads import gate_heads_bwd, gate_heads_fwd  # noqa: F401
+from .conv_in import conv_in_bwd, conv_in_fwd  # noqa: F401
 
 SGLA, GDN = 0, 1
 _HERE = os.path.dirname(os.path.abspath(__file__))
