@@ -399,6 +399,58 @@ def heads_bench(steps, warmup):
           flush=True)
 
 
+def conv_bench(steps, warmup):
+    """The mixer's input side after the projection GEMM (causal depthwise
+    convolution of width 4, SiLU / softplus, L2 normalisation) forward and
+    backward at the metric shape: B4 T4096 H8 K=V=128 E=8, bf16, Ctot = 3200
+    channels per token.  HBM-bound; algorithmic bytes per token and channel:
+    forward 2 + 2 (y read, output written), backward 2 + 2 + 2 (y and the
+    output gradient read, dy written), plus the fp32 tap-gradient partials
+    (written and read once)."""
+    import torch
+    import paper_2609_36529_amd as tla
+    B, T, H, K, V, E, W = 4, 4096, 8, 128, 128, 8, 4
+    C = H * (2 * K + V + 2 * E)
+    gen = torch.Generator().manual_seed(23)
+    y = torch.randn(B, T, C, generator=gen).to(torch.bfloat16).cuda()
+    w = ((torch.rand(W, C, generator=gen) * 2 - 1) / W ** 0.5).float().cuda()
+    grads = tuple(torch.randn(B, T, H, d, generator=gen).to(torch.bfloat16).cuda() for d in (K, K, V, E, E))
+
+    def one():
+        tla.conv_in_fwd(y, w, H, K, V, E)
+        tla.conv_in_bwd(y, w, H, K, V, E, grads)
+    for _ in range(warmup):
+        one()
+    torch.cuda.synchronize()
+    tla.prof_enable(True)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        one()
+    torch.cuda.synchronize()
+    elapsed = (time.perf_counter() - t0) / steps
+    prof = tla.prof_read()
+    tla.prof_enable(False)
+    kern = {k: round(v[0] / v[1], 4) for k, v in prof.items() if v[1]}
+    n = B * T
+    parts = (B * ((T + 31) // 32) + 3) // 4
+    bytes_fwd = 4 * n * C
+    bytes_bwd = 6 * n * C + 2 * parts * W * C * 4
+    gbs_f = bytes_fwd / (kern["conv_in_fwd"] * 1e-3) / 1e9
+    gbs_b = bytes_bwd / (kern["conv_in_bwd"] * 1e-3) / 1e9
+    print(json.dumps({
+        "metric": "input side fwd+bwd tokens/s, B4 T4096 H8 K=V=128 E=8 W4", "value": round(n / elapsed, 1),
+        "unit": "tokens/s", "n_gpus": 1, "steps": steps, "warmup": warmup,
+        "ms_per_step": round(1e3 * elapsed, 4), "higher_is_better": True, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "causal depthwise conv + SiLU/softplus + L2 norm, forward and backward",
+                   "tokens": n, "channels": C, "taps": W},
+        "kernels_ms": kern,
+        "roofline": {"bound": "hbm", "achieved": round(gbs_b, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(gbs_b / PEAK_HBM_GBS, 4), "kernel": "conv_in_bwd",
+                     "forward_gbs": round(gbs_f, 1), "forward_frac": round(gbs_f / PEAK_HBM_GBS, 4)}}),
+          flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -413,6 +465,8 @@ def main():
                     help="time the output gate (RMSNorm x sigmoid) forward and backward")
     ap.add_argument("--heads", action="store_true",
                     help="time the gate heads (forget gate, write strength) forward and backward")
+    ap.add_argument("--conv", action="store_true",
+                    help="time the input side (short convolution, activations, L2 norm) forward and backward")
     ap.add_argument("--forward", metavar="NAME",
                     help="time the inference forward of sgla_bf16, gdn_bf16 or gdn_long_bf16")
     args = ap.parse_args()
@@ -435,6 +489,9 @@ def main():
         return
     if args.heads:
         heads_bench(args.steps, args.warmup)
+        return
+    if args.conv:
+        conv_bench(args.steps, args.warmup)
         return
     if args.forward:
         forward_bench(args.forward, args.steps, args.warmup)

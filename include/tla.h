@@ -242,16 +242,53 @@ int tla_gate_heads_bwd(int dtype, long long tokens, int H, int E, const void* x,
                        size_t workspace_bytes, void* stream);
 
 /*
+ * The input side of the mixer after its projection GEMM (section "Input
+ * projections", Alg. 2): one causal depthwise convolution over the channels
+ * of q, k, v, q' and k' of every head, SiLU on the q, k, v channels and
+ * softplus on the q', k' channels, then q, k, q', k' each divided by its
+ * Euclidean norm per token and head (x / sqrt(sum x^2 + eps)); v is not
+ * normalised.  The results are tla_fwd's q, k, v, q2, k2.
+ *   y   [B][T][Ctot], Ctot = H (2K + V + 2E): the GEMM output, channel blocks
+ *       q | k | v | q' | k' in that order, each head-major ([H][K], [H][K],
+ *       [H][V], [H][E], [H][E]);
+ *   w   [W][Ctot] fp32 taps (no bias): the output at token t is
+ *       sum_j w[j] y[t - (W - 1) + j] over tokens of the same batch row,
+ *       tokens before t = 0 counting as zero;
+ *   q, k [B][T][H][K]; v [B][T][H][V]; q2, k2 [B][T][H][E].
+ * y, outputs and their gradients have element type dtype (TLA_F32 or
+ * TLA_BF16).  K and E are each one of 8, 16, 32, 64, 128, 256; V a multiple
+ * of 8 up to 1024; W 1 to 4; H (2K + V) / 8 a multiple of E / 8
+ * (TLA_E_UNSUPPORTED otherwise); B, T >= 0, 1 <= H <= 1024, eps >= 0
+ * finite.  Device pointers, 16-byte aligned, outputs not overlapping any
+ * input; arrays of zero size may be NULL.  Asynchronous on `stream`.
+ *
+ * tla_conv_in_bwd: given dq, dk, dv, dq2, dk2 (gradients of the outputs),
+ * writes dy [B][T][Ctot] and dw [W][Ctot] (fp32, summed over all tokens in a
+ * fixed order: bitwise reproducible).  It needs a device workspace of
+ * tla_conv_in_workspace_bytes(...) bytes (per-workgroup partials of dw;
+ * TLA_E_WORKSPACE if smaller), owned by the caller, free again when the
+ * call's work on `stream` is done.
+ */
+int tla_conv_in_fwd(int dtype, int B, int T, int H, int K, int V, int E, int W, float eps,
+                    const void* y, const float* w, void* q, void* k, void* v, void* q2, void* k2,
+                    void* stream);
+size_t tla_conv_in_workspace_bytes(int B, int T, int H, int K, int V, int E, int W);
+int tla_conv_in_bwd(int dtype, int B, int T, int H, int K, int V, int E, int W, float eps,
+                    const void* y, const float* w, const void* dq, const void* dk, const void* dv,
+                    const void* dq2, const void* dk2, void* dy, float* dw, void* workspace,
+                    size_t workspace_bytes, void* stream);
+
+/*
  * Per-kernel timing, for diagnostics and benchmarks (not needed otherwise).
  * tla_prof_enable(1) clears previous records and starts bracketing every
  * kernel launch of the library with a pair of HIP events on the launch
  * stream (events are created once and pooled); tla_prof_enable(0) stops and
  * clears.  tla_prof_read() waits for the recorded events and fills, for each
- * of the 11 kernel kinds named by tla_prof_name(0..10) ("prep",
+ * of the 13 kernel kinds named by tla_prof_name(0..12) ("prep",
  * "fwd_recurrent", "bwd_recurrent", "bwd_state", "bwd_chunk", "step",
  * "out_gate_fwd", "out_gate_bwd", "out_gate_dw", "gate_heads_fwd",
- * "gate_heads_bwd"), the summed event time in milliseconds and the number of
- * launches; n must be at least 11.  Not meant
+ * "gate_heads_bwd", "conv_in_fwd", "conv_in_bwd"), the summed event time in
+ * milliseconds and the number of launches; n must be at least 13.  Not meant
  * for use while another thread launches.
  */
 int tla_prof_enable(int on);

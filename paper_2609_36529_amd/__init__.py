@@ -34,7 +34,7 @@ class TLAError(RuntimeError):
     pass
 
 
-PROF_SLOTS = 11  # kernel kinds of tla_prof_read
+PROF_SLOTS = 13  # kernel kinds of tla_prof_read
 
 
 def lib():
@@ -81,6 +81,12 @@ def lib():
     L.tla_gate_heads_workspace_bytes.restype = S
     L.tla_gate_heads_bwd.argtypes = [I, LL, I, I] + [P] * 11 + [S, P]
     L.tla_gate_heads_bwd.restype = I
+    L.tla_conv_in_fwd.argtypes = [I] * 8 + [ctypes.c_float] + [P] * 8
+    L.tla_conv_in_fwd.restype = I
+    L.tla_conv_in_workspace_bytes.argtypes = [I] * 7
+    L.tla_conv_in_workspace_bytes.restype = S
+    L.tla_conv_in_bwd.argtypes = [I] * 8 + [ctypes.c_float] + [P] * 10 + [S, P]
+    L.tla_conv_in_bwd.restype = I
     L.tla_prof_enable.argtypes = [I]
     L.tla_prof_enable.restype = I
     L.tla_prof_read.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I), I]
@@ -355,6 +361,51 @@ def gate_heads_bwd(x, xb, A, b, dg, dbeta):
                                 _ptr(dbeta), _ptr(dx), _ptr(dxb), _ptr(dA), _ptr(db), _ptr(ws),
                                 ws.numel(), _stream(dev)))
     return dx, dxb, dA, db
+
+
+def _conv_shape(y, w, H, K, V, E):
+    _need(y, "y")
+    dev = y.device
+    if y.dim() != 3 or y.shape[-1] != H * (2 * K + V + 2 * E):
+        raise ValueError("y must be [B, T, H (2K + V + 2E)]")
+    _need(w, "w", torch.float32, dev)
+    if w.dim() != 2 or w.shape[1] != y.shape[-1]:
+        raise ValueError("w must be [W, Ctot]")
+    return y.shape[0], y.shape[1], w.shape[0], dev
+
+
+def conv_in_fwd(y, w, H, K, V, E, eps=1e-6):
+    """The mixer's input side after the projection GEMM (section "Input
+    projections", Alg. 2): causal depthwise convolution with taps w [W, Ctot]
+    over y [B, T, Ctot] (channel blocks q | k | v | q' | k', head-major), SiLU
+    on q, k, v, softplus on q', k', L2 normalisation of q, k, q', k'.
+    Returns (q, k, v, q2, k2) as [B, T, H, .] tensors of y's dtype.  Runs
+    tla_conv_in_fwd."""
+    B, T, W, dev = _conv_shape(y, w, H, K, V, E)
+    outs = [torch.empty((B, T, H, d), dtype=y.dtype, device=dev) for d in (K, K, V, E, E)]
+    _check(lib().tla_conv_in_fwd(_dtype_code(y.dtype), B, T, H, K, V, E, W, float(eps), _ptr(y), _ptr(w),
+                                 *[_ptr(o) for o in outs], _stream(dev)))
+    return tuple(outs)
+
+
+def conv_in_bwd(y, w, H, K, V, E, grads, eps=1e-6):
+    """Gradients (dy, dw) of the input side for the outputs' gradients
+    grads = (dq, dk, dv, dq2, dk2); dw is summed over all tokens in a fixed
+    order.  Runs tla_conv_in_bwd."""
+    B, T, W, dev = _conv_shape(y, w, H, K, V, E)
+    for gr, d, nm in zip(grads, (K, K, V, E, E), ("dq", "dk", "dv", "dq2", "dk2")):
+        _need(gr, nm, y.dtype, dev)
+        if tuple(gr.shape) != (B, T, H, d):
+            raise ValueError(f"{nm} must be [B, T, H, {d}]")
+    dy = torch.empty_like(y)
+    dw = torch.empty_like(w)
+    L = lib()
+    ws = torch.empty(max(L.tla_conv_in_workspace_bytes(B, T, H, K, V, E, W), 256), dtype=torch.uint8,
+                     device=dev)
+    _check(L.tla_conv_in_bwd(_dtype_code(y.dtype), B, T, H, K, V, E, W, float(eps), _ptr(y), _ptr(w),
+                             *[_ptr(g) for g in grads], _ptr(dy), _ptr(dw), _ptr(ws), ws.numel(),
+                             _stream(dev)))
+    return dy, dw
 
 
 def prof_enable(on=True):

@@ -176,11 +176,13 @@ int device_fail(hipError_t e, const char* what) {
 // bracketed by a pair of HIP events recorded on the launch stream.  Events are
 // pooled and reused; nothing is recorded when timing is off.
 enum { PROF_PREP, PROF_FWD, PROF_BWD_REC, PROF_BWD_STATE, PROF_BWD_CHUNK, PROF_STEP,
-       PROF_GATE_FWD, PROF_GATE_BWD, PROF_GATE_DW, PROF_HEADS_FWD, PROF_HEADS_BWD, PROF_N };
+       PROF_GATE_FWD, PROF_GATE_BWD, PROF_GATE_DW, PROF_HEADS_FWD, PROF_HEADS_BWD,
+       PROF_CONV_FWD, PROF_CONV_BWD, PROF_N };
 const char* const kProfNames[PROF_N] = {"prep",         "fwd_recurrent",  "bwd_recurrent",
                                         "bwd_state",    "bwd_chunk",      "step",
                                         "out_gate_fwd", "out_gate_bwd",   "out_gate_dw",
-                                        "gate_heads_fwd", "gate_heads_bwd"};
+                                        "gate_heads_fwd", "gate_heads_bwd", "conv_in_fwd",
+                                        "conv_in_bwd"};
 struct ProfRec {
   int kind;
   hipEvent_t a, b;
@@ -602,6 +604,98 @@ int tla_gate_heads_bwd(int dtype, long long tokens, int H, int E, const void* x,
                                  dA, db, (float*)workspace, st);
   });
   if (e != hipSuccess) return device_fail(e, "gate heads backward kernel");
+  return TLA_OK;
+}
+
+// ------------------------------------------------ input side of the mixer
+static bool pow2_8_256(int x) { return x >= 8 && x <= 256 && (x & (x - 1)) == 0; }
+
+static int conv_check(int dtype, int B, int T, int H, int K, int V, int E, int W, float eps) {
+  if (dtype != TLA_F32 && dtype != TLA_BF16) return fail(TLA_E_SHAPE, "dtype %d", dtype);
+  if (B < 0 || T < 0 || H < 1 || H > 1024) return fail(TLA_E_SHAPE, "B = %d, T = %d, H = %d", B, T, H);
+  if (!pow2_8_256(K) || !pow2_8_256(E))
+    return fail(TLA_E_UNSUPPORTED, "K = %d, E = %d (each one of 8, 16, ..., 256)", K, E);
+  if (V < 8 || V > 1024 || V % 8) return fail(TLA_E_UNSUPPORTED, "V = %d (a multiple of 8 up to 1024)", V);
+  if (W < 1 || W > 4) return fail(TLA_E_UNSUPPORTED, "W = %d (1 to 4 taps)", W);
+  if ((H * (2 * K + V) / 8) % (E / 8))
+    return fail(TLA_E_UNSUPPORTED, "H (2K + V) / 8 = %d is not a multiple of E / 8", H * (2 * K + V) / 8);
+  if (!(eps >= 0.f) || eps > 3.4e38f) return fail(TLA_E_SHAPE, "eps must be finite and >= 0");
+  if ((double)B * T * H * (2.0 * K + V + 2.0 * E) > 4e15) return fail(TLA_E_SHAPE, "problem too large");
+  return TLA_OK;
+}
+
+size_t tla_conv_in_workspace_bytes(int B, int T, int H, int K, int V, int E, int W) {
+  if (B < 0 || T < 0 || H < 1 || K < 1 || V < 1 || E < 1 || W < 1 || W > 4) return 0;
+  const tla::ConvArgs a = tla::conv_args(B, T, H, K, V, E, W, 0.f, true);
+  return align256((size_t)tla::conv_parts(a) * W * a.Ctot * sizeof(float));
+}
+
+int tla_conv_in_fwd(int dtype, int B, int T, int H, int K, int V, int E, int W, float eps,
+                    const void* y, const float* w, void* q, void* k, void* v, void* q2, void* k2,
+                    void* stream) {
+  g_err[0] = 0;
+  int rc = conv_check(dtype, B, T, H, K, V, E, W, eps);
+  if (rc) return rc;
+  const size_t n = (size_t)B * T * H, es = dtype == TLA_BF16 ? 2 : 4;
+  if (!w || (n > 0 && (!y || !q || !k || !v || !q2 || !k2)))
+    return fail(TLA_E_NULL, "y, w, q, k, v, q2 and k2 are required");
+  const void* ptrs[] = {y, w, q, k, v, q2, k2};
+  for (const void* p : ptrs)
+    if (misaligned(p)) return fail(TLA_E_ALIGN, "pointer %p is not 16-byte aligned", p);
+  const size_t C = (size_t)(2 * K + V + 2 * E);  // channels per token and head
+  const Range ins[] = {{y, n * C * es}, {w, (size_t)W * H * C * 4}};
+  const Range outs[] = {{q, n * K * es}, {k, n * K * es}, {v, n * V * es}, {q2, n * E * es},
+                        {k2, n * E * es}};
+  for (const Range& a : outs)
+    for (const Range& b : ins)
+      if (overlap(a, b)) return fail(TLA_E_ALIAS, "an output overlaps an input");
+  for (int i = 0; i < 5; ++i)
+    for (int j = i + 1; j < 5; ++j)
+      if (overlap(outs[i], outs[j])) return fail(TLA_E_ALIAS, "two outputs overlap");
+  if (n == 0) return TLA_OK;
+  const tla::ConvArgs a = tla::conv_args(B, T, H, K, V, E, W, eps, false);
+  void* const out[5] = {q, k, v, q2, k2};
+  hipError_t e = timed(PROF_CONV_FWD, (hipStream_t)stream, [&] {
+    return tla::launch_conv_fwd(dtype == TLA_BF16, a, y, w, out, (hipStream_t)stream);
+  });
+  if (e != hipSuccess) return device_fail(e, "input-side convolution kernel");
+  return TLA_OK;
+}
+
+int tla_conv_in_bwd(int dtype, int B, int T, int H, int K, int V, int E, int W, float eps,
+                    const void* y, const float* w, const void* dq, const void* dk, const void* dv,
+                    const void* dq2, const void* dk2, void* dy, float* dw, void* workspace,
+                    size_t workspace_bytes, void* stream) {
+  g_err[0] = 0;
+  int rc = conv_check(dtype, B, T, H, K, V, E, W, eps);
+  if (rc) return rc;
+  const size_t n = (size_t)B * T * H, es = dtype == TLA_BF16 ? 2 : 4;
+  if (!w || !dw || (n > 0 && (!y || !dq || !dk || !dv || !dq2 || !dk2 || !dy)))
+    return fail(TLA_E_NULL, "y, w, dq, dk, dv, dq2, dk2, dy and dw are required");
+  const void* ptrs[] = {y, w, dq, dk, dv, dq2, dk2, dy, dw, workspace};
+  for (const void* p : ptrs)
+    if (misaligned(p)) return fail(TLA_E_ALIGN, "pointer %p is not 16-byte aligned", p);
+  const size_t need = tla_conv_in_workspace_bytes(B, T, H, K, V, E, W);
+  if (!workspace || workspace_bytes < need)
+    return fail(TLA_E_WORKSPACE, "workspace of %zu bytes needed", need);
+  const size_t C = (size_t)(2 * K + V + 2 * E);
+  const Range ins[] = {{y, n * C * es},       {w, (size_t)W * H * C * 4}, {dq, n * K * es},
+                       {dk, n * K * es},      {dv, n * V * es},           {dq2, n * E * es},
+                       {dk2, n * E * es}};
+  const Range outs[] = {{dy, n * C * es}, {dw, (size_t)W * H * C * 4}, {workspace, need}};
+  for (const Range& a : outs)
+    for (const Range& b : ins)
+      if (overlap(a, b)) return fail(TLA_E_ALIAS, "an output or the workspace overlaps an input");
+  for (int i = 0; i < 3; ++i)
+    for (int j = i + 1; j < 3; ++j)
+      if (overlap(outs[i], outs[j])) return fail(TLA_E_ALIAS, "two outputs overlap");
+  const tla::ConvArgs a = tla::conv_args(B, T, H, K, V, E, W, eps, true);
+  const void* const dout[5] = {dq, dk, dv, dq2, dk2};
+  hipStream_t st = (hipStream_t)stream;
+  hipError_t e = timed(PROF_CONV_BWD, st, [&] {
+    return tla::launch_conv_bwd(dtype == TLA_BF16, a, y, w, dout, dy, dw, (float*)workspace, st);
+  });
+  if (e != hipSuccess) return device_fail(e, "input-side convolution backward kernel");
   return TLA_OK;
 }
 

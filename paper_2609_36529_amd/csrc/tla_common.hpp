@@ -712,4 +712,37 @@ __device__ __forceinline__ void xcd_map(int bid, int nheads, int ntiles, int& he
   }
 }
 
+// Row kernels: eight consecutive values of a row held by one lane, as bf16
+// (one 16-byte access) or fp32 (two).
+template <typename T>
+__device__ __forceinline__ void load8(const T* p, float (&x)[8]) {
+  if constexpr (sizeof(T) == 2) {
+    const uint4 u = *(const uint4*)p;
+    const bf16x8 b = __builtin_bit_cast(bf16x8, u);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] = (float)b[i];
+  } else {
+    const f32x4 a = *(const f32x4*)p, c = *(const f32x4*)(p + 4);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      x[i] = a[i];
+      x[4 + i] = c[i];
+    }
+  }
+}
+template <typename T>
+__device__ __forceinline__ void store8(T* p, const float (&x)[8]) {
+  if constexpr (sizeof(T) == 2) {
+    bf16x8 b;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) b[i] = (__bf16)x[i];
+    *(uint4*)p = __builtin_bit_cast(uint4, b);
+  } else {
+    *(f32x4*)p = f32x4{x[0], x[1], x[2], x[3]};
+    *(f32x4*)(p + 4) = f32x4{x[4], x[5], x[6], x[7]};
+  }
+}
+__device__ __forceinline__ float sigmoidf_(float z) { return 1.f / (1.f + __expf(-z)); }
+__device__ __forceinline__ float softplusf_(float y) { return y > 20.f ? y : log1pf(__expf(y)); }
+
 }  // namespace tla

@@ -16,35 +16,6 @@ namespace tla {
 
 constexpr int GATE_NTHR = 256;  // four waves
 
-// eight values of a row: bf16 (one 16-byte access) or fp32 (two)
-template <typename T>
-__device__ __forceinline__ void gate_load8(const T* p, float (&x)[8]) {
-  if constexpr (sizeof(T) == 2) {
-    const uint4 u = *(const uint4*)p;
-    const bf16x8 b = __builtin_bit_cast(bf16x8, u);
-#pragma unroll
-    for (int i = 0; i < 8; ++i) x[i] = (float)b[i];
-  } else {
-    const f32x4 a = *(const f32x4*)p, c = *(const f32x4*)(p + 4);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      x[i] = a[i];
-      x[4 + i] = c[i];
-    }
-  }
-}
-template <typename T>
-__device__ __forceinline__ void gate_store8(T* p, const float (&x)[8]) {
-  if constexpr (sizeof(T) == 2) {
-    bf16x8 b;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) b[i] = (__bf16)x[i];
-    *(uint4*)p = __builtin_bit_cast(uint4, b);
-  } else {
-    *(f32x4*)p = f32x4{x[0], x[1], x[2], x[3]};
-    *(f32x4*)(p + 4) = f32x4{x[4], x[5], x[6], x[7]};
-  }
-}
 // sum over the LPR lanes of a row's group (aligned, a power of two)
 template <int LPR>
 __device__ __forceinline__ float group_sum(float x) {
@@ -52,7 +23,6 @@ __device__ __forceinline__ float group_sum(float x) {
   for (int m = 1; m < LPR; m <<= 1) x += __shfl_xor(x, m, 64);
   return x;
 }
-__device__ __forceinline__ float sigmoidf_(float z) { return 1.f / (1.f + __expf(-z)); }
 
 // rows handled by one workgroup per grid-stride step
 template <int V> constexpr int gate_rows_per_block() { return (GATE_NTHR / 64) * (64 / (V / 8)); }
@@ -71,15 +41,15 @@ __global__ __launch_bounds__(GATE_NTHR) void k_gate_fwd(long long rows, const T*
     const bool ok = r < rows;
     const size_t off = (size_t)(ok ? r : 0) * V + c0;
     float x[8], g[8];
-    gate_load8(o + off, x);
-    gate_load8(z + off, g);
+    load8(o + off, x);
+    load8(z + off, g);
     float ss = 0.f;
 #pragma unroll
     for (int i = 0; i < 8; ++i) ss += x[i] * x[i];
     const float inv = 1.f / sqrtf(group_sum<LPR>(ss) / V + eps);
 #pragma unroll
     for (int i = 0; i < 8; ++i) x[i] = x[i] * inv * wg[i] * sigmoidf_(g[i]);
-    if (ok) gate_store8(y + off, x);
+    if (ok) store8(y + off, x);
   }
 }
 
@@ -102,9 +72,9 @@ __global__ __launch_bounds__(GATE_NTHR) void k_gate_bwd(long long rows, const T*
     const bool ok = r < rows;
     const size_t off = (size_t)(ok ? r : 0) * V + c0;
     float x[8], g[8], d[8];
-    gate_load8(o + off, x);
-    gate_load8(z + off, g);
-    gate_load8(dy + off, d);
+    load8(o + off, x);
+    load8(z + off, g);
+    load8(dy + off, d);
     float ss = 0.f;
 #pragma unroll
     for (int i = 0; i < 8; ++i) ss += x[i] * x[i];
@@ -124,8 +94,8 @@ __global__ __launch_bounds__(GATE_NTHR) void k_gate_bwd(long long rows, const T*
 #pragma unroll
     for (int i = 0; i < 8; ++i) dov[i] = inv * (dn[i] - nn[i] * mdot);
     if (ok) {
-      gate_store8(d_o + off, dov);
-      gate_store8(dz + off, dzv);
+      store8(d_o + off, dov);
+      store8(dz + off, dzv);
     }
   }
   // workgroup partial of dw: column c sums, in a fixed order, the lanes that
@@ -185,7 +155,6 @@ int gate_blocks(long long rows, int V) { return gate_grid(rows, V, 1024); }
 constexpr int HEAD_UMAX = 8;  // token runs per workgroup, at most
 constexpr int HEAD_BPT = 4;   // beta values per thread
 
-__device__ __forceinline__ float softplusf_(float y) { return y > 20.f ? y : log1pf(__expf(y)); }
 
 HeadsMap heads_map(long long tokens, int H, int E) {
   HeadsMap m;

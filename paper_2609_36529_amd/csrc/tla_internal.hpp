@@ -130,6 +130,22 @@ hipError_t launch_heads_fwd(bool bf16, long long tokens, int H, int E, const voi
 hipError_t launch_heads_bwd(bool bf16, long long tokens, int H, int E, const void* x, const void* xb,
                             const float* A, const float* b, const float* dg, const float* dbeta,
                             void* dx, void* dxb, float* dA, float* db, float* part, hipStream_t st);
+// The mixer's input side after the projection GEMM: causal depthwise
+// convolution, SiLU / softplus, L2 normalisation.
+struct ConvArgs {
+  int B, T, H, K, V, E, W;
+  int Ctot;          // H (2K + V + 2E) channels per token
+  int tb;            // tokens per run (one wave walks one run)
+  int runs_per_row;  // ceil(T / tb)
+  float eps;
+};
+ConvArgs conv_args(int B, int T, int H, int K, int V, int E, int W, float eps, bool backward);
+long long conv_parts(const ConvArgs& a);  // workgroups along the runs (= dw partial sets)
+hipError_t launch_conv_fwd(bool bf16, const ConvArgs& a, const void* y, const float* w,
+                           void* const* out, hipStream_t st);
+hipError_t launch_conv_bwd(bool bf16, const ConvArgs& a, const void* y, const float* w,
+                           const void* const* dout, void* dy, float* dw, float* part,
+                           hipStream_t st);
 
 // Which (K, C, E) combinations have kernel instances, and whether the
 // forward/backward shared-memory plan of an instance fits 160 KiB.

@@ -277,3 +277,49 @@ def test_gate_heads_validation():
     assert bwd(dx=dg) == E_ALIAS
     assert bwd(db=dA) == E_ALIAS
     assert bwd(ws=dx) == E_ALIAS
+
+
+def test_conv_in_validation():
+    """Input side: dtype, widths, taps, group alignment, required pointers,
+    alignment, aliasing and workspace are checked on the host (fake
+    addresses, nothing launched)."""
+    L = tla.lib()
+    P = ctypes.c_void_p
+    y, w, q, k, v, q2, k2 = (P(FAKE + i * 0x4000000) for i in range(7))
+    shp = dict(B=2, T=100, H=8, K=128, V=128, E=8, W=4)
+
+    def fwd(dtype=tla.BF16, eps=1e-6, **kw):
+        a = dict(shp, y=y, w=w, q=q, k=k, v=v, q2=q2, k2=k2)
+        a.update(kw)
+        return L.tla_conv_in_fwd(dtype, a["B"], a["T"], a["H"], a["K"], a["V"], a["E"], a["W"], eps, a["y"],
+                                 a["w"], a["q"], a["k"], a["v"], a["q2"], a["k2"], None)
+    assert fwd(dtype=5) == E_SHAPE
+    assert fwd(T=-1) == E_SHAPE
+    assert fwd(H=0) == E_SHAPE
+    assert fwd(K=96) == E_UNSUP
+    assert fwd(E=4) == E_UNSUP
+    assert fwd(V=12) == E_UNSUP
+    assert fwd(W=5) == E_UNSUP
+    assert fwd(W=0) == E_UNSUP
+    assert fwd(H=1, K=8, V=8, E=16) == E_UNSUP  # q2 block would start inside a norm group
+    assert fwd(eps=float("inf")) == E_SHAPE
+    assert fwd(v=None) == E_NULL
+    assert fwd(w=None) == E_NULL
+    assert fwd(q=P(FAKE + 2)) == E_ALIGN
+    assert fwd(k2=y) == E_ALIAS
+    assert fwd(k=q) == E_ALIAS
+    need = L.tla_conv_in_workspace_bytes(2, 100, 8, 128, 128, 8, 4)
+    assert need > 0 and need % 256 == 0
+    dq, dk, dv, dq2, dk2, dy, dw = (P(FAKE + 0x40000000 + i * 0x4000000) for i in range(7))
+    ws = P(FAKE + 0x80000000)
+
+    def bwd(ws_bytes=need, **kw):
+        a = dict(dq=dq, dk=dk, dv=dv, dq2=dq2, dk2=dk2, dy=dy, dw=dw, ws=ws)
+        a.update(kw)
+        return L.tla_conv_in_bwd(tla.F32, 2, 100, 8, 128, 128, 8, 4, 1e-6, y, w, a["dq"], a["dk"], a["dv"],
+                                 a["dq2"], a["dk2"], a["dy"], a["dw"], a["ws"], ws_bytes, None)
+    assert bwd(ws_bytes=need - 1) == E_WS
+    assert bwd(ws=None) == E_WS
+    assert bwd(dw=None) == E_NULL
+    assert bwd(dy=dq) == E_ALIAS
+    assert bwd(dw=dy) == E_ALIAS
