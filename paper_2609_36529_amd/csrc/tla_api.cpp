@@ -50,12 +50,12 @@ int check_desc(const tla_desc* d, tla::Shape* s, bool for_step) {
   if (d->B < 1 || d->H < 1) return fail(TLA_E_SHAPE, "B=%d H=%d must be >= 1", d->B, d->H);
   if (!for_step && d->T < 0) return fail(TLA_E_SHAPE, "T=%d must be >= 0", d->T);
   static const int Ks[] = {16, 32, 64, 128};
-  static const int Es[] = {1, 2, 4, 8, 16};
+  static const int Es[] = {1, 2, 4, 8, 16, 32};
   static const int Cs[] = {16, 32, 64};
   if (!pow2_in(d->K, Ks, 4)) return fail(TLA_E_UNSUPPORTED, "K=%d not in {16,32,64,128}", d->K);
   if (d->V < 16 || d->V > 1024 || d->V % 16 != 0)
     return fail(TLA_E_UNSUPPORTED, "V=%d must be a multiple of 16 in [16, 1024]", d->V);
-  if (!pow2_in(d->E, Es, 5)) return fail(TLA_E_UNSUPPORTED, "E=%d not in {1,2,4,8,16}", d->E);
+  if (!pow2_in(d->E, Es, 6)) return fail(TLA_E_UNSUPPORTED, "E=%d not in {1,2,4,8,16,32}", d->E);
   if (!for_step) {
     if (!pow2_in(d->chunk, Cs, 3)) return fail(TLA_E_UNSUPPORTED, "chunk=%d not in {16,32,64}", d->chunk);
     if (!tla::have_instance(d->K, d->chunk, d->E))

@@ -988,6 +988,9 @@ struct ChunkSmem {
   static constexpr bool STAGE_QK = sizeof(T) == 2;
   static constexpr int QR = STAGE_QK ? C : 1;
   static constexpr int KR = STAGE_QK ? KD : 1;
+  // dT later holds three C x E sums of the Gram backward: at least C rows,
+  // more where 3 C E exceeds C x CP (wide second keys at small chunks)
+  static constexpr int DT_ROWS = 3 * C * E > C * CP ? (3 * C * E + CP - 1) / CP : C;
   union U1 {
     struct { T sQ[QR][KP]; T sK[QR][KP]; } qk;           // Q, K rows
     struct { float dMT[C][CP]; float Dsym[C][CP]; } tr;  // dA_qk^T, dA_kk + dA_kk^T
@@ -1001,7 +1004,7 @@ struct ChunkSmem {
   alignas(16) float Aqk[C][CP];  // A_qk, then dR' = dM o A_qk
   alignas(16) float Akk[C][CP];  // A_kk, then dR = dA_hat o A_kk
   alignas(16) float dM[C][CP];   // dA_qk = dM o R'
-  alignas(16) float dT[C][CP];   // dTu, P = N^{-T} dTu, dA_kk; then the Gram-backward sums
+  alignas(16) float dT[DT_ROWS][CP];  // dTu, P = N^{-T} dTu, dA_kk; then the Gram-backward sums
   alignas(16) float Y[NT > 1 ? NT - 1 : 1][16][17];
   alignas(16) float q2[C][E];
   alignas(16) float k2[C][E];
@@ -1600,6 +1603,7 @@ __global__ __launch_bounds__(CHUNK_NTHR) void k_bwd_chunk(Shape s, FwdIn in, con
   // tiles of (r, c) pairs, c <= r:  d = Gamma_e[r, c] = exp(G_r[e] - G_c[e]),
   //   aq2[r] = sum_c dR'[r,c] d k2_c,   ak2[r] = sum_c dR[r,c] d k2_c,
   //   acol[c] = sum_r (dR'[r,c] q2_r + dR[r,c] k2_r) d
+  static_assert(3 * C * E <= Sm::DT_ROWS * Sm::CP, "room for the three sums");
   float* aq2s = &sm.dT[0][0];  // dA_kk is dead: its space holds the three sums
   float* ak2s = aq2s + C * E;
   float* acols = ak2s + C * E;
@@ -1772,6 +1776,8 @@ static hipError_t chunk_inst(const Shape& s, const FwdIn& in, const void* dO, co
   TLA_BWD_DISPATCH(16, 16, 4, CALL) \
   TLA_BWD_DISPATCH(32, 32, 4, CALL) \
   TLA_BWD_DISPATCH(64, 32, 8, CALL) \
+  TLA_BWD_DISPATCH(64, 64, 16, CALL) \
+  TLA_BWD_DISPATCH(32, 32, 32, CALL) \
   TLA_BWD_DISPATCH(128, 64, 1, CALL) \
   TLA_BWD_DISPATCH(128, 64, 4, CALL) \
   TLA_BWD_DISPATCH(128, 64, 8, CALL) \

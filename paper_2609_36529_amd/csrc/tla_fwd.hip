@@ -1489,6 +1489,8 @@ static hipError_t fwd_inst(const Shape& s, const FwdIn& in, const PrepBufs& p, v
   TLA_DISPATCH(16, 16, 4, CALL)     \
   TLA_DISPATCH(32, 32, 4, CALL)     \
   TLA_DISPATCH(64, 32, 8, CALL)     \
+  TLA_DISPATCH(64, 64, 16, CALL)     \
+  TLA_DISPATCH(32, 32, 32, CALL)     \
   TLA_DISPATCH(128, 64, 1, CALL)    \
   TLA_DISPATCH(128, 64, 4, CALL)    \
   TLA_DISPATCH(128, 64, 8, CALL)    \
@@ -1526,7 +1528,9 @@ bool fits_lds(int K, int C, int E, bool bf16) {
 
 bool have_instance(int K, int C, int E) {
   return (K == 16 && C == 16 && E == 4) || (K == 32 && C == 32 && E == 4) ||
-         (K == 64 && C == 32 && E == 8) || (K == 128 && C == 64 && (E == 1 || E == 4 || E == 8 || E == 16)) ||
+         (K == 32 && C == 32 && E == 32) || (K == 64 && C == 32 && E == 8) ||
+         (K == 64 && C == 64 && E == 16) ||
+         (K == 128 && C == 64 && (E == 1 || E == 4 || E == 8 || E == 16)) ||
          (K == 128 && C == 32 && E == 8);
 }
 

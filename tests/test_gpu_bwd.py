@@ -63,7 +63,7 @@ def test_f32_main_shape(variant, T):
 
 @pytest.mark.parametrize("variant", [SGLA, GDN])
 @pytest.mark.parametrize("K,E,chunk", [(16, 4, 16), (32, 4, 32), (64, 8, 32), (128, 4, 64),
-                                       (128, 1, 64), (128, 8, 32)])
+                                       (128, 1, 64), (128, 8, 32), (64, 16, 64), (32, 32, 32)])
 def test_f32_shapes(variant, K, E, chunk):
     check(cfg_of(variant, "f32", T=77, K=K, V=K, E=E, chunk=chunk), TOL_F32, dS_final=True)
 
@@ -73,7 +73,8 @@ def test_sgla_with_beta_f32():
 
 
 @pytest.mark.parametrize("variant", [SGLA, GDN])
-@pytest.mark.parametrize("K,E,chunk", [(128, 8, 64), (128, 4, 64), (64, 8, 32), (16, 4, 16)])
+@pytest.mark.parametrize("K,E,chunk", [(128, 8, 64), (128, 4, 64), (64, 8, 32), (16, 4, 16),
+                                       (64, 16, 64), (32, 32, 32)])
 def test_bf16_small(variant, K, E, chunk):
     check(cfg_of(variant, "bf16", T=203, K=K, V=K, E=E, chunk=chunk), TOL_BF16)
 

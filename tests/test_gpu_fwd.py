@@ -55,10 +55,20 @@ def test_f32_operands_main_shape(variant, T):
 
 @pytest.mark.parametrize("variant", [SGLA, GDN])
 @pytest.mark.parametrize("K,E,chunk", [(128, 8, 64), (128, 4, 64), (128, 1, 64), (64, 8, 32),
-                                       (32, 4, 32), (16, 4, 16), (128, 8, 32)])
+                                       (32, 4, 32), (16, 4, 16), (128, 8, 32), (64, 16, 64),
+                                       (32, 32, 32)])
 def test_bf16_small(variant, K, E, chunk):
     cfg = small_cfg(variant, "bf16", T=203, K=K, V=K, E=E, chunk=chunk)
     check_all_heads(cfg, synth.make_inputs(cfg), TOL_BF16)
+
+
+@pytest.mark.parametrize("variant", [SGLA, GDN])
+@pytest.mark.parametrize("K,E,chunk", [(64, 16, 64), (32, 32, 32)])
+def test_f32_wide_second_keys(variant, K, E, chunk):
+    """The generality shapes of the paper's Table 4 (E = 16 at K = 64,
+    E = 32 at K = 32) with fp32 operands."""
+    cfg = small_cfg(variant, "f32", B=1, T=97, H=2, K=K, V=K, E=E, chunk=chunk)
+    check_all_heads(cfg, synth.make_inputs(cfg), TOL_F32)
 
 
 def test_bf16_E16():
