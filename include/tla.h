@@ -86,7 +86,7 @@ typedef struct tla_desc {
  * (32, 32, 32), (64, 32, 8), (64, 64, 16), (128, 64, 1 / 4 / 8 / 16) and
  * (128, 32, 8); fp32 operands at (128, 64, 16) exceed the shared-memory
  * budget (tla_supported() tells).  tla_step has its own instances: (K, E) in
- * (16, 4), (32, 4), (64, 8), (128, 1 / 4 / 8 / 16).
+ * (16, 4), (32, 4), (32, 32), (64, 8), (64, 16), (128, 1 / 4 / 8 / 16).
  * tla_bwd further needs V <= 128 (TLA_E_UNSUPPORTED otherwise).
  * Returns 1 if the description is valid and has a kernel instance, else 0.
  */

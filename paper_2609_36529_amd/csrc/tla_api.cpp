@@ -66,7 +66,8 @@ int check_desc(const tla_desc* d, tla::Shape* s, bool for_step) {
                   d->K, d->chunk, d->E, d->in_dtype == TLA_BF16 ? "bf16" : "fp32");
   } else {
     const bool ok = (d->K == 16 && d->E == 4) || (d->K == 32 && d->E == 4) ||
-                    (d->K == 64 && d->E == 8) ||
+                    (d->K == 32 && d->E == 32) || (d->K == 64 && d->E == 8) ||
+                    (d->K == 64 && d->E == 16) ||
                     (d->K == 128 && (d->E == 1 || d->E == 4 || d->E == 8 || d->E == 16));
     if (!ok) return fail(TLA_E_UNSUPPORTED, "no step instance for K=%d E=%d", d->K, d->E);
   }

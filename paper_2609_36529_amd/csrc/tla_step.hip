@@ -146,7 +146,9 @@ static hipError_t step_vc(const Shape& s, const FwdIn& in, float* state, void* o
 hipError_t launch_step(const Shape& s, const FwdIn& in, float* state, void* o, hipStream_t st) {
   TLA_STEP_CASE(16, 4)
   TLA_STEP_CASE(32, 4)
+  TLA_STEP_CASE(32, 32)
   TLA_STEP_CASE(64, 8)
+  TLA_STEP_CASE(64, 16)
   TLA_STEP_CASE(128, 1)
   TLA_STEP_CASE(128, 4)
   TLA_STEP_CASE(128, 8)

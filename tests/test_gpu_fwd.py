@@ -209,7 +209,8 @@ def step_inputs(N, H, K, V, E, dtype, variant, seed):
 @pytest.mark.parametrize("variant", [SGLA, GDN])
 @pytest.mark.parametrize("dtype,K,V,E", [("f32", 16, 16, 4), ("f32", 128, 128, 8),
                                          ("bf16", 128, 128, 16), ("bf16", 128, 128, 1),
-                                         ("bf16", 32, 48, 4)])
+                                         ("bf16", 32, 48, 4), ("f32", 64, 64, 16),
+                                         ("bf16", 32, 32, 32)])
 def test_step_matches_oracle(variant, dtype, K, V, E):
     N, H = 3, 2
     state = synth.make_decode_state(N, H, E, K, V, seed=11)
