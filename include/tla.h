@@ -129,6 +129,13 @@ int tla_fwd(const tla_desc* desc, const void* q, const void* k, const void* v,
  * dk2 (type out_dtype, like o in the forward); dg: gradient with respect to
  * the log-gates g (fp32);
  * dbeta (fp32) must be NULL exactly when beta is NULL; ds0 (fp32) may be NULL.
+ * ws: device workspace of tla_workspace_bytes(desc, TLA_OP_BWD) bytes.  With
+ * bf16 operands and dS_final given, the chunk-end state gradients are kept
+ * as bf16 (hi, lo) pairs (a final-state gradient makes the last chunks'
+ * gradients much larger than the rest, and one bf16 rounding of them would
+ * dominate those chunks' input gradients); a call with dS_final == NULL
+ * needs only the workspace without the low parts, i.e. less than
+ * tla_workspace_bytes reports (TLA_E_WORKSPACE names the exact need).
  * Paper reference for the structure: Appendix A, "Kernels" (a reverse
  * recurrence over chunks for the state gradient, then every other gradient
  * chunk-parallel, fixed-order reductions).

@@ -141,6 +141,45 @@ def _need(t, name, dtype=None, device=None):
     return t
 
 
+def _shape(t, name, shape):
+    """Raises unless tensor t (if given) has exactly `shape`."""
+    if t is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    return t
+
+
+def _buffer(t, name, nbytes, device):
+    """A caller-supplied byte buffer: a contiguous device tensor of at least
+    nbytes bytes (any element type)."""
+    if t is None:
+        return None
+    _need(t, name, None, device)
+    have = t.numel() * t.element_size()
+    if have < nbytes:
+        raise ValueError(f"{name} holds {have} bytes, the call needs {nbytes}")
+    return t
+
+
+def _check_inputs(q, k, v, q2, k2, g, beta, s0, packed_B=None):
+    """Every operator input: device, contiguity, element type and shape
+    against q [B, T, H, K], v [.., V], q2 [.., E].  Raises before any launch.
+    packed_B: the number of packed sequences (states are [packed_B, H, E, K, V])."""
+    if q.dim() != 4 or v.dim() != 4 or q2.dim() != 4:
+        raise ValueError("q, v and q2 must be 4-d: [B, T, H, K], [B, T, H, V], [B, T, H, E]")
+    dev, dt = q.device, q.dtype
+    _dtype_code(dt)
+    B, T, H, K = q.shape
+    V, E = v.shape[-1], q2.shape[-1]
+    for name, t, last in (("q", q, K), ("k", k, K), ("v", v, V), ("q2", q2, E), ("k2", k2, E)):
+        _need(t, name, dt, dev)
+        _shape(t, name, (B, T, H, last))
+    _shape(_need(g, "g", torch.float32, dev), "g", (B, T, H, E))
+    _shape(_need(beta, "beta", torch.float32, dev), "beta", (B, T, H))
+    nb = B if packed_B is None else packed_B
+    _shape(_need(s0, "s0", torch.float32, dev), "s0", (nb, H, E, K, V))
+    return dev, dt
+
+
 def describe(variant, q, v, q2, chunk, out_dtype=None, cu_seqlens=None, max_seqlen=None):
     """Descriptor of a call; with cu_seqlens (packed sequences, q is
     [1, total, H, K]) B is the number of sequences and T = max_seqlen."""
@@ -179,29 +218,31 @@ def fwd(variant, q, k, v, q2, k2, g, beta=None, s0=None, chunk=64, out_dtype=Non
     With cu_seqlens (int32 device tensor of N + 1 offsets) the inputs hold N
     packed sequences, [1, total, H, .], each with its own state (s0 and
     s_final [N, H, E, K, V]); max_seqlen is the longest length."""
-    dev = q.device
-    dt = q.dtype
-    for name, t in (("q", q), ("k", k), ("v", v), ("q2", q2), ("k2", k2)):
-        _need(t, name, dt, dev)
-    _need(g, "g", torch.float32, dev)
-    _need(beta, "beta", torch.float32, dev)
-    _need(s0, "s0", torch.float32, dev)
-    cu = _cu(cu_seqlens, dev)
+    cu = _cu(cu_seqlens, q.device)
+    dev, dt = _check_inputs(q, k, v, q2, k2, g, beta, s0,
+                            None if cu is None else cu.numel() - 1)
     desc = describe(variant, q, v, q2, chunk, out_dtype, cu, max_seqlen)
     B, T = desc.B, desc.T
     H, K = q.shape[2], q.shape[3]
     V, E = v.shape[-1], q2.shape[-1]
+    odt = out_dtype or dt
     if o is None:
-        o = torch.empty(q.shape[:3] + (V,), dtype=out_dtype or dt, device=dev)
+        o = torch.empty(q.shape[:3] + (V,), dtype=odt, device=dev)
+    _shape(_need(o, "o", odt, dev), "o", q.shape[:3] + (V,))
     if want_final and s_final is None:
         s_final = torch.empty((B, H, E, K, V), dtype=torch.float32, device=dev)
-    if ws is None:
+    if want_final:
+        _shape(_need(s_final, "s_final", torch.float32, dev), "s_final", (B, H, E, K, V))
+    if training:
+        if saved is None:
+            saved = torch.empty(max(saved_bytes(desc), 1), dtype=torch.uint8, device=dev)
+        _buffer(saved, "saved", saved_bytes(desc), dev)
+    elif ws is None:
         ws = torch.empty(max(workspace_bytes(desc, OP_FWD), 1), dtype=torch.uint8, device=dev)
-    if training and saved is None:
-        saved = torch.empty(max(saved_bytes(desc), 1), dtype=torch.uint8, device=dev)
+    _buffer(ws, "ws", 0 if training else workspace_bytes(desc, OP_FWD), dev)
     args = (_ptr(q), _ptr(k), _ptr(v), _ptr(q2), _ptr(k2), _ptr(g), _ptr(beta), _ptr(s0), _ptr(o),
             _ptr(s_final if want_final else None), _ptr(saved if training else None), _ptr(ws),
-            ws.numel(), _stream(dev))
+            0 if ws is None else ws.numel() * ws.element_size(), _stream(dev))
     if cu is None:
         rc = lib().tla_fwd(ctypes.byref(desc), *args)
     else:
@@ -215,16 +256,19 @@ def bwd(variant, q, k, v, q2, k2, g, beta, s0, dO, saved, dS_final=None, chunk=6
     """Backward of a training forward.  Returns a dict of gradients
     (dq, dk, dv, dq2, dk2 in out_dtype (default: the input dtype); dg, dbeta or
     None, ds0 or None in fp32).  cu_seqlens / max_seqlen as for fwd."""
-    dev = q.device
-    dt = q.dtype
+    cu = _cu(cu_seqlens, q.device)
+    dev, dt = _check_inputs(q, k, v, q2, k2, g, beta, s0,
+                            None if cu is None else cu.numel() - 1)
     gt = out_dtype or dt
-    cu = _cu(cu_seqlens, dev)
     desc = describe(variant, q, v, q2, chunk, gt, cu, max_seqlen)
     B = desc.B
     H, K = q.shape[2], q.shape[3]
     V, E = v.shape[-1], q2.shape[-1]
-    _need(dO, "dO", dt, dev)
-    _need(dS_final, "dS_final", torch.float32, dev)
+    _shape(_need(dO, "dO", dt, dev), "dO", v.shape)
+    _shape(_need(dS_final, "dS_final", torch.float32, dev), "dS_final", (B, H, E, K, V))
+    if saved is None:
+        raise ValueError("bwd needs the `saved` buffer of a training forward")
+    _buffer(saved, "saved", saved_bytes(desc), dev)
     if grads is None:
         grads = {
             "dq": torch.empty_like(q, dtype=gt), "dk": torch.empty_like(k, dtype=gt),
@@ -234,12 +278,19 @@ def bwd(variant, q, k, v, q2, k2, g, beta, s0, dO, saved, dS_final=None, chunk=6
             "dbeta": None if beta is None else torch.empty(q.shape[:3], dtype=torch.float32, device=dev),
             "ds0": torch.empty((B, H, E, K, V), dtype=torch.float32, device=dev) if want_ds0 else None,
         }
+    expect = {"dq": (q.shape, gt), "dk": (q.shape, gt), "dv": (v.shape, gt), "dq2": (q2.shape, gt),
+              "dk2": (q2.shape, gt), "dg": (q2.shape, torch.float32),
+              "dbeta": (q.shape[:3], torch.float32), "ds0": ((B, H, E, K, V), torch.float32)}
+    for key, (shp, gdt) in expect.items():
+        _shape(_need(grads.get(key), key, gdt, dev), key, shp)
+    if (beta is None) != (grads.get("dbeta") is None):
+        raise ValueError("grads['dbeta'] must be given exactly when beta is")
     if ws is None:
         ws = torch.empty(max(workspace_bytes(desc, OP_BWD), 1), dtype=torch.uint8, device=dev)
+    _buffer(ws, "ws", workspace_bytes(desc, OP_BWD), dev)
     args = (_ptr(q), _ptr(k), _ptr(v), _ptr(q2), _ptr(k2), _ptr(g), _ptr(beta), _ptr(s0), _ptr(dO),
-            _ptr(dS_final), _ptr(saved), _ptr(grads["dq"]), _ptr(grads["dk"]), _ptr(grads["dv"]),
-            _ptr(grads["dq2"]), _ptr(grads["dk2"]), _ptr(grads["dg"]), _ptr(grads["dbeta"]),
-            _ptr(grads["ds0"]), _ptr(ws), ws.numel(), _stream(dev))
+            _ptr(dS_final), _ptr(saved), *[_ptr(grads.get(key)) for key in expect], _ptr(ws),
+            ws.numel() * ws.element_size(), _stream(dev))
     if cu is None:
         rc = lib().tla_bwd(ctypes.byref(desc), *args)
     else:
@@ -248,21 +299,61 @@ def bwd(variant, q, k, v, q2, k2, g, beta, s0, dO, saved, dS_final=None, chunk=6
     return grads
 
 
+class TriadicAttention(torch.autograd.Function):
+    """Autograd wrapper of one training forward (tla_fwd with a `saved`
+    buffer) and its backward (tla_bwd).  Inputs as for fwd(); returns
+    (o, s_final).  Gradients flow to q, k, v, q2, k2, g, beta and s0 (those
+    given).  The `saved` buffer of the forward is held until the backward."""
+
+    @staticmethod
+    def forward(ctx, q, k, v, q2, k2, g, beta, s0, variant, chunk, out_dtype):
+        o, s_final, saved = fwd(variant, q, k, v, q2, k2, g, beta, s0, chunk=chunk,
+                                out_dtype=out_dtype, training=True)
+        ctx.save_for_backward(q, k, v, q2, k2, g, beta, s0)
+        ctx.saved_buffer = saved
+        ctx.variant, ctx.chunk = variant, chunk
+        return o, s_final
+
+    @staticmethod
+    def backward(ctx, do, dsf):
+        q, k, v, q2, k2, g, beta, s0 = ctx.saved_tensors
+        if do is None:
+            do = torch.zeros(v.shape, dtype=q.dtype, device=q.device)
+        do = do.to(q.dtype).contiguous()
+        dsf = None if dsf is None else dsf.float().contiguous()
+        gr = bwd(ctx.variant, q, k, v, q2, k2, g, beta, s0, do, ctx.saved_buffer, dS_final=dsf,
+                 chunk=ctx.chunk, out_dtype=q.dtype, want_ds0=s0 is not None)
+        ctx.saved_buffer = None
+        return (gr["dq"], gr["dk"], gr["dv"], gr["dq2"], gr["dk2"], gr["dg"], gr["dbeta"],
+                gr["ds0"], None, None, None)
+
+
+def attention(variant, q, k, v, q2, k2, g, beta=None, s0=None, chunk=64, out_dtype=None):
+    """Differentiable triadic linear attention: (o, s_final) with autograd
+    support through TriadicAttention (training forward + tla_bwd)."""
+    return TriadicAttention.apply(q, k, v, q2, k2, g, beta, s0, variant, chunk, out_dtype)
+
+
 def step(variant, q, k, v, q2, k2, g, beta, state, out_dtype=None, o=None):
     """One decode token per (sequence, head); updates `state` in place.
     q, k [N,H,K]; v [N,H,V]; q2, k2, g [N,H,E]; beta [N,H] or None."""
     dev = q.device
+    if q.dim() != 3 or v.dim() != 3 or q2.dim() != 3:
+        raise ValueError("q, v and q2 must be 3-d: [N, H, K], [N, H, V], [N, H, E]")
     N, H, K = q.shape
     V, E = v.shape[-1], q2.shape[-1]
-    for name, t in (("q", q), ("k", k), ("v", v), ("q2", q2), ("k2", k2)):
-        _need(t, name, q.dtype, dev)
-    _need(g, "g", torch.float32, dev)
-    _need(beta, "beta", torch.float32, dev)
-    _need(state, "state", torch.float32, dev)
+    for name, t, last in (("q", q, K), ("k", k, K), ("v", v, V), ("q2", q2, E), ("k2", k2, E)):
+        _shape(_need(t, name, q.dtype, dev), name, (N, H, last))
+    _shape(_need(g, "g", torch.float32, dev), "g", (N, H, E))
+    _shape(_need(beta, "beta", torch.float32, dev), "beta", (N, H))
+    if state is None:
+        raise ValueError("step needs the state tensor")
+    _shape(_need(state, "state", torch.float32, dev), "state", (N, H, E, K, V))
     desc = make_desc(variant, N, 1, H, K, V, E, 16, _dtype_code(q.dtype),
                      _dtype_code(out_dtype or q.dtype))
     if o is None:
         o = torch.empty((N, H, V), dtype=out_dtype or q.dtype, device=dev)
+    _shape(_need(o, "o", out_dtype or q.dtype, dev), "o", (N, H, V))
     rc = lib().tla_step(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(q2), _ptr(k2), _ptr(g),
                         _ptr(beta), _ptr(state), _ptr(o), _stream(dev))
     _check(rc)

@@ -113,7 +113,7 @@ size_t esize(const tla::Shape& s) { return s.in_bf16 ? 2 : 4; }
 // writes them into `saved`, where the backward reads them again.
 struct Layout {
   size_t p_coef, p_gC, p_ops, p_ninv, p_size;  // prep region, relative offsets
-  size_t bwd_dS, bwd_dU, bwd_dW, bwd_dqs, bwd_dks, bwd_dcoef, bwd_dgC, bwd_end;
+  size_t bwd_dS, bwd_dSlo, bwd_dU, bwd_dW, bwd_dqs, bwd_dks, bwd_dcoef, bwd_dgC, bwd_end;
   size_t sv_S, sv_U, sv_X, sv_prep, sv_end;
 };
 
@@ -136,6 +136,10 @@ Layout layout(const tla::Shape& s) {
   L.bwd_dks = o;   o += align256(nch * s.C * s.K * 4);
   L.bwd_dcoef = o; o += align256(nch * 3 * s.E * s.C * 4);
   L.bwd_dgC = o;   o += align256(nch * E4 * 4);
+  // low parts of the state gradients (bf16 operands, used when a final-state
+  // gradient is given); last, so that a call without one needs only the
+  // first bwd_dSlo bytes
+  L.bwd_dSlo = o;  o += s.in_bf16 ? align256(nch * s.E * s.K * s.V * es) : 0;
   L.bwd_end = o;
   o = 0;
   L.sv_S = o;    o += align256(nch * s.E * s.K * s.V * es);
@@ -370,7 +374,9 @@ static int bwd_impl(const tla_desc* d, const int32_t* cu, long long total, const
   for (const void* p : ptrs)
     if (misaligned(p)) return fail(TLA_E_ALIGN, "pointer %p is not 16-byte aligned", p);
   const Layout L = layout(s);
-  if (ws_bytes < L.bwd_end) return fail(TLA_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, L.bwd_end);
+  const bool pds = s.in_bf16 && dS_final;  // state gradients as bf16 (hi, lo) pairs
+  const size_t ws_need = pds ? L.bwd_end : L.bwd_dSlo;
+  if (ws_bytes < ws_need) return fail(TLA_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, ws_need);
   const size_t es = esize(s), os = s.out_bf16 ? 2 : 4;
   const size_t sbytes = (size_t)s.NH * s.E * s.K * s.V * 4;
   const Range ins[] = {{q, ntok * s.K * es}, {k, ntok * s.K * es}, {v, ntok * s.V * es},
@@ -381,7 +387,7 @@ static int bwd_impl(const tla_desc* d, const int32_t* cu, long long total, const
   const Range outs[] = {{dq, ntok * s.K * os}, {dk, ntok * s.K * os}, {dv, ntok * s.V * os},
                         {dq2, ntok * s.E * os}, {dk2, ntok * s.E * os}, {dg, ntok * s.E * 4},
                         {dbeta, dbeta ? ntok * 4 : 0}, {ds0, ds0 ? sbytes : 0},
-                        {ws, L.bwd_end}};
+                        {ws, ws_need}};
   const int nouts = sizeof(outs) / sizeof(outs[0]);
   for (const Range& a : outs)
     for (const Range& b : ins)
@@ -395,7 +401,8 @@ static int bwd_impl(const tla_desc* d, const int32_t* cu, long long total, const
   tla::FwdIn in{q, k, v, q2, k2, g, beta, s0};
   const tla::PrepBufs pb = prep_bufs(L, (const char*)saved + L.sv_prep, true);  // from the forward
   char* wb = (char*)ws;
-  const tla::BwdBufs bb{wb + L.bwd_dS, (float*)(wb + L.bwd_dU), (float*)(wb + L.bwd_dW),
+  const tla::BwdBufs bb{wb + L.bwd_dS, pds ? wb + L.bwd_dSlo : nullptr,
+                        (float*)(wb + L.bwd_dU), (float*)(wb + L.bwd_dW),
                         (float*)(wb + L.bwd_dqs), (float*)(wb + L.bwd_dks),
                         (float*)(wb + L.bwd_dcoef), (float*)(wb + L.bwd_dgC)};
   const tla::SavedBufs sv = saved_bufs(L, saved);

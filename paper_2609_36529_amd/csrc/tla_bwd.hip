@@ -249,7 +249,12 @@ struct RecStage {
   }
 };
 
-template <typename T, int KD, int C, int E, int NW>
+// PDS (bf16 operands with a final-state gradient): the chunk-end state
+// gradients dS' enter K dS'_e as bf16 (hi, lo) pairs and are stored as two
+// bf16 tiles (dSck, dSck_lo).  A given final-state gradient makes dS' of the
+// last chunks far larger than elsewhere in the sequence, and one bf16
+// rounding of it would then dominate the gradients of those chunks.
+template <typename T, int KD, int C, int E, int NW, bool PDS>
 __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const void* dOv,
                                                      const float* dS_final, PrepBufs p,
                                                      BwdBufs bb, float* ds0) {
@@ -322,22 +327,28 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
 
     // ---- operand copies of dS' (gradient of the chunk-end state), stored for
     // the chunk-parallel kernel
-    F dSop[SPW][KT];
+    F dSop[SPW][KT], dSlo[PDS ? SPW : 1][PDS ? KT : 1];
 #pragma unroll
     for (int i = 0; i < SPW; ++i)
 #pragma unroll
-      for (int kt = 0; kt < KT; ++kt) dSop[i][kt] = cvt_frag<T>(dS[i][kt]);
+      for (int kt = 0; kt < KT; ++kt) {
+        dSop[i][kt] = cvt_frag<T>(dS[i][kt]);
+        if constexpr (PDS) dSlo[i][kt] = cvt_frag<T>(dS[i][kt] - frag_to_f(dSop[i][kt]));
+      }
 #pragma unroll
     for (int i = 0; i < SPW; ++i) {
       const int e = w * SPW + i;
       if (RAGGED && e >= E) continue;
-      T* dst = (T*)bb.dSck + ((ch * E + e) * (size_t)(V / 16) + vt) * KD * 16;
+      const size_t toff = ((ch * E + e) * (size_t)(V / 16) + vt) * KD * 16;
+      T* dst = (T*)bb.dSck + toff;
 #pragma unroll
       for (int kt = 0; kt < KT; ++kt) {
-        if constexpr (sizeof(T) == 2)
+        if constexpr (sizeof(T) == 2) {
           store_tile16_frag(dst + 256 * kt, dSop[i][kt], idf, g, n);
-        else
+          if constexpr (PDS) store_tile16_frag((T*)bb.dSck_lo + toff + 256 * kt, dSlo[i][kt], idf, g, n);
+        } else {
           store_tile16(dst + 256 * kt, dS[i][kt], g, n);
+        }
       }
     }
 
@@ -381,13 +392,19 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
           const Frag8<T> kk = kfrag8(kb);
 #pragma unroll
           for (int i = i0; i < i0 + GZ; ++i)
-            if (!RAGGED || w * SPW + i < E) mma32(z[i], kk, dSop[i][kb], dSop[i][kb + 1]);
+            if (!RAGGED || w * SPW + i < E) {
+              mma32(z[i], kk, dSop[i][kb], dSop[i][kb + 1]);
+              if constexpr (PDS) mma32(z[i], kk, dSlo[i][kb], dSlo[i][kb + 1]);
+            }
         }
         if constexpr (KT & 1) {
           const F k0 = kfrag(KT - 1);
 #pragma unroll
           for (int i = i0; i < i0 + GZ; ++i)
-            if (!RAGGED || w * SPW + i < E) mma16(z[i], k0, dSop[i][KT - 1]);
+            if (!RAGGED || w * SPW + i < E) {
+              mma16(z[i], k0, dSop[i][KT - 1]);
+              if constexpr (PDS) mma16(z[i], k0, dSlo[i][KT - 1]);
+            }
         }
       }
       f32x4 acc = zero4();
@@ -586,7 +603,9 @@ struct StateSmem {
   alignas(16) float gred[4][E];
 };
 
-template <typename T, int KD, int C, int E>
+// PDS: the chunk-end state gradients arrive as bf16 (hi, lo) tile pairs
+// (see k_bwd_rec) and enter U dS'^T and <S, dS'> with both parts.
+template <typename T, int KD, int C, int E, bool PDS>
 __global__ __launch_bounds__(STATE_NTHR) void k_bwd_state(Shape s, FwdIn in, const void* dOv,
                                                           PrepBufs p, SavedBufs sv, BwdBufs bb) {
   constexpr int NT = C / 16;
@@ -728,13 +747,15 @@ __global__ __launch_bounds__(STATE_NTHR) void k_bwd_state(Shape s, FwdIn in, con
   // below masks it)
   const T* Sck = (const T*)sv.Sck;
   const T* dSck = (const T*)bb.dSck;
-  Raw8<T> sbuf[CTW][NPMAX], dbuf[CTW][NPMAX];
+  const T* dSlk = (const T*)bb.dSck_lo;
+  Raw8<T> sbuf[CTW][NPMAX], dbuf[CTW][NPMAX], dlbuf[PDS ? CTW : 1][PDS ? NPMAX : 1];
   auto load_pair = [&](int e, int c, int pp) {
     const int ct = min(q * CTW + c, KT - 1);
     const int vb = min(2 * pp + (g >> 1), VB - 1);
     const size_t off = ((((size_t)ch * E + e) * VB + vb) * KD + 16 * ct + n) * 16 + 8 * (g & 1);
     sbuf[c][pp] = load8(Sck + off);
     dbuf[c][pp] = load8(dSck + off);
+    if constexpr (PDS) dlbuf[c][pp] = load8(dSlk + off);
   };
 #pragma unroll
   for (int pp = 0; pp < NPMAX; ++pp)
@@ -780,6 +801,12 @@ __global__ __launch_bounds__(STATE_NTHR) void k_bwd_state(Shape s, FwdIn in, con
           float a[8], d[8], part = 0.f;
           raw8_to_f(sbuf[c][pp], a);
           raw8_to_f(dbuf[c][pp], d);
+          if constexpr (PDS) {
+            float dl[8];
+            raw8_to_f(dlbuf[c][pp], dl);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) d[i] += dl[i];
+          }
 #pragma unroll
           for (int i = 0; i < 8; ++i) part += a[i] * d[i];
           gpart += (2 * pp + (g >> 1) < VB) ? part : 0.f;
@@ -808,6 +835,7 @@ __global__ __launch_bounds__(STATE_NTHR) void k_bwd_state(Shape s, FwdIn in, con
               mma8(Y[i][c], awl, sbuf[c][pp]);
               mma8(Vp[i][c], aul, dbuf[c][pp]);
             }
+            if constexpr (PDS) mma8(Vp[i][c], auh, dlbuf[c][pp]);
           }
         }
       }
@@ -1724,30 +1752,40 @@ static hipError_t rec_inst(const Shape& s, const FwdIn& in, const void* dO, cons
                            const PrepBufs& p, const BwdBufs& bb, float* ds0, hipStream_t st) {
   constexpr int NW = bwd_waves<E>();
   const size_t smem = sizeof(RecSmem<T, KD, C, E, NW>);
-  static bool attr = false;
-  if (!attr) {
-    (void)hipFuncSetAttribute((const void*)k_bwd_rec<T, KD, C, E, NW>,
-                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-    attr = true;
-  }
-  hipLaunchKernelGGL((k_bwd_rec<T, KD, C, E, NW>), dim3(s.NH * (s.V / 16)), dim3(NW * 64), smem,
-                     st, s, in, dO, dSf, p, bb, ds0);
-  return hipGetLastError();
+  auto go = [&](auto pds_c) {
+    constexpr bool PDS = decltype(pds_c)::value;
+    static bool attr = false;
+    if (!attr) {
+      (void)hipFuncSetAttribute((const void*)k_bwd_rec<T, KD, C, E, NW, PDS>,
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+      attr = true;
+    }
+    hipLaunchKernelGGL((k_bwd_rec<T, KD, C, E, NW, PDS>), dim3(s.NH * (s.V / 16)), dim3(NW * 64),
+                       smem, st, s, in, dO, dSf, p, bb, ds0);
+    return hipGetLastError();
+  };
+  if (sizeof(T) == 2 && bb.dSck_lo) return go(std::integral_constant<bool, sizeof(T) == 2>{});
+  return go(std::integral_constant<bool, false>{});
 }
 
 template <typename T, int KD, int C, int E>
 static hipError_t state_inst(const Shape& s, const FwdIn& in, const void* dO, const PrepBufs& p,
                              const SavedBufs& sv, const BwdBufs& bb, hipStream_t st) {
   const size_t smem = sizeof(StateSmem<T, KD, C, E>);
-  static bool attr = false;
-  if (!attr) {
-    (void)hipFuncSetAttribute((const void*)k_bwd_state<T, KD, C, E>,
-                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-    attr = true;
-  }
-  hipLaunchKernelGGL((k_bwd_state<T, KD, C, E>), dim3(s.NH * s.Nc), dim3(STATE_NTHR), smem, st, s, in, dO,
-                     p, sv, bb);
-  return hipGetLastError();
+  auto go = [&](auto pds_c) {
+    constexpr bool PDS = decltype(pds_c)::value;
+    static bool attr = false;
+    if (!attr) {
+      (void)hipFuncSetAttribute((const void*)k_bwd_state<T, KD, C, E, PDS>,
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+      attr = true;
+    }
+    hipLaunchKernelGGL((k_bwd_state<T, KD, C, E, PDS>), dim3(s.NH * s.Nc), dim3(STATE_NTHR), smem,
+                       st, s, in, dO, p, sv, bb);
+    return hipGetLastError();
+  };
+  if (sizeof(T) == 2 && bb.dSck_lo) return go(std::integral_constant<bool, sizeof(T) == 2>{});
+  return go(std::integral_constant<bool, false>{});
 }
 
 template <typename T, int KD, int C, int E>

@@ -82,6 +82,8 @@ struct SavedBufs {
 struct BwdBufs {
   void* dSck;    // [ch][E][V/16][K][16] state gradients at chunk ends, operand type
                  // (rows in the same key order as Sck)
+  void* dSck_lo; // bf16 operands with a final-state gradient: the low bf16 part of
+                 // the same gradients (dSck holds the rounded high part); else NULL
   float* dU;     // [ch][C][V]
   float* dW;     // [ch][C][V]
   float* dqs;    // [ch][C][K] state contributions to dq
