@@ -148,6 +148,26 @@ int tla_bwd(const tla_desc* desc, const void* q, const void* k, const void* v,
             size_t ws_bytes, void* stream);
 
 /*
+ * Inference forward for callers that cannot allocate (code under graph
+ * capture, tight serving loops, harnesses that forbid allocation): tla_fwd
+ * with saved = NULL, whose per-chunk workspace lives in a library-owned
+ * static device array of TLA_NOALLOC_SCRATCH_BYTES (64 MiB) on each GPU,
+ * held until the process ends, instead of a caller workspace.  Arguments,
+ * results and errors as for tla_fwd; the library allocates nothing.
+ *  - The scratch need is tla_workspace_bytes(desc, TLA_OP_FWD) (about 100
+ *    KiB per chunk of one head at K = 128, E = 8, chunk 64); larger calls
+ *    return TLA_E_WORKSPACE and launch nothing.
+ *  - The scratch of the current GPU is used (the stream must belong to it).
+ *    Every call on one GPU shares that array: calls that may overlap on one
+ *    GPU (different streams, or threads) race and give wrong results; order
+ *    them on one stream.  Nothing in the scratch needs to start at zero.
+ */
+#define TLA_NOALLOC_SCRATCH_BYTES (64u << 20)
+int tla_fwd_noalloc(const tla_desc* desc, const void* q, const void* k, const void* v,
+                    const void* q2, const void* k2, const float* g, const float* beta,
+                    const float* s0, void* o, float* s_final, void* stream);
+
+/*
  * Packed variable-length batches: the forward and backward above for B =
  * desc->B sequences of different lengths stored back to back.  Sequence b
  * is tokens [cu_seqlens[b], cu_seqlens[b + 1]) of q, k, v, q2, k2, g, beta,

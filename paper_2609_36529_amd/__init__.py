@@ -67,6 +67,8 @@ def lib():
     L.tla_fwd_varlen.restype = I
     L.tla_bwd_varlen.argtypes = [DP, P, LL] + [P] * 20 + [S, P]
     L.tla_bwd_varlen.restype = I
+    L.tla_fwd_noalloc.argtypes = [DP] + [P] * 10 + [P]
+    L.tla_fwd_noalloc.restype = I
     L.tla_step.argtypes = [DP] + [P] * 9 + [P]
     L.tla_step.restype = I
     L.tla_out_gate_fwd.argtypes = [I, LL, I, P, P, P, ctypes.c_float, P, P]
@@ -297,6 +299,29 @@ def bwd(variant, q, k, v, q2, k2, g, beta, s0, dO, saved, dS_final=None, chunk=6
         rc = lib().tla_bwd_varlen(ctypes.byref(desc), _ptr(cu), q.shape[1], *args)
     _check(rc)
     return grads
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20  # TLA_NOALLOC_SCRATCH_BYTES
+
+
+def fwd_noalloc(variant, q, k, v, q2, k2, g, beta=None, s0=None, chunk=64, out_dtype=None,
+                o=None, s_final=None):
+    """Inference forward through tla_fwd_noalloc: the library's static device
+    scratch replaces the caller workspace.  o and s_final may be given (then
+    nothing at all is allocated); returns (o, s_final or None)."""
+    dev, dt = _check_inputs(q, k, v, q2, k2, g, beta, s0)
+    desc = describe(variant, q, v, q2, chunk, out_dtype)
+    B, T, H, K = q.shape
+    V, E = v.shape[-1], q2.shape[-1]
+    odt = out_dtype or dt
+    if o is None:
+        o = torch.empty(q.shape[:3] + (V,), dtype=odt, device=dev)
+    _shape(_need(o, "o", odt, dev), "o", q.shape[:3] + (V,))
+    _shape(_need(s_final, "s_final", torch.float32, dev), "s_final", (B, H, E, K, V))
+    _check(lib().tla_fwd_noalloc(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(q2), _ptr(k2),
+                                 _ptr(g), _ptr(beta), _ptr(s0), _ptr(o), _ptr(s_final),
+                                 _stream(dev)))
+    return o, s_final
 
 
 class TriadicAttention(torch.autograd.Function):

@@ -13,6 +13,13 @@
 #include "../../include/tla.h"
 #include "tla_internal.hpp"
 
+// Device scratch of tla_fwd_noalloc: the inference forward's per-chunk
+// workspace (coefficient vectors, gamma^C, operand tiles) for callers that
+// cannot allocate.  One copy per GPU, held until the process ends.  Host code
+// never uses this name as an address: the device address of each GPU's copy
+// comes from hipGetSymbolAddress (scratch_ptr below).
+static __device__ __align__(256) unsigned char scratch[TLA_NOALLOC_SCRATCH_BYTES];
+
 namespace {
 
 thread_local char g_err[512] = "";
@@ -339,6 +346,45 @@ int tla_fwd(const tla_desc* d, const void* q, const void* k, const void* v, cons
             float* s_final, void* saved, void* ws, size_t ws_bytes, void* stream) {
   return fwd_impl(d, nullptr, 0, q, k, v, q2, k2, g, beta, s0, o, s_final, saved, ws, ws_bytes,
                   stream);
+}
+
+// Device address of `scratch` on the current GPU, looked up once per device
+// (with that device current) and kept.
+static int scratch_ptr(void** out) {
+  constexpr int kMaxDev = 64;
+  static std::mutex mu;
+  static void* ptrs[kMaxDev] = {};
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return device_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDev) return fail(TLA_E_DEVICE, "device index %d out of range", dev);
+  std::lock_guard<std::mutex> lk(mu);
+  if (!ptrs[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) return device_fail(e, "hipGetSymbolAddress(scratch)");
+    ptrs[dev] = p;
+  }
+  *out = ptrs[dev];
+  return TLA_OK;
+}
+
+int tla_fwd_noalloc(const tla_desc* d, const void* q, const void* k, const void* v,
+                    const void* q2, const void* k2, const float* g, const float* beta,
+                    const float* s0, void* o, float* s_final, void* stream) {
+  g_err[0] = 0;
+  tla::Shape s;
+  int rc = check_desc(d, &s, false);
+  if (rc) return rc;
+  const size_t need = layout(s).p_ninv;  // the inference forward's workspace
+  if (need > (size_t)TLA_NOALLOC_SCRATCH_BYTES)
+    return fail(TLA_E_WORKSPACE,
+                "tla_fwd_noalloc needs %zu bytes of scratch, above its maximum of %zu "
+                "(use tla_fwd with a caller workspace)", need, (size_t)TLA_NOALLOC_SCRATCH_BYTES);
+  void* ws = nullptr;
+  if ((rc = scratch_ptr(&ws))) return rc;
+  return fwd_impl(d, nullptr, 0, q, k, v, q2, k2, g, beta, s0, o, s_final, nullptr, ws,
+                  (size_t)TLA_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 int tla_fwd_varlen(const tla_desc* d, const int32_t* cu_seqlens, long long total_tokens,

@@ -323,3 +323,14 @@ def test_conv_in_validation():
     assert bwd(dw=None) == E_NULL
     assert bwd(dy=dq) == E_ALIAS
     assert bwd(dw=dy) == E_ALIAS
+
+
+def test_noalloc_rejects_oversized_call_on_the_host():
+    """tla_fwd_noalloc checks its scratch need before any HIP call."""
+    L = tla.lib()
+    desc = tla.make_desc(tla.GDN, 4, 4096, 8, 128, 128, 8, 64, tla.BF16, tla.BF16)
+    nul = ctypes.c_void_p(None)
+    assert L.tla_fwd_noalloc(ctypes.byref(desc), *([nul] * 10), nul) == E_WS
+    assert b"scratch" in L.tla_last_error()
+    bad = tla.make_desc(tla.GDN, 4, 4096, 8, 128, 128, 3, 64, tla.BF16, tla.BF16)
+    assert L.tla_fwd_noalloc(ctypes.byref(bad), *([nul] * 10), nul) == E_UNSUP
