@@ -979,7 +979,8 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
 // own E/4 slices of the state each, in fp32 registers, and run only what the
 // next chunk waits for: their partial of W = sum_e diag(a_e) K S_e, U
 // (Tu (V - W) for GDN, diag(beta) V for sGLA) and the update
-// S_e <- gamma^C_e S_e + K^T diag(c_e) U of the chunkwise form (Section 3).
+// S_e <- gamma^C_e S_e + K^T diag(c_e) U of the chunkwise form (Appendix A,
+// Eq. joint-chunk).
 // After each update they leave the bf16 operand copy of the new state in
 // shared memory.  Waves 4..7 (output waves; wave 4 + i shares a SIMD with
 // state wave i) take it from there and form the chunk's output rows,
@@ -1169,8 +1170,9 @@ __global__ __launch_bounds__(512) void k_fwd_dual(Shape s, FwdIn in, PrepBufs p,
       Dma::gc(sm, p, ch);
       Dma::m(sm, p, ch);
 
-      // ---- W partial: sum over the wave's slices of diag(a_e) K S_e
-      state_pass(sm.K, Sop, sm.coef01[0], sm.W[w]);
+      // ---- W partial: sum over the wave's slices of diag(a_e) K S_e (GDN;
+      // sGLA has no W)
+      if (s.variant == 1) state_pass(sm.K, Sop, sm.coef01[0], sm.W[w]);
       wait_vmcnt<Dma::N_KT + 1 + Dma::N_M>();  // this chunk's Tu, V and beta have landed
       __syncthreads();  // B1
       if (more) {  // K, Q, a_e and b_e are free
