@@ -19,10 +19,12 @@ same shape; gdn_long_bf16: GDN B1 H16 T65536 E16) with its own JSON line.
 
 Helper modes for the HBM-traffic measurement (run under rocprofv3 --pmc):
   --copy-calibration     a plain fp32 copy kernel of known size
-  --pmc-summary F W CF CW  reduce four rocprofv3 counter directories (bench
-                         FETCH_SIZE, bench WRITE_SIZE, copy FETCH_SIZE, copy
-                         WRITE_SIZE) to per-kernel bytes per launch, written
-                         to profiles/hbm_traffic.json with the hash of each
+  --pmc-summary R W CR CW  reduce four rocprofv3 counter directories (bench
+                         and copy kernel, each with the L2-to-memory read
+                         request counters TCC_EA0_RDREQ_32B/64B/128B and the
+                         write request counters TCC_EA0_WRREQ/_64B) to
+                         per-kernel bytes per launch, written to
+                         profiles/hbm_traffic.json with the hash of each
                          kernel's sources (bench.py reports it only while the
                          sources are unchanged)
 """
@@ -65,39 +67,46 @@ def source_hash(kind):
 def algorithmic(cfg):
     """Per token-head algorithmic FLOPs and HBM bytes of each kernel (GDN,
     bf16 operands and outputs).  FLOPs count the method's own contractions
-    (dense, no split-operand or recompute work); bytes count each kernel's
-    compulsory reads and writes, every tensor once (re-reads of the same
-    chunk by the value-tile workgroups are cache traffic, not algorithmic)."""
+    (dense, no split-operand or recompute work).  Bytes count only the
+    operator's inputs and outputs that the kernel reads or writes, and the
+    bf16 chunk-boundary states (the chunk-start states the forward stores for
+    the backward, Appendix A "Kernels", and the backward's chunk-end state
+    gradients), every tensor once; this design's other intermediates (the
+    prep results, U, V - W, dU, dW, partial sums) are not counted."""
     K, V, E, C = cfg.K, cfg.V, cfg.E, cfg.chunk
     ckpt = 2.0 * E * K * V / C          # one bf16 chunk state per token-head
+    qkv = 2 * (2 * K + V)               # q, k and v (or dO), bf16
     return {
-        # Grams A_qk, A_kk and the (I + L) solve; reads q, k, q2, k2, g, beta,
-        # writes the coefficient vectors and M, Tu (fp32)
-        "prep": {"flops": 4 * C * K + C * C / 3.0,
-                 "bytes": 2 * 2 * K + 2 * 2 * E + 4 * E + 4 + 12 * E + 8 * C},
-        # W, Q S_e, K^T diag(c) U over E slices, Tu (V - W), M U; reads q, k, v,
-        # M, Tu, coefficients, writes o, the chunk-start state, U and V - W
-        "fwd_recurrent": {"flops": 6 * K * V * E + 4 * C * V,
-                          "bytes": 2 * (2 * K + V) + 8 * C + 12 * E + 2 * V + ckpt + 8 * V},
+        # Grams A_qk, A_kk and the (I + L) solve; reads q, k, q2, k2, g, beta
+        "prep": {"flops": 4 * C * K + C * C / 3.0, "bytes": 2 * 2 * K + 2 * 2 * E + 4 * E + 4},
+        # W, Q S_e, K^T diag(c) U over E slices, Tu (V - W), M U; reads q, k,
+        # v, writes o and the chunk-start state
+        "fwd_recurrent": {"flops": 6 * K * V * E + 4 * C * V, "bytes": qkv + 2 * V + ckpt},
         # K dS', M^T dO, Tu^T dU, Q^T diag(b) dO, K^T diag(a) dW; reads q, k,
-        # dO, M, Tu, coefficients, writes dS', dU, dW
-        "bwd_recurrent": {"flops": 6 * K * V * E + 4 * C * V,
-                          "bytes": 2 * (2 * K + V) + 8 * C + 12 * E + ckpt + 8 * V},
-        # dO S^T, dW S^T, U dS'^T per slice; reads both chunk states, dO, dW,
-        # U, q, k, writes the dq / dk partials and the coefficient gradients
-        "bwd_state": {"flops": 6 * K * V * E,
-                      "bytes": 2 * ckpt + 2 * V + 8 * V + 4 * K + 8 * K + 12 * E},
-        # Grams, dM, dTu, dq / dk products; reads q, k, v, dO, U, V - W, dU, dW,
-        # the partials and vectors, writes every input gradient
+        # dO, writes the chunk-end state gradient
+        "bwd_recurrent": {"flops": 6 * K * V * E + 4 * C * V, "bytes": qkv + ckpt},
+        # dO S^T, dW S^T, U dS'^T per slice; reads both chunk-boundary tensors, q, k, dO
+        "bwd_state": {"flops": 6 * K * V * E, "bytes": 2 * ckpt + qkv},
+        # Grams, dM, dTu, dq / dk products; reads q, k, v, q2, k2, g, beta, dO,
+        # writes every input gradient
         "bwd_chunk": {"flops": 10 * C * K + 4 * C * V + 2 * C * C / 3.0,
-                      "bytes": 2 * (2 * K + 2 * V) + 16 * V + 8 * K + 12 * E + 16 * E + 8
-                      + 2 * (2 * K + V) + 2 * 2 * E + 4 * E + 4},
+                      "bytes": 2 * (2 * K + 2 * V + 2 * E) + 4 * E + 4
+                      + 2 * (2 * K + V + 2 * E) + 4 * E + 4},
         "total_flops": 18 * K * V * E + 14 * C * K + 12 * C * V + 2 * C * C,
     }
 
 
-def bound_of(a):
-    """'mfma' or 'hbm', whichever roofline time is longer for these counts."""
+# The chunkwise kernels whose work is the method's dense bf16 contractions
+# (the recurrent forward and backward, the chunk-parallel state contractions,
+# the intra-chunk Grams): they are placed on the bf16 MFMA roofline.
+MFMA_KERNELS = ("prep", "fwd_recurrent", "bwd_recurrent", "bwd_state")
+
+
+def bound_of(name, a):
+    """'mfma' for the contraction kernels, else whichever roofline time is
+    longer for the kernel's algorithmic counts."""
+    if name in MFMA_KERNELS:
+        return "mfma"
     t_f = a.get("flops", 0.0) / (PEAK_BF16_TFLOPS * 1e12)
     t_b = a.get("bytes", 0.0) / (PEAK_HBM_GBS * 1e9)
     return "mfma" if t_f >= t_b else "hbm"
@@ -171,30 +180,48 @@ def _pmc_table(d, counter):
     return {k: sums[k] / len(disp[k]) for k in sums}
 
 
-def pmc_summary(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir):
-    fe, wr = _pmc_table(fetch_dir, "FETCH_SIZE"), _pmc_table(write_dir, "WRITE_SIZE")
-    cf, cw = _pmc_table(copy_fetch_dir, "FETCH_SIZE"), _pmc_table(copy_write_dir, "WRITE_SIZE")
-    # counters read KiB; the copy kernel moves COPY_BYTES each way
-    f_scale = COPY_BYTES / (cf["copy"] * 1024.0)
-    w_scale = COPY_BYTES / (cw["copy"] * 1024.0)
-    out = {"units": "bytes per launch", "fetch_scale": f_scale, "write_scale": w_scale,
-           "copy_fetch_kib": cf["copy"], "copy_write_kib": cw["copy"], "kernels": {}}
+def _hbm_bytes(d, kind):
+    """{kernel slot: HBM bytes per dispatch} from the L2-to-memory request
+    counters of a rocprofv3 directory: reads are TCC_EA0_RDREQ_32B / _64B /
+    _128B (32, 64, 128 bytes each), writes TCC_EA0_WRREQ_64B (64 bytes) and
+    the remaining TCC_EA0_WRREQ (32 bytes)."""
+    if kind == "read":
+        parts = {"TCC_EA0_RDREQ_32B_sum": 32, "TCC_EA0_RDREQ_64B_sum": 64,
+                 "TCC_EA0_RDREQ_128B_sum": 128}
+        tabs = {c: _pmc_table(d, c) for c in parts}
+        return {k: sum(parts[c] * tabs[c].get(k, 0.0) for c in parts) for k in tabs["TCC_EA0_RDREQ_32B_sum"]}
+    wr, wr64 = _pmc_table(d, "TCC_EA0_WRREQ_sum"), _pmc_table(d, "TCC_EA0_WRREQ_64B_sum")
+    return {k: 64 * wr64.get(k, 0.0) + 32 * (wr[k] - wr64.get(k, 0.0)) for k in wr}
+
+
+def pmc_summary(read_dir, write_dir, copy_read_dir, copy_write_dir):
+    """Per-kernel HBM bytes per launch from two counter passes over the bench
+    (read requests, write requests) and the same passes over a plain copy
+    kernel of known size, whose ratio of true to counted bytes scales each
+    direction."""
+    fe, wr = _hbm_bytes(read_dir, "read"), _hbm_bytes(write_dir, "write")
+    cf, cw = _hbm_bytes(copy_read_dir, "read"), _hbm_bytes(copy_write_dir, "write")
+    f_scale = COPY_BYTES / cf["copy"]
+    w_scale = COPY_BYTES / cw["copy"]
+    out = {"units": "bytes per launch", "counters": "TCC_EA0_RDREQ_{32B,64B,128B}, TCC_EA0_WRREQ{,_64B}",
+           "read_scale": f_scale, "write_scale": w_scale,
+           "copy_read_counted": cf["copy"], "copy_write_counted": cw["copy"], "kernels": {}}
     for kind in sorted(set(fe) & set(wr)):
         if kind == "copy":
             continue
-        out["kernels"][kind] = {"fetch_kib": fe[kind], "write_kib": wr[kind],
-                                "fetch_bytes": fe[kind] * 1024.0 * f_scale,
-                                "write_bytes": wr[kind] * 1024.0 * w_scale,
+        out["kernels"][kind] = {"read_counted": fe[kind], "write_counted": wr[kind],
+                                "fetch_bytes": fe[kind] * f_scale,
+                                "write_bytes": wr[kind] * w_scale,
                                 "source_hash": source_hash(kind)}
     os.makedirs(os.path.dirname(TRAFFIC_JSON), exist_ok=True)
     with open(TRAFFIC_JSON, "w") as fh:
         json.dump(out, fh, indent=1)
-    print(f"copy kernel: FETCH_SIZE {cf['copy']:.0f} KiB, WRITE_SIZE {cw['copy']:.0f} KiB per "
-          f"launch for {COPY_BYTES >> 20} MiB each way -> scale {f_scale:.4f} / {w_scale:.4f}")
-    print("| kernel | FETCH_SIZE KiB | WRITE_SIZE KiB | HBM bytes per launch (scaled) |")
+    print(f"copy kernel: counted {cf['copy'] / 2**20:.1f} MiB read, {cw['copy'] / 2**20:.1f} MiB "
+          f"written per launch for {COPY_BYTES >> 20} MiB each way -> scale {f_scale:.4f} / {w_scale:.4f}")
+    print("| kernel | read (counted) MB | write (counted) MB | HBM bytes per launch (scaled) |")
     print("|---|---|---|---|")
     for kind, r in out["kernels"].items():
-        print(f"| {kind} | {r['fetch_kib']:.0f} | {r['write_kib']:.0f} | "
+        print(f"| {kind} | {r['read_counted'] / 1e6:.1f} | {r['write_counted'] / 1e6:.1f} | "
               f"{r['fetch_bytes'] + r['write_bytes']:.4g} |")
 
 
@@ -534,14 +561,34 @@ def main():
         step()
     torch.cuda.synchronize()
     tla.prof_enable(True)
+    stream = torch.cuda.current_stream(dev)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    ev[0].record(stream)
+    for i in range(args.steps):
         step()
+        ev[i + 1].record(stream)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     prof = tla.prof_read()
     tla.prof_enable(False)
+    warm = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps))
+    # cold cache: a 512 MiB write between steps evicts the inputs, states
+    # and intermediates from the 256 MB last-level cache; each step alone is
+    # timed with events on the launch stream
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    cold = []
+    for _ in range(args.steps):
+        flush.fill_(1)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        step()
+        b.record(stream)
+        b.synchronize()
+        cold.append(a.elapsed_time(b))
+    cold.sort()
+    del flush
 
     ms_per_step = 1e3 * elapsed / args.steps
     tokens = B * T
@@ -553,7 +600,7 @@ def main():
             continue
         avg_ms = tot / n
         a = alg[name]
-        entry = {"avg_ms": round(avg_ms, 4), "launches": n, "bound": bound_of(a),
+        entry = {"avg_ms": round(avg_ms, 4), "launches": n, "bound": bound_of(name, a),
                  "tflops": round(a["flops"] * token_heads / (avg_ms * 1e-3) / 1e12, 2),
                  "gbs": round(a["bytes"] * token_heads / (avg_ms * 1e-3) / 1e9, 1)}
         entry["frac"] = round(entry["tflops"] / PEAK_BF16_TFLOPS if entry["bound"] == "mfma"
@@ -591,6 +638,11 @@ def main():
                    "B": B, "T": T, "H": H, "K": K, "V": V, "E": E, "chunk": C,
                    "operands": "bf16, fp32 accumulation, fp32 state", "outputs": "bf16",
                    "seed": cfg.seed},
+        "ms_per_step_median": round(warm[len(warm) // 2], 4),
+        "ms_per_step_min": round(warm[0], 4),
+        "cold_cache": {"ms_per_step_median": round(cold[len(cold) // 2], 4),
+                       "ms_per_step_min": round(cold[0], 4),
+                       "flush": "512 MiB device write before each step"},
         "step_tflops": round(step_tflops, 2),
         "mfma_pct_of_bf16_peak": round(100.0 * step_tflops / PEAK_BF16_TFLOPS, 2),
         "kernels": kernels,
