@@ -356,7 +356,10 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
 }
 
 // ---------------------------------------------------------------- forward
-template <typename T, int KD, int C, int E, int NW>
+// PK (the forward with state and output waves at E = 16): two key slices
+// share one 16-column accumulator tile, 8 value columns each; the W and O
+// partials are then stored once per value column (32 lanes).
+template <typename T, int KD, int C, int E, int NW, bool PK = false>
 struct FwdSmem {
   static constexpr int NT = C / 16;
   static constexpr int E4 = (E + 3) & ~3;
@@ -365,7 +368,8 @@ struct FwdSmem {
   // instances read the queries straight from global memory so that the plan
   // fits the 160 KiB of LDS.
   static constexpr bool SPLIT = sizeof(T) == 2;
-  static constexpr bool STAGE_Q = sizeof(T) == 2 && E < 16;
+  static constexpr bool STAGE_Q = sizeof(T) == 2 && (E < 16 || PK);
+  static constexpr int PL = PK ? 32 : 64;  // lanes of a partial-sum tile
   SwzTile<T, C, KD> K;
   SwzTile<T, STAGE_Q ? C : 1, STAGE_Q ? KD : EC> Q;
   SwzTile<T, KD, C> Kt;
@@ -379,8 +383,8 @@ struct FwdSmem {
   alignas(16) float coef2[E][C];      // c_e
   alignas(16) float gC[E4];
   alignas(16) float beta[C];
-  alignas(16) f32x4 W[NW][NT][64];
-  alignas(16) f32x4 O[NW][NT][64];
+  alignas(16) f32x4 W[NW][NT][PL];
+  alignas(16) f32x4 O[NW][NT][PL];
   alignas(16) f32x4 Us[NT][64];  // U row tiles in the accumulator layout
 };
 
@@ -398,10 +402,10 @@ struct FwdSmem {
 // T are read from row T - 1 (and zeroed after arrival in the last chunk);
 // M, Tu and K^T come from the prep kernel's operand tiles, whose rows and
 // columns past T are already zero.
-template <typename T, int KD, int C, int E, int NW>
+template <typename T, int KD, int C, int E, int NW, bool PK = false>
 struct FwdDma : GroupDma<NW> {
   typedef GroupDma<NW> G;
-  typedef FwdSmem<T, KD, C, E, NW> Sm;
+  typedef FwdSmem<T, KD, C, E, NW, PK> Sm;
   typedef OpTiles<T, KD, C> OT;
   using G::tile;
   using G::wid;
@@ -479,6 +483,7 @@ struct FwdDma : GroupDma<NW> {
   // permuted row order of Sm::Vr; wave w copies 16-byte pieces
   // [w VL, (w + 1) VL) of the tile.  Rows past T read row T - 1 (zeroed after
   // arrival in the last chunk).  Vg points at the columns' start in row t0.
+  // PK: the workgroup's 8 columns fill both halves of each row.
   static constexpr int PPR = 16 * (int)sizeof(T) / 16;  // 16-byte pieces per row
   static constexpr int VL = C * PPR / NW;                // lanes per wave
   static_assert(C * PPR % NW == 0 && VL <= 64, "V tile split over the waves");
@@ -486,7 +491,7 @@ struct FwdDma : GroupDma<NW> {
     const int w = wid(), l = lane_id();
     const int q = w * VL + l, pos = q / PPR, part = q % PPR;
     const int r = (pos & ~15) + 4 * (pos & 3) + ((pos >> 2) & 3);  // row held at position pos
-    const uint32_t off = (uint32_t)(sizeof(T) * (size_t)min(r, last) * vrs) + 16 * part;
+    const uint32_t off = (uint32_t)(sizeof(T) * (size_t)min(r, last) * vrs) + (PK ? 0 : 16 * part);
     if (l < VL) lds_dma<16>(Vg, off, lds_addr(&sm.Vr[0][0]) + 16 * w * VL);
   }
   // beta of the chunk's rows (sGLA with beta), rows past T read row T - 1;
@@ -995,37 +1000,53 @@ __global__ __launch_bounds__(NW * 64) void k_fwd(Shape s, FwdIn in, PrepBufs p, 
 // memory: a wave's vmcnt wait for a copy also waits for the stores it issued
 // before the copy, which under the write traffic of all workgroups take
 // thousands of cycles to be acknowledged.
-template <typename T, int KD, int C, int E>
+template <typename T, int KD, int C, int E, bool PK = false>
 struct DualSmem {
-  FwdSmem<T, KD, C, E, 4> f;
-  // bf16 operand copy of the chunk-start state: [slice][key tile][lane], each
-  // lane's entry as the state wave's lane holds it in registers
-  alignas(16) typename Elem<T>::frag sop[E][KD / 16][64];
+  FwdSmem<T, KD, C, E, 4, PK> f;
+  // bf16 operand copy of the chunk-start state: [slice (PK: slice pair)][key
+  // tile][lane], each lane's entry as the state wave's lane holds it
+  alignas(16) typename Elem<T>::frag sop[PK ? E / 2 : E][KD / 16][64];
 };
 
-template <typename T, int KD, int C, int E>
+// PK (inference at E = 16, K = 128): the workgroup owns 8 value columns and
+// each accumulator tile holds two key slices side by side (columns 0..7:
+// slice 2 u, columns 8..15: slice 2 u + 1 of "unit" u), so that the per-unit
+// work and shared memory match the E = 8 instance and the long-context
+// shape (few heads) launches twice the workgroups.  The row coefficients
+// then differ between the two column halves of a tile, and the W and O
+// partials are summed over the halves (a DPP rotation by 8 lanes).  The
+// U tile is formed with both halves holding the same 8 columns (V is copied
+// into both).  No checkpoints: training forwards keep the 16-column kernel.
+template <typename T, int KD, int C, int E, bool PK = false>
 __global__ __launch_bounds__(512) void k_fwd_dual(Shape s, FwdIn in, PrepBufs p, void* out,
                                                   float* s_final, SavedBufs sv, int train) {
   constexpr int NG = 4;  // waves per role
-  constexpr int SPW = E / NG;
+  constexpr int UE = PK ? E / 2 : E;  // slices or slice pairs
+  constexpr int SPW = UE / NG;
   constexpr int NT = C / 16;
   constexpr int KT = KD / 16;
   constexpr int NTHR = 2 * NG * 64;
-  static_assert(E % NG == 0 && sizeof(T) == 2, "bf16 operands, whole slices per wave");
+  constexpr int VW = PK ? 8 : 16;     // value columns of a workgroup
+  static_assert(UE % NG == 0 && sizeof(T) == 2, "bf16 operands, whole slices per wave");
   typedef typename Elem<T>::frag F;
-  typedef FwdSmem<T, KD, C, E, NG> Sm;
-  typedef FwdDma<T, KD, C, E, NG> Dma;
+  typedef FwdSmem<T, KD, C, E, NG, PK> Sm;
+  typedef FwdDma<T, KD, C, E, NG, PK> Dma;
   static_assert(Sm::STAGE_Q && Sm::SPLIT, "queries staged, Tu and M as hi + lo pairs");
   extern __shared__ __align__(16) unsigned char smem_raw[];
-  DualSmem<T, KD, C, E>& smd = *reinterpret_cast<DualSmem<T, KD, C, E>*>(smem_raw);
+  DualSmem<T, KD, C, E, PK>& smd = *reinterpret_cast<DualSmem<T, KD, C, E, PK>*>(smem_raw);
   Sm& sm = smd.f;
+  if constexpr (PK) train = 0;
 
   const int wv = wave_id(), w = wv & (NG - 1), l = lane_id(), g = l >> 4, n = l & 15;
   const int V = s.V;
   int head, vt;
-  xcd_map(blockIdx.x, s.NH, V / 16, head, vt);
+  xcd_map(blockIdx.x, s.NH, V / VW, head, vt);
   const int b = head / s.H, h = head % s.H;
-  const int v0 = vt * 16;
+  const int v0 = vt * VW;
+  // the key slice and value column of this lane in unit i of its wave
+  const int vc = PK ? (n & 7) : n;
+  auto slc = [&](int i) { return PK ? 2 * (w * SPW + i) + (n >> 3) : w * SPW + i; };
+  const int pl = PK ? 8 * g + (n & 7) : l;  // this lane's entry of a partial-sum tile
   const size_t tok0 = seq_begin(s, b);
   s.T = seq_len(s, b);                 // this sequence's length from here on
   const int nc = (s.T + C - 1) / C;    // its chunks (s.Nc: the per-head stride)
@@ -1060,7 +1081,7 @@ __global__ __launch_bounds__(512) void k_fwd_dual(Shape s, FwdIn in, PrepBufs p,
   // The fragments of the next k-block pair are read before the MFMAs of the
   // current one.
   auto state_pass = [&](const decltype(sm.K)& X, const F(&So)[SPW][KT], const float(*cf)[C],
-                        f32x4(*dst)[64]) {
+                        f32x4(*dst)[Sm::PL]) {
     f32x4 P[SPW][NT];
 #pragma unroll
     for (int i = 0; i < SPW; ++i)
@@ -1100,8 +1121,14 @@ __global__ __launch_bounds__(512) void k_fwd_dual(Shape s, FwdIn in, PrepBufs p,
     for (int rt = 0; rt < NT; ++rt) {
       f32x4 acc = zero4();
 #pragma unroll
-      for (int i = 0; i < SPW; ++i) acc += *(const f32x4*)&cf[w * SPW + i][16 * rt + 4 * g] * P[i][rt];
-      dst[rt][l] = acc;
+      for (int i = 0; i < SPW; ++i) acc += *(const f32x4*)&cf[slc(i)][16 * rt + 4 * g] * P[i][rt];
+      if constexpr (PK) {  // the two slices of each unit: columns n and n + 8
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[j] += dpp_f<0x128>(acc[j]);  // row_ror:8
+        if (n < 8) dst[rt][pl] = acc;
+      } else {
+        dst[rt][l] = acc;
+      }
     }
   };
 
@@ -1137,18 +1164,18 @@ __global__ __launch_bounds__(512) void k_fwd_dual(Shape s, FwdIn in, PrepBufs p,
     F Sop[SPW][KT];
 #pragma unroll
     for (int i = 0; i < SPW; ++i) {
-      const int e = w * SPW + i;
+      const int e = slc(i);
 #pragma unroll
       for (int kt = 0; kt < KT; ++kt) {
         f32x4 x = zero4();
         if (in.s0) {
-          const float* src = in.s0 + (((size_t)head * E + e) * KD + key_col<KD>(kt, g)) * V + v0 + n;
+          const float* src = in.s0 + (((size_t)head * E + e) * KD + key_col<KD>(kt, g)) * V + v0 + vc;
 #pragma unroll
           for (int j = 0; j < 4; ++j) x[j] = src[(size_t)j * V];
         }
         S[i][kt] = x;
         Sop[i][kt] = cvt_frag<T>(x);
-        smd.sop[e][kt][l] = Sop[i][kt];
+        smd.sop[w * SPW + i][kt][l] = Sop[i][kt];
       }
     }
     if (nc > 0) {
@@ -1196,7 +1223,7 @@ __global__ __launch_bounds__(512) void k_fwd_dual(Shape s, FwdIn in, PrepBufs p,
 #pragma unroll
             for (int j = 0; j < 4; ++j) vr[kb][j] = sm.Vr[16 * kb + 4 * j + g][n];
 #pragma unroll
-            for (int ww = 0; ww < NG; ++ww) wq[ww][kb] = sm.W[ww][kb][l];
+            for (int ww = 0; ww < NG; ++ww) wq[ww][kb] = sm.W[ww][kb][pl];
             th[kb] = ld_frag(sm.Tu.at(r, 16 * kb + 4 * g));
             tl[kb] = ld_frag(sm.TuL.at(r, 16 * kb + 4 * g));
           }
@@ -1247,7 +1274,7 @@ __global__ __launch_bounds__(512) void k_fwd_dual(Shape s, FwdIn in, PrepBufs p,
       F Uc[SPW][NT], Ucl[SPW][NT];
 #pragma unroll
       for (int i = 0; i < SPW; ++i) {
-        const int e = w * SPW + i;
+        const int e = slc(i);
         const float gc = sm.gC[e];
 #pragma unroll
         for (int kt = 0; kt < KT; ++kt) S[i][kt] *= gc;
@@ -1301,10 +1328,10 @@ __global__ __launch_bounds__(512) void k_fwd_dual(Shape s, FwdIn in, PrepBufs p,
     if (s_final) {
 #pragma unroll
       for (int i = 0; i < SPW; ++i) {
-        const int e = w * SPW + i;
+        const int e = slc(i);
 #pragma unroll
         for (int kt = 0; kt < KT; ++kt) {
-          float* dst = s_final + (((size_t)head * E + e) * KD + key_col<KD>(kt, g)) * V + v0 + n;
+          float* dst = s_final + (((size_t)head * E + e) * KD + key_col<KD>(kt, g)) * V + v0 + vc;
 #pragma unroll
           for (int j = 0; j < 4; ++j) dst[(size_t)j * V] = S[i][kt][j];
         }
@@ -1362,7 +1389,7 @@ __global__ __launch_bounds__(512) void k_fwd_dual(Shape s, FwdIn in, PrepBufs p,
 #pragma unroll
         for (int j = 0; j < 4; ++j) vr[j] = sm.Vr[16 * rt + 4 * j + g][n];
 #pragma unroll
-        for (int ww = 0; ww < NG; ++ww) wq[ww] = sm.W[ww][rt][l];
+        for (int ww = 0; ww < NG; ++ww) wq[ww] = sm.W[ww][rt][pl];
         f32x4 x;
 #pragma unroll
         for (int j = 0; j < 4; ++j) x[j] = Elem<T>::to_f(vr[j]);
@@ -1389,7 +1416,7 @@ __global__ __launch_bounds__(512) void k_fwd_dual(Shape s, FwdIn in, PrepBufs p,
           U[kb] = sm.Us[kb][l];
         }
 #pragma unroll
-        for (int ww = 0; ww < NG; ++ww) op[ww] = sm.O[ww][rt][l];
+        for (int ww = 0; ww < NG; ++ww) op[ww] = sm.O[ww][rt][pl];
         __builtin_amdgcn_sched_barrier(0);  // the reads above stay together
 #pragma unroll
         for (int kb = 0; kb < NT; ++kb) split_frag(U[kb], Uh[kb], Ul[kb]);
@@ -1408,7 +1435,7 @@ __global__ __launch_bounds__(512) void k_fwd_dual(Shape s, FwdIn in, PrepBufs p,
         // 4 (n / 4) .. + 3
         const f32x4 y = quad_transpose(oacc, n);
         const int t = t0 + 16 * rt + 4 * g + (n & 3);
-        if (t < s.T) {
+        if (t < s.T && (!PK || n < 8)) {  // (PK: columns 8..15 repeat 0..7)
           const size_t off = ((tok0 + t) * s.H + h) * (size_t)V + v0 + 4 * (n >> 2);
           if (s.out_bf16)
             *(bf16x4*)((bf16_t*)out + off) = cvt_frag<bf16_t>(y);
@@ -1451,10 +1478,32 @@ constexpr bool fwd_dual() {
          sizeof(DualSmem<T, KD, C, E>) <= 160 * 1024;
 }
 
+// The same kernel with two slices per tile (inference at E = 16, K = 128,
+// chunk 64): 8 value columns per workgroup, twice the workgroups.
+template <typename T, int KD, int C, int E>
+constexpr bool fwd_pk() {
+  return sizeof(T) == 2 && E == 16 && KD == 128 && C == 64 &&
+         sizeof(DualSmem<T, KD, C, E, true>) <= 160 * 1024;
+}
+
 template <typename T, int KD, int C, int E>
 static hipError_t fwd_inst(const Shape& s, const FwdIn& in, const PrepBufs& p, void* o,
                            float* s_final, const SavedBufs* sv, hipStream_t st) {
   SavedBufs none{nullptr, nullptr, nullptr};
+  if constexpr (fwd_pk<T, KD, C, E>()) {
+    if (!sv) {
+      const size_t smem = sizeof(DualSmem<T, KD, C, E, true>);
+      static bool attr_pk = false;
+      if (!attr_pk) {
+        (void)hipFuncSetAttribute((const void*)k_fwd_dual<T, KD, C, E, true>,
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+        attr_pk = true;
+      }
+      hipLaunchKernelGGL((k_fwd_dual<T, KD, C, E, true>), dim3(s.NH * (s.V / 8)), dim3(512), smem,
+                         st, s, in, p, o, s_final, none, 0);
+      return hipGetLastError();
+    }
+  }
   if constexpr (fwd_dual<T, KD, C, E>()) {
     const size_t smem = sizeof(DualSmem<T, KD, C, E>);
     static bool attr_set = false;

@@ -159,3 +159,25 @@ def test_autograd_wrapper_matches_bwd(variant):
                     synth.to64(inp["s0"]), synth.to64(dO.cpu()), synth.to64(wf.cpu()))
     for n in NAMES:
         assert rel_err(host64(leaves[n].grad), rg["d" + n]) <= TOL_F32, n
+
+
+@pytest.mark.parametrize("variant", [SGLA, GDN])
+@pytest.mark.parametrize("V,T,s0", [(128, 150, 0.02), (64, 77, 0.0), (256, 200, 0.02)])
+def test_e16_inference_forward(variant, V, T, s0):
+    """E = 16, K = 128, chunk 64 with bf16 operands: the inference forward
+    (two key slices per accumulator tile, 8 value columns per workgroup) and
+    the training forward (16 columns per workgroup) against the oracle."""
+    cfg = cfg_of(variant, "bf16", B=1, T=T, H=3, K=128, V=V, E=16, chunk=64, s0=s0, seed=23)
+    inp = synth.make_inputs(cfg)
+    d = {k: dev(v) for k, v in inp.items()}
+    args = [d[n] for n in NAMES] + [d["beta"], d["s0"]]
+    o, sf, _ = tla.fwd(variant, *args, chunk=64, out_dtype=torch.float32)
+    o_t, sf_t, _ = tla.fwd(variant, *args, chunk=64, out_dtype=torch.float32, training=True)
+    torch.cuda.synchronize()
+    ro, rs = oracle.fwd(variant, *[synth.to64(inp[n]) for n in NAMES], synth.to64(inp["beta"]),
+                        synth.to64(inp["s0"]))
+    errs = {"o": rel_err(host64(o), ro), "s_final": rel_err(host64(sf), rs),
+            "o_train": rel_err(host64(o_t), ro), "s_final_train": rel_err(host64(sf_t), rs)}
+    print(f"E16 variant={variant} V={V} T={T}: " + " ".join(f"{k}={v:.1e}" for k, v in errs.items()),
+          flush=True)
+    assert all(v <= TOL_BF16 for v in errs.values()), errs
