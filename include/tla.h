@@ -82,7 +82,7 @@ typedef struct tla_desc {
 /*
  * Supported shapes: K in {16, 32, 64, 128}, V a multiple of 16 up to 1024,
  * E in {1, 2, 4, 8, 16, 32}, chunk in {16, 32, 64}, for the (K, chunk, E)
- * triples instantiated in the library: (16, 16, 4), (32, 32, 4),
+ * triples instantiated in the library: (16, 16, 1 / 2 / 4 / 8 / 16), (32, 32, 4),
  * (32, 32, 32), (64, 32, 8), (64, 64, 16), (128, 64, 1 / 4 / 8 / 16) and
  * (128, 32, 8); fp32 operands at (128, 64, 16) exceed the shared-memory
  * budget (tla_supported() tells).  tla_step has its own instances: (K, E) in

@@ -328,7 +328,9 @@ class TriadicAttention(torch.autograd.Function):
     """Autograd wrapper of one training forward (tla_fwd with a `saved`
     buffer) and its backward (tla_bwd).  Inputs as for fwd(); returns
     (o, s_final).  Gradients flow to q, k, v, q2, k2, g, beta and s0 (those
-    given).  The `saved` buffer of the forward is held until the backward."""
+    given); those of q, k, v, q2, k2 have out_dtype (default: the operand
+    type), as o does.  The `saved` buffer of the forward is held until the
+    backward."""
 
     @staticmethod
     def forward(ctx, q, k, v, q2, k2, g, beta, s0, variant, chunk, out_dtype):
@@ -336,7 +338,7 @@ class TriadicAttention(torch.autograd.Function):
                                 out_dtype=out_dtype, training=True)
         ctx.save_for_backward(q, k, v, q2, k2, g, beta, s0)
         ctx.saved_buffer = saved
-        ctx.variant, ctx.chunk = variant, chunk
+        ctx.variant, ctx.chunk, ctx.out_dtype = variant, chunk, out_dtype
         return o, s_final
 
     @staticmethod
@@ -347,7 +349,7 @@ class TriadicAttention(torch.autograd.Function):
         do = do.to(q.dtype).contiguous()
         dsf = None if dsf is None else dsf.float().contiguous()
         gr = bwd(ctx.variant, q, k, v, q2, k2, g, beta, s0, do, ctx.saved_buffer, dS_final=dsf,
-                 chunk=ctx.chunk, out_dtype=q.dtype, want_ds0=s0 is not None)
+                 chunk=ctx.chunk, out_dtype=ctx.out_dtype or q.dtype, want_ds0=s0 is not None)
         ctx.saved_buffer = None
         return (gr["dq"], gr["dk"], gr["dv"], gr["dq2"], gr["dk2"], gr["dg"], gr["dbeta"],
                 gr["ds0"], None, None, None)

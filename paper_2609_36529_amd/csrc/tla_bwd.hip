@@ -1811,7 +1811,11 @@ static hipError_t chunk_inst(const Shape& s, const FwdIn& in, const void* dO, co
     return CALL(float, KD_, C_, E_);                     \
   }
 #define TLA_BWD_FOR_EACH(CALL)      \
+  TLA_BWD_DISPATCH(16, 16, 1, CALL) \
+  TLA_BWD_DISPATCH(16, 16, 2, CALL) \
   TLA_BWD_DISPATCH(16, 16, 4, CALL) \
+  TLA_BWD_DISPATCH(16, 16, 8, CALL) \
+  TLA_BWD_DISPATCH(16, 16, 16, CALL) \
   TLA_BWD_DISPATCH(32, 32, 4, CALL) \
   TLA_BWD_DISPATCH(64, 32, 8, CALL) \
   TLA_BWD_DISPATCH(64, 64, 16, CALL) \

@@ -1537,7 +1537,11 @@ static hipError_t fwd_inst(const Shape& s, const FwdIn& in, const PrepBufs& p, v
   }
 
 #define TLA_FOR_EACH_INSTANCE(CALL) \
+  TLA_DISPATCH(16, 16, 1, CALL)     \
+  TLA_DISPATCH(16, 16, 2, CALL)     \
   TLA_DISPATCH(16, 16, 4, CALL)     \
+  TLA_DISPATCH(16, 16, 8, CALL)     \
+  TLA_DISPATCH(16, 16, 16, CALL)    \
   TLA_DISPATCH(32, 32, 4, CALL)     \
   TLA_DISPATCH(64, 32, 8, CALL)     \
   TLA_DISPATCH(64, 64, 16, CALL)     \
@@ -1578,7 +1582,8 @@ bool fits_lds(int K, int C, int E, bool bf16) {
 }
 
 bool have_instance(int K, int C, int E) {
-  return (K == 16 && C == 16 && E == 4) || (K == 32 && C == 32 && E == 4) ||
+  return (K == 16 && C == 16 && (E == 1 || E == 2 || E == 4 || E == 8 || E == 16)) ||
+         (K == 32 && C == 32 && E == 4) ||
          (K == 32 && C == 32 && E == 32) || (K == 64 && C == 32 && E == 8) ||
          (K == 64 && C == 64 && E == 16) ||
          (K == 128 && C == 64 && (E == 1 || E == 4 || E == 8 || E == 16)) ||

@@ -181,3 +181,12 @@ def test_e16_inference_forward(variant, V, T, s0):
     print(f"E16 variant={variant} V={V} T={T}: " + " ".join(f"{k}={v:.1e}" for k, v in errs.items()),
           flush=True)
     assert all(v <= TOL_BF16 for v in errs.values()), errs
+
+
+@pytest.mark.parametrize("variant", [SGLA, GDN])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("E", [1, 2, 4, 8, 16])
+def test_head_dim_16_instances(variant, dtype, E):
+    """K = V = 16, chunk 16 (the MQAR model's heads) at every E of its sweep."""
+    cfg = cfg_of(variant, dtype, B=2, T=45, H=3, K=16, V=16, E=E, chunk=16, seed=29)
+    check_fwd_bwd(cfg, TOL_F32 if dtype == "f32" else TOL_BF16, unit_dsf=(dtype == "f32"))
