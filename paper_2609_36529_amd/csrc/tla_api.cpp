@@ -157,11 +157,13 @@ Layout layout(const tla::Shape& s) {
   return L;
 }
 
-// `ninv`: whether the prep kernel also keeps (I + L)^{-1} for the backward
+// `ninv`: a training forward's prep results, which also keep (I + L)^{-1}
+// (GDN) and the transposed operand tiles for the backward
 tla::PrepBufs prep_bufs(const Layout& L, const void* base, bool ninv) {
   char* b = (char*)base;
   return tla::PrepBufs{(float*)(b + L.p_coef), (float*)(b + L.p_gC), (void*)(b + L.p_ops),
-                       (ninv && L.p_ninv < L.p_size) ? (float*)(b + L.p_ninv) : nullptr};
+                       (ninv && L.p_ninv < L.p_size) ? (float*)(b + L.p_ninv) : nullptr,
+                       ninv ? 1 : 0};
 }
 tla::SavedBufs saved_bufs(const Layout& L, const void* saved) {
   char* b = (char*)saved;

@@ -222,7 +222,8 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
 #pragma unroll
     for (int pt = 0; pt < OT::NS; ++pt) {
       store_tile16(ops + OT::M + pt * OT::MAT + (size_t)(16 * rt) * C + 16 * st, parts[pt], g, n, C);
-      put4<T>(ops + OT::MT + pt * OT::MAT + (size_t)(16 * st + n) * C + 16 * rt + 4 * g, parts[pt]);
+      if (p.bwd_tiles)
+        put4<T>(ops + OT::MT + pt * OT::MAT + (size_t)(16 * st + n) * C + 16 * rt + 4 * g, parts[pt]);
     }
   };
   for (int tile = w; tile < NT * NT; tile += 4) {
@@ -281,10 +282,12 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
     }
     put_m(rt, st, mv);
   }
-  // ---- K^T and Q^T of the chunk (4 x 4 blocks; rows past T are zero)
+  // ---- K^T (and for the backward Q^T) of the chunk (4 x 4 blocks; rows
+  // past T are zero)
   {
     constexpr int NB = (C / 4) * (KD / 4);
-    for (int idx = tid; idx < 2 * NB; idx += 256) {
+    const int nmat = p.bwd_tiles ? 2 : 1;
+    for (int idx = tid; idx < nmat * NB; idx += 256) {
       const int mtx = idx / NB, bi = idx % NB;
       const int rb = bi / (KD / 4), kb = bi % (KD / 4);
       float x[4][4];
@@ -344,11 +347,13 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
           const f32x4 hr = bf16x4_to_f(cvt_frag<bf16_t>(x[i])), hc = bf16x4_to_f(cvt_frag<bf16_t>(col));
           put4<T>(ops + OT::Tu + (size_t)(4 * rb + i) * C + 4 * cb, hr);
           put4<T>(ops + OT::Tu + OT::MAT + (size_t)(4 * rb + i) * C + 4 * cb, x[i] - hr);
-          put4<T>(ops + OT::TuT + (size_t)(4 * cb + i) * C + 4 * rb, hc);
-          put4<T>(ops + OT::TuT + OT::MAT + (size_t)(4 * cb + i) * C + 4 * rb, col - hc);
+          if (p.bwd_tiles) {
+            put4<T>(ops + OT::TuT + (size_t)(4 * cb + i) * C + 4 * rb, hc);
+            put4<T>(ops + OT::TuT + OT::MAT + (size_t)(4 * cb + i) * C + 4 * rb, col - hc);
+          }
         } else {
           put4<T>(ops + OT::Tu + (size_t)(4 * rb + i) * C + 4 * cb, x[i]);
-          put4<T>(ops + OT::TuT + (size_t)(4 * cb + i) * C + 4 * rb, col);
+          if (p.bwd_tiles) put4<T>(ops + OT::TuT + (size_t)(4 * cb + i) * C + 4 * rb, col);
         }
       }
     }

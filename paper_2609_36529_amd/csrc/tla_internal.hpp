@@ -47,6 +47,7 @@ struct PrepBufs {
   float* gC;     // [ch][E4]       gamma^C (E4 = E rounded up to 4)
   void* ops;     // [ch][op_tile_elems] operand tiles, see OpTiles
   float* ninv;   // [ch][C][C]     (I + L)^{-1} in fp32 (GDN training forward), or NULL
+  int bwd_tiles; // training forward: also write M^T, Tu^T and Q^T (read only by the backward)
 };
 
 // Operand tiles of one chunk, in the operand type T and in the layouts the
@@ -55,6 +56,8 @@ struct PrepBufs {
 // transposed, as bf16 (hi, lo) pairs for bf16 operands (one fp32 copy for
 // fp32 operands), then K^T and Q^T of the chunk (rows past T are zero; key k
 // in row row_of_key(k), the key order of the recurrent kernels' state tiles).
+// The transposed copies and Q^T serve the backward only: an inference
+// forward leaves them unwritten.
 // Element offsets within a chunk's block; part p (0 = hi, 1 = lo) of a
 // matrix X starts at X + p * MAT.
 template <typename T, int KD, int C>
