@@ -229,12 +229,15 @@ __device__ __forceinline__ float group16_sum(float x) {
 // multiple of 16), blockwise: the 16 x 16 diagonal blocks by forward
 // substitution (one column per thread), then the blocks below the diagonal
 // level by level, X_IJ = -X_II sum_{K=J}^{I-1} L_IK X_KJ (all blocks of one
-// level at once).  L(r, c) is an accessor; X is a C x ldx fp32 LDS array;
-// Y is (C/16 - 1) x 16 x 17 floats of LDS scratch.  Every thread of the
-// workgroup must call it; it ends with a barrier.
+// level at once, one wave per block, both products on the fp32 MFMA).
+// L(r, c) is an accessor; X is a C x ldx fp32 LDS array; Y is
+// (C/16 - 1) x 16 x 17 floats of LDS scratch.  Every thread of the
+// workgroup must call it (NTHR / 64 >= C / 16 - 1 waves); it ends with a
+// barrier.
 template <int C, int NTHR, typename LF>
 __device__ void unit_lower_inverse(LF L, float* X, int ldx, float* Y) {
   constexpr int NT = C / 16;
+  static_assert(NTHR / 64 >= NT - 1, "one wave per off-diagonal block of a level");
   const int tid = threadIdx.x;
   for (int idx = tid; idx < C * C; idx += NTHR) X[(idx / C) * ldx + idx % C] = 0.f;
   __syncthreads();
@@ -252,22 +255,29 @@ __device__ void unit_lower_inverse(LF L, float* X, int ldx, float* Y) {
     for (int i = 0; i < 16; ++i) X[(r0 + i) * ldx + r0 + col] = x[i];
   }
   __syncthreads();
+  // 16x16x4 fp32 MFMA: lane (g, n) gives A[n][g] and B[g][n] of each 4-deep
+  // step and holds C[4 g + j][n]
+  const int w = tid >> 6, g = (tid >> 4) & 3, n = tid & 15;
   for (int d = 1; d < NT; ++d) {
-    const int npairs = NT - d;
-    for (int idx = tid; idx < npairs * 256; idx += NTHR) {
-      const int pr = idx / 256, i = (idx / 16) % 16, j = idx % 16;
-      const int I = d + pr, J = pr;
-      float acc = 0.f;
-      for (int kk = 16 * J; kk < 16 * I; ++kk) acc += L(16 * I + i, kk) * X[kk * ldx + 16 * J + j];
-      Y[(pr * 16 + i) * 17 + j] = acc;
+    const bool act = w < NT - d;  // wave w: block (I, J) = (d + w, w)
+    const int I = d + w, J = w;
+    if (act) {
+      f32x4 y = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int kb = 16 * J; kb < 16 * I; kb += 4)
+        y = __builtin_amdgcn_mfma_f32_16x16x4f32(L(16 * I + n, kb + g), X[(kb + g) * ldx + 16 * J + n],
+                                                 y, 0, 0, 0);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) Y[(w * 16 + 4 * g + j) * 17 + n] = y[j];
     }
     __syncthreads();
-    for (int idx = tid; idx < npairs * 256; idx += NTHR) {
-      const int pr = idx / 256, i = (idx / 16) % 16, j = idx % 16;
-      const int I = d + pr, J = pr;
-      float acc = 0.f;
-      for (int m = 0; m <= i; ++m) acc += X[(16 * I + i) * ldx + 16 * I + m] * Y[(pr * 16 + m) * 17 + j];
-      X[(16 * I + i) * ldx + 16 * J + j] = -acc;
+    if (act) {
+      f32x4 x = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int m = 0; m < 16; m += 4)
+        x = __builtin_amdgcn_mfma_f32_16x16x4f32(X[(16 * I + n) * ldx + 16 * I + m + g],
+                                                 Y[(w * 16 + m + g) * 17 + n], x, 0, 0, 0);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) X[(16 * I + 4 * g + j) * ldx + 16 * J + n] = -x[j];
     }
     __syncthreads();
   }
