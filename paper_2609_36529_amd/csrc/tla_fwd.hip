@@ -60,14 +60,33 @@ __device__ __forceinline__ void mma_k(f32x4& acc, FA fa, FB fb) {
 // ------------------------------------------------------------------- prep
 // LDS plan: Q and K rows (bf16 instances) share their space with the inverse
 // of (I + L) and its scratch, which are formed after the Grams.
+//
+// Every operand tile leaves as whole 128-byte lines (eight consecutive
+// elements per lane, consecutive lanes along a row) with the nontemporal
+// hint: the recurrent kernel that runs next reads these tiles once, and
+// partly written lines left dirty in L2 were written back while it ran
+// (measured 40-50 us slower at B4 H8 T4096).  The transposed copies are
+// read out of shared memory column-wise: M from a copy of it (LINES), Tu
+// from the inverse, K^T and Q^T from the staged rows.  Instances whose plan
+// would then exceed two workgroups per CU keep the per-tile stores.
 template <typename T, int KD, int C, int E>
 struct PrepSmem {
   static constexpr int KP = KD + 8;  // 16-byte rows, conflict-free 16-byte fragment reads
   static constexpr int CP = C + 4;
   static constexpr int NT = C / 16;
   static constexpr bool STAGE = sizeof(T) == 2;  // fp32 rows are read from global memory
+  static constexpr size_t plan_bytes(bool lines) {
+    const size_t qk = 2 * (STAGE ? C : 1) * KP * sizeof(T) + (lines ? C * CP * 4 : 0);
+    const size_t inv = C * CP * 4 + (NT > 1 ? NT - 1 : 1) * 16 * 17 * 4;
+    return (qk > inv ? qk : inv) + C * CP * 4 + 2 * C * E * 4 + C * E * 8 + C * 4 + 64;
+  }
+  static constexpr bool LINES = STAGE && plan_bytes(true) <= 80 * 1024;
   union U {
-    struct { T sQ[STAGE ? C : 1][KP]; T sK[STAGE ? C : 1][KP]; } qk;
+    struct {
+      T sQ[STAGE ? C : 1][KP];
+      T sK[STAGE ? C : 1][KP];
+      float Mb[LINES ? C : 1][CP];  // M, for the line-wise row-major and transposed copies
+    } qk;
     struct { float X[C][CP]; float Y[NT > 1 ? NT - 1 : 1][16][17]; } inv;
   };
   alignas(16) U u;
@@ -77,6 +96,18 @@ struct PrepSmem {
   alignas(16) double G[C][E];  // in-chunk cumulative log-gates
   alignas(16) float beta[C];
 };
+
+// Eight consecutive values of a bf16 (hi, lo) operand tile: the high parts
+// at dst, the low parts one matrix (C x C elements) further, one 16-byte
+// nontemporal store each.
+template <int C>
+__device__ __forceinline__ void store8_split(bf16_t* dst, f32x4 x0, f32x4 x1) {
+  bf16x4 h0, l0, h1, l1;
+  split_frag(x0, h0, l0);
+  split_frag(x1, h1, l1);
+  gstore_b128(dst, __builtin_bit_cast(u32x4, __builtin_shufflevector(h0, h1, 0, 1, 2, 3, 4, 5, 6, 7)));
+  gstore_b128(dst + C * C, __builtin_bit_cast(u32x4, __builtin_shufflevector(l0, l1, 0, 1, 2, 3, 4, 5, 6, 7)));
+}
 
 template <typename T, int KD, int C, int E>
 __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
@@ -176,13 +207,21 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
 
   // ---- coefficient vectors a = k2 gamma, b = q2 gamma, c = k2 gamma^C / gamma; gamma^C
   float* coef = p.coef + (size_t)ch * 3 * E * C;
-  for (int idx = tid; idx < E * C; idx += 256) {
-    const int e = idx / C, r = idx % C;
-    const double G = sm.G[r][e], GC = sm.G[C - 1][e];
-    const float gam = exp_nonpos((float)G);
-    coef[(0 * E + e) * C + r] = sm.k2[r][e] * gam;
-    coef[(1 * E + e) * C + r] = sm.q2[r][e] * gam;
-    coef[(2 * E + e) * C + r] = sm.k2[r][e] * exp_nonpos((float)(GC - G));
+  for (int idx = tid; idx < E * C / 4; idx += 256) {  // four consecutive positions per thread
+    const int e = idx / (C / 4), r0 = 4 * (idx % (C / 4));
+    const double GC = sm.G[C - 1][e];
+    f32x4 a, bq, c;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const double G = sm.G[r0 + j][e];
+      const float gam = exp_nonpos((float)G);
+      a[j] = sm.k2[r0 + j][e] * gam;
+      bq[j] = sm.q2[r0 + j][e] * gam;
+      c[j] = sm.k2[r0 + j][e] * exp_nonpos((float)(GC - G));
+    }
+    gstore_b128(coef + (0 * E + e) * C + r0, __builtin_bit_cast(u32x4, a));
+    gstore_b128(coef + (1 * E + e) * C + r0, __builtin_bit_cast(u32x4, bq));
+    gstore_b128(coef + (2 * E + e) * C + r0, __builtin_bit_cast(u32x4, c));
   }
   if (tid < E4) p.gC[(size_t)ch * E4 + tid] = (tid < E) ? exp_nonpos((float)sm.G[C - 1][tid]) : 0.f;
 
@@ -244,7 +283,12 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
     if (st > rt) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) sm.L[16 * rt + 4 * g + j][c] = 0.f;
-      put_m(rt, st, zero4());
+      if constexpr (Sm::LINES) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) sm.u.qk.Mb[16 * rt + 4 * g + j][c] = 0.f;
+      } else {
+        put_m(rt, st, zero4());
+      }
       continue;
     }
     f32x4 aq = zero4(), ak = zero4();
@@ -280,11 +324,53 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
       mv[j] = (c <= r) ? aq[j] * rq : 0.f;
       sm.L[r][c] = (c < r) ? sm.beta[r] * ak[j] * rk : 0.f;
     }
-    put_m(rt, st, mv);
+    if constexpr (Sm::LINES) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) sm.u.qk.Mb[16 * rt + 4 * g + j][c] = mv[j];
+    } else {
+      put_m(rt, st, mv);
+    }
   }
-  // ---- K^T (and for the backward Q^T) of the chunk (4 x 4 blocks; rows
-  // past T are zero)
-  {
+  // ---- M (and for the backward M^T), K^T (and Q^T) as whole lines
+  if constexpr (Sm::LINES) {
+    __syncthreads();  // M complete
+    for (int idx = tid; idx < C * C / 8; idx += 256) {
+      const int r = idx / (C / 8), c8 = 8 * (idx % (C / 8));
+      const float* src = &sm.u.qk.Mb[r][c8];
+      store8_split<C>(ops + OT::M + (size_t)r * C + c8, *(const f32x4*)src, *(const f32x4*)(src + 4));
+    }
+    if (p.bwd_tiles) {
+      for (int idx = tid; idx < C * C / 8; idx += 256) {
+        const int c = idx / (C / 8), r8 = 8 * (idx % (C / 8));
+        f32x4 x0, x1;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          x0[i] = sm.u.qk.Mb[r8 + i][c];
+          x1[i] = sm.u.qk.Mb[r8 + 4 + i][c];
+        }
+        store8_split<C>(ops + OT::MT + (size_t)c * C + r8, x0, x1);
+      }
+    }
+    // row R of K^T holds key key_of_row(R); column c position row_of_key(c)
+    // (the key orders of the recurrent kernels' state tiles)
+    const int nmat = p.bwd_tiles ? 2 : 1;
+    for (int idx = tid; idx < nmat * KD * C / 8; idx += 256) {
+      const int mtx = idx / (KD * C / 8), rem = idx % (KD * C / 8);
+      const int R = rem / (C / 8), c8 = 8 * (rem % (C / 8));
+      const int key = key_of_row<KD>(R);
+      uint32_t wd[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int p0 = row_of_key<C>(c8 + 2 * i), p1 = row_of_key<C>(c8 + 2 * i + 1);
+        const uint16_t v0 = mtx ? sm.u.qk.sQ[p0][key] : sm.u.qk.sK[p0][key];
+        const uint16_t v1 = mtx ? sm.u.qk.sQ[p1][key] : sm.u.qk.sK[p1][key];
+        wd[i] = (uint32_t)v0 | ((uint32_t)v1 << 16);
+      }
+      gstore_b128(ops + (mtx ? OT::Qt : OT::Kt) + (size_t)R * C + c8,
+                  u32x4{wd[0], wd[1], wd[2], wd[3]});
+    }
+  } else {  // K^T (and for the backward Q^T) of the chunk (4 x 4 blocks; rows
+            // past T are zero)
     constexpr int NB = (C / 4) * (KD / 4);
     const int nmat = p.bwd_tiles ? 2 : 1;
     for (int idx = tid; idx < nmat * NB; idx += 256) {
@@ -330,9 +416,30 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
       float* dst = p.ninv + (size_t)ch * C * C;
       for (int idx = tid; idx < C * C / 4; idx += 256) {
         const int r = idx / (C / 4), c4 = idx % (C / 4);
-        *(f32x4*)(dst + r * C + 4 * c4) = *(const f32x4*)&sm.u.inv.X[r][4 * c4];
+        gstore_b128(dst + r * C + 4 * c4, __builtin_bit_cast(u32x4, *(const f32x4*)&sm.u.inv.X[r][4 * c4]));
       }
     }
+    if constexpr (Sm::LINES) {  // Tu = X diag(beta) row-major, then (backward) transposed
+      for (int idx = tid; idx < C * C / 8; idx += 256) {
+        const int r = idx / (C / 8), c8 = 8 * (idx % (C / 8));
+        const float* src = &sm.u.inv.X[r][c8];
+        store8_split<C>(ops + OT::Tu + (size_t)r * C + c8, *(const f32x4*)src * *(const f32x4*)&sm.beta[c8],
+                     *(const f32x4*)(src + 4) * *(const f32x4*)&sm.beta[c8 + 4]);
+      }
+      if (p.bwd_tiles) {
+        for (int idx = tid; idx < C * C / 8; idx += 256) {
+          const int c = idx / (C / 8), r8 = 8 * (idx % (C / 8));
+          const float bc = sm.beta[c];
+          f32x4 x0, x1;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            x0[i] = sm.u.inv.X[r8 + i][c] * bc;
+            x1[i] = sm.u.inv.X[r8 + 4 + i][c] * bc;
+          }
+          store8_split<C>(ops + OT::TuT + (size_t)c * C + r8, x0, x1);
+        }
+      }
+    } else
     // Tu row-major and transposed, from 4 x 4 blocks of the inverse
     for (int idx = tid; idx < (C / 4) * (C / 4); idx += 256) {
       const int rb = idx / (C / 4), cb = idx % (C / 4);
