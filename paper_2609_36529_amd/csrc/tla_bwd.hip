@@ -99,6 +99,7 @@ struct RecSmem {
   alignas(16) f32x4 X[NW][NT][64];  // per-wave partials of sum_e diag(c_e) K dS'_e
   alignas(16) typename Elem<T>::frag dUs[SPLIT ? 2 : 1][NT][64];  // dU as B operands (hi, lo)
   alignas(16) f32x4 dWs[NT][64];
+  alignas(16) f32x4 dUf[NT][64];  // fp32 dU, stored to global memory at the next step
 };
 
 // Register staging of one chunk's inputs for the reverse recurrence: the
@@ -305,6 +306,15 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
   const size_t krs = (size_t)s.H * KD;
 
   const bf16x4 idf = identity_frag();  // for the transposing dS' stores
+  // row tile w of dU and dW of chunk ch (from their shared-memory copies)
+  auto store_dudw = [&](size_t chs) {
+    if (w < NT) {
+      const int rt = w;
+      store_tile16(bb.dU + chs * C * (size_t)V + (size_t)(16 * rt) * V + v0, sm.dUf[rt][l], g, n, V);
+      store_tile16(bb.dW + chs * C * (size_t)V + (size_t)(16 * rt) * V + v0,
+                   s.variant == 1 ? sm.dWs[rt][l] : zero4(), g, n, V);
+    }
+  };
   RecStage<T, KD, C, E, NTHR> stage;
   if constexpr (PREFETCH)
     if (nc > 0) stage.load(s, p, Kg, Qg, dOg, (size_t)head * s.Nc + nc - 1, nc - 1);
@@ -323,6 +333,10 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
         now.store(sm, s.variant, t0, s.T, part);
       }
     }
+    // the previous chunk's dU and dW leave now: stored where they are formed,
+    // they would precede the prefetch loads that the staging above waits for,
+    // and a wave's wait for loads also waits for its earlier stores
+    if (ci + 1 < nc) store_dudw(ch + 1);
     __syncthreads();
 
     // ---- operand copies of dS' (gradient of the chunk-end state), stored for
@@ -436,9 +450,7 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
       split_frag(acc, hi, lo);
       sm.dUs[0][rt][l] = hi;
       if constexpr (Sm::SPLIT) sm.dUs[1][rt][l] = lo;
-      // (one 16-byte store per lane: a store instruction holds up the wave
-      // for hundreds of cycles under the write traffic of all workgroups)
-      store_tile16(bb.dU + ch * C * (size_t)V + (size_t)(16 * rt) * V + v0, acc, g, n, V);
+      sm.dUf[rt][l] = acc;
     }
     __syncthreads();
     if (w < NT) {
@@ -456,7 +468,6 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
         acc = -acc;
         sm.dWs[rt][l] = acc;
       }
-      store_tile16(bb.dW + ch * C * (size_t)V + (size_t)(16 * rt) * V + v0, acc, g, n, V);
     }
     f32x4 dW[NT];
     if (s.variant == 1) {
@@ -558,6 +569,7 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
     else
       update(std::integral_constant<bool, false>{});
   }
+  if (nc > 0) store_dudw((size_t)head * s.Nc);  // chunk 0 (its copies are unchanged since)
 
   if (ds0) {
 #pragma unroll
