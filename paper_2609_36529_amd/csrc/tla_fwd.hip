@@ -1548,11 +1548,14 @@ __global__ __launch_bounds__(512) void k_fwd_dual(Shape s, FwdIn in, PrepBufs p,
         const f32x4 y = quad_transpose(oacc, n);
         const int t = t0 + 16 * rt + 4 * g + (n & 3);
         if (t < s.T && (!PK || n < 8)) {  // (PK: columns 8..15 repeat 0..7)
+          // nontemporal: the tile's rows are whole 32-byte (bf16) or
+          // 64-byte pieces that no kernel of the step reads again, and left
+          // dirty in L2 their write-back slowed the next kernel
           const size_t off = ((tok0 + t) * s.H + h) * (size_t)V + v0 + 4 * (n >> 2);
           if (s.out_bf16)
-            *(bf16x4*)((bf16_t*)out + off) = cvt_frag<bf16_t>(y);
+            gstore_b64((bf16_t*)out + off, __builtin_bit_cast(u32x2, cvt_frag<bf16_t>(y)));
           else
-            *(f32x4*)((float*)out + off) = y;
+            gstore_b128((float*)out + off, __builtin_bit_cast(u32x4, y));
         }
       } else if (train) {
 #pragma unroll
