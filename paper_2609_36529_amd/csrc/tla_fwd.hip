@@ -97,6 +97,12 @@ struct PrepSmem {
   alignas(16) float beta[C];
 };
 
+// Eight waves per chunk for E <= 8: two workgroups fit a CU (the
+// shared-memory plan), so each phase's work is split over twice the waves
+// that four would give; larger E keeps four (their registers would not fit
+// 128 per lane).
+template <int E> constexpr int prep_waves() { return E <= 8 ? 8 : 4; }
+
 // Eight consecutive values of a bf16 (hi, lo) operand tile: the high parts
 // at dst, the low parts one matrix (C x C elements) further, one 16-byte
 // nontemporal store each.
@@ -110,7 +116,9 @@ __device__ __forceinline__ void store8_split(bf16_t* dst, f32x4 x0, f32x4 x1) {
 }
 
 template <typename T, int KD, int C, int E>
-__global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
+__global__ __launch_bounds__(prep_waves<E>() * 64) void k_prep(Shape s, FwdIn in, PrepBufs p) {
+  constexpr int PREP_NW = prep_waves<E>();
+  constexpr int PREP_NTHR = PREP_NW * 64;
   constexpr int NT = C / 16;
   constexpr int E4 = (E + 3) & ~3;
   typedef PrepSmem<T, KD, C, E> Sm;
@@ -135,15 +143,15 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
   // ---- per-position vectors; Q and K rows (rows past T read clamped, then
   // zeroed).  Every global load of the phase is issued before the first of
   // their results is stored (one memory latency instead of one per array).
-  constexpr int NQE = (C * E + 255) / 256;  // q2, k2 entries per thread
-  constexpr int IT = STAGE ? (C * KD / 8 + 255) / 256 : 1;
-  constexpr int NGE = (E + 3) / 4;          // slices per wave (g)
+  constexpr int NQE = (C * E + PREP_NTHR - 1) / PREP_NTHR;  // q2, k2 entries per thread
+  constexpr int IT = STAGE ? (C * KD / 8 + PREP_NTHR - 1) / PREP_NTHR : 1;
+  constexpr int NGE = (E + PREP_NW - 1) / PREP_NW;  // slices per wave (g)
   float q2v[NQE], k2v[NQE], bv = 0.f;
   Raw8<T> qv[IT], kv[IT];
   double gv[NGE];
 #pragma unroll
   for (int i = 0; i < NQE; ++i) {
-    const int idx = min(tid + 256 * i, C * E - 1), r = idx / E, e = idx % E;
+    const int idx = min(tid + PREP_NTHR * i, C * E - 1), r = idx / E, e = idx % E;
     const size_t off = eoff + (size_t)min(t0 + r, s.T - 1) * erow + e;
     q2v[i] = ld_f((const T*)in.q2 + off);
     k2v[i] = ld_f((const T*)in.k2 + off);
@@ -155,7 +163,7 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
   if constexpr (STAGE) {
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
-      const int idx = min(tid + 256 * it, C * KD / 8 - 1);
+      const int idx = min(tid + PREP_NTHR * it, C * KD / 8 - 1);
       const int r = idx / (KD / 8), c8 = idx % (KD / 8);
       const size_t off = (size_t)min(t0 + r, s.T - 1) * krs + 8 * c8;
       qv[it] = load8(Qg + off);
@@ -164,13 +172,13 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
   }
 #pragma unroll
   for (int i = 0; i < NGE; ++i) {
-    const int e = min(w + 4 * i, E - 1);
+    const int e = min(w + PREP_NW * i, E - 1);
     gv[i] = (double)in.g[eoff + (size_t)min(t0 + l, s.T - 1) * erow + e];
   }
   // ---- the stores
 #pragma unroll
   for (int i = 0; i < NQE; ++i) {
-    const int idx = tid + 256 * i, r = idx / E, e = idx % E;
+    const int idx = tid + PREP_NTHR * i, r = idx / E, e = idx % E;
     if (idx >= C * E) continue;
     const bool ok = t0 + r < s.T;
     sm.q2[r][e] = ok ? q2v[i] : 0.f;
@@ -180,7 +188,7 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
   if constexpr (STAGE) {
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
-      const int idx = tid + 256 * it;
+      const int idx = tid + PREP_NTHR * it;
       if (idx >= C * KD / 8) continue;
       const int r = idx / (KD / 8), c8 = idx % (KD / 8);
       const bool ok = t0 + r < s.T;
@@ -193,7 +201,7 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
   // and fp32 would lose the small gates that follow it
 #pragma unroll
   for (int i = 0; i < NGE; ++i) {
-    const int e = w + 4 * i;
+    const int e = w + PREP_NW * i;
     if (e >= E) continue;  // wave-uniform
     double x = (l < C && t0 + l < s.T) ? gv[i] : 0.0;
 #pragma unroll
@@ -207,7 +215,7 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
 
   // ---- coefficient vectors a = k2 gamma, b = q2 gamma, c = k2 gamma^C / gamma; gamma^C
   float* coef = p.coef + (size_t)ch * 3 * E * C;
-  for (int idx = tid; idx < E * C / 4; idx += 256) {  // four consecutive positions per thread
+  for (int idx = tid; idx < E * C / 4; idx += PREP_NTHR) {  // four consecutive positions per thread
     const int e = idx / (C / 4), r0 = 4 * (idx % (C / 4));
     const double GC = sm.G[C - 1][e];
     f32x4 a, bq, c;
@@ -265,7 +273,7 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
         put4<T>(ops + OT::MT + pt * OT::MAT + (size_t)(16 * st + n) * C + 16 * rt + 4 * g, parts[pt]);
     }
   };
-  for (int tile = w; tile < NT * NT; tile += 4) {
+  for (int tile = w; tile < NT * NT; tile += PREP_NW) {
     constexpr int NL = NT * (NT + 1) / 2;  // lower tiles first, then the upper ones
     int rt = 0, st = 0;
     if (tile < NL) {
@@ -334,13 +342,13 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
   // ---- M (and for the backward M^T), K^T (and Q^T) as whole lines
   if constexpr (Sm::LINES) {
     __syncthreads();  // M complete
-    for (int idx = tid; idx < C * C / 8; idx += 256) {
+    for (int idx = tid; idx < C * C / 8; idx += PREP_NTHR) {
       const int r = idx / (C / 8), c8 = 8 * (idx % (C / 8));
       const float* src = &sm.u.qk.Mb[r][c8];
       store8_split<C>(ops + OT::M + (size_t)r * C + c8, *(const f32x4*)src, *(const f32x4*)(src + 4));
     }
     if (p.bwd_tiles) {
-      for (int idx = tid; idx < C * C / 8; idx += 256) {
+      for (int idx = tid; idx < C * C / 8; idx += PREP_NTHR) {
         const int c = idx / (C / 8), r8 = 8 * (idx % (C / 8));
         f32x4 x0, x1;
 #pragma unroll
@@ -354,7 +362,7 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
     // row R of K^T holds key key_of_row(R); column c position row_of_key(c)
     // (the key orders of the recurrent kernels' state tiles)
     const int nmat = p.bwd_tiles ? 2 : 1;
-    for (int idx = tid; idx < nmat * KD * C / 8; idx += 256) {
+    for (int idx = tid; idx < nmat * KD * C / 8; idx += PREP_NTHR) {
       const int mtx = idx / (KD * C / 8), rem = idx % (KD * C / 8);
       const int R = rem / (C / 8), c8 = 8 * (rem % (C / 8));
       const int key = key_of_row<KD>(R);
@@ -373,7 +381,7 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
             // past T are zero)
     constexpr int NB = (C / 4) * (KD / 4);
     const int nmat = p.bwd_tiles ? 2 : 1;
-    for (int idx = tid; idx < nmat * NB; idx += 256) {
+    for (int idx = tid; idx < nmat * NB; idx += PREP_NTHR) {
       const int mtx = idx / NB, bi = idx % NB;
       const int rb = bi / (KD / 4), kb = bi % (KD / 4);
       float x[4][4];
@@ -410,24 +418,24 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
 
   // ---- Tu = (I + L)^{-1} diag(beta) (GDN), blocked unit-lower inverse in fp32
   if (s.variant == 1) {
-    unit_lower_inverse<C, 256>([&](int r, int c) { return sm.L[r][c]; }, &sm.u.inv.X[0][0],
+    unit_lower_inverse<C, PREP_NTHR>([&](int r, int c) { return sm.L[r][c]; }, &sm.u.inv.X[0][0],
                                Sm::CP, &sm.u.inv.Y[0][0][0]);
     if (p.ninv) {  // kept in fp32 for the backward of the solve
       float* dst = p.ninv + (size_t)ch * C * C;
-      for (int idx = tid; idx < C * C / 4; idx += 256) {
+      for (int idx = tid; idx < C * C / 4; idx += PREP_NTHR) {
         const int r = idx / (C / 4), c4 = idx % (C / 4);
         gstore_b128(dst + r * C + 4 * c4, __builtin_bit_cast(u32x4, *(const f32x4*)&sm.u.inv.X[r][4 * c4]));
       }
     }
     if constexpr (Sm::LINES) {  // Tu = X diag(beta) row-major, then (backward) transposed
-      for (int idx = tid; idx < C * C / 8; idx += 256) {
+      for (int idx = tid; idx < C * C / 8; idx += PREP_NTHR) {
         const int r = idx / (C / 8), c8 = 8 * (idx % (C / 8));
         const float* src = &sm.u.inv.X[r][c8];
         store8_split<C>(ops + OT::Tu + (size_t)r * C + c8, *(const f32x4*)src * *(const f32x4*)&sm.beta[c8],
                      *(const f32x4*)(src + 4) * *(const f32x4*)&sm.beta[c8 + 4]);
       }
       if (p.bwd_tiles) {
-        for (int idx = tid; idx < C * C / 8; idx += 256) {
+        for (int idx = tid; idx < C * C / 8; idx += PREP_NTHR) {
           const int c = idx / (C / 8), r8 = 8 * (idx % (C / 8));
           const float bc = sm.beta[c];
           f32x4 x0, x1;
@@ -441,7 +449,7 @@ __global__ __launch_bounds__(256) void k_prep(Shape s, FwdIn in, PrepBufs p) {
       }
     } else
     // Tu row-major and transposed, from 4 x 4 blocks of the inverse
-    for (int idx = tid; idx < (C / 4) * (C / 4); idx += 256) {
+    for (int idx = tid; idx < (C / 4) * (C / 4); idx += PREP_NTHR) {
       const int rb = idx / (C / 4), cb = idx % (C / 4);
       const f32x4 bc = *(const f32x4*)&sm.beta[4 * cb];
       f32x4 x[4];
@@ -1579,7 +1587,8 @@ static hipError_t prep_inst(const Shape& s, const FwdIn& in, const PrepBufs& p, 
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     attr_set = true;
   }
-  hipLaunchKernelGGL((k_prep<T, KD, C, E>), dim3(s.NH * s.Nc), dim3(256), smem, st, s, in, p);
+  hipLaunchKernelGGL((k_prep<T, KD, C, E>), dim3(s.NH * s.Nc), dim3(prep_waves<E>() * 64), smem, st,
+                     s, in, p);
   return hipGetLastError();
 }
 
