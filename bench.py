@@ -478,6 +478,59 @@ def conv_bench(steps, warmup):
           flush=True)
 
 
+def proj_bench(steps, warmup):
+    """The mixer's input projection with its epilogue fused (section "Input
+    projections", Alg. 2) at d_model 2048 (the 1.3B block) for this bench's
+    8 heads, B4 T4096 K=V=128 E=8 W4: forward tla_proj_in_fwd (GEMM u Wp^T
+    into the convolution, activations and norms, keeping y for the backward)
+    and backward tla_proj_in_bwd (input-side backward, transposes, the du and
+    dWp GEMMs).  MFMA-bound; algorithmic FLOP: forward 2 n Ctot Dm (the
+    16-row halo that each 256-token tile recomputes is not counted),
+    backward twice that."""
+    import torch
+    import paper_2609_36529_amd as tla
+    B, T, Dm, H, K, V, E, W = 4, 4096, 2048, 8, 128, 128, 8, 4
+    C = H * (2 * K + V + 2 * E)
+    gen = torch.Generator().manual_seed(29)
+    u = torch.randn(B, T, Dm, generator=gen).to(torch.bfloat16).cuda()
+    Wp = (torch.randn(C, Dm, generator=gen) / Dm ** 0.5).to(torch.bfloat16).cuda()
+    w = ((torch.rand(W, C, generator=gen) * 2 - 1) / W ** 0.5).float().cuda()
+    grads = tuple(torch.randn(B, T, H, d, generator=gen).to(torch.bfloat16).cuda() for d in (K, K, V, E, E))
+
+    def one():
+        outs = tla.proj_in_fwd(u, Wp, w, H, K, V, E, keep_y=True)
+        tla.proj_in_bwd(u, Wp, w, outs[5], H, K, V, E, grads)
+    for _ in range(warmup):
+        one()
+    torch.cuda.synchronize()
+    tla.prof_enable(True)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        one()
+    torch.cuda.synchronize()
+    elapsed = (time.perf_counter() - t0) / steps
+    prof = tla.prof_read()
+    tla.prof_enable(False)
+    kern = {k: round(v[0] / v[1], 4) for k, v in prof.items() if v[1]}
+    n = B * T
+    flop_fwd = 2.0 * n * C * Dm
+    tf_f = flop_fwd / (kern["proj_in_fwd"] * 1e-3) / 1e12
+    tf_g = 2 * flop_fwd / (kern["proj_gemm"] * 1e-3) / 1e12
+    print(json.dumps({
+        "metric": "input projection fwd+bwd tokens/s, B4 T4096 d_model 2048 H8 K=V=128 E=8 W4",
+        "value": round(n / elapsed, 1), "unit": "tokens/s", "n_gpus": 1, "steps": steps,
+        "warmup": warmup, "ms_per_step": round(1e3 * elapsed, 4), "higher_is_better": True,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "projection GEMM with fused conv + SiLU/softplus + L2 norm, forward and backward",
+                   "tokens": n, "d_model": Dm, "channels": C, "taps": W},
+        "kernels_ms": kern,
+        "roofline": {"bound": "mfma", "achieved": round(tf_f, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(tf_f / PEAK_BF16_TFLOPS, 4), "kernel": "proj_in_fwd",
+                     "backward_gemm_tflops": round(tf_g, 1),
+                     "backward_gemm_frac": round(tf_g / PEAK_BF16_TFLOPS, 4)}}),
+          flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -496,6 +549,8 @@ def main():
                     help="time the gate heads (forget gate, write strength) forward and backward")
     ap.add_argument("--conv", action="store_true",
                     help="time the input side (short convolution, activations, L2 norm) forward and backward")
+    ap.add_argument("--proj", action="store_true",
+                    help="time the fused input projection (GEMM + input side) forward and backward")
     ap.add_argument("--forward", metavar="NAME",
                     help="time the inference forward of sgla_bf16, gdn_bf16 or gdn_long_bf16")
     args = ap.parse_args()
@@ -521,6 +576,9 @@ def main():
         return
     if args.conv:
         conv_bench(args.steps, args.warmup)
+        return
+    if args.proj:
+        proj_bench(args.steps, args.warmup)
         return
     if args.forward:
         forward_bench(args.forward, args.steps, args.warmup)

@@ -310,16 +310,56 @@ int tla_conv_in_bwd(int dtype, int B, int T, int H, int K, int V, int E, int W, 
                     size_t workspace_bytes, void* stream);
 
 /*
+ * The mixer's input projection with the input side fused into it (section
+ * "Input projections", Alg. 2): one GEMM y = u Wp^T over d_model yields the
+ * channels of q, k, v, q' and k' of every head, and the same kernel applies
+ * tla_conv_in_fwd's convolution, activations and normalisations to them, so
+ * y need not be stored.  All operands are bf16 (fp32 accumulation).
+ *   u   [B][T][Dm]: the block's normalised input;
+ *   Wp  [Ctot][Dm]: row c is the projection of channel c, Ctot = H (2K + V +
+ *       2E), channels in tla_conv_in_fwd's order (blocks q | k | v | q' | k',
+ *       each head-major);
+ *   w   [W][Ctot] fp32 taps, as in tla_conv_in_fwd;
+ *   q, k [B][T][H][K]; v [B][T][H][V]; q2, k2 [B][T][H][E] (outputs);
+ *   y   [B][T][Ctot]: the projection itself rounded to bf16, written only if
+ *       y is not NULL (a training forward keeps it for tla_proj_in_bwd).
+ * Dm a multiple of 8 from 8 to 65536; K and E each one of 8, 16, 32, 64,
+ * 128; V a multiple of 8 up to 1024; W 1 to 4; H (2K + V) / 8 a multiple of
+ * E / 8 (TLA_E_UNSUPPORTED otherwise); B, T >= 0, 1 <= H <= 1024, eps >= 0
+ * finite.  Device pointers, 16-byte aligned, outputs overlapping neither each
+ * other nor an input; arrays of zero size may be NULL.  Asynchronous on
+ * `stream`.
+ *
+ * tla_proj_in_bwd: given dq, dk, dv, dq2, dk2 and the forward's y, writes
+ * du = dL/du [B][T][Dm] (bf16), dWp = dL/dWp [Ctot][Dm] (fp32) and the tap
+ * gradient dw [W][Ctot] (fp32): dy by tla_conv_in_bwd's kernels, then
+ * du = dy Wp and dWp = dy^T u as GEMMs on the matrix cores, every sum over
+ * tokens in a fixed order (bitwise reproducible).  It needs a device
+ * workspace of tla_proj_in_workspace_bytes(...) bytes (dy, transposed
+ * operands and partial sums; TLA_E_WORKSPACE if smaller), owned by the
+ * caller, free again when the call's work on `stream` is done.
+ */
+int tla_proj_in_fwd(int B, int T, int Dm, int H, int K, int V, int E, int W, float eps,
+                    const void* u, const void* Wp, const float* w, void* q, void* k, void* v,
+                    void* q2, void* k2, void* y, void* stream);
+size_t tla_proj_in_workspace_bytes(int B, int T, int Dm, int H, int K, int V, int E, int W);
+int tla_proj_in_bwd(int B, int T, int Dm, int H, int K, int V, int E, int W, float eps,
+                    const void* u, const void* Wp, const float* w, const void* y, const void* dq,
+                    const void* dk, const void* dv, const void* dq2, const void* dk2, void* du,
+                    float* dWp, float* dw, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * Per-kernel timing, for diagnostics and benchmarks (not needed otherwise).
  * tla_prof_enable(1) clears previous records and starts bracketing every
  * kernel launch of the library with a pair of HIP events on the launch
  * stream (events are created once and pooled); tla_prof_enable(0) stops and
  * clears.  tla_prof_read() waits for the recorded events and fills, for each
- * of the 13 kernel kinds named by tla_prof_name(0..12) ("prep",
+ * of the 16 kernel kinds named by tla_prof_name(0..15) ("prep",
  * "fwd_recurrent", "bwd_recurrent", "bwd_state", "bwd_chunk", "step",
  * "out_gate_fwd", "out_gate_bwd", "out_gate_dw", "gate_heads_fwd",
- * "gate_heads_bwd", "conv_in_fwd", "conv_in_bwd"), the summed event time in
- * milliseconds and the number of launches; n must be at least 13.  Not meant
+ * "gate_heads_bwd", "conv_in_fwd", "conv_in_bwd", "proj_in_fwd",
+ * "proj_gemm", "transpose"), the summed event time in milliseconds and the
+ * number of launches; n must be at least 16.  Not meant
  * for use while another thread launches.
  */
 int tla_prof_enable(int on);

@@ -34,7 +34,7 @@ class TLAError(RuntimeError):
     pass
 
 
-PROF_SLOTS = 13  # kernel kinds of tla_prof_read
+PROF_SLOTS = 16  # kernel kinds of tla_prof_read
 
 
 def lib():
@@ -89,6 +89,12 @@ def lib():
     L.tla_conv_in_workspace_bytes.restype = S
     L.tla_conv_in_bwd.argtypes = [I] * 8 + [ctypes.c_float] + [P] * 10 + [S, P]
     L.tla_conv_in_bwd.restype = I
+    L.tla_proj_in_fwd.argtypes = [I] * 8 + [ctypes.c_float] + [P] * 10
+    L.tla_proj_in_fwd.restype = I
+    L.tla_proj_in_workspace_bytes.argtypes = [I] * 8
+    L.tla_proj_in_workspace_bytes.restype = S
+    L.tla_proj_in_bwd.argtypes = [I] * 8 + [ctypes.c_float] + [P] * 13 + [S, P]
+    L.tla_proj_in_bwd.restype = I
     L.tla_prof_enable.argtypes = [I]
     L.tla_prof_enable.restype = I
     L.tla_prof_read.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I), I]
@@ -524,6 +530,59 @@ def conv_in_bwd(y, w, H, K, V, E, grads, eps=1e-6):
                              *[_ptr(g) for g in grads], _ptr(dy), _ptr(dw), _ptr(ws), ws.numel(),
                              _stream(dev)))
     return dy, dw
+
+
+def _proj_shape(u, Wp, w, H, K, V, E):
+    _need(u, "u", torch.bfloat16)
+    dev = u.device
+    _need(Wp, "Wp", torch.bfloat16, dev)
+    _need(w, "w", torch.float32, dev)
+    C = H * (2 * K + V + 2 * E)
+    if u.dim() != 3 or Wp.dim() != 2 or tuple(Wp.shape) != (C, u.shape[-1]):
+        raise ValueError("u must be [B, T, Dm] and Wp [H (2K + V + 2E), Dm]")
+    if w.dim() != 2 or w.shape[1] != C:
+        raise ValueError("w must be [W, Ctot]")
+    return u.shape[0], u.shape[1], u.shape[2], w.shape[0], C, dev
+
+
+def proj_in_fwd(u, Wp, w, H, K, V, E, eps=1e-6, keep_y=False):
+    """The mixer's input projection with the input side fused (section
+    "Input projections", Alg. 2): y = u Wp^T for every channel of q, k, v,
+    q', k', then the causal convolution with taps w [W, Ctot], SiLU /
+    softplus and the L2 normalisations, in one kernel (bf16 operands).
+    Returns (q, k, v, q2, k2, y); y [B, T, Ctot] (bf16) only with keep_y,
+    else None.  Runs tla_proj_in_fwd."""
+    B, T, Dm, W, C, dev = _proj_shape(u, Wp, w, H, K, V, E)
+    outs = [torch.empty((B, T, H, d), dtype=torch.bfloat16, device=dev) for d in (K, K, V, E, E)]
+    y = torch.empty((B, T, C), dtype=torch.bfloat16, device=dev) if keep_y else None
+    _check(lib().tla_proj_in_fwd(B, T, Dm, H, K, V, E, W, float(eps), _ptr(u), _ptr(Wp), _ptr(w),
+                                 *[_ptr(o) for o in outs], _ptr(y), _stream(dev)))
+    return (*outs, y)
+
+
+def proj_in_bwd(u, Wp, w, y, H, K, V, E, grads, eps=1e-6):
+    """Gradients (du, dWp, dw) of the fused input projection for the
+    outputs' gradients grads = (dq, dk, dv, dq2, dk2), given the forward's y
+    (proj_in_fwd with keep_y); du is bf16, dWp and dw fp32, every sum over
+    tokens in a fixed order.  Runs tla_proj_in_bwd."""
+    B, T, Dm, W, C, dev = _proj_shape(u, Wp, w, H, K, V, E)
+    _need(y, "y", torch.bfloat16, dev)
+    if tuple(y.shape) != (B, T, C):
+        raise ValueError("y must be [B, T, Ctot]")
+    for gr, d, nm in zip(grads, (K, K, V, E, E), ("dq", "dk", "dv", "dq2", "dk2")):
+        _need(gr, nm, torch.bfloat16, dev)
+        if tuple(gr.shape) != (B, T, H, d):
+            raise ValueError(f"{nm} must be [B, T, H, {d}]")
+    du = torch.empty_like(u)
+    dWp = torch.empty(Wp.shape, dtype=torch.float32, device=dev)
+    dw = torch.empty_like(w)
+    L = lib()
+    ws = torch.empty(max(L.tla_proj_in_workspace_bytes(B, T, Dm, H, K, V, E, W), 256),
+                     dtype=torch.uint8, device=dev)
+    _check(L.tla_proj_in_bwd(B, T, Dm, H, K, V, E, W, float(eps), _ptr(u), _ptr(Wp), _ptr(w), _ptr(y),
+                             *[_ptr(g) for g in grads], _ptr(du), _ptr(dWp), _ptr(dw), _ptr(ws),
+                             ws.numel(), _stream(dev)))
+    return du, dWp, dw
 
 
 def prof_enable(on=True):

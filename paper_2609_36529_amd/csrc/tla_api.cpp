@@ -191,12 +191,12 @@ int device_fail(hipError_t e, const char* what) {
 // pooled and reused; nothing is recorded when timing is off.
 enum { PROF_PREP, PROF_FWD, PROF_BWD_REC, PROF_BWD_STATE, PROF_BWD_CHUNK, PROF_STEP,
        PROF_GATE_FWD, PROF_GATE_BWD, PROF_GATE_DW, PROF_HEADS_FWD, PROF_HEADS_BWD,
-       PROF_CONV_FWD, PROF_CONV_BWD, PROF_N };
+       PROF_CONV_FWD, PROF_CONV_BWD, PROF_PROJ_FWD, PROF_GEMM, PROF_TRANSPOSE, PROF_N };
 const char* const kProfNames[PROF_N] = {"prep",         "fwd_recurrent",  "bwd_recurrent",
                                         "bwd_state",    "bwd_chunk",      "step",
                                         "out_gate_fwd", "out_gate_bwd",   "out_gate_dw",
                                         "gate_heads_fwd", "gate_heads_bwd", "conv_in_fwd",
-                                        "conv_in_bwd"};
+                                        "conv_in_bwd", "proj_in_fwd", "proj_gemm", "transpose"};
 struct ProfRec {
   int kind;
   hipEvent_t a, b;
@@ -752,6 +752,133 @@ int tla_conv_in_bwd(int dtype, int B, int T, int H, int K, int V, int E, int W, 
     return tla::launch_conv_bwd(dtype == TLA_BF16, a, y, w, dout, dy, dw, (float*)workspace, st);
   });
   if (e != hipSuccess) return device_fail(e, "input-side convolution backward kernel");
+  return TLA_OK;
+}
+
+// ------------------------------------------------ input projection (fused)
+static int proj_check(int B, int T, int Dm, int H, int K, int V, int E, int W, float eps) {
+  int rc = conv_check(TLA_BF16, B, T, H, K, V, E, W, eps);
+  if (rc) return rc;
+  if (K > 128 || E > 128)
+    return fail(TLA_E_UNSUPPORTED, "K = %d, E = %d (each at most 128: a channel tile holds whole heads)", K, E);
+  if (Dm < 8 || Dm > 65536 || Dm % 8)
+    return fail(TLA_E_UNSUPPORTED, "Dm = %d (a multiple of 8 from 8 to 65536)", Dm);
+  // row offsets within a tile are 32-bit: 256 rows of the longest contraction
+  if ((double)B * T > 8.0e6) return fail(TLA_E_SHAPE, "B T = %.0f tokens (at most 8e6)", (double)B * T);
+  return TLA_OK;
+}
+
+int tla_proj_in_fwd(int B, int T, int Dm, int H, int K, int V, int E, int W, float eps,
+                    const void* u, const void* Wp, const float* w, void* q, void* k, void* v,
+                    void* q2, void* k2, void* y, void* stream) {
+  g_err[0] = 0;
+  int rc = proj_check(B, T, Dm, H, K, V, E, W, eps);
+  if (rc) return rc;
+  const size_t n = (size_t)B * T, C = (size_t)H * (2 * K + V + 2 * E);
+  if (!w || !Wp || (n > 0 && (!u || !q || !k || !v || !q2 || !k2)))
+    return fail(TLA_E_NULL, "u, Wp, w, q, k, v, q2 and k2 are required");
+  const void* ptrs[] = {u, Wp, w, q, k, v, q2, k2, y};
+  for (const void* p : ptrs)
+    if (misaligned(p)) return fail(TLA_E_ALIGN, "pointer %p is not 16-byte aligned", p);
+  const Range ins[] = {{u, n * Dm * 2}, {Wp, C * Dm * 2}, {w, (size_t)W * C * 4}};
+  const Range outs[] = {{q, n * H * K * 2}, {k, n * H * K * 2}, {v, n * H * V * 2},
+                        {q2, n * H * E * 2}, {k2, n * H * E * 2}, {y, y ? n * C * 2 : 0}};
+  for (const Range& a : outs)
+    for (const Range& b : ins)
+      if (overlap(a, b)) return fail(TLA_E_ALIAS, "an output overlaps an input");
+  for (int i = 0; i < 6; ++i)
+    for (int j = i + 1; j < 6; ++j)
+      if (overlap(outs[i], outs[j])) return fail(TLA_E_ALIAS, "two outputs overlap");
+  if (n == 0) return TLA_OK;
+  const tla::ProjArgs a = tla::proj_args(B, T, Dm, H, K, V, E, W, eps);
+  void* const out[5] = {q, k, v, q2, k2};
+  hipStream_t st = (hipStream_t)stream;
+  hipError_t e = timed(PROF_PROJ_FWD, st, [&] { return tla::launch_proj_in(a, u, Wp, w, out, y, st); });
+  if (e != hipSuccess) return device_fail(e, "input projection kernel");
+  return TLA_OK;
+}
+
+// Workspace of the backward: dy [n][C], dy^T [C][n8], u^T [Dm][n8], Wp^T
+// [Dm][C] (bf16; n8 = n rounded up to 8, the padding zero), the partial sums
+// of the dWp GEMM's splits, and the convolution backward's partials.
+struct ProjWs {
+  size_t dy, dyT, uT, WpT, part, conv, end;
+  int splits;
+};
+static ProjWs proj_ws(int B, int T, int Dm, int H, int K, int V, int E, int W) {
+  ProjWs L;
+  const size_t n = (size_t)B * T, n8 = (n + 7) / 8 * 8, C = (size_t)H * (2 * K + V + 2 * E);
+  L.splits = tla::gemm_splits((long long)C, Dm, (long long)n8);
+  size_t o = 0;
+  L.dy = o;   o += align256(n * C * 2);
+  L.dyT = o;  o += align256(C * n8 * 2);
+  L.uT = o;   o += align256((size_t)Dm * n8 * 2);
+  L.WpT = o;  o += align256((size_t)Dm * C * 2);
+  L.part = o; o += L.splits > 1 ? align256((size_t)L.splits * C * Dm * 4) : 0;
+  L.conv = o; o += tla_conv_in_workspace_bytes(B, T, H, K, V, E, W);
+  L.end = o;
+  return L;
+}
+
+size_t tla_proj_in_workspace_bytes(int B, int T, int Dm, int H, int K, int V, int E, int W) {
+  if (B < 0 || T < 0 || Dm < 1 || H < 1 || K < 1 || V < 1 || E < 1 || W < 1 || W > 4) return 0;
+  return proj_ws(B, T, Dm, H, K, V, E, W).end;
+}
+
+int tla_proj_in_bwd(int B, int T, int Dm, int H, int K, int V, int E, int W, float eps,
+                    const void* u, const void* Wp, const float* w, const void* y, const void* dq,
+                    const void* dk, const void* dv, const void* dq2, const void* dk2, void* du,
+                    float* dWp, float* dw, void* workspace, size_t workspace_bytes, void* stream) {
+  g_err[0] = 0;
+  int rc = proj_check(B, T, Dm, H, K, V, E, W, eps);
+  if (rc) return rc;
+  const size_t n = (size_t)B * T, n8 = (n + 7) / 8 * 8, C = (size_t)H * (2 * K + V + 2 * E);
+  if (!Wp || !w || !dWp || !dw || (n > 0 && (!u || !y || !dq || !dk || !dv || !dq2 || !dk2 || !du)))
+    return fail(TLA_E_NULL, "u, Wp, w, y, dq, dk, dv, dq2, dk2, du, dWp and dw are required");
+  const void* ptrs[] = {u, Wp, w, y, dq, dk, dv, dq2, dk2, du, dWp, dw, workspace};
+  for (const void* p : ptrs)
+    if (misaligned(p)) return fail(TLA_E_ALIGN, "pointer %p is not 16-byte aligned", p);
+  const ProjWs L = proj_ws(B, T, Dm, H, K, V, E, W);
+  if (!workspace || workspace_bytes < L.end)
+    return fail(TLA_E_WORKSPACE, "workspace of %zu bytes needed", L.end);
+  const Range ins[] = {{u, n * Dm * 2},      {Wp, C * Dm * 2},     {w, (size_t)W * C * 4},
+                       {y, n * C * 2},       {dq, n * H * K * 2},  {dk, n * H * K * 2},
+                       {dv, n * H * V * 2},  {dq2, n * H * E * 2}, {dk2, n * H * E * 2}};
+  const Range outs[] = {{du, n * Dm * 2}, {dWp, C * Dm * 4}, {dw, (size_t)W * C * 4},
+                        {workspace, L.end}};
+  for (const Range& a : outs)
+    for (const Range& b : ins)
+      if (overlap(a, b)) return fail(TLA_E_ALIAS, "an output or the workspace overlaps an input");
+  for (int i = 0; i < 4; ++i)
+    for (int j = i + 1; j < 4; ++j)
+      if (overlap(outs[i], outs[j])) return fail(TLA_E_ALIAS, "two outputs overlap");
+  char* ws = (char*)workspace;
+  hipStream_t st = (hipStream_t)stream;
+  const tla::ConvArgs ca = tla::conv_args(B, T, H, K, V, E, W, eps, true);
+  const void* const dout[5] = {dq, dk, dv, dq2, dk2};
+  void* dy = ws + L.dy;
+  hipError_t e = timed(PROF_CONV_BWD, st, [&] {
+    return tla::launch_conv_bwd(true, ca, y, w, dout, dy, dw, (float*)(ws + L.conv), st);
+  });
+  if (e != hipSuccess) return device_fail(e, "input-side convolution backward kernel");
+  e = timed(PROF_TRANSPOSE, st, [&] {
+    hipError_t r = tla::launch_transpose((long long)C, Dm, (long long)C, Wp, ws + L.WpT, st);
+    if (r == hipSuccess) r = tla::launch_transpose((long long)n, (long long)C, (long long)n8, dy, ws + L.dyT, st);
+    if (r == hipSuccess) r = tla::launch_transpose((long long)n, Dm, (long long)n8, u, ws + L.uT, st);
+    return r;
+  });
+  if (e != hipSuccess) return device_fail(e, "transpose kernel");
+  e = timed(PROF_GEMM, st, [&] {
+    // du [n][Dm] = dy [n][C] (Wp^T [Dm][C])^T
+    hipError_t r = tla::launch_gemm_nt((long long)n, Dm, (long long)C, dy, ws + L.WpT, du, true, Dm,
+                                       1, nullptr, st);
+    // dWp [C][Dm] = dy^T [C][n8] (u^T [Dm][n8])^T
+    if (r == hipSuccess)
+      r = tla::launch_gemm_nt((long long)C, Dm, (long long)n8, ws + L.dyT, ws + L.uT, dWp, false, Dm,
+                              L.splits, (float*)(ws + L.part), st);
+    return r;
+  });
+  if (e != hipSuccess) return device_fail(e, "projection gradient GEMM");
   return TLA_OK;
 }
 

@@ -24,87 +24,13 @@
 #include <hip/hip_runtime.h>
 
 #include "tla_common.hpp"
+#include "tla_input_side.hpp"
 #include "tla_internal.hpp"
 
 namespace tla {
 
 constexpr int CONV_NTHR = 256;  // four waves, one run of tokens each
 constexpr int CONV_U = 2;       // forward: tokens per load batch (two batches in flight)
-
-// The destination of a lane's eight channels: kind (0 q, 1 k, 2 v, 3 q', 4 k'),
-// offset within that kind's [H][width] row, width, and the lanes of its norm
-// group (0: not normalised).
-struct ConvLane {
-  int kind, off, width, lpr;
-};
-
-__device__ __forceinline__ ConvLane conv_lane(const ConvArgs& a, int c) {
-  const int e0 = a.H * a.K, e1 = 2 * e0, e2 = e1 + a.H * a.V, e3 = e2 + a.H * a.E;
-  if (c < e0) return {0, c, a.K, a.K / 8};
-  if (c < e1) return {1, c - e0, a.K, a.K / 8};
-  if (c < e2) return {2, c - e1, a.V, 0};
-  if (c < e3) return {3, c - e2, a.E, a.E / 8};
-  return {4, c - e3, a.E, a.E / 8};
-}
-
-// sum over the lpr aligned lanes of the caller's group (lpr a power of two
-// dividing 64; every lane of the wave takes part in every exchange)
-__device__ __forceinline__ float lane_group_sum(float x, int lpr) {
-#pragma unroll
-  for (int m = 1; m < 64; m <<= 1) {
-    const float y = __shfl_xor(x, m, 64);
-    if (m < lpr) x += y;
-  }
-  return x;
-}
-
-template <typename P>
-__device__ __forceinline__ P pick(int kind, P p0, P p1, P p2, P p3, P p4) {
-  return kind == 0 ? p0 : kind == 1 ? p1 : kind == 2 ? p2 : kind == 3 ? p3 : p4;
-}
-
-__device__ __forceinline__ float sig_rcp(float z) { return __builtin_amdgcn_rcpf(1.f + __expf(-z)); }
-
-// softplus(y) = max(y, 0) + log1p(e), e = exp(-|y|) in (0, 1], with log1p by
-// the compensated form log(u) e / (u - 1), u = 1 + e rounded (exact where
-// u = 1): a few ulps, far cheaper than a general log1p.
-__device__ __forceinline__ float softplus_c(float y) {
-  const float e = __expf(-fabsf(y));
-  const float u = 1.f + e;
-  const float l = u == 1.f ? e : logf(u) * (e * __builtin_amdgcn_rcpf(u - 1.f));
-  return fmaxf(y, 0.f) + l;
-}
-
-// Activation of a lane's eight channels (SiLU for kinds q, k, v, softplus for
-// q', k'), and with it the slope.  The choice is made once per lane, so a wave
-// runs only its own branch (waves mix the two only where the v and q' blocks
-// meet).  SiLU' = s (1 + z (1 - s)), s = sigmoid(z); softplus' = sigmoid.
-__device__ __forceinline__ void act8(bool silu, const float (&z)[8], float (&r)[8]) {
-  if (silu) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) r[i] = z[i] * sig_rcp(z[i]);
-  } else {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) r[i] = softplus_c(z[i]);
-  }
-}
-__device__ __forceinline__ void act8_slope(bool silu, const float (&z)[8], float (&r)[8],
-                                           float (&d)[8]) {
-  if (silu) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const float sg = sig_rcp(z[i]);
-      r[i] = z[i] * sg;
-      d[i] = sg * (1.f + z[i] * (1.f - sg));
-    }
-  } else {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      r[i] = softplus_c(z[i]);
-      d[i] = sig_rcp(z[i]);
-    }
-  }
-}
 
 // Eight values of one token as loaded (packed bf16, or fp32), converted only
 // where used: loads are unconditional from clamped addresses, so a batch of
@@ -142,28 +68,6 @@ __device__ __forceinline__ void load_tokens(const T* p, size_t stride, int t, in
                                             Tok8<T> (&x)[N]) {
 #pragma unroll
   for (int u = 0; u < N; ++u) x[u].ld(p + (size_t)min(t + u, end - 1) * stride);
-}
-
-// conv output of one token: taps over the history (hist[h] = y[t - 1 - h]) and y[t]
-template <int W>
-__device__ __forceinline__ void conv8(const float (&wt)[W][8], const float (&hist)[W > 1 ? W - 1 : 1][8],
-                                      const float (&x)[8], float (&z)[8]) {
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    z[i] = wt[W - 1][i] * x[i];
-#pragma unroll
-    for (int h = 0; h < W - 1; ++h) z[i] += wt[W - 2 - h][i] * hist[h][i];
-  }
-}
-template <int W>
-__device__ __forceinline__ void push_hist(float (&hist)[W > 1 ? W - 1 : 1][8], const float (&x)[8]) {
-#pragma unroll
-  for (int h = W - 2; h > 0; --h)
-#pragma unroll
-    for (int i = 0; i < 8; ++i) hist[h][i] = hist[h - 1][i];
-  if (W > 1)
-#pragma unroll
-    for (int i = 0; i < 8; ++i) hist[0][i] = x[i];
 }
 
 // taps of the lane's channels and the W - 1 inputs before token t0 (zero

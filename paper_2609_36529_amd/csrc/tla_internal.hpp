@@ -152,6 +152,30 @@ hipError_t launch_conv_bwd(bool bf16, const ConvArgs& a, const void* y, const fl
                            const void* const* dout, void* dy, float* dw, float* part,
                            hipStream_t st);
 
+// The input projection with its epilogue fused (GEMM u Wp^T, then the
+// input side above), and the plain GEMMs and transposes of its backward.
+struct ProjArgs {
+  int B, T, Dm, H, K, V, E, W;
+  int Ctot;            // H (2K + V + 2E) channels per token
+  int tiles_per_row;   // token tiles per batch row, ceil(T / 256)
+  int n_mt, n_ct;      // token tiles (B tiles_per_row) and channel tiles (ceil(Ctot / 128))
+  float eps;
+};
+ProjArgs proj_args(int B, int T, int Dm, int H, int K, int V, int E, int W, float eps);
+hipError_t launch_proj_in(const ProjArgs& a, const void* u, const void* Wp, const float* w,
+                          void* const* out, void* y, hipStream_t st);
+// C[M][N] = A[M][K] B[N][K]^T (bf16 operands, rows K elements apart, K a
+// multiple of 8); C fp32 or bf16 with rows ldc apart.  With splits > 1 the
+// contraction is cut into that many ranges whose fp32 partial products go to
+// part ([splits][M][N]) and are then summed in split order into C.
+int gemm_splits(long long M, long long N, long long K);
+hipError_t launch_gemm_nt(long long M, long long N, long long K, const void* A, const void* Bm,
+                          void* C, bool c_bf16, long long ldc, int splits, float* part,
+                          hipStream_t st);
+// out [C][Rp] = in [R][C]^T (bf16), rows R .. Rp - 1 of the result zero
+hipError_t launch_transpose(long long R, long long C, long long Rp, const void* in, void* out,
+                            hipStream_t st);
+
 // Which (K, C, E) combinations have kernel instances, and whether the
 // forward/backward shared-memory plan of an instance fits 160 KiB.
 bool have_instance(int K, int C, int E);

@@ -1,0 +1,488 @@
+// The mixer's input projection with its epilogue fused (section "Input
+// projections", Alg. 2), and the plain GEMMs and transposes of its backward.
+//
+// Forward: y = u Wp^T, one GEMM over d_model that yields the channels of q,
+// k, v, q' and k' of every head, followed in the same kernel by the causal
+// depthwise convolution, SiLU / softplus and the Euclidean normalisations of
+// the input side.  y therefore never makes a round trip through HBM; a
+// training forward may still write it (bf16) for the backward.
+//
+// GEMM tiles: bf16 operands, fp32 accumulation on v_mfma_f32_16x16x32_bf16.
+// A workgroup of four waves computes 256 rows by 128 columns; wave (mi, ni)
+// owns rows 128 mi .. 128 mi + 127 and columns 64 ni .. 64 ni + 63 (32
+// accumulator tiles; per 32-deep step 8 + 4 fragment reads feed 32 MFMAs).
+// The projection tile is 256 consecutive tokens of one batch row plus 16 rows
+// above them, whose last W - 1 the convolution reads: recomputed rather than
+// taken from the neighbouring tile (6% more MFMA work, no wait between
+// workgroups); each wave takes two of the halo's eight 16-column tiles.  The
+// contraction runs in stages of 64 through a ring of three shared-memory
+// buffers, filled by direct global-to-LDS copies two stages ahead.  Rows past
+// an operand's end are copied from clamped addresses and never stored; a
+// partial last stage has its chunks past the contraction length zeroed in
+// shared memory.  LDS rows are XOR-swizzled in 16-byte chunks, so fragment
+// reads are free of bank conflicts while whole 1 KiB copies still fill them.
+//
+// Projection epilogue: the fp32 accumulators go through shared memory (the
+// stage buffers' space); a thread then walks a run of 16 tokens for eight
+// channels, keeping the last W - 1 inputs in registers, applies the taps, the
+// activation and the norm (a sum over the K / 8 or E / 8 lanes of the head,
+// all inside one 16-lane row group since a tile holds whole heads), and writes
+// 16 bytes per token and output.
+#include <hip/hip_runtime.h>
+
+#include "tla_common.hpp"
+#include "tla_input_side.hpp"
+#include "tla_internal.hpp"
+
+namespace tla {
+
+constexpr int GM_NTHR = 256;  // four waves
+constexpr int GM_BM = 256;    // rows of a tile (tokens of a projection tile)
+constexpr int GM_BN = 128;    // columns of a tile (channels of a projection tile)
+constexpr int GM_BK = 64;     // contraction depth of a stage
+constexpr int GM_NS = 3;      // stages in the shared-memory ring
+constexpr int PJ_HALO = 16;   // rows above a projection tile
+constexpr int PJ_YLD = GM_BN + 4;  // fp32 row pitch of the epilogue tile (no bank conflicts)
+
+template <int HALO>
+struct GemmRing {
+  static constexpr int RA = GM_BM + HALO;
+  typedef SwzTile<bf16_t, RA, GM_BK> TA;
+  typedef SwzTile<bf16_t, GM_BN, GM_BK> TB;
+  TA a[GM_NS];
+  TB b[GM_NS];
+  // 1 KiB copies per stage, and per wave (round-robin over the four waves)
+  static constexpr int NBA = TA::NCHK / 64, NBB = TB::NCHK / 64;
+  static constexpr int MA = (NBA + 3) / 4, MB = NBB / 4;
+  static_assert(TA::NCHK % 64 == 0 && NBB % 4 == 0, "whole 1 KiB copies");
+};
+
+struct ProjSmem {
+  union {
+    GemmRing<PJ_HALO> ring;
+    float y[GM_BM + PJ_HALO][PJ_YLD];
+  };
+};
+static_assert(sizeof(ProjSmem) <= 160 * 1024, "projection tile exceeds shared memory");
+static_assert(sizeof(GemmRing<0>) <= 160 * 1024, "GEMM ring exceeds shared memory");
+
+// The logical chunk a lane copies is the same in every 1 KiB block of a wave:
+// physical chunk p = 64 blk + lane holds row r = p / 8, chunk (p % 8) ^ sw(r)
+// with sw(r) = (r / 2) % 8, and blk = wave + 4 i keeps (r / 2) % 8 fixed.
+__device__ __forceinline__ int copy_chunk(int wv, int lane) {
+  return (lane & 7) ^ ((4 * (wv & 1) + (lane >> 4)) & 7);
+}
+__device__ __forceinline__ int copy_row(int wv, int i, int lane) { return 8 * (wv + 4 * i) + (lane >> 3); }
+
+// Issue the copies of the stage starting at contraction index k0 into ring
+// slot `slot`; ra / rb are the lanes' row byte offsets from the bases.
+template <int HALO>
+__device__ __forceinline__ void issue_stage(GemmRing<HALO>& R, int slot, const bf16_t* baseA,
+                                            const bf16_t* baseB,
+                                            const uint32_t (&ra)[GemmRing<HALO>::MA],
+                                            const uint32_t (&rb)[GemmRing<HALO>::MB], int wv,
+                                            int chunk, int k0, int K) {
+  typedef GemmRing<HALO> RG;
+  const uint32_t kb = 2u * (uint32_t)min(k0 + 8 * chunk, K - 8);
+  const uint32_t la = lds_addr(R.a[slot].d), lb = lds_addr(R.b[slot].d);
+#pragma unroll
+  for (int i = 0; i < RG::MA; ++i) {
+    const int blk = wv + 4 * i;
+    if (RG::NBA % 4 != 0 && blk >= RG::NBA) break;  // wave-uniform
+    lds_dma<16>(baseA, ra[i] + kb, la + 1024 * blk);
+  }
+#pragma unroll
+  for (int i = 0; i < RG::MB; ++i) lds_dma<16>(baseB, rb[i] + kb, lb + 1024 * (wv + 4 * i));
+}
+
+// Zero the chunks at contraction index K and beyond of a partial stage.
+template <int HALO>
+__device__ __forceinline__ void zero_tail(GemmRing<HALO>& R, int slot, int k0, int K) {
+  typedef GemmRing<HALO> RG;
+  for (int p = threadIdx.x; p < RG::TA::NCHK + RG::TB::NCHK; p += GM_NTHR) {
+    const bool isa = p < RG::TA::NCHK;
+    const int pp = isa ? p : p - RG::TA::NCHK;
+    int r, c;
+    RG::TA::logical(pp, r, c);  // the same chunk map for both tiles (eight chunks per row)
+    if (k0 + 8 * c >= K) {
+      char* d = isa ? (char*)R.a[slot].d : (char*)R.b[slot].d;
+      *(uint4*)(d + 16 * pp) = make_uint4(0, 0, 0, 0);
+    }
+  }
+}
+
+// One stage of the wave's products: two 32-deep steps over its 8 x 4 tiles
+// (and, with a halo, two halo tiles: rows 0..15, columns 16 (4 ni + 2 mi + h)).
+template <int HALO>
+__device__ __forceinline__ void mma_stage(const GemmRing<HALO>& R, int slot, int mi, int ni,
+                                          int lane, f32x4 (&acc)[8][4], f32x4 (&acch)[2]) {
+  const int n = lane & 15, g = lane >> 4;
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int col = 8 * (4 * s + g);
+    bf16x8 fa[8], fb[4];
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      fa[i] = *(const bf16x8*)R.a[slot].at(HALO + 128 * mi + 16 * i + n, col);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) fb[j] = *(const bf16x8*)R.b[slot].at(64 * ni + 16 * j + n, col);
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+    if constexpr (HALO > 0) {
+      const bf16x8 fh = *(const bf16x8*)R.a[slot].at(n, col);
+      acch[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fh, mi ? fb[2] : fb[0], acch[0], 0, 0, 0);
+      acch[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fh, mi ? fb[3] : fb[1], acch[1], 0, 0, 0);
+    }
+  }
+}
+
+// The contraction over stages [s0, s1) of 64 (K the full length).  Every wave
+// waits for its own copies of a stage, then the barrier makes all of them
+// visible and frees the slot that the next issue refills.
+template <int HALO>
+__device__ __forceinline__ void gemm_mainloop(GemmRing<HALO>& R, const bf16_t* baseA,
+                                              const bf16_t* baseB,
+                                              const uint32_t (&ra)[GemmRing<HALO>::MA],
+                                              const uint32_t (&rb)[GemmRing<HALO>::MB], int K,
+                                              int s0, int s1, f32x4 (&acc)[8][4],
+                                              f32x4 (&acch)[2]) {
+  typedef GemmRing<HALO> RG;
+  const int wv = wave_id(), lane = lane_id();
+  const int mi = wv >> 1, ni = wv & 1;
+  const int chunk = copy_chunk(wv, lane);
+  // copies per stage of this wave
+  const int per = min(RG::MA, (RG::NBA - wv + 3) / 4) + RG::MB;
+  const int ns = s1 - s0;
+#pragma unroll
+  for (int s = 0; s < GM_NS - 1; ++s)
+    if (s < ns) issue_stage<HALO>(R, s, baseA, baseB, ra, rb, wv, chunk, (s0 + s) * GM_BK, K);
+  for (int s = 0; s < ns; ++s) {
+    const int ahead = min(GM_NS - 2, ns - 1 - s);
+    wait_vmcnt_rt(ahead * per);
+    __syncthreads();
+    const int k0 = (s0 + s) * GM_BK;
+    if (k0 + GM_BK > K) {  // partial last stage (uniform)
+      zero_tail<HALO>(R, s % GM_NS, k0, K);
+      __syncthreads();
+    }
+    if (s + GM_NS - 1 < ns)
+      issue_stage<HALO>(R, (s + GM_NS - 1) % GM_NS, baseA, baseB, ra, rb, wv, chunk,
+                        (s0 + s + GM_NS - 1) * GM_BK, K);
+    mma_stage<HALO>(R, s % GM_NS, mi, ni, lane, acc, acch);
+  }
+}
+
+// ------------------------------------------------------------ fused forward
+template <int W>
+__global__ __launch_bounds__(GM_NTHR) void k_proj_in(ProjArgs a, const bf16_t* __restrict__ u,
+                                                     const bf16_t* __restrict__ Wp,
+                                                     const float* __restrict__ w, bf16_t* q,
+                                                     bf16_t* k, bf16_t* v, bf16_t* q2, bf16_t* k2,
+                                                     bf16_t* ysave) {
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  ProjSmem& sm = *reinterpret_cast<ProjSmem*>(smem_raw);
+  typedef GemmRing<PJ_HALO> RG;
+  const int wv = wave_id(), lane = lane_id();
+
+  // Tile: the eight accelerator dies take contiguous ranges of token tiles
+  // (each token tile's rows are then read into one die's L2 only) and walk
+  // every channel tile of one token tile before the next.
+  int mt, ct;
+  if ((a.n_mt & 7) == 0) {
+    const int j = blockIdx.x >> 3;
+    mt = (blockIdx.x & 7) * (a.n_mt >> 3) + j / a.n_ct;
+    ct = j % a.n_ct;
+  } else {
+    mt = blockIdx.x / a.n_ct;
+    ct = blockIdx.x % a.n_ct;
+  }
+  const int b = mt / a.tiles_per_row, t0 = (mt % a.tiles_per_row) * GM_BM, n0 = ct * GM_BN;
+  const int tbase = max(t0 - PJ_HALO, 0);
+  const bf16_t* baseA = uniform_ptr(u + ((size_t)b * a.T + tbase) * a.Dm);
+  const bf16_t* baseB = uniform_ptr(Wp + (size_t)n0 * a.Dm);
+  uint32_t ra[RG::MA], rb[RG::MB];
+#pragma unroll
+  for (int i = 0; i < RG::MA; ++i) {
+    const int t = min(max(t0 - PJ_HALO + copy_row(wv, i, lane), 0), a.T - 1);
+    ra[i] = (uint32_t)(t - tbase) * (uint32_t)a.Dm * 2u;
+  }
+#pragma unroll
+  for (int i = 0; i < RG::MB; ++i) {
+    const int c = min(n0 + copy_row(wv, i, lane), a.Ctot - 1);
+    rb[i] = (uint32_t)(c - n0) * (uint32_t)a.Dm * 2u;
+  }
+  f32x4 acc[8][4], acch[2];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = zero4();
+  acch[0] = acch[1] = zero4();
+  gemm_mainloop<PJ_HALO>(sm.ring, baseA, baseB, ra, rb, a.Dm, 0, (a.Dm + GM_BK - 1) / GM_BK, acc,
+                         acch);
+
+  // accumulators -> fp32 tile (row = 16 + token - t0, column = channel - n0)
+  __syncthreads();  // every wave is done with the ring
+  {
+    const int mi = wv >> 1, ni = wv & 1, n = lane & 15, g = lane >> 4;
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          sm.y[PJ_HALO + 128 * mi + 16 * i + 4 * g + r][64 * ni + 16 * j + n] = acc[i][j][r];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sm.y[4 * g + r][16 * (4 * ni + 2 * mi + h) + n] = acch[h][r];
+  }
+  __syncthreads();
+
+  // epilogue: thread = 8 channels (16 lanes per token) x a run of 16 tokens
+  const int cl = threadIdx.x & 15, run = threadIdx.x >> 4;
+  const int c = n0 + 8 * cl;
+  const bool on_c = c < a.Ctot;
+  const int cc = on_c ? c : a.Ctot - 8;  // lanes past the channels compute (and never store) the last ones
+  const ConvLane L = conv_lane(a, cc);
+  const bool silu = L.kind <= 2;
+  bf16_t* out = pick(L.kind, q, k, v, q2, k2) + (size_t)b * a.T * a.H * L.width + L.off;
+  const size_t orow = (size_t)a.H * L.width;
+  float wt[W][8];
+#pragma unroll
+  for (int j = 0; j < W; ++j) {
+    const f32x4 x0 = *(const f32x4*)(w + (size_t)j * a.Ctot + cc);
+    const f32x4 x1 = *(const f32x4*)(w + (size_t)j * a.Ctot + cc + 4);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      wt[j][i] = x0[i];
+      wt[j][4 + i] = x1[i];
+    }
+  }
+  const int r0 = 16 * run;
+  float hist[W > 1 ? W - 1 : 1][8];
+#pragma unroll
+  for (int h = 0; h < W - 1; ++h) {
+    const float* yr = &sm.y[PJ_HALO + r0 - 1 - h][8 * cl];
+    const bool live = t0 + r0 - 1 - h >= 0;  // tokens before the row's start count as zero
+#pragma unroll
+    for (int i = 0; i < 8; ++i) hist[h][i] = live ? yr[i] : 0.f;
+  }
+  bf16_t* yout = ysave ? ysave + (size_t)b * a.T * a.Ctot + c : nullptr;
+  for (int rr = 0; rr < 16; ++rr) {
+    const int t = t0 + r0 + rr;
+    float x[8], z[8], r[8], ss = 0.f;
+    const float* yr = &sm.y[PJ_HALO + r0 + rr][8 * cl];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] = yr[i];
+    conv8<W>(wt, hist, x, z);
+    push_hist<W>(hist, x);
+    act8(silu, z, r);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) ss += r[i] * r[i];
+    ss = lane_group_sum(ss, L.lpr);  // every lane of the wave takes part
+    if (L.lpr) {
+      const float inv = rsqrtf(ss + a.eps);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) r[i] *= inv;
+    }
+    if (on_c && t < a.T) {
+      store8(out + (size_t)t * orow, r);
+      if (yout) store8(yout + (size_t)t * a.Ctot, x);
+    }
+  }
+}
+
+ProjArgs proj_args(int B, int T, int Dm, int H, int K, int V, int E, int W, float eps) {
+  ProjArgs a;
+  a.B = B, a.T = T, a.Dm = Dm, a.H = H, a.K = K, a.V = V, a.E = E, a.W = W;
+  a.Ctot = H * (2 * K + V + 2 * E);
+  a.tiles_per_row = (T + GM_BM - 1) / GM_BM;
+  a.n_mt = B * a.tiles_per_row;
+  a.n_ct = (a.Ctot + GM_BN - 1) / GM_BN;
+  a.eps = eps;
+  return a;
+}
+
+hipError_t launch_proj_in(const ProjArgs& a, const void* u, const void* Wp, const float* w,
+                          void* const* out, void* y, hipStream_t st) {
+  const unsigned nblk = (unsigned)a.n_mt * (unsigned)a.n_ct;
+  if (nblk == 0) return hipSuccess;
+  const size_t smem = sizeof(ProjSmem);
+#define PROJ_L(W_)                                                                               \
+  case W_:                                                                                       \
+    (void)hipFuncSetAttribute((const void*)k_proj_in<W_>,                                        \
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);            \
+    hipLaunchKernelGGL((k_proj_in<W_>), dim3(nblk), dim3(GM_NTHR), smem, st, a, (const bf16_t*)u, \
+                       (const bf16_t*)Wp, w, (bf16_t*)out[0], (bf16_t*)out[1], (bf16_t*)out[2],   \
+                       (bf16_t*)out[3], (bf16_t*)out[4], (bf16_t*)y);                            \
+    break;
+  switch (a.W) {
+    PROJ_L(1) PROJ_L(2) PROJ_L(3) PROJ_L(4)
+    default: return hipErrorInvalidValue;
+  }
+#undef PROJ_L
+  return hipGetLastError();
+}
+
+// --------------------------------------------------------------- plain GEMM
+// C[M][N] = A[M][K] B[N][K]^T over the stages of split blockIdx.y.
+template <bool OUT_BF16>
+__global__ __launch_bounds__(GM_NTHR) void k_gemm_nt(long long M, long long N, int K,
+                                                     const bf16_t* __restrict__ A,
+                                                     const bf16_t* __restrict__ Bm, void* C,
+                                                     long long ldc, int splits, float* part) {
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  typedef GemmRing<0> RG;
+  RG& R = *reinterpret_cast<RG*>(smem_raw);
+  const int wv = wave_id(), lane = lane_id();
+  const long long nmt = (M + GM_BM - 1) / GM_BM;
+  const long long mt = blockIdx.x % nmt, nt = blockIdx.x / nmt;  // tiles sharing B adjacent
+  const long long m0 = mt * GM_BM, n0 = nt * GM_BN;
+  const bf16_t* baseA = uniform_ptr(A + m0 * K);
+  const bf16_t* baseB = uniform_ptr(Bm + n0 * K);
+  uint32_t ra[RG::MA], rb[RG::MB];
+#pragma unroll
+  for (int i = 0; i < RG::MA; ++i)
+    ra[i] = (uint32_t)(min(m0 + copy_row(wv, i, lane), M - 1) - m0) * (uint32_t)K * 2u;
+#pragma unroll
+  for (int i = 0; i < RG::MB; ++i)
+    rb[i] = (uint32_t)(min(n0 + copy_row(wv, i, lane), N - 1) - n0) * (uint32_t)K * 2u;
+  const int nst = (K + GM_BK - 1) / GM_BK, z = blockIdx.y;
+  const int s0 = (int)((long long)nst * z / splits), s1 = (int)((long long)nst * (z + 1) / splits);
+  f32x4 acc[8][4], acch[2];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = zero4();
+  acch[0] = acch[1] = zero4();
+  gemm_mainloop<0>(R, baseA, baseB, ra, rb, K, s0, s1, acc, acch);
+
+  // lane (g, n) of tile (i, j) holds rows 4 g + r, column n; after the quad
+  // transpose it holds row 4 g + n % 4, columns 4 (n / 4) .. + 3
+  const int mi = wv >> 1, ni = wv & 1, n = lane & 15, g = lane >> 4;
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const f32x4 x = quad_transpose(acc[i][j], n);
+      const long long row = m0 + 128 * mi + 16 * i + 4 * g + (n & 3);
+      const long long col = n0 + 64 * ni + 16 * j + 4 * (n >> 2);
+      if (row < M && col < N) {  // N is a multiple of 4
+        if (splits > 1) {
+          *(f32x4*)(part + ((long long)z * M + row) * N + col) = x;
+        } else if constexpr (OUT_BF16) {
+          *(u32x2*)((bf16_t*)C + row * ldc + col) = __builtin_bit_cast(u32x2, cvt_frag<bf16_t>(x));
+        } else {
+          *(f32x4*)((float*)C + row * ldc + col) = x;
+        }
+      }
+    }
+}
+
+// C = sum over splits of the partial products, in split order
+template <bool OUT_BF16>
+__global__ __launch_bounds__(256) void k_sum_splits(long long M, long long N, int splits,
+                                                    const float* __restrict__ part, void* C,
+                                                    long long ldc) {
+  const long long i4 = (long long)blockIdx.x * 256 + threadIdx.x;  // index of 4 columns
+  const long long nq = N / 4;
+  if (i4 >= M * nq) return;
+  const long long row = i4 / nq, col = 4 * (i4 % nq);
+  f32x4 s = *(const f32x4*)(part + row * N + col);
+  for (int z = 1; z < splits; ++z) s += *(const f32x4*)(part + ((long long)z * M + row) * N + col);
+  if constexpr (OUT_BF16)
+    *(u32x2*)((bf16_t*)C + row * ldc + col) = __builtin_bit_cast(u32x2, cvt_frag<bf16_t>(s));
+  else
+    *(f32x4*)((float*)C + row * ldc + col) = s;
+}
+
+int gemm_splits(long long M, long long N, long long K) {
+  const long long tiles = ((M + GM_BM - 1) / GM_BM) * ((N + GM_BN - 1) / GM_BN);
+  const long long nst = (K + GM_BK - 1) / GM_BK;
+  // fill the 256 compute units in whole rounds of one tile each, with at
+  // least eight stages per split
+  int best = 1;
+  double best_eff = 0.0;
+  for (int s = 1; s <= 8 && nst / s >= 8; ++s) {
+    const long long work = tiles * s;
+    const double eff = (double)work / (double)(((work + 255) / 256) * 256);
+    if (eff > best_eff + 0.05) best = s, best_eff = eff;
+  }
+  return best;
+}
+
+hipError_t launch_gemm_nt(long long M, long long N, long long K, const void* A, const void* Bm,
+                          void* C, bool c_bf16, long long ldc, int splits, float* part,
+                          hipStream_t st) {
+  if (M <= 0 || N <= 0) return hipSuccess;
+  const long long tiles = ((M + GM_BM - 1) / GM_BM) * ((N + GM_BN - 1) / GM_BN);
+  const size_t smem = sizeof(GemmRing<0>);
+  const dim3 grid((unsigned)tiles, (unsigned)splits);
+  if (c_bf16) {
+    (void)hipFuncSetAttribute((const void*)k_gemm_nt<true>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)smem);
+    hipLaunchKernelGGL(k_gemm_nt<true>, grid, dim3(GM_NTHR), smem, st, M, N, (int)K,
+                       (const bf16_t*)A, (const bf16_t*)Bm, C, ldc, splits, part);
+  } else {
+    (void)hipFuncSetAttribute((const void*)k_gemm_nt<false>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)smem);
+    hipLaunchKernelGGL(k_gemm_nt<false>, grid, dim3(GM_NTHR), smem, st, M, N, (int)K,
+                       (const bf16_t*)A, (const bf16_t*)Bm, C, ldc, splits, part);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || splits == 1) return e;
+  const long long n4 = M * (N / 4);
+  const unsigned nb = (unsigned)((n4 + 255) / 256);
+  if (c_bf16)
+    hipLaunchKernelGGL(k_sum_splits<true>, dim3(nb), dim3(256), 0, st, M, N, splits, part, C, ldc);
+  else
+    hipLaunchKernelGGL(k_sum_splits<false>, dim3(nb), dim3(256), 0, st, M, N, splits, part, C, ldc);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- transpose
+// out [C][Rp] = in [R][C]^T for 64 x 64 tiles through shared memory; rows R ..
+// Rp - 1 of the result are zero.  C is a multiple of 8.
+__global__ __launch_bounds__(256) void k_transpose(long long R, long long C, long long Rp,
+                                                   const bf16_t* __restrict__ in,
+                                                   bf16_t* __restrict__ out) {
+  __shared__ bf16_t tile[64][64 + 2];
+  const long long r0 = (long long)blockIdx.x * 64, c0 = (long long)blockIdx.y * 64;
+  // load: 64 rows x 8 chunks of 8 elements, two chunks per thread
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int idx = threadIdx.x + 256 * h, rr = idx >> 3, ch = idx & 7;
+    const long long r = r0 + rr, c = c0 + 8 * ch;
+    uint4 x = make_uint4(0, 0, 0, 0);
+    if (r < R && c < C) x = *(const uint4*)(in + r * C + c);
+    const bf16_t* e = (const bf16_t*)&x;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) tile[rr][8 * ch + i] = e[i];
+  }
+  __syncthreads();
+  // store: 64 result rows (columns of in) x 8 chunks of 8 elements
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int idx = threadIdx.x + 256 * h, cc = idx >> 3, ch = idx & 7;
+    const long long c = c0 + cc, r = r0 + 8 * ch;
+    if (c >= C || r >= Rp) continue;
+    bf16_t e[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) e[i] = tile[8 * ch + i][cc];
+    *(uint4*)(out + c * Rp + r) = *(const uint4*)e;
+  }
+}
+
+hipError_t launch_transpose(long long R, long long C, long long Rp, const void* in, void* out,
+                            hipStream_t st) {
+  if (Rp <= 0 || C <= 0) return hipSuccess;
+  const dim3 grid((unsigned)((Rp + 63) / 64), (unsigned)((C + 63) / 64));
+  hipLaunchKernelGGL(k_transpose, grid, dim3(256), 0, st, R, C, Rp, (const bf16_t*)in,
+                     (bf16_t*)out);
+  return hipGetLastError();
+}
+
+}  // namespace tla

@@ -110,6 +110,13 @@ int main() {
   (void)tla_out_gate_workspace_bytes(1 << 20, 128);
   (void)tla_gate_heads_workspace_bytes(1 << 20, 8, 8);
   (void)tla_conv_in_workspace_bytes(4, 4096, 8, 128, 128, 8, 4);
+  EXPECT(tla_proj_in_fwd(1, 10, 100, 2, 128, 128, 8, 4, 1e-6f, P, P, (float*)P, P, P, P, P, P, 0, 0) ==
+         TLA_E_UNSUPPORTED);
+  EXPECT(tla_proj_in_fwd(1, 10, 128, 2, 128, 128, 8, 4, 1e-6f, P, P, (float*)P, P, P, Q, P, P, 0, 0) ==
+         TLA_E_ALIGN);
+  EXPECT(tla_proj_in_bwd(1, 10, 128, 2, 128, 128, 8, 4, 1e-6f, P, P, (float*)P, P, P, P, P, P, P, P,
+                         (float*)P, (float*)P, P, 0, 0) == TLA_E_WORKSPACE);
+  (void)tla_proj_in_workspace_bytes(4, 4096, 2048, 8, 128, 128, 8, 4);
   for (int i = -1; i < 9; ++i) (void)tla_status_string(i);
   printf(fails ? "api check: %d FAILED\n" : "api check: ok\n", fails);
   return fails != 0;

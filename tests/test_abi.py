@@ -325,6 +325,55 @@ def test_conv_in_validation():
     assert bwd(dw=dy) == E_ALIAS
 
 
+def test_proj_in_validation():
+    """Fused input projection: widths, d_model, taps, group alignment,
+    required pointers, alignment, aliasing and workspace are checked on the
+    host (fake addresses, nothing launched)."""
+    L = tla.lib()
+    P = ctypes.c_void_p
+    u, Wp, w, q, k, v, q2, k2, y = (P(FAKE + i * 0x4000000) for i in range(9))
+    shp = dict(B=2, T=100, Dm=256, H=8, K=128, V=128, E=8, W=4)
+
+    def fwd(eps=1e-6, **kw):
+        a = dict(shp, u=u, Wp=Wp, w=w, q=q, k=k, v=v, q2=q2, k2=k2, y=y)
+        a.update(kw)
+        return L.tla_proj_in_fwd(a["B"], a["T"], a["Dm"], a["H"], a["K"], a["V"], a["E"], a["W"], eps,
+                                 a["u"], a["Wp"], a["w"], a["q"], a["k"], a["v"], a["q2"], a["k2"],
+                                 a["y"], None)
+    assert fwd(T=-1) == E_SHAPE
+    assert fwd(H=0) == E_SHAPE
+    assert fwd(K=256) == E_UNSUP  # a channel tile holds whole heads (at most 128)
+    assert fwd(E=4) == E_UNSUP
+    assert fwd(Dm=12) == E_UNSUP
+    assert fwd(Dm=0) == E_UNSUP
+    assert fwd(W=5) == E_UNSUP
+    assert fwd(H=1, K=8, V=8, E=16) == E_UNSUP
+    assert fwd(eps=float("nan")) == E_SHAPE
+    assert fwd(Wp=None) == E_NULL
+    assert fwd(k2=None) == E_NULL
+    assert fwd(q=P(FAKE + 8)) == E_ALIGN
+    assert fwd(q=u) == E_ALIAS
+    assert fwd(y=k) == E_ALIAS
+    assert fwd(B=0, u=None, q=None, k=None, v=None, q2=None, k2=None, y=None) == 0  # nothing to do
+    need = L.tla_proj_in_workspace_bytes(2, 100, 256, 8, 128, 128, 8, 4)
+    assert need > 0 and need % 256 == 0
+    dq, dk, dv, dq2, dk2, du, dWp, dw = (P(FAKE + 0x40000000 + i * 0x4000000) for i in range(8))
+    ws = P(FAKE + 0x80000000)
+
+    def bwd(ws_bytes=need, **kw):
+        a = dict(dq=dq, dk=dk, dv=dv, dq2=dq2, dk2=dk2, du=du, dWp=dWp, dw=dw, ws=ws, y=y)
+        a.update(kw)
+        return L.tla_proj_in_bwd(2, 100, 256, 8, 128, 128, 8, 4, 1e-6, u, Wp, w, a["y"], a["dq"], a["dk"],
+                                 a["dv"], a["dq2"], a["dk2"], a["du"], a["dWp"], a["dw"], a["ws"],
+                                 ws_bytes, None)
+    assert bwd(ws_bytes=need - 1) == E_WS
+    assert bwd(ws=None) == E_WS
+    assert bwd(y=None) == E_NULL
+    assert bwd(dWp=None) == E_NULL
+    assert bwd(du=dq) == E_ALIAS
+    assert bwd(dWp=dw) == E_ALIAS
+
+
 def test_noalloc_rejects_oversized_call_on_the_host():
     """tla_fwd_noalloc checks its scratch need before any HIP call."""
     L = tla.lib()
