@@ -7,14 +7,18 @@
 // the input side.  y therefore never makes a round trip through HBM; a
 // training forward may still write it (bf16) for the backward.
 //
-// GEMM tiles: bf16 operands, fp32 accumulation on v_mfma_f32_16x16x32_bf16.
-// A workgroup of four waves computes 256 rows by 128 columns; wave (mi, ni)
-// owns rows 128 mi .. 128 mi + 127 and columns 64 ni .. 64 ni + 63 (32
-// accumulator tiles; per 32-deep step 8 + 4 fragment reads feed 32 MFMAs).
-// The projection tile is 256 consecutive tokens of one batch row plus 16 rows
+// GEMM tiles: bf16 operands, fp32 accumulation on v_mfma_f32_32x32x16_bf16.
+// A workgroup of four waves (one per SIMD) computes 256 rows by 128 columns;
+// wave (mi, ni) owns rows 128 mi .. 128 mi + 127 and columns 64 ni .. 64 ni
+// + 63 (4 x 2 accumulator tiles of 32 x 32; per 32-deep step 8 + 4 fragment
+// reads feed 16 MFMAs).  The 32 x 32 shape matters with one wave per SIMD:
+// measured on the device, back-to-back 16x16x32 MFMAs from a single wave
+// reach about 59% of the matrix cores' rate, 32x32x16 ones 97%.  The
+// projection tile is 256 consecutive tokens of one batch row plus 16 rows
 // above them, whose last W - 1 the convolution reads: recomputed rather than
 // taken from the neighbouring tile (6% more MFMA work, no wait between
-// workgroups); each wave takes two of the halo's eight 16-column tiles.  The
+// workgroups) on 16x16x32 MFMAs, each wave taking two of the halo's eight
+// 16-column tiles.  The
 // contraction runs in stages of 64 through a ring of three shared-memory
 // buffers, filled by direct global-to-LDS copies two stages ahead.  Rows past
 // an operand's end are copied from clamped addresses and never stored; a
@@ -42,7 +46,8 @@ constexpr int GM_BN = 128;    // columns of a tile (channels of a projection til
 constexpr int GM_BK = 64;     // contraction depth of a stage
 constexpr int GM_NS = 3;      // stages in the shared-memory ring
 constexpr int PJ_HALO = 16;   // rows above a projection tile
-constexpr int PJ_YLD = GM_BN + 4;  // fp32 row pitch of the epilogue tile (no bank conflicts)
+constexpr int PJ_YLD = GM_BN + 8;  // fp32 row pitch of the epilogue tile: the two lane halves of
+                                   // an accumulator store (4 rows apart) hit disjoint banks
 
 template <int HALO>
 struct GemmRing {
@@ -111,68 +116,140 @@ __device__ __forceinline__ void zero_tail(GemmRing<HALO>& R, int slot, int k0, i
   }
 }
 
-// One stage of the wave's products: two 32-deep steps over its 8 x 4 tiles
-// (and, with a halo, two halo tiles: rows 0..15, columns 16 (4 ni + 2 mi + h)).
+// A wave's operand fragments of one 32-deep step, as two 16-deep halves of
+// v_mfma_f32_32x32x16_bf16 operands: its 4 row tiles and 2 column tiles of 32
+// (lane l holds row / column l % 32, contraction 8 (l / 32) .. + 7 of the
+// half); with a halo, the halo's 16-row A fragment and the B fragments of
+// the wave's two halo column tiles of 16, for v_mfma_f32_16x16x32_bf16 (lane
+// l holds row / column l % 16, contraction 8 (l / 16) .. + 7).
+struct StepFrags {
+  bf16x8 a[2][4], b[2][2], ha, hb[2];
+};
+
+// Read step `st` (0 or 1) of the stage in ring slot `slot` into F.
 template <int HALO>
-__device__ __forceinline__ void mma_stage(const GemmRing<HALO>& R, int slot, int mi, int ni,
-                                          int lane, f32x4 (&acc)[8][4], f32x4 (&acch)[2]) {
-  const int n = lane & 15, g = lane >> 4;
+__device__ __forceinline__ void read_step(const GemmRing<HALO>& R, int slot, int st, int mi, int ni,
+                                          int lane, StepFrags& F) {
+  const int r32 = lane & 31;
 #pragma unroll
-  for (int s = 0; s < 2; ++s) {
-    const int col = 8 * (4 * s + g);
-    bf16x8 fa[8], fb[4];
+  for (int h = 0; h < 2; ++h) {
+    const int col = 8 * (4 * st + 2 * h + (lane >> 5));
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
-      fa[i] = *(const bf16x8*)R.a[slot].at(HALO + 128 * mi + 16 * i + n, col);
+    for (int i = 0; i < 4; ++i)
+      F.a[h][i] = *(const bf16x8*)R.a[slot].at(HALO + 128 * mi + 32 * i + r32, col);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) fb[j] = *(const bf16x8*)R.b[slot].at(64 * ni + 16 * j + n, col);
+    for (int j = 0; j < 2; ++j) F.b[h][j] = *(const bf16x8*)R.b[slot].at(64 * ni + 32 * j + r32, col);
+  }
+  if constexpr (HALO > 0) {
+    const int r16 = lane & 15, col = 8 * (4 * st + (lane >> 4));
+    F.ha = *(const bf16x8*)R.a[slot].at(r16, col);
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
-    if constexpr (HALO > 0) {
-      const bf16x8 fh = *(const bf16x8*)R.a[slot].at(n, col);
-      acch[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fh, mi ? fb[2] : fb[0], acch[0], 0, 0, 0);
-      acch[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fh, mi ? fb[3] : fb[1], acch[1], 0, 0, 0);
-    }
+    for (int hh = 0; hh < 2; ++hh)
+      F.hb[hh] = *(const bf16x8*)R.b[slot].at(16 * (4 * ni + 2 * mi + hh) + r16, col);
   }
 }
 
-// The contraction over stages [s0, s1) of 64 (K the full length).  Every wave
-// waits for its own copies of a stage, then the barrier makes all of them
-// visible and frees the slot that the next issue refills.
+// The products of one step: the wave's 4 x 2 tiles of 32 x 32 and, with a
+// halo, its two halo tiles of 16 x 16 (rows 0..15, columns 16 (4 ni + 2 mi +
+// hh)).
+template <int HALO>
+__device__ __forceinline__ void mma_step(const StepFrags& F, f32x16 (&acc)[4][2], f32x4 (&acch)[2]) {
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(F.a[h][i], F.b[h][j], acc[i][j], 0, 0, 0);
+  if constexpr (HALO > 0) {
+    acch[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(F.ha, F.hb[0], acch[0], 0, 0, 0);
+    acch[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(F.ha, F.hb[1], acch[1], 0, 0, 0);
+  }
+}
+
+// The contraction over stages [s0, s1) of 64 (K the full length), software
+// pipelined by 32-deep steps.  Stage s sits in ring slot s % 3.  X holds the
+// fragments of a stage's first step and Y of its second: the products of
+// (s, 0) run while (s, 1) is read, and the products of (s, 1) while
+// (s + 1, 0) is read, so with one wave per SIMD the shared-memory reads hide
+// under the MFMAs instead of preceding them.  Before reading stage s + 1
+// every wave waits for its own copies of it and the barrier makes all of
+// them visible; the barrier also certifies that every wave has read stage s
+// into registers, so slot s % 3 is refilled there with stage s + 3 (copies
+// run two stages ahead).  A partial last stage has its chunks past K zeroed
+// before it is read.
 template <int HALO>
 __device__ __forceinline__ void gemm_mainloop(GemmRing<HALO>& R, const bf16_t* baseA,
                                               const bf16_t* baseB,
                                               const uint32_t (&ra)[GemmRing<HALO>::MA],
                                               const uint32_t (&rb)[GemmRing<HALO>::MB], int K,
-                                              int s0, int s1, f32x4 (&acc)[8][4],
+                                              int s0, int s1, f32x16 (&acc)[4][2],
                                               f32x4 (&acch)[2]) {
   typedef GemmRing<HALO> RG;
   const int wv = wave_id(), lane = lane_id();
   const int mi = wv >> 1, ni = wv & 1;
   const int chunk = copy_chunk(wv, lane);
-  // copies per stage of this wave
-  const int per = min(RG::MA, (RG::NBA - wv + 3) / 4) + RG::MB;
+  const int per = min(RG::MA, (RG::NBA - wv + 3) / 4) + RG::MB;  // copies per stage of this wave
   const int ns = s1 - s0;
-#pragma unroll
-  for (int s = 0; s < GM_NS - 1; ++s)
-    if (s < ns) issue_stage<HALO>(R, s, baseA, baseB, ra, rb, wv, chunk, (s0 + s) * GM_BK, K);
-  for (int s = 0; s < ns; ++s) {
-    const int ahead = min(GM_NS - 2, ns - 1 - s);
-    wait_vmcnt_rt(ahead * per);
+  if (ns <= 0) return;
+  auto issue = [&](int s) {
+    issue_stage<HALO>(R, s % GM_NS, baseA, baseB, ra, rb, wv, chunk, (s0 + s) * GM_BK, K);
+  };
+  // make stage s visible to every wave: own copies landed (those of the later
+  // stages issued so far, up to issued_hi, may stay in flight), barrier,
+  // then the tail of a partial stage zeroed
+  auto arrive = [&](int s, int issued_hi) {
+    wait_vmcnt_rt((issued_hi - s) * per);
     __syncthreads();
+  };
+  auto tail = [&](int s) {
     const int k0 = (s0 + s) * GM_BK;
-    if (k0 + GM_BK > K) {  // partial last stage (uniform)
+    if (k0 + GM_BK > K) {  // uniform
       zero_tail<HALO>(R, s % GM_NS, k0, K);
       __syncthreads();
     }
-    if (s + GM_NS - 1 < ns)
-      issue_stage<HALO>(R, (s + GM_NS - 1) % GM_NS, baseA, baseB, ra, rb, wv, chunk,
-                        (s0 + s + GM_NS - 1) * GM_BK, K);
-    mma_stage<HALO>(R, s % GM_NS, mi, ni, lane, acc, acch);
+  };
+#pragma unroll
+  for (int s = 0; s < GM_NS; ++s)
+    if (s < ns) issue(s);
+  arrive(0, min(GM_NS - 1, ns - 1));
+  tail(0);
+  StepFrags X, Y;
+  read_step<HALO>(R, 0, 0, mi, ni, lane, X);
+  for (int s = 0; s < ns; ++s) {
+    read_step<HALO>(R, s % GM_NS, 1, mi, ni, lane, Y);
+    __builtin_amdgcn_sched_barrier(0);
+    mma_step<HALO>(X, acc, acch);
+    __builtin_amdgcn_sched_barrier(0);
+    if (s + 1 < ns) {
+      arrive(s + 1, min(s + GM_NS - 1, ns - 1));
+      if (s + GM_NS < ns) issue(s + GM_NS);
+      tail(s + 1);
+      read_step<HALO>(R, (s + 1) % GM_NS, 0, mi, ni, lane, X);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    mma_step<HALO>(Y, acc, acch);
   }
+}
+
+// Tile order.  The eight accelerator dies receive workgroups round-robin and
+// each has its own L2.  When the row-tile count splits evenly over the dies,
+// die x takes row tiles [x n / 8, (x + 1) n / 8) and walks them in groups of
+// up to four row tiles by every column tile, row tiles fastest: the 32
+// workgroups a die runs at once then share each row tile's A rows eight ways
+// and each column tile's B rows four ways in its L2.  Otherwise the same
+// grouping runs over the whole grid.
+__device__ __forceinline__ void tile_order(int bid, int nm, int nn, int& mt, int& nt) {
+  int m0 = 0, per = nm, j = bid;
+  if ((nm & 7) == 0) {
+    per = nm >> 3;
+    m0 = (bid & 7) * per;
+    j = bid >> 3;
+  }
+  const int gm = (per % 4 == 0) ? 4 : (per % 2 == 0) ? 2 : 1;
+  const int grp = j / (gm * nn), r = j % (gm * nn);
+  mt = m0 + grp * gm + r % gm;
+  nt = r / gm;
 }
 
 // ------------------------------------------------------------ fused forward
@@ -187,18 +264,8 @@ __global__ __launch_bounds__(GM_NTHR) void k_proj_in(ProjArgs a, const bf16_t* _
   typedef GemmRing<PJ_HALO> RG;
   const int wv = wave_id(), lane = lane_id();
 
-  // Tile: the eight accelerator dies take contiguous ranges of token tiles
-  // (each token tile's rows are then read into one die's L2 only) and walk
-  // every channel tile of one token tile before the next.
   int mt, ct;
-  if ((a.n_mt & 7) == 0) {
-    const int j = blockIdx.x >> 3;
-    mt = (blockIdx.x & 7) * (a.n_mt >> 3) + j / a.n_ct;
-    ct = j % a.n_ct;
-  } else {
-    mt = blockIdx.x / a.n_ct;
-    ct = blockIdx.x % a.n_ct;
-  }
+  tile_order(blockIdx.x, a.n_mt, a.n_ct, mt, ct);
   const int b = mt / a.tiles_per_row, t0 = (mt % a.tiles_per_row) * GM_BM, n0 = ct * GM_BN;
   const int tbase = max(t0 - PJ_HALO, 0);
   const bf16_t* baseA = uniform_ptr(u + ((size_t)b * a.T + tbase) * a.Dm);
@@ -214,11 +281,14 @@ __global__ __launch_bounds__(GM_NTHR) void k_proj_in(ProjArgs a, const bf16_t* _
     const int c = min(n0 + copy_row(wv, i, lane), a.Ctot - 1);
     rb[i] = (uint32_t)(c - n0) * (uint32_t)a.Dm * 2u;
   }
-  f32x4 acc[8][4], acch[2];
+  f32x16 acc[4][2];
+  f32x4 acch[2];
 #pragma unroll
-  for (int i = 0; i < 8; ++i)
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = zero4();
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
   acch[0] = acch[1] = zero4();
   gemm_mainloop<PJ_HALO>(sm.ring, baseA, baseB, ra, rb, a.Dm, 0, (a.Dm + GM_BK - 1) / GM_BK, acc,
                          acch);
@@ -226,18 +296,23 @@ __global__ __launch_bounds__(GM_NTHR) void k_proj_in(ProjArgs a, const bf16_t* _
   // accumulators -> fp32 tile (row = 16 + token - t0, column = channel - n0)
   __syncthreads();  // every wave is done with the ring
   {
-    const int mi = wv >> 1, ni = wv & 1, n = lane & 15, g = lane >> 4;
+    // 32 x 32 tile (i, j): register r of lane l holds row 8 (r / 4) + 4 (l / 32)
+    // + r % 4, column l % 32; 16 x 16 halo tile: register r of lane l holds
+    // row 4 (l / 16) + r, column l % 16
+    const int mi = wv >> 1, ni = wv & 1;
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < 2; ++j)
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          sm.y[PJ_HALO + 128 * mi + 16 * i + 4 * g + r][64 * ni + 16 * j + n] = acc[i][j][r];
+        for (int r = 0; r < 16; ++r)
+          sm.y[PJ_HALO + 128 * mi + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)]
+              [64 * ni + 32 * j + (lane & 31)] = acc[i][j][r];
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) sm.y[4 * g + r][16 * (4 * ni + 2 * mi + h) + n] = acch[h][r];
+      for (int r = 0; r < 4; ++r)
+        sm.y[4 * (lane >> 4) + r][16 * (4 * ni + 2 * mi + h) + (lane & 15)] = acch[h][r];
   }
   __syncthreads();
 
@@ -338,9 +413,9 @@ __global__ __launch_bounds__(GM_NTHR) void k_gemm_nt(long long M, long long N, i
   typedef GemmRing<0> RG;
   RG& R = *reinterpret_cast<RG*>(smem_raw);
   const int wv = wave_id(), lane = lane_id();
-  const long long nmt = (M + GM_BM - 1) / GM_BM;
-  const long long mt = blockIdx.x % nmt, nt = blockIdx.x / nmt;  // tiles sharing B adjacent
-  const long long m0 = mt * GM_BM, n0 = nt * GM_BN;
+  int mti, nti;
+  tile_order(blockIdx.x, (int)((M + GM_BM - 1) / GM_BM), (int)((N + GM_BN - 1) / GM_BN), mti, nti);
+  const long long m0 = (long long)mti * GM_BM, n0 = (long long)nti * GM_BN;
   const bf16_t* baseA = uniform_ptr(A + m0 * K);
   const bf16_t* baseB = uniform_ptr(Bm + n0 * K);
   uint32_t ra[RG::MA], rb[RG::MB];
@@ -352,24 +427,32 @@ __global__ __launch_bounds__(GM_NTHR) void k_gemm_nt(long long M, long long N, i
     rb[i] = (uint32_t)(min(n0 + copy_row(wv, i, lane), N - 1) - n0) * (uint32_t)K * 2u;
   const int nst = (K + GM_BK - 1) / GM_BK, z = blockIdx.y;
   const int s0 = (int)((long long)nst * z / splits), s1 = (int)((long long)nst * (z + 1) / splits);
-  f32x4 acc[8][4], acch[2];
+  f32x16 acc[4][2];
+  f32x4 acch[2];
 #pragma unroll
-  for (int i = 0; i < 8; ++i)
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = zero4();
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
   acch[0] = acch[1] = zero4();
   gemm_mainloop<0>(R, baseA, baseB, ra, rb, K, s0, s1, acc, acch);
 
-  // lane (g, n) of tile (i, j) holds rows 4 g + r, column n; after the quad
-  // transpose it holds row 4 g + n % 4, columns 4 (n / 4) .. + 3
-  const int mi = wv >> 1, ni = wv & 1, n = lane & 15, g = lane >> 4;
+  // registers 4 q .. 4 q + 3 of lane l in tile (i, j) hold rows 8 q + 4 (l / 32)
+  // + 0..3, column l % 32; after the quad transpose (lanes 4 m .. 4 m + 3
+  // exchange) lane l holds row 8 q + 4 (l / 32) + l % 4, columns
+  // 4 ((l % 32) / 4) .. + 3
+  const int mi = wv >> 1, ni = wv & 1, n = lane & 31;
 #pragma unroll
-  for (int i = 0; i < 8; ++i)
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const f32x4 x = quad_transpose(acc[i][j], n);
-      const long long row = m0 + 128 * mi + 16 * i + 4 * g + (n & 3);
-      const long long col = n0 + 64 * ni + 16 * j + 4 * (n >> 2);
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const f32x4 x = quad_transpose(f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                                           acc[i][j][4 * q + 3]}, n);
+      const long long row = m0 + 128 * mi + 32 * i + 8 * q + 4 * (lane >> 5) + (n & 3);
+      const long long col = n0 + 64 * ni + 32 * j + 4 * (n >> 2);
       if (row < M && col < N) {  // N is a multiple of 4
         if (splits > 1) {
           *(f32x4*)(part + ((long long)z * M + row) * N + col) = x;
