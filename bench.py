@@ -531,6 +531,38 @@ def proj_bench(steps, warmup):
           flush=True)
 
 
+def mfma_peak_bench(steps, warmup):
+    """Measured side of the MFMA roofline's peak: back-to-back bf16 MFMAs on
+    register accumulators (no memory traffic), 16x16x32 and 32x32x16, at one
+    and two waves per SIMD (256 and 512 workgroups of four waves on the 256
+    compute units), timed with HIP events on the launch stream."""
+    import torch
+    import paper_2609_36529_amd as tla
+    sink = torch.empty(512 * 256, dtype=torch.float32, device="cuda")
+    iters = 4000
+    res = []
+    for shape, name in ((0, "16x16x32"), (1, "32x32x16")):
+        for blocks in (256, 512):
+            for _ in range(max(warmup, 3)):
+                tla.mfma_rate(shape, blocks, iters, sink)
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            flop = 0
+            for _ in range(steps):
+                flop += tla.mfma_rate(shape, blocks, iters, sink)
+            b.record()
+            torch.cuda.synchronize()
+            tf = flop / (a.elapsed_time(b) * 1e-3) / 1e12
+            res.append({"mfma": name, "waves_per_simd": blocks // 256, "tflops": round(tf, 1),
+                        "frac_of_datasheet": round(tf / PEAK_BF16_TFLOPS, 4)})
+    best = max(r["tflops"] for r in res)
+    print(json.dumps({
+        "metric": "bf16 MFMA rate, register accumulators", "value": best, "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": steps, "warmup": warmup, "higher_is_better": True, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "back-to-back MFMAs on independent accumulators, no memory traffic"},
+        "datasheet_peak": PEAK_BF16_TFLOPS, "runs": res}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -549,6 +581,8 @@ def main():
                     help="time the gate heads (forget gate, write strength) forward and backward")
     ap.add_argument("--conv", action="store_true",
                     help="time the input side (short convolution, activations, L2 norm) forward and backward")
+    ap.add_argument("--mfma-peak", action="store_true",
+                    help="measure the bf16 MFMA rate with no memory traffic (the roofline's measured peak)")
     ap.add_argument("--proj", action="store_true",
                     help="time the fused input projection (GEMM + input side) forward and backward")
     ap.add_argument("--forward", metavar="NAME",
@@ -579,6 +613,9 @@ def main():
         return
     if args.proj:
         proj_bench(args.steps, args.warmup)
+        return
+    if args.mfma_peak:
+        mfma_peak_bench(args.steps, args.warmup)
         return
     if args.forward:
         forward_bench(args.forward, args.steps, args.warmup)

@@ -349,6 +349,21 @@ int tla_proj_in_bwd(int B, int T, int Dm, int H, int K, int V, int E, int W, flo
                     float* dWp, float* dw, void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * Diagnostics: the bf16 matrix-core rate as seen by back-to-back MFMAs with
+ * no memory traffic, the measured counterpart of the datasheet peak.  Each of
+ * `blocks` workgroups of four waves runs `iters` rounds of 32
+ * v_mfma_f32_16x16x32_bf16 (shape 0) or 8 v_mfma_f32_32x32x16_bf16 (shape 1)
+ * on independent register accumulators and writes one float per thread to
+ * sink (device, blocks * 256 floats, 16-byte aligned; the values mean
+ * nothing).  tla_mfma_rate_flop gives the floating-point operations of such a
+ * call (0 for invalid arguments); the caller times it.  With 256 workgroups
+ * on the 256 compute units each SIMD runs one wave, with 512 two.
+ * Asynchronous on `stream`.
+ */
+size_t tla_mfma_rate_flop(int shape, int blocks, int iters);
+int tla_mfma_rate(int shape, int blocks, int iters, float* sink, void* stream);
+
+/*
  * Per-kernel timing, for diagnostics and benchmarks (not needed otherwise).
  * tla_prof_enable(1) clears previous records and starts bracketing every
  * kernel launch of the library with a pair of HIP events on the launch

@@ -95,6 +95,10 @@ def lib():
     L.tla_proj_in_workspace_bytes.restype = S
     L.tla_proj_in_bwd.argtypes = [I] * 8 + [ctypes.c_float] + [P] * 13 + [S, P]
     L.tla_proj_in_bwd.restype = I
+    L.tla_mfma_rate_flop.argtypes = [I, I, I]
+    L.tla_mfma_rate_flop.restype = S
+    L.tla_mfma_rate.argtypes = [I, I, I, P, P]
+    L.tla_mfma_rate.restype = I
     L.tla_prof_enable.argtypes = [I]
     L.tla_prof_enable.restype = I
     L.tla_prof_read.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I), I]
@@ -583,6 +587,18 @@ def proj_in_bwd(u, Wp, w, y, H, K, V, E, grads, eps=1e-6):
                              *[_ptr(g) for g in grads], _ptr(du), _ptr(dWp), _ptr(dw), _ptr(ws),
                              ws.numel(), _stream(dev)))
     return du, dWp, dw
+
+
+def mfma_rate(shape, blocks, iters, sink):
+    """Launch the MFMA-rate diagnostic (shape 0: 16x16x32, 1: 32x32x16 bf16)
+    on the current stream; returns its FLOP count.  sink: a float32 device
+    tensor of at least blocks * 256 elements.  Runs tla_mfma_rate."""
+    _need(sink, "sink", torch.float32)
+    if sink.numel() < blocks * 256:
+        raise ValueError("sink needs blocks * 256 floats")
+    L = lib()
+    _check(L.tla_mfma_rate(shape, blocks, iters, _ptr(sink), _stream(sink.device)))
+    return L.tla_mfma_rate_flop(shape, blocks, iters)
 
 
 def prof_enable(on=True):

@@ -20,7 +20,7 @@ FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950", "-x", "hip",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-Wall", "-Wno-unused-function"]
 SOURCES = ["tla_api.cpp", "tla_fwd.hip", "tla_step.hip", "tla_bwd.hip", "tla_gate.hip",
-           "tla_conv.hip", "tla_proj.hip"]
+           "tla_conv.hip", "tla_proj.hip", "tla_diag.hip"]
 
 
 def _compile(src):

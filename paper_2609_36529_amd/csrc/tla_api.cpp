@@ -882,6 +882,25 @@ int tla_proj_in_bwd(int B, int T, int Dm, int H, int K, int V, int E, int W, flo
   return TLA_OK;
 }
 
+// ----------------------------------------------------------- diagnostics
+size_t tla_mfma_rate_flop(int shape, int blocks, int iters) {
+  if ((shape != 0 && shape != 1) || blocks < 1 || iters < 1) return 0;
+  // per wave and round: 32 x 16x16x32 (16384 each) or 8 x 32x32x16 (32768 each)
+  return (size_t)blocks * 4 * (size_t)iters * (shape == 0 ? 32 * 16384 : 8 * 32768);
+}
+
+int tla_mfma_rate(int shape, int blocks, int iters, float* sink, void* stream) {
+  g_err[0] = 0;
+  if (shape != 0 && shape != 1) return fail(TLA_E_SHAPE, "shape %d (0: 16x16x32, 1: 32x32x16)", shape);
+  if (blocks < 1 || blocks > 65536 || iters < 1 || iters > (1 << 24))
+    return fail(TLA_E_SHAPE, "blocks = %d, iters = %d", blocks, iters);
+  if (!sink) return fail(TLA_E_NULL, "sink is required");
+  if (misaligned(sink)) return fail(TLA_E_ALIGN, "pointer %p is not 16-byte aligned", (void*)sink);
+  hipError_t e = tla::launch_mfma_rate(shape == 1, blocks, iters, sink, (hipStream_t)stream);
+  if (e != hipSuccess) return device_fail(e, "MFMA rate kernel");
+  return TLA_OK;
+}
+
 int tla_prof_enable(int on) {
   std::lock_guard<std::mutex> lk(g_prof_mu);
   for (ProfRec& r : g_prof) {

@@ -176,6 +176,9 @@ hipError_t launch_gemm_nt(long long M, long long N, long long K, const void* A, 
 hipError_t launch_transpose(long long R, long long C, long long Rp, const void* in, void* out,
                             hipStream_t st);
 
+// Diagnostics: back-to-back bf16 MFMAs on register accumulators.
+hipError_t launch_mfma_rate(bool wide, int blocks, int iters, float* sink, hipStream_t st);
+
 // Which (K, C, E) combinations have kernel instances, and whether the
 // forward/backward shared-memory plan of an instance fits 160 KiB.
 bool have_instance(int K, int C, int E);

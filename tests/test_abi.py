@@ -374,6 +374,21 @@ def test_proj_in_validation():
     assert bwd(dWp=dw) == E_ALIAS
 
 
+def test_mfma_rate_validation_and_flop_count():
+    """The MFMA-rate diagnostic checks its arguments on the host; its FLOP
+    count is 4 waves x rounds x (32 x 16x16x32 or 8 x 32x32x16) per block."""
+    L = tla.lib()
+    P = ctypes.c_void_p
+    assert L.tla_mfma_rate(2, 256, 10, P(FAKE), None) == E_SHAPE
+    assert L.tla_mfma_rate(0, 0, 10, P(FAKE), None) == E_SHAPE
+    assert L.tla_mfma_rate(1, 256, 0, P(FAKE), None) == E_SHAPE
+    assert L.tla_mfma_rate(0, 256, 10, None, None) == E_NULL
+    assert L.tla_mfma_rate(0, 256, 10, P(FAKE + 4), None) == E_ALIGN
+    assert L.tla_mfma_rate_flop(0, 256, 10) == 256 * 4 * 10 * 32 * 16 * 16 * 32 * 2
+    assert L.tla_mfma_rate_flop(1, 256, 10) == 256 * 4 * 10 * 8 * 32 * 32 * 16 * 2
+    assert L.tla_mfma_rate_flop(3, 256, 10) == 0
+
+
 def test_noalloc_rejects_oversized_call_on_the_host():
     """tla_fwd_noalloc checks its scratch need before any HIP call."""
     L = tla.lib()

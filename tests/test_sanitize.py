@@ -41,7 +41,7 @@ def test_oracle_under_asan_ubsan(tmp_path):
 def test_abi_host_validation_under_asan_ubsan(tmp_path):
     objs = [os.path.join(BUILD, f + ".o") for f in
             ("tla_fwd.hip", "tla_bwd.hip", "tla_step.hip", "tla_gate.hip", "tla_conv.hip",
-             "tla_proj.hip")]
+             "tla_proj.hip", "tla_diag.hip")]
     if not all(os.path.exists(o) for o in objs):
         from paper_2609_36529_amd import build as hip_build
         hip_build.build()
