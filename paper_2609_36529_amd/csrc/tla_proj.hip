@@ -34,6 +34,8 @@
 // 16 bytes per token and output.
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "tla_common.hpp"
 #include "tla_input_side.hpp"
 #include "tla_internal.hpp"
@@ -149,18 +151,59 @@ __device__ __forceinline__ void read_step(const GemmRing<HALO>& R, int slot, int
   }
 }
 
+// A compile-time loop: f(std::integral_constant<int, I>) for I = B .. E - 1.
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
+
+// Copy number C (0 .. MA + MB - 1) of this wave's share of a stage: A blocks
+// wv, wv + 4, ... then B blocks wv, wv + 4, ...; a wave with fewer A blocks
+// than MA skips the missing ones.  kb is the byte offset of the lane's chunk
+// within the stage's rows.
+template <int HALO, int C>
+__device__ __forceinline__ void stage_copy(GemmRing<HALO>& R, int slot, const bf16_t* baseA,
+                                           const bf16_t* baseB,
+                                           const uint32_t (&ra)[GemmRing<HALO>::MA],
+                                           const uint32_t (&rb)[GemmRing<HALO>::MB], int wv,
+                                           uint32_t kb) {
+  typedef GemmRing<HALO> RG;
+  if constexpr (C < RG::MA) {
+    const int blk = wv + 4 * C;
+    if (RG::NBA % 4 != 0 && blk >= RG::NBA) return;  // wave-uniform
+    lds_dma<16>(baseA, ra[C] + kb, lds_addr(R.a[slot].d) + 1024 * blk);
+  } else {
+    lds_dma<16>(baseB, rb[C - RG::MA] + kb, lds_addr(R.b[slot].d) + 1024 * (wv + 4 * (C - RG::MA)));
+  }
+}
+
 // The products of one step: the wave's 4 x 2 tiles of 32 x 32 and, with a
 // halo, its two halo tiles of 16 x 16 (rows 0..15, columns 16 (4 ni + 2 mi +
-// hh)).
-template <int HALO>
-__device__ __forceinline__ void mma_step(const StepFrags& F, f32x16 (&acc)[4][2], f32x4 (&acch)[2]) {
-#pragma unroll
-  for (int h = 0; h < 2; ++h)
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(F.a[h][i], F.b[h][j], acc[i][j], 0, 0, 0);
+// hh)).  With COPY, the copies of a later stage into ring slot `slot` are
+// issued one after each MFMA (a copy instruction holds up the wave that
+// issues it; between products that time overlaps the matrix core's work).
+template <int HALO, bool COPY>
+__device__ __forceinline__ void mma_step(const StepFrags& F, f32x16 (&acc)[4][2], f32x4 (&acch)[2],
+                                         GemmRing<HALO>& R, int slot, const bf16_t* baseA,
+                                         const bf16_t* baseB,
+                                         const uint32_t (&ra)[GemmRing<HALO>::MA],
+                                         const uint32_t (&rb)[GemmRing<HALO>::MB], int wv,
+                                         uint32_t kb) {
+  typedef GemmRing<HALO> RG;
+  constexpr int NC = RG::MA + RG::MB;
+  static_for<0, 16>([&](auto m) {
+    constexpr int h = decltype(m)::value / 8, i = (decltype(m)::value / 2) % 4, j = decltype(m)::value % 2;
+    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(F.a[h][i], F.b[h][j], acc[i][j], 0, 0, 0);
+    if constexpr (COPY && decltype(m)::value < NC) {
+      stage_copy<HALO, decltype(m)::value>(R, slot, baseA, baseB, ra, rb, wv, kb);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  });
+  if constexpr (COPY && NC > 16)
+    static_for<16, NC>([&](auto c) { stage_copy<HALO, decltype(c)::value>(R, slot, baseA, baseB, ra, rb, wv, kb); });
   if constexpr (HALO > 0) {
     acch[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(F.ha, F.hb[0], acch[0], 0, 0, 0);
     acch[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(F.ha, F.hb[1], acch[1], 0, 0, 0);
@@ -174,10 +217,14 @@ __device__ __forceinline__ void mma_step(const StepFrags& F, f32x16 (&acc)[4][2]
 // (s + 1, 0) is read, so with one wave per SIMD the shared-memory reads hide
 // under the MFMAs instead of preceding them.  Before reading stage s + 1
 // every wave waits for its own copies of it and the barrier makes all of
-// them visible; the barrier also certifies that every wave has read stage s
-// into registers, so slot s % 3 is refilled there with stage s + 3 (copies
-// run two stages ahead).  A partial last stage has its chunks past K zeroed
-// before it is read.
+// them visible (the barrier waits for the wave's shared-memory reads, not
+// for its copies); it also certifies that every wave has read stage s into
+// registers, so slot s % 3 is refilled with stage s + 3 (copies run two
+// stages ahead), its copies interleaved with the products of (s, 1).  The
+// waits count copies with immediates: in the steady state one stage's
+// copies may stay in flight (counted as the fewest any wave issues, so a
+// wave that issues one more waits a little longer), otherwise none.  A
+// partial last stage has its chunks past K zeroed before it is read.
 template <int HALO>
 __device__ __forceinline__ void gemm_mainloop(GemmRing<HALO>& R, const bf16_t* baseA,
                                               const bf16_t* baseB,
@@ -186,23 +233,24 @@ __device__ __forceinline__ void gemm_mainloop(GemmRing<HALO>& R, const bf16_t* b
                                               int s0, int s1, f32x16 (&acc)[4][2],
                                               f32x4 (&acch)[2]) {
   typedef GemmRing<HALO> RG;
+  static_assert(GM_NS == 3, "the waits below assume one stage in flight beyond the next");
+  constexpr int MINPER = RG::NBA / 4 + RG::MB;  // copies per stage of the wave with the fewest
+  static_assert(MINPER <= 63, "vmcnt range");
   const int wv = wave_id(), lane = lane_id();
   const int mi = wv >> 1, ni = wv & 1;
   const int chunk = copy_chunk(wv, lane);
-  const int per = min(RG::MA, (RG::NBA - wv + 3) / 4) + RG::MB;  // copies per stage of this wave
   const int ns = s1 - s0;
   if (ns <= 0) return;
-  auto issue = [&](int s) {
-    issue_stage<HALO>(R, s % GM_NS, baseA, baseB, ra, rb, wv, chunk, (s0 + s) * GM_BK, K);
-  };
-  // make stage s visible to every wave: own copies landed (those of the later
-  // stages issued so far, up to issued_hi, may stay in flight), barrier,
-  // then the tail of a partial stage zeroed
-  auto arrive = [&](int s, int issued_hi) {
-    wait_vmcnt_rt((issued_hi - s) * per);
+  auto kbyte = [&](int s) { return 2u * (uint32_t)min((s0 + s) * GM_BK + 8 * chunk, K - 8); };
+  // make stage s visible to every wave (own copies landed, barrier), then the
+  // tail of a partial stage zeroed; `more` says whether stage s + 1 has been
+  // issued and may stay in flight
+  auto arrive = [&](int s, bool more) {
+    if (more)
+      wait_vmcnt<MINPER>();
+    else
+      wait_vmcnt<0>();
     __syncthreads();
-  };
-  auto tail = [&](int s) {
     const int k0 = (s0 + s) * GM_BK;
     if (k0 + GM_BK > K) {  // uniform
       zero_tail<HALO>(R, s % GM_NS, k0, K);
@@ -211,25 +259,28 @@ __device__ __forceinline__ void gemm_mainloop(GemmRing<HALO>& R, const bf16_t* b
   };
 #pragma unroll
   for (int s = 0; s < GM_NS; ++s)
-    if (s < ns) issue(s);
-  arrive(0, min(GM_NS - 1, ns - 1));
-  tail(0);
+    if (s < ns) issue_stage<HALO>(R, s, baseA, baseB, ra, rb, wv, chunk, (s0 + s) * GM_BK, K);
+  arrive(0, ns > 1);
   StepFrags X, Y;
   read_step<HALO>(R, 0, 0, mi, ni, lane, X);
-  for (int s = 0; s < ns; ++s) {
+  // one stage; with COPY, slot s % 3 is refilled with stage s + 3 under the
+  // products of (s, 1)
+  auto body = [&](int s, auto copy) {
     read_step<HALO>(R, s % GM_NS, 1, mi, ni, lane, Y);
     __builtin_amdgcn_sched_barrier(0);
-    mma_step<HALO>(X, acc, acch);
+    mma_step<HALO, false>(X, acc, acch, R, 0, baseA, baseB, ra, rb, wv, 0u);
     __builtin_amdgcn_sched_barrier(0);
     if (s + 1 < ns) {
-      arrive(s + 1, min(s + GM_NS - 1, ns - 1));
-      if (s + GM_NS < ns) issue(s + GM_NS);
-      tail(s + 1);
+      arrive(s + 1, s + 2 < ns);
       read_step<HALO>(R, (s + 1) % GM_NS, 0, mi, ni, lane, X);
     }
     __builtin_amdgcn_sched_barrier(0);
-    mma_step<HALO>(Y, acc, acch);
-  }
+    mma_step<HALO, decltype(copy)::value>(Y, acc, acch, R, s % GM_NS, baseA, baseB, ra, rb, wv,
+                                          decltype(copy)::value ? kbyte(s + GM_NS) : 0u);
+  };
+  int s = 0;
+  for (; s + GM_NS < ns; ++s) body(s, std::true_type{});
+  for (; s < ns; ++s) body(s, std::false_type{});
 }
 
 // Tile order.  The eight accelerator dies receive workgroups round-robin and
