@@ -1379,7 +1379,12 @@ __global__ __launch_bounds__(512) void k_fwd_dual(Shape s, FwdIn in, PrepBufs p,
         }
         sm.Us[rt][l] = u;
       }
-      wait_vmcnt_rt(more ? Dma::N_KC + Dma::N_Q : 0);  // K^T, c_e, gamma^C and M have landed
+      // K^T, c_e, gamma^C and M have landed (immediate counts: a wait with a
+      // count known only at run time costs a chain of scalar branches)
+      if (more)
+        wait_vmcnt<Dma::N_KC + Dma::N_Q>();
+      else
+        wait_vmcnt<0>();
       __syncthreads();  // B2
       if (more) {  // Tu, the V tile and beta are free
         Dma::tu(sm, p, ch + 1);
@@ -1442,7 +1447,12 @@ __global__ __launch_bounds__(512) void k_fwd_dual(Shape s, FwdIn in, PrepBufs p,
         }
       // K, Q, a_e and b_e of the next chunk have landed (the Tu, V and beta
       // copies were issued after them)
-      if (more) wait_vmcnt_rt(Dma::N_TU + 1 + (sbeta ? 1 : 0));
+      if (more) {
+        if (sbeta)
+          wait_vmcnt<Dma::N_TU + 2>();
+        else
+          wait_vmcnt<Dma::N_TU + 1>();
+      }
     }
 
     if (s_final) {
