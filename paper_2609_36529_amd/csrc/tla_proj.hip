@@ -182,28 +182,27 @@ __device__ __forceinline__ void stage_copy(GemmRing<HALO>& R, int slot, const bf
 
 // The products of one step: the wave's 4 x 2 tiles of 32 x 32 and, with a
 // halo, its two halo tiles of 16 x 16 (rows 0..15, columns 16 (4 ni + 2 mi +
-// hh)).  With COPY, the copies of a later stage into ring slot `slot` are
-// issued one after each MFMA (a copy instruction holds up the wave that
+// hh)).  Copies C0 .. C1 - 1 of a later stage into ring slot `slot` are
+// issued spread over the 16 MFMAs (a copy instruction holds up the wave that
 // issues it; between products that time overlaps the matrix core's work).
-template <int HALO, bool COPY>
+template <int HALO, int C0, int C1>
 __device__ __forceinline__ void mma_step(const StepFrags& F, f32x16 (&acc)[4][2], f32x4 (&acch)[2],
                                          GemmRing<HALO>& R, int slot, const bf16_t* baseA,
                                          const bf16_t* baseB,
                                          const uint32_t (&ra)[GemmRing<HALO>::MA],
                                          const uint32_t (&rb)[GemmRing<HALO>::MB], int wv,
                                          uint32_t kb) {
-  typedef GemmRing<HALO> RG;
-  constexpr int NC = RG::MA + RG::MB;
   static_for<0, 16>([&](auto m) {
-    constexpr int h = decltype(m)::value / 8, i = (decltype(m)::value / 2) % 4, j = decltype(m)::value % 2;
+    constexpr int M = decltype(m)::value, h = M / 8, i = (M / 2) % 4, j = M % 2;
     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(F.a[h][i], F.b[h][j], acc[i][j], 0, 0, 0);
-    if constexpr (COPY && decltype(m)::value < NC) {
-      stage_copy<HALO, decltype(m)::value>(R, slot, baseA, baseB, ra, rb, wv, kb);
-      __builtin_amdgcn_sched_barrier(0);
-    }
+    static_for<C0, C1>([&](auto c) {
+      constexpr int C = decltype(c)::value;
+      if constexpr ((C - C0) * 16 / (C1 - C0) == M) {  // copy C after product M
+        stage_copy<HALO, C>(R, slot, baseA, baseB, ra, rb, wv, kb);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    });
   });
-  if constexpr (COPY && NC > 16)
-    static_for<16, NC>([&](auto c) { stage_copy<HALO, decltype(c)::value>(R, slot, baseA, baseB, ra, rb, wv, kb); });
   if constexpr (HALO > 0) {
     acch[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(F.ha, F.hb[0], acch[0], 0, 0, 0);
     acch[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(F.ha, F.hb[1], acch[1], 0, 0, 0);
@@ -220,7 +219,8 @@ __device__ __forceinline__ void mma_step(const StepFrags& F, f32x16 (&acc)[4][2]
 // them visible (the barrier waits for the wave's shared-memory reads, not
 // for its copies); it also certifies that every wave has read stage s into
 // registers, so slot s % 3 is refilled with stage s + 3 (copies run two
-// stages ahead), its copies interleaved with the products of (s, 1).  The
+// stages ahead): its first CS copies under the products of (s, 1), the
+// rest under those of (s + 1, 0), all before the wait for stage s + 2.  The
 // waits count copies with immediates: in the steady state one stage's
 // copies may stay in flight (counted as the fewest any wave issues, so a
 // wave that issues one more waits a little longer), otherwise none.  A
@@ -235,7 +235,8 @@ __device__ __forceinline__ void gemm_mainloop(GemmRing<HALO>& R, const bf16_t* b
   typedef GemmRing<HALO> RG;
   static_assert(GM_NS == 3, "the waits below assume one stage in flight beyond the next");
   constexpr int MINPER = RG::NBA / 4 + RG::MB;  // copies per stage of the wave with the fewest
-  static_assert(MINPER <= 63, "vmcnt range");
+  constexpr int NC = RG::MA + RG::MB, CS = 8;   // copies per stage (at most); the first CS early
+  static_assert(MINPER <= 63 && CS < NC, "copy split");
   const int wv = wave_id(), lane = lane_id();
   const int mi = wv >> 1, ni = wv & 1;
   const int chunk = copy_chunk(wv, lane);
@@ -263,24 +264,33 @@ __device__ __forceinline__ void gemm_mainloop(GemmRing<HALO>& R, const bf16_t* b
   arrive(0, ns > 1);
   StepFrags X, Y;
   read_step<HALO>(R, 0, 0, mi, ni, lane, X);
-  // one stage; with COPY, slot s % 3 is refilled with stage s + 3 under the
-  // products of (s, 1)
-  auto body = [&](int s, auto copy) {
+  // one stage: XC adds the late copies of stage s + 2 under (s, 0), YC the
+  // early copies of stage s + 3 under (s, 1)
+  auto body = [&](int s, auto xc, auto yc) {
+    constexpr bool XC = decltype(xc)::value, YC = decltype(yc)::value;
     read_step<HALO>(R, s % GM_NS, 1, mi, ni, lane, Y);
     __builtin_amdgcn_sched_barrier(0);
-    mma_step<HALO, false>(X, acc, acch, R, 0, baseA, baseB, ra, rb, wv, 0u);
+    mma_step<HALO, CS, XC ? NC : CS>(X, acc, acch, R, (s + 2) % GM_NS, baseA, baseB, ra, rb, wv,
+                                     XC ? kbyte(s + 2) : 0u);
     __builtin_amdgcn_sched_barrier(0);
     if (s + 1 < ns) {
       arrive(s + 1, s + 2 < ns);
       read_step<HALO>(R, (s + 1) % GM_NS, 0, mi, ni, lane, X);
     }
     __builtin_amdgcn_sched_barrier(0);
-    mma_step<HALO, decltype(copy)::value>(Y, acc, acch, R, s % GM_NS, baseA, baseB, ra, rb, wv,
-                                          decltype(copy)::value ? kbyte(s + GM_NS) : 0u);
+    mma_step<HALO, 0, YC ? CS : 0>(Y, acc, acch, R, s % GM_NS, baseA, baseB, ra, rb, wv,
+                                   YC ? kbyte(s + GM_NS) : 0u);
   };
-  int s = 0;
-  for (; s + GM_NS < ns; ++s) body(s, std::true_type{});
-  for (; s < ns; ++s) body(s, std::false_type{});
+  typedef std::true_type Y_;
+  typedef std::false_type N_;
+  if (ns > GM_NS)
+    body(0, N_{}, Y_{});  // stage 2 came whole with the prologue
+  else
+    body(0, N_{}, N_{});
+  int s = 1;
+  for (; s + GM_NS < ns; ++s) body(s, Y_{}, Y_{});
+  if (s + GM_NS - 1 < ns) body(s++, Y_{}, N_{});  // the last stage's late copies
+  for (; s < ns; ++s) body(s, N_{}, N_{});
 }
 
 // Tile order.  The eight accelerator dies receive workgroups round-robin and
