@@ -8,26 +8,27 @@
 // training forward may still write it (bf16) for the backward.
 //
 // GEMM tiles: bf16 operands, fp32 accumulation on v_mfma_f32_32x32x16_bf16.
-// A workgroup of four waves (one per SIMD) computes 256 rows by 128 columns;
-// wave (mi, ni) owns rows 128 mi .. 128 mi + 127 and columns 64 ni .. 64 ni
-// + 63 (4 x 2 accumulator tiles of 32 x 32; per 32-deep step 8 + 4 fragment
-// reads feed 16 MFMAs).  The 32 x 32 shape matters with one wave per SIMD:
+// A workgroup of eight waves (two per SIMD) computes 256 rows by 128 columns;
+// wave (mi, ni) owns rows 64 mi .. 64 mi + 63 and columns 64 ni .. 64 ni + 63
+// (2 x 2 accumulator tiles of 32 x 32; per 32-deep step 4 + 4 fragment reads
+// feed 8 MFMAs).  The 32 x 32 shape and the second wave per SIMD both matter:
 // measured on the device, back-to-back 16x16x32 MFMAs from a single wave
-// reach about 59% of the matrix cores' rate, 32x32x16 ones 97%.  The
-// projection tile is 256 consecutive tokens of one batch row plus 16 rows
-// above them, whose last W - 1 the convolution reads: recomputed rather than
-// taken from the neighbouring tile (6% more MFMA work, no wait between
-// workgroups) on 16x16x32 MFMAs, each wave taking two of the halo's eight
-// 16-column tiles.  The
-// contraction runs in stages of 64 through a ring of three shared-memory
-// buffers, filled by direct global-to-LDS copies two stages ahead.  Rows past
-// an operand's end are copied from clamped addresses and never stored; a
-// partial last stage has its chunks past the contraction length zeroed in
-// shared memory.  LDS rows are XOR-swizzled in 16-byte chunks, so fragment
-// reads are free of bank conflicts while whole 1 KiB copies still fill them.
+// reach about 59% of the matrix cores' rate, 32x32x16 ones 95-97%, and a
+// copy instruction holds up the wave that issues it, which the SIMD's other
+// wave covers.  The projection tile is 256 consecutive tokens of one batch
+// row plus 16 rows above them, whose last W - 1 the convolution reads:
+// recomputed rather than taken from the neighbouring tile (6% more MFMA
+// work, no wait between workgroups) on 16x16x32 MFMAs, one 16-column halo
+// tile per wave.  The contraction runs in stages of 64 through a ring of
+// three shared-memory buffers, filled by direct global-to-LDS copies two
+// stages ahead.  Rows past an operand's end are copied from clamped
+// addresses and never stored; a partial last stage has its chunks past the
+// contraction length zeroed in shared memory.  LDS rows are XOR-swizzled in
+// 16-byte chunks, so fragment reads are free of bank conflicts while whole
+// 1 KiB copies still fill them.
 //
 // Projection epilogue: the fp32 accumulators go through shared memory (the
-// stage buffers' space); a thread then walks a run of 16 tokens for eight
+// stage buffers' space); a thread then walks a run of 8 tokens for eight
 // channels, keeping the last W - 1 inputs in registers, applies the taps, the
 // activation and the norm (a sum over the K / 8 or E / 8 lanes of the head,
 // all inside one 16-lane row group since a tile holds whole heads), and writes
@@ -42,7 +43,8 @@
 
 namespace tla {
 
-constexpr int GM_NTHR = 256;  // four waves
+constexpr int GM_NW = 8;      // waves: two per SIMD, 4 (rows) x 2 (columns)
+constexpr int GM_NTHR = GM_NW * 64;
 constexpr int GM_BM = 256;    // rows of a tile (tokens of a projection tile)
 constexpr int GM_BN = 128;    // columns of a tile (channels of a projection tile)
 constexpr int GM_BK = 64;     // contraction depth of a stage
@@ -58,10 +60,10 @@ struct GemmRing {
   typedef SwzTile<bf16_t, GM_BN, GM_BK> TB;
   TA a[GM_NS];
   TB b[GM_NS];
-  // 1 KiB copies per stage, and per wave (round-robin over the four waves)
+  // 1 KiB copies per stage, and per wave (round-robin over the eight waves)
   static constexpr int NBA = TA::NCHK / 64, NBB = TB::NCHK / 64;
-  static constexpr int MA = (NBA + 3) / 4, MB = NBB / 4;
-  static_assert(TA::NCHK % 64 == 0 && NBB % 4 == 0, "whole 1 KiB copies");
+  static constexpr int MA = (NBA + GM_NW - 1) / GM_NW, MB = NBB / GM_NW;
+  static_assert(TA::NCHK % 64 == 0 && NBB % GM_NW == 0, "whole 1 KiB copies");
 };
 
 struct ProjSmem {
@@ -75,11 +77,13 @@ static_assert(sizeof(GemmRing<0>) <= 160 * 1024, "GEMM ring exceeds shared memor
 
 // The logical chunk a lane copies is the same in every 1 KiB block of a wave:
 // physical chunk p = 64 blk + lane holds row r = p / 8, chunk (p % 8) ^ sw(r)
-// with sw(r) = (r / 2) % 8, and blk = wave + 4 i keeps (r / 2) % 8 fixed.
+// with sw(r) = (r / 2) % 8, and blk = wave + 8 i keeps (r / 2) % 8 fixed.
 __device__ __forceinline__ int copy_chunk(int wv, int lane) {
   return (lane & 7) ^ ((4 * (wv & 1) + (lane >> 4)) & 7);
 }
-__device__ __forceinline__ int copy_row(int wv, int i, int lane) { return 8 * (wv + 4 * i) + (lane >> 3); }
+__device__ __forceinline__ int copy_row(int wv, int i, int lane) {
+  return 8 * (wv + GM_NW * i) + (lane >> 3);
+}
 
 // Issue the copies of the stage starting at contraction index k0 into ring
 // slot `slot`; ra / rb are the lanes' row byte offsets from the bases.
@@ -94,12 +98,12 @@ __device__ __forceinline__ void issue_stage(GemmRing<HALO>& R, int slot, const b
   const uint32_t la = lds_addr(R.a[slot].d), lb = lds_addr(R.b[slot].d);
 #pragma unroll
   for (int i = 0; i < RG::MA; ++i) {
-    const int blk = wv + 4 * i;
-    if (RG::NBA % 4 != 0 && blk >= RG::NBA) break;  // wave-uniform
+    const int blk = wv + GM_NW * i;
+    if (RG::NBA % GM_NW != 0 && blk >= RG::NBA) break;  // wave-uniform
     lds_dma<16>(baseA, ra[i] + kb, la + 1024 * blk);
   }
 #pragma unroll
-  for (int i = 0; i < RG::MB; ++i) lds_dma<16>(baseB, rb[i] + kb, lb + 1024 * (wv + 4 * i));
+  for (int i = 0; i < RG::MB; ++i) lds_dma<16>(baseB, rb[i] + kb, lb + 1024 * (wv + GM_NW * i));
 }
 
 // Zero the chunks at contraction index K and beyond of a partial stage.
@@ -119,16 +123,18 @@ __device__ __forceinline__ void zero_tail(GemmRing<HALO>& R, int slot, int k0, i
 }
 
 // A wave's operand fragments of one 32-deep step, as two 16-deep halves of
-// v_mfma_f32_32x32x16_bf16 operands: its 4 row tiles and 2 column tiles of 32
+// v_mfma_f32_32x32x16_bf16 operands: its 2 row tiles and 2 column tiles of 32
 // (lane l holds row / column l % 32, contraction 8 (l / 32) .. + 7 of the
-// half); with a halo, the halo's 16-row A fragment and the B fragments of
-// the wave's two halo column tiles of 16, for v_mfma_f32_16x16x32_bf16 (lane
-// l holds row / column l % 16, contraction 8 (l / 16) .. + 7).
+// half); with a halo, the halo's 16-row A fragment and the B fragment of the
+// wave's halo column tile of 16, for v_mfma_f32_16x16x32_bf16 (lane l holds
+// row / column l % 16, contraction 8 (l / 16) .. + 7).
 struct StepFrags {
-  bf16x8 a[2][4], b[2][2], ha, hb[2];
+  bf16x8 a[2][2], b[2][2], ha, hb;
 };
 
-// Read step `st` (0 or 1) of the stage in ring slot `slot` into F.
+// Read step `st` (0 or 1) of the stage in ring slot `slot` into F.  Wave (mi,
+// ni) owns rows 64 mi .. 64 mi + 63 and columns 64 ni .. 64 ni + 63 of the
+// tile, and the halo's columns 16 (4 ni + mi) .. + 15.
 template <int HALO>
 __device__ __forceinline__ void read_step(const GemmRing<HALO>& R, int slot, int st, int mi, int ni,
                                           int lane, StepFrags& F) {
@@ -137,17 +143,15 @@ __device__ __forceinline__ void read_step(const GemmRing<HALO>& R, int slot, int
   for (int h = 0; h < 2; ++h) {
     const int col = 8 * (4 * st + 2 * h + (lane >> 5));
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      F.a[h][i] = *(const bf16x8*)R.a[slot].at(HALO + 128 * mi + 32 * i + r32, col);
+    for (int i = 0; i < 2; ++i)
+      F.a[h][i] = *(const bf16x8*)R.a[slot].at(HALO + 64 * mi + 32 * i + r32, col);
 #pragma unroll
     for (int j = 0; j < 2; ++j) F.b[h][j] = *(const bf16x8*)R.b[slot].at(64 * ni + 32 * j + r32, col);
   }
   if constexpr (HALO > 0) {
     const int r16 = lane & 15, col = 8 * (4 * st + (lane >> 4));
     F.ha = *(const bf16x8*)R.a[slot].at(r16, col);
-#pragma unroll
-    for (int hh = 0; hh < 2; ++hh)
-      F.hb[hh] = *(const bf16x8*)R.b[slot].at(16 * (4 * ni + 2 * mi + hh) + r16, col);
+    F.hb = *(const bf16x8*)R.b[slot].at(16 * (4 * ni + mi) + r16, col);
   }
 }
 
@@ -172,41 +176,40 @@ __device__ __forceinline__ void stage_copy(GemmRing<HALO>& R, int slot, const bf
                                            uint32_t kb) {
   typedef GemmRing<HALO> RG;
   if constexpr (C < RG::MA) {
-    const int blk = wv + 4 * C;
-    if (RG::NBA % 4 != 0 && blk >= RG::NBA) return;  // wave-uniform
+    const int blk = wv + GM_NW * C;
+    if (RG::NBA % GM_NW != 0 && blk >= RG::NBA) return;  // wave-uniform
     lds_dma<16>(baseA, ra[C] + kb, lds_addr(R.a[slot].d) + 1024 * blk);
   } else {
-    lds_dma<16>(baseB, rb[C - RG::MA] + kb, lds_addr(R.b[slot].d) + 1024 * (wv + 4 * (C - RG::MA)));
+    lds_dma<16>(baseB, rb[C - RG::MA] + kb,
+                lds_addr(R.b[slot].d) + 1024 * (wv + GM_NW * (C - RG::MA)));
   }
 }
 
-// The products of one step: the wave's 4 x 2 tiles of 32 x 32 and, with a
-// halo, its two halo tiles of 16 x 16 (rows 0..15, columns 16 (4 ni + 2 mi +
-// hh)).  Copies C0 .. C1 - 1 of a later stage into ring slot `slot` are
-// issued spread over the 16 MFMAs (a copy instruction holds up the wave that
-// issues it; between products that time overlaps the matrix core's work).
+// The products of one step: the wave's 2 x 2 tiles of 32 x 32 and, with a
+// halo, its halo tile of 16 x 16 (rows 0..15, columns 16 (4 ni + mi)).
+// Copies C0 .. C1 - 1 of a later stage into ring slot `slot` are issued
+// spread over the 8 MFMAs (a copy instruction holds up the wave that issues
+// it for about 85 cycles; between products, and with the SIMD's other wave
+// issuing its own, that time overlaps the matrix core's work).
 template <int HALO, int C0, int C1>
-__device__ __forceinline__ void mma_step(const StepFrags& F, f32x16 (&acc)[4][2], f32x4 (&acch)[2],
+__device__ __forceinline__ void mma_step(const StepFrags& F, f32x16 (&acc)[2][2], f32x4& acch,
                                          GemmRing<HALO>& R, int slot, const bf16_t* baseA,
                                          const bf16_t* baseB,
                                          const uint32_t (&ra)[GemmRing<HALO>::MA],
                                          const uint32_t (&rb)[GemmRing<HALO>::MB], int wv,
                                          uint32_t kb) {
-  static_for<0, 16>([&](auto m) {
-    constexpr int M = decltype(m)::value, h = M / 8, i = (M / 2) % 4, j = M % 2;
+  static_for<0, 8>([&](auto m) {
+    constexpr int M = decltype(m)::value, h = M / 4, i = (M / 2) % 2, j = M % 2;
     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(F.a[h][i], F.b[h][j], acc[i][j], 0, 0, 0);
     static_for<C0, C1>([&](auto c) {
       constexpr int C = decltype(c)::value;
-      if constexpr ((C - C0) * 16 / (C1 - C0) == M) {  // copy C after product M
+      if constexpr ((C - C0) * 8 / (C1 - C0) == M) {  // copy C after product M
         stage_copy<HALO, C>(R, slot, baseA, baseB, ra, rb, wv, kb);
         __builtin_amdgcn_sched_barrier(0);
       }
     });
   });
-  if constexpr (HALO > 0) {
-    acch[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(F.ha, F.hb[0], acch[0], 0, 0, 0);
-    acch[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(F.ha, F.hb[1], acch[1], 0, 0, 0);
-  }
+  if constexpr (HALO > 0) acch = __builtin_amdgcn_mfma_f32_16x16x32_bf16(F.ha, F.hb, acch, 0, 0, 0);
 }
 
 // The contraction over stages [s0, s1) of 64 (K the full length), software
@@ -230,12 +233,12 @@ __device__ __forceinline__ void gemm_mainloop(GemmRing<HALO>& R, const bf16_t* b
                                               const bf16_t* baseB,
                                               const uint32_t (&ra)[GemmRing<HALO>::MA],
                                               const uint32_t (&rb)[GemmRing<HALO>::MB], int K,
-                                              int s0, int s1, f32x16 (&acc)[4][2],
-                                              f32x4 (&acch)[2]) {
+                                              int s0, int s1, f32x16 (&acc)[2][2],
+                                              f32x4& acch) {
   typedef GemmRing<HALO> RG;
   static_assert(GM_NS == 3, "the waits below assume one stage in flight beyond the next");
-  constexpr int MINPER = RG::NBA / 4 + RG::MB;  // copies per stage of the wave with the fewest
-  constexpr int NC = RG::MA + RG::MB, CS = 8;   // copies per stage (at most); the first CS early
+  constexpr int MINPER = RG::NBA / GM_NW + RG::MB;  // copies per stage of the wave with the fewest
+  constexpr int NC = RG::MA + RG::MB, CS = 4;       // copies per stage (at most); the first CS early
   static_assert(MINPER <= 63 && CS < NC, "copy split");
   const int wv = wave_id(), lane = lane_id();
   const int mi = wv >> 1, ni = wv & 1;
@@ -342,15 +345,14 @@ __global__ __launch_bounds__(GM_NTHR) void k_proj_in(ProjArgs a, const bf16_t* _
     const int c = min(n0 + copy_row(wv, i, lane), a.Ctot - 1);
     rb[i] = (uint32_t)(c - n0) * (uint32_t)a.Dm * 2u;
   }
-  f32x16 acc[4][2];
-  f32x4 acch[2];
+  f32x16 acc[2][2];
+  f32x4 acch = zero4();
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-  acch[0] = acch[1] = zero4();
   gemm_mainloop<PJ_HALO>(sm.ring, baseA, baseB, ra, rb, a.Dm, 0, (a.Dm + GM_BK - 1) / GM_BK, acc,
                          acch);
 
@@ -362,22 +364,21 @@ __global__ __launch_bounds__(GM_NTHR) void k_proj_in(ProjArgs a, const bf16_t* _
     // row 4 (l / 16) + r, column l % 16
     const int mi = wv >> 1, ni = wv & 1;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
       for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int r = 0; r < 16; ++r)
-          sm.y[PJ_HALO + 128 * mi + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)]
+          sm.y[PJ_HALO + 64 * mi + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)]
               [64 * ni + 32 * j + (lane & 31)] = acc[i][j][r];
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-        sm.y[4 * (lane >> 4) + r][16 * (4 * ni + 2 * mi + h) + (lane & 15)] = acch[h][r];
+    for (int r = 0; r < 4; ++r)
+      sm.y[4 * (lane >> 4) + r][16 * (4 * ni + mi) + (lane & 15)] = acch[r];
   }
   __syncthreads();
 
-  // epilogue: thread = 8 channels (16 lanes per token) x a run of 16 tokens
+  // epilogue: thread = 8 channels (16 lanes per token) x a run of PJ_RUN tokens
+  constexpr int PJ_RUN = GM_BM / (GM_NTHR / 16);
   const int cl = threadIdx.x & 15, run = threadIdx.x >> 4;
   const int c = n0 + 8 * cl;
   const bool on_c = c < a.Ctot;
@@ -397,7 +398,7 @@ __global__ __launch_bounds__(GM_NTHR) void k_proj_in(ProjArgs a, const bf16_t* _
       wt[j][4 + i] = x1[i];
     }
   }
-  const int r0 = 16 * run;
+  const int r0 = PJ_RUN * run;
   float hist[W > 1 ? W - 1 : 1][8];
 #pragma unroll
   for (int h = 0; h < W - 1; ++h) {
@@ -407,7 +408,7 @@ __global__ __launch_bounds__(GM_NTHR) void k_proj_in(ProjArgs a, const bf16_t* _
     for (int i = 0; i < 8; ++i) hist[h][i] = live ? yr[i] : 0.f;
   }
   bf16_t* yout = ysave ? ysave + (size_t)b * a.T * a.Ctot + c : nullptr;
-  for (int rr = 0; rr < 16; ++rr) {
+  for (int rr = 0; rr < PJ_RUN; ++rr) {
     const int t = t0 + r0 + rr;
     float x[8], z[8], r[8], ss = 0.f;
     const float* yr = &sm.y[PJ_HALO + r0 + rr][8 * cl];
@@ -488,15 +489,14 @@ __global__ __launch_bounds__(GM_NTHR) void k_gemm_nt(long long M, long long N, i
     rb[i] = (uint32_t)(min(n0 + copy_row(wv, i, lane), N - 1) - n0) * (uint32_t)K * 2u;
   const int nst = (K + GM_BK - 1) / GM_BK, z = blockIdx.y;
   const int s0 = (int)((long long)nst * z / splits), s1 = (int)((long long)nst * (z + 1) / splits);
-  f32x16 acc[4][2];
-  f32x4 acch[2];
+  f32x16 acc[2][2];
+  f32x4 acch = zero4();
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-  acch[0] = acch[1] = zero4();
   gemm_mainloop<0>(R, baseA, baseB, ra, rb, K, s0, s1, acc, acch);
 
   // registers 4 q .. 4 q + 3 of lane l in tile (i, j) hold rows 8 q + 4 (l / 32)
@@ -505,14 +505,14 @@ __global__ __launch_bounds__(GM_NTHR) void k_gemm_nt(long long M, long long N, i
   // 4 ((l % 32) / 4) .. + 3
   const int mi = wv >> 1, ni = wv & 1, n = lane & 31;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const f32x4 x = quad_transpose(f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
                                            acc[i][j][4 * q + 3]}, n);
-      const long long row = m0 + 128 * mi + 32 * i + 8 * q + 4 * (lane >> 5) + (n & 3);
+      const long long row = m0 + 64 * mi + 32 * i + 8 * q + 4 * (lane >> 5) + (n & 3);
       const long long col = n0 + 64 * ni + 32 * j + 4 * (n >> 2);
       if (row < M && col < N) {  // N is a multiple of 4
         if (splits > 1) {
