@@ -27,15 +27,24 @@ __device__ __forceinline__ ConvLane conv_lane(const A& a, int c) {
   return {4, c - e3, a.E, a.E / 8};
 }
 
-// sum over the lpr aligned lanes of the caller's group (lpr a power of two
-// dividing 64; every lane of the wave takes part in every exchange)
+// sum over the lpr aligned lanes of the caller's group (lpr 0 or a power of
+// two dividing 64, the same for every lane of a group; every lane of the wave
+// takes part in every exchange).  Within a 16-lane row the partial sums of 2,
+// 4, 8 and 16 lanes come from DPP moves (no shared-memory round trip), and
+// each lane keeps the one of its group's size; groups of 32 or 64 lanes,
+// when the wave has any, add the cross-row exchanges.
 __device__ __forceinline__ float lane_group_sum(float x, int lpr) {
-#pragma unroll
-  for (int m = 1; m < 64; m <<= 1) {
-    const float y = __shfl_xor(x, m, 64);
-    if (m < lpr) x += y;
+  const float s2 = x + dpp_f<0xB1>(x);      // quad_perm [1,0,3,2]
+  const float s4 = s2 + dpp_f<0x4E>(s2);    // quad_perm [2,3,0,1]
+  const float s8 = s4 + dpp_f<0x141>(s4);   // row_half_mirror
+  const float s16 = s8 + dpp_f<0x140>(s8);  // row_mirror
+  float r = lpr >= 16 ? s16 : lpr >= 8 ? s8 : lpr >= 4 ? s4 : lpr >= 2 ? s2 : x;
+  if (__builtin_amdgcn_ballot_w64(lpr >= 32)) {  // uniform over the wave
+    const float s32 = s16 + __shfl_xor(s16, 16, 64);
+    const float s64 = s32 + __shfl_xor(s32, 32, 64);
+    r = lpr >= 64 ? s64 : lpr >= 32 ? s32 : r;
   }
-  return x;
+  return r;
 }
 
 template <typename P>
