@@ -594,7 +594,7 @@ def main():
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the operator's work shards over batch, heads "
               "and value tiles with no exchange, so per-GPU throughput at N GPUs is the N=1 "
-              "figure; multi-GPU runs are not part of this build.", file=sys.stderr)
+              "figure; it takes no multi-GPU runs.", file=sys.stderr)
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration()
