@@ -516,6 +516,24 @@ def proj_bench(steps, warmup):
     flop_fwd = 2.0 * n * C * Dm
     tf_f = flop_fwd / (kern["proj_in_fwd"] * 1e-3) / 1e12
     tf_g = 2 * flop_fwd / (kern["proj_gemm"] * 1e-3) / 1e12
+
+    # context only: the library GEMM that PyTorch calls for the same three
+    # products (plain 2-D products of resident bf16 tensors, no epilogue)
+    def lib_gemm_ms(a, b_t):
+        for _ in range(5):
+            torch.matmul(a, b_t)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            torch.matmul(a, b_t)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+    u2, dy2 = u.reshape(n, Dm), torch.randn(n, C, generator=gen).to(torch.bfloat16).cuda()
+    lib = {"u Wp^T (16384 x 3200 x 2048)": lib_gemm_ms(u2, Wp.t().contiguous()),
+           "dy Wp (16384 x 2048 x 3200)": lib_gemm_ms(dy2, Wp),
+           "dy^T u (3200 x 2048 x 16384)": lib_gemm_ms(dy2.t(), u2)}
+    lib = {k: round(v, 4) for k, v in lib.items()}
     print(json.dumps({
         "metric": "input projection fwd+bwd tokens/s, B4 T4096 d_model 2048 H8 K=V=128 E=8 W4",
         "value": round(n / elapsed, 1), "unit": "tokens/s", "n_gpus": 1, "steps": steps,
@@ -527,7 +545,8 @@ def proj_bench(steps, warmup):
         "roofline": {"bound": "mfma", "achieved": round(tf_f, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(tf_f / PEAK_BF16_TFLOPS, 4), "kernel": "proj_in_fwd",
                      "backward_gemm_tflops": round(tf_g, 1),
-                     "backward_gemm_frac": round(tf_g / PEAK_BF16_TFLOPS, 4)}}),
+                     "backward_gemm_frac": round(tf_g / PEAK_BF16_TFLOPS, 4)},
+        "library_gemm_ms_context": lib}),
           flush=True)
 
 
