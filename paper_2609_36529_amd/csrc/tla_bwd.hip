@@ -1101,16 +1101,19 @@ __global__ __launch_bounds__(CHUNK_NTHR) void k_bwd_chunk(Shape s, FwdIn in, con
 
   // ---- phase 0: per-position vectors, Q and K rows, in-chunk cumulative
   // log-gates.  Every global load of the phase is issued before the first of
-  // their results is stored (one memory latency instead of one per array).
+  // their results is stored (one memory latency instead of one per array),
+  // and so are the loads of dv, which needs nothing the kernel computes.
   constexpr int NQE = (C * E + NTHR - 1) / NTHR;             // q2, k2 entries per thread
   constexpr int IT = STAGE_QK ? (C * KD / 8 + NTHR - 1) / NTHR : 1;  // Q, K pieces
   constexpr int NNV = (C * C / 4 + NTHR - 1) / NTHR;        // (I + L)^{-1} pieces
   constexpr int NGE = (E + NW - 1) / NW;                     // slices per wave (g)
+  constexpr int IDV = (C * 128 / 8 + NTHR - 1) / NTHR;      // 8-value pieces of dv
   const bool have_ninv = gdn && p.ninv != nullptr;
   float q2v[NQE], k2v[NQE], bv = 0.f;
   Raw8<T> qv[IT], kv[IT];
   f32x4 nv[NNV];
   double gv[NGE];
+  f32x4 dvx[IDV][2];
 #pragma unroll
   for (int i = 0; i < NQE; ++i) {
     const int idx = tid + NTHR * i, r = idx / E, e = idx % E, t = t0 + r;
@@ -1150,6 +1153,18 @@ __global__ __launch_bounds__(CHUNK_NTHR) void k_bwd_chunk(Shape s, FwdIn in, con
   for (int i = 0; i < NGE; ++i) {
     const int e = w + NW * i, t = t0 + l;
     gv[i] = (e < E && l < C && t < s.T) ? (double)in.g[eoff + (size_t)t * erow + e] : 0.0;
+  }
+  // rows of dv = Tu^T dU = -dW (GDN) or diag(beta) dU (sGLA), 8 values a piece
+#pragma unroll
+  for (int it = 0; it < IDV; ++it) {
+    const int idx = tid + NTHR * it, n8 = V / 8;
+    const int r = idx / n8, c = 8 * (idx % n8);
+    dvx[it][0] = dvx[it][1] = zero4();
+    if (idx < C * n8 && t0 + r < s.T) {
+      const float* src = (gdn ? dWg : dUg) + (size_t)r * V + c;
+      dvx[it][0] = *(const f32x4*)src;
+      dvx[it][1] = *(const f32x4*)(src + 4);
+    }
   }
   // ---- the stores
 #pragma unroll
@@ -1193,6 +1208,18 @@ __global__ __launch_bounds__(CHUNK_NTHR) void k_bwd_chunk(Shape s, FwdIn in, con
     if (l < C) sm.G[l][e] = x;
   }
   __syncthreads();
+
+  // ---- dv = Tu^T dU = -dW (GDN) or diag(beta) dU (sGLA)
+#pragma unroll
+  for (int it = 0; it < IDV; ++it) {
+    const int idx = tid + NTHR * it, n8 = V / 8;
+    const int r = idx / n8, c = 8 * (idx % n8);
+    const int t = t0 + r;
+    if (idx >= C * n8 || t >= s.T) continue;
+    const float sc = gdn ? -1.f : sm.beta[r];
+    store8_out(dvv, ((tok0 + t) * s.H + h) * (size_t)V + c, sc * dvx[it][0], sc * dvx[it][1],
+               s.out_bf16);
+  }
 
   // Q / K rows as 8-element operands at columns [col, col + 8) (zero past KD or T)
   auto qrow8 = [&](int r, int col) -> Raw8<T> {
@@ -1611,34 +1638,6 @@ __global__ __launch_bounds__(CHUNK_NTHR) void k_bwd_chunk(Shape s, FwdIn in, con
     }
   }
 
-  // ---- dv = Tu^T dU = -dW (GDN) or diag(beta) dU (sGLA), 8 values per item
-  {
-    constexpr int IT = (C * 128 / 8 + NTHR - 1) / NTHR;
-    const int n8 = V / 8;
-    f32x4 x[IT][2];
-#pragma unroll
-    for (int it = 0; it < IT; ++it) {
-      const int idx = tid + NTHR * it;
-      const int r = idx / n8, c = 8 * (idx % n8);
-      x[it][0] = x[it][1] = zero4();
-      if (idx < C * n8 && t0 + r < s.T) {
-        const float* src = (gdn ? dWg : dUg) + (size_t)r * V + c;
-        x[it][0] = *(const f32x4*)src;
-        x[it][1] = *(const f32x4*)(src + 4);
-      }
-    }
-#pragma unroll
-    for (int it = 0; it < IT; ++it) {
-      const int idx = tid + NTHR * it;
-      const int r = idx / n8, c = 8 * (idx % n8);
-      const int t = t0 + r;
-      if (idx >= C * n8 || t >= s.T) continue;
-      const float sc = gdn ? -1.f : sm.beta[r];
-      store8_out(dvv, ((tok0 + t) * s.H + h) * (size_t)V + c, sc * x[it][0],
-                 sc * x[it][1], s.out_bf16);
-    }
-  }
-
   // ---- backward of the decayed Grams R, R'.  Per slice e (one wave), lane
   // tiles of (r, c) pairs, c <= r:  d = Gamma_e[r, c] = exp(G_r[e] - G_c[e]),
   //   aq2[r] = sum_c dR'[r,c] d k2_c,   ak2[r] = sum_c dR[r,c] d k2_c,
@@ -1647,6 +1646,22 @@ __global__ __launch_bounds__(CHUNK_NTHR) void k_bwd_chunk(Shape s, FwdIn in, con
   float* aq2s = &sm.dT[0][0];  // dA_kk is dead: its space holds the three sums
   float* ak2s = aq2s + C * E;
   float* acols = ak2s + C * E;
+  // the last phase's global operands go out now, under this one: the
+  // coefficient-vector gradients of (r, e) = (idx / E, idx % E) and dgamma^C
+  // of the wave's slices (used by lane C - 1)
+  float dcfv[NQE][3], dgcv[NGE];
+#pragma unroll
+  for (int i = 0; i < NQE; ++i) {
+    const int idx = tid + NTHR * i, r = idx / E, e = idx % E;
+#pragma unroll
+    for (int kind = 0; kind < 3; ++kind)
+      dcfv[i][kind] = idx < C * E ? dcf[(kind * E + e) * C + r] : 0.f;
+  }
+#pragma unroll
+  for (int i = 0; i < NGE; ++i) {
+    const int e = w + NW * i;
+    dgcv[i] = (e < E && l == C - 1) ? bb.dgC[(size_t)ch * E4 + e] : 0.f;
+  }
   __syncthreads();
   for (int e = w; e < E; e += NW) {
     float rowq[16], rowk[16], colacc[NT];
@@ -1718,12 +1733,14 @@ __global__ __launch_bounds__(CHUNK_NTHR) void k_bwd_chunk(Shape s, FwdIn in, con
 
   // ---- per (r, e): Gram terms and the coefficient vectors
   //   a = k2 gamma, b = q2 gamma, c = k2 gamma^C / gamma
-  for (int idx = tid; idx < C * E; idx += NTHR) {
+#pragma unroll
+  for (int i = 0; i < NQE; ++i) {
+    const int idx = tid + NTHR * i;
+    if (idx >= C * E) continue;
     const int r = idx / E, e = idx % E;
     const float aq2 = aq2s[idx], ak2 = ak2s[idx], acol = acols[idx];
     const float q2 = sm.q2[r][e], k2 = sm.k2[r][e];
-    const float da = dcf[(0 * E + e) * C + r], db = dcf[(1 * E + e) * C + r],
-                dc = dcf[(2 * E + e) * C + r];
+    const float da = dcfv[i][0], db = dcfv[i][1], dc = dcfv[i][2];
     const double G = sm.G[r][e], GC = sm.G[C - 1][e];
     const float gm = exp_nonpos((float)G), gt = exp_nonpos((float)(GC - G));
     sm.dG[r][e] = (q2 * aq2 + k2 * ak2) - acol * k2 + da * k2 * gm + db * q2 * gm - dc * k2 * gt;
@@ -1738,11 +1755,13 @@ __global__ __launch_bounds__(CHUNK_NTHR) void k_bwd_chunk(Shape s, FwdIn in, con
   __syncthreads();
   // dG at the chunk end gains sum_r dc c + gamma^C dgamma^C; then dg_j = sum_{r >= j} dG_r
   // (one wave per slice, lane r holds row r)
-  for (int e = w; e < E; e += NW) {
+#pragma unroll
+  for (int i = 0; i < NGE; ++i) {
+    const int e = w + NW * i;
+    if (e >= E) continue;  // wave-uniform
     const float tail = wave_sum(l < C ? acols[l * E + e] : 0.f);
     float x = (l < C) ? sm.dG[l][e] : 0.f;
-    if (l == C - 1)
-      x += tail + exp_nonpos((float)sm.G[C - 1][e]) * bb.dgC[(size_t)ch * E4 + e];
+    if (l == C - 1) x += tail + exp_nonpos((float)sm.G[C - 1][e]) * dgcv[i];
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
       const float y = __shfl_down(x, off, 64);
