@@ -3,11 +3,16 @@ depthwise convolution, SiLU on q, k, v, softplus on q', k', L2 normalisation
 of q, k, q', k'; section "Input projections", Alg. 2): tla_conv_in_fwd /
 tla_conv_in_bwd against the fp64 oracle.
 
-Tolerances.  fp32 outputs: max|err| / RMS(ref) <= 3e-5 per tensor (a few
-fp32 operations per value; the tap gradient sums at most a few hundred
-products per partial).  bf16 outputs are one rounding of an fp32 result:
-elementwise |err| <= 2^-8 |ref| + 1e-5 RMS(ref).  dw stays fp32 for both
-dtypes; at the full shape it sums 16384 tokens, so there it gets 1e-4."""
+Tolerances.  fp32 outputs and the tap gradient dw (fp32 for both dtypes):
+max|err| / RMS(ref) <= 1e-5 per tensor, the operator's fp32 bar.  A value
+is a W-tap sum, an activation and a division by the norm of its K or E
+entries (a sum of at most 128 squares, log2 128 + 1 roundings): a few tens
+of fp32 roundings at most, so the error is a few 1e-6 of RMS(ref)
+(measured at most 3.4e-6, including inputs scaled by 1e4 and eps = 0).  dw
+sums tokens in a fixed order, a few hundred products per partial and then
+the partials pairwise; at the full shape (16384 tokens) its measured error
+is 1.3e-6 of RMS(dw).  bf16 outputs are one rounding of an fp32 result:
+elementwise |err| <= 2^-8 |ref| + 1e-5 RMS(ref)."""
 import numpy as np
 import pytest
 import torch
@@ -17,7 +22,7 @@ import paper_2609_36529_amd as tla
 from helpers import rel_err
 
 pytestmark = pytest.mark.gpu
-TOL = 3e-5
+TOL = 1e-5
 NAMES = ("q", "k", "v", "q2", "k2")
 
 
@@ -128,4 +133,4 @@ def test_metric_shape_windows_and_determinism():
             assert within_bf16_rounding(f64(o[b, s:s + e - a]), ref[n][0, a:e]), (n, b, s)
         assert within_bf16_rounding(f64(dy[b, s:s + e - a]), rdy[0, a:e]), ("dy", b, s)
     _, rdw = oracle.conv_in_bwd(f64(y), f64(w), H, K, V, E, 1e-6, dict(zip(NAMES, (f64(g) for g in grads))))
-    assert rel_err(f64(dw), rdw) <= 1e-4
+    assert rel_err(f64(dw), rdw) <= TOL

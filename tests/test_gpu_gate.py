@@ -1,6 +1,15 @@
 """GPU parity of the mixer's output side (RMSNorm times a sigmoid gate, the
 last line of the mixer in Alg. 2): tla_out_gate_fwd / tla_out_gate_bwd
-against the fp64 oracle, max|err| / RMS(ref) per tensor."""
+against the fp64 oracle, max|err| / RMS(ref) per tensor.
+
+Tolerance (fp32 outputs and dw, both dtypes): 1e-5, the operator's fp32
+bar.  Each output element is a chain of about ten fp32 roundings (2^-24
+each) after the row's mean square, a sum of V <= 256 squares reduced over
+a lane group (log2 V + 1 roundings); with Gaussian inputs max|ref| is a few
+RMS(ref), so the expected max|err| / RMS(ref) is a few 1e-6 (measured at
+most 4e-6 over these cases).  dw sums the rows in a fixed order (a
+workgroup's lanes, then the workgroups), each term exact to about ten
+roundings: the same few 1e-6 relative to RMS(dw) at these row counts."""
 import numpy as np
 import pytest
 import torch
@@ -10,7 +19,7 @@ import paper_2609_36529_amd as tla
 from helpers import rel_err
 
 pytestmark = pytest.mark.gpu
-TOL_F32 = 2e-5  # max|err| / RMS(ref), fp32 outputs and dw
+TOL_F32 = 1e-5  # max|err| / RMS(ref), fp32 outputs and dw
 
 
 def within_bf16_rounding(got, ref):
