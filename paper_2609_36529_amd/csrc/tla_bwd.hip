@@ -65,6 +65,20 @@ __device__ __forceinline__ void store_out(void* base, size_t off, float x, int o
     ((float*)base)[off] = x;
 }
 
+// Rows i .. i + 3 of column c of a row-major shared-memory tile, p =
+// &tile[i][c] with a row pitch of P elements: the fragment that row c of the
+// transposed tile would give at columns i .. i + 3.
+template <int P>
+__device__ __forceinline__ f32x4 col_frag(const float* p) {
+  return f32x4{p[0], p[P], p[2 * P], p[3 * P]};
+}
+template <int P>
+__device__ __forceinline__ bf16x4 col_frag(const bf16_t* p) {
+  const uint32_t a = (uint32_t)p[0] | ((uint32_t)p[P] << 16);
+  const uint32_t b = (uint32_t)p[2 * P] | ((uint32_t)p[3 * P] << 16);
+  return __builtin_bit_cast(bf16x4, make_uint2(a, b));
+}
+
 template <int D, typename FA, typename FB>
 __device__ __forceinline__ void bmma_k(f32x4& acc, FA fa, FB fb) {
   constexpr int NB = D / 16;
@@ -90,10 +104,12 @@ struct RecSmem {
   alignas(16) T Kt[KD][CP];      // K^T
   alignas(16) T Qt[KD][CP];      // Q^T
   alignas(16) T dOt[16][CP];     // dO tile, transposed
-  alignas(16) T MT[C][CP];       // M^T (hi)
-  alignas(16) T TuT[C][CP];      // Tu^T (hi)
-  alignas(16) T MTL[SPLIT ? C : 1][CP];
-  alignas(16) T TuTL[SPLIT ? C : 1][CP];
+  // M and Tu row-major (hi; lo below): the A operands of M^T dO and Tu^T dU
+  // are read down their columns
+  alignas(16) T M[C][CP];
+  alignas(16) T Tu[C][CP];
+  alignas(16) T ML[SPLIT ? C : 1][CP];
+  alignas(16) T TuL[SPLIT ? C : 1][CP];
   alignas(16) float coef[3][E][C];
   alignas(16) float gC[E4];
   alignas(16) f32x4 X[NW][NT][64];  // per-wave partials of sum_e diag(c_e) K dS'_e
@@ -104,8 +120,8 @@ struct RecSmem {
 
 // Register staging of one chunk's inputs for the reverse recurrence: the
 // global loads for chunk ci - 1 are issued while chunk ci is computed, and
-// copied to shared memory at the top of the next step.  K^T, Q^T, M^T and
-// Tu^T arrive from the prep kernel already transposed and split, so only the
+// copied to shared memory at the top of the next step.  K^T, Q^T, M and Tu
+// arrive from the prep kernel already in operand layout and split, so only the
 // dO tile is transposed here.  Loads are unconditional (rows past T read a
 // clamped row and are zeroed when stored) and waves past the last piece of a
 // loop step skip it (a scalar branch).
@@ -115,7 +131,7 @@ struct RecStage {
   static constexpr int EC = 16 / (int)sizeof(T);        // elements per 16-byte chunk
   static constexpr int NRC = C * KD / EC;                // chunks of the K rows
   static constexpr int NTC = 2 * KD * C / EC;            // chunks of K^T and Q^T
-  static constexpr int NMC = 2 * OT::NS * C * C / EC;    // chunks of M^T and Tu^T (hi, lo)
+  static constexpr int NMC = 2 * OT::NS * C * C / EC;    // chunks of M and Tu (hi, lo)
   static constexpr int RB = C / 4;
   static constexpr int NR = (NRC + NTHR - 1) / NTHR;
   static constexpr int NTT = (NTC + NTHR - 1) / NTHR;
@@ -130,7 +146,7 @@ struct RecStage {
   f32x4 c[NCB];
   float gc;
 
-  // parts: 1 = the K rows, K^T, Q^T and the dO tile; 2 = M^T, Tu^T and the
+  // parts: 1 = the K rows, K^T, Q^T and the dO tile; 2 = M, Tu and the
   // vectors (the two halves are issued at different points of a chunk step)
   __device__ __forceinline__ void load(const Shape& s, const PrepBufs& p, const T* Kg,
                                        const T* Qg, const T* dOg, size_t ch, int ci,
@@ -171,7 +187,7 @@ struct RecStage {
 #pragma unroll
     for (int i = 0; i < NM; ++i) {
       if (w0 + i * NTHR >= NMC) continue;
-      mt[i] = ((const uint4*)(ops + OT::MT))[min(tid + i * NTHR, NMC - 1)];
+      mt[i] = ((const uint4*)(ops + OT::M))[min(tid + i * NTHR, NMC - 1)];
     }
     const float* cg = p.coef + ch * 3 * E * C;
 #pragma unroll
@@ -225,7 +241,7 @@ struct RecStage {
     }
     }
     if (!(parts & 2)) return;
-    // M^T and Tu^T chunks: matrix m (M^T hi, lo, Tu^T hi, lo for bf16; M^T, Tu^T for fp32)
+    // M and Tu chunks: matrix m (M hi, lo, Tu hi, lo for bf16; M, Tu for fp32)
     constexpr int PER = C * C / EC;
 #pragma unroll
     for (int i = 0; i < NM; ++i) {
@@ -235,9 +251,9 @@ struct RecStage {
       const int r = j / (C / EC), c0 = EC * (j % (C / EC));
       T* dst;
       if constexpr (OT::NS == 2)
-        dst = (mtx == 0) ? &sm.MT[r][c0] : (mtx == 1) ? &sm.MTL[r][c0] : (mtx == 2) ? &sm.TuT[r][c0] : &sm.TuTL[r][c0];
+        dst = (mtx == 0) ? &sm.M[r][c0] : (mtx == 1) ? &sm.ML[r][c0] : (mtx == 2) ? &sm.Tu[r][c0] : &sm.TuL[r][c0];
       else
-        dst = (mtx == 0) ? &sm.MT[r][c0] : &sm.TuT[r][c0];
+        dst = (mtx == 0) ? &sm.M[r][c0] : &sm.Tu[r][c0];
       lds_put16(dst, mt[i]);
     }
     float* cs = &sm.coef[0][0][0];
@@ -270,6 +286,10 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
   // each chunk's inputs at its own start instead of one chunk ahead, and
   // reuse operand fragments over fewer slices at a time
   constexpr bool PREFETCH = SPW == 1 || NW <= 4;
+  // the Tu^T operand of dW, gathered from the columns of the staged Tu, is
+  // read while dU is formed (instances with registers to spare)
+  constexpr bool EARLY_T = PREFETCH && !PDS;
+  constexpr int NKB = C / 16;
   extern __shared__ __align__(16) unsigned char smem_raw[];
   Sm& sm = *reinterpret_cast<Sm*>(smem_raw);
 
@@ -436,16 +456,26 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
       if (ci > 0) stage.load(s, p, Kg, Qg, dOg, ch - 1, ci - 1, 1);
     // ---- dU = M^T dO + sum of the partials, then dW = -Tu^T dU: wave w < NT
     // forms row tile w of each, and the tiles are exchanged through LDS
+    F tuf[2][NKB];
     if (w < NT) {
       const int rt = w;
+      const int r = 16 * rt + n;
+      if constexpr (EARLY_T) {  // Tu^T fragments for dW below, read under dU
+        if (s.variant == 1) {
+#pragma unroll
+          for (int kb = 0; kb < NKB; ++kb) {
+            tuf[0][kb] = col_frag<Sm::CP>(&sm.Tu[16 * kb + 4 * g][r]);
+            if constexpr (Sm::SPLIT) tuf[1][kb] = col_frag<Sm::CP>(&sm.TuL[16 * kb + 4 * g][r]);
+          }
+        }
+      }
       f32x4 acc = zero4();
 #pragma unroll
       for (int ww = 0; ww < NW; ++ww) acc += sm.X[ww][rt][l];
-      const int r = 16 * rt + n;
       auto dof = [&](int kb) { return ld_frag(&sm.dOt[n][16 * kb + 4 * g]); };
-      bmma_k<C>(acc, [&](int kb) { return ld_frag(&sm.MT[r][16 * kb + 4 * g]); }, dof);
+      bmma_k<C>(acc, [&](int kb) { return col_frag<Sm::CP>(&sm.M[16 * kb + 4 * g][r]); }, dof);
       if constexpr (Sm::SPLIT)
-        bmma_k<C>(acc, [&](int kb) { return ld_frag(&sm.MTL[r][16 * kb + 4 * g]); }, dof);
+        bmma_k<C>(acc, [&](int kb) { return col_frag<Sm::CP>(&sm.ML[16 * kb + 4 * g][r]); }, dof);
       F hi, lo;
       split_frag(acc, hi, lo);
       sm.dUs[0][rt][l] = hi;
@@ -458,11 +488,15 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
       f32x4 acc = zero4();
       if (s.variant == 1) {
         const int r = 16 * rt + n;
-        auto th = [&](int kb) { return ld_frag(&sm.TuT[r][16 * kb + 4 * g]); };
+        auto tfr = [&](int part, int kb) -> F {
+          if constexpr (EARLY_T) return tuf[part][kb];
+          else return col_frag<Sm::CP>(part ? &sm.TuL[16 * kb + 4 * g][r] : &sm.Tu[16 * kb + 4 * g][r]);
+        };
+        auto th = [&](int kb) { return tfr(0, kb); };
         bmma_k<C>(acc, th, [&](int kb) { return sm.dUs[0][kb][l]; });
         if constexpr (Sm::SPLIT) {
           bmma_k<C>(acc, th, [&](int kb) { return sm.dUs[1][kb][l]; });
-          bmma_k<C>(acc, [&](int kb) { return ld_frag(&sm.TuTL[r][16 * kb + 4 * g]); },
+          bmma_k<C>(acc, [&](int kb) { return tfr(1, kb); },
                     [&](int kb) { return sm.dUs[0][kb][l]; });
         }
         acc = -acc;

@@ -65,10 +65,10 @@ __device__ __forceinline__ void mma_k(f32x4& acc, FA fa, FB fb) {
 // elements per lane, consecutive lanes along a row) with the nontemporal
 // hint: the recurrent kernel that runs next reads these tiles once, and
 // partly written lines left dirty in L2 were written back while it ran
-// (measured 40-50 us slower at B4 H8 T4096).  The transposed copies are
-// read out of shared memory column-wise: M from a copy of it (LINES), Tu
-// from the inverse, K^T and Q^T from the staged rows.  Instances whose plan
-// would then exceed two workgroups per CU keep the per-tile stores.
+// (measured 40-50 us slower at B4 H8 T4096).  M leaves from a row-major
+// copy of it (LINES), Tu from the inverse; K^T and Q^T are read out of the
+// staged rows column-wise.  Instances whose plan would then exceed two
+// workgroups per CU keep the per-tile stores.
 template <typename T, int KD, int C, int E>
 struct PrepSmem {
   static constexpr int KP = KD + 8;  // 16-byte rows, conflict-free 16-byte fragment reads
@@ -85,7 +85,7 @@ struct PrepSmem {
     struct {
       T sQ[STAGE ? C : 1][KP];
       T sK[STAGE ? C : 1][KP];
-      float Mb[LINES ? C : 1][CP];  // M, for the line-wise row-major and transposed copies
+      float Mb[LINES ? C : 1][CP];  // M, for the line-wise stores
     } qk;
     struct { float X[C][CP]; float Y[NT > 1 ? NT - 1 : 1][16][17]; } inv;
   };
@@ -256,8 +256,8 @@ __global__ __launch_bounds__(prep_waves<E>() * 64) void k_prep(Shape s, FwdIn in
   };
   typedef OpTiles<T, KD, C> OT;
   T* ops = (T*)p.ops + (size_t)ch * OT::STRIDE;
-  // M tile (rt, st) of the lane layout into the row-major and transposed
-  // copies, split into (hi, lo) for bf16 operands
+  // M tile (rt, st) of the lane layout into the row-major copy, split into
+  // (hi, lo) for bf16 operands
   auto put_m = [&](int rt, int st, f32x4 mv) {
     f32x4 parts[2];
     if constexpr (OT::NS == 2) {
@@ -269,8 +269,6 @@ __global__ __launch_bounds__(prep_waves<E>() * 64) void k_prep(Shape s, FwdIn in
 #pragma unroll
     for (int pt = 0; pt < OT::NS; ++pt) {
       store_tile16(ops + OT::M + pt * OT::MAT + (size_t)(16 * rt) * C + 16 * st, parts[pt], g, n, C);
-      if (p.bwd_tiles)
-        put4<T>(ops + OT::MT + pt * OT::MAT + (size_t)(16 * st + n) * C + 16 * rt + 4 * g, parts[pt]);
     }
   };
   for (int tile = w; tile < NT * NT; tile += PREP_NW) {
@@ -339,25 +337,13 @@ __global__ __launch_bounds__(prep_waves<E>() * 64) void k_prep(Shape s, FwdIn in
       put_m(rt, st, mv);
     }
   }
-  // ---- M (and for the backward M^T), K^T (and Q^T) as whole lines
+  // ---- M, K^T (and for the backward Q^T) as whole lines
   if constexpr (Sm::LINES) {
     __syncthreads();  // M complete
     for (int idx = tid; idx < C * C / 8; idx += PREP_NTHR) {
       const int r = idx / (C / 8), c8 = 8 * (idx % (C / 8));
       const float* src = &sm.u.qk.Mb[r][c8];
       store8_split<C>(ops + OT::M + (size_t)r * C + c8, *(const f32x4*)src, *(const f32x4*)(src + 4));
-    }
-    if (p.bwd_tiles) {
-      for (int idx = tid; idx < C * C / 8; idx += PREP_NTHR) {
-        const int c = idx / (C / 8), r8 = 8 * (idx % (C / 8));
-        f32x4 x0, x1;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          x0[i] = sm.u.qk.Mb[r8 + i][c];
-          x1[i] = sm.u.qk.Mb[r8 + 4 + i][c];
-        }
-        store8_split<C>(ops + OT::MT + (size_t)c * C + r8, x0, x1);
-      }
     }
     // row R of K^T holds key key_of_row(R); column c position row_of_key(c)
     // (the key orders of the recurrent kernels' state tiles)
@@ -427,28 +413,15 @@ __global__ __launch_bounds__(prep_waves<E>() * 64) void k_prep(Shape s, FwdIn in
         gstore_b128(dst + r * C + 4 * c4, __builtin_bit_cast(u32x4, *(const f32x4*)&sm.u.inv.X[r][4 * c4]));
       }
     }
-    if constexpr (Sm::LINES) {  // Tu = X diag(beta) row-major, then (backward) transposed
+    if constexpr (Sm::LINES) {  // Tu = X diag(beta), row-major
       for (int idx = tid; idx < C * C / 8; idx += PREP_NTHR) {
         const int r = idx / (C / 8), c8 = 8 * (idx % (C / 8));
         const float* src = &sm.u.inv.X[r][c8];
         store8_split<C>(ops + OT::Tu + (size_t)r * C + c8, *(const f32x4*)src * *(const f32x4*)&sm.beta[c8],
                      *(const f32x4*)(src + 4) * *(const f32x4*)&sm.beta[c8 + 4]);
       }
-      if (p.bwd_tiles) {
-        for (int idx = tid; idx < C * C / 8; idx += PREP_NTHR) {
-          const int c = idx / (C / 8), r8 = 8 * (idx % (C / 8));
-          const float bc = sm.beta[c];
-          f32x4 x0, x1;
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            x0[i] = sm.u.inv.X[r8 + i][c] * bc;
-            x1[i] = sm.u.inv.X[r8 + 4 + i][c] * bc;
-          }
-          store8_split<C>(ops + OT::TuT + (size_t)c * C + r8, x0, x1);
-        }
-      }
     } else
-    // Tu row-major and transposed, from 4 x 4 blocks of the inverse
+    // Tu row-major, from 4 x 4 blocks of the inverse
     for (int idx = tid; idx < (C / 4) * (C / 4); idx += PREP_NTHR) {
       const int rb = idx / (C / 4), cb = idx % (C / 4);
       const f32x4 bc = *(const f32x4*)&sm.beta[4 * cb];
@@ -457,18 +430,12 @@ __global__ __launch_bounds__(prep_waves<E>() * 64) void k_prep(Shape s, FwdIn in
       for (int i = 0; i < 4; ++i) x[i] = *(const f32x4*)&sm.u.inv.X[4 * rb + i][4 * cb] * bc;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const f32x4 col{x[0][i], x[1][i], x[2][i], x[3][i]};
         if constexpr (OT::NS == 2) {
-          const f32x4 hr = bf16x4_to_f(cvt_frag<bf16_t>(x[i])), hc = bf16x4_to_f(cvt_frag<bf16_t>(col));
+          const f32x4 hr = bf16x4_to_f(cvt_frag<bf16_t>(x[i]));
           put4<T>(ops + OT::Tu + (size_t)(4 * rb + i) * C + 4 * cb, hr);
           put4<T>(ops + OT::Tu + OT::MAT + (size_t)(4 * rb + i) * C + 4 * cb, x[i] - hr);
-          if (p.bwd_tiles) {
-            put4<T>(ops + OT::TuT + (size_t)(4 * cb + i) * C + 4 * rb, hc);
-            put4<T>(ops + OT::TuT + OT::MAT + (size_t)(4 * cb + i) * C + 4 * rb, col - hc);
-          }
         } else {
           put4<T>(ops + OT::Tu + (size_t)(4 * rb + i) * C + 4 * cb, x[i]);
-          if (p.bwd_tiles) put4<T>(ops + OT::TuT + (size_t)(4 * cb + i) * C + 4 * rb, col);
         }
       }
     }

@@ -47,31 +47,31 @@ struct PrepBufs {
   float* gC;     // [ch][E4]       gamma^C (E4 = E rounded up to 4)
   void* ops;     // [ch][op_tile_elems] operand tiles, see OpTiles
   float* ninv;   // [ch][C][C]     (I + L)^{-1} in fp32 (GDN training forward), or NULL
-  int bwd_tiles; // training forward: also write M^T, Tu^T and Q^T (read only by the backward)
+  int bwd_tiles; // training forward: also write Q^T (read only by the backward)
 };
 
 // Operand tiles of one chunk, in the operand type T and in the layouts the
 // recurrent kernels copy into shared memory: M = (Q K^T) o R' (lower incl.
-// diagonal) and Tu = (I + L)^{-1} diag(beta) (GDN), each row-major and
-// transposed, as bf16 (hi, lo) pairs for bf16 operands (one fp32 copy for
-// fp32 operands), then K^T and Q^T of the chunk (rows past T are zero; key k
-// in row row_of_key(k), the key order of the recurrent kernels' state tiles).
-// The transposed copies and Q^T serve the backward only: an inference
-// forward leaves them unwritten.
+// diagonal) and Tu = (I + L)^{-1} diag(beta) (GDN), row-major, as bf16
+// (hi, lo) pairs for bf16 operands (one fp32 copy for fp32 operands), then
+// K^T and Q^T of the chunk (rows past T are zero; key k in row row_of_key(k),
+// the key order of the recurrent kernels' state tiles).  Q^T serves the
+// backward only: an inference forward leaves it unwritten.  (The backward
+// reads M and Tu by columns for its M^T and Tu^T operands.)
 // Element offsets within a chunk's block; part p (0 = hi, 1 = lo) of a
 // matrix X starts at X + p * MAT.
 template <typename T, int KD, int C>
 struct OpTiles {
   static constexpr int NS = sizeof(T) == 2 ? 2 : 1;
   static constexpr size_t MAT = (size_t)C * C;
-  static constexpr size_t M = 0, Tu = NS * MAT, MT = 2 * NS * MAT, TuT = 3 * NS * MAT;
-  static constexpr size_t Kt = 4 * NS * MAT, Qt = Kt + (size_t)KD * C;
+  static constexpr size_t M = 0, Tu = NS * MAT;
+  static constexpr size_t Kt = 2 * NS * MAT, Qt = Kt + (size_t)KD * C;
   static constexpr size_t STRIDE = Qt + (size_t)KD * C;
 };
 // Bytes of one chunk's operand tiles (host side).
 inline size_t op_tile_bytes(int K, int C, bool bf16) {
   const size_t ns = bf16 ? 2 : 1, es = bf16 ? 2 : 4;
-  return (4 * ns * (size_t)C * C + 2 * (size_t)K * C) * es;
+  return (2 * ns * (size_t)C * C + 2 * (size_t)K * C) * es;
 }
 
 // Buffers the training forward stores for the backward (opaque layout).

@@ -161,8 +161,8 @@ def test_size_queries():
                       tla.saved_bytes(d))
     nch = 4 * 8 * 64
     # forward workspace: per-chunk coefficient vectors, gamma^C and the bf16
-    # operand tiles (M, Tu as hi + lo pairs, row-major and transposed; K^T, Q^T)
-    assert ws_f == nch * (3 * 8 * 64 * 4 + 8 * 4 + (8 * 64 * 64 + 2 * 128 * 64) * 2)
+    # operand tiles (M, Tu as hi + lo pairs, row-major; K^T, Q^T)
+    assert ws_f == nch * (3 * 8 * 64 * 4 + 8 * 4 + (4 * 64 * 64 + 2 * 128 * 64) * 2)
     # saved: bf16 chunk-start states, fp32 U and V - W, the same prep terms
     # and, for GDN, the fp32 (I + L)^{-1} of every chunk for the backward
     assert sv == nch * (8 * 128 * 128 * 2 + 2 * 64 * 128 * 4 + 64 * 64 * 4) + ws_f

@@ -50,7 +50,7 @@ def test_noalloc_two_calls_second_smaller(variant, dtype):
 
 def test_noalloc_rejects_oversized_call_without_launch():
     L = tla.lib()
-    # B4 H8 T4096 K = V = 128 E8 chunk 64: about 200 MB of per-chunk workspace
+    # B4 H8 T4096 K = V = 128 E8 chunk 64: about 147 MB of per-chunk workspace
     desc = tla.make_desc(tla.GDN, 4, 4096, 8, 128, 128, 8, 64, tla.BF16, tla.BF16)
     assert tla.workspace_bytes(desc, tla.OP_FWD) > tla.NOALLOC_SCRATCH_BYTES
     nul = ctypes.c_void_p(None)
