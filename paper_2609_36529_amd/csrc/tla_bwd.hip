@@ -521,8 +521,13 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
     // (B operands of a group of owned slices first; each Q^T / K^T fragment is
     // read once per group, one key tile ahead of its MFMAs; four-wave
     // instances take all owned slices at once).  The variant is a constant
-    // inside: no branch splits the loop.
+    // inside: no branch splits the loop.  Operands: diag(b_e) dO enters as a
+    // bf16 (hi, lo) pair; diag(a_e) dW as one bf16 rounding (its low part
+    // moves the gradients by less than a tenth of the bf16 parity bound, the
+    // high part alone of diag(b_e) dO puts dv past it), except in the
+    // instances for a given final-state gradient, which keep both parts.
     constexpr int GS = PREFETCH ? SPW : 1;
+    constexpr bool DW_LO = Sm::SPLIT && PDS;
     auto update = [&](auto gdn_c) {
       constexpr bool GDN = decltype(gdn_c)::value;
 #pragma unroll
@@ -575,7 +580,7 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
               if constexpr (Sm::SPLIT) mma32(acc[ii], q[kb], q[kb + 1], bl[ii][kb], bl[ii][kb + 1]);
               if constexpr (GDN) {
                 mma32(acc[ii], k[kb], k[kb + 1], ah[ii][kb], ah[ii][kb + 1]);
-                if constexpr (Sm::SPLIT) mma32(acc[ii], k[kb], k[kb + 1], al[ii][kb], al[ii][kb + 1]);
+                if constexpr (DW_LO) mma32(acc[ii], k[kb], k[kb + 1], al[ii][kb], al[ii][kb + 1]);
               }
             }
           }
@@ -588,7 +593,7 @@ __global__ __launch_bounds__(NW * 64) void k_bwd_rec(Shape s, FwdIn in, const vo
               if constexpr (Sm::SPLIT) mma16(acc[ii], q[kb], bl[ii][kb]);
               if constexpr (GDN) {
                 mma16(acc[ii], k[kb], ah[ii][kb]);
-                if constexpr (Sm::SPLIT) mma16(acc[ii], k[kb], al[ii][kb]);
+                if constexpr (DW_LO) mma16(acc[ii], k[kb], al[ii][kb]);
               }
             }
           }
