@@ -3,7 +3,8 @@ position, every gradient), against the fp64 oracle run on all heads in one
 call (OpenMP over heads):
   * sGLA and GDN inference forwards at B4 H8 T4096 K=V=128 E8 chunk 64
     (outputs and final states of all 32 heads);
-  * the GDN backward on the same inputs (all 8 gradients, all 32 heads);
+  * the GDN backward on the same inputs (all 8 gradients, all 32 heads),
+    with a zero and with a unit-scale final-state gradient;
   * the long-context GDN forward at B1 H16 T65536 E16 (all 16 heads, the
     whole output and the final state);
   * the decode step at N256 H16 E16: 1000 steps on 8 sequences followed by
@@ -48,27 +49,47 @@ def test_forward_all_heads(name):
     assert eo <= TOL_BF16 and es <= TOL_BF16, (eo, es)
 
 
-@pytest.mark.timeout(900)
-def test_gdn_backward_all_heads():
-    """The GDN backward workload: dO ~ N(0, 1) bf16, zero final-state gradient."""
+def _gdn_backward_all_heads(with_final_state_gradient):
     cfg = synth.CONFIGS["gdn_bf16"]
     inp = synth.make_inputs(cfg)
     dO = synth.make_dO(cfg)
+    dSf = None
+    if with_final_state_gradient:
+        rng = np.random.default_rng(17)
+        dSf = torch.from_numpy(rng.standard_normal((cfg.B, cfg.H, cfg.E, cfg.K, cfg.V))).float()
     d = _dev(inp)
     _, _, saved = tla.fwd(cfg.variant, *[d[n] for n in NAMES], d["beta"], d["s0"], chunk=cfg.chunk,
                           out_dtype=torch.float32, training=True)
     gr = tla.bwd(cfg.variant, *[d[n] for n in NAMES], d["beta"], d["s0"], dO.cuda(), saved,
-                 chunk=cfg.chunk, out_dtype=torch.float32)
+                 dS_final=None if dSf is None else dSf.cuda(), chunk=cfg.chunk,
+                 out_dtype=torch.float32)
     torch.cuda.synchronize()
-    ref = oracle.bwd(cfg.variant, *_oracle_args(inp), synth.to64(dO))
+    ref = oracle.bwd(cfg.variant, *_oracle_args(inp), synth.to64(dO),
+                     None if dSf is None else synth.to64(dSf))
     errs = {}
     for key in ("dq", "dk", "dv", "dq2", "dk2", "dg", "dbeta", "ds0"):
         got = host64(gr[key])
         assert np.all(np.isfinite(got)), key
         errs[key] = rel_err(got, ref[key])
-    print("gdn backward all heads: " + " ".join(f"{k}={v:.1e}" for k, v in errs.items()), flush=True)
+    label = "with unit final-state gradient" if with_final_state_gradient else ""
+    print(f"gdn backward all heads{' ' + label if label else ''}: " + " ".join(f"{k}={v:.1e}" for k, v in errs.items()),
+          flush=True)
     bad = {k: v for k, v in errs.items() if v > TOL_BF16}
     assert not bad, bad
+
+
+@pytest.mark.timeout(900)
+def test_gdn_backward_all_heads():
+    """The GDN backward workload: dO ~ N(0, 1) bf16, zero final-state gradient."""
+    _gdn_backward_all_heads(False)
+
+
+@pytest.mark.timeout(900)
+def test_gdn_backward_all_heads_with_final_state_gradient():
+    """The same backward when the caller carries state on: a unit-scale
+    dS_final ~ N(0, 1) (the chunk-end state gradients then travel as bf16
+    (hi, lo) pairs)."""
+    _gdn_backward_all_heads(True)
 
 
 @pytest.mark.timeout(900)
