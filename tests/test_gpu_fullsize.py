@@ -4,7 +4,8 @@ call (OpenMP over heads):
   * sGLA and GDN inference forwards at B4 H8 T4096 K=V=128 E8 chunk 64
     (outputs and final states of all 32 heads);
   * the GDN backward on the same inputs (all 8 gradients, all 32 heads),
-    with a zero and with a unit-scale final-state gradient;
+    with a zero and with a unit-scale final-state gradient, and the sGLA
+    backward on the sGLA inputs;
   * the long-context GDN forward at B1 H16 T65536 E16 (all 16 heads, the
     whole output and the final state);
   * the decode step at N256 H16 E16: 1000 steps on 8 sequences followed by
@@ -49,8 +50,8 @@ def test_forward_all_heads(name):
     assert eo <= TOL_BF16 and es <= TOL_BF16, (eo, es)
 
 
-def _gdn_backward_all_heads(with_final_state_gradient):
-    cfg = synth.CONFIGS["gdn_bf16"]
+def _backward_all_heads(with_final_state_gradient, name="gdn_bf16"):
+    cfg = synth.CONFIGS[name]
     inp = synth.make_inputs(cfg)
     dO = synth.make_dO(cfg)
     dSf = None
@@ -68,11 +69,14 @@ def _gdn_backward_all_heads(with_final_state_gradient):
                      None if dSf is None else synth.to64(dSf))
     errs = {}
     for key in ("dq", "dk", "dv", "dq2", "dk2", "dg", "dbeta", "ds0"):
+        if ref[key] is None:  # sGLA without beta
+            assert gr[key] is None, key
+            continue
         got = host64(gr[key])
         assert np.all(np.isfinite(got)), key
         errs[key] = rel_err(got, ref[key])
     label = "with unit final-state gradient" if with_final_state_gradient else ""
-    print(f"gdn backward all heads{' ' + label if label else ''}: " + " ".join(f"{k}={v:.1e}" for k, v in errs.items()),
+    print(f"{name} backward all heads{' ' + label if label else ''}: " + " ".join(f"{k}={v:.1e}" for k, v in errs.items()),
           flush=True)
     bad = {k: v for k, v in errs.items() if v > TOL_BF16}
     assert not bad, bad
@@ -81,7 +85,7 @@ def _gdn_backward_all_heads(with_final_state_gradient):
 @pytest.mark.timeout(900)
 def test_gdn_backward_all_heads():
     """The GDN backward workload: dO ~ N(0, 1) bf16, zero final-state gradient."""
-    _gdn_backward_all_heads(False)
+    _backward_all_heads(False)
 
 
 @pytest.mark.timeout(900)
@@ -89,7 +93,14 @@ def test_gdn_backward_all_heads_with_final_state_gradient():
     """The same backward when the caller carries state on: a unit-scale
     dS_final ~ N(0, 1) (the chunk-end state gradients then travel as bf16
     (hi, lo) pairs)."""
-    _gdn_backward_all_heads(True)
+    _backward_all_heads(True)
+
+
+@pytest.mark.timeout(900)
+def test_sgla_backward_all_heads():
+    """The sGLA backward on the sGLA forward workload's inputs (B4 H8 T4096
+    E8 bf16), zero final-state gradient."""
+    _backward_all_heads(False, "sgla_bf16")
 
 
 @pytest.mark.timeout(900)
