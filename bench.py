@@ -225,7 +225,22 @@ def pmc_summary(read_dir, write_dir, copy_read_dir, copy_write_dir):
               f"{r['fetch_bytes'] + r['write_bytes']:.4g} |")
 
 
-def decode_bench(steps, warmup):
+def _warm_up(call, n, min_seconds=0.1):
+    """n untimed calls, then more (in tens) until at least min_seconds of
+    work have run: the part needs about 70 ms of work before its clocks
+    settle, and a short call (0.2 ms) would otherwise be timed on the way up."""
+    import torch
+    for _ in range(n):
+        call()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < min_seconds:
+        for _ in range(10):
+            call()
+        torch.cuda.synchronize()
+
+
+def decode_bench(steps, warmup, emit=True):
     """The recurrent decode step (tla_step) at N=256 sequences, H=16, E=16,
     K=V=128, bf16 token inputs, fp32 state [N,H,E,K,V] (4 GiB) updated in
     place; 8 pre-generated tokens are cycled so no input generation is timed.
@@ -245,9 +260,12 @@ def decode_bench(steps, warmup):
         t = toks[i % len(toks)]
         tla.step(tla.GDN, t["q"], t["k"], t["v"], t["q2"], t["k2"], t["g"], t["beta"], state,
                  out_dtype=torch.bfloat16, o=o)
-    for i in range(warmup):
-        one(i)
-    torch.cuda.synchronize()
+    cnt = [0]
+
+    def next_call():
+        one(cnt[0])
+        cnt[0] += 1
+    _warm_up(next_call, warmup)
     tla.prof_enable(True)
     t0 = time.perf_counter()
     for i in range(steps):
@@ -259,7 +277,7 @@ def decode_bench(steps, warmup):
     avg_ms = tot / n
     state_bytes = 2.0 * N * H * E * K * V * 4
     gbs = state_bytes / (avg_ms * 1e-3) / 1e9
-    print(json.dumps({
+    res = {
         "metric": "decode tokens/s, triadic GDN tla_step N=256 H=16 E=16 K=V=128",
         "value": round(N / (elapsed / steps), 1), "unit": "tokens/s", "n_gpus": 1,
         "steps": steps, "warmup": warmup, "ms_per_step": round(1e3 * elapsed / steps, 4),
@@ -268,10 +286,13 @@ def decode_bench(steps, warmup):
         "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
                      "kernel": "step", "algorithmic_bytes_per_launch": state_bytes,
-                     "avg_ms": round(avg_ms, 4)}}), flush=True)
+                     "avg_ms": round(avg_ms, 4)}}
+    if emit:
+        print(json.dumps(res), flush=True)
+    return res
 
 
-def forward_bench(name, steps, warmup):
+def forward_bench(name, steps, warmup, emit=True):
     """Inference forward (tla_fwd without `saved`) of a named workload: prep +
     recurrent forward, bf16 operands, bf16 output, final state returned.
     MFMA-bound by its algorithmic counts (inputs and outputs only move about
@@ -292,9 +313,7 @@ def forward_bench(name, steps, warmup):
     def one():
         tla.fwd(cfg.variant, d["q"], d["k"], d["v"], d["q2"], d["k2"], d["g"], d["beta"], d["s0"],
                 chunk=C, out_dtype=torch.bfloat16, o=o, s_final=sf, ws=ws)
-    for _ in range(warmup):
-        one()
-    torch.cuda.synchronize()
+    _warm_up(one, warmup)
     tla.prof_enable(True)
     t0 = time.perf_counter()
     for _ in range(steps):
@@ -310,7 +329,7 @@ def forward_bench(name, steps, warmup):
     th = B * T * H
     tflops = flops * th / elapsed / 1e12
     kern = {k: round(v[0] / v[1], 4) for k, v in prof.items() if v[1]}
-    print(json.dumps({
+    res = {
         "metric": f"forward tokens/s, {name}", "value": round(B * T / elapsed, 1),
         "unit": "tokens/s", "n_gpus": 1, "steps": steps, "warmup": warmup,
         "ms_per_step": round(1e3 * elapsed, 4), "higher_is_better": True, "dtype": "bf16",
@@ -320,7 +339,28 @@ def forward_bench(name, steps, warmup):
         "kernels_ms": kern,
         "roofline": {"bound": "mfma", "achieved": round(tflops, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
-                     "kernel": "prep + fwd_recurrent"}}), flush=True)
+                     "kernel": "prep + fwd_recurrent"}}
+    if emit:
+        print(json.dumps(res), flush=True)
+    return res
+
+
+def other_workloads(steps=10, warmup=20):
+    """The inference forwards and the decode step, timed after the training
+    step and reported beside it: throughput, time per call and the roofline
+    fraction of each (each after at least 100 ms of untimed calls, see
+    _warm_up: its inputs are generated on the host while the part idles)."""
+    out = {}
+    for name in ("sgla_bf16", "gdn_bf16", "gdn_long_bf16"):
+        r = forward_bench(name, steps, warmup, emit=False)
+        out[name + "_forward"] = {"value": r["value"], "unit": r["unit"],
+                                  "ms_per_step": r["ms_per_step"], "config": r["config"],
+                                  "mfma_frac": r["roofline"]["frac"]}
+    r = decode_bench(steps, warmup, emit=False)
+    out["gdn_decode_N256H16E16"] = {"value": r["value"], "unit": r["unit"],
+                                    "ms_per_step": r["ms_per_step"], "config": r["config"],
+                                    "hbm_frac": r["roofline"]["frac"]}
+    return out
 
 
 def gate_bench(steps, warmup):
@@ -590,6 +630,8 @@ def main():
     # warm-up steps the timed training steps ran about 5% slower)
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the inference forwards and decode reported beside the training step")
     ap.add_argument("--copy-calibration", action="store_true")
     ap.add_argument("--pmc-summary", nargs=4, metavar="DIR")
     ap.add_argument("--decode", action="store_true",
@@ -764,6 +806,10 @@ def main():
         "kernels": kernels,
         "roofline": roof,
     }
+    if not args.no_extras:
+        del ws_f, ws_b, saved, grads
+        torch.cuda.empty_cache()
+        result["other_workloads"] = other_workloads()
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(cfg, inp, dO)
     print(json.dumps(result), flush=True)
