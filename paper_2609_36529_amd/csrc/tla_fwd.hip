@@ -514,7 +514,6 @@ struct FwdDma : GroupDma<NW> {
   static constexpr int N_TU = tile_count<decltype(Sm::Tu)>() * (Sm::SPLIT ? 2 : 1);
   static constexpr int N_M = tile_count<decltype(Sm::M)>() * (Sm::SPLIT ? 2 : 1);
   static constexpr int N_KT = tile_count<decltype(Sm::Kt)>() + co_count<NCO2>();
-  static constexpr int N_C2 = co_count<NCO2>();
   static constexpr int N_KC = tile_count<decltype(Sm::K)>() + co_count<NCO01>();
   static constexpr int N_Q = tile_count<decltype(Sm::Q)>();
   static __device__ __forceinline__ void kq(Sm& sm, const Shape& s, const PrepBufs& p, const T* Kg,
@@ -558,10 +557,6 @@ struct FwdDma : GroupDma<NW> {
   static __device__ __forceinline__ void kt(Sm& sm, const PrepBufs& p, size_t ch) {
     const T* ops = (const T*)p.ops + ch * OT::STRIDE;
     op_tile(sm.Kt, ops + OT::Kt);
-    copy<NCO2>(&sm.coef2[0][0], p.coef + ch * 3 * E * C + 2 * E * C);
-  }
-  // the coefficients c_e alone (for kernels that form K^T in shared memory)
-  static __device__ __forceinline__ void c2(Sm& sm, const PrepBufs& p, size_t ch) {
     copy<NCO2>(&sm.coef2[0][0], p.coef + ch * 3 * E * C + 2 * E * C);
   }
 
@@ -1285,14 +1280,14 @@ __global__ __launch_bounds__(512) void k_fwd_dual(Shape s, FwdIn in, PrepBufs p,
       const bool more = ci + 1 < nc;
       __syncthreads();  // B0
       if (t0 + C > s.T) zero_tail(t0);
-      Dma::c2(sm, p, ch);  // (K^T is formed by the output waves from the K rows)
+      Dma::kt(sm, p, ch);
       Dma::gc(sm, p, ch);
       Dma::m(sm, p, ch);
 
       // ---- W partial: sum over the wave's slices of diag(a_e) K S_e (GDN;
       // sGLA has no W)
       if (s.variant == 1) state_pass(sm.K, Sop, sm.coef01[0], sm.W[w]);
-      wait_vmcnt<Dma::N_C2 + 1 + Dma::N_M>();  // this chunk's Tu, V and beta have landed
+      wait_vmcnt<Dma::N_KT + 1 + Dma::N_M>();  // this chunk's Tu, V and beta have landed
       __syncthreads();  // B1
       if (more) {  // K, Q, a_e and b_e are free
         Dma::kc(sm, s, p, Kg, ch + 1, t0 + C);
@@ -1477,34 +1472,6 @@ __global__ __launch_bounds__(512) void k_fwd_dual(Shape s, FwdIn in, PrepBufs p,
         }
       };
       state_pass(sm.Q, So, sm.coef01[1], sm.O[w]);
-      // ---- K^T of this chunk, for the state waves' update after B2, from the
-      // K rows in shared memory (the layout of the prep kernel's K^T tile: key
-      // k in row row_of_key(k), position r in column key_of_row(r), both
-      // keeping groups of four together).  The previous chunk's update read
-      // the tile before B0; the next chunk's K rows arrive after B1.  Rows
-      // past T enter as zeros whether or not the tail has been cleared yet.
-      {
-        constexpr int NBLK = (C / 4) * (KD / 4);
-        for (int b = (wv - NG) * 64 + l; b < NBLK; b += NG * 64) {
-          const int rb = b / (KD / 4), kb = b % (KD / 4);
-          uint2 x[4];
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int r = 4 * rb + i;
-            x[i] = (t0 + r < s.T) ? *(const uint2*)sm.K.at(r, 4 * kb) : make_uint2(0u, 0u);
-          }
-          const int row0 = row_of_key<KD>(4 * kb), col0 = key_of_row<C>(4 * rb);
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int sh = 16 * (j & 1);
-            const uint32_t e0 = ((j < 2 ? x[0].x : x[0].y) >> sh) & 0xffffu;
-            const uint32_t e1 = ((j < 2 ? x[1].x : x[1].y) >> sh) & 0xffffu;
-            const uint32_t e2 = ((j < 2 ? x[2].x : x[2].y) >> sh) & 0xffffu;
-            const uint32_t e3 = ((j < 2 ? x[3].x : x[3].y) >> sh) & 0xffffu;
-            *(uint2*)const_cast<T*>(sm.Kt.at(row0 + j, col0)) = make_uint2(e0 | (e1 << 16), e2 | (e3 << 16));
-          }
-        }
-      }
       __syncthreads();  // B1
       // the checkpoint pieces, read before the state waves replace the copy
       // after B2
